@@ -1,0 +1,201 @@
+"""TEST INFRASTRUCTURE ONLY: ctypes front end of the CPU oracle.
+
+Only tests/, the smoke check and the benchmark's CPU-baseline leg may import
+this package.  The product path (the HIP library and its binding) never does.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+# A test may point the oracle at another build of its source (mutation tests).
+LIB_PATH = os.environ.get("EPROP_ORACLE_LIB") or os.path.join(HERE, "liboracle.so")
+
+
+class OracleConfig(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("batch", ctypes.c_int32), ("n_in", ctypes.c_int32),
+        ("n_rec", ctypes.c_int32), ("n_out", ctypes.c_int32), ("recurrent", ctypes.c_int32),
+        ("n_adaptive", ctypes.c_int32),
+        ("alpha", ctypes.c_double), ("rho", ctypes.c_double), ("kappa", ctypes.c_double),
+        ("thr", ctypes.c_double), ("beta", ctypes.c_double), ("gamma", ctypes.c_double),
+        ("reset", ctypes.c_double),
+        ("fwd_fp32", ctypes.c_int32), ("smooth", ctypes.c_int32),
+    ]
+
+
+class OracleRecord(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("v", "a", "psi", "L", "z", "y")]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        from . import build as _b
+        _b.build(out=path)
+    lib = ctypes.CDLL(path)
+    lib.oracle_eprop_run.restype = ctypes.c_int
+    lib.oracle_eprop_run.argtypes = [
+        ctypes.POINTER(OracleConfig), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+        ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p,
+    ]
+    lib.oracle_state_bytes.restype = ctypes.c_size_t
+    lib.oracle_state_bytes.argtypes = [ctypes.POINTER(OracleConfig), ctypes.c_int32]
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+def make_config(shape, fwd_fp32: bool = True, smooth: bool = False,
+                reset: Optional[float] = None, **over) -> OracleConfig:
+    """Oracle config from an EpropShape (any object with the same fields)."""
+    c = OracleConfig()
+    c.n_layers, c.batch, c.n_in, c.n_rec = shape.n_layers, shape.batch, shape.n_in, shape.n_rec
+    c.n_out, c.recurrent, c.n_adaptive = shape.n_out, shape.recurrent, shape.n_adaptive
+    c.alpha, c.rho, c.kappa = shape.alpha, shape.rho, shape.kappa
+    c.thr, c.beta, c.gamma = shape.thr, shape.beta, shape.gamma
+    c.reset = shape.thr if reset is None else reset
+    c.fwd_fp32, c.smooth = int(fwd_fp32), int(smooth)
+    for k, v in over.items():
+        setattr(c, k, v)
+    return c
+
+
+@dataclass
+class OracleResult:
+    dW: list            # per layer fp64 [n_rec, n_pre] (all synapses) or [n_sample] (sampled)
+    dWout: list         # per layer fp64 [n_out, n_rec]
+    loss: float
+    spikes: Optional[np.ndarray]  # uint32 [T, L, B, ceil(n_rec/32)]
+    record: Optional[dict]
+
+
+def run(shape, W: Sequence[np.ndarray], Wout: Sequence[np.ndarray], x: np.ndarray,
+        labels: np.ndarray, *, T: Optional[int] = None, b_lo: int = 0, b_hi: Optional[int] = None,
+        sample: Optional[np.ndarray] = None, want_spikes: bool = True, want_record: bool = False,
+        fwd_fp32: bool = True, smooth: bool = False, reset: Optional[float] = None,
+        spikes_out: Optional[np.ndarray] = None, lib_path: str = LIB_PATH,
+        **over) -> OracleResult:
+    """Runs the oracle on batch elements [b_lo, b_hi).  ``sample`` is an int32
+    array of (layer, j, i) rows; when given, only those synapses' gradients are
+    computed (returned as dW[0] of length len(sample)).  ``spikes_out``, if
+    given, is the uint32 [T, L, B, ceil(n_rec/32)] record to write into."""
+    lib = load(lib_path)
+    cfg = make_config(shape, fwd_fp32=fwd_fp32, smooth=smooth, reset=reset, **over)
+    T = x.shape[0] if T is None else T
+    b_hi = shape.batch if b_hi is None else b_hi
+    L, N, K, B = shape.n_layers, shape.n_rec, shape.n_out, shape.batch
+    Wc = [np.ascontiguousarray(w, dtype=np.float32) for w in W]
+    Woc = [np.ascontiguousarray(w, dtype=np.float32) for w in Wout]
+    xc = np.ascontiguousarray(x, dtype=np.uint8)
+    lab = np.ascontiguousarray(labels, dtype=np.int32)
+    assert xc.shape[0] >= T and xc.shape[1] == B and xc.shape[2] == shape.n_in
+    Wp = (ctypes.c_void_p * L)(*[_ptr(w) for w in Wc])
+    Wop = (ctypes.c_void_p * L)(*[_ptr(w) for w in Woc])
+    if sample is None:
+        dW = [np.zeros(w.shape, dtype=np.float64) for w in Wc]
+        smp_ptr, n_sample = None, -1
+    else:
+        smp = np.ascontiguousarray(sample, dtype=np.int32).reshape(-1, 3)
+        dW = [np.zeros(len(smp), dtype=np.float64)]
+        smp_ptr, n_sample = _ptr(smp), len(smp)
+    dWp = (ctypes.c_void_p * len(dW))(*[_ptr(d) for d in dW])
+    dWout = [np.zeros((K, N), dtype=np.float64) for _ in range(L)]
+    dWop = (ctypes.c_void_p * L)(*[_ptr(d) for d in dWout])
+    loss = np.zeros(1, dtype=np.float64)
+    spikes = None
+    if spikes_out is not None:
+        assert spikes_out.shape == (T, L, B, (N + 31) // 32) and spikes_out.dtype == np.uint32
+        assert spikes_out.flags.c_contiguous
+        spikes = spikes_out
+    elif want_spikes:
+        spikes = np.zeros((T, L, B, (N + 31) // 32), dtype=np.uint32)
+    rec = None
+    recs = None
+    if want_record:
+        recs = {k: np.zeros((T, L, B, N)) for k in ("v", "a", "psi", "L", "z")}
+        recs["y"] = np.zeros((T, L, B, K))
+        rec = OracleRecord(*[_ptr(recs[k]) for k in ("v", "a", "psi", "L", "z", "y")])
+    rc = lib.oracle_eprop_run(ctypes.byref(cfg), ctypes.cast(Wp, ctypes.c_void_p),
+                              ctypes.cast(Wop, ctypes.c_void_p), _ptr(xc), T, _ptr(lab),
+                              b_lo, b_hi, smp_ptr, n_sample,
+                              _ptr(spikes) if spikes is not None else None,
+                              ctypes.cast(dWp, ctypes.c_void_p), ctypes.cast(dWop, ctypes.c_void_p),
+                              _ptr(loss), ctypes.byref(rec) if rec is not None else None)
+    if rc != 0:
+        raise ValueError(f"oracle_eprop_run returned {rc}")
+    return OracleResult(dW=dW, dWout=dWout, loss=float(loss[0]), spikes=spikes, record=recs)
+
+
+def state_bytes(shape, n_sample: int = -1, fwd_fp32: bool = True) -> int:
+    return int(load().oracle_state_bytes(ctypes.byref(make_config(shape, fwd_fp32)), n_sample))
+
+
+_SHARD_ARGS = None
+
+
+def _shard(bounds):
+    lo, hi = bounds
+    shape, W, Wout, x, labels, T, sample, spikes, kw = _SHARD_ARGS
+    # Each shard writes its own batch rows of the shared spike record.
+    res = run(shape, W, Wout, x, labels, T=T, b_lo=lo, b_hi=hi, sample=sample,
+              want_spikes=False, spikes_out=spikes, **kw)
+    return res.dW, res.dWout, res.loss
+
+
+def run_sharded(shape, W, Wout, x, labels, *, workers: int, T: Optional[int] = None,
+                sample: Optional[np.ndarray] = None, want_spikes: bool = True,
+                **kw) -> OracleResult:
+    """The same result as ``run`` over the whole batch, computed as independent
+    single-threaded oracle runs on contiguous batch shards in forked worker
+    processes.  The gradient is a sum over batch elements; the shards' fp64
+    partial sums are added in shard order.  Each shard writes its own batch rows
+    of a spike record shared between the processes."""
+    import mmap
+    import multiprocessing as mp
+    global _SHARD_ARGS
+    B, L, N = shape.batch, shape.n_layers, shape.n_rec
+    T = x.shape[0] if T is None else T
+    workers = max(1, min(workers, B))
+    edges = [B * k // workers for k in range(workers + 1)]
+    bounds = [(edges[k], edges[k + 1]) for k in range(workers) if edges[k + 1] > edges[k]]
+    spikes = None
+    if want_spikes:
+        shp = (T, L, B, (N + 31) // 32)
+        buf = mmap.mmap(-1, max(1, int(np.prod(shp)) * 4))
+        spikes = np.frombuffer(buf, dtype=np.uint32, count=int(np.prod(shp))).reshape(shp)
+    _SHARD_ARGS = (shape, W, Wout, x, labels, T, sample, spikes, kw)
+    try:
+        if len(bounds) == 1:
+            parts = [_shard(bounds[0])]
+        else:
+            ctx = mp.get_context("fork")
+            with ctx.Pool(len(bounds)) as pool:
+                parts = pool.map(_shard, bounds)
+    finally:
+        _SHARD_ARGS = None
+    dW, dWout, loss = parts[0]
+    for pdW, pdWout, ploss in parts[1:]:
+        for l in range(len(dW)):
+            dW[l] += pdW[l]
+        for l in range(len(dWout)):
+            dWout[l] += pdWout[l]
+        loss += ploss
+    return OracleResult(dW=dW, dWout=dWout, loss=loss,
+                        spikes=None if spikes is None else np.array(spikes), record=None)

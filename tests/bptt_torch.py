@@ -1,0 +1,92 @@
+"""Reverse-mode reference for pinning the oracle (CPU, float64 autograd).
+
+The same network function the oracle differentiates, written as a plain
+forward pass in PyTorch and differentiated by backpropagation through time
+(the adjoint recursion, Eq. 6-7 of the paper) instead of the forward RTRL
+recursion of Eq. (5).  The three gradient stops of the method are
+``detach()`` calls: the recurrent spikes (Sec. III-B, the stop_gradient
+footnote), the reset term, and in two-layer stacks the spikes passed from
+layer 1 to layer 2.  With these stops the forward recursion of e-prop and
+backpropagation give the same gradient, which is what the paper checks in
+Table II for a feed-forward layer.
+
+The spike nonlinearity is the Heaviside step with the triangular surrogate
+in the backward pass (the footnote on the surrogate in Sec. III-C).
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+F64 = torch.float64
+
+
+class _Spike(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x, gamma, thr):
+        ctx.save_for_backward(x)
+        ctx.gamma, ctx.thr = gamma, thr
+        return (x > 0).to(x.dtype)
+
+    @staticmethod
+    def backward(ctx, g):
+        (x,) = ctx.saved_tensors
+        psi = (ctx.gamma / ctx.thr) * torch.clamp(1.0 - x.abs() / ctx.thr, min=0.0)
+        return g * psi, None, None
+
+
+def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True):
+    """Returns (dW list, dWout list, loss) as float64 numpy arrays.
+
+    ``stop=False`` keeps every path (true surrogate gradient); it is only used
+    to show the gradient stops matter.
+    """
+    T = x.shape[0] if T is None else T
+    L, B, N = shape.n_layers, shape.batch, shape.n_rec
+    reset = shape.thr if reset is None else reset
+    sg = (lambda v: v.detach()) if stop else (lambda v: v)
+    Ws = [torch.tensor(np.asarray(w, dtype=np.float64), requires_grad=True) for w in W]
+    Wos = [torch.tensor(np.asarray(w, dtype=np.float64), requires_grad=True) for w in Wout]
+    beta = torch.zeros(N, dtype=F64)
+    beta[: shape.n_adaptive] = shape.beta
+    lab = torch.tensor(np.asarray(labels, dtype=np.int64))
+    xs = torch.tensor(np.asarray(x[:T], dtype=np.float64))
+    v = [torch.zeros(B, N, dtype=F64) for _ in range(L)]
+    a = [torch.zeros(B, N, dtype=F64) for _ in range(L)]
+    zp = [torch.zeros(B, N, dtype=F64) for _ in range(L)]
+    y = [torch.zeros(B, shape.n_out, dtype=F64) for _ in range(L)]
+    loss = torch.zeros((), dtype=F64)
+    for t in range(T):
+        z_now = []
+        for l in range(L):
+            inp = xs[t] if l == 0 else sg(z_now[l - 1])
+            p = torch.cat([inp, sg(zp[l])], dim=1) if shape.recurrent else inp
+            I = p @ Ws[l].T
+            vl = shape.alpha * v[l]
+            vl = vl + I
+            vl = vl - reset * sg(zp[l])
+            al = shape.rho * a[l]
+            al = al + zp[l]                 # spike -> adaptation path is kept
+            A = beta * al
+            A = shape.thr + A
+            z = _Spike.apply(vl - A, shape.gamma, shape.thr)
+            y[l] = shape.kappa * y[l] + z @ Wos[l].T
+            loss = loss + torch.nn.functional.cross_entropy(y[l], lab, reduction="sum")
+            v[l], a[l] = vl, al
+            z_now.append(z)
+        zp = z_now
+    loss.backward()
+    dW = [w.grad.numpy().copy() for w in Ws]
+    if shape.recurrent:
+        for l in range(L):
+            n_in_l = shape.n_in if l == 0 else N
+            idx = np.arange(N)
+            dW[l][idx, n_in_l + idx] = 0.0   # no self-connections
+    return dW, [w.grad.numpy().copy() for w in Wos], float(loss.detach())
+
+
+def rel_l2(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64).ravel()
+    b = np.asarray(b, dtype=np.float64).ravel()
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (den if den > 0 else 1.0))

@@ -1,0 +1,321 @@
+"""Pins of the CPU oracle to things other than itself (CPU only).
+
+* reverse-mode autograd of the gradient-stopped network (the paper's own
+  check, Table II: e-prop equals BPTT when H_E is dropped);
+* central finite differences of the loss in a smooth-spike network where the
+  gradient stops cut nothing (no recurrence, no reset), Eq. (3) being then the
+  exact gradient;
+* finite differences on the readout weights of the spiking network, whose
+  spikes do not depend on the readout;
+* closed forms and special cases: one step, a single sub-threshold neuron,
+  the adaptation sum, silent inputs, beta = 0, batch symmetries;
+* memory independent of sequence length (Table I, Sec. III-A).
+"""
+import math
+import os
+import resource
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2501_11407_amd import synth
+from tests.bptt_torch import bptt_grads, rel_l2
+
+f32 = synth.f32
+
+
+def small(**kw):
+    base = dict(batch=3, n_in=37, n_rec=29, n_out=5, T=80, recurrent=1, n_adaptive=0)
+    base.update(kw)
+    return synth.EpropShape(**base)
+
+
+# Distinct alpha, kappa, rho so that swapping two of them changes the result.
+DISTINCT = dict(alpha=f32(math.exp(-1 / 20)), kappa=f32(math.exp(-1 / 7)), rho=f32(math.exp(-1 / 50)))
+
+AUTOGRAD_CASES = {
+    "ff_lif_b4_n32_t50": (synth.WORKLOADS["ff_lif_b4_n32_t50"], 1, 1.0),
+    "rlif_ragged": (small(**DISTINCT), 2, 4.0),
+    "ralif_ragged": (small(T=120, n_adaptive=13, **DISTINCT), 3, 4.0),
+    "ralif_all_adaptive": (small(T=60, n_adaptive=29, **DISTINCT), 5, 4.0),
+    "ff_alif": (small(T=70, recurrent=0, n_adaptive=11, **DISTINCT), 6, 4.0),
+    "ralif2_two_layers": (small(batch=2, n_in=21, n_rec=19, n_out=4, T=90, n_layers=2,
+                                n_adaptive=9, **DISTINCT), 4, 4.0),
+    # Full recurrent-LIF workload: B=32, 700 in, 256 neurons, T=250.
+    "rlif_b32_n256_t250": (synth.WORKLOADS["rlif_b32_n256_t250"], 2, 1.0),
+    # The recurrent-ALIF shape (700 in, 512 neurons, 204 adaptive) with B=6, T=120.
+    "ralif_n512_b6_t120": (synth.WORKLOADS["ralif_b64_n512_t500"].replace(batch=6, T=120), 3, 1.0),
+}
+
+
+@pytest.mark.parametrize("name", list(AUTOGRAD_CASES))
+def test_oracle_equals_backprop_with_stop_gradients(name):
+    shape, seed, scale = AUTOGRAD_CASES[name]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    dW, dWout, loss = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels)
+    assert r.spikes.any(), "workload produced no spikes; the check would be vacuous"
+    assert abs(r.loss - loss) <= 1e-12 * abs(loss)
+    for l in range(shape.n_layers):
+        assert np.abs(dW[l]).max() > 0
+        assert rel_l2(r.dW[l], dW[l]) <= 1e-11, (l, rel_l2(r.dW[l], dW[l]))
+        assert rel_l2(r.dWout[l], dWout[l]) <= 1e-11
+
+
+def test_recurrence_breaks_exactness():
+    # Without the stops the true surrogate gradient differs: the stops are real.
+    shape, seed, scale = AUTOGRAD_CASES["ralif_ragged"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    dW, _, _ = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels, stop=False)
+    assert rel_l2(r.dW[0], dW[0]) > 1e-3
+
+
+def test_fp32_and_fp64_forward_agree():
+    shape, seed, scale = AUTOGRAD_CASES["ralif_ragged"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    r32 = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=True)
+    r64 = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    assert np.array_equal(r32.spikes, r64.spikes)
+    assert rel_l2(r32.dW[0], r64.dW[0]) < 1e-5
+
+
+# ---------------------------------------------------------------- finite differences
+H = 2.0 ** -20          # exactly representable step on weights that sit on a 2**-10 grid
+
+
+def _grid(a):
+    return (np.round(np.asarray(a) * 1024) / 1024).astype(np.float32)
+
+
+def _fd(shape, W, Wout, x, labels, which, layer, idx, **kw):
+    def loss_at(delta):
+        Ws = [w.copy() for w in W]
+        Wos = [w.copy() for w in Wout]
+        tgt = Ws if which == "W" else Wos
+        tgt[layer][idx] += delta
+        assert tgt[layer][idx] - (W if which == "W" else Wout)[layer][idx] == delta
+        return oracle.run(shape, Ws, Wos, x, labels, want_spikes=False, **kw).loss
+    return (loss_at(H) - loss_at(-H)) / (2 * H)
+
+
+def _smooth_case(n_layers=1, seed=7):
+    shape = synth.EpropShape(batch=2, n_in=3, n_rec=4, n_out=3, T=12, recurrent=1, n_adaptive=2,
+                             n_layers=n_layers, alpha=f32(math.exp(-1 / 6)),
+                             kappa=f32(math.exp(-1 / 5)), rho=f32(math.exp(-1 / 9)))
+    rng = np.random.default_rng(seed)
+    W, Wout = [], []
+    for l in range(n_layers):
+        n_in_l = 3 if l == 0 else 4
+        w = _grid(rng.normal(0.4, 0.8, size=(4, n_in_l + 4)))
+        w[:, n_in_l:] = 0.0     # no recurrent influence at the base point
+        W.append(w)
+        Wout.append(_grid(rng.normal(0, 1, size=(3, 4))))
+    x = (rng.random((12, 2, 3)) < 0.5).astype(np.uint8)
+    labels = np.array([1, 2], dtype=np.int32)
+    return shape, W, Wout, x, labels
+
+
+@pytest.mark.parametrize("n_layers", [1, 2])
+def test_finite_differences_smooth_network(n_layers):
+    # Smooth spikes z = S(v - A), S' = psi; reset amount 0; W_rec = 0 at the
+    # base point.  Then no gradient stop cuts a live path and the forward
+    # recursion yields the exact gradient of the loss.  In a two-layer stack
+    # only layer 2 is checked: layer-1 weights also reach layer 2's loss, a
+    # path the method cuts on purpose.
+    shape, W, Wout, x, labels = _smooth_case(n_layers)
+    kw = dict(fwd_fp32=False, smooth=True, reset=0.0)
+    base = oracle.run(shape, W, Wout, x, labels, want_spikes=False, **kw)
+    layer = n_layers - 1
+    n_in_l = 3 if layer == 0 else 4
+    fd = np.zeros_like(base.dW[layer])
+    for j in range(4):
+        for i in range(W[layer].shape[1]):
+            if i == n_in_l + j:
+                continue                    # the diagonal is not a parameter
+            fd[j, i] = _fd(shape, W, Wout, x, labels, "W", layer, (j, i), **kw)
+    assert np.abs(fd[:, n_in_l:]).max() > 0   # recurrent columns carry gradient
+    assert rel_l2(base.dW[layer], fd) <= 1e-7
+    fdo = np.zeros_like(base.dWout[layer])
+    for k in range(3):
+        for j in range(4):
+            fdo[k, j] = _fd(shape, W, Wout, x, labels, "Wout", layer, (k, j), **kw)
+    assert rel_l2(base.dWout[layer], fdo) <= 1e-7
+
+
+@pytest.mark.parametrize("case", ["ff_lif_b4_n32_t50", "ralif_ragged"])
+def test_finite_differences_readout_of_spiking_network(case):
+    # Spikes do not depend on W_out, so the loss is smooth in W_out and
+    # dW_out = sum_t delta^t ztilde^t is exact.
+    shape, seed, scale = AUTOGRAD_CASES[case]
+    shape = shape.replace(T=min(shape.T, 40), batch=2)
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    Wout = [_grid(w) for w in wl.Wout]
+    base = oracle.run(shape, wl.W, Wout, wl.x, wl.labels, fwd_fp32=True, want_spikes=False)
+    rng = np.random.default_rng(0)
+    for _ in range(12):
+        k, j = int(rng.integers(shape.n_out)), int(rng.integers(shape.n_rec))
+        fd = _fd(shape, wl.W, Wout, wl.x, wl.labels, "Wout", 0, (k, j), fwd_fp32=True)
+        assert abs(fd - base.dWout[0][k, j]) <= 1e-7 * max(1.0, abs(fd))
+
+
+# ---------------------------------------------------------------- closed forms
+def test_single_step_closed_form():
+    # T = 1: zbar = p, eps^a = 0, ebar = e = psi p, so dW = sum_b (L psi)_b p_b^T
+    # and dW_out = sum_b delta_b z_b^T, from v = W p, x = v - thr.
+    shape = small(T=1, n_adaptive=10, **DISTINCT)
+    wl = synth.make_workload(shape, 11, input_scale=8.0)
+    wl.W[0] *= 4.0        # strong drive so that one step both spikes and stays sub-threshold
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    p = np.concatenate([wl.x[0].astype(np.float64), np.zeros((shape.batch, shape.n_rec))], axis=1)
+    v = p @ wl.W[0].astype(np.float64).T
+    xm = v - shape.thr
+    psi = shape.gamma / shape.thr * np.maximum(0.0, 1.0 - np.abs(xm) / shape.thr)
+    z = (xm > 0).astype(np.float64)
+    y = z @ wl.Wout[0].astype(np.float64).T
+    pi = np.exp(y - y.max(1, keepdims=True))
+    pi /= pi.sum(1, keepdims=True)
+    delta = pi - np.eye(shape.n_out)[wl.labels]
+    L = delta @ wl.Wout[0].astype(np.float64)
+    dW = (L * psi).T @ p
+    idx = np.arange(shape.n_rec)
+    dW[idx, shape.n_in + idx] = 0.0
+    assert z.any() and psi.any()
+    assert rel_l2(r.dW[0], dW) < 1e-13
+    assert rel_l2(r.dWout[0], delta.T @ z) < 1e-13
+
+
+def test_single_neuron_membrane_closed_form():
+    # One input channel into one LIF neuron below threshold:
+    # v^t = w * sum_{s<=t} alpha^(t-s) x^s.
+    shape = synth.EpropShape(batch=1, n_in=1, n_rec=1, n_out=2, T=60, recurrent=0, n_adaptive=0)
+    rng = np.random.default_rng(3)
+    x = (rng.random((60, 1, 1)) < 0.3).astype(np.uint8)
+    w = 0.0390625
+    r = oracle.run(shape, [np.array([[w]], np.float32)], [np.array([[0.5], [-0.25]], np.float32)],
+                   x, np.array([0], np.int32), fwd_fp32=False, want_record=True)
+    t = np.arange(60)
+    expect = np.array([w * sum(shape.alpha ** (tt - s) * x[s, 0, 0] for s in range(tt + 1)) for tt in t])
+    assert expect.max() < shape.thr
+    np.testing.assert_allclose(r.record["v"][:, 0, 0, 0], expect, rtol=1e-12, atol=1e-15)
+
+
+def test_adaptation_closed_form():
+    # ALIF: a^t = sum_{s<t} rho^(t-1-s) z^s and the threshold is thr + beta a^t.
+    shape = synth.EpropShape(batch=1, n_in=2, n_rec=3, n_out=2, T=80, recurrent=0, n_adaptive=3,
+                             rho=f32(math.exp(-1 / 30)))
+    rng = np.random.default_rng(5)
+    x = (rng.random((80, 1, 2)) < 0.6).astype(np.uint8)
+    W = [np.array([[1.25, 0.5], [0.75, 1.0], [2.0, 0.25]], np.float32)]
+    r = oracle.run(shape, W, [np.ones((2, 3), np.float32)], x, np.array([1], np.int32),
+                   fwd_fp32=False, want_record=True)
+    z = r.record["z"][:, 0, 0, :]
+    a = r.record["a"][:, 0, 0, :]
+    assert z.sum() > 5
+    for t in range(80):
+        expect = sum(shape.rho ** (t - 1 - s) * z[s] for s in range(t))
+        np.testing.assert_allclose(a[t], expect, rtol=1e-12, atol=1e-15)
+
+
+def test_beta_zero_alif_is_lif_bitwise():
+    shape = small(T=50, **DISTINCT)
+    wl = synth.make_workload(shape, 9, input_scale=4.0)
+    lif = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels)
+    alif0 = oracle.run(shape.replace(n_adaptive=shape.n_rec, beta=0.0), wl.W, wl.Wout, wl.x, wl.labels)
+    assert np.array_equal(lif.spikes, alif0.spikes)
+    assert np.array_equal(lif.dW[0], alif0.dW[0])
+    assert np.array_equal(lif.dWout[0], alif0.dWout[0])
+
+
+def test_silent_input():
+    # No input spikes: v = 0, psi = gamma*max(0, 1 - 1) = 0, no spikes, no
+    # gradient, and the loss is that of a uniform prediction, log K per step.
+    shape = small(T=30, n_adaptive=7)
+    wl = synth.make_workload(shape, 4, input_scale=0.0)
+    assert not wl.x.any()
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels)
+    assert not r.spikes.any()
+    assert not r.dW[0].any() and not r.dWout[0].any()
+    assert abs(r.loss - shape.batch * shape.T * math.log(shape.n_out)) < 1e-9
+
+
+def test_batch_symmetries():
+    shape = small(T=40, n_adaptive=9, **DISTINCT)
+    wl = synth.make_workload(shape, 12, input_scale=4.0)
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels)
+    perm = np.array([2, 0, 1])
+    rp = oracle.run(shape, wl.W, wl.Wout, wl.x[:, perm], wl.labels[perm])
+    assert rel_l2(rp.dW[0], r.dW[0]) < 1e-14
+    assert np.array_equal(rp.spikes, r.spikes[:, :, perm])
+    s2 = shape.replace(batch=6)
+    rd = oracle.run(s2, wl.W, wl.Wout, np.concatenate([wl.x, wl.x], 1), np.concatenate([wl.labels] * 2))
+    assert rel_l2(rd.dW[0], 2 * r.dW[0]) < 1e-14
+    assert abs(rd.loss - 2 * r.loss) < 1e-12 * abs(r.loss)
+
+
+def test_shards_and_samples_agree_with_full_run():
+    shape = small(batch=5, T=40, n_layers=2, n_adaptive=9, **DISTINCT)
+    wl = synth.make_workload(shape, 13, input_scale=4.0)
+    full = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels)
+    sh = oracle.run_sharded(shape, wl.W, wl.Wout, wl.x, wl.labels, workers=3)
+    assert np.array_equal(sh.spikes, full.spikes)
+    for l in range(2):
+        assert rel_l2(sh.dW[l], full.dW[l]) < 1e-14
+        assert rel_l2(sh.dWout[l], full.dWout[l]) < 1e-14
+    rng = np.random.default_rng(1)
+    smp = np.array([[l, rng.integers(shape.n_rec), rng.integers(shape.n_pre(l))]
+                    for l in (0, 1) for _ in range(20)]
+                   + [[0, 3, shape.n_in + 3], [1, 0, 0]], dtype=np.int32)
+    rs = oracle.run_sharded(shape, wl.W, wl.Wout, wl.x, wl.labels, workers=2, sample=smp)
+    expect = np.array([full.dW[l][j, i] for l, j, i in smp])
+    np.testing.assert_allclose(rs.dW[0], expect, rtol=1e-13, atol=1e-300)
+
+
+# ---------------------------------------------------------------- memory independent of T
+def test_state_bytes_has_no_sequence_length():
+    # The state is the per-synapse eligibility (ebar for every synapse, eps^a
+    # for adaptive neurons) plus O(N) vectors: O(n) per synapse row, no T.
+    shape = synth.WORKLOADS["ralif_b128_n1024_t1000"]
+    n_pre = shape.n_pre(0)
+    b = oracle.state_bytes(shape)
+    trace = 8 * n_pre * (shape.n_rec + shape.n_adaptive)
+    assert trace <= b < trace + 200_000
+
+
+_RSS_PROBE = r"""
+import sys
+sys.path.insert(0, {root!r})
+import numpy as np, oracle
+from paper_2501_11407_amd import synth
+
+def status(key):
+    for line in open("/proc/self/status"):
+        if line.startswith(key):
+            return int(line.split()[1])   # KiB
+
+T = int(sys.argv[1])
+shape = synth.EpropShape(batch=1, n_in=500, n_rec=1200, n_out=4, T=T, n_adaptive=600)
+wl = synth.make_workload(shape, 1, input_scale=0.2)
+oracle.load()
+with open("/proc/self/clear_refs", "w") as f:
+    f.write("5")                      # reset the peak-RSS mark
+before = status("VmRSS:")
+oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, want_spikes=False)
+print(status("VmHWM:") - before)
+"""
+
+
+def test_peak_memory_independent_of_sequence_length():
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = _RSS_PROBE.format(root=root)
+    grow = {}
+    for T in (10, 200):
+        out = subprocess.run([sys.executable, "-c", code, str(T)], capture_output=True, text=True,
+                             check=True)
+        grow[T] = int(out.stdout.strip().splitlines()[-1])   # KiB
+    # ~28 MB of trace state either way; a per-step record would add T-fold.
+    assert grow[10] > 20_000
+    assert abs(grow[200] - grow[10]) < 2_000, grow
