@@ -1,0 +1,185 @@
+/*
+ * eprop.h -- C ABI of the MI355X (gfx950) online e-prop library.
+ *
+ * The library runs the per-timestep hot path of gradient-based synaptic
+ * plasticity (arxiv 2501.11407) for recurrent spiking networks of LIF and
+ * ALIF neurons: the synaptic drive, the neuron step with its surrogate
+ * pseudo-derivative, the per-synapse eligibility-vector update and the
+ * learning-signal-weighted gradient accumulation.
+ *
+ * The calls follow the paper's statement of the problem (Sec. III-A):
+ *   - Eq. (1): a state recursion h_{t+1} = f(h_t, x_t, theta) driven by the
+ *     inputs x_t  -> eprop_step / eprop_run_sequence;
+ *   - Eq. (2): a loss that is a sum of per-step losses (softmax cross-entropy
+ *     of a leaky non-spiking readout at every step);
+ *   - Eq. (3) with the recursion of Eq. (5): the gradient accumulated forward
+ *     in time, G_t = H_t G_{t-1} + F_t, with H_t restricted to its diagonal
+ *     neuron-on-itself part (Sec. III-B), so that the state the library keeps
+ *     does not depend on the sequence length  -> eprop_get_grads.
+ *
+ * Model (per layer, per batch element b, per step t; j = neuron, i = input):
+ *   p^t      = [in^t ; z^{t-1}]            (in = x for layer 0, layer-1 spikes of
+ *                                           the same step for layer 1; no z part
+ *                                           when recurrent == 0)
+ *   v^t_j    = alpha v^{t-1}_j + sum_i W_ji p^t_i - thr z^{t-1}_j
+ *   a^t_j    = rho a^{t-1}_j + z^{t-1}_j ;  A_j = thr + beta_j a^t_j
+ *              (beta_j = beta for j < n_adaptive, else 0)
+ *   z^t_j    = [v^t_j - A_j > 0] ;  psi_j = (gamma/thr) max(0, 1 - |v_j - A_j|/thr)
+ *   y^t      = kappa y^{t-1} + W_out z^t ;  loss += CE(softmax(y^t), label_b)
+ * Gradient stops: the recurrent spikes z^{t-1} in the drive and the reset,
+ * and (two layers) the layer-1 spikes fed to layer 2.  Each layer learns from
+ * its own readout.  The gradient is dE/dW for E = sum_b sum_t sum_layers CE,
+ * not averaged; the recurrent diagonal (self-connections) is reported as 0.
+ *
+ * Memory: every device buffer belongs to the caller.  The library works in
+ * one caller-provided device workspace whose size depends on the shape but
+ * not on the sequence length, and borrows the weight buffers until
+ * eprop_destroy.
+ *
+ * Streams: every call that takes a context enqueues work on the stream given
+ * to eprop_init and returns without waiting, except eprop_status and
+ * eprop_profile_end, which wait for that stream.  A context belongs to one
+ * stream and one host thread at a time.
+ */
+#ifndef EPROP_H
+#define EPROP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define EPROP_OK 0
+#define EPROP_EINVAL (-1)   /* null pointer, bad dimension or constant, T < 1 */
+#define EPROP_ENOSPACE (-2) /* workspace smaller than eprop_workspace_bytes */
+#define EPROP_EDEVICE (-3)  /* HIP runtime or launch error; see eprop_last_error */
+#define EPROP_ESTATE (-4)   /* context not initialised, or a device-side input error */
+
+typedef struct eprop_ctx eprop_ctx; /* opaque, host-side */
+
+/* Network shape and constants.  All constants are used as given, in fp32. */
+typedef struct {
+  int32_t n_layers;   /* 1, or 2 for a stack fed layer-1 spikes of the same step */
+  int32_t batch;      /* B >= 1 */
+  int32_t n_in;       /* inputs of layer 0 */
+  int32_t n_rec;      /* neurons per layer */
+  int32_t n_out;      /* readout classes K */
+  int32_t recurrent;  /* 1: presynaptic vector [in ; z^{t-1}], 0: in only */
+  int32_t n_adaptive; /* neurons j < n_adaptive are ALIF (0 <= n_adaptive <= n_rec) */
+  float alpha;        /* membrane decay exp(-dt/tau_m), Eq. (8a) */
+  float rho;          /* adaptation decay */
+  float kappa;        /* readout decay */
+  float thr;          /* threshold theta > 0, also the reset amount */
+  float beta;         /* threshold adaptation strength of ALIF neurons */
+  float gamma;        /* surrogate height */
+} eprop_config;
+
+/*
+ * Bytes of device workspace a context with this shape needs; 0 if the
+ * configuration is invalid.  There is no sequence-length argument: the
+ * e-prop state is O(B * N_pre * N_post) and independent of T (Table I).
+ */
+size_t eprop_workspace_bytes(const eprop_config* cfg);
+
+/*
+ * Creates a context in the caller's device workspace (>= 256-byte aligned,
+ * at least eprop_workspace_bytes(cfg) bytes) and copies the weights into it.
+ *   d_weights: host array of 2*n_layers device pointers, per layer l:
+ *     d_weights[2l]   = W     fp32 [n_rec][n_pre_l] row-major, n_pre_l =
+ *                       n_in_l + (recurrent ? n_rec : 0), columns [W_in | W_rec]
+ *     d_weights[2l+1] = W_out fp32 [n_out][n_rec] row-major
+ *   The weights are read here and again by every eprop_reset, and must not be
+ *   freed before eprop_destroy.
+ *   hip_stream: a hipStream_t (NULL = the null stream).
+ * State, traces and accumulators start at zero.  On success *out is the new
+ * context and 0 is returned; on failure *out is NULL and the reason is in
+ * eprop_last_error(NULL).
+ */
+int eprop_init(const eprop_config* cfg, void* d_workspace, size_t ws_bytes,
+               const float* const* d_weights, void* hip_stream, eprop_ctx** out);
+
+/*
+ * One online e-prop step (one timestep) for every layer:
+ *   d_x_t:     device uint8 [B][n_in]; a nonzero byte is an input spike
+ *   d_labels:  device int32 [B], class of each batch element, in [0, n_out)
+ *              (an out-of-range label is a device-side error reported by
+ *              eprop_status; its step gets no target term)
+ *   d_spikes_t: NULL, or device uint32 [n_layers][B][ceil(n_rec/32)] receiving
+ *              the step's spikes, bit j%32 of word j/32
+ * Updates the neuron state, the eligibility vectors and the gradient
+ * accumulators in the workspace.
+ */
+int eprop_step(eprop_ctx* ctx, const uint8_t* d_x_t, const int32_t* d_labels,
+               uint32_t* d_spikes_t);
+
+/*
+ * T >= 1 consecutive steps, identical to T calls of eprop_step:
+ *   d_x: device uint8 [T][B][n_in];  d_labels: as for eprop_step, used at
+ *   every step;  d_spikes: NULL or device uint32 [T][n_layers][B][ceil(n_rec/32)].
+ * Calls may be chained: a sequence split into several calls gives the same
+ * state and gradients as one call.
+ */
+int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int32_t* d_labels,
+                       uint32_t* d_spikes);
+
+/*
+ * Writes the gradient accumulated since the last reset, summed over batch
+ * elements and steps:
+ *   d_grads: host array of 2*n_layers device pointers, per layer l:
+ *     d_grads[2l] = dE/dW fp32 [n_rec][n_pre_l] (layout of W; the recurrent
+ *                   diagonal is 0), d_grads[2l+1] = dE/dW_out fp32 [n_out][n_rec]
+ *   d_loss: NULL or device double[1] receiving E = sum of the per-step losses.
+ * Accumulation happens in fp64 and is rounded to fp32 here.  The context
+ * keeps accumulating; the caller synchronises the stream before reading.
+ */
+int eprop_get_grads(eprop_ctx* ctx, float* const* d_grads, double* d_loss);
+
+/*
+ * Starts a new sequence: zeroes neuron state, filters, eligibility vectors,
+ * gradient and loss accumulators, and re-reads the weights.
+ */
+int eprop_reset(eprop_ctx* ctx);
+
+/*
+ * Waits for the context's stream and reports device-side input errors seen
+ * since the last reset: EPROP_ESTATE if a label was out of range, else 0 (or
+ * EPROP_EDEVICE on a runtime error).
+ */
+int eprop_status(eprop_ctx* ctx);
+
+/* Frees the host-side context; the workspace and weights stay the caller's. */
+void eprop_destroy(eprop_ctx* ctx);
+
+/*
+ * Message of the last failure on ctx, or of the last failed eprop_init /
+ * workspace query of this thread when ctx is NULL.  Never NULL.
+ */
+const char* eprop_last_error(const eprop_ctx* ctx);
+
+/*
+ * Kernel timing.  eprop_profile_begin makes the next steps record a pair of
+ * HIP events, on the context's stream, around each launch of the eligibility
+ * kernel (at most max_launches pairs).  eprop_profile_end waits for the
+ * stream and returns the summed duration in milliseconds and the number of
+ * timed launches, then stops recording.
+ */
+int eprop_profile_begin(eprop_ctx* ctx, int32_t max_launches);
+int eprop_profile_end(eprop_ctx* ctx, double* total_ms, int32_t* n_launches);
+
+/*
+ * Diagnostics: device address and shape of one internal per-neuron buffer of
+ * layer `layer` as left by the last step, for checking intermediate values.
+ *   which: 0 = v, 1 = a, 2 = psi, 3 = L (learning signal), 4 = y (readout)
+ *   fp32, rows = B, row stride *ld elements, *cols valid columns.
+ */
+int eprop_debug_buffer(eprop_ctx* ctx, int32_t layer, int32_t which, const float** d_ptr,
+                       int64_t* cols, int64_t* ld);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EPROP_H */

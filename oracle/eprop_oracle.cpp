@@ -171,7 +171,7 @@ int run(const oracle_config& c, const float* const* W, const float* const* Wout,
         // Presynaptic vector p^t = [input^t ; z^{t-1}] and its alpha filter:
         // the eps^v component of G_t, since dv/dv = alpha and dv/dW_ji = p_i.
         for (int i = 0; i < s.n_in_l; ++i)
-          s.p[i] = (l == 0) ? (double)x[((size_t)t * B + b) * c.n_in + i] : st[l - 1].z[i];
+          s.p[i] = (l == 0) ? (x[((size_t)t * B + b) * c.n_in + i] ? 1.0 : 0.0) : st[l - 1].z[i];
         if (c.recurrent)
           for (int j = 0; j < N; ++j) s.p[s.n_in_l + j] = s.z_prev[j];
         for (int i = 0; i < s.n_pre; ++i) s.zbar[i] = c.alpha * s.zbar[i] + s.p[i];
@@ -333,7 +333,7 @@ size_t oracle_state_bytes(const oracle_config* c, int32_t n_sample) {
 // Runs batch elements [b_lo, b_hi) over T steps and ADDS their gradient into
 // the caller's fp64 buffers (zero them first to get dE/dW of those elements).
 //   W[l]: [n_rec][n_pre_l] fp32 = [W_in | W_rec];  Wout[l]: [n_out][n_rec] fp32
-//   x: [T][batch][n_in] bytes in {0,1};  labels: [batch]
+//   x: [T][batch][n_in] bytes, nonzero = spike;  labels: [batch]
 //   sample: NULL with n_sample < 0 for every synapse, dW[l] = [n_rec][n_pre_l];
 //           else n_sample triples (layer, j, i) and dW[0] = [n_sample]
 //   spikes: NULL or [T][n_layers][batch][ceil(n_rec/32)], bit j%32 of word j/32

@@ -1,0 +1,270 @@
+"""Thin ctypes binding of the e-prop C ABI (include/eprop.h).
+
+Argument marshalling only: every step of the hot path runs in the HIP kernels
+of libeprop.so.  PyTorch supplies device memory (the workspace, inputs and
+outputs are CUDA/HIP tensors) and the current stream.  There is no CPU
+fallback: without the built library or a GPU the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence, Tuple
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libeprop.so")
+
+EPROP_OK, EPROP_EINVAL, EPROP_ENOSPACE, EPROP_EDEVICE, EPROP_ESTATE = 0, -1, -2, -3, -4
+
+# Every function the header declares, in declaration order.
+SYMBOLS = (
+    "eprop_workspace_bytes", "eprop_init", "eprop_step", "eprop_run_sequence", "eprop_get_grads",
+    "eprop_reset", "eprop_status", "eprop_destroy", "eprop_last_error", "eprop_profile_begin",
+    "eprop_profile_end", "eprop_debug_buffer",
+)
+
+
+class eprop_config(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("batch", ctypes.c_int32), ("n_in", ctypes.c_int32),
+        ("n_rec", ctypes.c_int32), ("n_out", ctypes.c_int32), ("recurrent", ctypes.c_int32),
+        ("n_adaptive", ctypes.c_int32),
+        ("alpha", ctypes.c_float), ("rho", ctypes.c_float), ("kappa", ctypes.c_float),
+        ("thr", ctypes.c_float), ("beta", ctypes.c_float), ("gamma", ctypes.c_float),
+    ]
+
+
+class EpropError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"e-prop error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Loads libeprop.so; raises if it was not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2501_11407_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    cfgp = ctypes.POINTER(eprop_config)
+    sig = {
+        "eprop_workspace_bytes": (ctypes.c_size_t, [cfgp]),
+        "eprop_init": (ctypes.c_int, [cfgp, vp, ctypes.c_size_t, vp, vp, ctypes.POINTER(vp)]),
+        "eprop_step": (ctypes.c_int, [vp, vp, vp, vp]),
+        "eprop_run_sequence": (ctypes.c_int, [vp, vp, i32, vp, vp]),
+        "eprop_get_grads": (ctypes.c_int, [vp, vp, vp]),
+        "eprop_reset": (ctypes.c_int, [vp]),
+        "eprop_status": (ctypes.c_int, [vp]),
+        "eprop_destroy": (None, [vp]),
+        "eprop_last_error": (ctypes.c_char_p, [vp]),
+        "eprop_profile_begin": (ctypes.c_int, [vp, i32]),
+        "eprop_profile_end": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double),
+                                             ctypes.POINTER(i32)]),
+        "eprop_debug_buffer": (ctypes.c_int, [vp, i32, i32, ctypes.POINTER(vp),
+                                              ctypes.POINTER(i64), ctypes.POINTER(i64)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype, fn.argtypes = res, args
+    _lib = lib
+    return lib
+
+
+def make_config(shape) -> eprop_config:
+    """C config from an EpropShape (or any object with the same fields)."""
+    return eprop_config(shape.n_layers, shape.batch, shape.n_in, shape.n_rec, shape.n_out,
+                        shape.recurrent, shape.n_adaptive, shape.alpha, shape.rho, shape.kappa,
+                        shape.thr, shape.beta, shape.gamma)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _ptr_array(ts: Sequence[torch.Tensor]):
+    return (ctypes.c_void_p * len(ts))(*[t.data_ptr() for t in ts])
+
+
+def eprop_workspace_bytes(cfg: eprop_config) -> int:
+    return int(load_library().eprop_workspace_bytes(ctypes.byref(cfg)))
+
+
+def eprop_last_error(ctx=None) -> str:
+    return load_library().eprop_last_error(ctx).decode()
+
+
+def _check(rc: int, ctx=None):
+    if rc != EPROP_OK:
+        raise EpropError(rc, eprop_last_error(ctx))
+
+
+def eprop_init(cfg: eprop_config, workspace: torch.Tensor, weights: Sequence[torch.Tensor],
+               stream: Optional[torch.cuda.Stream] = None):
+    """weights: [W_0, Wout_0, (W_1, Wout_1)] fp32 contiguous device tensors."""
+    lib = load_library()
+    for w in weights:
+        assert w.is_cuda and w.dtype == torch.float32 and w.is_contiguous()
+    s = (stream or torch.cuda.current_stream()).cuda_stream
+    ctx = ctypes.c_void_p()
+    rc = lib.eprop_init(ctypes.byref(cfg), _ptr(workspace), workspace.numel(),
+                        _ptr_array(weights), ctypes.c_void_p(s), ctypes.byref(ctx))
+    _check(rc)
+    return ctx
+
+
+def eprop_step(ctx, x_t: torch.Tensor, labels: torch.Tensor, spikes_t: Optional[torch.Tensor] = None):
+    _check(load_library().eprop_step(ctx, _ptr(x_t), _ptr(labels), _ptr(spikes_t)), ctx)
+
+
+def eprop_run_sequence(ctx, x: torch.Tensor, T: int, labels: torch.Tensor,
+                       spikes: Optional[torch.Tensor] = None):
+    _check(load_library().eprop_run_sequence(ctx, _ptr(x), int(T), _ptr(labels), _ptr(spikes)), ctx)
+
+
+def eprop_get_grads(ctx, grads: Sequence[torch.Tensor], loss: Optional[torch.Tensor] = None):
+    _check(load_library().eprop_get_grads(ctx, _ptr_array(grads), _ptr(loss)), ctx)
+
+
+def eprop_reset(ctx):
+    _check(load_library().eprop_reset(ctx), ctx)
+
+
+def eprop_status(ctx) -> int:
+    return int(load_library().eprop_status(ctx))
+
+
+def eprop_destroy(ctx):
+    load_library().eprop_destroy(ctx)
+
+
+def eprop_profile_begin(ctx, max_launches: int):
+    _check(load_library().eprop_profile_begin(ctx, int(max_launches)), ctx)
+
+
+def eprop_profile_end(ctx) -> Tuple[float, int]:
+    ms, n = ctypes.c_double(), ctypes.c_int32()
+    _check(load_library().eprop_profile_end(ctx, ctypes.byref(ms), ctypes.byref(n)), ctx)
+    return ms.value, n.value
+
+
+def eprop_debug_buffer(ctx, layer: int, which: int) -> Tuple[int, int, int]:
+    ptr, cols, ld = ctypes.c_void_p(), ctypes.c_int64(), ctypes.c_int64()
+    _check(load_library().eprop_debug_buffer(ctx, layer, which, ctypes.byref(ptr),
+                                             ctypes.byref(cols), ctypes.byref(ld)), ctx)
+    return ptr.value, cols.value, ld.value
+
+
+class EpropContext:
+    """One network on one GPU: workspace, borrowed weights and the C context.
+
+    All work is queued on the stream that is current at construction.
+    """
+
+    DEBUG = {"v": 0, "a": 1, "psi": 2, "L": 3, "y": 4}
+
+    def __init__(self, shape, W: Sequence, Wout: Sequence, device: str = "cuda"):
+        if not torch.cuda.is_available():
+            raise RuntimeError("no GPU visible: the e-prop library runs only on the GPU")
+        self.shape = shape
+        self.cfg = make_config(shape)
+        self.device = torch.device(device)
+        nbytes = eprop_workspace_bytes(self.cfg)
+        if nbytes == 0:
+            raise EpropError(EPROP_EINVAL, eprop_last_error())
+        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=self.device)
+        off = (-self.workspace.data_ptr()) % 256
+        self.workspace = self.workspace[off:off + nbytes]
+        self.weights: List[torch.Tensor] = []
+        for l in range(shape.n_layers):
+            w = torch.as_tensor(W[l], dtype=torch.float32).to(self.device).contiguous()
+            wo = torch.as_tensor(Wout[l], dtype=torch.float32).to(self.device).contiguous()
+            if tuple(w.shape) != (shape.n_rec, shape.n_pre(l)):
+                raise ValueError(f"W[{l}] must be {(shape.n_rec, shape.n_pre(l))}, got {tuple(w.shape)}")
+            if tuple(wo.shape) != (shape.n_out, shape.n_rec):
+                raise ValueError(f"Wout[{l}] must be {(shape.n_out, shape.n_rec)}, got {tuple(wo.shape)}")
+            self.weights += [w, wo]
+        self.stream = torch.cuda.current_stream(self.device)
+        self.ctx = eprop_init(self.cfg, self.workspace, self.weights, self.stream)
+
+    # -- host-side checks: every buffer a kernel touches has the shape it assumes
+    def _check_dev(self, t, dtype, shape, what):
+        if not (isinstance(t, torch.Tensor) and t.device.type == "cuda" and t.dtype == dtype
+                and tuple(t.shape) == tuple(shape) and t.is_contiguous()):
+            got = (tuple(t.shape), t.dtype, t.device) if isinstance(t, torch.Tensor) else type(t)
+            raise ValueError(f"{what}: expected contiguous {dtype} {tuple(shape)} on the GPU, got {got}")
+
+    def _check_step_args(self, x, T, labels, spikes):
+        s = self.shape
+        self._check_dev(x, torch.uint8, ((T,) if T is not None else ()) + (s.batch, s.n_in), "x")
+        self._check_dev(labels, torch.int32, (s.batch,), "labels")
+        if spikes is not None:
+            w32 = (s.n_rec + 31) // 32
+            self._check_dev(spikes, torch.int32,
+                            ((T,) if T is not None else ()) + (s.n_layers, s.batch, w32), "spikes")
+
+    # -- the C calls
+    def step(self, x_t, labels, spikes_t=None):
+        self._check_step_args(x_t, None, labels, spikes_t)
+        eprop_step(self.ctx, x_t, labels, spikes_t)
+
+    def run_sequence(self, x, labels, spikes=None):
+        T = x.shape[0] if isinstance(x, torch.Tensor) and x.dim() == 3 else -1
+        self._check_step_args(x, T, labels, spikes)
+        eprop_run_sequence(self.ctx, x, T, labels, spikes)
+
+    def get_grads(self):
+        L, N, K = self.shape.n_layers, self.shape.n_rec, self.shape.n_out
+        grads = []
+        for l in range(L):
+            grads.append(torch.empty(N, self.shape.n_pre(l), dtype=torch.float32, device=self.device))
+            grads.append(torch.empty(K, N, dtype=torch.float32, device=self.device))
+        loss = torch.empty(1, dtype=torch.float64, device=self.device)
+        eprop_get_grads(self.ctx, grads, loss)
+        return grads[0::2], grads[1::2], loss
+
+    def reset(self):
+        eprop_reset(self.ctx)
+
+    def status(self) -> int:
+        return eprop_status(self.ctx)
+
+    def profile_begin(self, max_launches: int):
+        eprop_profile_begin(self.ctx, max_launches)
+
+    def profile_end(self):
+        return eprop_profile_end(self.ctx)
+
+    def debug(self, name: str, layer: int = 0) -> torch.Tensor:
+        """Copy of an internal per-neuron buffer [B, cols] after the last step."""
+        ptr, cols, ld = eprop_debug_buffer(self.ctx, layer, self.DEBUG[name])
+        off = ptr - self.workspace.data_ptr()
+        rows = self.shape.batch
+        flat = self.workspace[off:off + 4 * rows * ld].view(torch.float32)
+        return flat.view(rows, ld)[:, :cols].clone()
+
+    # -- helpers
+    def new_spike_buffer(self, T: Optional[int] = None) -> torch.Tensor:
+        w32 = (self.shape.n_rec + 31) // 32
+        shp = (self.shape.n_layers, self.shape.batch, w32)
+        if T is not None:
+            shp = (T,) + shp
+        return torch.zeros(shp, dtype=torch.int32, device=self.device)
+
+    def close(self):
+        if getattr(self, "ctx", None) is not None:
+            eprop_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

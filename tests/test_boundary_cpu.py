@@ -1,0 +1,96 @@
+"""The C-ABI library on the CPU (no GPU calls): it loads, exports every
+function include/eprop.h declares, and validates configurations host-side."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2501_11407_amd import eprop, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "eprop.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"\b(eprop_[a-z_]+)\s*\(", text)
+
+
+def test_header_and_binding_agree():
+    names = declared_functions()
+    assert len(names) == len(set(names))
+    assert tuple(names) == eprop.SYMBOLS
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(eprop.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
+    for name, shape in synth.WORKLOADS.items():
+        n = eprop.eprop_workspace_bytes(eprop.make_config(shape))
+        traces = sum(4 * shape.batch * shape.n_pre(l) * (shape.n_rec + shape.n_adaptive)
+                     for l in range(shape.n_layers))
+        assert traces <= n <= traces * 1.05 + (8 << 20), (name, n, traces)
+    # the same shape with any T needs the same workspace: T is not an input
+    s = synth.WORKLOADS["ralif_b64_n512_t500"]
+    assert eprop.eprop_workspace_bytes(eprop.make_config(s)) == \
+        eprop.eprop_workspace_bytes(eprop.make_config(s.replace(T=5)))
+
+
+@pytest.mark.parametrize("bad", [
+    dict(n_layers=3), dict(n_layers=0), dict(batch=0), dict(n_in=0), dict(n_rec=0),
+    dict(n_out=0), dict(n_adaptive=-1), dict(n_adaptive=30), dict(recurrent=2),
+    dict(thr=0.0), dict(alpha=float("nan")), dict(batch=70000),
+])
+def test_invalid_configs_are_rejected_on_the_host(bad):
+    shape = synth.EpropShape(batch=3, n_in=7, n_rec=29, n_out=5, T=10)
+    cfg = eprop.make_config(shape)
+    for k, v in bad.items():
+        setattr(cfg, k, v)
+    assert eprop.eprop_workspace_bytes(cfg) == 0
+    assert eprop.eprop_last_error() != ""
+    lib = eprop.load_library()
+    out = ctypes.c_void_p(1)
+    ws = ctypes.c_void_p(256)
+    w = (ctypes.c_void_p * 4)(256, 256, 256, 256)
+    rc = lib.eprop_init(ctypes.byref(cfg), ws, 1 << 40, w, None, ctypes.byref(out))
+    assert rc == eprop.EPROP_EINVAL and out.value is None
+
+
+def test_init_argument_errors_before_any_device_call():
+    shape = synth.EpropShape(batch=3, n_in=7, n_rec=29, n_out=5, T=10)
+    cfg = eprop.make_config(shape)
+    lib = eprop.load_library()
+    out = ctypes.c_void_p()
+    w = (ctypes.c_void_p * 2)(256, 256)
+    need = eprop.eprop_workspace_bytes(cfg)
+    assert lib.eprop_init(ctypes.byref(cfg), None, need, w, None, ctypes.byref(out)) == eprop.EPROP_EINVAL
+    assert lib.eprop_init(ctypes.byref(cfg), ctypes.c_void_p(257), need, w, None,
+                          ctypes.byref(out)) == eprop.EPROP_EINVAL      # misaligned
+    assert lib.eprop_init(ctypes.byref(cfg), ctypes.c_void_p(256), need - 1, w, None,
+                          ctypes.byref(out)) == eprop.EPROP_ENOSPACE
+    assert "workspace too small" in eprop.eprop_last_error()
+    w0 = (ctypes.c_void_p * 2)(256, None)
+    assert lib.eprop_init(ctypes.byref(cfg), ctypes.c_void_p(256), need, w0, None,
+                          ctypes.byref(out)) == eprop.EPROP_EINVAL
+    # calls on a missing context
+    assert lib.eprop_step(None, None, None, None) == eprop.EPROP_ESTATE
+    assert lib.eprop_reset(None) == eprop.EPROP_ESTATE
+    lib.eprop_destroy(None)
+
+
+def test_binding_refuses_to_run_without_a_gpu_or_library(monkeypatch):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is visible")
+    shape = synth.EpropShape(batch=1, n_in=2, n_rec=3, n_out=2, T=1)
+    with pytest.raises(RuntimeError):
+        eprop.EpropContext(shape, [None], [None])
+    monkeypatch.setattr(eprop, "_lib", None)
+    with pytest.raises(RuntimeError):
+        eprop.load_library("/nonexistent/libeprop.so")
