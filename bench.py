@@ -30,19 +30,17 @@ COUNTERS = os.path.join(ROOT, "profiles", "trace_kernel_counters.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2501_11407_amd", "csrc", "kernels.hip")
 
 
-def trace_bytes_per_launch(shape, layer: int, first: bool) -> int:
-    """Algorithmic HBM bytes of one eligibility-kernel launch: ebar (every
-    synapse) and eps^a (synapses onto adaptive neurons) read and written,
-    the fp64 accumulator of every (i, j) read and written, the per-step
-    vectors zbar [N_pre, B], psi and L [B, N_post] read once.  The first step
-    after a reset reads no traces or accumulators."""
+def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: int) -> int:
+    """Algorithmic HBM bytes of eligibility-kernel launches on one layer.
+    Per launch: ebar (every synapse) and eps^a (synapses onto adaptive
+    neurons) read once and written once, the fp64 accumulator of every (i, j)
+    read and written once; the first launch after a reset reads neither.  Per
+    timestep covered: the filtered presynaptic vector [N_pre, B] and psi, L
+    [B, N_post] read once."""
     B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
     npre = shape.n_pre(layer)
-    rw = 1 if first else 2
-    b = rw * 4 * B * npre * (N + NA)
-    b += rw * 8 * npre * N
-    b += 4 * (B * npre + 2 * B * N)
-    return b
+    trace = 4 * B * npre * (N + NA) + 8 * npre * N      # one direction
+    return (2 * launches - first_launches) * trace + steps * 4 * (B * npre + 2 * B * N)
 
 
 def source_digest() -> str:
@@ -115,30 +113,31 @@ def main():
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
-    n_launch = args.steps * shape.T * shape.n_layers
-    ctx.profile_begin(n_launch)
+    max_launch = args.steps * shape.T * shape.n_layers
+    ctx.profile_begin(max_launch)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         grads = one_step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    trace_ms, n_timed = ctx.profile_end()
-    assert n_timed == n_launch
+    trace_ms, n_timed, timed_steps = ctx.profile_end()
+    assert timed_steps == args.steps * shape.T * shape.n_layers
     assert ctx.status() == 0
     assert all(bool(torch.isfinite(g).all()) for g in grads[0] + grads[1])
 
     syn_steps = shape.syn_per_step() * shape.T * args.steps
     value = syn_steps / elapsed
-    alg_bytes = args.steps * sum(
-        trace_bytes_per_launch(shape, l, True) + (shape.T - 1) * trace_bytes_per_launch(shape, l, False)
-        for l in range(shape.n_layers))
+    per_layer_launches = n_timed // shape.n_layers
+    alg_bytes = sum(trace_bytes(shape, l, per_layer_launches, args.steps, args.steps * shape.T)
+                    for l in range(shape.n_layers))
     achieved = alg_bytes / (trace_ms * 1e-3) / 1e9
     traffic = stored_traffic(shape)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": "trace_kernel", "avg_launch_us": round(trace_ms * 1e3 / n_timed, 2),
-                "alg_bytes_per_launch": trace_bytes_per_launch(shape, 0, False)}
+                "steps_per_launch": round(timed_steps / n_timed, 2),
+                "alg_bytes_per_launch": round(alg_bytes / n_timed)}
     line = {
         "metric": "synapse-timestep e-prop updates/sec (B*N_pre*N_post*T/s) + % HBM peak",
         "value": value, "unit": "syn-steps/s", "n_gpus": 1, "steps": args.steps,

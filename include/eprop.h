@@ -116,11 +116,16 @@ int eprop_step(eprop_ctx* ctx, const uint8_t* d_x_t, const int32_t* d_labels,
                uint32_t* d_spikes_t);
 
 /*
- * T >= 1 consecutive steps, identical to T calls of eprop_step:
+ * T >= 1 consecutive steps, equivalent to T calls of eprop_step:
  *   d_x: device uint8 [T][B][n_in];  d_labels: as for eprop_step, used at
  *   every step;  d_spikes: NULL or device uint32 [T][n_layers][B][ceil(n_rec/32)].
- * Calls may be chained: a sequence split into several calls gives the same
- * state and gradients as one call.
+ * The steps are processed in blocks of consecutive timesteps: the forward
+ * dynamics never read the eligibility vectors, so the network is run ahead
+ * through a block and the traces then advance through all of its steps with
+ * one pass over them.  Spike trains, neuron state and traces are identical
+ * however a sequence is split into calls; the accumulated gradients agree up
+ * to the order of floating-point summation (relative differences ~1e-7).
+ * Identical call sequences give bit-identical results.
  */
 int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int32_t* d_labels,
                        uint32_t* d_spikes);
@@ -160,14 +165,15 @@ void eprop_destroy(eprop_ctx* ctx);
 const char* eprop_last_error(const eprop_ctx* ctx);
 
 /*
- * Kernel timing.  eprop_profile_begin makes the next steps record a pair of
+ * Kernel timing.  eprop_profile_begin makes the next calls record a pair of
  * HIP events, on the context's stream, around each launch of the eligibility
- * kernel (at most max_launches pairs).  eprop_profile_end waits for the
- * stream and returns the summed duration in milliseconds and the number of
- * timed launches, then stops recording.
+ * kernel (at most max_launches pairs; one launch advances the traces through
+ * a block of consecutive timesteps).  eprop_profile_end waits for the stream
+ * and returns the summed duration in milliseconds, the number of timed
+ * launches and the number of timesteps they covered, then stops recording.
  */
 int eprop_profile_begin(eprop_ctx* ctx, int32_t max_launches);
-int eprop_profile_end(eprop_ctx* ctx, double* total_ms, int32_t* n_launches);
+int eprop_profile_end(eprop_ctx* ctx, double* total_ms, int32_t* n_launches, int64_t* n_steps);
 
 /*
  * Diagnostics: device address and shape of one internal per-neuron buffer of

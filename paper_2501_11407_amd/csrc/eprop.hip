@@ -33,30 +33,35 @@ void choose_splits(int M, int N, int K, int max_splits, int* splits, int* k_chun
   *splits = (K + kc - 1) / kc;
 }
 
+// Timesteps per forward/eligibility block: the eligibility traces are read
+// and written once per block.  The workspace holds per-step vectors for this
+// many steps, independent of the sequence length.
+constexpr int kBlockSteps = 32;
+
 struct Layer {
   int n_inl = 0, n_pre = 0;
-  // padded extents
-  int kpad = 0;   // n_pre rounded to 16: drive GEMM K and row stride of P, Wp
-  int bpad = 0;   // batch rounded to 32: rows of P and Zf
-  int npad = 0;   // n_rec rounded to 32: rows of Wp
-  int nrk = 0;    // n_rec rounded to 16: readout GEMM K, row stride of Zf, Wop
-  int kout = 0;   // n_out rounded to 32: rows of Wop
-  int ldj = 0;    // n_rec rounded to 4: row stride of per-neuron buffers and traces
+  int ldj = 0;    // n_rec rounded to 4: row stride of per-neuron vectors and traces
   int lda = 0;    // n_adaptive rounded to 4: row stride of epsa
-  int ldz = 0;    // batch rounded to 4: row stride of zbarT
-  int s_drive = 1, kc_drive = 16, s_out = 1, kc_out = 16;
+  int kout = 0;   // n_out rounded to 32: rows of deltaK
+  int npad = 0;   // n_rec rounded to 32: rows of ztK
+  int rows_per_wave = 0;
   const float* W_src = nullptr;
   const float* Wout_src = nullptr;
-  float *Wp, *Wop, *P, *zbarT, *Ipart, *v, *a, *Zf, *psi, *L, *ztil, *Ypart, *y, *delta;
-  uint8_t* z[2];
-  double *lossacc, *acc, *accout;
-  float *ebar, *epsa;
+  float *Wt, *Wop;                       // packed weights
+  float *v, *a, *ztil, *zbar, *y;        // neuron, filter and readout state
+  uint8_t* z;                            // spikes of the last step
+  double* lossacc;                       // [B]
+  float *psiK, *LK, *zbarK, *deltaK, *ztK, *Cpart;   // per-block vectors
+  double *acc, *accout;                  // gradient accumulators
+  float *ebar, *epsa;                    // eligibility traces
 };
 
 struct Plan {
   eprop_config cfg;
   std::vector<Layer> layers;
   int* err_flag = nullptr;
+  int Kmax = kBlockSteps, Bp = 0, ldbk = 0, jlist = 0, out_splits = 1;
+  size_t smem = 0;
   size_t bytes = 0;
 };
 
@@ -68,7 +73,9 @@ bool valid_config(const eprop_config* c, std::string* why) {
     return false;
   }
   if (c->batch > 65535) { *why = "batch must be <= 65535"; return false; }
-  if (c->n_out > 8192) { *why = "n_out must be <= 8192"; return false; }
+  if (c->n_out > 1024) { *why = "n_out must be <= 1024"; return false; }
+  if (c->n_rec > 16384) { *why = "n_rec must be <= 16384"; return false; }
+  if (c->n_in > 65536) { *why = "n_in must be <= 65536"; return false; }
   if (c->recurrent != 0 && c->recurrent != 1) { *why = "recurrent must be 0 or 1"; return false; }
   if (c->n_adaptive < 0 || c->n_adaptive > c->n_rec) {
     *why = "n_adaptive must be in [0, n_rec]";
@@ -78,8 +85,6 @@ bool valid_config(const eprop_config* c, std::string* why) {
   for (float v : k)
     if (!std::isfinite(v)) { *why = "constants must be finite"; return false; }
   if (!(c->thr > 0.0f)) { *why = "thr must be > 0"; return false; }
-  const long long n_pre_max = (long long)std::max(c->n_in, c->n_rec) + (c->recurrent ? c->n_rec : 0);
-  if (n_pre_max > (1LL << 30) / 4) { *why = "presynaptic dimension too large"; return false; }
   return true;
 }
 
@@ -94,46 +99,59 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     off += round_up(std::max<size_t>(bytes, 1), 256);
     return p;
   };
-  const size_t B = c.batch, N = c.n_rec, K = c.n_out;
+  const size_t B = c.batch, N = c.n_rec, K = c.n_out, KM = plan->Kmax;
+  plan->Bp = (int)round_up(B, 16);
+  plan->ldbk = (int)(KM * plan->Bp);
+  plan->jlist = (int)round_up(N, eprop::kFwdThreads) / eprop::kFwdThreads * 64;
+  {
+    int dummy;
+    choose_splits(c.n_out, c.n_rec, plan->ldbk, 16, &plan->out_splits, &dummy);
+  }
   plan->err_flag = (int*)take(sizeof(int));
+  int rwmax = 0;
   for (int l = 0; l < c.n_layers; ++l) {
     Layer& L = plan->layers[l];
     L.n_inl = (l == 0) ? c.n_in : c.n_rec;
     L.n_pre = L.n_inl + (c.recurrent ? c.n_rec : 0);
-    L.kpad = (int)round_up(L.n_pre, 16);
-    L.bpad = (int)round_up(B, 32);
-    L.npad = (int)round_up(N, 32);
-    L.nrk = (int)round_up(N, 16);
-    L.kout = (int)round_up(K, 32);
     L.ldj = (int)round_up(N, 4);
     L.lda = (int)round_up(std::max(c.n_adaptive, 1), 4);
-    L.ldz = (int)round_up(B, 4);
-    choose_splits(c.batch, c.n_rec, L.kpad, 16, &L.s_drive, &L.kc_drive);
-    choose_splits(c.batch, c.n_out, L.nrk, 16, &L.s_out, &L.kc_out);
+    L.kout = (int)round_up(K, 32);
+    L.npad = (int)round_up(N, 32);
+    L.rows_per_wave = (int)round_up((L.n_pre + 3) / 4, 64);
+    rwmax = std::max(rwmax, L.rows_per_wave);
     const size_t np = L.n_pre;
-    L.Wp = (float*)take(sizeof(float) * L.npad * L.kpad);
-    L.Wop = (float*)take(sizeof(float) * L.kout * L.nrk);
-    L.P = (float*)take(sizeof(float) * L.bpad * L.kpad);
-    L.zbarT = (float*)take(sizeof(float) * np * L.ldz);
-    L.Ipart = (float*)take(sizeof(float) * L.s_drive * B * L.ldj);
+    L.Wt = (float*)take(sizeof(float) * np * L.ldj);
+    L.Wop = (float*)take(sizeof(float) * K * L.ldj);
     L.v = (float*)take(sizeof(float) * B * N);
     L.a = (float*)take(sizeof(float) * B * N);
-    L.z[0] = (uint8_t*)take(B * N);
-    L.z[1] = (uint8_t*)take(B * N);
-    L.Zf = (float*)take(sizeof(float) * L.bpad * L.nrk);
-    L.psi = (float*)take(sizeof(float) * B * L.ldj);
-    L.L = (float*)take(sizeof(float) * B * L.ldj);
-    L.ztil = (float*)take(sizeof(float) * B * L.ldj);
-    L.Ypart = (float*)take(sizeof(float) * L.s_out * B * K);
+    L.ztil = (float*)take(sizeof(float) * B * N);
+    L.zbar = (float*)take(sizeof(float) * B * np);
     L.y = (float*)take(sizeof(float) * B * K);
-    L.delta = (float*)take(sizeof(float) * B * K);
+    L.z = (uint8_t*)take(B * N);
     L.lossacc = (double*)take(sizeof(double) * B);
+    L.psiK = (float*)take(sizeof(float) * B * KM * L.ldj);
+    L.LK = (float*)take(sizeof(float) * B * KM * L.ldj);
+    L.zbarK = (float*)take(sizeof(float) * np * B * KM);
+    L.deltaK = (float*)take(sizeof(float) * L.kout * plan->ldbk);
+    L.ztK = (float*)take(sizeof(float) * L.npad * plan->ldbk);
+    L.Cpart = (float*)take(sizeof(float) * plan->out_splits * K * N);
     L.acc = (double*)take(sizeof(double) * np * L.ldj);
     L.accout = (double*)take(sizeof(double) * K * L.ldj);
     L.ebar = (float*)take(sizeof(float) * B * np * L.ldj);
     L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * np * L.lda : 0);
   }
+  const size_t npad4 = round_up(N, 4);
+  plan->smem = sizeof(int) * (4 * (size_t)rwmax + 4 * (size_t)plan->jlist + 8) +
+               sizeof(float) * (2 * K + 2) + (size_t)c.n_layers * 2 * npad4;
   plan->bytes = round_up(off, 256);
+}
+
+bool plan_fits(const Plan& p, std::string* why) {
+  if (p.smem > 64 * 1024) {
+    *why = "shape needs more than 64 KiB of shared memory in the forward kernel";
+    return false;
+  }
+  return true;
 }
 
 }  // namespace
@@ -144,12 +162,13 @@ struct eprop_ctx {
   size_t ws_bytes = 0;
   hipStream_t stream = nullptr;
   long long t = 0;      // steps since the last reset
-  int cur = 0;          // index of z^{t-1} in Layer::z
+  int last_steps = 1;   // steps of the last block (where the last step's vectors sit)
   bool alive = false;
   std::string err;
   // profiling of the eligibility kernel
   bool prof = false;
   std::vector<hipEvent_t> ev;
+  std::vector<int> prof_steps;
   int prof_max = 0, prof_n = 0;
 };
 
@@ -166,20 +185,22 @@ int check(eprop_ctx* ctx, hipError_t e, const char* what) {
 }
 
 int pack_weights(eprop_ctx* ctx) {
+  const eprop_config& c = ctx->plan.cfg;
   for (Layer& L : ctx->plan.layers) {
-    const eprop_config& c = ctx->plan.cfg;
-    int rc = check(ctx, eprop::launch_pack(L.W_src, c.n_rec, L.n_pre, L.Wp, L.kpad, L.npad, ctx->stream),
-                   "weight packing");
+    // drive weights transposed: Wt[i][j] = W[j][i], rows contiguous over j
+    int rc = check(ctx, eprop::launch_pack(L.W_src, c.n_rec, L.n_pre, L.Wt, L.ldj, L.n_pre, 1,
+                                           ctx->stream), "weight packing");
     if (rc) return rc;
-    rc = check(ctx, eprop::launch_pack(L.Wout_src, c.n_out, c.n_rec, L.Wop, L.nrk, L.kout, ctx->stream),
-               "readout weight packing");
+    rc = check(ctx, eprop::launch_pack(L.Wout_src, c.n_out, c.n_rec, L.Wop, L.ldj, c.n_out, 0,
+                                       ctx->stream), "readout weight packing");
     if (rc) return rc;
   }
   return EPROP_OK;
 }
 
-// Zeroes the small state.  Traces and accumulators are not cleared: the
-// first step after a reset treats them as zero without reading them.
+// Zeroes the neuron, filter and readout state.  Traces and accumulators are
+// not cleared: the first block after a reset treats them as zero without
+// reading them.
 int clear_state(eprop_ctx* ctx) {
   const eprop_config& c = ctx->plan.cfg;
   const size_t B = c.batch, N = c.n_rec, K = c.n_out;
@@ -188,80 +209,68 @@ int clear_state(eprop_ctx* ctx) {
   for (Layer& L : ctx->plan.layers) {
     if (rc) return rc;
     hipError_t e = hipSuccess;
-    e = e ? e : hipMemsetAsync(L.zbarT, 0, sizeof(float) * L.n_pre * L.ldz, s);
     e = e ? e : hipMemsetAsync(L.v, 0, sizeof(float) * B * N, s);
     e = e ? e : hipMemsetAsync(L.a, 0, sizeof(float) * B * N, s);
-    e = e ? e : hipMemsetAsync(L.z[0], 0, B * N, s);
-    e = e ? e : hipMemsetAsync(L.z[1], 0, B * N, s);
-    e = e ? e : hipMemsetAsync(L.ztil, 0, sizeof(float) * B * L.ldj, s);
+    e = e ? e : hipMemsetAsync(L.ztil, 0, sizeof(float) * B * N, s);
+    e = e ? e : hipMemsetAsync(L.zbar, 0, sizeof(float) * B * L.n_pre, s);
     e = e ? e : hipMemsetAsync(L.y, 0, sizeof(float) * B * K, s);
+    e = e ? e : hipMemsetAsync(L.z, 0, B * N, s);
     e = e ? e : hipMemsetAsync(L.lossacc, 0, sizeof(double) * B, s);
     rc = check(ctx, e, "reset");
   }
   ctx->t = 0;
-  ctx->cur = 0;
   return rc;
 }
 
-int do_step(eprop_ctx* ctx, const uint8_t* x_t, const int32_t* labels, uint32_t* spikes_t) {
-  const eprop_config& c = ctx->plan.cfg;
+// `steps` (1..Kmax) consecutive timesteps: forward of every layer, readout
+// gradient, eligibility traces and gradient accumulation.
+int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels, uint32_t* spikes) {
+  const Plan& P = ctx->plan;
+  const eprop_config& c = P.cfg;
   hipStream_t s = ctx->stream;
-  const int prev = ctx->cur, now = ctx->cur ^ 1;
-  const int W32 = (c.n_rec + 31) / 32;
   const int first = ctx->t == 0;
   int rc;
-  for (int l = 0; l < c.n_layers; ++l) {
-    Layer& L = ctx->plan.layers[l];
-    eprop::PresynArgs pa;
-    pa.in = (l == 0) ? x_t : ctx->plan.layers[l - 1].z[now];
-    pa.zprev = L.z[prev];
-    pa.P = L.P; pa.zbarT = L.zbarT;
-    pa.B = c.batch; pa.n_inl = L.n_inl; pa.n_rec = c.n_rec; pa.n_pre = L.n_pre;
-    pa.ldp = L.kpad; pa.ldz = L.ldz; pa.alpha = c.alpha;
-    if ((rc = check(ctx, eprop::launch_presyn(pa, s), "presynaptic kernel"))) return rc;
 
-    eprop::GemmArgs g;
-    g.A = L.P; g.Bm = L.Wp; g.C = L.Ipart;
-    g.M = c.batch; g.N = c.n_rec; g.K = L.kpad; g.lda = L.kpad; g.ldb = L.kpad; g.ldc = L.ldj;
-    g.splits = L.s_drive; g.k_chunk = L.kc_drive; g.split_stride = (size_t)c.batch * L.ldj;
-    if ((rc = check(ctx, eprop::launch_gemm_nt(g, s), "drive GEMM"))) return rc;
-
-    eprop::NeuronArgs na;
-    na.Ipart = L.Ipart; na.splits = L.s_drive; na.split_stride = g.split_stride; na.ldI = L.ldj;
-    na.v = L.v; na.a = L.a; na.zprev = L.z[prev]; na.zcur = L.z[now];
-    na.Zf = L.Zf; na.ldzf = L.nrk; na.psi = L.psi; na.ldj = L.ldj;
-    na.spikes = spikes_t ? spikes_t + (size_t)l * c.batch * W32 : nullptr;
-    na.W32 = W32; na.B = c.batch; na.n_rec = c.n_rec; na.n_adaptive = c.n_adaptive;
-    na.alpha = c.alpha; na.rho = c.rho; na.thr = c.thr; na.beta = c.beta;
-    na.gamma_over_thr = c.gamma / c.thr;
-    if ((rc = check(ctx, eprop::launch_neuron(na, s), "neuron kernel"))) return rc;
+  eprop::FwdArgs fa;
+  for (int l = 0; l < 2; ++l) {
+    eprop::FwdLayer& f = fa.L[l];
+    if (l >= c.n_layers) { f = fa.L[0]; continue; }
+    const Layer& L = P.layers[l];
+    f.Wt = L.Wt; f.ldw = L.ldj; f.Wout = L.Wop; f.ldo = L.ldj;
+    f.v = L.v; f.a = L.a; f.ztil = L.ztil; f.z = L.z; f.zbar = L.zbar; f.y = L.y;
+    f.lossacc = L.lossacc; f.psiK = L.psiK; f.LK = L.LK; f.zbarK = L.zbarK;
+    f.deltaK = L.deltaK; f.ztK = L.ztK;
+    f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.rows_per_wave = L.rows_per_wave;
   }
+  fa.n_layers = c.n_layers; fa.x = x; fa.n_in = c.n_in; fa.labels = labels;
+  fa.err_flag = P.err_flag; fa.spikes = spikes; fa.W32 = (c.n_rec + 31) / 32;
+  fa.B = c.batch; fa.Bp = P.Bp; fa.n_rec = c.n_rec; fa.K_out = c.n_out;
+  fa.n_adaptive = c.n_adaptive; fa.Kmax = P.Kmax; fa.steps = steps;
+  fa.ldj = P.layers[0].ldj; fa.ldbk = P.ldbk; fa.jlist = P.jlist;
+  fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
+  fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem;
+  if ((rc = check(ctx, eprop::launch_forward(fa, s), "forward kernel"))) return rc;
+
   for (int l = 0; l < c.n_layers; ++l) {
-    Layer& L = ctx->plan.layers[l];
+    const Layer& L = P.layers[l];
+    // dW_out += sum over (t, b) of delta (x) ztilde: MFMA GEMM, then fp64 accumulation
     eprop::GemmArgs g;
-    g.A = L.Zf; g.Bm = L.Wop; g.C = L.Ypart;
-    g.M = c.batch; g.N = c.n_out; g.K = L.nrk; g.lda = L.nrk; g.ldb = L.nrk; g.ldc = c.n_out;
-    g.splits = L.s_out; g.k_chunk = L.kc_out; g.split_stride = (size_t)c.batch * c.n_out;
-    if ((rc = check(ctx, eprop::launch_gemm_nt(g, s), "readout GEMM"))) return rc;
-
-    eprop::ReadoutArgs ra;
-    ra.Ypart = L.Ypart; ra.splits = L.s_out; ra.split_stride = g.split_stride; ra.ldY = c.n_out;
-    ra.y = L.y; ra.delta = L.delta; ra.labels = labels; ra.Wout = L.Wop; ra.ldo = L.nrk;
-    ra.zcur = L.z[now]; ra.L = L.L; ra.ztil = L.ztil; ra.ldj = L.ldj; ra.lossacc = L.lossacc;
-    ra.err_flag = ctx->plan.err_flag; ra.B = c.batch; ra.K = c.n_out; ra.n_rec = c.n_rec;
-    ra.kappa = c.kappa;
-    if ((rc = check(ctx, eprop::launch_readout(ra, s), "readout kernel"))) return rc;
-
-    eprop::DwoutArgs da;
-    da.delta = L.delta; da.ztil = L.ztil; da.ldj = L.ldj; da.accout = L.accout; da.ld_acc = L.ldj;
-    da.B = c.batch; da.K = c.n_out; da.n_rec = c.n_rec; da.first = first;
-    if ((rc = check(ctx, eprop::launch_dwout(da, s), "readout gradient kernel"))) return rc;
+    g.A = L.deltaK; g.Bm = L.ztK; g.C = L.Cpart;
+    g.M = c.n_out; g.N = c.n_rec; g.K = steps * P.Bp; g.lda = P.ldbk; g.ldb = P.ldbk;
+    g.ldc = c.n_rec;
+    choose_splits(g.M, g.N, g.K, P.out_splits, &g.splits, &g.k_chunk);
+    g.split_stride = (size_t)c.n_out * c.n_rec;
+    if ((rc = check(ctx, eprop::launch_gemm_nt(g, s), "readout gradient GEMM"))) return rc;
+    if ((rc = check(ctx, eprop::launch_accumulate(L.Cpart, g.splits, g.split_stride, c.n_out,
+                                                  c.n_rec, L.accout, L.ldj, first, s),
+                    "readout gradient accumulation")))
+      return rc;
 
     eprop::TraceArgs ta;
-    ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.zbarT = L.zbarT; ta.ldz = L.ldz;
-    ta.psi = L.psi; ta.L = L.L; ta.B = c.batch; ta.n_pre = L.n_pre; ta.n_post = c.n_rec;
-    ta.ldj = L.ldj; ta.n_adaptive = c.n_adaptive; ta.lda = L.lda;
-    ta.kappa = c.kappa; ta.rho = c.rho; ta.beta = c.beta; ta.first = first;
+    ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.zbarK = L.zbarK;
+    ta.psiK = L.psiK; ta.LK = L.LK; ta.B = c.batch; ta.n_pre = L.n_pre; ta.n_post = c.n_rec;
+    ta.ldj = L.ldj; ta.n_adaptive = c.n_adaptive; ta.lda = L.lda; ta.Kmax = P.Kmax;
+    ta.steps = steps; ta.kappa = c.kappa; ta.rho = c.rho; ta.beta = c.beta; ta.first = first;
     const bool timed = ctx->prof && ctx->prof_n < ctx->prof_max;
     if (timed && (rc = check(ctx, hipEventRecord(ctx->ev[2 * ctx->prof_n], s), "event record")))
       return rc;
@@ -269,11 +278,12 @@ int do_step(eprop_ctx* ctx, const uint8_t* x_t, const int32_t* labels, uint32_t*
     if (timed) {
       if ((rc = check(ctx, hipEventRecord(ctx->ev[2 * ctx->prof_n + 1], s), "event record")))
         return rc;
+      ctx->prof_steps[ctx->prof_n] = steps;
       ctx->prof_n++;
     }
   }
-  ctx->cur = now;
-  ctx->t++;
+  ctx->t += steps;
+  ctx->last_steps = steps;
   return EPROP_OK;
 }
 
@@ -291,6 +301,10 @@ size_t eprop_workspace_bytes(const eprop_config* cfg) {
   }
   Plan p;
   make_plan(*cfg, nullptr, &p);
+  if (!plan_fits(p, &why)) {
+    g_last_error = why;
+    return 0;
+  }
   return p.bytes;
 }
 
@@ -307,6 +321,7 @@ int eprop_init(const eprop_config* cfg, void* d_workspace, size_t ws_bytes,
     if (!d_weights[k]) return fail(nullptr, EPROP_EINVAL, "a weight pointer is NULL");
   Plan probe;
   make_plan(*cfg, nullptr, &probe);
+  if (!plan_fits(probe, &why)) return fail(nullptr, EPROP_EINVAL, why);
   if (ws_bytes < probe.bytes)
     return fail(nullptr, EPROP_ENOSPACE,
                 "workspace too small: need " + std::to_string(probe.bytes) + " bytes");
@@ -336,7 +351,7 @@ int eprop_init(const eprop_config* cfg, void* d_workspace, size_t ws_bytes,
 int eprop_step(eprop_ctx* ctx, const uint8_t* d_x_t, const int32_t* d_labels, uint32_t* d_spikes_t) {
   if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
   if (!d_x_t || !d_labels) return fail(ctx, EPROP_EINVAL, "x or labels is NULL");
-  return do_step(ctx, d_x_t, d_labels, d_spikes_t);
+  return do_block(ctx, d_x_t, 1, d_labels, d_spikes_t);
 }
 
 int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int32_t* d_labels,
@@ -347,9 +362,12 @@ int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int3
   const eprop_config& c = ctx->plan.cfg;
   const size_t x_step = (size_t)c.batch * c.n_in;
   const size_t s_step = (size_t)c.n_layers * c.batch * ((c.n_rec + 31) / 32);
-  for (int32_t t = 0; t < T; ++t) {
-    int rc = do_step(ctx, d_x + t * x_step, d_labels, d_spikes ? d_spikes + t * s_step : nullptr);
+  for (int32_t t = 0; t < T;) {
+    const int steps = std::min<int32_t>(ctx->plan.Kmax, T - t);
+    int rc = do_block(ctx, d_x + t * x_step, steps, d_labels,
+                      d_spikes ? d_spikes + t * s_step : nullptr);
     if (rc) return rc;
+    t += steps;
   }
   return EPROP_OK;
 }
@@ -421,12 +439,13 @@ int eprop_profile_begin(eprop_ctx* ctx, int32_t max_launches) {
   ctx->prof = true;
   ctx->prof_max = max_launches;
   ctx->prof_n = 0;
+  ctx->prof_steps.assign(max_launches, 0);
   return EPROP_OK;
 }
 
-int eprop_profile_end(eprop_ctx* ctx, double* total_ms, int32_t* n_launches) {
+int eprop_profile_end(eprop_ctx* ctx, double* total_ms, int32_t* n_launches, int64_t* n_steps) {
   if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
-  if (!total_ms || !n_launches) return fail(ctx, EPROP_EINVAL, "output pointer is NULL");
+  if (!total_ms || !n_launches || !n_steps) return fail(ctx, EPROP_EINVAL, "output pointer is NULL");
   int rc = check(ctx, hipStreamSynchronize(ctx->stream), "stream synchronize");
   if (rc) return rc;
   double sum = 0.0;
@@ -436,8 +455,11 @@ int eprop_profile_end(eprop_ctx* ctx, double* total_ms, int32_t* n_launches) {
     if (rc) return rc;
     sum += ms;
   }
+  int64_t steps = 0;
+  for (int k = 0; k < ctx->prof_n; ++k) steps += ctx->prof_steps[k];
   *total_ms = sum;
   *n_launches = ctx->prof_n;
+  *n_steps = steps;
   ctx->prof = false;
   ctx->prof_n = 0;
   return EPROP_OK;
@@ -450,11 +472,13 @@ int eprop_debug_buffer(eprop_ctx* ctx, int32_t layer, int32_t which, const float
   const eprop_config& c = ctx->plan.cfg;
   if (layer < 0 || layer >= c.n_layers) return fail(ctx, EPROP_EINVAL, "bad layer");
   const Layer& L = ctx->plan.layers[layer];
+  const int64_t kstride = (int64_t)ctx->plan.Kmax * L.ldj;   // rows of psiK, LK are [b][t]
+  const int64_t tl = ctx->last_steps - 1;
   switch (which) {
     case 0: *d_ptr = L.v; *cols = c.n_rec; *ld = c.n_rec; break;
     case 1: *d_ptr = L.a; *cols = c.n_rec; *ld = c.n_rec; break;
-    case 2: *d_ptr = L.psi; *cols = c.n_rec; *ld = L.ldj; break;
-    case 3: *d_ptr = L.L; *cols = c.n_rec; *ld = L.ldj; break;
+    case 2: *d_ptr = L.psiK + tl * L.ldj; *cols = c.n_rec; *ld = kstride; break;
+    case 3: *d_ptr = L.LK + tl * L.ldj; *cols = c.n_rec; *ld = kstride; break;
     case 4: *d_ptr = L.y; *cols = c.n_out; *ld = c.n_out; break;
     default: return fail(ctx, EPROP_EINVAL, "unknown buffer");
   }

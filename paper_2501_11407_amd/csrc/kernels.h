@@ -1,5 +1,16 @@
 // Internal launch interface between the host library (eprop.hip) and the
 // gfx950 kernels (kernels.hip).  Not part of the public ABI.
+//
+// The sequence is processed in blocks of up to Kmax timesteps.  For a block,
+// the forward kernel runs the network for every step (one workgroup per
+// batch element) and leaves per-step vectors in "K buffers":
+//   psiK, LK  [B][Kmax][ldj]   pseudo-derivative and learning signal
+//   zbarK     [n_pre][B][Kmax] filtered presynaptic vector
+//   deltaK    [K_out][ldbk]    readout error, column t*Bp + b
+//   ztK       [n_rec][ldbk]    kappa-filtered spikes, column t*Bp + b
+// then the readout-gradient GEMM contracts deltaK and ztK over (t, b), and
+// the eligibility kernel advances every synapse's traces through the block's
+// steps with one read and one write of the traces.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -8,17 +19,36 @@
 
 namespace eprop {
 
-// Presynaptic vector p^t = [in^t ; z^{t-1}] as fp32 rows of P (the A operand of
-// the drive GEMM) and its alpha filter zbarT[i][b] = alpha*zbarT[i][b] + p.
-struct PresynArgs {
-  const uint8_t* in;   // [B][n_inl]
-  const uint8_t* zprev;  // [B][n_rec]
-  float* P;            // [>=B][ldp]
-  float* zbarT;        // [n_pre][ldz]
-  int B, n_inl, n_rec, n_pre, ldp, ldz;
-  float alpha;
+constexpr int kFwdThreads = 256;
+
+struct FwdLayer {
+  const float* Wt; int ldw;      // transposed drive weights [n_pre][ldw]
+  const float* Wout; int ldo;    // readout weights [K_out][ldo]
+  float* v; float* a; float* ztil;   // state [B][n_rec]
+  uint8_t* z;                    // state: spikes of the last step [B][n_rec]
+  float* zbar;                   // state [B][n_pre]
+  float* y;                      // state [B][K_out]
+  double* lossacc;               // [B]
+  float* psiK; float* LK;        // [B][Kmax][ldj]
+  float* zbarK;                  // [n_pre][B][Kmax]
+  float* deltaK; float* ztK;     // [K_out_pad][ldbk], [n_rec_pad][ldbk]
+  int n_inl, n_pre, rows_per_wave;
 };
-hipError_t launch_presyn(const PresynArgs& a, hipStream_t s);
+
+struct FwdArgs {
+  FwdLayer L[2];
+  int n_layers;
+  const uint8_t* x;              // [steps][B][n_in]
+  int n_in;
+  const int32_t* labels;
+  int* err_flag;
+  uint32_t* spikes;              // NULL or [steps][n_layers][B][W32]
+  int W32;
+  int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldbk, jlist;
+  float alpha, rho, kappa, thr, beta, gamma_over_thr;
+  size_t smem;
+};
+hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
 
 // C_part[s][m][n] = sum_{k in split s} A[m][k] * Bm[n][k]   (fp32 MFMA).
 // A has >= round_up(M,32) rows, Bm >= round_up(N,32) rows, both zero padded
@@ -33,58 +63,25 @@ struct GemmArgs {
 };
 hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s);
 
-// Neuron step (Eq. 8 with reset and adaptive threshold) and surrogate.
-struct NeuronArgs {
-  const float* Ipart; int splits; size_t split_stride; int ldI;
-  float* v; float* a;          // [B][n_rec]
-  const uint8_t* zprev; uint8_t* zcur;   // [B][n_rec]
-  float* Zf; int ldzf;         // fp32 spikes, A operand of the readout GEMM
-  float* psi; int ldj;         // [B][ldj]
-  uint32_t* spikes; int W32;   // optional [B][W32]
-  int B, n_rec, n_adaptive;
-  float alpha, rho, thr, beta, gamma_over_thr;
-};
-hipError_t launch_neuron(const NeuronArgs& a, hipStream_t s);
+// acc[m][n] (fp64, row stride ld_acc) = (first ? 0 : acc) + sum_s part[s][m][n].
+hipError_t launch_accumulate(const float* part, int splits, size_t split_stride, int M, int N,
+                             double* acc, int ld_acc, int first, hipStream_t s);
 
-// Leaky readout, softmax cross-entropy, learning signal L = W_out^T delta,
-// kappa-filtered spikes.
-struct ReadoutArgs {
-  const float* Ypart; int splits; size_t split_stride; int ldY;
-  float* y; float* delta;      // [B][K]
-  const int32_t* labels;
-  const float* Wout; int ldo;  // packed [K][ldo]
-  const uint8_t* zcur;         // [B][n_rec]
-  float* L; float* ztil; int ldj;   // [B][ldj]
-  double* lossacc;             // [B]
-  int* err_flag;
-  int B, K, n_rec;
-  float kappa;
-};
-hipError_t launch_readout(const ReadoutArgs& a, hipStream_t s);
-
-// dW_out[k][j] += sum_b delta[b][k] * ztil[b][j]   (fp64 accumulator).
-struct DwoutArgs {
-  const float* delta; const float* ztil; int ldj;
-  double* accout; int ld_acc;
-  int B, K, n_rec, first;
-};
-hipError_t launch_dwout(const DwoutArgs& a, hipStream_t s);
-
-// Eligibility vectors and gradient accumulation, one pass over the traces.
+// Eligibility vectors and gradient accumulation over `steps` timesteps.
 struct TraceArgs {
   float* ebar;     // [B][n_pre][ldj]
   float* epsa;     // [B][n_pre][lda]
   double* acc;     // [n_pre][ldj]
-  const float* zbarT; int ldz;   // [n_pre][ldz]
-  const float* psi; const float* L;   // [B][ldj]
-  int B, n_pre, n_post, ldj, n_adaptive, lda;
+  const float* zbarK;                 // [n_pre][B][Kmax]
+  const float* psiK; const float* LK; // [B][Kmax][ldj]
+  int B, n_pre, n_post, ldj, n_adaptive, lda, Kmax, steps;
   float kappa, rho, beta;
-  int first;       // 1: previous traces and accumulators are zero (not read)
+  int first;       // 1: traces and accumulators start at zero (not read)
 };
 hipError_t launch_trace(const TraceArgs& a, hipStream_t s);
 
 // Gradient read-out: dW[j][i] = acc[i][j] (recurrent diagonal zeroed),
-// dWout[k][j] = accout[k][j], loss = sum_b lossacc[b]; valid = 0 writes zeros.
+// dWout[k][j] = accout[k][j]; valid = 0 writes zeros.
 struct GradsArgs {
   const double* acc; int ldj; float* dW; int n_pre, n_post, n_inl, recurrent;
   const double* accout; int ld_acc; float* dWout; int K;
@@ -94,8 +91,9 @@ hipError_t launch_grads(const GradsArgs& a, hipStream_t s);
 hipError_t launch_loss(const double* lossacc, int B, int n_layers, size_t layer_stride,
                        double* out, hipStream_t s);
 
-// W [rows][cols] (row-major, ld = cols) -> dst [>=rows][ldd], zero padded.
-hipError_t launch_pack(const float* src, int rows, int cols, float* dst, int ldd, int rows_pad,
-                       hipStream_t s);
+// src [rows][cols] row-major -> dst [rows_pad][ldd] (transpose = 0) or
+// dst [cols_pad][ldd] with dst[c][r] = src[r][c] (transpose = 1); zero padded.
+hipError_t launch_pack(const float* src, int rows, int cols, float* dst, int ldd, int dst_rows,
+                       int transpose, hipStream_t s);
 
 }  // namespace eprop

@@ -2,9 +2,9 @@
 //
 // Built with -ffp-contract=off: every a*b+c written below is a rounded
 // multiply followed by a rounded add unless fmaf/fma is spelled out.  The
-// neuron step relies on this to reproduce fp32 spike decisions operation by
-// operation; the trace and accumulation kernels use explicit fused
-// multiply-adds where precision only gains from them.
+// forward kernel relies on this to reproduce fp32 spike decisions operation
+// by operation; the eligibility kernel uses explicit fused multiply-adds where
+// precision only gains from them.
 #include "kernels.h"
 
 #include <math.h>
@@ -28,21 +28,196 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
+__device__ inline int lanes_below(unsigned long long m, int lane) {
+  return __popcll(m & ((1ull << lane) - 1ull));
+}
+
+__device__ inline f32x4 load_nt(const float* p) {
+  return __builtin_nontemporal_load((const f32x4*)p);
+}
+__device__ inline void store_nt(float* p, f32x4 v) { __builtin_nontemporal_store(v, (f32x4*)p); }
+
 inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
-// ---------------------------------------------------------------- presynaptic
-// One thread per (i, b), b fastest so the zbarT row update is coalesced.
-__global__ __launch_bounds__(256) void presyn_kernel(PresynArgs a) {
-  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long long)a.n_pre * a.B) return;
-  const int b = (int)(idx % a.B);
-  const int i = (int)(idx / a.B);
-  const uint8_t s = (i < a.n_inl) ? a.in[(size_t)b * a.n_inl + i]
-                                  : a.zprev[(size_t)b * a.n_rec + (i - a.n_inl)];
-  const float p = s ? 1.0f : 0.0f;
-  a.P[(size_t)b * a.ldp + i] = p;
-  float* zb = a.zbarT + (size_t)i * a.ldz + b;
-  *zb = a.alpha * *zb + p;
+// ---------------------------------------------------------------- forward
+// One workgroup per batch element runs `steps` timesteps of every layer.
+// Per step and layer:
+//   1. p = [in ; z_prev]; zbar = alpha*zbar + p; each wave lists the indices
+//      of its contiguous slice of p that are 1, in ascending order.
+//   2. drive I_j = sum of W_ji over the listed i, visited in ascending i (the
+//      order of a plain sequential sum), then the neuron step with one
+//      rounding per operation:
+//        v = alpha*v; v = v + I; v = v - thr*z_prev
+//        a = rho*a;   a = a + z_prev
+//        A = beta_j*a; A = thr + A;  x = v - A;  z = x > 0
+//        psi = (gamma/thr) * max(0, 1 - |x|/thr)
+//   3. readout y = kappa*y + W_out z (over the spiking neurons), softmax,
+//      delta = softmax - onehot(label), cross-entropy into the loss;
+//   4. learning signal L = W_out^T delta and ztilde = kappa*ztilde + z.
+__global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs A) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int rwmax = A.L[0].rows_per_wave;
+  if (A.n_layers > 1) rwmax = max(rwmax, A.L[1].rows_per_wave);
+  int* act = (int*)smem;                 // [4][rwmax]  active presynaptic indices
+  int* spk = act + 4 * rwmax;            // [4][jlist]  spiking neurons
+  int* cnt = spk + 4 * A.jlist;          // [8]         list lengths
+  float* sy = (float*)(cnt + 8);         // [K_out]
+  float* sd = sy + A.K_out;              // [K_out]
+  float* red = sd + A.K_out;             // [2]         max, sum of the softmax
+  uint8_t* zc = (uint8_t*)(red + 2);     // [n_layers][2][npad] spikes at t-1 and t
+  const int npad = (A.n_rec + 3) & ~3;
+  const int label = A.labels[b];
+  const bool label_ok = label >= 0 && label < A.K_out;
+  const int QN = (A.n_rec + kFwdThreads - 1) / kFwdThreads;
+
+  for (int l = 0; l < A.n_layers; ++l)
+    for (int j = tid; j < A.n_rec; j += kFwdThreads)
+      zc[(l * 2) * npad + j] = A.L[l].z[(size_t)b * A.n_rec + j];
+  double loss0 = 0.0, loss1 = 0.0;
+  int cur = 0;
+  __syncthreads();
+
+  for (int t = 0; t < A.steps; ++t) {
+    for (int l = 0; l < A.n_layers; ++l) {
+      const FwdLayer& Ly = A.L[l];
+      const uint8_t* zprev = zc + (l * 2 + cur) * npad;
+      uint8_t* znow = zc + (l * 2 + (cur ^ 1)) * npad;
+      const uint8_t* inp = (l == 0) ? A.x + ((size_t)t * A.B + b) * A.n_in
+                                    : zc + ((l - 1) * 2 + (cur ^ 1)) * npad;
+
+      // 1. presynaptic vector, its filter, ordered active lists
+      const int rw = Ly.rows_per_wave;
+      const int i_beg = w * rw, i_end = min(Ly.n_pre, i_beg + rw);
+      int n_act = 0;
+      for (int base = i_beg; base < i_end; base += kWave) {
+        const int i = base + lane;
+        bool on = false;
+        if (i < i_end) {
+          const uint8_t sv = (i < Ly.n_inl) ? inp[i] : zprev[i - Ly.n_inl];
+          on = sv != 0;
+          float* zp = Ly.zbar + (size_t)b * Ly.n_pre + i;
+          const float zv = A.alpha * *zp + (on ? 1.0f : 0.0f);
+          *zp = zv;
+          Ly.zbarK[((size_t)i * A.B + b) * A.Kmax + t] = zv;
+        }
+        const unsigned long long m = __ballot(on);
+        if (on) act[w * rwmax + n_act + lanes_below(m, lane)] = i;
+        n_act += __popcll(m);
+      }
+      if (lane == 0) cnt[w] = n_act;
+      __syncthreads();
+
+      // 2. drive and neuron step
+      int n_spk = 0;
+      for (int q = 0; q < QN; ++q) {
+        const int j = q * kFwdThreads + tid;
+        bool z = false;
+        if (j < A.n_rec) {
+          float I = 0.0f;
+          for (int ww = 0; ww < 4; ++ww) {
+            const int c = cnt[ww];
+            const int* lst = act + ww * rwmax;
+#pragma unroll 8
+            for (int k = 0; k < c; ++k) I += Ly.Wt[(size_t)lst[k] * Ly.ldw + j];
+          }
+          const size_t o = (size_t)b * A.n_rec + j;
+          const float zp = zprev[j] ? 1.0f : 0.0f;
+          float v = A.alpha * Ly.v[o];
+          v = v + I;
+          v = v - A.thr * zp;
+          float ad = A.rho * Ly.a[o];
+          ad = ad + zp;
+          const float bj = (j < A.n_adaptive) ? A.beta : 0.0f;
+          float th = bj * ad;
+          th = A.thr + th;
+          const float x = v - th;
+          Ly.v[o] = v;
+          Ly.a[o] = ad;
+          z = x > 0.0f;
+          znow[j] = z ? 1 : 0;
+          const float u = 1.0f - fabsf(x) / A.thr;
+          Ly.psiK[((size_t)b * A.Kmax + t) * A.ldj + j] = A.gamma_over_thr * fmaxf(u, 0.0f);
+        }
+        const unsigned long long m = __ballot(z);
+        if (z) spk[w * A.jlist + n_spk + lanes_below(m, lane)] = j;
+        n_spk += __popcll(m);
+        if (A.spikes) {
+          const int w0 = (q * kFwdThreads + w * kWave) >> 5;
+          uint32_t* row = A.spikes + (((size_t)t * A.n_layers + l) * A.B + b) * A.W32;
+          if (lane == 0 && w0 < A.W32) row[w0] = (uint32_t)m;
+          if (lane == 1 && w0 + 1 < A.W32) row[w0 + 1] = (uint32_t)(m >> 32);
+        }
+      }
+      if (lane == 0) cnt[4 + w] = n_spk;
+      __syncthreads();
+
+      // 3. readout, softmax cross-entropy
+      for (int k = tid; k < A.K_out; k += kFwdThreads) {
+        float Y = 0.0f;
+        for (int ww = 0; ww < 4; ++ww) {
+          const int c = cnt[4 + ww];
+          const int* lst = spk + ww * A.jlist;
+          for (int s = 0; s < c; ++s) Y += Ly.Wout[(size_t)k * Ly.ldo + lst[s]];
+        }
+        float yy = A.kappa * Ly.y[(size_t)b * A.K_out + k];
+        yy = yy + Y;
+        Ly.y[(size_t)b * A.K_out + k] = yy;
+        sy[k] = yy;
+      }
+      __syncthreads();
+      if (w == 0) {
+        float m = -INFINITY;
+        for (int k = lane; k < A.K_out; k += kWave) m = fmaxf(m, sy[k]);
+        m = wave_max(m);
+        float se = 0.0f;
+        for (int k = lane; k < A.K_out; k += kWave) se += expf(sy[k] - m);
+        se = wave_sum(se);
+        if (lane == 0) {
+          red[0] = m;
+          red[1] = se;
+          if (label_ok) {
+            const double ce = log((double)se) - ((double)sy[label] - (double)m);
+            if (l == 0) loss0 += ce; else loss1 += ce;
+          } else {
+            *A.err_flag = 1;
+          }
+        }
+      }
+      __syncthreads();
+      {
+        const float m = red[0], se = red[1];
+        for (int k = tid; k < A.K_out; k += kFwdThreads) {
+          const float d = expf(sy[k] - m) / se - ((k == label) ? 1.0f : 0.0f);
+          sd[k] = d;
+          Ly.deltaK[(size_t)k * A.ldbk + (size_t)t * A.Bp + b] = d;
+        }
+      }
+      __syncthreads();
+
+      // 4. learning signal and filtered spikes
+      for (int j = tid; j < A.n_rec; j += kFwdThreads) {
+        float Lj = 0.0f;
+        for (int k = 0; k < A.K_out; ++k) Lj = fmaf(Ly.Wout[(size_t)k * Ly.ldo + j], sd[k], Lj);
+        Ly.LK[((size_t)b * A.Kmax + t) * A.ldj + j] = Lj;
+        const size_t o = (size_t)b * A.n_rec + j;
+        float zt = A.kappa * Ly.ztil[o];
+        zt = zt + (znow[j] ? 1.0f : 0.0f);
+        Ly.ztil[o] = zt;
+        Ly.ztK[(size_t)j * A.ldbk + (size_t)t * A.Bp + b] = zt;
+      }
+      __syncthreads();
+    }
+    cur ^= 1;
+  }
+  for (int l = 0; l < A.n_layers; ++l)
+    for (int j = tid; j < A.n_rec; j += kFwdThreads)
+      A.L[l].z[(size_t)b * A.n_rec + j] = zc[(l * 2 + cur) * npad + j];
+  if (tid == 0) {
+    A.L[0].lossacc[b] += loss0;
+    if (A.n_layers > 1) A.L[1].lossacc[b] += loss1;
+  }
 }
 
 // ---------------------------------------------------------------- MFMA GEMM
@@ -99,126 +274,29 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
   }
 }
 
-// ---------------------------------------------------------------- neuron step
-// One thread per (b, j).  Operation order, one rounding each:
-//   v = alpha*v; v = v + I; v = v - thr*z_prev
-//   a = rho*a;   a = a + z_prev
-//   A = beta_j*a; A = thr + A;  x = v - A;  z = x > 0
-//   psi = (gamma/thr) * max(0, 1 - |x|/thr)
-__global__ __launch_bounds__(256) void neuron_kernel(NeuronArgs a) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  const int b = blockIdx.y;
-  bool z = false;
-  if (j < a.n_rec) {
-    float I = 0.0f;
-    for (int s = 0; s < a.splits; ++s) I += a.Ipart[s * a.split_stride + (size_t)b * a.ldI + j];
-    const size_t o = (size_t)b * a.n_rec + j;
-    const float zp = a.zprev[o] ? 1.0f : 0.0f;
-    float v = a.alpha * a.v[o];
-    v = v + I;
-    v = v - a.thr * zp;
-    float ad = a.rho * a.a[o];
-    ad = ad + zp;
-    const float bj = (j < a.n_adaptive) ? a.beta : 0.0f;
-    float A = bj * ad;
-    A = a.thr + A;
-    const float x = v - A;
-    a.v[o] = v;
-    a.a[o] = ad;
-    z = x > 0.0f;
-    a.zcur[o] = z ? 1 : 0;
-    a.Zf[(size_t)b * a.ldzf + j] = z ? 1.0f : 0.0f;
-    const float u = 1.0f - fabsf(x) / a.thr;
-    a.psi[(size_t)b * a.ldj + j] = a.gamma_over_thr * fmaxf(u, 0.0f);
-  }
-  if (a.spikes) {
-    const unsigned long long m = __ballot(z);
-    const int lane = threadIdx.x & 63;
-    const int w0 = (j - lane) >> 5;   // first 32-bit word of this wave's 64 neurons
-    uint32_t* row = a.spikes + (size_t)b * a.W32;
-    if (lane == 0 && w0 < a.W32) row[w0] = (uint32_t)m;
-    if (lane == 1 && w0 + 1 < a.W32) row[w0 + 1] = (uint32_t)(m >> 32);
-  }
-}
-
-// ---------------------------------------------------------------- readout
-// One block per batch element.  Shared memory: y[K], delta[K].
-__global__ __launch_bounds__(256) void readout_kernel(ReadoutArgs a) {
-  extern __shared__ float sm[];
-  float* sy = sm;
-  float* sd = sm + a.K;
-  __shared__ float s_max, s_sum;
-  const int b = blockIdx.x;
-  const int tid = threadIdx.x;
-  const int label = a.labels[b];
-  const bool label_ok = label >= 0 && label < a.K;
-
-  for (int k = tid; k < a.K; k += blockDim.x) {
-    float Y = 0.0f;
-    for (int s = 0; s < a.splits; ++s) Y += a.Ypart[s * a.split_stride + (size_t)b * a.ldY + k];
-    float y = a.kappa * a.y[(size_t)b * a.K + k];
-    y = y + Y;
-    a.y[(size_t)b * a.K + k] = y;
-    sy[k] = y;
-  }
-  __syncthreads();
-  if (tid < kWave) {
-    float m = -INFINITY;
-    for (int k = tid; k < a.K; k += kWave) m = fmaxf(m, sy[k]);
-    m = wave_max(m);
-    float se = 0.0f;
-    for (int k = tid; k < a.K; k += kWave) se += expf(sy[k] - m);
-    se = wave_sum(se);
-    if (tid == 0) {
-      s_max = m;
-      s_sum = se;
-      if (label_ok) {
-        a.lossacc[b] += log((double)se) - ((double)sy[label] - (double)m);
-      } else {
-        *a.err_flag = 1;
-      }
-    }
-  }
-  __syncthreads();
-  const float m = s_max, se = s_sum;
-  for (int k = tid; k < a.K; k += blockDim.x) {
-    const float d = expf(sy[k] - m) / se - ((k == label) ? 1.0f : 0.0f);
-    sd[k] = d;
-    a.delta[(size_t)b * a.K + k] = d;
-  }
-  __syncthreads();
-  for (int j = tid; j < a.n_rec; j += blockDim.x) {
-    float Lj = 0.0f;
-    for (int k = 0; k < a.K; ++k) Lj = fmaf(a.Wout[(size_t)k * a.ldo + j], sd[k], Lj);
-    a.L[(size_t)b * a.ldj + j] = Lj;
-    const float zt = a.zcur[(size_t)b * a.n_rec + j] ? 1.0f : 0.0f;
-    float* zt_p = a.ztil + (size_t)b * a.ldj + j;
-    *zt_p = a.kappa * *zt_p + zt;
-  }
-}
-
-// ---------------------------------------------------------------- readout gradient
-__global__ __launch_bounds__(256) void dwout_kernel(DwoutArgs a) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  const int k = blockIdx.y;
-  if (j >= a.n_rec) return;
-  double* p = a.accout + (size_t)k * a.ld_acc + j;
-  double s = a.first ? 0.0 : *p;
-  for (int b = 0; b < a.B; ++b)
-    s = fma((double)a.delta[(size_t)b * a.K + k], (double)a.ztil[(size_t)b * a.ldj + j], s);
-  *p = s;
+// Split-K partials added into an fp64 accumulator in split order.
+__global__ __launch_bounds__(256) void accumulate_kernel(const float* part, int splits, size_t ss,
+                                                        int M, int N, double* acc, int ld, int first) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)M * N) return;
+  const int m = (int)(idx / N), n = (int)(idx % N);
+  double s = first ? 0.0 : acc[(size_t)m * ld + n];
+  for (int sp = 0; sp < splits; ++sp) s += (double)part[sp * ss + (size_t)m * N + n];
+  acc[(size_t)m * ld + n] = s;
 }
 
 // ---------------------------------------------------------------- eligibility
 // One thread owns 4 consecutive postsynaptic neurons j0..j0+3 of IT
 // consecutive presynaptic rows i0..i0+IT-1 and walks the batch.  For each
-// (b, i, j):
+// (b, i, j) it reads the traces once, advances them through the block's
+// steps, and writes them once.  Per step:
 //   e    = psi_j (zbar_i - beta_j epsa)          (dz_j/dW_ji)
 //   ebar = kappa ebar + e                        (readout filter on the trace)
 //   acc += L_j ebar                              (fp64)
 //   epsa = psi_j zbar_i + (rho - beta_j psi_j) epsa   (adaptive j only)
-// zbar_i of a (b, i) is the same for the whole block: a scalar load.  Trace
-// rows are j-contiguous, so a wave moves 1 KiB per 16-byte lane access.
+// zbar_i of a (b, i, t) is the same for the whole block: a scalar load.  Trace
+// rows are j-contiguous, so a wave moves 1 KiB per 16-byte lane access; the
+// next batch element's traces are loaded before the current ones are stored.
 template <int IT, bool FIRST>
 __global__ __launch_bounds__(256) void trace_kernel(TraceArgs a) {
   const int j0 = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
@@ -239,40 +317,80 @@ __global__ __launch_bounds__(256) void trace_kernel(TraceArgs a) {
 
   const size_t bs_e = (size_t)a.n_pre * a.ldj;
   const size_t bs_a = (size_t)a.n_pre * a.lda;
+  const size_t zrow = (size_t)a.B * a.Kmax;
   float* pe0 = a.ebar + (size_t)i0 * a.ldj + j0;
   float* pa0 = a.epsa + (size_t)i0 * a.lda + j0;
-  const float* zb0 = a.zbarT + (size_t)i0 * a.ldz;
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 
-  for (int b = 0; b < a.B; ++b) {
-    const f32x4 ps = *(const f32x4*)(a.psi + (size_t)b * a.ldj + j0);
-    const f32x4 lv = *(const f32x4*)(a.L + (size_t)b * a.ldj + j0);
-    float rb[4];
+  f32x4 E[IT], Aa[IT];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) rb[r] = a.rho - bj[r] * ps[r];
+  for (int ii = 0; ii < IT; ++ii) {
+    E[ii] = zero;
+    Aa[ii] = zero;
+    if (!FIRST && ii < nit) {
+      E[ii] = load_nt(pe0 + (size_t)ii * a.ldj);
+      if (adapt) Aa[ii] = load_nt(pa0 + (size_t)ii * a.lda);
+    }
+  }
+  for (int b = 0; b < a.B; ++b) {
+    f32x4 En[IT], An[IT];
+#pragma unroll
+    for (int ii = 0; ii < IT; ++ii) {
+      En[ii] = zero;
+      An[ii] = zero;
+      if (!FIRST && b + 1 < a.B && ii < nit) {
+        En[ii] = load_nt(pe0 + (size_t)(b + 1) * bs_e + (size_t)ii * a.ldj);
+        if (adapt) An[ii] = load_nt(pa0 + (size_t)(b + 1) * bs_a + (size_t)ii * a.lda);
+      }
+    }
+    const float* zk = a.zbarK + ((size_t)i0 * a.B + b) * a.Kmax;
+    const float* pp = a.psiK + (size_t)b * a.Kmax * a.ldj + j0;
+    const float* lp = a.LK + (size_t)b * a.Kmax * a.ldj + j0;
+    for (int t = 0; t < a.steps; ++t) {
+      const f32x4 ps = *(const f32x4*)(pp + (size_t)t * a.ldj);
+      const f32x4 lv = *(const f32x4*)(lp + (size_t)t * a.ldj);
+      double ld[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ld[r] = (double)lv[r];
+      if (adapt) {
+        float rb[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) rb[r] = a.rho - bj[r] * ps[r];
+#pragma unroll
+        for (int ii = 0; ii < IT; ++ii) {
+          if (ii < nit) {
+            const float zb = zk[(size_t)ii * zrow + t];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float et = ps[r] * (zb - bj[r] * Aa[ii][r]);
+              E[ii][r] = fmaf(a.kappa, E[ii][r], et);
+              Aa[ii][r] = fmaf(rb[r], Aa[ii][r], ps[r] * zb);
+              acc[ii][r] = fma(ld[r], (double)E[ii][r], acc[ii][r]);
+            }
+          }
+        }
+      } else {
+#pragma unroll
+        for (int ii = 0; ii < IT; ++ii) {
+          if (ii < nit) {
+            const float zb = zk[(size_t)ii * zrow + t];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              E[ii][r] = fmaf(a.kappa, E[ii][r], ps[r] * zb);
+              acc[ii][r] = fma(ld[r], (double)E[ii][r], acc[ii][r]);
+            }
+          }
+        }
+      }
+    }
 #pragma unroll
     for (int ii = 0; ii < IT; ++ii) {
       if (ii < nit) {
-        const float zb = zb0[(size_t)ii * a.ldz + b];
-        f32x4* pe = (f32x4*)(pe0 + (size_t)b * bs_e + (size_t)ii * a.ldj);
-        f32x4 e = FIRST ? f32x4{0.f, 0.f, 0.f, 0.f} : *pe;
-        if (adapt) {
-          f32x4* pa = (f32x4*)(pa0 + (size_t)b * bs_a + (size_t)ii * a.lda);
-          f32x4 ea = FIRST ? f32x4{0.f, 0.f, 0.f, 0.f} : *pa;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float et = ps[r] * (zb - bj[r] * ea[r]);
-            e[r] = fmaf(a.kappa, e[r], et);
-            ea[r] = fmaf(rb[r], ea[r], ps[r] * zb);
-          }
-          *pa = ea;
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) e[r] = fmaf(a.kappa, e[r], ps[r] * zb);
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[ii][r] = fma((double)lv[r], (double)e[r], acc[ii][r]);
-        *pe = e;
+        store_nt(pe0 + (size_t)b * bs_e + (size_t)ii * a.ldj, E[ii]);
+        if (adapt) store_nt(pa0 + (size_t)b * bs_a + (size_t)ii * a.lda, Aa[ii]);
       }
+      E[ii] = En[ii];
+      Aa[ii] = An[ii];
     }
   }
 #pragma unroll
@@ -320,19 +438,24 @@ __global__ void loss_kernel(const double* lossacc, int B, int n_layers, size_t l
 }
 
 __global__ __launch_bounds__(256) void pack_kernel(const float* src, int rows, int cols, float* dst,
-                                                   int ldd, int rows_pad) {
+                                                   int ldd, int dst_rows, int transpose) {
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long long)rows_pad * ldd) return;
+  if (idx >= (long long)dst_rows * ldd) return;
   const int r = (int)(idx / ldd), c = (int)(idx % ldd);
-  dst[idx] = (r < rows && c < cols) ? src[(size_t)r * cols + c] : 0.0f;
+  float v = 0.0f;
+  if (!transpose) {
+    if (r < rows && c < cols) v = src[(size_t)r * cols + c];
+  } else {
+    if (r < cols && c < rows) v = src[(size_t)c * cols + r];
+  }
+  dst[idx] = v;
 }
 
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
-hipError_t launch_presyn(const PresynArgs& a, hipStream_t s) {
-  const long long n = (long long)a.n_pre * a.B;
-  presyn_kernel<<<cdiv(n, 256), 256, 0, s>>>(a);
+hipError_t launch_forward(const FwdArgs& a, hipStream_t s) {
+  forward_kernel<<<a.B, kFwdThreads, a.smem, s>>>(a);
   return hipGetLastError();
 }
 
@@ -342,20 +465,10 @@ hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_neuron(const NeuronArgs& a, hipStream_t s) {
-  dim3 grid(cdiv(a.n_rec, 256), a.B);
-  neuron_kernel<<<grid, 256, 0, s>>>(a);
-  return hipGetLastError();
-}
-
-hipError_t launch_readout(const ReadoutArgs& a, hipStream_t s) {
-  readout_kernel<<<a.B, 256, 2 * a.K * sizeof(float), s>>>(a);
-  return hipGetLastError();
-}
-
-hipError_t launch_dwout(const DwoutArgs& a, hipStream_t s) {
-  dim3 grid(cdiv(a.n_rec, 256), a.K);
-  dwout_kernel<<<grid, 256, 0, s>>>(a);
+hipError_t launch_accumulate(const float* part, int splits, size_t split_stride, int M, int N,
+                             double* acc, int ld_acc, int first, hipStream_t s) {
+  accumulate_kernel<<<cdiv((long long)M * N, 256), 256, 0, s>>>(part, splits, split_stride, M, N,
+                                                               acc, ld_acc, first);
   return hipGetLastError();
 }
 
@@ -383,10 +496,10 @@ hipError_t launch_loss(const double* lossacc, int B, int n_layers, size_t layer_
   return hipGetLastError();
 }
 
-hipError_t launch_pack(const float* src, int rows, int cols, float* dst, int ldd, int rows_pad,
-                       hipStream_t s) {
-  const long long n = (long long)rows_pad * ldd;
-  pack_kernel<<<cdiv(n, 256), 256, 0, s>>>(src, rows, cols, dst, ldd, rows_pad);
+hipError_t launch_pack(const float* src, int rows, int cols, float* dst, int ldd, int dst_rows,
+                       int transpose, hipStream_t s) {
+  const long long n = (long long)dst_rows * ldd;
+  pack_kernel<<<cdiv(n, 256), 256, 0, s>>>(src, rows, cols, dst, ldd, dst_rows, transpose);
   return hipGetLastError();
 }
 

@@ -67,7 +67,7 @@ def load_library(path: str = LIB_PATH):
         "eprop_last_error": (ctypes.c_char_p, [vp]),
         "eprop_profile_begin": (ctypes.c_int, [vp, i32]),
         "eprop_profile_end": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double),
-                                             ctypes.POINTER(i32)]),
+                                             ctypes.POINTER(i32), ctypes.POINTER(i64)]),
         "eprop_debug_buffer": (ctypes.c_int, [vp, i32, i32, ctypes.POINTER(vp),
                                               ctypes.POINTER(i64), ctypes.POINTER(i64)]),
     }
@@ -149,10 +149,12 @@ def eprop_profile_begin(ctx, max_launches: int):
     _check(load_library().eprop_profile_begin(ctx, int(max_launches)), ctx)
 
 
-def eprop_profile_end(ctx) -> Tuple[float, int]:
-    ms, n = ctypes.c_double(), ctypes.c_int32()
-    _check(load_library().eprop_profile_end(ctx, ctypes.byref(ms), ctypes.byref(n)), ctx)
-    return ms.value, n.value
+def eprop_profile_end(ctx) -> Tuple[float, int, int]:
+    """(summed eligibility-kernel milliseconds, timed launches, timesteps they covered)"""
+    ms, n, steps = ctypes.c_double(), ctypes.c_int32(), ctypes.c_int64()
+    _check(load_library().eprop_profile_end(ctx, ctypes.byref(ms), ctypes.byref(n),
+                                            ctypes.byref(steps)), ctx)
+    return ms.value, n.value, steps.value
 
 
 def eprop_debug_buffer(ctx, layer: int, which: int) -> Tuple[int, int, int]:

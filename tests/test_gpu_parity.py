@@ -126,9 +126,20 @@ def _wl():
     return synth.make_workload(shape, seed, input_scale=scale)
 
 
-def test_sequence_equals_steps_bitwise():
+def _same_forward_close_grads(x, y, tol=1e-6):
+    assert np.array_equal(x["spikes"], y["spikes"])
+    for l in range(len(x["dW"])):
+        assert rel_l2(x["dW"][l], y["dW"][l]) <= tol
+        assert rel_l2(x["dWout"][l], y["dWout"][l]) <= tol
+    assert abs(x["loss"] - y["loss"]) <= tol * abs(y["loss"])
+
+
+def test_sequence_equals_steps():
+    # run_sequence works in blocks of steps; T single steps give the same
+    # spikes and neuron state, and the gradient up to summation order.
     wl = _wl()
-    a = gpu_run(wl)
+    ctx_a = eprop.EpropContext(wl.shape, wl.W, wl.Wout)
+    a = gpu_run(wl, ctx=ctx_a)
     ctx = eprop.EpropContext(wl.shape, wl.W, wl.Wout)
     x, labels = to_dev(wl)
     spikes = ctx.new_spike_buffer(wl.shape.T)
@@ -136,12 +147,14 @@ def test_sequence_equals_steps_bitwise():
         ctx.step(x[t], labels, spikes[t])
     dW, dWout, loss = ctx.get_grads()
     torch.cuda.synchronize()
-    assert np.array_equal(spikes.cpu().numpy().view(np.uint32), a["spikes"])
+    b = dict(spikes=spikes.cpu().numpy().view(np.uint32), dW=[d.cpu().numpy() for d in dW],
+             dWout=[d.cpu().numpy() for d in dWout], loss=float(loss.cpu()))
+    _same_forward_close_grads(b, a)
     for l in range(wl.shape.n_layers):
-        assert np.array_equal(dW[l].cpu().numpy(), a["dW"][l])
-        assert np.array_equal(dWout[l].cpu().numpy(), a["dWout"][l])
-    assert float(loss.cpu()) == a["loss"]
+        for name in ("v", "a"):
+            assert torch.equal(ctx.debug(name, l), ctx_a.debug(name, l))
     ctx.close()
+    ctx_a.close()
 
 
 def test_split_sequence_and_determinism():
@@ -149,12 +162,12 @@ def test_split_sequence_and_determinism():
     a = gpu_run(wl)
     b = gpu_run(wl, chunks=[7, 1, wl.shape.T - 8])
     c = gpu_run(wl)
-    for other in (b, c):
-        assert np.array_equal(other["spikes"], a["spikes"])
-        for l in range(wl.shape.n_layers):
-            assert np.array_equal(other["dW"][l], a["dW"][l])
-            assert np.array_equal(other["dWout"][l], a["dWout"][l])
-        assert other["loss"] == a["loss"]
+    _same_forward_close_grads(b, a)
+    assert np.array_equal(c["spikes"], a["spikes"])
+    for l in range(wl.shape.n_layers):
+        assert np.array_equal(c["dW"][l], a["dW"][l])
+        assert np.array_equal(c["dWout"][l], a["dWout"][l])
+    assert c["loss"] == a["loss"]
 
 
 def test_reset_starts_a_new_sequence_and_reads_new_weights():
