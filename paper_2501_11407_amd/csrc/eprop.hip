@@ -40,18 +40,21 @@ constexpr int kBlockSteps = 32;
 
 struct Layer {
   int n_inl = 0, n_pre = 0;
-  int ldj = 0;    // n_rec rounded to 4: row stride of per-neuron vectors and traces
+  int n_pre_pad = 0;   // n_pre rounded to the eligibility kernel's row group
+  int ldj = 0;    // n_rec rounded to 4: row stride of traces and accumulators
+  int ldv = 0;    // n_rec rounded to 256: row stride of Wt, psiK, LK
   int lda = 0;    // n_adaptive rounded to 4: row stride of epsa
-  int kout = 0;   // n_out rounded to 32: rows of deltaK
-  int npad = 0;   // n_rec rounded to 32: rows of ztK
   int rows_per_wave = 0;
   const float* W_src = nullptr;
   const float* Wout_src = nullptr;
-  float *Wt, *Wop;                       // packed weights
+  float *Wt, *WoutT;                     // packed weights
   float *v, *a, *ztil, *zbar, *y;        // neuron, filter and readout state
   uint8_t* z;                            // spikes of the last step
   double* lossacc;                       // [B]
-  float *psiK, *LK, *zbarK, *deltaK, *ztK, *Cpart;   // per-block vectors
+  // per-block vectors, two slots: the forward of block k+1 fills one while
+  // the eligibility pass of block k reads the other
+  float *psiK[2], *LK[2], *zbarK[2], *deltaK[2], *ztK[2];
+  float* Cpart;
   double *acc, *accout;                  // gradient accumulators
   float *ebar, *epsa;                    // eligibility traces
 };
@@ -60,7 +63,7 @@ struct Plan {
   eprop_config cfg;
   std::vector<Layer> layers;
   int* err_flag = nullptr;
-  int Kmax = kBlockSteps, Bp = 0, ldbk = 0, jlist = 0, out_splits = 1;
+  int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, jlist = 0, out_splits = 1;
   size_t smem = 0;
   size_t bytes = 0;
 };
@@ -101,27 +104,32 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   };
   const size_t B = c.batch, N = c.n_rec, K = c.n_out, KM = plan->Kmax;
   plan->Bp = (int)round_up(B, 16);
-  plan->ldbk = (int)(KM * plan->Bp);
-  plan->jlist = (int)round_up(N, eprop::kFwdThreads) / eprop::kFwdThreads * 64;
+  plan->rows = (int)round_up(KM * plan->Bp, 32);     // rows of deltaK, ztK, psiK, LK
+  plan->ldk = (int)round_up(K, 32);
+  plan->ldn = (int)round_up(N, 32);
+  plan->jlist = (int)(round_up(N, eprop::kFwdThreads) / eprop::kFwdThreads * 64);
   {
     int dummy;
-    choose_splits(c.n_out, c.n_rec, plan->ldbk, 16, &plan->out_splits, &dummy);
+    choose_splits(c.n_out, c.n_rec, (int)(KM * plan->Bp), 16, &plan->out_splits, &dummy);
   }
+  const size_t R = plan->rows;
   plan->err_flag = (int*)take(sizeof(int));
   int rwmax = 0;
+  size_t npre_total = 0;
   for (int l = 0; l < c.n_layers; ++l) {
     Layer& L = plan->layers[l];
     L.n_inl = (l == 0) ? c.n_in : c.n_rec;
     L.n_pre = L.n_inl + (c.recurrent ? c.n_rec : 0);
+    L.n_pre_pad = (int)round_up(L.n_pre, eprop::kRowPad);
     L.ldj = (int)round_up(N, 4);
+    L.ldv = (int)round_up(N, 256);
     L.lda = (int)round_up(std::max(c.n_adaptive, 1), 4);
-    L.kout = (int)round_up(K, 32);
-    L.npad = (int)round_up(N, 32);
     L.rows_per_wave = (int)round_up((L.n_pre + 3) / 4, 64);
     rwmax = std::max(rwmax, L.rows_per_wave);
-    const size_t np = L.n_pre;
-    L.Wt = (float*)take(sizeof(float) * np * L.ldj);
-    L.Wop = (float*)take(sizeof(float) * K * L.ldj);
+    npre_total += L.n_pre;
+    const size_t np = L.n_pre, npp = L.n_pre_pad;
+    L.Wt = (float*)take(sizeof(float) * np * L.ldv);
+    L.WoutT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.v = (float*)take(sizeof(float) * B * N);
     L.a = (float*)take(sizeof(float) * B * N);
     L.ztil = (float*)take(sizeof(float) * B * N);
@@ -129,20 +137,23 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.y = (float*)take(sizeof(float) * B * K);
     L.z = (uint8_t*)take(B * N);
     L.lossacc = (double*)take(sizeof(double) * B);
-    L.psiK = (float*)take(sizeof(float) * B * KM * L.ldj);
-    L.LK = (float*)take(sizeof(float) * B * KM * L.ldj);
-    L.zbarK = (float*)take(sizeof(float) * np * B * KM);
-    L.deltaK = (float*)take(sizeof(float) * L.kout * plan->ldbk);
-    L.ztK = (float*)take(sizeof(float) * L.npad * plan->ldbk);
+    for (int sl = 0; sl < 2; ++sl) {
+      L.psiK[sl] = (float*)take(sizeof(float) * R * L.ldv);
+      L.LK[sl] = (float*)take(sizeof(float) * R * L.ldv);
+      L.zbarK[sl] = (float*)take(sizeof(float) * B * KM * npp);
+      L.deltaK[sl] = (float*)take(sizeof(float) * R * plan->ldk);
+      L.ztK[sl] = (float*)take(sizeof(float) * R * plan->ldn);
+    }
     L.Cpart = (float*)take(sizeof(float) * plan->out_splits * K * N);
-    L.acc = (double*)take(sizeof(double) * np * L.ldj);
+    L.acc = (double*)take(sizeof(double) * npp * L.ldj);
     L.accout = (double*)take(sizeof(double) * K * L.ldj);
-    L.ebar = (float*)take(sizeof(float) * B * np * L.ldj);
-    L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * np * L.lda : 0);
+    L.ebar = (float*)take(sizeof(float) * B * npp * L.ldj);
+    L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * L.lda : 0);
   }
   const size_t npad4 = round_up(N, 4);
   plan->smem = sizeof(int) * (4 * (size_t)rwmax + 4 * (size_t)plan->jlist + 8) +
-               sizeof(float) * (2 * K + 2) + (size_t)c.n_layers * 2 * npad4;
+               sizeof(float) * (2 + (size_t)c.n_layers * K + npre_total) +
+               (size_t)c.n_layers * 2 * npad4;
   plan->bytes = round_up(off, 256);
 }
 
@@ -163,6 +174,11 @@ struct eprop_ctx {
   hipStream_t stream = nullptr;
   long long t = 0;      // steps since the last reset
   int last_steps = 1;   // steps of the last block (where the last step's vectors sit)
+  int slot = 0;         // K-buffer slot the next block writes
+  int last_slot = 0;    // slot of the last block
+  bool slot_used[2] = {false, false};
+  hipStream_t fwd_stream = nullptr;   // internal stream of the forward kernel
+  hipEvent_t ev_entry = nullptr, ev_fwd[2] = {nullptr, nullptr}, ev_done[2] = {nullptr, nullptr};
   bool alive = false;
   std::string err;
   // profiling of the eligibility kernel
@@ -187,12 +203,13 @@ int check(eprop_ctx* ctx, hipError_t e, const char* what) {
 int pack_weights(eprop_ctx* ctx) {
   const eprop_config& c = ctx->plan.cfg;
   for (Layer& L : ctx->plan.layers) {
-    // drive weights transposed: Wt[i][j] = W[j][i], rows contiguous over j
-    int rc = check(ctx, eprop::launch_pack(L.W_src, c.n_rec, L.n_pre, L.Wt, L.ldj, L.n_pre, 1,
+    // drive weights transposed, Wt[i][j] = W[j][i], columns padded to 256
+    int rc = check(ctx, eprop::launch_pack(L.W_src, c.n_rec, L.n_pre, L.Wt, L.ldv, L.n_pre, 1,
                                            ctx->stream), "weight packing");
     if (rc) return rc;
-    rc = check(ctx, eprop::launch_pack(L.Wout_src, c.n_out, c.n_rec, L.Wop, L.ldj, c.n_out, 0,
-                                       ctx->stream), "readout weight packing");
+    // WoutT[j][k] = Wout[k][j]: the B operand of the learning-signal GEMM
+    rc = check(ctx, eprop::launch_pack(L.Wout_src, c.n_out, c.n_rec, L.WoutT, ctx->plan.ldk,
+                                       ctx->plan.ldn, 1, ctx->stream), "readout weight packing");
     if (rc) return rc;
   }
   return EPROP_OK;
@@ -228,49 +245,65 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   const Plan& P = ctx->plan;
   const eprop_config& c = P.cfg;
   hipStream_t s = ctx->stream;
+  hipStream_t sf = ctx->fwd_stream;
   const int first = ctx->t == 0;
+  const int sl = ctx->slot;
   int rc;
+  // The forward may overwrite this slot once the passes that read it two
+  // blocks ago are done.
+  if (ctx->slot_used[sl] &&
+      (rc = check(ctx, hipStreamWaitEvent(sf, ctx->ev_done[sl], 0), "stream wait")))
+    return rc;
 
   eprop::FwdArgs fa;
   for (int l = 0; l < 2; ++l) {
     eprop::FwdLayer& f = fa.L[l];
-    if (l >= c.n_layers) { f = fa.L[0]; continue; }
-    const Layer& L = P.layers[l];
-    f.Wt = L.Wt; f.ldw = L.ldj; f.Wout = L.Wop; f.ldo = L.ldj;
+    const Layer& L = P.layers[std::min(l, c.n_layers - 1)];
+    f.Wt = L.Wt; f.ldw = L.ldv; f.WoutT = L.WoutT;
     f.v = L.v; f.a = L.a; f.ztil = L.ztil; f.z = L.z; f.zbar = L.zbar; f.y = L.y;
-    f.lossacc = L.lossacc; f.psiK = L.psiK; f.LK = L.LK; f.zbarK = L.zbarK;
-    f.deltaK = L.deltaK; f.ztK = L.ztK;
-    f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.rows_per_wave = L.rows_per_wave;
+    f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.zbarK = L.zbarK[sl];
+    f.deltaK = L.deltaK[sl]; f.ztK = L.ztK[sl];
+    f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.rows_per_wave = L.rows_per_wave; f.ldi = L.n_pre_pad;
   }
   fa.n_layers = c.n_layers; fa.x = x; fa.n_in = c.n_in; fa.labels = labels;
   fa.err_flag = P.err_flag; fa.spikes = spikes; fa.W32 = (c.n_rec + 31) / 32;
   fa.B = c.batch; fa.Bp = P.Bp; fa.n_rec = c.n_rec; fa.K_out = c.n_out;
   fa.n_adaptive = c.n_adaptive; fa.Kmax = P.Kmax; fa.steps = steps;
-  fa.ldj = P.layers[0].ldj; fa.ldbk = P.ldbk; fa.jlist = P.jlist;
+  fa.ldj = P.layers[0].ldv; fa.ldk = P.ldk; fa.ldn = P.ldn; fa.jlist = P.jlist;
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
   fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem;
-  if ((rc = check(ctx, eprop::launch_forward(fa, s), "forward kernel"))) return rc;
+  if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
+  if ((rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
+  if ((rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
 
+  const int rows = steps * P.Bp;
   for (int l = 0; l < c.n_layers; ++l) {
     const Layer& L = P.layers[l];
-    // dW_out += sum over (t, b) of delta (x) ztilde: MFMA GEMM, then fp64 accumulation
+    // learning signal L[(t,b)][j] = sum_k delta[(t,b)][k] W_out[k][j]
+    eprop::GemmArgs gl;
+    gl.A = L.deltaK[sl]; gl.Bm = L.WoutT; gl.C = L.LK[sl];
+    gl.M = rows; gl.N = c.n_rec; gl.K = P.ldk; gl.lda = P.ldk; gl.ldb = P.ldk; gl.ldc = L.ldv;
+    gl.splits = 1; gl.k_chunk = P.ldk; gl.split_stride = 0;
+    if ((rc = check(ctx, eprop::launch_gemm_nt(gl, s), "learning-signal GEMM"))) return rc;
+
+    // dW_out += sum over (t, b) of delta (x) ztilde, then fp64 accumulation
     eprop::GemmArgs g;
-    g.A = L.deltaK; g.Bm = L.ztK; g.C = L.Cpart;
-    g.M = c.n_out; g.N = c.n_rec; g.K = steps * P.Bp; g.lda = P.ldbk; g.ldb = P.ldbk;
-    g.ldc = c.n_rec;
+    g.A = L.deltaK[sl]; g.Bm = L.ztK[sl]; g.C = L.Cpart;
+    g.M = c.n_out; g.N = c.n_rec; g.K = rows; g.lda = P.ldk; g.ldb = P.ldn; g.ldc = c.n_rec;
     choose_splits(g.M, g.N, g.K, P.out_splits, &g.splits, &g.k_chunk);
     g.split_stride = (size_t)c.n_out * c.n_rec;
-    if ((rc = check(ctx, eprop::launch_gemm_nt(g, s), "readout gradient GEMM"))) return rc;
+    if ((rc = check(ctx, eprop::launch_gemm_tn(g, s), "readout gradient GEMM"))) return rc;
     if ((rc = check(ctx, eprop::launch_accumulate(L.Cpart, g.splits, g.split_stride, c.n_out,
                                                   c.n_rec, L.accout, L.ldj, first, s),
                     "readout gradient accumulation")))
       return rc;
 
     eprop::TraceArgs ta;
-    ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.zbarK = L.zbarK;
-    ta.psiK = L.psiK; ta.LK = L.LK; ta.B = c.batch; ta.n_pre = L.n_pre; ta.n_post = c.n_rec;
-    ta.ldj = L.ldj; ta.n_adaptive = c.n_adaptive; ta.lda = L.lda; ta.Kmax = P.Kmax;
-    ta.steps = steps; ta.kappa = c.kappa; ta.rho = c.rho; ta.beta = c.beta; ta.first = first;
+    ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.zbarK = L.zbarK[sl];
+    ta.psiK = L.psiK[sl]; ta.LK = L.LK[sl]; ta.B = c.batch; ta.Bp = P.Bp; ta.n_pre_pad = L.n_pre_pad;
+    ta.n_post = c.n_rec; ta.ldj = L.ldj; ta.ldv = L.ldv; ta.n_adaptive = c.n_adaptive;
+    ta.lda = L.lda; ta.Kmax = P.Kmax; ta.ldi = L.n_pre_pad; ta.steps = steps;
+    ta.kappa = c.kappa; ta.rho = c.rho; ta.beta = c.beta; ta.first = first;
     const bool timed = ctx->prof && ctx->prof_n < ctx->prof_max;
     if (timed && (rc = check(ctx, hipEventRecord(ctx->ev[2 * ctx->prof_n], s), "event record")))
       return rc;
@@ -282,12 +315,24 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
       ctx->prof_n++;
     }
   }
+  if ((rc = check(ctx, hipEventRecord(ctx->ev_done[sl], s), "event record"))) return rc;
+  ctx->slot_used[sl] = true;
+  ctx->last_slot = sl;
+  ctx->slot ^= 1;
   ctx->t += steps;
   ctx->last_steps = steps;
   return EPROP_OK;
 }
 
 bool usable(const eprop_ctx* ctx) { return ctx && ctx->alive; }
+
+// Work queued on the caller's stream before this call (inputs, a reset, new
+// weights) happens before the forward kernels of this call.
+int join_forward_stream(eprop_ctx* ctx) {
+  int rc = check(ctx, hipEventRecord(ctx->ev_entry, ctx->stream), "event record");
+  if (!rc) rc = check(ctx, hipStreamWaitEvent(ctx->fwd_stream, ctx->ev_entry, 0), "stream wait");
+  return rc;
+}
 
 }  // namespace
 
@@ -334,13 +379,21 @@ int eprop_init(const eprop_config* cfg, void* d_workspace, size_t ws_bytes,
     ctx->plan.layers[l].W_src = d_weights[2 * l];
     ctx->plan.layers[l].Wout_src = d_weights[2 * l + 1];
   }
+  int rc = check(ctx, hipStreamCreateWithFlags(&ctx->fwd_stream, hipStreamNonBlocking),
+                 "stream create");
+  if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_entry, hipEventDisableTiming), "event create");
+  for (int k = 0; k < 2 && !rc; ++k) {
+    rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_fwd[k], hipEventDisableTiming), "event create");
+    if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_done[k], hipEventDisableTiming),
+                        "event create");
+  }
   // Padding of every buffer must read as zero; clear the whole layout once.
-  int rc = check(ctx, hipMemsetAsync(ctx->ws, 0, ctx->plan.bytes, ctx->stream), "workspace clear");
+  if (!rc) rc = check(ctx, hipMemsetAsync(ctx->ws, 0, ctx->plan.bytes, ctx->stream), "workspace clear");
   if (!rc) rc = pack_weights(ctx);
   if (!rc) rc = clear_state(ctx);
   if (rc) {
     g_last_error = ctx->err;
-    delete ctx;
+    eprop_destroy(ctx);
     return rc;
   }
   ctx->alive = true;
@@ -351,6 +404,8 @@ int eprop_init(const eprop_config* cfg, void* d_workspace, size_t ws_bytes,
 int eprop_step(eprop_ctx* ctx, const uint8_t* d_x_t, const int32_t* d_labels, uint32_t* d_spikes_t) {
   if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
   if (!d_x_t || !d_labels) return fail(ctx, EPROP_EINVAL, "x or labels is NULL");
+  int rc = join_forward_stream(ctx);
+  if (rc) return rc;
   return do_block(ctx, d_x_t, 1, d_labels, d_spikes_t);
 }
 
@@ -362,6 +417,8 @@ int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int3
   const eprop_config& c = ctx->plan.cfg;
   const size_t x_step = (size_t)c.batch * c.n_in;
   const size_t s_step = (size_t)c.n_layers * c.batch * ((c.n_rec + 31) / 32);
+  int rc0 = join_forward_stream(ctx);
+  if (rc0) return rc0;
   for (int32_t t = 0; t < T;) {
     const int steps = std::min<int32_t>(ctx->plan.Kmax, T - t);
     int rc = do_block(ctx, d_x + t * x_step, steps, d_labels,
@@ -418,6 +475,13 @@ int eprop_status(eprop_ctx* ctx) {
 
 void eprop_destroy(eprop_ctx* ctx) {
   if (!ctx) return;
+  if (ctx->fwd_stream) {
+    (void)hipStreamSynchronize(ctx->fwd_stream);
+    (void)hipStreamDestroy(ctx->fwd_stream);
+  }
+  hipEvent_t own[] = {ctx->ev_entry, ctx->ev_fwd[0], ctx->ev_fwd[1], ctx->ev_done[0], ctx->ev_done[1]};
+  for (hipEvent_t e : own)
+    if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
   ctx->alive = false;
   delete ctx;
@@ -472,13 +536,13 @@ int eprop_debug_buffer(eprop_ctx* ctx, int32_t layer, int32_t which, const float
   const eprop_config& c = ctx->plan.cfg;
   if (layer < 0 || layer >= c.n_layers) return fail(ctx, EPROP_EINVAL, "bad layer");
   const Layer& L = ctx->plan.layers[layer];
-  const int64_t kstride = (int64_t)ctx->plan.Kmax * L.ldj;   // rows of psiK, LK are [b][t]
-  const int64_t tl = ctx->last_steps - 1;
+  // psiK and LK rows are t*Bp + b: the last step's rows start at (last_steps-1)*Bp
+  const int64_t tl = (int64_t)(ctx->last_steps - 1) * ctx->plan.Bp;
   switch (which) {
     case 0: *d_ptr = L.v; *cols = c.n_rec; *ld = c.n_rec; break;
     case 1: *d_ptr = L.a; *cols = c.n_rec; *ld = c.n_rec; break;
-    case 2: *d_ptr = L.psiK + tl * L.ldj; *cols = c.n_rec; *ld = kstride; break;
-    case 3: *d_ptr = L.LK + tl * L.ldj; *cols = c.n_rec; *ld = kstride; break;
+    case 2: *d_ptr = L.psiK[ctx->last_slot] + tl * L.ldv; *cols = c.n_rec; *ld = L.ldv; break;
+    case 3: *d_ptr = L.LK[ctx->last_slot] + tl * L.ldv; *cols = c.n_rec; *ld = L.ldv; break;
     case 4: *d_ptr = L.y; *cols = c.n_out; *ld = c.n_out; break;
     default: return fail(ctx, EPROP_EINVAL, "unknown buffer");
   }

@@ -3,14 +3,15 @@
 //
 // The sequence is processed in blocks of up to Kmax timesteps.  For a block,
 // the forward kernel runs the network for every step (one workgroup per
-// batch element) and leaves per-step vectors in "K buffers":
-//   psiK, LK  [B][Kmax][ldj]   pseudo-derivative and learning signal
-//   zbarK     [n_pre][B][Kmax] filtered presynaptic vector
-//   deltaK    [K_out][ldbk]    readout error, column t*Bp + b
-//   ztK       [n_rec][ldbk]    kappa-filtered spikes, column t*Bp + b
-// then the readout-gradient GEMM contracts deltaK and ztK over (t, b), and
-// the eligibility kernel advances every synapse's traces through the block's
-// steps with one read and one write of the traces.
+// batch element) and leaves per-step vectors in "K buffers" (row r = t*Bp + b):
+//   psiK   [Kmax*Bp][ldv]  pseudo-derivative (ldv = n_rec rounded to 256)
+//   deltaK [rows][ldk]     readout error (softmax - onehot)
+//   ztK    [rows][ldn]     kappa-filtered spikes
+//   zbarK  [B][Kmax][ldi]  filtered presynaptic vector
+// Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
+// psiK) and the readout gradient dW_out += deltaK^T * ztK.  The eligibility
+// kernel then advances every synapse's traces through the block's steps with
+// one read and one write of the traces.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -20,19 +21,23 @@
 namespace eprop {
 
 constexpr int kFwdThreads = 256;
+constexpr int kTraceRows = 2;          // presynaptic rows per eligibility thread
+constexpr int kTraceWaves = 4;         // waves per eligibility workgroup (same 256 neurons)
+constexpr int kTraceChunk = 16;        // steps staged in shared memory at a time
+constexpr int kRowPad = kTraceRows * kTraceWaves;   // n_pre padded to a multiple of this
 
 struct FwdLayer {
   const float* Wt; int ldw;      // transposed drive weights [n_pre][ldw]
-  const float* Wout; int ldo;    // readout weights [K_out][ldo]
+  const float* WoutT;            // transposed readout weights [n_rec_pad][ldk]
   float* v; float* a; float* ztil;   // state [B][n_rec]
   uint8_t* z;                    // state: spikes of the last step [B][n_rec]
   float* zbar;                   // state [B][n_pre]
   float* y;                      // state [B][K_out]
   double* lossacc;               // [B]
-  float* psiK; float* LK;        // [B][Kmax][ldj]
-  float* zbarK;                  // [n_pre][B][Kmax]
-  float* deltaK; float* ztK;     // [K_out_pad][ldbk], [n_rec_pad][ldbk]
-  int n_inl, n_pre, rows_per_wave;
+  float* psiK;                   // [rows][ldj]
+  float* zbarK;                  // [B][Kmax][ldi]
+  float* deltaK; float* ztK;     // [rows][ldk], [rows][ldn]
+  int n_inl, n_pre, rows_per_wave, ldi;
 };
 
 struct FwdArgs {
@@ -44,15 +49,17 @@ struct FwdArgs {
   int* err_flag;
   uint32_t* spikes;              // NULL or [steps][n_layers][B][W32]
   int W32;
-  int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldbk, jlist;
+  int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldk, ldn, jlist;  // ldj: row stride of psiK
   float alpha, rho, kappa, thr, beta, gamma_over_thr;
   size_t smem;
 };
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
 
-// C_part[s][m][n] = sum_{k in split s} A[m][k] * Bm[n][k]   (fp32 MFMA).
-// A has >= round_up(M,32) rows, Bm >= round_up(N,32) rows, both zero padded
-// to K columns (K a multiple of 16).  Split s covers [s*k_chunk, min(K,(s+1)*k_chunk)).
+// NT: C_part[s][m][n] = sum_{k in split s} A[m][k] * Bm[n][k]
+// TN: C_part[s][m][n] = sum_{k in split s} A[k][m] * Bm[k][n]
+// fp32 MFMA.  Operands are zero padded: A and Bm provide round_up(M,32) and
+// round_up(N,32) rows (NT) or columns (TN), and K is a multiple of 16.
+// Split s covers k in [s*k_chunk, min(K,(s+1)*k_chunk)).
 struct GemmArgs {
   const float* A;
   const float* Bm;
@@ -62,6 +69,7 @@ struct GemmArgs {
   size_t split_stride;  // elements between consecutive split outputs
 };
 hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_tn(const GemmArgs& a, hipStream_t s);
 
 // acc[m][n] (fp64, row stride ld_acc) = (first ? 0 : acc) + sum_s part[s][m][n].
 hipError_t launch_accumulate(const float* part, int splits, size_t split_stride, int M, int N,
@@ -69,12 +77,12 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 
 // Eligibility vectors and gradient accumulation over `steps` timesteps.
 struct TraceArgs {
-  float* ebar;     // [B][n_pre][ldj]
-  float* epsa;     // [B][n_pre][lda]
-  double* acc;     // [n_pre][ldj]
-  const float* zbarK;                 // [n_pre][B][Kmax]
-  const float* psiK; const float* LK; // [B][Kmax][ldj]
-  int B, n_pre, n_post, ldj, n_adaptive, lda, Kmax, steps;
+  float* ebar;     // [B][n_pre_pad][ldj]
+  float* epsa;     // [B][n_pre_pad][lda]
+  double* acc;     // [n_pre_pad][ldj]
+  const float* zbarK;                 // [B][Kmax][ldi]
+  const float* psiK; const float* LK; // [rows][ldv], row t*Bp + b, ldv a multiple of 256
+  int B, Bp, n_pre_pad, n_post, ldj, ldv, n_adaptive, lda, Kmax, ldi, steps;
   float kappa, rho, beta;
   int first;       // 1: traces and accumulators start at zero (not read)
 };
@@ -91,8 +99,8 @@ hipError_t launch_grads(const GradsArgs& a, hipStream_t s);
 hipError_t launch_loss(const double* lossacc, int B, int n_layers, size_t layer_stride,
                        double* out, hipStream_t s);
 
-// src [rows][cols] row-major -> dst [rows_pad][ldd] (transpose = 0) or
-// dst [cols_pad][ldd] with dst[c][r] = src[r][c] (transpose = 1); zero padded.
+// src [rows][cols] row-major -> dst [dst_rows][ldd] (transpose = 0) or
+// dst[c][r] = src[r][c] (transpose = 1); every other element of dst is zero.
 hipError_t launch_pack(const float* src, int rows, int cols, float* dst, int ldd, int dst_rows,
                        int transpose, hipStream_t s);
 

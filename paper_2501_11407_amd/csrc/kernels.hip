@@ -40,8 +40,9 @@ __device__ inline void store_nt(float* p, f32x4 v) { __builtin_nontemporal_store
 inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
 // ---------------------------------------------------------------- forward
-// One workgroup per batch element runs `steps` timesteps of every layer.
-// Per step and layer:
+// One workgroup per batch element runs `steps` timesteps of every layer; the
+// neuron state of the threads' neurons stays in registers, the filtered
+// presynaptic vector and the readout in shared memory.  Per step and layer:
 //   1. p = [in ; z_prev]; zbar = alpha*zbar + p; each wave lists the indices
 //      of its contiguous slice of p that are 1, in ascending order.
 //   2. drive I_j = sum of W_ji over the listed i, visited in ascending i (the
@@ -53,168 +54,222 @@ inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 //        psi = (gamma/thr) * max(0, 1 - |x|/thr)
 //   3. readout y = kappa*y + W_out z (over the spiking neurons), softmax,
 //      delta = softmax - onehot(label), cross-entropy into the loss;
-//   4. learning signal L = W_out^T delta and ztilde = kappa*ztilde + z.
+//   4. ztilde = kappa*ztilde + z.
+// The learning signal L = W_out^T delta is one GEMM over the whole block.
+struct FwdLds {
+  int* act; int* spk; int* cnt; float* red; float* sy; float* szb; uint8_t* zc;
+  int rwmax, npad;
+};
+
+template <int QN, int LI>
+__device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLds& S, int t, int b,
+                                                   int cur, float (&v)[QN], float (&ad)[QN],
+                                                   float (&zt)[QN], double& loss) {
+  const FwdLayer& Ly = A.L[LI];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint8_t* zprev = S.zc + (LI * 2 + cur) * S.npad;
+  uint8_t* znow = S.zc + (LI * 2 + (cur ^ 1)) * S.npad;
+  const uint8_t* inp;
+  if constexpr (LI == 0)
+    inp = A.x + ((size_t)t * A.B + b) * A.n_in;
+  else
+    inp = S.zc + ((LI - 1) * 2 + (cur ^ 1)) * S.npad;
+  float* szb = S.szb + (LI == 0 ? 0 : A.L[0].n_pre);
+  float* sy = S.sy + LI * A.K_out;
+  const size_t row = (size_t)t * A.Bp + b;
+
+  // 1. presynaptic vector, its filter, ordered active lists
+  const int rw = Ly.rows_per_wave;
+  const int i_beg = w * rw, i_end = min(Ly.n_pre, i_beg + rw);
+  float* zbk = Ly.zbarK + ((size_t)b * A.Kmax + t) * Ly.ldi;
+  int n_act = 0;
+  for (int base = i_beg; base < i_end; base += kWave) {
+    const int i = base + lane;
+    bool on = false;
+    if (i < i_end) {
+      const uint8_t sv = (i < Ly.n_inl) ? inp[i] : zprev[i - Ly.n_inl];
+      on = sv != 0;
+      const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
+      szb[i] = zv;
+      zbk[i] = zv;
+    }
+    const unsigned long long m = __ballot(on);
+    if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
+    n_act += __popcll(m);
+  }
+  if (lane == 0) S.cnt[w] = n_act;
+  __syncthreads();
+
+  // 2. drive and neuron step.  Rows of Wt are padded to a multiple of 256
+  // columns; chunks q with q*256 >= n_rec are skipped (QN is rounded up).
+  float I[QN];
+#pragma unroll
+  for (int q = 0; q < QN; ++q) I[q] = 0.0f;
+  for (int ww = 0; ww < 4; ++ww) {
+    const int c = S.cnt[ww];
+    const int* lst = S.act + ww * S.rwmax;
+#pragma unroll 4
+    for (int k = 0; k < c; ++k) {
+      const float* wrow = Ly.Wt + (size_t)lst[k] * Ly.ldw + tid;
+#pragma unroll
+      for (int q = 0; q < QN; ++q)
+        if (q * kFwdThreads < A.n_rec) I[q] += wrow[q * kFwdThreads];
+    }
+  }
+  int n_spk = 0;
+#pragma unroll
+  for (int q = 0; q < QN; ++q) {
+    const int j = q * kFwdThreads + tid;
+    bool z = false;
+    if (j < A.n_rec) {
+      const float zp = zprev[j] ? 1.0f : 0.0f;
+      float vv = A.alpha * v[q];
+      vv = vv + I[q];
+      vv = vv - A.thr * zp;
+      float aa = A.rho * ad[q];
+      aa = aa + zp;
+      const float bj = (j < A.n_adaptive) ? A.beta : 0.0f;
+      float th = bj * aa;
+      th = A.thr + th;
+      const float x = vv - th;
+      v[q] = vv;
+      ad[q] = aa;
+      z = x > 0.0f;
+      znow[j] = z ? 1 : 0;
+      const float u = 1.0f - fabsf(x) / A.thr;
+      Ly.psiK[row * A.ldj + j] = A.gamma_over_thr * fmaxf(u, 0.0f);
+    }
+    const unsigned long long m = __ballot(z);
+    if (z) S.spk[w * A.jlist + n_spk + lanes_below(m, lane)] = j;
+    n_spk += __popcll(m);
+    if (A.spikes) {
+      const int w0 = (q * kFwdThreads + w * kWave) >> 5;
+      uint32_t* srow = A.spikes + (((size_t)t * A.n_layers + LI) * A.B + b) * A.W32;
+      if (lane == 0 && w0 < A.W32) srow[w0] = (uint32_t)m;
+      if (lane == 1 && w0 + 1 < A.W32) srow[w0 + 1] = (uint32_t)(m >> 32);
+    }
+  }
+  if (lane == 0) S.cnt[4 + w] = n_spk;
+  __syncthreads();
+
+  // 3. readout (rows of the transposed readout weights of the spiking
+  // neurons, read coalesced over k), softmax cross-entropy
+  for (int k = tid; k < A.K_out; k += kFwdThreads) {
+    float Y = 0.0f;
+    for (int ww = 0; ww < 4; ++ww) {
+      const int c = S.cnt[4 + ww];
+      const int* lst = S.spk + ww * A.jlist;
+#pragma unroll 8
+      for (int s = 0; s < c; ++s) Y += Ly.WoutT[(size_t)lst[s] * A.ldk + k];
+    }
+    float yy = A.kappa * sy[k];
+    yy = yy + Y;
+    sy[k] = yy;
+  }
+  __syncthreads();
+  const int label = A.labels[b];
+  const bool label_ok = label >= 0 && label < A.K_out;
+  if (w == 0) {
+    float m = -INFINITY;
+    for (int k = lane; k < A.K_out; k += kWave) m = fmaxf(m, sy[k]);
+    m = wave_max(m);
+    float se = 0.0f;
+    for (int k = lane; k < A.K_out; k += kWave) se += expf(sy[k] - m);
+    se = wave_sum(se);
+    if (lane == 0) {
+      S.red[0] = m;
+      S.red[1] = se;
+      if (label_ok)
+        loss += log((double)se) - ((double)sy[label] - (double)m);
+      else
+        *A.err_flag = 1;
+    }
+  }
+  __syncthreads();
+  {
+    const float m = S.red[0], se = S.red[1];
+    for (int k = tid; k < A.K_out; k += kFwdThreads) {
+      const float d = expf(sy[k] - m) / se - ((k == label) ? 1.0f : 0.0f);
+      Ly.deltaK[row * A.ldk + k] = d;
+    }
+  }
+
+  // 4. filtered spikes
+#pragma unroll
+  for (int q = 0; q < QN; ++q) {
+    const int j = q * kFwdThreads + tid;
+    if (j < A.n_rec) {
+      float zz = A.kappa * zt[q];
+      zz = zz + (znow[j] ? 1.0f : 0.0f);
+      zt[q] = zz;
+      Ly.ztK[row * A.ldn + j] = zz;
+    }
+  }
+  __syncthreads();
+}
+
+template <int QN, int LI>
+__device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S, int b, bool load,
+                                              float (&v)[QN], float (&ad)[QN], float (&zt)[QN],
+                                              int cur) {
+  const FwdLayer& Ly = A.L[LI];
+  const int tid = threadIdx.x;
+  float* szb = S.szb + (LI == 0 ? 0 : A.L[0].n_pre);
+  float* sy = S.sy + LI * A.K_out;
+  uint8_t* zc = S.zc + (LI * 2 + cur) * S.npad;
+#pragma unroll
+  for (int q = 0; q < QN; ++q) {
+    const int j = q * kFwdThreads + tid;
+    if (j < A.n_rec) {
+      const size_t o = (size_t)b * A.n_rec + j;
+      if (load) {
+        v[q] = Ly.v[o]; ad[q] = Ly.a[o]; zt[q] = Ly.ztil[o]; zc[j] = Ly.z[o];
+      } else {
+        Ly.v[o] = v[q]; Ly.a[o] = ad[q]; Ly.ztil[o] = zt[q]; Ly.z[o] = zc[j];
+      }
+    }
+  }
+  for (int i = tid; i < Ly.n_pre; i += kFwdThreads) {
+    if (load) szb[i] = Ly.zbar[(size_t)b * Ly.n_pre + i];
+    else Ly.zbar[(size_t)b * Ly.n_pre + i] = szb[i];
+  }
+  for (int k = tid; k < A.K_out; k += kFwdThreads) {
+    if (load) sy[k] = Ly.y[(size_t)b * A.K_out + k];
+    else Ly.y[(size_t)b * A.K_out + k] = sy[k];
+  }
+}
+
+template <int QN>
 __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs A) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int b = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  int rwmax = A.L[0].rows_per_wave;
-  if (A.n_layers > 1) rwmax = max(rwmax, A.L[1].rows_per_wave);
-  int* act = (int*)smem;                 // [4][rwmax]  active presynaptic indices
-  int* spk = act + 4 * rwmax;            // [4][jlist]  spiking neurons
-  int* cnt = spk + 4 * A.jlist;          // [8]         list lengths
-  float* sy = (float*)(cnt + 8);         // [K_out]
-  float* sd = sy + A.K_out;              // [K_out]
-  float* red = sd + A.K_out;             // [2]         max, sum of the softmax
-  uint8_t* zc = (uint8_t*)(red + 2);     // [n_layers][2][npad] spikes at t-1 and t
-  const int npad = (A.n_rec + 3) & ~3;
-  const int label = A.labels[b];
-  const bool label_ok = label >= 0 && label < A.K_out;
-  const int QN = (A.n_rec + kFwdThreads - 1) / kFwdThreads;
+  FwdLds S;
+  S.rwmax = A.L[0].rows_per_wave;
+  if (A.n_layers > 1) S.rwmax = max(S.rwmax, A.L[1].rows_per_wave);
+  S.npad = (A.n_rec + 3) & ~3;
+  S.act = (int*)smem;                          // [4][rwmax]
+  S.spk = S.act + 4 * S.rwmax;                 // [4][jlist]
+  S.cnt = S.spk + 4 * A.jlist;                 // [8]
+  S.red = (float*)(S.cnt + 8);                 // [2]
+  S.sy = S.red + 2;                            // [n_layers][K_out]
+  S.szb = S.sy + A.n_layers * A.K_out;         // [n_pre_0 + n_pre_1]
+  const int npre_total = A.L[0].n_pre + (A.n_layers > 1 ? A.L[1].n_pre : 0);
+  S.zc = (uint8_t*)(S.szb + npre_total);       // [n_layers][2][npad]
 
-  for (int l = 0; l < A.n_layers; ++l)
-    for (int j = tid; j < A.n_rec; j += kFwdThreads)
-      zc[(l * 2) * npad + j] = A.L[l].z[(size_t)b * A.n_rec + j];
+  float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
+  forward_state<QN, 0>(A, S, b, true, v0, a0, zt0, 0);
+  if (A.n_layers > 1) forward_state<QN, 1>(A, S, b, true, v1, a1, zt1, 0);
   double loss0 = 0.0, loss1 = 0.0;
   int cur = 0;
   __syncthreads();
-
   for (int t = 0; t < A.steps; ++t) {
-    for (int l = 0; l < A.n_layers; ++l) {
-      const FwdLayer& Ly = A.L[l];
-      const uint8_t* zprev = zc + (l * 2 + cur) * npad;
-      uint8_t* znow = zc + (l * 2 + (cur ^ 1)) * npad;
-      const uint8_t* inp = (l == 0) ? A.x + ((size_t)t * A.B + b) * A.n_in
-                                    : zc + ((l - 1) * 2 + (cur ^ 1)) * npad;
-
-      // 1. presynaptic vector, its filter, ordered active lists
-      const int rw = Ly.rows_per_wave;
-      const int i_beg = w * rw, i_end = min(Ly.n_pre, i_beg + rw);
-      int n_act = 0;
-      for (int base = i_beg; base < i_end; base += kWave) {
-        const int i = base + lane;
-        bool on = false;
-        if (i < i_end) {
-          const uint8_t sv = (i < Ly.n_inl) ? inp[i] : zprev[i - Ly.n_inl];
-          on = sv != 0;
-          float* zp = Ly.zbar + (size_t)b * Ly.n_pre + i;
-          const float zv = A.alpha * *zp + (on ? 1.0f : 0.0f);
-          *zp = zv;
-          Ly.zbarK[((size_t)i * A.B + b) * A.Kmax + t] = zv;
-        }
-        const unsigned long long m = __ballot(on);
-        if (on) act[w * rwmax + n_act + lanes_below(m, lane)] = i;
-        n_act += __popcll(m);
-      }
-      if (lane == 0) cnt[w] = n_act;
-      __syncthreads();
-
-      // 2. drive and neuron step
-      int n_spk = 0;
-      for (int q = 0; q < QN; ++q) {
-        const int j = q * kFwdThreads + tid;
-        bool z = false;
-        if (j < A.n_rec) {
-          float I = 0.0f;
-          for (int ww = 0; ww < 4; ++ww) {
-            const int c = cnt[ww];
-            const int* lst = act + ww * rwmax;
-#pragma unroll 8
-            for (int k = 0; k < c; ++k) I += Ly.Wt[(size_t)lst[k] * Ly.ldw + j];
-          }
-          const size_t o = (size_t)b * A.n_rec + j;
-          const float zp = zprev[j] ? 1.0f : 0.0f;
-          float v = A.alpha * Ly.v[o];
-          v = v + I;
-          v = v - A.thr * zp;
-          float ad = A.rho * Ly.a[o];
-          ad = ad + zp;
-          const float bj = (j < A.n_adaptive) ? A.beta : 0.0f;
-          float th = bj * ad;
-          th = A.thr + th;
-          const float x = v - th;
-          Ly.v[o] = v;
-          Ly.a[o] = ad;
-          z = x > 0.0f;
-          znow[j] = z ? 1 : 0;
-          const float u = 1.0f - fabsf(x) / A.thr;
-          Ly.psiK[((size_t)b * A.Kmax + t) * A.ldj + j] = A.gamma_over_thr * fmaxf(u, 0.0f);
-        }
-        const unsigned long long m = __ballot(z);
-        if (z) spk[w * A.jlist + n_spk + lanes_below(m, lane)] = j;
-        n_spk += __popcll(m);
-        if (A.spikes) {
-          const int w0 = (q * kFwdThreads + w * kWave) >> 5;
-          uint32_t* row = A.spikes + (((size_t)t * A.n_layers + l) * A.B + b) * A.W32;
-          if (lane == 0 && w0 < A.W32) row[w0] = (uint32_t)m;
-          if (lane == 1 && w0 + 1 < A.W32) row[w0 + 1] = (uint32_t)(m >> 32);
-        }
-      }
-      if (lane == 0) cnt[4 + w] = n_spk;
-      __syncthreads();
-
-      // 3. readout, softmax cross-entropy
-      for (int k = tid; k < A.K_out; k += kFwdThreads) {
-        float Y = 0.0f;
-        for (int ww = 0; ww < 4; ++ww) {
-          const int c = cnt[4 + ww];
-          const int* lst = spk + ww * A.jlist;
-          for (int s = 0; s < c; ++s) Y += Ly.Wout[(size_t)k * Ly.ldo + lst[s]];
-        }
-        float yy = A.kappa * Ly.y[(size_t)b * A.K_out + k];
-        yy = yy + Y;
-        Ly.y[(size_t)b * A.K_out + k] = yy;
-        sy[k] = yy;
-      }
-      __syncthreads();
-      if (w == 0) {
-        float m = -INFINITY;
-        for (int k = lane; k < A.K_out; k += kWave) m = fmaxf(m, sy[k]);
-        m = wave_max(m);
-        float se = 0.0f;
-        for (int k = lane; k < A.K_out; k += kWave) se += expf(sy[k] - m);
-        se = wave_sum(se);
-        if (lane == 0) {
-          red[0] = m;
-          red[1] = se;
-          if (label_ok) {
-            const double ce = log((double)se) - ((double)sy[label] - (double)m);
-            if (l == 0) loss0 += ce; else loss1 += ce;
-          } else {
-            *A.err_flag = 1;
-          }
-        }
-      }
-      __syncthreads();
-      {
-        const float m = red[0], se = red[1];
-        for (int k = tid; k < A.K_out; k += kFwdThreads) {
-          const float d = expf(sy[k] - m) / se - ((k == label) ? 1.0f : 0.0f);
-          sd[k] = d;
-          Ly.deltaK[(size_t)k * A.ldbk + (size_t)t * A.Bp + b] = d;
-        }
-      }
-      __syncthreads();
-
-      // 4. learning signal and filtered spikes
-      for (int j = tid; j < A.n_rec; j += kFwdThreads) {
-        float Lj = 0.0f;
-        for (int k = 0; k < A.K_out; ++k) Lj = fmaf(Ly.Wout[(size_t)k * Ly.ldo + j], sd[k], Lj);
-        Ly.LK[((size_t)b * A.Kmax + t) * A.ldj + j] = Lj;
-        const size_t o = (size_t)b * A.n_rec + j;
-        float zt = A.kappa * Ly.ztil[o];
-        zt = zt + (znow[j] ? 1.0f : 0.0f);
-        Ly.ztil[o] = zt;
-        Ly.ztK[(size_t)j * A.ldbk + (size_t)t * A.Bp + b] = zt;
-      }
-      __syncthreads();
-    }
+    forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0);
+    if (A.n_layers > 1) forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1);
     cur ^= 1;
   }
-  for (int l = 0; l < A.n_layers; ++l)
-    for (int j = tid; j < A.n_rec; j += kFwdThreads)
-      A.L[l].z[(size_t)b * A.n_rec + j] = zc[(l * 2 + cur) * npad + j];
-  if (tid == 0) {
+  forward_state<QN, 0>(A, S, b, false, v0, a0, zt0, cur);
+  if (A.n_layers > 1) forward_state<QN, 1>(A, S, b, false, v1, a1, zt1, cur);
+  if (threadIdx.x == 0) {
     A.L[0].lossacc[b] += loss0;
     if (A.n_layers > 1) A.L[1].lossacc[b] += loss1;
   }
@@ -274,6 +329,53 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
   }
 }
 
+// Same tiling with both operands stored k-major: lane (r, g) takes
+// A[k][m0 + r] and Bm[k][n0 + r] for its four k of every 16-k chunk.
+__global__ __launch_bounds__(256) void gemm_tn_kernel(GemmArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int m0 = blockIdx.y * 32;
+  const int n0 = (blockIdx.x * 4 + wave) * 32;
+  if (n0 >= a.N) return;
+  const int split = blockIdx.z;
+  const int kb = split * a.k_chunk;
+  const int ke = min(a.K, kb + a.k_chunk);
+  const int r = lane & 15, g = lane >> 4;
+  f32x4 c00 = {0.f, 0.f, 0.f, 0.f}, c01 = c00, c10 = c00, c11 = c00;
+  for (int k = kb; k < ke; k += 16) {
+    f32x4 va0, va1, vb0, vb1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const size_t kk = (size_t)(k + 4 * g + q);
+      va0[q] = a.A[kk * a.lda + m0 + r];
+      va1[q] = a.A[kk * a.lda + m0 + 16 + r];
+      vb0[q] = a.Bm[kk * a.ldb + n0 + r];
+      vb1[q] = a.Bm[kk * a.ldb + n0 + 16 + r];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      c00 = __builtin_amdgcn_mfma_f32_16x16x4f32(va0[q], vb0[q], c00, 0, 0, 0);
+      c01 = __builtin_amdgcn_mfma_f32_16x16x4f32(va0[q], vb1[q], c01, 0, 0, 0);
+      c10 = __builtin_amdgcn_mfma_f32_16x16x4f32(va1[q], vb0[q], c10, 0, 0, 0);
+      c11 = __builtin_amdgcn_mfma_f32_16x16x4f32(va1[q], vb1[q], c11, 0, 0, 0);
+    }
+  }
+  float* out = a.C + (size_t)split * a.split_stride;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int mA = m0 + 4 * g + q, mB = mA + 16;
+    const int nA = n0 + r, nB = nA + 16;
+    if (mA < a.M) {
+      if (nA < a.N) out[(size_t)mA * a.ldc + nA] = c00[q];
+      if (nB < a.N) out[(size_t)mA * a.ldc + nB] = c01[q];
+    }
+    if (mB < a.M) {
+      if (nA < a.N) out[(size_t)mB * a.ldc + nA] = c10[q];
+      if (nB < a.N) out[(size_t)mB * a.ldc + nB] = c11[q];
+    }
+  }
+}
+
 // Split-K partials added into an fp64 accumulator in split order.
 __global__ __launch_bounds__(256) void accumulate_kernel(const float* part, int splits, size_t ss,
                                                         int M, int N, double* acc, int ld, int first) {
@@ -286,118 +388,149 @@ __global__ __launch_bounds__(256) void accumulate_kernel(const float* part, int 
 }
 
 // ---------------------------------------------------------------- eligibility
-// One thread owns 4 consecutive postsynaptic neurons j0..j0+3 of IT
-// consecutive presynaptic rows i0..i0+IT-1 and walks the batch.  For each
-// (b, i, j) it reads the traces once, advances them through the block's
-// steps, and writes them once.  Per step:
-//   e    = psi_j (zbar_i - beta_j epsa)          (dz_j/dW_ji)
+// A workgroup owns one 256-wide segment of postsynaptic neurons and
+// kTraceWaves*kTraceRows presynaptic rows; lane l of every wave owns the four
+// neurons j0 = seg*256 + 4l..4l+3, wave w the rows i0 = ib + w*kTraceRows...
+// The workgroup walks the batch; for each batch element the traces are read
+// once (prefetched while the previous element computes), advanced through
+// the block's steps and written once.  psi and L of the segment and zbar of
+// the rows are staged in shared memory kTraceChunk steps at a time and shared
+// by all waves.  Per step, for each (i, j):
+//   e    = psi_j zbar_i - psi_j beta_j epsa      (dz_j/dW_ji)
 //   ebar = kappa ebar + e                        (readout filter on the trace)
-//   acc += L_j ebar                              (fp64)
-//   epsa = psi_j zbar_i + (rho - beta_j psi_j) epsa   (adaptive j only)
-// zbar_i of a (b, i, t) is the same for the whole block: a scalar load.  Trace
-// rows are j-contiguous, so a wave moves 1 KiB per 16-byte lane access; the
-// next batch element's traces are loaded before the current ones are stored.
-template <int IT, bool FIRST>
-__global__ __launch_bounds__(256) void trace_kernel(TraceArgs a) {
-  const int j0 = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
-  const int i0 = blockIdx.x * IT;
-  if (j0 >= a.n_post) return;
-  const int nit = min(IT, a.n_pre - i0);
+//   acc += L_j ebar                              (fp32 within a chunk, fp64 across)
+//   epsa = (rho - beta_j psi_j) epsa + psi_j zbar_i   (adaptive j only)
+template <bool FIRST>
+__global__ __launch_bounds__(kTraceWaves * 64) void trace_kernel(TraceArgs a) {
+  constexpr int R = kTraceRows;
+  __shared__ f32x4 s_ps[kTraceChunk][64];
+  __shared__ f32x4 s_lv[kTraceChunk][64];
+  __shared__ float s_zb[kTraceChunk][kRowPad];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int seg = blockIdx.y;
+  const int j0 = seg * 256 + lane * 4;
+  const bool active = j0 < a.n_post;
+  const int ib = blockIdx.x * kRowPad;
+  const int i0 = ib + w * R;
   const bool adapt = j0 < a.n_adaptive;
   float bj[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) bj[r] = (j0 + r < a.n_adaptive) ? a.beta : 0.0f;
 
-  double acc[IT][4];
+  double acc[R][4];
 #pragma unroll
-  for (int ii = 0; ii < IT; ++ii)
+  for (int ii = 0; ii < R; ++ii)
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      acc[ii][r] = (FIRST || ii >= nit) ? 0.0 : a.acc[(size_t)(i0 + ii) * a.ldj + j0 + r];
+      acc[ii][r] = (FIRST || !active) ? 0.0 : a.acc[(size_t)(i0 + ii) * a.ldj + j0 + r];
 
-  const size_t bs_e = (size_t)a.n_pre * a.ldj;
-  const size_t bs_a = (size_t)a.n_pre * a.lda;
-  const size_t zrow = (size_t)a.B * a.Kmax;
+  const size_t bs_e = (size_t)a.n_pre_pad * a.ldj;
+  const size_t bs_a = (size_t)a.n_pre_pad * a.lda;
   float* pe0 = a.ebar + (size_t)i0 * a.ldj + j0;
   float* pa0 = a.epsa + (size_t)i0 * a.lda + j0;
   const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 
-  f32x4 E[IT], Aa[IT];
+  f32x4 E[R], Aa[R];
 #pragma unroll
-  for (int ii = 0; ii < IT; ++ii) {
+  for (int ii = 0; ii < R; ++ii) {
     E[ii] = zero;
     Aa[ii] = zero;
-    if (!FIRST && ii < nit) {
+    if (!FIRST && active) {
       E[ii] = load_nt(pe0 + (size_t)ii * a.ldj);
       if (adapt) Aa[ii] = load_nt(pa0 + (size_t)ii * a.lda);
     }
   }
   for (int b = 0; b < a.B; ++b) {
-    f32x4 En[IT], An[IT];
+    f32x4 En[R], An[R];
 #pragma unroll
-    for (int ii = 0; ii < IT; ++ii) {
+    for (int ii = 0; ii < R; ++ii) {
       En[ii] = zero;
       An[ii] = zero;
-      if (!FIRST && b + 1 < a.B && ii < nit) {
+      if (!FIRST && active && b + 1 < a.B) {
         En[ii] = load_nt(pe0 + (size_t)(b + 1) * bs_e + (size_t)ii * a.ldj);
         if (adapt) An[ii] = load_nt(pa0 + (size_t)(b + 1) * bs_a + (size_t)ii * a.lda);
       }
     }
-    const float* zk = a.zbarK + ((size_t)i0 * a.B + b) * a.Kmax;
-    const float* pp = a.psiK + (size_t)b * a.Kmax * a.ldj + j0;
-    const float* lp = a.LK + (size_t)b * a.Kmax * a.ldj + j0;
-    for (int t = 0; t < a.steps; ++t) {
-      const f32x4 ps = *(const f32x4*)(pp + (size_t)t * a.ldj);
-      const f32x4 lv = *(const f32x4*)(lp + (size_t)t * a.ldj);
-      double ld[4];
+    for (int c0 = 0; c0 < a.steps; c0 += kTraceChunk) {
+      const int nt = min(kTraceChunk, a.steps - c0);
+      __syncthreads();   // the previous chunk's shared vectors are consumed
+      for (int k = tid; k < nt * 64; k += kTraceWaves * 64) {
+        const int tt = k >> 6, l = k & 63;
+        const size_t row = (size_t)(c0 + tt) * a.Bp + b;
+        s_ps[tt][l] = *(const f32x4*)(a.psiK + row * a.ldv + seg * 256 + 4 * l);
+        s_lv[tt][l] = *(const f32x4*)(a.LK + row * a.ldv + seg * 256 + 4 * l);
+      }
+      for (int k = tid; k < nt * kRowPad; k += kTraceWaves * 64) {
+        const int tt = k / kRowPad, r = k % kRowPad;
+        s_zb[tt][r] = a.zbarK[((size_t)b * a.Kmax + c0 + tt) * a.ldi + ib + r];
+      }
+      __syncthreads();
+      if (active) {
+        // L * ebar summed over the chunk in fp32, then added to the fp64 accumulator
+        float part[R][4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) ld[r] = (double)lv[r];
-      if (adapt) {
-        float rb[4];
+        for (int ii = 0; ii < R; ++ii)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) rb[r] = a.rho - bj[r] * ps[r];
-#pragma unroll
-        for (int ii = 0; ii < IT; ++ii) {
-          if (ii < nit) {
-            const float zb = zk[(size_t)ii * zrow + t];
+          for (int r = 0; r < 4; ++r) part[ii][r] = 0.0f;
+        for (int tt = 0; tt < nt; ++tt) {
+          const f32x4 ps = s_ps[tt][lane];
+          const f32x4 lv = s_lv[tt][lane];
+          if (adapt) {
+            float pb[4], rb[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-              const float et = ps[r] * (zb - bj[r] * Aa[ii][r]);
-              E[ii][r] = fmaf(a.kappa, E[ii][r], et);
-              Aa[ii][r] = fmaf(rb[r], Aa[ii][r], ps[r] * zb);
-              acc[ii][r] = fma(ld[r], (double)E[ii][r], acc[ii][r]);
+              pb[r] = ps[r] * bj[r];
+              rb[r] = a.rho - pb[r];
+            }
+#pragma unroll
+            for (int ii = 0; ii < R; ++ii) {
+              const float zb = s_zb[tt][w * R + ii];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const float pz = ps[r] * zb;
+                const float e = fmaf(-pb[r], Aa[ii][r], pz);
+                E[ii][r] = fmaf(a.kappa, E[ii][r], e);
+                Aa[ii][r] = fmaf(rb[r], Aa[ii][r], pz);
+                part[ii][r] = fmaf(lv[r], E[ii][r], part[ii][r]);
+              }
+            }
+          } else {
+#pragma unroll
+            for (int ii = 0; ii < R; ++ii) {
+              const float zb = s_zb[tt][w * R + ii];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                E[ii][r] = fmaf(a.kappa, E[ii][r], ps[r] * zb);
+                part[ii][r] = fmaf(lv[r], E[ii][r], part[ii][r]);
+              }
             }
           }
         }
-      } else {
 #pragma unroll
-        for (int ii = 0; ii < IT; ++ii) {
-          if (ii < nit) {
-            const float zb = zk[(size_t)ii * zrow + t];
+        for (int ii = 0; ii < R; ++ii)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              E[ii][r] = fmaf(a.kappa, E[ii][r], ps[r] * zb);
-              acc[ii][r] = fma(ld[r], (double)E[ii][r], acc[ii][r]);
-            }
-          }
-        }
+          for (int r = 0; r < 4; ++r) acc[ii][r] += (double)part[ii][r];
       }
     }
+    if (active) {
 #pragma unroll
-    for (int ii = 0; ii < IT; ++ii) {
-      if (ii < nit) {
+      for (int ii = 0; ii < R; ++ii) {
         store_nt(pe0 + (size_t)b * bs_e + (size_t)ii * a.ldj, E[ii]);
         if (adapt) store_nt(pa0 + (size_t)b * bs_a + (size_t)ii * a.lda, Aa[ii]);
       }
+    }
+#pragma unroll
+    for (int ii = 0; ii < R; ++ii) {
       E[ii] = En[ii];
       Aa[ii] = An[ii];
     }
   }
+  if (active) {
 #pragma unroll
-  for (int ii = 0; ii < IT; ++ii)
-    if (ii < nit)
+    for (int ii = 0; ii < R; ++ii)
 #pragma unroll
       for (int r = 0; r < 4; ++r) a.acc[(size_t)(i0 + ii) * a.ldj + j0 + r] = acc[ii][r];
+  }
 }
 
 // ---------------------------------------------------------------- gradient read-out
@@ -455,13 +588,31 @@ __global__ __launch_bounds__(256) void pack_kernel(const float* src, int rows, i
 
 // ---------------------------------------------------------------- launchers
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s) {
-  forward_kernel<<<a.B, kFwdThreads, a.smem, s>>>(a);
+  const int qn = (a.n_rec + kFwdThreads - 1) / kFwdThreads;
+  if (qn <= 1)
+    forward_kernel<1><<<a.B, kFwdThreads, a.smem, s>>>(a);
+  else if (qn <= 2)
+    forward_kernel<2><<<a.B, kFwdThreads, a.smem, s>>>(a);
+  else if (qn <= 4)
+    forward_kernel<4><<<a.B, kFwdThreads, a.smem, s>>>(a);
+  else if (qn <= 8)
+    forward_kernel<8><<<a.B, kFwdThreads, a.smem, s>>>(a);
+  else if (qn <= 16)
+    forward_kernel<16><<<a.B, kFwdThreads, a.smem, s>>>(a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.N, 128), cdiv(a.M, 32), a.splits);
   gemm_nt_kernel<<<grid, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_tn(const GemmArgs& a, hipStream_t s) {
+  dim3 grid(cdiv(a.N, 128), cdiv(a.M, 32), a.splits);
+  gemm_tn_kernel<<<grid, 256, 0, s>>>(a);
   return hipGetLastError();
 }
 
@@ -473,12 +624,11 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 }
 
 hipError_t launch_trace(const TraceArgs& a, hipStream_t s) {
-  constexpr int IT = 4;
-  dim3 grid(cdiv(a.n_pre, IT), cdiv(a.n_post, 1024));
+  dim3 grid(a.n_pre_pad / kRowPad, cdiv(a.n_post, 256));
   if (a.first)
-    trace_kernel<IT, true><<<grid, 256, 0, s>>>(a);
+    trace_kernel<true><<<grid, kTraceWaves * 64, 0, s>>>(a);
   else
-    trace_kernel<IT, false><<<grid, 256, 0, s>>>(a);
+    trace_kernel<false><<<grid, kTraceWaves * 64, 0, s>>>(a);
   return hipGetLastError();
 }
 

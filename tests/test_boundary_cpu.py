@@ -35,12 +35,14 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
         n = eprop.eprop_workspace_bytes(eprop.make_config(shape))
         traces = sum(4 * shape.batch * shape.n_pre(l) * (shape.n_rec + shape.n_adaptive)
                      for l in range(shape.n_layers))
-        # per-step vectors kept for one block of at most 32 steps
+        # per-step vectors for two blocks of at most 32 steps (one being
+        # written by the forward pass while the other is read)
         bp = -(-shape.batch // 16) * 16
-        per_step = sum(4 * (2 * shape.batch * shape.n_rec + shape.n_pre(l) * shape.batch
+        nv = -(-shape.n_rec // 256) * 256
+        per_step = sum(4 * (2 * bp * nv + shape.n_pre(l) * shape.batch
                             + (shape.n_out + 32 + shape.n_rec + 32) * bp)
                        for l in range(shape.n_layers))
-        assert traces <= n <= traces * 1.05 + 32 * per_step + (16 << 20), (name, n, traces)
+        assert traces <= n <= traces * 1.05 + 2 * 32 * per_step + (16 << 20), (name, n, traces)
     # the same shape with any T needs the same workspace: T is not an input
     s = synth.WORKLOADS["ralif_b64_n512_t500"]
     assert eprop.eprop_workspace_bytes(eprop.make_config(s)) == \
