@@ -9,9 +9,15 @@ synthetic data already resident in HBM when the clock starts.
 
 Prints one JSON line: synapse-timestep updates per second
 (sum over layers of B * N_pre * N_post * T per second), the roofline of the
-eligibility kernel (algorithmic HBM bytes per launch over its measured
-duration, from HIP events on its stream) and the CPU oracle timed on a
-bounded sample on this host.
+eligibility kernel, which dominates the step (algorithmic fp32 operations per
+launch over its measured duration, from HIP events on its stream; its HBM
+bytes alongside), and the CPU oracle timed on a bounded sample on this host.
+
+Counter runs: `--calibrate-copy MIB` adds device-to-device copies of a known
+size after the timed steps, so that FETCH_SIZE/WRITE_SIZE of the eligibility
+kernel can be scaled by what the same counters read for a plain copy;
+`--summarize-counters FETCH_DIR WRITE_DIR` turns the two rocprofv3 CSV
+outputs into profiles/trace_kernel_counters.json.
 """
 import argparse
 import hashlib
@@ -26,6 +32,8 @@ if ROOT not in sys.path:
 
 WORKLOAD = "ralif_b128_n1024_t1000"
 HBM_PEAK_GBS = 8000.0
+FP32_VECTOR_PEAK_TFLOPS = 157.3    # MI355X published fp32 vector peak
+COPY_KERNEL = "copyBuffer"
 COUNTERS = os.path.join(ROOT, "profiles", "trace_kernel_counters.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2501_11407_amd", "csrc", "kernels.hip")
 
@@ -41,6 +49,17 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     npre = shape.n_pre(layer)
     trace = 4 * B * npre * (N + NA) + 8 * npre * N      # one direction
     return (2 * launches - first_launches) * trace + steps * 4 * (B * npre + 2 * B * N)
+
+
+def trace_flops(shape, layer: int, steps: int) -> int:
+    """Algorithmic fp32 operations of the eligibility recursion per covered
+    timestep (a fused multiply-add counts 2): LIF synapse psi*zbar (1),
+    ebar = kappa*ebar + e (2), acc += L*ebar (2): 5; adaptive synapse adds
+    e = psi*zbar - (psi*beta)*epsa (2) and epsa = (rho - beta*psi)*epsa +
+    psi*zbar (2): 9."""
+    B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
+    npre = shape.n_pre(layer)
+    return steps * B * npre * (5 * (N - NA) + 9 * NA)
 
 
 def source_digest() -> str:
@@ -61,24 +80,61 @@ def stored_traffic(shape):
     return c.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, seconds_hint: float = 20.0):
-    """The oracle (one thread, fp64 traces) on batch element 0, every synapse,
-    the first T_s timesteps, T_s chosen to take about seconds_hint."""
+def summarize_counters(fetch_dir: str, write_dir: str, copy_mib: int) -> dict:
+    """Reads the FETCH_SIZE and WRITE_SIZE rocprofv3 CSVs (KiB per dispatch),
+    scales each by copy bytes / the counter's reading for the plain copies,
+    and writes profiles/trace_kernel_counters.json."""
+    import csv
+    import glob
+
+    def per_kernel(d, counter):
+        rows = []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            rows += list(csv.DictReader(open(f)))
+        trace = [float(r["Counter_Value"]) for r in rows
+                 if r["Counter_Name"] == counter and "trace_kernel<false>" in r["Kernel_Name"]]
+        copies = [r for r in rows if r["Counter_Name"] == counter and COPY_KERNEL in r["Kernel_Name"]]
+        big = max(int(r["Grid_Size"]) for r in copies)      # the calibration copies, not small ones
+        copy = [float(r["Counter_Value"]) for r in copies if int(r["Grid_Size"]) == big]
+        return trace, copy
+
+    fetch_t, fetch_c = per_kernel(fetch_dir, "FETCH_SIZE")
+    write_t, write_c = per_kernel(write_dir, "WRITE_SIZE")
+    copy_kib = copy_mib * 1024.0
+    f_scale = copy_kib / (sum(fetch_c) / len(fetch_c))
+    w_scale = copy_kib / (sum(write_c) / len(write_c))
+    fetch = sum(fetch_t) / len(fetch_t) * 1024.0 * f_scale
+    write = sum(write_t) / len(write_t) * 1024.0 * w_scale
+    out = {"workload": WORKLOAD, "kernel": "trace_kernel<false>",
+           "kernel_source_sha256": source_digest(),
+           "dispatches": len(fetch_t), "fetch_bytes_per_launch": round(fetch),
+           "write_bytes_per_launch": round(write), "hbm_bytes_per_launch": round(fetch + write),
+           "copy_calibration": {"copy_bytes": copy_mib << 20, "fetch_scale": f_scale,
+                                "write_scale": w_scale}}
+    with open(COUNTERS, "w") as f:
+        json.dump(out, f, indent=1)
+    return out
+
+
+def cpu_baseline(wl, seconds_hint: float = 15.0):
+    """The oracle (one thread, fp64 traces) over every synapse and all T
+    steps of the first n_b batch elements, n_b chosen so that the run takes
+    about seconds_hint on this host."""
     import oracle
     shape = wl.shape
-    per_step = shape.n_pre(0) * shape.n_rec
-    # probe a few steps to size the sample
-    T_probe = 20
+    per_step = shape.n_pre(0) * shape.n_rec * shape.n_layers
     t0 = time.perf_counter()
-    oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, T=T_probe, b_lo=0, b_hi=1, want_spikes=False)
-    dt = time.perf_counter() - t0
-    T_s = int(min(shape.T, max(T_probe, T_probe * seconds_hint / max(dt, 1e-6))))
+    oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, b_lo=0, b_hi=1, want_spikes=False)
+    probe = time.perf_counter() - t0
+    n_b = int(min(shape.batch, max(1, round(seconds_hint / max(probe, 1e-6)))))
     t0 = time.perf_counter()
-    oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, T=T_s, b_lo=0, b_hi=1, want_spikes=False)
+    oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, b_lo=0, b_hi=n_b, want_spikes=False)
     dt = time.perf_counter() - t0
-    return {"value": per_step * T_s / dt, "unit": "syn-steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"batch element 0 of {WORKLOAD}, all {per_step} synapses, first {T_s} of "
-                      f"{shape.T} timesteps, {dt:.1f} s, single-threaded fp64 oracle"}
+    return {"value": n_b * per_step * shape.T / dt, "unit": "syn-steps/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"batch elements 0..{n_b - 1} of {WORKLOAD} (of {shape.batch}), all "
+                      f"{per_step} synapses, all {shape.T} timesteps: {dt:.1f} s on one thread "
+                      f"(fp64 traces)"}
 
 
 def main():
@@ -87,7 +143,13 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--copy-mib", type=int, default=1024)
     args = ap.parse_args()
+    if args.summarize_counters:
+        print(json.dumps(summarize_counters(*args.summarize_counters, args.copy_mib)))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               "(the batch-sharded multi-GPU design is not built)", file=sys.stderr)
@@ -131,13 +193,18 @@ def main():
     per_layer_launches = n_timed // shape.n_layers
     alg_bytes = sum(trace_bytes(shape, l, per_layer_launches, args.steps, args.steps * shape.T)
                     for l in range(shape.n_layers))
-    achieved = alg_bytes / (trace_ms * 1e-3) / 1e9
-    traffic = stored_traffic(shape)
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+    alg_flops = sum(trace_flops(shape, l, args.steps * shape.T) for l in range(shape.n_layers))
+    sec = trace_ms * 1e-3
+    achieved = alg_flops / sec / 1e12
+    roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": FP32_VECTOR_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / FP32_VECTOR_PEAK_TFLOPS, 4),
+                "traffic": stored_traffic(shape),
                 "kernel": "trace_kernel", "avg_launch_us": round(trace_ms * 1e3 / n_timed, 2),
                 "steps_per_launch": round(timed_steps / n_timed, 2),
-                "alg_bytes_per_launch": round(alg_bytes / n_timed)}
+                "alg_flops_per_launch": round(alg_flops / n_timed),
+                "alg_hbm_bytes_per_launch": round(alg_bytes / n_timed),
+                "hbm_achieved_gbs": round(alg_bytes / sec / 1e9, 1),
+                "hbm_frac": round(alg_bytes / sec / 1e9 / HBM_PEAK_GBS, 4)}
     line = {
         "metric": "synapse-timestep e-prop updates/sec (B*N_pre*N_post*T/s) + % HBM peak",
         "value": value, "unit": "syn-steps/s", "n_gpus": 1, "steps": args.steps,
@@ -149,6 +216,14 @@ def main():
                    "T": shape.T, "layers": shape.n_layers, "parallelism": "single GPU"},
         "roofline": roofline,
     }
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl)
     ctx.close()

@@ -42,7 +42,8 @@ struct Layer {
   int n_inl = 0, n_pre = 0;
   int n_pre_pad = 0;   // n_pre rounded to the eligibility kernel's row group
   int ldj = 0;    // n_rec rounded to 4: row stride of traces and accumulators
-  int ldv = 0;    // n_rec rounded to 256: row stride of Wt, psiK, LK
+  int ldv = 0;    // n_rec rounded to 256: row stride of psiK, LK
+  int ldw = 0;    // n_rec rounded to the forward workgroup size: row stride of Wt
   int lda = 0;    // n_adaptive rounded to 4: row stride of epsa
   int rows_per_wave = 0;
   const float* W_src = nullptr;
@@ -123,12 +124,13 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.n_pre_pad = (int)round_up(L.n_pre, eprop::kRowPad);
     L.ldj = (int)round_up(N, 4);
     L.ldv = (int)round_up(N, 256);
+    L.ldw = (int)round_up(N, eprop::kFwdThreads);
     L.lda = (int)round_up(std::max(c.n_adaptive, 1), 4);
-    L.rows_per_wave = (int)round_up((L.n_pre + 3) / 4, 64);
+    L.rows_per_wave = (int)round_up((L.n_pre + eprop::kFwdWaves - 1) / eprop::kFwdWaves, 64);
     rwmax = std::max(rwmax, L.rows_per_wave);
     npre_total += L.n_pre;
     const size_t np = L.n_pre, npp = L.n_pre_pad;
-    L.Wt = (float*)take(sizeof(float) * np * L.ldv);
+    L.Wt = (float*)take(sizeof(float) * np * L.ldw);
     L.WoutT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.v = (float*)take(sizeof(float) * B * N);
     L.a = (float*)take(sizeof(float) * B * N);
@@ -151,15 +153,16 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * L.lda : 0);
   }
   const size_t npad4 = round_up(N, 4);
-  plan->smem = sizeof(int) * (4 * (size_t)rwmax + 4 * (size_t)plan->jlist + 8) +
+  plan->smem = sizeof(int) * (eprop::kFwdWaves * ((size_t)rwmax + (size_t)plan->jlist) +
+                              2 * eprop::kFwdWaves) +
                sizeof(float) * (2 + (size_t)c.n_layers * K + npre_total) +
-               (size_t)c.n_layers * 2 * npad4;
+               (size_t)c.n_layers * 2 * npad4 + (size_t)eprop::kFwdXSteps * c.n_in;
   plan->bytes = round_up(off, 256);
 }
 
 bool plan_fits(const Plan& p, std::string* why) {
-  if (p.smem > 64 * 1024) {
-    *why = "shape needs more than 64 KiB of shared memory in the forward kernel";
+  if (p.smem > 160 * 1024) {
+    *why = "shape needs more than 160 KiB of shared memory in the forward kernel";
     return false;
   }
   return true;
@@ -203,8 +206,9 @@ int check(eprop_ctx* ctx, hipError_t e, const char* what) {
 int pack_weights(eprop_ctx* ctx) {
   const eprop_config& c = ctx->plan.cfg;
   for (Layer& L : ctx->plan.layers) {
-    // drive weights transposed, Wt[i][j] = W[j][i], columns padded to 256
-    int rc = check(ctx, eprop::launch_pack(L.W_src, c.n_rec, L.n_pre, L.Wt, L.ldv, L.n_pre, 1,
+    // drive weights transposed, Wt[i][j] = W[j][i], columns padded to the
+    // forward workgroup size
+    int rc = check(ctx, eprop::launch_pack(L.W_src, c.n_rec, L.n_pre, L.Wt, L.ldw, L.n_pre, 1,
                                            ctx->stream), "weight packing");
     if (rc) return rc;
     // WoutT[j][k] = Wout[k][j]: the B operand of the learning-signal GEMM
@@ -259,7 +263,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   for (int l = 0; l < 2; ++l) {
     eprop::FwdLayer& f = fa.L[l];
     const Layer& L = P.layers[std::min(l, c.n_layers - 1)];
-    f.Wt = L.Wt; f.ldw = L.ldv; f.WoutT = L.WoutT;
+    f.Wt = L.Wt; f.ldw = L.ldw; f.WoutT = L.WoutT;
     f.v = L.v; f.a = L.a; f.ztil = L.ztil; f.z = L.z; f.zbar = L.zbar; f.y = L.y;
     f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.zbarK = L.zbarK[sl];
     f.deltaK = L.deltaK[sl]; f.ztK = L.ztK[sl];
@@ -303,6 +307,8 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ta.psiK = L.psiK[sl]; ta.LK = L.LK[sl]; ta.B = c.batch; ta.Bp = P.Bp; ta.n_pre_pad = L.n_pre_pad;
     ta.n_post = c.n_rec; ta.ldj = L.ldj; ta.ldv = L.ldv; ta.n_adaptive = c.n_adaptive;
     ta.lda = L.lda; ta.Kmax = P.Kmax; ta.ldi = L.n_pre_pad; ta.steps = steps;
+    ta.n_seg_a = (c.n_adaptive + 255) / 256;
+    ta.n_seg_l = (c.n_rec + 255) / 256 - ta.n_seg_a;
     ta.kappa = c.kappa; ta.rho = c.rho; ta.beta = c.beta; ta.first = first;
     const bool timed = ctx->prof && ctx->prof_n < ctx->prof_max;
     if (timed && (rc = check(ctx, hipEventRecord(ctx->ev[2 * ctx->prof_n], s), "event record")))

@@ -20,11 +20,12 @@
 
 namespace eprop {
 
-constexpr int kFwdThreads = 256;
-constexpr int kTraceRows = 2;          // presynaptic rows per eligibility thread
+constexpr int kFwdThreads = 1024;              // forward workgroup: one batch element
+constexpr int kFwdWaves = kFwdThreads / 64;
+constexpr int kFwdXSteps = 8;                  // input spikes staged in shared memory per load
 constexpr int kTraceWaves = 4;         // waves per eligibility workgroup (same 256 neurons)
-constexpr int kTraceChunk = 16;        // steps staged in shared memory at a time
-constexpr int kRowPad = kTraceRows * kTraceWaves;   // n_pre padded to a multiple of this
+constexpr int kTraceChunk = 8;         // steps staged in shared memory at a time
+constexpr int kRowPad = 16;            // n_pre padded to a multiple of this (row group)
 
 struct FwdLayer {
   const float* Wt; int ldw;      // transposed drive weights [n_pre][ldw]
@@ -83,6 +84,7 @@ struct TraceArgs {
   const float* zbarK;                 // [B][Kmax][ldi]
   const float* psiK; const float* LK; // [rows][ldv], row t*Bp + b, ldv a multiple of 256
   int B, Bp, n_pre_pad, n_post, ldj, ldv, n_adaptive, lda, Kmax, ldi, steps;
+  int n_seg_a, n_seg_l;   // 256-neuron segments holding adaptive neurons, and the rest
   float kappa, rho, beta;
   int first;       // 1: traces and accumulators start at zero (not read)
 };

@@ -57,7 +57,7 @@ inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 //   4. ztilde = kappa*ztilde + z.
 // The learning signal L = W_out^T delta is one GEMM over the whole block.
 struct FwdLds {
-  int* act; int* spk; int* cnt; float* red; float* sy; float* szb; uint8_t* zc;
+  int* act; int* spk; int* cnt; float* red; float* sy; float* szb; uint8_t* zc; uint8_t* xs;
   int rwmax, npad;
 };
 
@@ -71,7 +71,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   uint8_t* znow = S.zc + (LI * 2 + (cur ^ 1)) * S.npad;
   const uint8_t* inp;
   if constexpr (LI == 0)
-    inp = A.x + ((size_t)t * A.B + b) * A.n_in;
+    inp = S.xs + (t % kFwdXSteps) * A.n_in;      // staged input spikes of this step
   else
     inp = S.zc + ((LI - 1) * 2 + (cur ^ 1)) * S.npad;
   float* szb = S.szb + (LI == 0 ? 0 : A.L[0].n_pre);
@@ -100,12 +100,13 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   if (lane == 0) S.cnt[w] = n_act;
   __syncthreads();
 
-  // 2. drive and neuron step.  Rows of Wt are padded to a multiple of 256
-  // columns; chunks q with q*256 >= n_rec are skipped (QN is rounded up).
+  // 2. drive and neuron step.  Rows of Wt are padded to a multiple of the
+  // workgroup size; chunks q with q*kFwdThreads >= n_rec are skipped (QN is
+  // rounded up to a power of two).
   float I[QN];
 #pragma unroll
   for (int q = 0; q < QN; ++q) I[q] = 0.0f;
-  for (int ww = 0; ww < 4; ++ww) {
+  for (int ww = 0; ww < kFwdWaves; ++ww) {
     const int c = S.cnt[ww];
     const int* lst = S.act + ww * S.rwmax;
 #pragma unroll 4
@@ -149,15 +150,15 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       if (lane == 1 && w0 + 1 < A.W32) srow[w0 + 1] = (uint32_t)(m >> 32);
     }
   }
-  if (lane == 0) S.cnt[4 + w] = n_spk;
+  if (lane == 0) S.cnt[kFwdWaves + w] = n_spk;
   __syncthreads();
 
   // 3. readout (rows of the transposed readout weights of the spiking
   // neurons, read coalesced over k), softmax cross-entropy
   for (int k = tid; k < A.K_out; k += kFwdThreads) {
     float Y = 0.0f;
-    for (int ww = 0; ww < 4; ++ww) {
-      const int c = S.cnt[4 + ww];
+    for (int ww = 0; ww < kFwdWaves; ++ww) {
+      const int c = S.cnt[kFwdWaves + ww];
       const int* lst = S.spk + ww * A.jlist;
 #pragma unroll 8
       for (int s = 0; s < c; ++s) Y += Ly.WoutT[(size_t)lst[s] * A.ldk + k];
@@ -247,14 +248,15 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs A) {
   S.rwmax = A.L[0].rows_per_wave;
   if (A.n_layers > 1) S.rwmax = max(S.rwmax, A.L[1].rows_per_wave);
   S.npad = (A.n_rec + 3) & ~3;
-  S.act = (int*)smem;                          // [4][rwmax]
-  S.spk = S.act + 4 * S.rwmax;                 // [4][jlist]
-  S.cnt = S.spk + 4 * A.jlist;                 // [8]
-  S.red = (float*)(S.cnt + 8);                 // [2]
+  S.act = (int*)smem;                          // [waves][rwmax]
+  S.spk = S.act + kFwdWaves * S.rwmax;         // [waves][jlist]
+  S.cnt = S.spk + kFwdWaves * A.jlist;         // [2 * waves]
+  S.red = (float*)(S.cnt + 2 * kFwdWaves);     // [2]
   S.sy = S.red + 2;                            // [n_layers][K_out]
   S.szb = S.sy + A.n_layers * A.K_out;         // [n_pre_0 + n_pre_1]
   const int npre_total = A.L[0].n_pre + (A.n_layers > 1 ? A.L[1].n_pre : 0);
   S.zc = (uint8_t*)(S.szb + npre_total);       // [n_layers][2][npad]
+  S.xs = S.zc + A.n_layers * 2 * S.npad;       // [kFwdXSteps][n_in]
 
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
   forward_state<QN, 0>(A, S, b, true, v0, a0, zt0, 0);
@@ -263,6 +265,18 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs A) {
   int cur = 0;
   __syncthreads();
   for (int t = 0; t < A.steps; ++t) {
+    if (t % kFwdXSteps == 0) {
+      // stage the input spikes of the next kFwdXSteps steps (one round trip)
+      const int ns = min(kFwdXSteps, A.steps - t);
+#pragma unroll
+      for (int tt = 0; tt < kFwdXSteps; ++tt) {
+        if (tt < ns) {
+          const uint8_t* xrow = A.x + ((size_t)(t + tt) * A.B + b) * A.n_in;
+          for (int i = threadIdx.x; i < A.n_in; i += kFwdThreads) S.xs[tt * A.n_in + i] = xrow[i];
+        }
+      }
+      __syncthreads();
+    }
     forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0);
     if (A.n_layers > 1) forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1);
     cur ^= 1;
@@ -388,34 +402,89 @@ __global__ __launch_bounds__(256) void accumulate_kernel(const float* part, int 
 }
 
 // ---------------------------------------------------------------- eligibility
-// A workgroup owns one 256-wide segment of postsynaptic neurons and
-// kTraceWaves*kTraceRows presynaptic rows; lane l of every wave owns the four
-// neurons j0 = seg*256 + 4l..4l+3, wave w the rows i0 = ib + w*kTraceRows...
+// A workgroup owns one 256-wide segment of postsynaptic neurons and a group
+// of presynaptic rows; lane l of every wave owns the four neurons
+// j0 = seg*256 + 4l..4l+3 and wave w rows ib + w*R .. ib + w*R + R-1.
+// Segments holding adaptive neurons move two trace arrays per synapse and use
+// R = 2 rows per thread, LIF segments one array and R = 4, so every wave does
+// about the same arithmetic; groups of 16 rows list their adaptive and LIF
+// workgroups next to each other in dispatch order.
 // The workgroup walks the batch; for each batch element the traces are read
-// once (prefetched while the previous element computes), advanced through
-// the block's steps and written once.  psi and L of the segment and zbar of
-// the rows are staged in shared memory kTraceChunk steps at a time and shared
-// by all waves.  Per step, for each (i, j):
+// once, advanced through the block's steps and written once.  psi and L of
+// the segment and zbar of the rows are shared through shared memory,
+// kTraceChunk steps at a time, in a pipeline over chunks (batch element,
+// step range): the next chunk's vectors are loaded into registers and the
+// next batch element's traces prefetched while the current chunk computes.
+// Per step, for each (i, j):
 //   e    = psi_j zbar_i - psi_j beta_j epsa      (dz_j/dW_ji)
 //   ebar = kappa ebar + e                        (readout filter on the trace)
 //   acc += L_j ebar                              (fp32 within a chunk, fp64 across)
-//   epsa = (rho - beta_j psi_j) epsa + psi_j zbar_i   (adaptive j only)
-template <bool FIRST>
-__global__ __launch_bounds__(kTraceWaves * 64) void trace_kernel(TraceArgs a) {
-  constexpr int R = kTraceRows;
-  __shared__ f32x4 s_ps[kTraceChunk][64];
-  __shared__ f32x4 s_lv[kTraceChunk][64];
-  __shared__ float s_zb[kTraceChunk][kRowPad];
+//   epsa = (rho - beta_j psi_j) epsa + psi_j zbar_i   (adaptive j)
+// On LIF lanes of an adaptive segment beta_j = 0, so e = psi_j zbar_i exactly.
+constexpr int kStage = kTraceChunk * 64 / (kTraceWaves * 64);   // float4 per thread per vector
+static_assert(kStage * kTraceWaves * 64 == kTraceChunk * 64, "chunk must split evenly");
+static_assert(kTraceChunk * kRowPad <= kTraceWaves * 64, "zbar chunk must fit one load per thread");
+
+struct TraceShared {
+  f32x4 ps[kTraceChunk][64];
+  f32x4 lv[kTraceChunk][64];
+  float zb[kTraceChunk][kRowPad];
+};
+
+struct TraceStage {
+  f32x4 ps[kStage], lv[kStage];
+  float zb;
+};
+
+// Every lane issues the same loads whatever the chunk (indices are clamped
+// to valid rows), so the number of loads in flight is the same on every path
+// and waits on them never have to drain the whole queue.
+template <int ROWS>
+__device__ __forceinline__ void trace_stage_load(const TraceArgs& a, TraceStage& g, int b, int c0,
+                                                 int nt, int seg, int ib) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int u = 0; u < kStage; ++u) {
+    const int k = tid + u * kTraceWaves * 64;
+    const int tt = min(k >> 6, nt - 1), l = k & 63;
+    const size_t row = (size_t)(c0 + tt) * a.Bp + b;
+    g.ps[u] = *(const f32x4*)(a.psiK + row * a.ldv + seg * 256 + 4 * l);
+    g.lv[u] = *(const f32x4*)(a.LK + row * a.ldv + seg * 256 + 4 * l);
+  }
+  const int kz = tid % (kTraceChunk * ROWS);
+  const int tt = min(kz / ROWS, nt - 1), r = kz % ROWS;
+  g.zb = a.zbarK[((size_t)b * a.Kmax + c0 + tt) * a.ldi + ib + r];
+}
+
+template <int ROWS>
+__device__ __forceinline__ void trace_stage_store(const TraceStage& g, int nt, TraceShared& S) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int u = 0; u < kStage; ++u) {
+    const int k = tid + u * kTraceWaves * 64;
+    const int tt = k >> 6, l = k & 63;
+    if (tt < nt) {
+      S.ps[tt][l] = g.ps[u];
+      S.lv[tt][l] = g.lv[u];
+    }
+  }
+  if (tid < kTraceChunk * ROWS) {
+    const int tt = tid / ROWS, r = tid % ROWS;
+    if (tt < nt) S.zb[tt][r] = g.zb;
+  }
+}
+
+template <int R, bool ALIF, bool FIRST>
+__device__ __forceinline__ void trace_body(const TraceArgs& a, TraceShared& S, int seg, int ib) {
+  constexpr int ROWS = R * kTraceWaves;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int seg = blockIdx.y;
   const int j0 = seg * 256 + lane * 4;
   const bool active = j0 < a.n_post;
-  const int ib = blockIdx.x * kRowPad;
+  const bool has_a = ALIF && j0 < a.n_adaptive;   // lane holds eps^a
   const int i0 = ib + w * R;
-  const bool adapt = j0 < a.n_adaptive;
   float bj[4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) bj[r] = (j0 + r < a.n_adaptive) ? a.beta : 0.0f;
+  for (int r = 0; r < 4; ++r) bj[r] = (ALIF && j0 + r < a.n_adaptive) ? a.beta : 0.0f;
 
   double acc[R][4];
 #pragma unroll
@@ -429,101 +498,110 @@ __global__ __launch_bounds__(kTraceWaves * 64) void trace_kernel(TraceArgs a) {
   float* pe0 = a.ebar + (size_t)i0 * a.ldj + j0;
   float* pa0 = a.epsa + (size_t)i0 * a.lda + j0;
   const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  const int nch = (a.steps + kTraceChunk - 1) / kTraceChunk;
+  const int total = a.B * nch;
 
-  f32x4 E[R], Aa[R];
+  f32x4 E[R], Aa[ALIF ? R : 1], En[R], An[ALIF ? R : 1];
 #pragma unroll
   for (int ii = 0; ii < R; ++ii) {
     E[ii] = zero;
-    Aa[ii] = zero;
-    if (!FIRST && active) {
-      E[ii] = load_nt(pe0 + (size_t)ii * a.ldj);
-      if (adapt) Aa[ii] = load_nt(pa0 + (size_t)ii * a.lda);
-    }
+    En[ii] = zero;
+    if (!FIRST && active) E[ii] = load_nt(pe0 + (size_t)ii * a.ldj);
   }
-  for (int b = 0; b < a.B; ++b) {
-    f32x4 En[R], An[R];
+  if constexpr (ALIF) {
 #pragma unroll
     for (int ii = 0; ii < R; ++ii) {
-      En[ii] = zero;
+      Aa[ii] = zero;
       An[ii] = zero;
-      if (!FIRST && active && b + 1 < a.B) {
-        En[ii] = load_nt(pe0 + (size_t)(b + 1) * bs_e + (size_t)ii * a.ldj);
-        if (adapt) An[ii] = load_nt(pa0 + (size_t)(b + 1) * bs_a + (size_t)ii * a.lda);
-      }
+      if (!FIRST && has_a) Aa[ii] = load_nt(pa0 + (size_t)ii * a.lda);
     }
-    for (int c0 = 0; c0 < a.steps; c0 += kTraceChunk) {
-      const int nt = min(kTraceChunk, a.steps - c0);
-      __syncthreads();   // the previous chunk's shared vectors are consumed
-      for (int k = tid; k < nt * 64; k += kTraceWaves * 64) {
-        const int tt = k >> 6, l = k & 63;
-        const size_t row = (size_t)(c0 + tt) * a.Bp + b;
-        s_ps[tt][l] = *(const f32x4*)(a.psiK + row * a.ldv + seg * 256 + 4 * l);
-        s_lv[tt][l] = *(const f32x4*)(a.LK + row * a.ldv + seg * 256 + 4 * l);
-      }
-      for (int k = tid; k < nt * kRowPad; k += kTraceWaves * 64) {
-        const int tt = k / kRowPad, r = k % kRowPad;
-        s_zb[tt][r] = a.zbarK[((size_t)b * a.Kmax + c0 + tt) * a.ldi + ib + r];
-      }
-      __syncthreads();
-      if (active) {
-        // L * ebar summed over the chunk in fp32, then added to the fp64 accumulator
-        float part[R][4];
+  }
+  TraceStage g;
+  trace_stage_load<ROWS>(a, g, 0, 0, min(kTraceChunk, a.steps), seg, ib);
+  trace_stage_store<ROWS>(g, min(kTraceChunk, a.steps), S);
+  __syncthreads();
+
+  for (int q = 0; q < total; ++q) {
+    const int b = q / nch, c = q - b * nch;
+    const int nt = min(kTraceChunk, a.steps - c * kTraceChunk);
+    // Order of issue: next batch element's traces (during its last chunk),
+    // then the next chunk's shared vectors.
+    if (!FIRST && c == nch - 1 && b + 1 < a.B) {
+#pragma unroll
+      for (int ii = 0; ii < R; ++ii)
+        if (active) En[ii] = load_nt(pe0 + (size_t)(b + 1) * bs_e + (size_t)ii * a.ldj);
+      if constexpr (ALIF) {
 #pragma unroll
         for (int ii = 0; ii < R; ++ii)
+          if (has_a) An[ii] = load_nt(pa0 + (size_t)(b + 1) * bs_a + (size_t)ii * a.lda);
+      }
+    }
+    const int qn = min(q + 1, total - 1);
+    const int nb = qn / nch, nc = qn - nb * nch;
+    const int nnt = min(kTraceChunk, a.steps - nc * kTraceChunk);
+    trace_stage_load<ROWS>(a, g, nb, nc * kTraceChunk, nnt, seg, ib);
+
+    // L * ebar summed over the chunk in fp32, then added to the fp64 accumulator
+    float part[R][4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) part[ii][r] = 0.0f;
-        for (int tt = 0; tt < nt; ++tt) {
-          const f32x4 ps = s_ps[tt][lane];
-          const f32x4 lv = s_lv[tt][lane];
-          if (adapt) {
-            float pb[4], rb[4];
+    for (int ii = 0; ii < R; ++ii)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              pb[r] = ps[r] * bj[r];
-              rb[r] = a.rho - pb[r];
-            }
+      for (int r = 0; r < 4; ++r) part[ii][r] = 0.0f;
+    for (int tt = 0; tt < nt; ++tt) {
+      const f32x4 ps = S.ps[tt][lane];
+      const f32x4 lv = S.lv[tt][lane];
+      float zb[R];
 #pragma unroll
-            for (int ii = 0; ii < R; ++ii) {
-              const float zb = s_zb[tt][w * R + ii];
+      for (int ii = 0; ii < R; ++ii) zb[ii] = S.zb[tt][w * R + ii];
+      if constexpr (ALIF) {
+        float pb[4], rb[4];
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const float pz = ps[r] * zb;
-                const float e = fmaf(-pb[r], Aa[ii][r], pz);
-                E[ii][r] = fmaf(a.kappa, E[ii][r], e);
-                Aa[ii][r] = fmaf(rb[r], Aa[ii][r], pz);
-                part[ii][r] = fmaf(lv[r], E[ii][r], part[ii][r]);
-              }
-            }
-          } else {
-#pragma unroll
-            for (int ii = 0; ii < R; ++ii) {
-              const float zb = s_zb[tt][w * R + ii];
-#pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                E[ii][r] = fmaf(a.kappa, E[ii][r], ps[r] * zb);
-                part[ii][r] = fmaf(lv[r], E[ii][r], part[ii][r]);
-              }
-            }
-          }
+        for (int r = 0; r < 4; ++r) {
+          pb[r] = ps[r] * bj[r];
+          rb[r] = a.rho - pb[r];
         }
 #pragma unroll
         for (int ii = 0; ii < R; ++ii)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[ii][r] += (double)part[ii][r];
+          for (int r = 0; r < 4; ++r) {
+            const float pz = ps[r] * zb[ii];
+            const float e = fmaf(-pb[r], Aa[ii][r], pz);
+            E[ii][r] = fmaf(a.kappa, E[ii][r], e);
+            Aa[ii][r] = fmaf(rb[r], Aa[ii][r], pz);
+            part[ii][r] = fmaf(lv[r], E[ii][r], part[ii][r]);
+          }
+      } else {
+#pragma unroll
+        for (int ii = 0; ii < R; ++ii)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            E[ii][r] = fmaf(a.kappa, E[ii][r], ps[r] * zb[ii]);
+            part[ii][r] = fmaf(lv[r], E[ii][r], part[ii][r]);
+          }
       }
     }
-    if (active) {
+#pragma unroll
+    for (int ii = 0; ii < R; ++ii)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[ii][r] += (double)part[ii][r];
+
+    if (c == nch - 1) {
 #pragma unroll
       for (int ii = 0; ii < R; ++ii) {
-        store_nt(pe0 + (size_t)b * bs_e + (size_t)ii * a.ldj, E[ii]);
-        if (adapt) store_nt(pa0 + (size_t)b * bs_a + (size_t)ii * a.lda, Aa[ii]);
+        if (active) store_nt(pe0 + (size_t)b * bs_e + (size_t)ii * a.ldj, E[ii]);
+        E[ii] = En[ii];
+      }
+      if constexpr (ALIF) {
+#pragma unroll
+        for (int ii = 0; ii < R; ++ii) {
+          if (has_a) store_nt(pa0 + (size_t)b * bs_a + (size_t)ii * a.lda, Aa[ii]);
+          Aa[ii] = An[ii];
+        }
       }
     }
-#pragma unroll
-    for (int ii = 0; ii < R; ++ii) {
-      E[ii] = En[ii];
-      Aa[ii] = An[ii];
-    }
+    __syncthreads();   // every wave is done with this chunk's shared vectors
+    if (q + 1 < total) trace_stage_store<ROWS>(g, nnt, S);
+    __syncthreads();
   }
   if (active) {
 #pragma unroll
@@ -531,6 +609,22 @@ __global__ __launch_bounds__(kTraceWaves * 64) void trace_kernel(TraceArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) a.acc[(size_t)(i0 + ii) * a.ldj + j0 + r] = acc[ii][r];
   }
+}
+
+// Block index -> (row group of kRowPad rows, kind, segment): per group, two
+// adaptive workgroups of kRowPad/2 rows per adaptive segment, then one LIF
+// workgroup of kRowPad rows per LIF segment.
+template <bool FIRST>
+__global__ __launch_bounds__(kTraceWaves * 64) void trace_kernel(TraceArgs a) {
+  __shared__ TraceShared S;
+  const int per_group = 2 * a.n_seg_a + a.n_seg_l;
+  const int grp = blockIdx.x / per_group, k = blockIdx.x - grp * per_group;
+  if (k < 2 * a.n_seg_a)
+    trace_body<kRowPad / (2 * kTraceWaves), true, FIRST>(a, S, k >> 1,
+                                                         grp * kRowPad + (k & 1) * (kRowPad / 2));
+  else
+    trace_body<kRowPad / kTraceWaves, false, FIRST>(a, S, a.n_seg_a + (k - 2 * a.n_seg_a),
+                                                    grp * kRowPad);
 }
 
 // ---------------------------------------------------------------- gradient read-out
@@ -587,21 +681,29 @@ __global__ __launch_bounds__(256) void pack_kernel(const float* src, int rows, i
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
+template <int QN>
+hipError_t launch_forward_qn(const FwdArgs& a, hipStream_t s) {
+  // gfx950 gives a workgroup up to the whole 160 KiB of shared memory, but
+  // more than 64 KiB must be requested per kernel.
+  static size_t granted = 64 * 1024;
+  if (a.smem > granted) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&forward_kernel<QN>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.smem);
+    if (e != hipSuccess) return e;
+    granted = a.smem;
+  }
+  forward_kernel<QN><<<a.B, kFwdThreads, a.smem, s>>>(a);
+  return hipGetLastError();
+}
+
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s) {
   const int qn = (a.n_rec + kFwdThreads - 1) / kFwdThreads;
-  if (qn <= 1)
-    forward_kernel<1><<<a.B, kFwdThreads, a.smem, s>>>(a);
-  else if (qn <= 2)
-    forward_kernel<2><<<a.B, kFwdThreads, a.smem, s>>>(a);
-  else if (qn <= 4)
-    forward_kernel<4><<<a.B, kFwdThreads, a.smem, s>>>(a);
-  else if (qn <= 8)
-    forward_kernel<8><<<a.B, kFwdThreads, a.smem, s>>>(a);
-  else if (qn <= 16)
-    forward_kernel<16><<<a.B, kFwdThreads, a.smem, s>>>(a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (qn <= 1) return launch_forward_qn<1>(a, s);
+  if (qn <= 2) return launch_forward_qn<2>(a, s);
+  if (qn <= 4) return launch_forward_qn<4>(a, s);
+  if (qn <= 8) return launch_forward_qn<8>(a, s);
+  if (qn <= 16) return launch_forward_qn<16>(a, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s) {
@@ -624,7 +726,8 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 }
 
 hipError_t launch_trace(const TraceArgs& a, hipStream_t s) {
-  dim3 grid(a.n_pre_pad / kRowPad, cdiv(a.n_post, 256));
+  const int groups = a.n_pre_pad / kRowPad;
+  const int grid = groups * (2 * a.n_seg_a + a.n_seg_l);
   if (a.first)
     trace_kernel<true><<<grid, kTraceWaves * 64, 0, s>>>(a);
   else
