@@ -319,3 +319,18 @@ def test_peak_memory_independent_of_sequence_length():
     # ~28 MB of trace state either way; a per-step record would add T-fold.
     assert grow[10] > 20_000
     assert abs(grow[200] - grow[10]) < 2_000, grow
+
+
+def test_oracle_matches_its_stored_regression_fixture():
+    # tests/golden/tiny_alif2.json was written by tests/golden/make_golden.py,
+    # which calls only the oracle.
+    import json
+    from tests.golden import make_golden
+    ref = json.load(open(make_golden.OUT))
+    _, r = make_golden.compute()
+    assert r.spikes.reshape(-1).tolist() == ref["spike_words"]
+    assert any(ref["spike_words"])
+    for l in range(2):
+        np.testing.assert_allclose(r.dW[l], np.array(ref["dW"][l]), rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(r.dWout[l], np.array(ref["dWout"][l]), rtol=1e-12, atol=1e-15)
+    assert abs(r.loss - ref["loss"]) <= 1e-12 * abs(ref["loss"])
