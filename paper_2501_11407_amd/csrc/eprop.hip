@@ -33,10 +33,11 @@ void choose_splits(int M, int N, int K, int max_splits, int* splits, int* k_chun
   *splits = (K + kc - 1) / kc;
 }
 
-// Timesteps per forward/eligibility block: the eligibility traces are read
-// and written once per block.  The workspace holds per-step vectors for this
-// many steps, independent of the sequence length.
-constexpr int kBlockSteps = 32;
+// Timesteps per forward/eligibility block (eprop::kBlockSteps): the
+// eligibility traces are read and written once per block, and the block's
+// contractions over its steps run on the matrix cores.  The workspace holds
+// per-step vectors for this many steps, independent of the sequence length.
+using eprop::kBlockSteps;
 
 struct Layer {
   int n_inl = 0, n_pre = 0;
@@ -44,7 +45,6 @@ struct Layer {
   int ldj = 0;    // n_rec rounded to 4: row stride of traces and accumulators
   int ldv = 0;    // n_rec rounded to 256: row stride of psiK, LK
   int ldw = 0;    // n_rec rounded to the forward workgroup size: row stride of Wt
-  int lda = 0;    // n_adaptive rounded to 4: row stride of epsa
   int rows_per_wave = 0;
   const float* W_src = nullptr;
   const float* Wout_src = nullptr;
@@ -56,7 +56,9 @@ struct Layer {
   // the eligibility pass of block k reads the other
   float *psiK[2], *LK[2], *zbarK[2], *deltaK[2], *ztK[2];
   float* Cpart;
-  double *acc, *accout;                  // gradient accumulators
+  double *acc, *accout;                  // gradient accumulators (acc: n_split partials)
+  int n_split = 1;                       // batch splits of the eligibility kernel
+  size_t acc_stride = 0;                 // doubles between partial accumulators
   float *ebar, *epsa;                    // eligibility traces
 };
 
@@ -64,7 +66,10 @@ struct Plan {
   eprop_config cfg;
   std::vector<Layer> layers;
   int* err_flag = nullptr;
-  int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, jlist = 0, out_splits = 1;
+  int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, ldc = 0, jlist = 0, out_splits = 1;
+  // block coefficients of the eligibility recursion, shared by the layers
+  // (they are processed one after the other on one stream)
+  float *coefU = nullptr, *coefV = nullptr, *coefH = nullptr, *coefS = nullptr;
   size_t smem = 0;
   size_t bytes = 0;
 };
@@ -108,6 +113,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   plan->rows = (int)round_up(KM * plan->Bp, 32);     // rows of deltaK, ztK, psiK, LK
   plan->ldk = (int)round_up(K, 32);
   plan->ldn = (int)round_up(N, 32);
+  plan->ldc = (int)round_up(N, eprop::kColPad);
   plan->jlist = (int)(round_up(N, eprop::kFwdThreads) / eprop::kFwdThreads * 64);
   {
     int dummy;
@@ -125,7 +131,6 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.ldj = (int)round_up(N, 4);
     L.ldv = (int)round_up(N, 256);
     L.ldw = (int)round_up(N, eprop::kFwdThreads);
-    L.lda = (int)round_up(std::max(c.n_adaptive, 1), 4);
     L.rows_per_wave = (int)round_up((L.n_pre + eprop::kFwdWaves - 1) / eprop::kFwdWaves, 64);
     rwmax = std::max(rwmax, L.rows_per_wave);
     npre_total += L.n_pre;
@@ -142,20 +147,35 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     for (int sl = 0; sl < 2; ++sl) {
       L.psiK[sl] = (float*)take(sizeof(float) * R * L.ldv);
       L.LK[sl] = (float*)take(sizeof(float) * R * L.ldv);
-      L.zbarK[sl] = (float*)take(sizeof(float) * B * KM * npp);
+      L.zbarK[sl] = (float*)take(sizeof(float) * B * npp * KM);
       L.deltaK[sl] = (float*)take(sizeof(float) * R * plan->ldk);
       L.ztK[sl] = (float*)take(sizeof(float) * R * plan->ldn);
     }
     L.Cpart = (float*)take(sizeof(float) * plan->out_splits * K * N);
-    L.acc = (double*)take(sizeof(double) * npp * L.ldj);
+    // batch splits of the eligibility kernel: about 2048 workgroups (four
+    // rounds of two per compute unit), at most 8 and at most one per element
+    const size_t tiles = (npp / eprop::kTile) * ((N + eprop::kTile - 1) / eprop::kTile);
+    L.n_split = (int)std::max<size_t>(1, std::min<size_t>({8, B, (2048 + tiles - 1) / tiles}));
+    L.acc_stride = npp * L.ldj;
+    L.acc = (double*)take(sizeof(double) * L.n_split * L.acc_stride);
     L.accout = (double*)take(sizeof(double) * K * L.ldj);
-    L.ebar = (float*)take(sizeof(float) * B * npp * L.ldj);
-    L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * L.lda : 0);
+    // traces tile by tile: all j tiles, and the tiles holding adaptive neurons
+    const size_t ldc = round_up(N, eprop::kColPad);
+    const size_t lda_t = round_up(c.n_adaptive, eprop::kTile);
+    L.ebar = (float*)take(sizeof(float) * B * npp * ldc);
+    L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * lda_t : 0);
   }
+  const size_t ldc = plan->ldc;
+  plan->coefU = (float*)take(sizeof(float) * B * ldc * KM);
+  plan->coefV = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * ldc * KM : 0);
+  plan->coefH = (float*)take(sizeof(float) * B * ldc * KM);
+  plan->coefS = (float*)take(sizeof(float) * 4 * B * ldc);
   const size_t npad4 = round_up(N, 4);
+  size_t npre_max = 0;
+  for (const Layer& L : plan->layers) npre_max = std::max<size_t>(npre_max, L.n_pre);
   plan->smem = sizeof(int) * (eprop::kFwdWaves * ((size_t)rwmax + (size_t)plan->jlist) +
-                              2 * eprop::kFwdWaves) +
-               sizeof(float) * (2 + (size_t)c.n_layers * K + npre_total) +
+                              npre_max + 2 * eprop::kFwdWaves + 2) +
+               sizeof(float) * ((size_t)eprop::kFwdWaves * K + (size_t)c.n_layers * K + npre_total) +
                (size_t)c.n_layers * 2 * npad4 + (size_t)eprop::kFwdXSteps * c.n_in;
   plan->bytes = round_up(off, 256);
 }
@@ -302,14 +322,27 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
                     "readout gradient accumulation")))
       return rc;
 
+    const int kpad = (int)round_up(steps, 16);
+    eprop::CoefArgs ca;
+    ca.psiK = L.psiK[sl]; ca.LK = L.LK[sl]; ca.ldv = L.ldv; ca.Bp = P.Bp;
+    ca.U = P.coefU; ca.V = c.n_adaptive > 0 ? P.coefV : nullptr; ca.H = P.coefH; ca.S = P.coefS;
+    ca.B = c.batch; ca.n_post = c.n_rec; ca.n_adaptive = c.n_adaptive;
+    ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(c.n_adaptive, eprop::kTile));
+    ca.steps = steps; ca.kpad = kpad; ca.ldc = P.ldc;
+    ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta;
+    if ((rc = check(ctx, eprop::launch_coef(ca, s), "eligibility coefficient kernel"))) return rc;
+
     eprop::TraceArgs ta;
-    ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.zbarK = L.zbarK[sl];
-    ta.psiK = L.psiK[sl]; ta.LK = L.LK[sl]; ta.B = c.batch; ta.Bp = P.Bp; ta.n_pre_pad = L.n_pre_pad;
-    ta.n_post = c.n_rec; ta.ldj = L.ldj; ta.ldv = L.ldv; ta.n_adaptive = c.n_adaptive;
-    ta.lda = L.lda; ta.Kmax = P.Kmax; ta.ldi = L.n_pre_pad; ta.steps = steps;
-    ta.n_seg_a = (c.n_adaptive + 255) / 256;
-    ta.n_seg_l = (c.n_rec + 255) / 256 - ta.n_seg_a;
-    ta.kappa = c.kappa; ta.rho = c.rho; ta.beta = c.beta; ta.first = first;
+    ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
+    ta.n_split = L.n_split; ta.zbarK = L.zbarK[sl];
+    ta.U = P.coefU; ta.V = ca.V; ta.H = P.coefH; ta.S = P.coefS;
+    ta.B = c.batch; ta.n_pre_pad = L.n_pre_pad; ta.n_post = c.n_rec; ta.ldj = L.ldj;
+    ta.n_adaptive = c.n_adaptive; ta.ldi = L.n_pre_pad;
+    ta.n_jt = (c.n_rec + eprop::kTile - 1) / eprop::kTile;
+    ta.n_jt_a = (c.n_adaptive + eprop::kTile - 1) / eprop::kTile;
+    ta.ldc = P.ldc; ta.kpad = kpad;
+    ta.kappa_K = (float)std::pow((double)c.kappa, (double)steps);
+    ta.first = first;
     const bool timed = ctx->prof && ctx->prof_n < ctx->prof_max;
     if (timed && (rc = check(ctx, hipEventRecord(ctx->ev[2 * ctx->prof_n], s), "event record")))
       return rc;
@@ -444,7 +477,8 @@ int eprop_get_grads(eprop_ctx* ctx, float* const* d_grads, double* d_loss) {
   for (int l = 0; l < c.n_layers; ++l) {
     Layer& L = ctx->plan.layers[l];
     eprop::GradsArgs g;
-    g.acc = L.acc; g.ldj = L.ldj; g.dW = d_grads[2 * l]; g.n_pre = L.n_pre; g.n_post = c.n_rec;
+    g.acc = L.acc; g.ldj = L.ldj; g.n_split = L.n_split; g.acc_stride = L.acc_stride;
+    g.dW = d_grads[2 * l]; g.n_pre = L.n_pre; g.n_post = c.n_rec;
     g.n_inl = L.n_inl; g.recurrent = c.recurrent;
     g.accout = L.accout; g.ld_acc = L.ldj; g.dWout = d_grads[2 * l + 1]; g.K = c.n_out;
     g.valid = ctx->t > 0;

@@ -7,7 +7,7 @@
 //   psiK   [Kmax*Bp][ldv]  pseudo-derivative (ldv = n_rec rounded to 256)
 //   deltaK [rows][ldk]     readout error (softmax - onehot)
 //   ztK    [rows][ldn]     kappa-filtered spikes
-//   zbarK  [B][Kmax][ldi]  filtered presynaptic vector
+//   zbarK  [B][Kmax/4][ldi][4]  filtered presynaptic vector (4 steps contiguous)
 // Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
 // psiK) and the readout gradient dW_out += deltaK^T * ztK.  The eligibility
 // kernel then advances every synapse's traces through the block's steps with
@@ -23,9 +23,11 @@ namespace eprop {
 constexpr int kFwdThreads = 1024;              // forward workgroup: one batch element
 constexpr int kFwdWaves = kFwdThreads / 64;
 constexpr int kFwdXSteps = 8;                  // input spikes staged in shared memory per load
-constexpr int kTraceWaves = 4;         // waves per eligibility workgroup (same 256 neurons)
-constexpr int kTraceChunk = 8;         // steps staged in shared memory at a time
-constexpr int kRowPad = 16;            // n_pre padded to a multiple of this (row group)
+constexpr int kBlockSteps = 128;       // timesteps per block (Kmax)
+constexpr int kKQ = kBlockSteps / 4;   // step quads per block
+constexpr int kTile = 64;              // eligibility workgroup tile: 64 (i) x 64 (j)
+constexpr int kRowPad = kTile;         // n_pre padded to the tile height (ldi)
+constexpr int kColPad = kTile;         // n_rec padded to the tile width (ldc)
 
 struct FwdLayer {
   const float* Wt; int ldw;      // transposed drive weights [n_pre][ldw]
@@ -36,7 +38,7 @@ struct FwdLayer {
   float* y;                      // state [B][K_out]
   double* lossacc;               // [B]
   float* psiK;                   // [rows][ldj]
-  float* zbarK;                  // [B][Kmax][ldi]
+  float* zbarK;                  // [B][Kmax/4][ldi][4]
   float* deltaK; float* ztK;     // [rows][ldk], [rows][ldn]
   int n_inl, n_pre, rows_per_wave, ldi;
 };
@@ -76,24 +78,47 @@ hipError_t launch_gemm_tn(const GemmArgs& a, hipStream_t s);
 hipError_t launch_accumulate(const float* part, int splits, size_t split_stride, int M, int N,
                              double* acc, int ld_acc, int first, hipStream_t s);
 
-// Eligibility vectors and gradient accumulation over `steps` timesteps.
-struct TraceArgs {
-  float* ebar;     // [B][n_pre_pad][ldj]
-  float* epsa;     // [B][n_pre_pad][lda]
-  double* acc;     // [n_pre_pad][ldj]
-  const float* zbarK;                 // [B][Kmax][ldi]
-  const float* psiK; const float* LK; // [rows][ldv], row t*Bp + b, ldv a multiple of 256
-  int B, Bp, n_pre_pad, n_post, ldj, ldv, n_adaptive, lda, Kmax, ldi, steps;
-  int n_seg_a, n_seg_l;   // 256-neuron segments holding adaptive neurons, and the rest
+// Block coefficients of the eligibility recursion, one thread per (b, j):
+// U, V, H [B][Kmax/4][ldc][4] (zero for steps <= s < kpad; V written for
+// j < n_vcols only, NULL when no neuron adapts) and the scalars c, q, P, D in
+// S [4][B][ldc].
+struct CoefArgs {
+  const float* psiK; const float* LK; int ldv, Bp;   // [t*Bp + b][ldv]
+  float* U; float* V; float* H; float* S;
+  int B, n_post, n_adaptive, n_vcols, steps, kpad, ldc;
   float kappa, rho, beta;
+};
+hipError_t launch_coef(const CoefArgs& a, hipStream_t s);
+
+// Eligibility vectors and gradient accumulation over a block of `steps`
+// timesteps, from the block coefficients.  The batch is split n_split ways;
+// split s accumulates the batch elements b = s (mod n_split) into its own
+// fp64 accumulator acc + s * acc_stride.
+// The traces are stored tile by tile: for batch element b and 64 x 64 tile
+// (it, jt), 16 KiB holding the four 32 x 32 wave sub-tiles, each as four
+// 16 x 16 blocks (bj, bi) of 64 lanes x 4 floats, in the order the kernel's
+// lanes hold them (see trace_kernel).  epsa covers the n_jt_a tiles that hold
+// adaptive neurons.
+struct TraceArgs {
+  float* ebar;     // [B][n_pre_pad / 64][n_jt][64 * 64]
+  float* epsa;     // [B][n_pre_pad / 64][n_jt_a][64 * 64]
+  double* acc;     // [n_split][n_pre_pad][ldj] (row-major)
+  size_t acc_stride;
+  const float* zbarK;                 // [B][Kmax/4][ldi][4], ldi = n_pre_pad
+  const float* U; const float* V; const float* H; const float* S;   // as CoefArgs
+  int B, n_pre_pad, n_post, ldj, n_adaptive, ldi, ldc, kpad, n_split;
+  int n_jt, n_jt_a;   // tiles along j: all, and those holding adaptive neurons
+  float kappa_K;   // kappa^steps
   int first;       // 1: traces and accumulators start at zero (not read)
 };
 hipError_t launch_trace(const TraceArgs& a, hipStream_t s);
 
-// Gradient read-out: dW[j][i] = acc[i][j] (recurrent diagonal zeroed),
-// dWout[k][j] = accout[k][j]; valid = 0 writes zeros.
+// Gradient read-out: dW[j][i] = sum over splits s of acc[s][i][j] (in split
+// order; recurrent diagonal zeroed), dWout[k][j] = accout[k][j]; valid = 0
+// writes zeros.
 struct GradsArgs {
-  const double* acc; int ldj; float* dW; int n_pre, n_post, n_inl, recurrent;
+  const double* acc; int ldj; int n_split; size_t acc_stride;
+  float* dW; int n_pre, n_post, n_inl, recurrent;
   const double* accout; int ld_acc; float* dWout; int K;
   int valid;
 };

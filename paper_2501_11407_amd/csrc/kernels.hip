@@ -9,6 +9,8 @@
 
 #include <math.h>
 
+#include <utility>
+
 namespace eprop {
 namespace {
 
@@ -32,11 +34,6 @@ __device__ inline int lanes_below(unsigned long long m, int lane) {
   return __popcll(m & ((1ull << lane) - 1ull));
 }
 
-__device__ inline f32x4 load_nt(const float* p) {
-  return __builtin_nontemporal_load((const f32x4*)p);
-}
-__device__ inline void store_nt(float* p, f32x4 v) { __builtin_nontemporal_store(v, (f32x4*)p); }
-
 inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
 // ---------------------------------------------------------------- forward
@@ -44,20 +41,23 @@ inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 // neuron state of the threads' neurons stays in registers, the filtered
 // presynaptic vector and the readout in shared memory.  Per step and layer:
 //   1. p = [in ; z_prev]; zbar = alpha*zbar + p; each wave lists the indices
-//      of its contiguous slice of p that are 1, in ascending order.
-//   2. drive I_j = sum of W_ji over the listed i, visited in ascending i (the
-//      order of a plain sequential sum), then the neuron step with one
-//      rounding per operation:
+//      of its contiguous slice of p that are 1, in ascending order, and the
+//      lists are merged into one ascending list.
+//   2. drive I_j = sum of W_ji over the listed i, added in ascending i (the
+//      order of a plain sequential sum; the rows are loaded a batch at a
+//      time), then the neuron step with one rounding per operation:
 //        v = alpha*v; v = v + I; v = v - thr*z_prev
 //        a = rho*a;   a = a + z_prev
 //        A = beta_j*a; A = thr + A;  x = v - A;  z = x > 0
 //        psi = (gamma/thr) * max(0, 1 - |x|/thr)
-//   3. readout y = kappa*y + W_out z (over the spiking neurons), softmax,
-//      delta = softmax - onehot(label), cross-entropy into the loss;
-//   4. ztilde = kappa*ztilde + z.
+//   3. each wave sums the readout weights of its spiking neurons for every
+//      class; ztilde = kappa*ztilde + z.
+//   4. wave 0: y = kappa*y + (sum of the waves' partial sums, in wave order),
+//      softmax, delta = softmax - onehot(label), cross-entropy into the loss.
 // The learning signal L = W_out^T delta is one GEMM over the whole block.
 struct FwdLds {
-  int* act; int* spk; int* cnt; float* red; float* sy; float* szb; uint8_t* zc; uint8_t* xs;
+  int* act; int* mrg; int* spk; int* cnt; float* part; float* sy; float* szb; uint8_t* zc;
+  uint8_t* xs;
   int rwmax, npad;
 };
 
@@ -81,7 +81,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // 1. presynaptic vector, its filter, ordered active lists
   const int rw = Ly.rows_per_wave;
   const int i_beg = w * rw, i_end = min(Ly.n_pre, i_beg + rw);
-  float* zbk = Ly.zbarK + ((size_t)b * A.Kmax + t) * Ly.ldi;
+  float* zbk = Ly.zbarK + ((size_t)b * kKQ + t / 4) * Ly.ldi * 4 + (t & 3);   // [b][t/4][i][4]
   int n_act = 0;
   for (int base = i_beg; base < i_end; base += kWave) {
     const int i = base + lane;
@@ -91,7 +91,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       on = sv != 0;
       const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
       szb[i] = zv;
-      zbk[i] = zv;
+      zbk[(size_t)i * 4] = zv;
     }
     const unsigned long long m = __ballot(on);
     if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
@@ -99,23 +99,37 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   }
   if (lane == 0) S.cnt[w] = n_act;
   __syncthreads();
+  {
+    int off = 0;
+    for (int ww = 0; ww < w; ++ww) off += S.cnt[ww];
+    for (int k = lane; k < n_act; k += kWave) S.mrg[off + k] = S.act[w * S.rwmax + k];
+    if (w == kFwdWaves - 1 && lane == 0) S.cnt[2 * kFwdWaves] = off + n_act;
+  }
+  __syncthreads();
 
   // 2. drive and neuron step.  Rows of Wt are padded to a multiple of the
   // workgroup size; chunks q with q*kFwdThreads >= n_rec are skipped (QN is
-  // rounded up to a power of two).
+  // rounded up to a power of two).  UB rows are loaded before any is added.
+  constexpr int UB = QN >= 16 ? 1 : 16 / QN;
+  const int total = S.cnt[2 * kFwdWaves];
   float I[QN];
 #pragma unroll
   for (int q = 0; q < QN; ++q) I[q] = 0.0f;
-  for (int ww = 0; ww < kFwdWaves; ++ww) {
-    const int c = S.cnt[ww];
-    const int* lst = S.act + ww * S.rwmax;
-#pragma unroll 4
-    for (int k = 0; k < c; ++k) {
-      const float* wrow = Ly.Wt + (size_t)lst[k] * Ly.ldw + tid;
+  for (int k0 = 0; k0 < total; k0 += UB) {
+    float wv[UB][QN];
 #pragma unroll
-      for (int q = 0; q < QN; ++q)
-        if (q * kFwdThreads < A.n_rec) I[q] += wrow[q * kFwdThreads];
+    for (int u = 0; u < UB; ++u) {
+      // the same row for every lane: a scalar base
+      const int i = __builtin_amdgcn_readfirstlane(S.mrg[min(k0 + u, total - 1)]);
+      const float* wrow = Ly.Wt + (size_t)i * Ly.ldw + tid;
+#pragma unroll
+      for (int q = 0; q < QN; ++q) wv[u][q] = (q * kFwdThreads < A.n_rec) ? wrow[q * kFwdThreads] : 0.0f;
     }
+#pragma unroll
+    for (int u = 0; u < UB; ++u)
+      if (k0 + u < total)
+#pragma unroll
+        for (int q = 0; q < QN; ++q) I[q] += wv[u][q];
   }
   int n_spk = 0;
 #pragma unroll
@@ -139,6 +153,10 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       znow[j] = z ? 1 : 0;
       const float u = 1.0f - fabsf(x) / A.thr;
       Ly.psiK[row * A.ldj + j] = A.gamma_over_thr * fmaxf(u, 0.0f);
+      float zz = A.kappa * zt[q];
+      zz = zz + (z ? 1.0f : 0.0f);
+      zt[q] = zz;
+      Ly.ztK[row * A.ldn + j] = zz;
     }
     const unsigned long long m = __ballot(z);
     if (z) S.spk[w * A.jlist + n_spk + lanes_below(m, lane)] = j;
@@ -150,63 +168,51 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       if (lane == 1 && w0 + 1 < A.W32) srow[w0 + 1] = (uint32_t)(m >> 32);
     }
   }
-  if (lane == 0) S.cnt[kFwdWaves + w] = n_spk;
-  __syncthreads();
 
-  // 3. readout (rows of the transposed readout weights of the spiking
-  // neurons, read coalesced over k), softmax cross-entropy
-  for (int k = tid; k < A.K_out; k += kFwdThreads) {
-    float Y = 0.0f;
-    for (int ww = 0; ww < kFwdWaves; ++ww) {
-      const int c = S.cnt[kFwdWaves + ww];
-      const int* lst = S.spk + ww * A.jlist;
+  // 3. this wave's share of the readout: rows of the transposed readout
+  // weights of its spiking neurons, read coalesced over the classes
+  for (int kb = 0; kb < A.K_out; kb += kWave) {
+    const int k = kb + lane;
+    if (k < A.K_out) {
+      float Y = 0.0f;
 #pragma unroll 8
-      for (int s = 0; s < c; ++s) Y += Ly.WoutT[(size_t)lst[s] * A.ldk + k];
+      for (int s2 = 0; s2 < n_spk; ++s2) {
+        const int j = __builtin_amdgcn_readfirstlane(S.spk[w * A.jlist + s2]);
+        Y += Ly.WoutT[(size_t)j * A.ldk + k];
+      }
+      S.part[w * A.K_out + k] = Y;
     }
-    float yy = A.kappa * sy[k];
-    yy = yy + Y;
-    sy[k] = yy;
   }
   __syncthreads();
-  const int label = A.labels[b];
-  const bool label_ok = label >= 0 && label < A.K_out;
+
+  // 4. readout, softmax cross-entropy (wave 0; the other waves go on)
   if (w == 0) {
+    const int label = A.labels[b];
+    const bool label_ok = label >= 0 && label < A.K_out;
     float m = -INFINITY;
-    for (int k = lane; k < A.K_out; k += kWave) m = fmaxf(m, sy[k]);
+    for (int k = lane; k < A.K_out; k += kWave) {
+      float Y = 0.0f;
+      for (int ww = 0; ww < kFwdWaves; ++ww) Y += S.part[ww * A.K_out + k];
+      float yy = A.kappa * sy[k];
+      yy = yy + Y;
+      sy[k] = yy;
+      m = fmaxf(m, yy);
+    }
     m = wave_max(m);
     float se = 0.0f;
     for (int k = lane; k < A.K_out; k += kWave) se += expf(sy[k] - m);
     se = wave_sum(se);
     if (lane == 0) {
-      S.red[0] = m;
-      S.red[1] = se;
       if (label_ok)
         loss += log((double)se) - ((double)sy[label] - (double)m);
       else
         *A.err_flag = 1;
     }
-  }
-  __syncthreads();
-  {
-    const float m = S.red[0], se = S.red[1];
-    for (int k = tid; k < A.K_out; k += kFwdThreads) {
+    for (int k = lane; k < A.K_out; k += kWave) {
       const float d = expf(sy[k] - m) / se - ((k == label) ? 1.0f : 0.0f);
       Ly.deltaK[row * A.ldk + k] = d;
     }
   }
-
-  // 4. filtered spikes
-#pragma unroll
-  for (int q = 0; q < QN; ++q) {
-    const int j = q * kFwdThreads + tid;
-    if (j < A.n_rec) {
-      float zz = A.kappa * zt[q];
-      zz = zz + (znow[j] ? 1.0f : 0.0f);
-      zt[q] = zz;
-      Ly.ztK[row * A.ldn + j] = zz;
-    }
-  }
-  __syncthreads();
 }
 
 template <int QN, int LI>
@@ -248,11 +254,13 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs A) {
   S.rwmax = A.L[0].rows_per_wave;
   if (A.n_layers > 1) S.rwmax = max(S.rwmax, A.L[1].rows_per_wave);
   S.npad = (A.n_rec + 3) & ~3;
+  const int npre_max = max(A.L[0].n_pre, A.n_layers > 1 ? A.L[1].n_pre : 0);
   S.act = (int*)smem;                          // [waves][rwmax]
-  S.spk = S.act + kFwdWaves * S.rwmax;         // [waves][jlist]
-  S.cnt = S.spk + kFwdWaves * A.jlist;         // [2 * waves]
-  S.red = (float*)(S.cnt + 2 * kFwdWaves);     // [2]
-  S.sy = S.red + 2;                            // [n_layers][K_out]
+  S.mrg = S.act + kFwdWaves * S.rwmax;         // [npre_max]
+  S.spk = S.mrg + npre_max;                    // [waves][jlist]
+  S.cnt = S.spk + kFwdWaves * A.jlist;         // [2 * waves + 2]
+  S.part = (float*)(S.cnt + 2 * kFwdWaves + 2);   // [waves][K_out]
+  S.sy = S.part + kFwdWaves * A.K_out;         // [n_layers][K_out]
   S.szb = S.sy + A.n_layers * A.K_out;         // [n_pre_0 + n_pre_1]
   const int npre_total = A.L[0].n_pre + (A.n_layers > 1 ? A.L[1].n_pre : 0);
   S.zc = (uint8_t*)(S.szb + npre_total);       // [n_layers][2][npad]
@@ -402,229 +410,350 @@ __global__ __launch_bounds__(256) void accumulate_kernel(const float* part, int 
 }
 
 // ---------------------------------------------------------------- eligibility
-// A workgroup owns one 256-wide segment of postsynaptic neurons and a group
-// of presynaptic rows; lane l of every wave owns the four neurons
-// j0 = seg*256 + 4l..4l+3 and wave w rows ib + w*R .. ib + w*R + R-1.
-// Segments holding adaptive neurons move two trace arrays per synapse and use
-// R = 2 rows per thread, LIF segments one array and R = 4, so every wave does
-// about the same arithmetic; groups of 16 rows list their adaptive and LIF
-// workgroups next to each other in dispatch order.
-// The workgroup walks the batch; for each batch element the traces are read
-// once, advanced through the block's steps and written once.  psi and L of
-// the segment and zbar of the rows are shared through shared memory,
-// kTraceChunk steps at a time, in a pipeline over chunks (batch element,
-// step range): the next chunk's vectors are loaded into registers and the
-// next batch element's traces prefetched while the current chunk computes.
-// Per step, for each (i, j):
-//   e    = psi_j zbar_i - psi_j beta_j epsa      (dz_j/dW_ji)
-//   ebar = kappa ebar + e                        (readout filter on the trace)
-//   acc += L_j ebar                              (fp32 within a chunk, fp64 across)
-//   epsa = (rho - beta_j psi_j) epsa + psi_j zbar_i   (adaptive j)
-// On LIF lanes of an adaptive segment beta_j = 0, so e = psi_j zbar_i exactly.
-constexpr int kStage = kTraceChunk * 64 / (kTraceWaves * 64);   // float4 per thread per vector
-static_assert(kStage * kTraceWaves * 64 == kTraceChunk * 64, "chunk must split evenly");
-static_assert(kTraceChunk * kRowPad <= kTraceWaves * 64, "zbar chunk must fit one load per thread");
+// Over a block of K steps the recursion of one synapse (i, j) of batch
+// element b,
+//   e = psi_j (zbar_i - beta_j epsa);  ebar = kappa ebar + e;  g += L_j ebar;
+//   epsa = psi_j zbar_i + (rho - beta_j psi_j) epsa,
+// is linear in the block's starting traces E0 = ebar, A0 = epsa and in the
+// presynaptic values zbar_{i,s}, with coefficients that depend only on
+// (b, j, s).  So
+//   ebar_K = kappa^K E0 + P_j A0 + sum_s zbar_{i,s} U_{j,s}
+//   epsa_K = D_j A0           + sum_s zbar_{i,s} V_{j,s}
+//   g     += c_j E0 + q_j A0  + sum_s zbar_{i,s} H_{j,s}
+// The sums over s are dense contractions (MFMA); the rest is elementwise.
+// Coefficients (d_s = rho - beta_j psi_s, M_s = sum_{t>=s} kappa^{t-s} L_t,
+// N_s = sum_{r>s} beta_j psi_r M_r prod_{s<u<r} d_u):
+//   H_s = psi_s (M_s - N_s),  c = kappa M_0,  q = -N_{-1},
+//   U_s, P: the same with L replaced by the unit vector at the block's last
+//   step,  V_s = psi_s prod_{u>s} d_u,  D = prod_u d_u.
+// For LIF neurons beta_j = 0: N = 0, the epsa terms vanish.
+__global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  const int b = blockIdx.y;
+  if (j >= a.n_post) return;
+  const float bt = (j < a.n_adaptive) ? a.beta : 0.0f;
+  const bool wv = a.V != nullptr && j < a.n_vcols;
+  const float* __restrict__ psiK = a.psiK;
+  const float* __restrict__ LK = a.LK;
+  const size_t o = ((size_t)b * kKQ * a.ldc + j) * 4, qs = (size_t)a.ldc * 4;
+  float M = 0.0f, Mu = 0.0f, nx = 0.0f, nxu = 0.0f, Dsuf = 1.0f;
+  for (int qd = a.kpad / 4 - 1; qd >= 0; --qd) {
+    float ps[4], L[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int s = 4 * qd + e;
+      const size_t row = ((size_t)s * a.Bp + b) * a.ldv + j;
+      ps[e] = s < a.steps ? psiK[row] : 0.0f;
+      L[e] = s < a.steps ? LK[row] : 0.0f;
+    }
+    f32x4 u, v, h;
+#pragma unroll
+    for (int e = 3; e >= 0; --e) {
+      const int s = 4 * qd + e;
+      if (s >= a.steps) {
+        u[e] = v[e] = h[e] = 0.0f;
+        continue;
+      }
+      const float d = a.rho - bt * ps[e];
+      M = fmaf(a.kappa, M, L[e]);
+      Mu = (s == a.steps - 1) ? 1.0f : a.kappa * Mu;
+      h[e] = ps[e] * (M - nx);
+      u[e] = ps[e] * (Mu - nxu);
+      v[e] = ps[e] * Dsuf;
+      nx = fmaf(bt * ps[e], M, d * nx);
+      nxu = fmaf(bt * ps[e], Mu, d * nxu);
+      Dsuf = d * Dsuf;
+    }
+    *(f32x4*)(a.U + o + qd * qs) = u;
+    *(f32x4*)(a.H + o + qd * qs) = h;
+    if (wv) *(f32x4*)(a.V + o + qd * qs) = v;
+  }
+  const size_t so = (size_t)b * a.ldc + j, plane = (size_t)a.B * a.ldc;
+  a.S[so] = a.kappa * M;       // c
+  a.S[plane + so] = -nx;       // q
+  a.S[2 * plane + so] = -nxu;  // P
+  a.S[3 * plane + so] = Dsuf;  // D
+}
 
-struct TraceShared {
-  f32x4 ps[kTraceChunk][64];
-  f32x4 lv[kTraceChunk][64];
-  float zb[kTraceChunk][kRowPad];
+// A workgroup of 4 waves owns a 64 (i) x 64 (j) tile of synapses and one
+// split of the batch; wave w computes the 32 x 32 sub-tile (w / 2, w % 2).
+// For each batch element b of the split:
+//  * MFMA contractions C_U, C_V, C_H = coef_b[j][s] x zbar_b[i][s] over the
+//    block's steps (v_mfma_f32_16x16x4f32, 2x2 blocks of 16x16 per wave),
+//    16 steps ("a chunk") at a time, operands read from shared memory;
+//  * then the elementwise update of the traces, each read once and written
+//    once (1 KiB contiguous per wave instruction), and of the gradient.
+// Operands stream through a ring of kRing chunk slots in shared memory:
+// zbar_b rows i and U, H (and V) rows j of the chunk's 16 steps are copied by
+// direct global-to-LDS loads (16 bytes per lane, no registers) kPrefetch
+// chunks ahead of the chunk being contracted, across batch elements.  The
+// block-start traces of a batch element (registers) and its scalars c, q, P,
+// D (shared memory, double-buffered) travel with its first chunk.
+// Waits: copies and loads complete in order, so a chunk's copies are waited
+// for with an exact vmcnt; trace stores (which may complete out of order with
+// respect to loads) are drained once per batch element, at its first chunk.
+// The workgroup barrier carries no memory fence (a fence would drain every
+// copy in flight); shared-memory hazards are ordered by the waits and the
+// barrier alone.
+// Lane (r, g) of block (bj, bi) holds the 4 columns j = jw + 16 bj + 4 g ..+3
+// of row i = iw + 16 bi + r; the traces of a wave sub-tile are stored in
+// exactly this order (block (bj, bi) at (2 bj + bi) KiB, lane l at 16 l
+// bytes).  The gradient of the batch elements of one launch is summed in
+// fp32 per lane and added to the split's fp64 accumulator at the end.
+// Buffer access: a wave-uniform base with a byte range (accesses outside it
+// read zero and write nothing) and a 32-bit per-lane byte offset.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ f32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, 0);
+}
+
+constexpr int kChunkQuads = 4;                        // 16 steps per MFMA chunk
+constexpr int kRing = 4;                              // chunk slots
+constexpr int kPrefetch = 3;                          // chunks copied ahead (< kRing)
+constexpr int kSlot = 4 * kChunkQuads * kTile * 4;    // floats per slot: 4 operands (16 KiB)
+constexpr int kScal = 4 * kTile;                      // floats of c, q, P, D for 64 columns
+constexpr size_t kTraceSmem = sizeof(float) * (kRing * kSlot + 2 * kScal);
+constexpr uint32_t kSubTileBytes = 32 * 32 * 4;
+
+// s_waitcnt immediate that waits for vmcnt <= n only (gfx9 encoding)
+constexpr int vm_wait(int n) { return (n & 0xF) | ((n >> 4) << 14) | 0x70 | 0xF00; }
+
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Calls f(std::integral_constant<int, I>) for I = 0, 1, ... in order.
+template <typename F, int... I>
+__device__ __forceinline__ void for_each_index(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+// Lane l copies 16 bytes from its own address g to lds + 16 l.
+__device__ __forceinline__ void dma16(const float* g, float* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
+}
+
+template <bool ALIF, int NCH>
+struct TraceTile {
+  static constexpr int D = NCH < kPrefetch ? NCH : kPrefetch;   // chunks in flight ahead
+  static constexpr int Q = ALIF ? 4 : 3;     // copies per wave per chunk
+  static constexpr int QB = 1 + (ALIF ? 8 : 4);   // + scalars and trace loads with chunk 0
+  static constexpr int ops(int c) { return Q + (c == 0 ? QB : 0); }
+  // vector-memory operations issued after the copies of chunk ch (> 0) when
+  // it is waited for: those of chunks ch+1 .. ch+D-1, the ones past the end
+  // of the batch element belonging to the next one (if there is one).
+  static constexpr int pending(int ch, bool next) {
+    int n = 0;
+    for (int m = ch + 1; m <= ch + D - 1; ++m) n += m < NCH ? ops(m) : (next ? ops(m - NCH) : 0);
+    return n;
+  }
+  static_assert(pending(1, true) <= 63, "vmcnt range");
+
+  const TraceArgs& a;
+  float* sm;
+  int i0, j0, it, jt, split, lane, r, g, w, wi, wj;
+  bool first;
+
+  __device__ __forceinline__ TraceTile(const TraceArgs& a_, float* sm_, int it_, int jt_, int split_,
+                                       bool first_)
+      : a(a_), sm(sm_), i0(it_ * kTile), j0(jt_ * kTile), it(it_), jt(jt_), split(split_),
+        first(first_) {
+    lane = threadIdx.x & 63;
+    r = lane & 15;
+    g = lane >> 4;
+    w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index, uniform
+    wi = w >> 1;
+    wj = w & 1;
+  }
+
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t ebar_rsrc(int b) const {
+    const size_t t = ((size_t)b * (a.n_pre_pad / kTile) + it) * a.n_jt + jt;
+    return make_rsrc((const char*)a.ebar + (t * 4 + w) * kSubTileBytes, kSubTileBytes);
+  }
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t epsa_rsrc(int b) const {
+    const size_t t = ((size_t)b * (a.n_pre_pad / kTile) + it) * a.n_jt_a + jt;
+    return make_rsrc((const char*)a.epsa + (t * 4 + w) * kSubTileBytes, kSubTileBytes);
+  }
+
+  // Copies of chunk c of batch element b into ring slot sl (this wave: quad
+  // 4c + w of each operand).  With chunk 0 also the scalars (plane w) into
+  // scalar buffer par and the block-start traces into E/A.
+  __device__ __forceinline__ void issue(int b, int c, int sl, int par, f32x4 (&E)[2][2],
+                                        f32x4 (&A)[2][2]) const {
+    float* slot = sm + sl * kSlot;
+    const size_t qd = (size_t)b * kKQ + kChunkQuads * c + w;
+    dma16(a.zbarK + (qd * a.ldi + i0) * 4 + lane * 4, slot + (0 * kChunkQuads + w) * kTile * 4);
+    dma16(a.U + (qd * a.ldc + j0) * 4 + lane * 4, slot + (1 * kChunkQuads + w) * kTile * 4);
+    dma16(a.H + (qd * a.ldc + j0) * 4 + lane * 4, slot + (2 * kChunkQuads + w) * kTile * 4);
+    if constexpr (ALIF)
+      dma16(a.V + (qd * a.ldc + j0) * 4 + lane * 4, slot + (3 * kChunkQuads + w) * kTile * 4);
+    if (c == 0) {
+      if (lane < 16)
+        dma16(a.S + ((size_t)w * a.B + b) * a.ldc + j0 + lane * 4,
+              sm + kRing * kSlot + par * kScal + w * kTile);
+      const auto eR = ebar_rsrc(b);
+#pragma unroll
+      for (int x = 0; x < 4; ++x) E[x >> 1][x & 1] = bload(eR, x * 1024u + lane * 16u);
+      if constexpr (ALIF) {
+        const auto aR = epsa_rsrc(b);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) A[x >> 1][x & 1] = bload(aR, x * 1024u + lane * 16u);
+      }
+    }
+  }
+
+  // One batch element (k-th of the split): its traces are in E/A; the next
+  // one's arrive in En/An.
+  __device__ __forceinline__ void batch(int k, int nk, f32x4 (&E)[2][2], f32x4 (&A)[2][2],
+                                        f32x4 (&En)[2][2], f32x4 (&An)[2][2],
+                                        f32x4 (&gacc)[2][2]) const {
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    const int b = split + k * a.n_split;
+    const bool next = k + 1 < nk;
+    f32x4 cU[2][2], cV[2][2], cH[2][2];
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+        cU[bj][bi] = zero;
+        cV[bj][bi] = zero;
+        cH[bj][bi] = zero;
+      }
+    auto chunk = [&](auto chc) {
+      constexpr int ch = decltype(chc)::value;
+      const int n = k * NCH + ch;
+      if constexpr (ch == 0)
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+      else if (next)
+        __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, true)));
+      else
+        __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, false)));
+      wg_barrier();   // chunk n is in shared memory; slot (n - 1) % kRing is free
+      constexpr int c2 = ch + D;
+      if constexpr (c2 < NCH)
+        issue(b, c2, (n + D) % kRing, k & 1, En, An);
+      else if (next)
+        issue(b + a.n_split, c2 - NCH, (n + D) % kRing, (k + 1) & 1, En, An);
+
+      const float* slot = sm + (n % kRing) * kSlot;
+      f32x4 z[2], u[2], h[2], v[2];
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        z[x] = *(const f32x4*)(slot + ((0 * kChunkQuads + g) * kTile + 32 * wi + 16 * x + r) * 4);
+        u[x] = *(const f32x4*)(slot + ((1 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4);
+        h[x] = *(const f32x4*)(slot + ((2 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4);
+        v[x] = ALIF ? *(const f32x4*)(slot + ((3 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4)
+                    : zero;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+          for (int bi = 0; bi < 2; ++bi) {
+            cU[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(u[bj][q], z[bi][q], cU[bj][bi], 0, 0, 0);
+            cH[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[bj][q], z[bi][q], cH[bj][bi], 0, 0, 0);
+            if constexpr (ALIF)
+              cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(v[bj][q], z[bi][q], cV[bj][bi], 0, 0, 0);
+          }
+    };
+    for_each_index(chunk, std::make_integer_sequence<int, NCH>{});
+
+    // traces and gradient of batch element b
+    const float* st = sm + kRing * kSlot + (k & 1) * kScal;   // [4][64]: c, q, P, D
+    const auto eR = ebar_rsrc(b);
+    const auto aR = ALIF ? epsa_rsrc(b) : eR;
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) {
+      const int cj = 32 * wj + 16 * bj + 4 * g;
+      const f32x4 c = *(const f32x4*)(st + cj), qq = *(const f32x4*)(st + kTile + cj);
+      const f32x4 P = ALIF ? *(const f32x4*)(st + 2 * kTile + cj) : zero;
+      const f32x4 Dd = ALIF ? *(const f32x4*)(st + 3 * kTile + cj) : zero;
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+        const f32x4 e0 = first ? zero : E[bj][bi];
+        const f32x4 a0 = (first || !ALIF) ? zero : A[bj][bi];
+        f32x4 ek, ak, gk;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], cU[bj][bi][q]));
+          gk[q] = fmaf(c[q], e0[q], fmaf(qq[q], a0[q], cH[bj][bi][q]));
+          ak[q] = fmaf(Dd[q], a0[q], cV[bj][bi][q]);
+        }
+        gacc[bj][bi] += gk;
+        const uint32_t o = (2 * bj + bi) * 1024u + lane * 16u;
+        bstore(eR, o, ek);
+        if constexpr (ALIF) bstore(aR, o, ak);
+      }
+    }
+  }
+
+  __device__ __forceinline__ void run() const {
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    const int nk = (a.B - split + a.n_split - 1) / a.n_split;
+    f32x4 gacc[2][2];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) gacc[x >> 1][x & 1] = zero;
+    f32x4 Ea[2][2], Aa[2][2], Eb[2][2], Ab[2][2];
+#pragma unroll
+    for (int c = 0; c < D; ++c) issue(split, c, c, 0, Ea, Aa);
+    for (int k = 0; k < nk; k += 2) {
+      batch(k, nk, Ea, Aa, Eb, Ab, gacc);
+      if (k + 1 >= nk) break;
+      batch(k + 1, nk, Eb, Ab, Ea, Aa, gacc);
+    }
+    // the split's fp64 accumulator (row-major [n_pre_pad][ldj])
+    const int iw = i0 + 32 * wi, jw = j0 + 32 * wj;
+    double* accp = a.acc + (size_t)split * a.acc_stride;
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) {
+      const int jb = jw + 16 * bj + 4 * g;
+      if (jb >= a.n_post) continue;
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+        double* p = accp + (size_t)(iw + 16 * bi + r) * a.ldj + jb;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) p[q] = (first ? 0.0 : p[q]) + (double)gacc[bj][bi][q];
+      }
+    }
+  }
 };
 
-struct TraceStage {
-  f32x4 ps[kStage], lv[kStage];
-  float zb;
-};
-
-// Every lane issues the same loads whatever the chunk (indices are clamped
-// to valid rows), so the number of loads in flight is the same on every path
-// and waits on them never have to drain the whole queue.
-template <int ROWS>
-__device__ __forceinline__ void trace_stage_load(const TraceArgs& a, TraceStage& g, int b, int c0,
-                                                 int nt, int seg, int ib) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int u = 0; u < kStage; ++u) {
-    const int k = tid + u * kTraceWaves * 64;
-    const int tt = min(k >> 6, nt - 1), l = k & 63;
-    const size_t row = (size_t)(c0 + tt) * a.Bp + b;
-    g.ps[u] = *(const f32x4*)(a.psiK + row * a.ldv + seg * 256 + 4 * l);
-    g.lv[u] = *(const f32x4*)(a.LK + row * a.ldv + seg * 256 + 4 * l);
-  }
-  const int kz = tid % (kTraceChunk * ROWS);
-  const int tt = min(kz / ROWS, nt - 1), r = kz % ROWS;
-  g.zb = a.zbarK[((size_t)b * a.Kmax + c0 + tt) * a.ldi + ib + r];
-}
-
-template <int ROWS>
-__device__ __forceinline__ void trace_stage_store(const TraceStage& g, int nt, TraceShared& S) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int u = 0; u < kStage; ++u) {
-    const int k = tid + u * kTraceWaves * 64;
-    const int tt = k >> 6, l = k & 63;
-    if (tt < nt) {
-      S.ps[tt][l] = g.ps[u];
-      S.lv[tt][l] = g.lv[u];
-    }
-  }
-  if (tid < kTraceChunk * ROWS) {
-    const int tt = tid / ROWS, r = tid % ROWS;
-    if (tt < nt) S.zb[tt][r] = g.zb;
+template <bool ALIF>
+__device__ __forceinline__ void trace_tile_n(const TraceArgs& a, float* sm, int it, int jt,
+                                             int split, bool first) {
+  static_assert(kBlockSteps == 128, "chunk dispatch assumes 128-step blocks");
+  switch (a.kpad >> 4) {
+    case 1: TraceTile<ALIF, 1>(a, sm, it, jt, split, first).run(); break;
+    case 2: TraceTile<ALIF, 2>(a, sm, it, jt, split, first).run(); break;
+    case 3: TraceTile<ALIF, 3>(a, sm, it, jt, split, first).run(); break;
+    case 4: TraceTile<ALIF, 4>(a, sm, it, jt, split, first).run(); break;
+    case 5: TraceTile<ALIF, 5>(a, sm, it, jt, split, first).run(); break;
+    case 6: TraceTile<ALIF, 6>(a, sm, it, jt, split, first).run(); break;
+    case 7: TraceTile<ALIF, 7>(a, sm, it, jt, split, first).run(); break;
+    default: TraceTile<ALIF, 8>(a, sm, it, jt, split, first).run(); break;
   }
 }
 
-template <int R, bool ALIF, bool FIRST>
-__device__ __forceinline__ void trace_body(const TraceArgs& a, TraceShared& S, int seg, int ib) {
-  constexpr int ROWS = R * kTraceWaves;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int j0 = seg * 256 + lane * 4;
-  const bool active = j0 < a.n_post;
-  const bool has_a = ALIF && j0 < a.n_adaptive;   // lane holds eps^a
-  const int i0 = ib + w * R;
-  float bj[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) bj[r] = (ALIF && j0 + r < a.n_adaptive) ? a.beta : 0.0f;
-
-  double acc[R][4];
-#pragma unroll
-  for (int ii = 0; ii < R; ++ii)
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      acc[ii][r] = (FIRST || !active) ? 0.0 : a.acc[(size_t)(i0 + ii) * a.ldj + j0 + r];
-
-  const size_t bs_e = (size_t)a.n_pre_pad * a.ldj;
-  const size_t bs_a = (size_t)a.n_pre_pad * a.lda;
-  float* pe0 = a.ebar + (size_t)i0 * a.ldj + j0;
-  float* pa0 = a.epsa + (size_t)i0 * a.lda + j0;
-  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-  const int nch = (a.steps + kTraceChunk - 1) / kTraceChunk;
-  const int total = a.B * nch;
-
-  f32x4 E[R], Aa[ALIF ? R : 1], En[R], An[ALIF ? R : 1];
-#pragma unroll
-  for (int ii = 0; ii < R; ++ii) {
-    E[ii] = zero;
-    En[ii] = zero;
-    if (!FIRST && active) E[ii] = load_nt(pe0 + (size_t)ii * a.ldj);
-  }
-  if constexpr (ALIF) {
-#pragma unroll
-    for (int ii = 0; ii < R; ++ii) {
-      Aa[ii] = zero;
-      An[ii] = zero;
-      if (!FIRST && has_a) Aa[ii] = load_nt(pa0 + (size_t)ii * a.lda);
-    }
-  }
-  TraceStage g;
-  trace_stage_load<ROWS>(a, g, 0, 0, min(kTraceChunk, a.steps), seg, ib);
-  trace_stage_store<ROWS>(g, min(kTraceChunk, a.steps), S);
-  __syncthreads();
-
-  for (int q = 0; q < total; ++q) {
-    const int b = q / nch, c = q - b * nch;
-    const int nt = min(kTraceChunk, a.steps - c * kTraceChunk);
-    // Order of issue: next batch element's traces (during its last chunk),
-    // then the next chunk's shared vectors.
-    if (!FIRST && c == nch - 1 && b + 1 < a.B) {
-#pragma unroll
-      for (int ii = 0; ii < R; ++ii)
-        if (active) En[ii] = load_nt(pe0 + (size_t)(b + 1) * bs_e + (size_t)ii * a.ldj);
-      if constexpr (ALIF) {
-#pragma unroll
-        for (int ii = 0; ii < R; ++ii)
-          if (has_a) An[ii] = load_nt(pa0 + (size_t)(b + 1) * bs_a + (size_t)ii * a.lda);
-      }
-    }
-    const int qn = min(q + 1, total - 1);
-    const int nb = qn / nch, nc = qn - nb * nch;
-    const int nnt = min(kTraceChunk, a.steps - nc * kTraceChunk);
-    trace_stage_load<ROWS>(a, g, nb, nc * kTraceChunk, nnt, seg, ib);
-
-    // L * ebar summed over the chunk in fp32, then added to the fp64 accumulator
-    float part[R][4];
-#pragma unroll
-    for (int ii = 0; ii < R; ++ii)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) part[ii][r] = 0.0f;
-    for (int tt = 0; tt < nt; ++tt) {
-      const f32x4 ps = S.ps[tt][lane];
-      const f32x4 lv = S.lv[tt][lane];
-      float zb[R];
-#pragma unroll
-      for (int ii = 0; ii < R; ++ii) zb[ii] = S.zb[tt][w * R + ii];
-      if constexpr (ALIF) {
-        float pb[4], rb[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          pb[r] = ps[r] * bj[r];
-          rb[r] = a.rho - pb[r];
-        }
-#pragma unroll
-        for (int ii = 0; ii < R; ++ii)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float pz = ps[r] * zb[ii];
-            const float e = fmaf(-pb[r], Aa[ii][r], pz);
-            E[ii][r] = fmaf(a.kappa, E[ii][r], e);
-            Aa[ii][r] = fmaf(rb[r], Aa[ii][r], pz);
-            part[ii][r] = fmaf(lv[r], E[ii][r], part[ii][r]);
-          }
-      } else {
-#pragma unroll
-        for (int ii = 0; ii < R; ++ii)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            E[ii][r] = fmaf(a.kappa, E[ii][r], ps[r] * zb[ii]);
-            part[ii][r] = fmaf(lv[r], E[ii][r], part[ii][r]);
-          }
-      }
-    }
-#pragma unroll
-    for (int ii = 0; ii < R; ++ii)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[ii][r] += (double)part[ii][r];
-
-    if (c == nch - 1) {
-#pragma unroll
-      for (int ii = 0; ii < R; ++ii) {
-        if (active) store_nt(pe0 + (size_t)b * bs_e + (size_t)ii * a.ldj, E[ii]);
-        E[ii] = En[ii];
-      }
-      if constexpr (ALIF) {
-#pragma unroll
-        for (int ii = 0; ii < R; ++ii) {
-          if (has_a) store_nt(pa0 + (size_t)b * bs_a + (size_t)ii * a.lda, Aa[ii]);
-          Aa[ii] = An[ii];
-        }
-      }
-    }
-    __syncthreads();   // every wave is done with this chunk's shared vectors
-    if (q + 1 < total) trace_stage_store<ROWS>(g, nnt, S);
-    __syncthreads();
-  }
-  if (active) {
-#pragma unroll
-    for (int ii = 0; ii < R; ++ii)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) a.acc[(size_t)(i0 + ii) * a.ldj + j0 + r] = acc[ii][r];
-  }
-}
-
-// Block index -> (row group of kRowPad rows, kind, segment): per group, two
-// adaptive workgroups of kRowPad/2 rows per adaptive segment, then one LIF
-// workgroup of kRowPad rows per LIF segment.
-template <bool FIRST>
-__global__ __launch_bounds__(kTraceWaves * 64) void trace_kernel(TraceArgs a) {
-  __shared__ TraceShared S;
-  const int per_group = 2 * a.n_seg_a + a.n_seg_l;
-  const int grp = blockIdx.x / per_group, k = blockIdx.x - grp * per_group;
-  if (k < 2 * a.n_seg_a)
-    trace_body<kRowPad / (2 * kTraceWaves), true, FIRST>(a, S, k >> 1,
-                                                         grp * kRowPad + (k & 1) * (kRowPad / 2));
+// blockIdx.x: tile in row-major order; blockIdx.y: batch split.  A tile
+// holding any adaptive neuron takes the three-contraction path.
+__global__ __launch_bounds__(256, 2) void trace_kernel(TraceArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float trace_smem[];
+  const int it = blockIdx.x / a.n_jt, jt = blockIdx.x - it * a.n_jt;
+  const bool first = a.first != 0;
+  if (jt < a.n_jt_a)
+    trace_tile_n<true>(a, trace_smem, it, jt, blockIdx.y, first);
   else
-    trace_body<kRowPad / kTraceWaves, false, FIRST>(a, S, a.n_seg_a + (k - 2 * a.n_seg_a),
-                                                    grp * kRowPad);
+    trace_tile_n<false>(a, trace_smem, it, jt, blockIdx.y, first);
 }
 
 // ---------------------------------------------------------------- gradient read-out
@@ -635,7 +764,10 @@ __global__ __launch_bounds__(256) void grads_kernel(GradsArgs a) {
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;   // 32 x 8
   for (int yy = ty; yy < 32; yy += 8) {
     const int i = i0 + yy, j = j0 + tx;
-    tile[yy][tx] = (a.valid && i < a.n_pre && j < a.n_post) ? a.acc[(size_t)i * a.ldj + j] : 0.0;
+    double v = 0.0;
+    if (a.valid && i < a.n_pre && j < a.n_post)
+      for (int sp = 0; sp < a.n_split; ++sp) v += a.acc[sp * a.acc_stride + (size_t)i * a.ldj + j];
+    tile[yy][tx] = v;
   }
   __syncthreads();
   for (int yy = ty; yy < 32; yy += 8) {
@@ -725,13 +857,24 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
   return hipGetLastError();
 }
 
+hipError_t launch_coef(const CoefArgs& a, hipStream_t s) {
+  dim3 grid(cdiv(a.n_post, 256), a.B);
+  coef_kernel<<<grid, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
 hipError_t launch_trace(const TraceArgs& a, hipStream_t s) {
-  const int groups = a.n_pre_pad / kRowPad;
-  const int grid = groups * (2 * a.n_seg_a + a.n_seg_l);
-  if (a.first)
-    trace_kernel<true><<<grid, kTraceWaves * 64, 0, s>>>(a);
-  else
-    trace_kernel<false><<<grid, kTraceWaves * 64, 0, s>>>(a);
+  // more than 64 KiB of shared memory must be requested per kernel
+  static bool granted = false;
+  if (!granted) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&trace_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)kTraceSmem);
+    if (e != hipSuccess) return e;
+    granted = true;
+  }
+  dim3 grid((a.n_pre_pad / kTile) * a.n_jt, a.n_split);
+  trace_kernel<<<grid, 256, kTraceSmem, s>>>(a);
   return hipGetLastError();
 }
 

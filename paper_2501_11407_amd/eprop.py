@@ -3,7 +3,8 @@
 Argument marshalling only: every step of the hot path runs in the HIP kernels
 of libeprop.so.  PyTorch supplies device memory (the workspace, inputs and
 outputs are CUDA/HIP tensors) and the current stream.  There is no CPU
-fallback: without the built library or a GPU the calls raise.
+fallback: without the built library or a GPU the calls raise.  EPROP_LIB
+names another build of the same library (for comparing kernel variants).
 """
 from __future__ import annotations
 
@@ -13,7 +14,8 @@ from typing import List, Optional, Sequence, Tuple
 
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libeprop.so")
+LIB_PATH = os.environ.get("EPROP_LIB") or \
+    os.path.join(os.path.dirname(os.path.abspath(__file__)), "libeprop.so")
 
 EPROP_OK, EPROP_EINVAL, EPROP_ENOSPACE, EPROP_EDEVICE, EPROP_ESTATE = 0, -1, -2, -3, -4
 

@@ -3,6 +3,7 @@
 Spike trains must be bit-identical; gradients (fp32 HIP path, fp64 oracle)
 within relative L2 1e-4 per tensor; the loss within 1e-4 relative.
 """
+import gc
 import math
 
 import numpy as np
@@ -243,9 +244,11 @@ def test_error_codes_on_device():
 def test_device_memory_does_not_grow_with_sequence_length():
     shape = synth.WORKLOADS["rlif_b32_n256_t250"]
     used = {}
+    ws = eprop.eprop_workspace_bytes(eprop.make_config(shape))
     for T in (50, 400):
         wl = synth.make_workload(shape, 2, T=T)
         x, labels = to_dev(wl)
+        gc.collect()        # contexts of earlier tests must not be freed mid-measurement
         torch.cuda.synchronize()
         torch.cuda.reset_peak_memory_stats()
         base = torch.cuda.memory_allocated()
@@ -257,3 +260,4 @@ def test_device_memory_does_not_grow_with_sequence_length():
         ctx.close()
         del ctx, x
     assert used[50] == used[400], used
+    assert ws <= used[50] <= ws + (8 << 20), (used, ws)
