@@ -9,9 +9,10 @@ synthetic data already resident in HBM when the clock starts.
 
 Prints one JSON line: synapse-timestep updates per second
 (sum over layers of B * N_pre * N_post * T per second), the roofline of the
-eligibility kernel, which dominates the step (algorithmic fp32 operations per
-launch over its measured duration, from HIP events on its stream; its HBM
-bytes alongside), and the CPU oracle timed on a bounded sample on this host.
+eligibility kernel, which dominates the step (algorithmic fp32 matrix
+operations per launch over its measured duration, from HIP events on its
+stream, against the fp32 MFMA peak; its algorithmic HBM bytes alongside), and
+the CPU oracle timed on a bounded sample on this host.
 
 Counter runs: `--calibrate-copy MIB` adds device-to-device copies of a known
 size after the timed steps, so that FETCH_SIZE/WRITE_SIZE of the eligibility
@@ -32,7 +33,7 @@ if ROOT not in sys.path:
 
 WORKLOAD = "ralif_b128_n1024_t1000"
 HBM_PEAK_GBS = 8000.0
-FP32_VECTOR_PEAK_TFLOPS = 157.3    # MI355X published fp32 vector peak
+FP32_MATRIX_PEAK_TFLOPS = 157.3    # MI355X published dense fp32 matrix (MFMA) peak
 COPY_KERNEL = "copyBuffer"
 COUNTERS = os.path.join(ROOT, "profiles", "trace_kernel_counters.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2501_11407_amd", "csrc", "kernels.hip")
@@ -41,25 +42,26 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2501_11407_amd", "csrc", "kernels.hip")
 def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: int) -> int:
     """Algorithmic HBM bytes of eligibility-kernel launches on one layer.
     Per launch: ebar (every synapse) and eps^a (synapses onto adaptive
-    neurons) read once and written once, the fp64 accumulator of every (i, j)
-    read and written once; the first launch after a reset reads neither.  Per
-    timestep covered: the filtered presynaptic vector [N_pre, B] and psi, L
-    [B, N_post] read once."""
+    neurons) read once and written once, one fp64 gradient accumulator of
+    every (i, j) read and written once; the first launch after a reset reads
+    neither.  Per timestep covered, the operands read once: the filtered
+    presynaptic vector [B, N_pre], the coefficients U, H [B, N] and V
+    [B, N_adaptive]; per launch the four scalars c, q, P, D [B, N]."""
     B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
     npre = shape.n_pre(layer)
     trace = 4 * B * npre * (N + NA) + 8 * npre * N      # one direction
-    return (2 * launches - first_launches) * trace + steps * 4 * (B * npre + 2 * B * N)
+    operands = steps * 4 * B * (npre + 2 * N + NA) + launches * 4 * 4 * B * N
+    return (2 * launches - first_launches) * trace + operands
 
 
 def trace_flops(shape, layer: int, steps: int) -> int:
-    """Algorithmic fp32 operations of the eligibility recursion per covered
-    timestep (a fused multiply-add counts 2): LIF synapse psi*zbar (1),
-    ebar = kappa*ebar + e (2), acc += L*ebar (2): 5; adaptive synapse adds
-    e = psi*zbar - (psi*beta)*epsa (2) and epsa = (rho - beta*psi)*epsa +
-    psi*zbar (2): 9."""
+    """Algorithmic fp32 matrix operations of the eligibility kernel: per
+    covered timestep and synapse, one multiply-add (2 operations) in each of
+    the contractions over the block's steps -- C_U and C_H for every
+    synapse, C_V as well for synapses onto adaptive neurons."""
     B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
     npre = shape.n_pre(layer)
-    return steps * B * npre * (5 * (N - NA) + 9 * NA)
+    return steps * B * npre * 2 * (2 * N + NA)
 
 
 def source_digest() -> str:
@@ -92,7 +94,7 @@ def summarize_counters(fetch_dir: str, write_dir: str, copy_mib: int) -> dict:
         for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             rows += list(csv.DictReader(open(f)))
         trace = [float(r["Counter_Value"]) for r in rows
-                 if r["Counter_Name"] == counter and "trace_kernel<false>" in r["Kernel_Name"]]
+                 if r["Counter_Name"] == counter and "trace_kernel(" in r["Kernel_Name"]]
         copies = [r for r in rows if r["Counter_Name"] == counter and COPY_KERNEL in r["Kernel_Name"]]
         big = max(int(r["Grid_Size"]) for r in copies)      # the calibration copies, not small ones
         copy = [float(r["Counter_Value"]) for r in copies if int(r["Grid_Size"]) == big]
@@ -105,7 +107,7 @@ def summarize_counters(fetch_dir: str, write_dir: str, copy_mib: int) -> dict:
     w_scale = copy_kib / (sum(write_c) / len(write_c))
     fetch = sum(fetch_t) / len(fetch_t) * 1024.0 * f_scale
     write = sum(write_t) / len(write_t) * 1024.0 * w_scale
-    out = {"workload": WORKLOAD, "kernel": "trace_kernel<false>",
+    out = {"workload": WORKLOAD, "kernel": "trace_kernel",
            "kernel_source_sha256": source_digest(),
            "dispatches": len(fetch_t), "fetch_bytes_per_launch": round(fetch),
            "write_bytes_per_launch": round(write), "hbm_bytes_per_launch": round(fetch + write),
@@ -196,8 +198,8 @@ def main():
     alg_flops = sum(trace_flops(shape, l, args.steps * shape.T) for l in range(shape.n_layers))
     sec = trace_ms * 1e-3
     achieved = alg_flops / sec / 1e12
-    roofline = {"bound": "alu", "achieved": round(achieved, 2), "peak": FP32_VECTOR_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / FP32_VECTOR_PEAK_TFLOPS, 4),
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": FP32_MATRIX_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / FP32_MATRIX_PEAK_TFLOPS, 4),
                 "traffic": stored_traffic(shape),
                 "kernel": "trace_kernel", "avg_launch_us": round(trace_ms * 1e3 / n_timed, 2),
                 "steps_per_launch": round(timed_steps / n_timed, 2),

@@ -55,6 +55,8 @@ struct Layer {
   // per-block vectors, two slots: the forward of block k+1 fills one while
   // the eligibility pass of block k reads the other
   float *psiK[2], *LK[2], *zbarK[2], *deltaK[2], *ztK[2];
+  // block coefficients of the eligibility recursion (same two slots)
+  float *coefU[2], *coefV[2], *coefH[2], *coefS[2];
   float* Cpart;
   double *acc, *accout;                  // gradient accumulators (acc: n_split partials)
   int n_split = 1;                       // batch splits of the eligibility kernel
@@ -67,9 +69,6 @@ struct Plan {
   std::vector<Layer> layers;
   int* err_flag = nullptr;
   int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, ldc = 0, jlist = 0, out_splits = 1;
-  // block coefficients of the eligibility recursion, shared by the layers
-  // (they are processed one after the other on one stream)
-  float *coefU = nullptr, *coefV = nullptr, *coefH = nullptr, *coefS = nullptr;
   size_t smem = 0;
   size_t bytes = 0;
 };
@@ -165,11 +164,15 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.ebar = (float*)take(sizeof(float) * B * npp * ldc);
     L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * lda_t : 0);
   }
-  const size_t ldc = plan->ldc;
-  plan->coefU = (float*)take(sizeof(float) * B * ldc * KM);
-  plan->coefV = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * ldc * KM : 0);
-  plan->coefH = (float*)take(sizeof(float) * B * ldc * KM);
-  plan->coefS = (float*)take(sizeof(float) * 4 * B * ldc);
+  for (Layer& L : plan->layers) {
+    const size_t ldc = plan->ldc;
+    for (int sl = 0; sl < 2; ++sl) {
+      L.coefU[sl] = (float*)take(sizeof(float) * B * ldc * KM);
+      L.coefV[sl] = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * ldc * KM : 0);
+      L.coefH[sl] = (float*)take(sizeof(float) * B * ldc * KM);
+      L.coefS[sl] = (float*)take(sizeof(float) * 4 * B * ldc);
+    }
+  }
   const size_t npad4 = round_up(N, 4);
   size_t npre_max = 0;
   for (const Layer& L : plan->layers) npre_max = std::max<size_t>(npre_max, L.n_pre);
@@ -297,18 +300,19 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
   fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem;
   if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
-  if ((rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
-  if ((rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
 
+  // On the forward stream, per layer: learning signal, readout gradient and
+  // the block coefficients of the eligibility recursion.
   const int rows = steps * P.Bp;
+  const int kpad = (int)round_up(steps, 16);
   for (int l = 0; l < c.n_layers; ++l) {
-    const Layer& L = P.layers[l];
+    Layer& L = ctx->plan.layers[l];
     // learning signal L[(t,b)][j] = sum_k delta[(t,b)][k] W_out[k][j]
     eprop::GemmArgs gl;
     gl.A = L.deltaK[sl]; gl.Bm = L.WoutT; gl.C = L.LK[sl];
     gl.M = rows; gl.N = c.n_rec; gl.K = P.ldk; gl.lda = P.ldk; gl.ldb = P.ldk; gl.ldc = L.ldv;
     gl.splits = 1; gl.k_chunk = P.ldk; gl.split_stride = 0;
-    if ((rc = check(ctx, eprop::launch_gemm_nt(gl, s), "learning-signal GEMM"))) return rc;
+    if ((rc = check(ctx, eprop::launch_gemm_nt(gl, sf), "learning-signal GEMM"))) return rc;
 
     // dW_out += sum over (t, b) of delta (x) ztilde, then fp64 accumulation
     eprop::GemmArgs g;
@@ -316,26 +320,33 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     g.M = c.n_out; g.N = c.n_rec; g.K = rows; g.lda = P.ldk; g.ldb = P.ldn; g.ldc = c.n_rec;
     choose_splits(g.M, g.N, g.K, P.out_splits, &g.splits, &g.k_chunk);
     g.split_stride = (size_t)c.n_out * c.n_rec;
-    if ((rc = check(ctx, eprop::launch_gemm_tn(g, s), "readout gradient GEMM"))) return rc;
+    if ((rc = check(ctx, eprop::launch_gemm_tn(g, sf), "readout gradient GEMM"))) return rc;
     if ((rc = check(ctx, eprop::launch_accumulate(L.Cpart, g.splits, g.split_stride, c.n_out,
-                                                  c.n_rec, L.accout, L.ldj, first, s),
+                                                  c.n_rec, L.accout, L.ldj, first, sf),
                     "readout gradient accumulation")))
       return rc;
 
-    const int kpad = (int)round_up(steps, 16);
     eprop::CoefArgs ca;
     ca.psiK = L.psiK[sl]; ca.LK = L.LK[sl]; ca.ldv = L.ldv; ca.Bp = P.Bp;
-    ca.U = P.coefU; ca.V = c.n_adaptive > 0 ? P.coefV : nullptr; ca.H = P.coefH; ca.S = P.coefS;
+    ca.U = L.coefU[sl]; ca.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ca.H = L.coefH[sl];
+    ca.S = L.coefS[sl];
     ca.B = c.batch; ca.n_post = c.n_rec; ca.n_adaptive = c.n_adaptive;
     ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(c.n_adaptive, eprop::kTile));
     ca.steps = steps; ca.kpad = kpad; ca.ldc = P.ldc;
     ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta;
-    if ((rc = check(ctx, eprop::launch_coef(ca, s), "eligibility coefficient kernel"))) return rc;
+    if ((rc = check(ctx, eprop::launch_coef(ca, sf), "eligibility coefficient kernel"))) return rc;
+  }
+  if ((rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
+  if ((rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
 
+  // On the caller's stream: the eligibility pass of every layer.
+  for (int l = 0; l < c.n_layers; ++l) {
+    const Layer& L = P.layers[l];
     eprop::TraceArgs ta;
     ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
     ta.n_split = L.n_split; ta.zbarK = L.zbarK[sl];
-    ta.U = P.coefU; ta.V = ca.V; ta.H = P.coefH; ta.S = P.coefS;
+    ta.U = L.coefU[sl]; ta.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
+    ta.S = L.coefS[sl];
     ta.B = c.batch; ta.n_pre_pad = L.n_pre_pad; ta.n_post = c.n_rec; ta.ldj = L.ldj;
     ta.n_adaptive = c.n_adaptive; ta.ldi = L.n_pre_pad;
     ta.n_jt = (c.n_rec + eprop::kTile - 1) / eprop::kTile;

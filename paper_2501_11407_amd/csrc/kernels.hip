@@ -110,7 +110,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // 2. drive and neuron step.  Rows of Wt are padded to a multiple of the
   // workgroup size; chunks q with q*kFwdThreads >= n_rec are skipped (QN is
   // rounded up to a power of two).  UB rows are loaded before any is added.
-  constexpr int UB = QN >= 16 ? 1 : 16 / QN;
+  constexpr int UB = QN >= 32 ? 1 : 32 / QN;
   const int total = S.cnt[2 * kFwdWaves];
   float I[QN];
 #pragma unroll
@@ -246,29 +246,29 @@ __device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S,
   }
 }
 
-template <int QN>
+template <int QN, int NL>
 __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs A) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int b = blockIdx.x;
   FwdLds S;
   S.rwmax = A.L[0].rows_per_wave;
-  if (A.n_layers > 1) S.rwmax = max(S.rwmax, A.L[1].rows_per_wave);
+  if constexpr (NL > 1) S.rwmax = max(S.rwmax, A.L[1].rows_per_wave);
   S.npad = (A.n_rec + 3) & ~3;
-  const int npre_max = max(A.L[0].n_pre, A.n_layers > 1 ? A.L[1].n_pre : 0);
+  const int npre_max = max(A.L[0].n_pre, NL > 1 ? A.L[1].n_pre : 0);
   S.act = (int*)smem;                          // [waves][rwmax]
   S.mrg = S.act + kFwdWaves * S.rwmax;         // [npre_max]
   S.spk = S.mrg + npre_max;                    // [waves][jlist]
   S.cnt = S.spk + kFwdWaves * A.jlist;         // [2 * waves + 2]
   S.part = (float*)(S.cnt + 2 * kFwdWaves + 2);   // [waves][K_out]
   S.sy = S.part + kFwdWaves * A.K_out;         // [n_layers][K_out]
-  S.szb = S.sy + A.n_layers * A.K_out;         // [n_pre_0 + n_pre_1]
-  const int npre_total = A.L[0].n_pre + (A.n_layers > 1 ? A.L[1].n_pre : 0);
+  S.szb = S.sy + NL * A.K_out;                 // [n_pre_0 + n_pre_1]
+  const int npre_total = A.L[0].n_pre + (NL > 1 ? A.L[1].n_pre : 0);
   S.zc = (uint8_t*)(S.szb + npre_total);       // [n_layers][2][npad]
-  S.xs = S.zc + A.n_layers * 2 * S.npad;       // [kFwdXSteps][n_in]
+  S.xs = S.zc + NL * 2 * S.npad;               // [kFwdXSteps][n_in]
 
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
   forward_state<QN, 0>(A, S, b, true, v0, a0, zt0, 0);
-  if (A.n_layers > 1) forward_state<QN, 1>(A, S, b, true, v1, a1, zt1, 0);
+  if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, true, v1, a1, zt1, 0);
   double loss0 = 0.0, loss1 = 0.0;
   int cur = 0;
   __syncthreads();
@@ -286,14 +286,14 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs A) {
       __syncthreads();
     }
     forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0);
-    if (A.n_layers > 1) forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1);
+    if constexpr (NL > 1) forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1);
     cur ^= 1;
   }
   forward_state<QN, 0>(A, S, b, false, v0, a0, zt0, cur);
-  if (A.n_layers > 1) forward_state<QN, 1>(A, S, b, false, v1, a1, zt1, cur);
+  if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, false, v1, a1, zt1, cur);
   if (threadIdx.x == 0) {
     A.L[0].lossacc[b] += loss0;
-    if (A.n_layers > 1) A.L[1].lossacc[b] += loss1;
+    if constexpr (NL > 1) A.L[1].lossacc[b] += loss1;
   }
 }
 
@@ -544,15 +544,20 @@ __device__ __forceinline__ void dma16(const float* g, float* lds) {
 
 template <bool ALIF, int NCH>
 struct TraceTile {
-  static constexpr int D = NCH < kPrefetch ? NCH : kPrefetch;   // chunks in flight ahead
-  static constexpr int Q = ALIF ? 4 : 3;     // copies per wave per chunk
-  static constexpr int QB = 1 + (ALIF ? 8 : 4);   // + scalars and trace loads with chunk 0
-  static constexpr int ops(int c) { return Q + (c == 0 ? QB : 0); }
-  // vector-memory operations issued after the copies of chunk ch (> 0) when
-  // it is waited for: those of chunks ch+1 .. ch+D-1, the ones past the end
-  // of the batch element belonging to the next one (if there is one).
+  // chunks in flight ahead; fewer than NCH so that a batch element's copies
+  // never reach past the next element's first chunk
+  static constexpr int D = NCH == 1 ? 1 : (NCH - 1 < kPrefetch ? NCH - 1 : kPrefetch);
+  static constexpr int Q = ALIF ? 4 : 3;            // copies per wave per chunk
+  static constexpr int EA = ALIF ? 8 : 4;           // trace loads per wave per batch element
+  static constexpr int ops(int c) { return Q + (c == 0 ? 1 : 0); }   // + scalars with chunk 0
+  // Loads issued after those of chunk ch when it is waited for: the copies
+  // of chunks ch+1 .. ch+D-1 (past the end of the batch element: the next
+  // element's, if there is one), and the element's trace loads when they
+  // were issued in between (at chunk 0, after that chunk's copies).  Loads
+  // complete in order, so at most that many outstanding operations means
+  // chunk ch has landed, whatever stores are still in flight.
   static constexpr int pending(int ch, bool next) {
-    int n = 0;
+    int n = (ch >= 1 && ch <= D) ? EA : 0;
     for (int m = ch + 1; m <= ch + D - 1; ++m) n += m < NCH ? ops(m) : (next ? ops(m - NCH) : 0);
     return n;
   }
@@ -585,10 +590,9 @@ struct TraceTile {
   }
 
   // Copies of chunk c of batch element b into ring slot sl (this wave: quad
-  // 4c + w of each operand).  With chunk 0 also the scalars (plane w) into
-  // scalar buffer par and the block-start traces into E/A.
-  __device__ __forceinline__ void issue(int b, int c, int sl, int par, f32x4 (&E)[2][2],
-                                        f32x4 (&A)[2][2]) const {
+  // 4c + w of each operand); with chunk 0 also the scalars (plane w) into
+  // scalar buffer par.
+  __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
     float* slot = sm + sl * kSlot;
     const size_t qd = (size_t)b * kKQ + kChunkQuads * c + w;
     dma16(a.zbarK + (qd * a.ldi + i0) * 4 + lane * 4, slot + (0 * kChunkQuads + w) * kTile * 4);
@@ -596,79 +600,29 @@ struct TraceTile {
     dma16(a.H + (qd * a.ldc + j0) * 4 + lane * 4, slot + (2 * kChunkQuads + w) * kTile * 4);
     if constexpr (ALIF)
       dma16(a.V + (qd * a.ldc + j0) * 4 + lane * 4, slot + (3 * kChunkQuads + w) * kTile * 4);
-    if (c == 0) {
-      if (lane < 16)
-        dma16(a.S + ((size_t)w * a.B + b) * a.ldc + j0 + lane * 4,
-              sm + kRing * kSlot + par * kScal + w * kTile);
-      const auto eR = ebar_rsrc(b);
+    if (c == 0 && lane < 16)
+      dma16(a.S + ((size_t)w * a.B + b) * a.ldc + j0 + lane * 4,
+            sm + kRing * kSlot + par * kScal + w * kTile);
+  }
+
+  // block-start traces of batch element b into E/A
+  __device__ __forceinline__ void load_traces(int b, f32x4 (&E)[2][2], f32x4 (&A)[2][2]) const {
+    const auto eR = ebar_rsrc(b);
 #pragma unroll
-      for (int x = 0; x < 4; ++x) E[x >> 1][x & 1] = bload(eR, x * 1024u + lane * 16u);
-      if constexpr (ALIF) {
-        const auto aR = epsa_rsrc(b);
+    for (int x = 0; x < 4; ++x) E[x >> 1][x & 1] = bload(eR, x * 1024u + lane * 16u);
+    if constexpr (ALIF) {
+      const auto aR = epsa_rsrc(b);
 #pragma unroll
-        for (int x = 0; x < 4; ++x) A[x >> 1][x & 1] = bload(aR, x * 1024u + lane * 16u);
-      }
+      for (int x = 0; x < 4; ++x) A[x >> 1][x & 1] = bload(aR, x * 1024u + lane * 16u);
     }
   }
 
-  // One batch element (k-th of the split): its traces are in E/A; the next
-  // one's arrive in En/An.
-  __device__ __forceinline__ void batch(int k, int nk, f32x4 (&E)[2][2], f32x4 (&A)[2][2],
-                                        f32x4 (&En)[2][2], f32x4 (&An)[2][2],
-                                        f32x4 (&gacc)[2][2]) const {
+  // traces and gradient of the k-th batch element from its contractions
+  __device__ __forceinline__ void finish(int k, const f32x4 (&E)[2][2], const f32x4 (&A)[2][2],
+                                         const f32x4 (&cU)[2][2], const f32x4 (&cV)[2][2],
+                                         const f32x4 (&cH)[2][2], f32x4 (&gacc)[2][2]) const {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     const int b = split + k * a.n_split;
-    const bool next = k + 1 < nk;
-    f32x4 cU[2][2], cV[2][2], cH[2][2];
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-        cU[bj][bi] = zero;
-        cV[bj][bi] = zero;
-        cH[bj][bi] = zero;
-      }
-    auto chunk = [&](auto chc) {
-      constexpr int ch = decltype(chc)::value;
-      const int n = k * NCH + ch;
-      if constexpr (ch == 0)
-        __builtin_amdgcn_s_waitcnt(vm_wait(0));
-      else if (next)
-        __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, true)));
-      else
-        __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, false)));
-      wg_barrier();   // chunk n is in shared memory; slot (n - 1) % kRing is free
-      constexpr int c2 = ch + D;
-      if constexpr (c2 < NCH)
-        issue(b, c2, (n + D) % kRing, k & 1, En, An);
-      else if (next)
-        issue(b + a.n_split, c2 - NCH, (n + D) % kRing, (k + 1) & 1, En, An);
-
-      const float* slot = sm + (n % kRing) * kSlot;
-      f32x4 z[2], u[2], h[2], v[2];
-#pragma unroll
-      for (int x = 0; x < 2; ++x) {
-        z[x] = *(const f32x4*)(slot + ((0 * kChunkQuads + g) * kTile + 32 * wi + 16 * x + r) * 4);
-        u[x] = *(const f32x4*)(slot + ((1 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4);
-        h[x] = *(const f32x4*)(slot + ((2 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4);
-        v[x] = ALIF ? *(const f32x4*)(slot + ((3 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4)
-                    : zero;
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-          for (int bi = 0; bi < 2; ++bi) {
-            cU[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(u[bj][q], z[bi][q], cU[bj][bi], 0, 0, 0);
-            cH[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[bj][q], z[bi][q], cH[bj][bi], 0, 0, 0);
-            if constexpr (ALIF)
-              cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(v[bj][q], z[bi][q], cV[bj][bi], 0, 0, 0);
-          }
-    };
-    for_each_index(chunk, std::make_integer_sequence<int, NCH>{});
-
-    // traces and gradient of batch element b
     const float* st = sm + kRing * kSlot + (k & 1) * kScal;   // [4][64]: c, q, P, D
     const auto eR = ebar_rsrc(b);
     const auto aR = ALIF ? epsa_rsrc(b) : eR;
@@ -700,17 +654,68 @@ struct TraceTile {
   __device__ __forceinline__ void run() const {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     const int nk = (a.B - split + a.n_split - 1) / a.n_split;
-    f32x4 gacc[2][2];
+    f32x4 gacc[2][2], cU[2][2], cV[2][2], cH[2][2], E[2][2], A[2][2];
 #pragma unroll
-    for (int x = 0; x < 4; ++x) gacc[x >> 1][x & 1] = zero;
-    f32x4 Ea[2][2], Aa[2][2], Eb[2][2], Ab[2][2];
-#pragma unroll
-    for (int c = 0; c < D; ++c) issue(split, c, c, 0, Ea, Aa);
-    for (int k = 0; k < nk; k += 2) {
-      batch(k, nk, Ea, Aa, Eb, Ab, gacc);
-      if (k + 1 >= nk) break;
-      batch(k + 1, nk, Eb, Ab, Ea, Aa, gacc);
+    for (int x = 0; x < 4; ++x) {
+      gacc[x >> 1][x & 1] = zero;
+      cU[x >> 1][x & 1] = cV[x >> 1][x & 1] = cH[x >> 1][x & 1] = zero;
+      E[x >> 1][x & 1] = A[x >> 1][x & 1] = zero;
     }
+#pragma unroll
+    for (int c = 0; c < D; ++c) issue(split, c, c, 0);
+    for (int k = 0; k < nk; ++k) {
+      const int b = split + k * a.n_split;
+      const bool next = k + 1 < nk;
+      auto chunk = [&](auto chc) {
+        constexpr int ch = decltype(chc)::value;
+        const int n = k * NCH + ch;
+        if (next)
+          __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, true)));
+        else
+          __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, false)));
+        wg_barrier();   // chunk n is in shared memory; slot (n - 1) % kRing is free
+        if constexpr (ch == 0) {
+          // element k-1 is finished now: its stores overlap this chunk's MFMAs
+          if (k > 0) finish(k - 1, E, A, cU, cV, cH, gacc);
+#pragma unroll
+          for (int x = 0; x < 4; ++x) cU[x >> 1][x & 1] = cV[x >> 1][x & 1] = cH[x >> 1][x & 1] = zero;
+          // with D == NCH the next copies overwrite what finish() just read
+          if constexpr (D == NCH) wg_barrier();
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        constexpr int c2 = ch + D;
+        if constexpr (c2 < NCH)
+          issue(b, c2, (n + D) % kRing, k & 1);
+        else if (next)
+          issue(b + a.n_split, c2 - NCH, (n + D) % kRing, (k + 1) & 1);
+        if constexpr (ch == 0) load_traces(b, E, A);
+
+        const float* slot = sm + (n % kRing) * kSlot;
+        f32x4 z[2], u[2], h[2], v[2];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+          z[x] = *(const f32x4*)(slot + ((0 * kChunkQuads + g) * kTile + 32 * wi + 16 * x + r) * 4);
+          u[x] = *(const f32x4*)(slot + ((1 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4);
+          h[x] = *(const f32x4*)(slot + ((2 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4);
+          v[x] = ALIF ? *(const f32x4*)(slot + ((3 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4)
+                      : zero;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+            for (int bi = 0; bi < 2; ++bi) {
+              cU[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(u[bj][q], z[bi][q], cU[bj][bi], 0, 0, 0);
+              cH[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[bj][q], z[bi][q], cH[bj][bi], 0, 0, 0);
+              if constexpr (ALIF)
+                cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(v[bj][q], z[bi][q], cV[bj][bi], 0, 0, 0);
+            }
+      };
+      for_each_index(chunk, std::make_integer_sequence<int, NCH>{});
+    }
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));   // the last element's traces
+    finish(nk - 1, E, A, cU, cV, cH, gacc);
     // the split's fp64 accumulator (row-major [n_pre_pad][ldj])
     const int iw = i0 + 32 * wi, jw = j0 + 32 * wj;
     double* accp = a.acc + (size_t)split * a.acc_stride;
@@ -813,28 +818,28 @@ __global__ __launch_bounds__(256) void pack_kernel(const float* src, int rows, i
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
-template <int QN>
+template <int QN, int NL>
 hipError_t launch_forward_qn(const FwdArgs& a, hipStream_t s) {
   // gfx950 gives a workgroup up to the whole 160 KiB of shared memory, but
   // more than 64 KiB must be requested per kernel.
   static size_t granted = 64 * 1024;
   if (a.smem > granted) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&forward_kernel<QN>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&forward_kernel<QN, NL>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.smem);
     if (e != hipSuccess) return e;
     granted = a.smem;
   }
-  forward_kernel<QN><<<a.B, kFwdThreads, a.smem, s>>>(a);
+  forward_kernel<QN, NL><<<a.B, kFwdThreads, a.smem, s>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s) {
   const int qn = (a.n_rec + kFwdThreads - 1) / kFwdThreads;
-  if (qn <= 1) return launch_forward_qn<1>(a, s);
-  if (qn <= 2) return launch_forward_qn<2>(a, s);
-  if (qn <= 4) return launch_forward_qn<4>(a, s);
-  if (qn <= 8) return launch_forward_qn<8>(a, s);
-  if (qn <= 16) return launch_forward_qn<16>(a, s);
+  if (qn <= 1) return a.n_layers > 1 ? launch_forward_qn<1, 2>(a, s) : launch_forward_qn<1, 1>(a, s);
+  if (qn <= 2) return a.n_layers > 1 ? launch_forward_qn<2, 2>(a, s) : launch_forward_qn<2, 1>(a, s);
+  if (qn <= 4) return a.n_layers > 1 ? launch_forward_qn<4, 2>(a, s) : launch_forward_qn<4, 1>(a, s);
+  if (qn <= 8) return a.n_layers > 1 ? launch_forward_qn<8, 2>(a, s) : launch_forward_qn<8, 1>(a, s);
+  if (qn <= 16) return a.n_layers > 1 ? launch_forward_qn<16, 2>(a, s) : launch_forward_qn<16, 1>(a, s);
   return hipErrorInvalidValue;
 }
 

@@ -37,7 +37,8 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
                      for l in range(shape.n_layers))
         # per-step vectors for two blocks of at most 128 steps (one being
         # written by the forward pass while the other is read), plus one
-        # block's eligibility coefficients (three per neuron and step)
+        # block's eligibility coefficients per layer and slot (three per neuron
+        # and step)
         bp = -(-shape.batch // 16) * 16
         nv = -(-shape.n_rec // 256) * 256
         per_step = sum(4 * (2 * bp * nv + (shape.n_pre(l) + 63) * shape.batch
@@ -46,7 +47,8 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
         coef = 4 * 3 * shape.batch * (shape.n_rec + 63)
         # at most 8 fp64 partial gradient accumulators (batch splits) per layer
         partial = sum(8 * 8 * (shape.n_pre(l) + 63) * shape.n_rec for l in range(shape.n_layers))
-        assert traces <= n <= traces * 1.05 + 2 * 128 * per_step + 128 * coef + partial + (16 << 20), \
+        assert traces <= n <= (traces * 1.05 + 2 * 128 * per_step + 2 * shape.n_layers * 128 * coef
+                               + partial + (16 << 20)), \
             (name, n, traces)
     # the same shape with any T needs the same workspace: T is not an input
     s = synth.WORKLOADS["ralif_b64_n512_t500"]
