@@ -20,11 +20,13 @@ thread_local std::string g_last_error = "";
 
 size_t round_up(size_t v, size_t m) { return (v + m - 1) / m * m; }
 
-// Split-K choice for a GEMM of M x N over K (multiple of 16): enough waves
-// to cover the chip (~1024), at most max_splits, chunks a multiple of 16.
+// Split-K choice for a GEMM of M x N over K (multiple of 16): about 4096
+// waves (four per SIMD: the k loop is latency-bound), at most max_splits,
+// chunks a multiple of 16.
+constexpr int kMaxOutSplits = 64;
 void choose_splits(int M, int N, int K, int max_splits, int* splits, int* k_chunk) {
   const long long tiles = (long long)((M + 31) / 32) * ((N + 31) / 32);
-  long long want = std::max<long long>(1, (1024 + tiles - 1) / tiles);
+  long long want = std::max<long long>(1, (4096 + tiles - 1) / tiles);
   want = std::min<long long>(want, std::max(1, K / 16));
   want = std::min<long long>(want, max_splits);
   int kc = (int)round_up((K + want - 1) / want, 16);
@@ -54,9 +56,13 @@ struct Layer {
   double* lossacc;                       // [B]
   // per-block vectors, two slots: the forward of block k+1 fills one while
   // the eligibility pass of block k reads the other
-  float *psiK[2], *LK[2], *zbarK[2], *deltaK[2], *ztK[2];
-  // block coefficients of the eligibility recursion (same two slots)
-  float *coefU[2], *coefV[2], *coefH[2], *coefS[2];
+  float *psiK[2], *LK[2], *deltaK[2], *ztK[2];
+  // the filtered presynaptic values as scaled fp16 pairs, and the block
+  // coefficients of the eligibility recursion (same two slots)
+  uint32_t* z16[2];
+  uint32_t *coefU[2], *coefV[2], *coefH[2];
+  float* coefS[2];
+  float zscale = 1.0f;                   // power of two: zbar * zscale < 2^15
   float* Cpart;
   double *acc, *accout;                  // gradient accumulators (acc: n_split partials)
   int n_split = 1;                       // batch splits of the eligibility kernel
@@ -93,6 +99,10 @@ bool valid_config(const eprop_config* c, std::string* why) {
   for (float v : k)
     if (!std::isfinite(v)) { *why = "constants must be finite"; return false; }
   if (!(c->thr > 0.0f)) { *why = "thr must be > 0"; return false; }
+  if (!(c->alpha >= 0.0f && c->alpha < 1.0f)) {
+    *why = "alpha must be in [0, 1) (the presynaptic filter must be bounded)";
+    return false;
+  }
   return true;
 }
 
@@ -116,7 +126,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   plan->jlist = (int)(round_up(N, eprop::kFwdThreads) / eprop::kFwdThreads * 64);
   {
     int dummy;
-    choose_splits(c.n_out, c.n_rec, (int)(KM * plan->Bp), 16, &plan->out_splits, &dummy);
+    choose_splits(c.n_out, c.n_rec, (int)(KM * plan->Bp), kMaxOutSplits, &plan->out_splits, &dummy);
   }
   const size_t R = plan->rows;
   plan->err_flag = (int*)take(sizeof(int));
@@ -146,7 +156,6 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     for (int sl = 0; sl < 2; ++sl) {
       L.psiK[sl] = (float*)take(sizeof(float) * R * L.ldv);
       L.LK[sl] = (float*)take(sizeof(float) * R * L.ldv);
-      L.zbarK[sl] = (float*)take(sizeof(float) * B * npp * KM);
       L.deltaK[sl] = (float*)take(sizeof(float) * R * plan->ldk);
       L.ztK[sl] = (float*)take(sizeof(float) * R * plan->ldn);
     }
@@ -167,10 +176,17 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   for (Layer& L : plan->layers) {
     const size_t ldc = plan->ldc;
     for (int sl = 0; sl < 2; ++sl) {
-      L.coefU[sl] = (float*)take(sizeof(float) * B * ldc * KM);
-      L.coefV[sl] = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * ldc * KM : 0);
-      L.coefH[sl] = (float*)take(sizeof(float) * B * ldc * KM);
-      L.coefS[sl] = (float*)take(sizeof(float) * 4 * B * ldc);
+      // a scaled fp16 pair per value: 4 bytes, as fp32
+      L.z16[sl] = (uint32_t*)take(sizeof(uint32_t) * B * L.n_pre_pad * KM);
+      L.coefU[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
+      L.coefV[sl] = (uint32_t*)take(c.n_adaptive > 0 ? sizeof(uint32_t) * B * ldc * KM : 0);
+      L.coefH[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
+      L.coefS[sl] = (float*)take(sizeof(float) * eprop::kScalarPlanes * B * ldc);
+    }
+    // zbar <= 1/(1-alpha): the largest power of two that keeps it below 2^15
+    {
+      const double zmax = 1.0 / (1.0 - (double)c.alpha);
+      L.zscale = (float)std::ldexp(1.0, (int)std::floor(std::log2(32768.0 / zmax)));
     }
   }
   const size_t npad4 = round_up(N, 4);
@@ -288,7 +304,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     const Layer& L = P.layers[std::min(l, c.n_layers - 1)];
     f.Wt = L.Wt; f.ldw = L.ldw; f.WoutT = L.WoutT;
     f.v = L.v; f.a = L.a; f.ztil = L.ztil; f.z = L.z; f.zbar = L.zbar; f.y = L.y;
-    f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.zbarK = L.zbarK[sl];
+    f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.z16 = L.z16[sl]; f.zscale = L.zscale;
     f.deltaK = L.deltaK[sl]; f.ztK = L.ztK[sl];
     f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.rows_per_wave = L.rows_per_wave; f.ldi = L.n_pre_pad;
   }
@@ -335,6 +351,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ca.steps = steps; ca.kpad = kpad; ca.ldc = P.ldc;
     ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta;
     if ((rc = check(ctx, eprop::launch_coef(ca, sf), "eligibility coefficient kernel"))) return rc;
+
   }
   if ((rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
   if ((rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
@@ -344,7 +361,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     const Layer& L = P.layers[l];
     eprop::TraceArgs ta;
     ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
-    ta.n_split = L.n_split; ta.zbarK = L.zbarK[sl];
+    ta.n_split = L.n_split; ta.z16 = L.z16[sl]; ta.zinv = 1.0f / L.zscale;
     ta.U = L.coefU[sl]; ta.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
     ta.S = L.coefS[sl];
     ta.B = c.batch; ta.n_pre_pad = L.n_pre_pad; ta.n_post = c.n_rec; ta.ldj = L.ldj;

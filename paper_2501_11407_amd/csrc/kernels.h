@@ -7,11 +7,13 @@
 //   psiK   [Kmax*Bp][ldv]  pseudo-derivative (ldv = n_rec rounded to 256)
 //   deltaK [rows][ldk]     readout error (softmax - onehot)
 //   ztK    [rows][ldn]     kappa-filtered spikes
-//   zbarK  [B][Kmax/4][ldi][4]  filtered presynaptic vector (4 steps contiguous)
+//   z16    [B][Kmax/16][ldi][16] filtered presynaptic vector as scaled fp16
+//                                 pairs, one 32-bit word per step (see below)
 // Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
-// psiK) and the readout gradient dW_out += deltaK^T * ztK.  The eligibility
-// kernel then advances every synapse's traces through the block's steps with
-// one read and one write of the traces.
+// psiK) and the readout gradient dW_out += deltaK^T * ztK; then the block
+// coefficients of the eligibility recursion and the eligibility kernel, which
+// advances every synapse's traces through the block's steps with one read and
+// one write of the traces.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -20,7 +22,7 @@
 
 namespace eprop {
 
-constexpr int kFwdThreads = 1024;              // forward workgroup: one batch element
+constexpr int kFwdThreads = 512;               // forward workgroup: one batch element
 constexpr int kFwdWaves = kFwdThreads / 64;
 constexpr int kFwdXSteps = 8;                  // input spikes staged in shared memory per load
 constexpr int kBlockSteps = 128;       // timesteps per block (Kmax)
@@ -38,7 +40,8 @@ struct FwdLayer {
   float* y;                      // state [B][K_out]
   double* lossacc;               // [B]
   float* psiK;                   // [rows][ldj]
-  float* zbarK;                  // [B][Kmax/4][ldi][4]
+  uint32_t* z16;                 // [B][Kmax/16][ldi][16]
+  float zscale;
   float* deltaK; float* ztK;     // [rows][ldk], [rows][ldn]
   int n_inl, n_pre, rows_per_wave, ldi;
 };
@@ -78,22 +81,28 @@ hipError_t launch_gemm_tn(const GemmArgs& a, hipStream_t s);
 hipError_t launch_accumulate(const float* part, int splits, size_t split_stride, int M, int N,
                              double* acc, int ld_acc, int first, hipStream_t s);
 
+// The operands of the eligibility contractions are stored as scaled fp16
+// pairs: a value x (times a power-of-two scale 2^e) is hi = fp16(x 2^e) plus
+// lo = fp16(x 2^e - hi), together about 22 significant bits, in one 32-bit
+// word (hi in the low half).  Per 16-step chunk and row, 16 words (64 bytes).
+constexpr int kChunk = 16;                     // steps per chunk
+constexpr int kKC = kBlockSteps / kChunk;      // chunks per block
+constexpr int kScalarPlanes = 8;               // c, q, P, D, 1/sU, 1/sH, 1/sV, unused
+
 // Block coefficients of the eligibility recursion, one thread per (b, j):
-// U, V, H [B][Kmax/4][ldc][4] (zero for steps <= s < kpad; V written for
-// j < n_vcols only, NULL when no neuron adapts) and the scalars c, q, P, D in
-// S [4][B][ldc].
+// U, V, H as scaled fp16 pair words [B][kKC][ldc][16] (zero for steps <=
+// s < kpad; V written for j < n_vcols only, NULL when no neuron adapts), each
+// row with its own power-of-two scale, and S [8][B][ldc]: c, q, P, D and the
+// inverse scales of U, H, V.
 struct CoefArgs {
   const float* psiK; const float* LK; int ldv, Bp;   // [t*Bp + b][ldv]
-  float* U; float* V; float* H; float* S;
+  uint32_t* U; uint32_t* V; uint32_t* H; float* S;
   int B, n_post, n_adaptive, n_vcols, steps, kpad, ldc;
   float kappa, rho, beta;
 };
 hipError_t launch_coef(const CoefArgs& a, hipStream_t s);
 
-// Eligibility vectors and gradient accumulation over a block of `steps`
-// timesteps, from the block coefficients.  The batch is split n_split ways;
-// split s accumulates the batch elements b = s (mod n_split) into its own
-// fp64 accumulator acc + s * acc_stride.
+
 // The traces are stored tile by tile: for batch element b and 64 x 64 tile
 // (it, jt), 16 KiB holding the four 32 x 32 wave sub-tiles, each as four
 // 16 x 16 blocks (bj, bi) of 64 lanes x 4 floats, in the order the kernel's
@@ -104,11 +113,12 @@ struct TraceArgs {
   float* epsa;     // [B][n_pre_pad / 64][n_jt_a][64 * 64]
   double* acc;     // [n_split][n_pre_pad][ldj] (row-major)
   size_t acc_stride;
-  const float* zbarK;                 // [B][Kmax/4][ldi][4], ldi = n_pre_pad
-  const float* U; const float* V; const float* H; const float* S;   // as CoefArgs
+  const uint32_t* z16;                // [B][kKC][ldi][16], ldi = n_pre_pad
+  const uint32_t* U; const uint32_t* V; const uint32_t* H; const float* S;   // as CoefArgs
   int B, n_pre_pad, n_post, ldj, n_adaptive, ldi, ldc, kpad, n_split;
   int n_jt, n_jt_a;   // tiles along j: all, and those holding adaptive neurons
   float kappa_K;   // kappa^steps
+  float zinv;      // 1 / zscale
   int first;       // 1: traces and accumulators start at zero (not read)
 };
 hipError_t launch_trace(const TraceArgs& a, hipStream_t s);

@@ -36,6 +36,42 @@ __device__ inline int lanes_below(unsigned long long m, int lane) {
 
 inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
+// ---------------------------------------------------------------- scaled fp16 pairs
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Power-of-two scale that puts a row's largest magnitude m in [2^13, 2^14)
+// (exponent clamped for rows of tiny values); 0 for m == 0.
+__device__ __forceinline__ int pair_exponent(float m) {
+  if (!(m > 0.0f)) return 0;
+  int k;
+  (void)frexpf(m, &k);
+  return min(100, max(-100, 14 - k));
+}
+
+// x (already scaled) -> hi = fp16(x), lo = fp16(x - hi)
+__device__ __forceinline__ void split16(float x, _Float16& hi, _Float16& lo) {
+  hi = (_Float16)x;
+  lo = (_Float16)(x - (float)hi);
+}
+
+// scaled value -> one 32-bit word: hi in the low half, lo in the high half
+__device__ __forceinline__ uint32_t pair_word(float x) {
+  _Float16 hi, lo;
+  split16(x, hi, lo);
+  return (uint32_t)__builtin_bit_cast(uint16_t, hi) | ((uint32_t)__builtin_bit_cast(uint16_t, lo) << 16);
+}
+
+// 16 values x scale -> the 64-byte pair record of a chunk row (one word per step)
+__device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChunk], float scale) {
+  u32x4* d = (u32x4*)dst;
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    d[u] = u32x4{pair_word(x[4 * u] * scale), pair_word(x[4 * u + 1] * scale),
+                 pair_word(x[4 * u + 2] * scale), pair_word(x[4 * u + 3] * scale)};
+}
+
+
 // ---------------------------------------------------------------- forward
 // One workgroup per batch element runs `steps` timesteps of every layer; the
 // neuron state of the threads' neurons stays in registers, the filtered
@@ -81,7 +117,6 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // 1. presynaptic vector, its filter, ordered active lists
   const int rw = Ly.rows_per_wave;
   const int i_beg = w * rw, i_end = min(Ly.n_pre, i_beg + rw);
-  float* zbk = Ly.zbarK + ((size_t)b * kKQ + t / 4) * Ly.ldi * 4 + (t & 3);   // [b][t/4][i][4]
   int n_act = 0;
   for (int base = i_beg; base < i_end; base += kWave) {
     const int i = base + lane;
@@ -91,7 +126,6 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       on = sv != 0;
       const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
       szb[i] = zv;
-      zbk[(size_t)i * 4] = zv;
     }
     const unsigned long long m = __ballot(on);
     if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
@@ -100,8 +134,13 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   if (lane == 0) S.cnt[w] = n_act;
   __syncthreads();
   {
+    // offset of this wave's list: the counts of the waves before it (one
+    // LDS read, then lane reads without waits)
+    const int cl = (lane < kFwdWaves) ? S.cnt[lane] : 0;
     int off = 0;
-    for (int ww = 0; ww < w; ++ww) off += S.cnt[ww];
+#pragma unroll
+    for (int ww = 0; ww < kFwdWaves; ++ww)
+      if (ww < w) off += __builtin_amdgcn_readlane(cl, ww);
     for (int k = lane; k < n_act; k += kWave) S.mrg[off + k] = S.act[w * S.rwmax + k];
     if (w == kFwdWaves - 1 && lane == 0) S.cnt[2 * kFwdWaves] = off + n_act;
   }
@@ -109,21 +148,27 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
 
   // 2. drive and neuron step.  Rows of Wt are padded to a multiple of the
   // workgroup size; chunks q with q*kFwdThreads >= n_rec are skipped (QN is
-  // rounded up to a power of two).  UB rows are loaded before any is added.
+  // rounded up to a power of two).  UB rows are loaded before any is added:
+  // lane u reads list entry k0 + u, every wave takes the entries from its
+  // lanes, and each row's load is a scalar row base plus the lane offset.
   constexpr int UB = QN >= 32 ? 1 : 32 / QN;
   const int total = S.cnt[2 * kFwdWaves];
+  const uint32_t tidoff = (uint32_t)tid * 4u;
   float I[QN];
 #pragma unroll
   for (int q = 0; q < QN; ++q) I[q] = 0.0f;
   for (int k0 = 0; k0 < total; k0 += UB) {
+    const int ent = S.mrg[min(k0 + (lane & (UB - 1)), total - 1)];   // past the end: the last row
     float wv[UB][QN];
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      // the same row for every lane: a scalar base
-      const int i = __builtin_amdgcn_readfirstlane(S.mrg[min(k0 + u, total - 1)]);
-      const float* wrow = Ly.Wt + (size_t)i * Ly.ldw + tid;
+      const int i = __builtin_amdgcn_readlane(ent, u);
+      const char* rowp = (const char*)(Ly.Wt + (size_t)i * Ly.ldw);
 #pragma unroll
-      for (int q = 0; q < QN; ++q) wv[u][q] = (q * kFwdThreads < A.n_rec) ? wrow[q * kFwdThreads] : 0.0f;
+      for (int q = 0; q < QN; ++q)
+        wv[u][q] = (q == 0 || q * kFwdThreads < A.n_rec)
+                       ? *(const float*)(rowp + tidoff + (uint32_t)q * kFwdThreads * 4u)
+                       : 0.0f;
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u)
@@ -132,10 +177,13 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
         for (int q = 0; q < QN; ++q) I[q] += wv[u][q];
   }
   int n_spk = 0;
+  float psv[QN];
+  unsigned long long smask[QN];
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
     const int j = q * kFwdThreads + tid;
     bool z = false;
+    psv[q] = 0.0f;
     if (j < A.n_rec) {
       const float zp = zprev[j] ? 1.0f : 0.0f;
       float vv = A.alpha * v[q];
@@ -152,36 +200,60 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       z = x > 0.0f;
       znow[j] = z ? 1 : 0;
       const float u = 1.0f - fabsf(x) / A.thr;
-      Ly.psiK[row * A.ldj + j] = A.gamma_over_thr * fmaxf(u, 0.0f);
+      psv[q] = A.gamma_over_thr * fmaxf(u, 0.0f);
       float zz = A.kappa * zt[q];
       zz = zz + (z ? 1.0f : 0.0f);
       zt[q] = zz;
-      Ly.ztK[row * A.ldn + j] = zz;
     }
     const unsigned long long m = __ballot(z);
+    smask[q] = m;
     if (z) S.spk[w * A.jlist + n_spk + lanes_below(m, lane)] = j;
     n_spk += __popcll(m);
-    if (A.spikes) {
-      const int w0 = (q * kFwdThreads + w * kWave) >> 5;
-      uint32_t* srow = A.spikes + (((size_t)t * A.n_layers + LI) * A.B + b) * A.W32;
-      if (lane == 0 && w0 < A.W32) srow[w0] = (uint32_t)m;
-      if (lane == 1 && w0 + 1 < A.W32) srow[w0 + 1] = (uint32_t)(m >> 32);
-    }
   }
 
   // 3. this wave's share of the readout: rows of the transposed readout
   // weights of its spiking neurons, read coalesced over the classes
   for (int kb = 0; kb < A.K_out; kb += kWave) {
     const int k = kb + lane;
-    if (k < A.K_out) {
-      float Y = 0.0f;
-#pragma unroll 8
-      for (int s2 = 0; s2 < n_spk; ++s2) {
-        const int j = __builtin_amdgcn_readfirstlane(S.spk[w * A.jlist + s2]);
-        Y += Ly.WoutT[(size_t)j * A.ldk + k];
+    const uint32_t koff = (uint32_t)min(k, A.K_out - 1) * 4u;
+    float Y = 0.0f;
+    for (int s0 = 0; s0 < n_spk; s0 += 16) {
+      const int ent = S.spk[w * A.jlist + min(s0 + (lane & 15), n_spk - 1)];
+      float wv[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int j = __builtin_amdgcn_readlane(ent, u);
+        wv[u] = *(const float*)((const char*)(Ly.WoutT + (size_t)j * A.ldk) + koff);
       }
-      S.part[w * A.K_out + k] = Y;
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (s0 + u < n_spk) Y += wv[u];
     }
+    if (k < A.K_out) S.part[w * A.K_out + k] = Y;
+  }
+
+  // Global stores of the step go last: a load waits for every store issued
+  // before it, so stores ahead of the drive and readout loads would lengthen
+  // the step.  Per-step vectors: psi, ztilde, the spike words, and the
+  // filtered presynaptic values as scaled fp16 pairs ([b][t/16][i][16] words,
+  // step t % 16).
+#pragma unroll
+  for (int q = 0; q < QN; ++q) {
+    const int j = q * kFwdThreads + tid;
+    if (j < A.n_rec) {
+      Ly.psiK[row * A.ldj + j] = psv[q];
+      Ly.ztK[row * A.ldn + j] = zt[q];
+    }
+    if (A.spikes) {
+      const int w0 = (q * kFwdThreads + w * kWave) >> 5;
+      uint32_t* srow = A.spikes + (((size_t)t * A.n_layers + LI) * A.B + b) * A.W32;
+      if (lane == 0 && w0 < A.W32) srow[w0] = (uint32_t)smask[q];
+      if (lane == 1 && w0 + 1 < A.W32) srow[w0 + 1] = (uint32_t)(smask[q] >> 32);
+    }
+  }
+  {
+    uint32_t* zpk = Ly.z16 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * kChunk + (t % kChunk);
+    for (int i = i_beg + lane; i < i_end; i += kWave) zpk[(size_t)i * kChunk] = pair_word(szb[i] * Ly.zscale);
   }
   __syncthreads();
 
@@ -247,7 +319,7 @@ __device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S,
 }
 
 template <int QN, int NL>
-__global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs A) {
+__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))) void forward_kernel(FwdArgs A) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int b = blockIdx.x;
   FwdLds S;
@@ -301,10 +373,11 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs A) {
 // v_mfma_f32_16x16x4f32 operand layout (64 lanes, lane = r + 16*g):
 //   A[16 x 4]:  lane holds A[r][g];  B[4 x 16]: lane holds B[g][r];
 //   D[16 x 16]: lane holds D[4*g + q][r] in accumulator register q.
-// Each lane loads 4 consecutive k (float4) of its row of A and of Bm and feeds
-// them to 4 MFMAs; both operands use the same k permutation, so the 4 MFMAs
-// together contract 16 consecutive k.  One wave computes a 32x32 tile
-// (2x2 blocks of 16x16); a block of 4 waves covers 32 (m) x 128 (n).
+// Each lane takes its row's (NT) or column's (TN) values at 4 consecutive k
+// of A and of Bm and feeds them to 4 MFMAs; both operands use the same k
+// permutation, so the 4 MFMAs together contract 16 consecutive k.  One wave
+// computes a 32x32 tile (2x2 blocks of 16x16); a block of 4 waves covers
+// 32 (m) x 128 (n); blockIdx.z is the split of k.
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -364,6 +437,7 @@ __global__ __launch_bounds__(256) void gemm_tn_kernel(GemmArgs a) {
   const int ke = min(a.K, kb + a.k_chunk);
   const int r = lane & 15, g = lane >> 4;
   f32x4 c00 = {0.f, 0.f, 0.f, 0.f}, c01 = c00, c10 = c00, c11 = c00;
+#pragma unroll 4
   for (int k = kb; k < ke; k += 16) {
     f32x4 va0, va1, vb0, vb1;
 #pragma unroll
@@ -405,6 +479,7 @@ __global__ __launch_bounds__(256) void accumulate_kernel(const float* part, int 
   if (idx >= (long long)M * N) return;
   const int m = (int)(idx / N), n = (int)(idx % N);
   double s = first ? 0.0 : acc[(size_t)m * ld + n];
+#pragma unroll 8
   for (int sp = 0; sp < splits; ++sp) s += (double)part[sp * ss + (size_t)m * N + n];
   acc[(size_t)m * ld + n] = s;
 }
@@ -427,6 +502,8 @@ __global__ __launch_bounds__(256) void accumulate_kernel(const float* part, int 
 //   U_s, P: the same with L replaced by the unit vector at the block's last
 //   step,  V_s = psi_s prod_{u>s} d_u,  D = prod_u d_u.
 // For LIF neurons beta_j = 0: N = 0, the epsa terms vanish.
+// Two passes of the backward recursion: the first finds each array's largest
+// magnitude (its scale), the second writes the scaled pairs chunk by chunk.
 __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   const int b = blockIdx.y;
@@ -435,21 +512,56 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
   const bool wv = a.V != nullptr && j < a.n_vcols;
   const float* __restrict__ psiK = a.psiK;
   const float* __restrict__ LK = a.LK;
-  const size_t o = ((size_t)b * kKQ * a.ldc + j) * 4, qs = (size_t)a.ldc * 4;
-  float M = 0.0f, Mu = 0.0f, nx = 0.0f, nxu = 0.0f, Dsuf = 1.0f;
-  for (int qd = a.kpad / 4 - 1; qd >= 0; --qd) {
-    float ps[4], L[4];
+  auto load = [&](int s, float& ps, float& L) {
+    const size_t row = ((size_t)s * a.Bp + b) * a.ldv + j;
+    ps = psiK[row];
+    L = LK[row];
+  };
+  float mU = 0.0f, mH = 0.0f, mV = 0.0f;
+  {
+    float M = 0.0f, Mu = 0.0f, nx = 0.0f, nxu = 0.0f, Dsuf = 1.0f;
+    for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
+      float ps[kChunk], L[kChunk];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int s = 4 * qd + e;
-      const size_t row = ((size_t)s * a.Bp + b) * a.ldv + j;
-      ps[e] = s < a.steps ? psiK[row] : 0.0f;
-      L[e] = s < a.steps ? LK[row] : 0.0f;
+      for (int e = 0; e < kChunk; ++e) {
+        ps[e] = 0.0f;
+        L[e] = 0.0f;
+        if (kChunk * c + e < a.steps) load(kChunk * c + e, ps[e], L[e]);
+      }
+#pragma unroll
+      for (int e = kChunk - 1; e >= 0; --e) {
+        const int s = kChunk * c + e;
+        if (s >= a.steps) continue;
+        const float d = a.rho - bt * ps[e];
+        M = fmaf(a.kappa, M, L[e]);
+        Mu = (s == a.steps - 1) ? 1.0f : a.kappa * Mu;
+        mH = fmaxf(mH, fabsf(ps[e] * (M - nx)));
+        mU = fmaxf(mU, fabsf(ps[e] * (Mu - nxu)));
+        mV = fmaxf(mV, fabsf(ps[e] * Dsuf));
+        nx = fmaf(bt * ps[e], M, d * nx);
+        nxu = fmaf(bt * ps[e], Mu, d * nxu);
+        Dsuf = d * Dsuf;
+      }
     }
-    f32x4 u, v, h;
+  }
+  const int eU = pair_exponent(mU), eH = pair_exponent(mH), eV = pair_exponent(mV);
+  const float sU = ldexpf(1.0f, eU), sH = ldexpf(1.0f, eH), sV = ldexpf(1.0f, eV);
+  const size_t rs = (size_t)a.ldc * kChunk;         // words between chunks
+  const size_t o = ((size_t)b * kKC * a.ldc + j) * kChunk;
+  float M = 0.0f, Mu = 0.0f, nx = 0.0f, nxu = 0.0f, Dsuf = 1.0f;
+  for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
+    float ps[kChunk], L[kChunk];
 #pragma unroll
-    for (int e = 3; e >= 0; --e) {
-      const int s = 4 * qd + e;
+    for (int e = 0; e < kChunk; ++e) {
+      const int s = kChunk * c + e;
+      ps[e] = 0.0f;
+      L[e] = 0.0f;
+      if (s < a.steps) load(s, ps[e], L[e]);
+    }
+    float u[kChunk], v[kChunk], h[kChunk];
+#pragma unroll
+    for (int e = kChunk - 1; e >= 0; --e) {
+      const int s = kChunk * c + e;
       if (s >= a.steps) {
         u[e] = v[e] = h[e] = 0.0f;
         continue;
@@ -464,15 +576,18 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
       nxu = fmaf(bt * ps[e], Mu, d * nxu);
       Dsuf = d * Dsuf;
     }
-    *(f32x4*)(a.U + o + qd * qs) = u;
-    *(f32x4*)(a.H + o + qd * qs) = h;
-    if (wv) *(f32x4*)(a.V + o + qd * qs) = v;
+    store_pairs(a.U + o + c * rs, u, sU);
+    store_pairs(a.H + o + c * rs, h, sH);
+    if (wv) store_pairs(a.V + o + c * rs, v, sV);
   }
   const size_t so = (size_t)b * a.ldc + j, plane = (size_t)a.B * a.ldc;
-  a.S[so] = a.kappa * M;       // c
-  a.S[plane + so] = -nx;       // q
-  a.S[2 * plane + so] = -nxu;  // P
-  a.S[3 * plane + so] = Dsuf;  // D
+  a.S[so] = a.kappa * M;              // c
+  a.S[plane + so] = -nx;              // q
+  a.S[2 * plane + so] = -nxu;         // P
+  a.S[3 * plane + so] = Dsuf;         // D
+  a.S[4 * plane + so] = 1.0f / sU;    // inverse scales (exact powers of two)
+  a.S[5 * plane + so] = 1.0f / sH;
+  a.S[6 * plane + so] = 1.0f / sV;
 }
 
 // A workgroup of 4 waves owns a 64 (i) x 64 (j) tile of synapses and one
@@ -502,7 +617,6 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
 // fp32 per lane and added to the split's fp64 accumulator at the end.
 // Buffer access: a wave-uniform base with a byte range (accesses outside it
 // read zero and write nothing) and a 32-bit per-lane byte offset.
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
 }
@@ -513,11 +627,11 @@ __device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, uint32_t off, f
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, 0);
 }
 
-constexpr int kChunkQuads = 4;                        // 16 steps per MFMA chunk
 constexpr int kRing = 4;                              // chunk slots
 constexpr int kPrefetch = 3;                          // chunks copied ahead (< kRing)
-constexpr int kSlot = 4 * kChunkQuads * kTile * 4;    // floats per slot: 4 operands (16 KiB)
-constexpr int kScal = 4 * kTile;                      // floats of c, q, P, D for 64 columns
+constexpr int kOpBytes = kTile * 64;                  // one operand of a chunk: 64 rows x 64 B
+constexpr int kSlot = 4 * kOpBytes / 4;               // floats per slot: z, U, H, V (16 KiB)
+constexpr int kScal = kScalarPlanes * kTile;          // floats of the scalars of 64 columns
 constexpr size_t kTraceSmem = sizeof(float) * (kRing * kSlot + 2 * kScal);
 constexpr uint32_t kSubTileBytes = 32 * 32 * 4;
 
@@ -549,7 +663,7 @@ struct TraceTile {
   static constexpr int D = NCH == 1 ? 1 : (NCH - 1 < kPrefetch ? NCH - 1 : kPrefetch);
   static constexpr int Q = ALIF ? 4 : 3;            // copies per wave per chunk
   static constexpr int EA = ALIF ? 8 : 4;           // trace loads per wave per batch element
-  static constexpr int ops(int c) { return Q + (c == 0 ? 1 : 0); }   // + scalars with chunk 0
+  static constexpr int ops(int c) { return Q + (c == 0 ? 2 : 0); }   // + scalars with chunk 0
   // Loads issued after those of chunk ch when it is waited for: the copies
   // of chunks ch+1 .. ch+D-1 (past the end of the batch element: the next
   // element's, if there is one), and the element's trace loads when they
@@ -589,20 +703,29 @@ struct TraceTile {
     return make_rsrc((const char*)a.epsa + (t * 4 + w) * kSubTileBytes, kSubTileBytes);
   }
 
-  // Copies of chunk c of batch element b into ring slot sl (this wave: quad
-  // 4c + w of each operand); with chunk 0 also the scalars (plane w) into
+  // Copies of chunk c of batch element b into ring slot sl.  Wave w copies
+  // rows 16w .. 16w+15 of each operand (1 KiB: lane l takes 16 bytes of row
+  // 16w + l/4); within a row the four 16-byte units are stored in the order
+  // u ^ ((row / 4) % 4), which keeps the MFMA operand reads free of bank
+  // conflicts.  With chunk 0 also the scalars (planes w and w + 4) into
   // scalar buffer par.
   __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
-    float* slot = sm + sl * kSlot;
-    const size_t qd = (size_t)b * kKQ + kChunkQuads * c + w;
-    dma16(a.zbarK + (qd * a.ldi + i0) * 4 + lane * 4, slot + (0 * kChunkQuads + w) * kTile * 4);
-    dma16(a.U + (qd * a.ldc + j0) * 4 + lane * 4, slot + (1 * kChunkQuads + w) * kTile * 4);
-    dma16(a.H + (qd * a.ldc + j0) * 4 + lane * 4, slot + (2 * kChunkQuads + w) * kTile * 4);
+    char* slot = (char*)(sm + sl * kSlot);
+    const int rw = 16 * w + (lane >> 2);
+    const uint32_t unit = (uint32_t)((lane & 3) ^ (lane >> 4)) * 16u;
+    const size_t zc = ((size_t)b * kKC + c) * a.ldi + i0 + rw;
+    const size_t cc = ((size_t)b * kKC + c) * a.ldc + j0 + rw;
+    float* dst = (float*)(slot + w * 1024);
+    dma16((const float*)((const char*)a.z16 + zc * 64 + unit), dst);
+    dma16((const float*)((const char*)a.U + cc * 64 + unit), dst + kOpBytes / 4);
+    dma16((const float*)((const char*)a.H + cc * 64 + unit), dst + 2 * kOpBytes / 4);
     if constexpr (ALIF)
-      dma16(a.V + (qd * a.ldc + j0) * 4 + lane * 4, slot + (3 * kChunkQuads + w) * kTile * 4);
-    if (c == 0 && lane < 16)
-      dma16(a.S + ((size_t)w * a.B + b) * a.ldc + j0 + lane * 4,
-            sm + kRing * kSlot + par * kScal + w * kTile);
+      dma16((const float*)((const char*)a.V + cc * 64 + unit), dst + 3 * kOpBytes / 4);
+    if (c == 0 && lane < 16) {
+      float* sb = sm + kRing * kSlot + par * kScal;
+      dma16(a.S + ((size_t)w * a.B + b) * a.ldc + j0 + lane * 4, sb + w * kTile);
+      dma16(a.S + ((size_t)(w + 4) * a.B + b) * a.ldc + j0 + lane * 4, sb + (w + 4) * kTile);
+    }
   }
 
   // block-start traces of batch element b into E/A
@@ -618,12 +741,13 @@ struct TraceTile {
   }
 
   // traces and gradient of the k-th batch element from its contractions
+  // (accumulated in the scaled units of the fp16 pairs)
   __device__ __forceinline__ void finish(int k, const f32x4 (&E)[2][2], const f32x4 (&A)[2][2],
                                          const f32x4 (&cU)[2][2], const f32x4 (&cV)[2][2],
                                          const f32x4 (&cH)[2][2], f32x4 (&gacc)[2][2]) const {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     const int b = split + k * a.n_split;
-    const float* st = sm + kRing * kSlot + (k & 1) * kScal;   // [4][64]: c, q, P, D
+    const float* st = sm + kRing * kSlot + (k & 1) * kScal;   // c, q, P, D, 1/sU, 1/sH, 1/sV
     const auto eR = ebar_rsrc(b);
     const auto aR = ALIF ? epsa_rsrc(b) : eR;
 #pragma unroll
@@ -632,6 +756,9 @@ struct TraceTile {
       const f32x4 c = *(const f32x4*)(st + cj), qq = *(const f32x4*)(st + kTile + cj);
       const f32x4 P = ALIF ? *(const f32x4*)(st + 2 * kTile + cj) : zero;
       const f32x4 Dd = ALIF ? *(const f32x4*)(st + 3 * kTile + cj) : zero;
+      const f32x4 fU = *(const f32x4*)(st + 4 * kTile + cj) * a.zinv;
+      const f32x4 fH = *(const f32x4*)(st + 5 * kTile + cj) * a.zinv;
+      const f32x4 fV = ALIF ? *(const f32x4*)(st + 6 * kTile + cj) * a.zinv : zero;
 #pragma unroll
       for (int bi = 0; bi < 2; ++bi) {
         const f32x4 e0 = first ? zero : E[bj][bi];
@@ -639,9 +766,9 @@ struct TraceTile {
         f32x4 ek, ak, gk;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], cU[bj][bi][q]));
-          gk[q] = fmaf(c[q], e0[q], fmaf(qq[q], a0[q], cH[bj][bi][q]));
-          ak[q] = fmaf(Dd[q], a0[q], cV[bj][bi][q]);
+          ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], cU[bj][bi][q] * fU[q]));
+          gk[q] = fmaf(c[q], e0[q], fmaf(qq[q], a0[q], cH[bj][bi][q] * fH[q]));
+          ak[q] = fmaf(Dd[q], a0[q], cV[bj][bi][q] * fV[q]);
         }
         gacc[bj][bi] += gk;
         const uint32_t o = (2 * bj + bi) * 1024u + lane * 16u;
@@ -690,27 +817,48 @@ struct TraceTile {
           issue(b + a.n_split, c2 - NCH, (n + D) % kRing, (k + 1) & 1);
         if constexpr (ch == 0) load_traces(b, E, A);
 
-        const float* slot = sm + (n % kRing) * kSlot;
-        f32x4 z[2], u[2], h[2], v[2];
+        // Per output block and contraction X, two fp16 MFMAs (K = 32) over the
+        // chunk's 16 steps.  Lane g holds steps 4g..4g+3 as (hi, lo) pairs of
+        // k slots: A = X's words as they are; B = (z_hi, z_hi) per step, then
+        // (z_lo, 0) with the same A: X_hi z_hi + X_lo z_hi + X_hi z_lo.
+        const char* slot = (const char*)(sm + (n % kRing) * kSlot);
+        const int sw = (r >> 2) & 3;   // unit order of this lane's rows
+        const f16x8 zero8 = {};
+        f16x8 bz1[2], bz2[2];
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
-          z[x] = *(const f32x4*)(slot + ((0 * kChunkQuads + g) * kTile + 32 * wi + 16 * x + r) * 4);
-          u[x] = *(const f32x4*)(slot + ((1 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4);
-          h[x] = *(const f32x4*)(slot + ((2 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4);
-          v[x] = ALIF ? *(const f32x4*)(slot + ((3 * kChunkQuads + g) * kTile + 32 * wj + 16 * x + r) * 4)
-                      : zero;
+          const int zr = 32 * wi + 16 * x + r;
+          const u32x4 zw = *(const u32x4*)(slot + zr * 64 + ((g ^ sw) << 4));
+          u32x4 w1, w2;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            w1[e] = (zw[e] & 0xFFFFu) | (zw[e] << 16);
+            w2[e] = zw[e] >> 16;
+          }
+          bz1[x] = __builtin_bit_cast(f16x8, w1);
+          bz2[x] = __builtin_bit_cast(f16x8, w2);
         }
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
+        for (int bj = 0; bj < 2; ++bj) {
+          const int cr = 32 * wj + 16 * bj + r;
+          f16x8 ax[3];
 #pragma unroll
-          for (int bj = 0; bj < 2; ++bj)
+          for (int X = 0; X < 3; ++X)
+            ax[X] = (X < 2 || ALIF)
+                        ? *(const f16x8*)(slot + (X + 1) * kOpBytes + cr * 64 + ((g ^ sw) << 4))
+                        : zero8;
+#pragma unroll
+          for (int pass = 0; pass < 2; ++pass)
 #pragma unroll
             for (int bi = 0; bi < 2; ++bi) {
-              cU[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(u[bj][q], z[bi][q], cU[bj][bi], 0, 0, 0);
-              cH[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[bj][q], z[bi][q], cH[bj][bi], 0, 0, 0);
+              const f16x8 bz = pass == 0 ? bz1[bi] : bz2[bi];
+              cU[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[0], bz, cU[bj][bi], 0, 0, 0);
+              cH[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz, cH[bj][bi], 0, 0, 0);
               if constexpr (ALIF)
-                cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x4f32(v[bj][q], z[bi][q], cV[bj][bi], 0, 0, 0);
+                cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[2], bz, cV[bj][bi], 0, 0, 0);
             }
+          __builtin_amdgcn_sched_barrier(0);
+        }
       };
       for_each_index(chunk, std::make_integer_sequence<int, NCH>{});
     }

@@ -36,12 +36,13 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
         traces = sum(4 * shape.batch * shape.n_pre(l) * (shape.n_rec + shape.n_adaptive)
                      for l in range(shape.n_layers))
         # per-step vectors for two blocks of at most 128 steps (one being
-        # written by the forward pass while the other is read), plus one
+        # written by the forward pass while the other is read; the filtered
+        # presynaptic vector twice: fp32 and as fp16 pairs), plus one
         # block's eligibility coefficients per layer and slot (three per neuron
         # and step)
         bp = -(-shape.batch // 16) * 16
         nv = -(-shape.n_rec // 256) * 256
-        per_step = sum(4 * (2 * bp * nv + (shape.n_pre(l) + 63) * shape.batch
+        per_step = sum(4 * (2 * bp * nv + 2 * (shape.n_pre(l) + 63) * shape.batch
                             + (shape.n_out + 32 + shape.n_rec + 32) * bp)
                        for l in range(shape.n_layers))
         coef = 4 * 3 * shape.batch * (shape.n_rec + 63)
