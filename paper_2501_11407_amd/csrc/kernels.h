@@ -25,7 +25,7 @@ namespace eprop {
 constexpr int kFwdThreads = 512;               // forward workgroup: one batch element
 constexpr int kFwdWaves = kFwdThreads / 64;
 constexpr int kFwdXSteps = 8;                  // input spikes staged in shared memory per load
-constexpr int kBlockSteps = 128;       // timesteps per block (Kmax)
+constexpr int kBlockSteps = 256;       // timesteps per block (Kmax)
 constexpr int kKQ = kBlockSteps / 4;   // step quads per block
 constexpr int kTile = 64;              // eligibility workgroup tile: 64 (i) x 64 (j)
 constexpr int kRowPad = kTile;         // n_pre padded to the tile height (ldi)

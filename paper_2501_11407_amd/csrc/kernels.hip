@@ -616,15 +616,19 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
 // bytes).  The gradient of the batch elements of one launch is summed in
 // fp32 per lane and added to the split's fp64 accumulator at the end.
 // Buffer access: a wave-uniform base with a byte range (accesses outside it
-// read zero and write nothing) and a 32-bit per-lane byte offset.
+// read zero and write nothing) and a 32-bit per-lane byte offset.  The trace
+// streams use the non-temporal cache policy (bit 1 of the policy operand):
+// each trace is touched once per block, and keeping it out of the caches
+// leaves room for the operand tiles that neighbouring workgroups reuse.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
 }
+constexpr int kNonTemporal = 2;
 __device__ __forceinline__ f32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal));
 }
 __device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, 0);
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, kNonTemporal);
 }
 
 constexpr int kRing = 4;                              // chunk slots
@@ -884,7 +888,7 @@ struct TraceTile {
 template <bool ALIF>
 __device__ __forceinline__ void trace_tile_n(const TraceArgs& a, float* sm, int it, int jt,
                                              int split, bool first) {
-  static_assert(kBlockSteps == 128, "chunk dispatch assumes 128-step blocks");
+  static_assert(kBlockSteps == 256, "chunk dispatch assumes 256-step blocks");
   switch (a.kpad >> 4) {
     case 1: TraceTile<ALIF, 1>(a, sm, it, jt, split, first).run(); break;
     case 2: TraceTile<ALIF, 2>(a, sm, it, jt, split, first).run(); break;
@@ -893,7 +897,15 @@ __device__ __forceinline__ void trace_tile_n(const TraceArgs& a, float* sm, int 
     case 5: TraceTile<ALIF, 5>(a, sm, it, jt, split, first).run(); break;
     case 6: TraceTile<ALIF, 6>(a, sm, it, jt, split, first).run(); break;
     case 7: TraceTile<ALIF, 7>(a, sm, it, jt, split, first).run(); break;
-    default: TraceTile<ALIF, 8>(a, sm, it, jt, split, first).run(); break;
+    case 8: TraceTile<ALIF, 8>(a, sm, it, jt, split, first).run(); break;
+    case 9: TraceTile<ALIF, 9>(a, sm, it, jt, split, first).run(); break;
+    case 10: TraceTile<ALIF, 10>(a, sm, it, jt, split, first).run(); break;
+    case 11: TraceTile<ALIF, 11>(a, sm, it, jt, split, first).run(); break;
+    case 12: TraceTile<ALIF, 12>(a, sm, it, jt, split, first).run(); break;
+    case 13: TraceTile<ALIF, 13>(a, sm, it, jt, split, first).run(); break;
+    case 14: TraceTile<ALIF, 14>(a, sm, it, jt, split, first).run(); break;
+    case 15: TraceTile<ALIF, 15>(a, sm, it, jt, split, first).run(); break;
+    default: TraceTile<ALIF, 16>(a, sm, it, jt, split, first).run(); break;
   }
 }
 

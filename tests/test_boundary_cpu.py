@@ -35,7 +35,7 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
         n = eprop.eprop_workspace_bytes(eprop.make_config(shape))
         traces = sum(4 * shape.batch * shape.n_pre(l) * (shape.n_rec + shape.n_adaptive)
                      for l in range(shape.n_layers))
-        # per-step vectors for two blocks of at most 128 steps (one being
+        # per-step vectors for two blocks of at most 256 steps (one being
         # written by the forward pass while the other is read; the filtered
         # presynaptic vector twice: fp32 and as fp16 pairs), plus one
         # block's eligibility coefficients per layer and slot (three per neuron
@@ -48,7 +48,7 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
         coef = 4 * 3 * shape.batch * (shape.n_rec + 63)
         # at most 8 fp64 partial gradient accumulators (batch splits) per layer
         partial = sum(8 * 8 * (shape.n_pre(l) + 63) * shape.n_rec for l in range(shape.n_layers))
-        assert traces <= n <= (traces * 1.05 + 2 * 128 * per_step + 2 * shape.n_layers * 128 * coef
+        assert traces <= n <= (traces * 1.05 + 2 * 256 * per_step + 2 * shape.n_layers * 256 * coef
                                + partial + (16 << 20)), \
             (name, n, traces)
     # the same shape with any T needs the same workspace: T is not an input

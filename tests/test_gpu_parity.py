@@ -35,7 +35,7 @@ DISTINCT = dict(kappa=f32(math.exp(-1 / 7)), rho=f32(math.exp(-1 / 50)))
 # Small shapes the oracle finishes in well under a second: ragged sizes that
 # leave partial 64x64 eligibility tiles, partial 16-step chunks and 4-step
 # quads, partial spike words, an adaptive/LIF boundary inside a tile, several
-# tiles over j, several batch splits, and sequences of several 128-step blocks
+# tiles over j, several batch splits, and sequences of several 256-step blocks
 # whose last block is short (one chunk; four chunks).
 RAGGED = {
     "rlif_ragged": (small(**DISTINCT), 2, 4.0),
@@ -49,8 +49,8 @@ RAGGED = {
     "wide_1100": (small(batch=2, n_in=50, n_rec=1100, n_out=7, T=12, n_adaptive=550), 9, 4.0),
     "batch37_k33": (small(batch=37, n_in=70, n_rec=70, n_out=33, T=25, n_adaptive=35), 10, 4.0),
     "single_step": (small(T=1, n_adaptive=13), 11, 8.0),
-    "blocks_128_9": (small(n_adaptive=13, T=137, **DISTINCT), 12, 4.0),
-    "blocks_128_128_50": (small(batch=6, n_adaptive=29, T=306, **DISTINCT), 13, 4.0),
+    "blocks_256_256_9": (small(n_adaptive=13, T=521, **DISTINCT), 12, 4.0),
+    "blocks_256_50": (small(batch=6, n_adaptive=29, T=306, **DISTINCT), 13, 4.0),
 }
 # Weight multipliers (powers of two keep the 2**-14 grid): one step needs a
 # strong drive to spike.  Partial sums stay far below 2**10, so they are exact.
