@@ -76,6 +76,7 @@ struct Plan {
   int* err_flag = nullptr;
   int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, ldc = 0, jlist = 0, out_splits = 1;
   size_t smem = 0;
+  int zgroup = 1;
   size_t bytes = 0;
 };
 
@@ -192,10 +193,20 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   const size_t npad4 = round_up(N, 4);
   size_t npre_max = 0;
   for (const Layer& L : plan->layers) npre_max = std::max<size_t>(npre_max, L.n_pre);
-  plan->smem = sizeof(int) * (eprop::kFwdWaves * ((size_t)rwmax + (size_t)plan->jlist) +
-                              npre_max + 2 * eprop::kFwdWaves + 2) +
-               sizeof(float) * ((size_t)eprop::kFwdWaves * K + (size_t)c.n_layers * K + npre_total) +
-               (size_t)c.n_layers * 2 * npad4 + (size_t)eprop::kFwdXSteps * c.n_in;
+  const size_t smem_base = sizeof(int) * (eprop::kFwdWaves * ((size_t)rwmax + (size_t)plan->jlist) +
+                                          npre_max + 2 * eprop::kFwdWaves + 2) +
+                           sizeof(float) * ((size_t)eprop::kFwdWaves * K + (size_t)c.n_layers * K +
+                                            npre_total) +
+                           (size_t)c.n_layers * 2 * npad4 + (size_t)eprop::kFwdXSteps * c.n_in;
+  // pair words of the presynaptic filter are written 4 steps at a time when
+  // that keeps the forward's shared memory small enough for an eligibility
+  // workgroup to share its compute unit, else 2 or 1
+  plan->zgroup = 1;
+  for (int zg : {4, 2}) {
+    const size_t sm = smem_base + sizeof(uint32_t) * zg * npre_total;
+    if (sm <= (zg == 4 ? 96 : 160) * 1024) { plan->zgroup = zg; break; }
+  }
+  plan->smem = smem_base + sizeof(uint32_t) * plan->zgroup * npre_total;
   plan->bytes = round_up(off, 256);
 }
 
@@ -314,7 +325,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   fa.n_adaptive = c.n_adaptive; fa.Kmax = P.Kmax; fa.steps = steps;
   fa.ldj = P.layers[0].ldv; fa.ldk = P.ldk; fa.ldn = P.ldn; fa.jlist = P.jlist;
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
-  fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem;
+  fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.zgroup = P.zgroup;
   if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
 
   // On the forward stream, per layer: learning signal, readout gradient and

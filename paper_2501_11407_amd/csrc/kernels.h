@@ -57,6 +57,7 @@ struct FwdArgs {
   int W32;
   int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldk, ldn, jlist;  // ldj: row stride of psiK
   float alpha, rho, kappa, thr, beta, gamma_over_thr;
+  int zgroup;                    // steps of pair words written together (1, 2 or 4)
   size_t smem;
 };
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s);

@@ -36,6 +36,16 @@ __device__ inline int lanes_below(unsigned long long m, int lane) {
 
 inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
+// Workgroup barrier for shared-memory data only: waits for this wave's LDS
+// operations, not for its global stores (a __syncthreads fence would), which
+// in the forward kernel are read only by later kernels.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt and expcnt unrestricted
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // ---------------------------------------------------------------- scaled fp16 pairs
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -92,7 +102,10 @@ __device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChu
 //      softmax, delta = softmax - onehot(label), cross-entropy into the loss.
 // The learning signal L = W_out^T delta is one GEMM over the whole block.
 struct FwdLds {
-  int* act; int* mrg; int* spk; int* cnt; float* part; float* sy; float* szb; uint8_t* zc;
+  int* act; int* mrg; int* spk; int* cnt; float* part; float* sy; float* szb;
+  uint32_t* zh;                  // [zgroup][npre_total]: pair words of the last zgroup steps
+  int npre_total;
+  uint8_t* zc;
   uint8_t* xs;
   int rwmax, npad;
 };
@@ -100,7 +113,7 @@ struct FwdLds {
 template <int QN, int LI>
 __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLds& S, int t, int b,
                                                    int cur, float (&v)[QN], float (&ad)[QN],
-                                                   float (&zt)[QN], double& loss) {
+                                                   float (&zt)[QN], double& loss, int label) {
   const FwdLayer& Ly = A.L[LI];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const uint8_t* zprev = S.zc + (LI * 2 + cur) * S.npad;
@@ -111,6 +124,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   else
     inp = S.zc + ((LI - 1) * 2 + (cur ^ 1)) * S.npad;
   float* szb = S.szb + (LI == 0 ? 0 : A.L[0].n_pre);
+  uint32_t* zring = S.zh + (LI == 0 ? 0 : A.L[0].n_pre);
   float* sy = S.sy + LI * A.K_out;
   const size_t row = (size_t)t * A.Bp + b;
 
@@ -126,13 +140,14 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       on = sv != 0;
       const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
       szb[i] = zv;
+      zring[(t & (A.zgroup - 1)) * S.npre_total + i] = pair_word(zv * Ly.zscale);
     }
     const unsigned long long m = __ballot(on);
     if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
     n_act += __popcll(m);
   }
   if (lane == 0) S.cnt[w] = n_act;
-  __syncthreads();
+  lds_barrier();
   {
     // offset of this wave's list: the counts of the waves before it (one
     // LDS read, then lane reads without waits)
@@ -144,7 +159,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     for (int k = lane; k < n_act; k += kWave) S.mrg[off + k] = S.act[w * S.rwmax + k];
     if (w == kFwdWaves - 1 && lane == 0) S.cnt[2 * kFwdWaves] = off + n_act;
   }
-  __syncthreads();
+  lds_barrier();
 
   // 2. drive and neuron step.  Rows of Wt are padded to a multiple of the
   // workgroup size; chunks q with q*kFwdThreads >= n_rec are skipped (QN is
@@ -251,15 +266,24 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       if (lane == 1 && w0 + 1 < A.W32) srow[w0 + 1] = (uint32_t)(smask[q] >> 32);
     }
   }
-  {
-    uint32_t* zpk = Ly.z16 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * kChunk + (t % kChunk);
-    for (int i = i_beg + lane; i < i_end; i += kWave) zpk[(size_t)i * kChunk] = pair_word(szb[i] * Ly.zscale);
+  // the pair words go out zgroup steps at a time (4 * zgroup bytes per row)
+  if ((t & (A.zgroup - 1)) == A.zgroup - 1 || t == A.steps - 1) {
+    uint32_t* zpk = Ly.z16 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * kChunk + ((t % kChunk) & ~(A.zgroup - 1));
+    const int np = S.npre_total;
+    for (int i = i_beg + lane; i < i_end; i += kWave) {
+      uint32_t* d = zpk + (size_t)i * kChunk;
+      if (A.zgroup == 4)
+        *(u32x4*)d = u32x4{zring[i], zring[np + i], zring[2 * np + i], zring[3 * np + i]};
+      else if (A.zgroup == 2)
+        *(uint2*)d = uint2{zring[i], zring[np + i]};
+      else
+        *d = zring[i];
+    }
   }
-  __syncthreads();
+  lds_barrier();
 
   // 4. readout, softmax cross-entropy (wave 0; the other waves go on)
   if (w == 0) {
-    const int label = A.labels[b];
     const bool label_ok = label >= 0 && label < A.K_out;
     float m = -INFINITY;
     for (int k = lane; k < A.K_out; k += kWave) {
@@ -335,15 +359,20 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
   S.sy = S.part + kFwdWaves * A.K_out;         // [n_layers][K_out]
   S.szb = S.sy + NL * A.K_out;                 // [n_pre_0 + n_pre_1]
   const int npre_total = A.L[0].n_pre + (NL > 1 ? A.L[1].n_pre : 0);
-  S.zc = (uint8_t*)(S.szb + npre_total);       // [n_layers][2][npad]
+  S.zh = (uint32_t*)(S.szb + npre_total);      // [zgroup][npre_total]
+  S.npre_total = npre_total;
+  S.zc = (uint8_t*)(S.zh + A.zgroup * npre_total);   // [n_layers][2][npad]
   S.xs = S.zc + NL * 2 * S.npad;               // [kFwdXSteps][n_in]
 
+  for (int e = threadIdx.x; e < A.zgroup * npre_total; e += kFwdThreads) S.zh[e] = 0u;
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
   forward_state<QN, 0>(A, S, b, true, v0, a0, zt0, 0);
   if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, true, v1, a1, zt1, 0);
   double loss0 = 0.0, loss1 = 0.0;
+  // loaded once: a global load inside the step would wait for the step's stores
+  const int label = __builtin_amdgcn_readfirstlane(A.labels[b]);
   int cur = 0;
-  __syncthreads();
+  lds_barrier();
   for (int t = 0; t < A.steps; ++t) {
     if (t % kFwdXSteps == 0) {
       // stage the input spikes of the next kFwdXSteps steps (one round trip)
@@ -355,10 +384,10 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
           for (int i = threadIdx.x; i < A.n_in; i += kFwdThreads) S.xs[tt * A.n_in + i] = xrow[i];
         }
       }
-      __syncthreads();
+      lds_barrier();
     }
-    forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0);
-    if constexpr (NL > 1) forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1);
+    forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0, label);
+    if constexpr (NL > 1) forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1, label);
     cur ^= 1;
   }
   forward_state<QN, 0>(A, S, b, false, v0, a0, zt0, cur);
