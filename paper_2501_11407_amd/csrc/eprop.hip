@@ -195,7 +195,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   for (const Layer& L : plan->layers) npre_max = std::max<size_t>(npre_max, L.n_pre);
   const size_t smem_base = sizeof(int) * (eprop::kFwdWaves * ((size_t)rwmax + (size_t)plan->jlist) +
                                           npre_max + 2 * eprop::kFwdWaves + 2) +
-                           sizeof(float) * ((size_t)eprop::kFwdWaves * K + (size_t)c.n_layers * K +
+                           sizeof(float) * ((size_t)2 * c.n_layers * eprop::kFwdWaves * K + (size_t)c.n_layers * K +
                                             npre_total) +
                            (size_t)c.n_layers * 2 * npad4 + (size_t)eprop::kFwdXSteps * c.n_in;
   // pair words of the presynaptic filter are written 4 steps at a time when

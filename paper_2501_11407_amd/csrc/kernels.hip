@@ -110,12 +110,41 @@ struct FwdLds {
   int rwmax, npad;
 };
 
+// Softmax cross-entropy of one step for K_out <= 64, in wave 0: lane k holds
+// class k's output y (updated here) and gets delta_k = softmax_k - onehot_k.
+// The waves' partial sums are added in wave order.
+__device__ __forceinline__ float softmax_lanes(const FwdArgs& A, const float* part, float& y,
+                                               int label, double& loss) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const bool in = lane < A.K_out;
+  float Y = 0.0f;
+#pragma unroll
+  for (int ww = 0; ww < kFwdWaves; ++ww) Y += in ? part[ww * A.K_out + lane] : 0.0f;
+  float yy = A.kappa * y;
+  yy = yy + Y;
+  if (in) y = yy;
+  const float m = wave_max(in ? yy : -INFINITY);
+  const float ex = in ? expf(yy - m) : 0.0f;
+  const float se = wave_sum(ex);
+  const bool label_ok = label >= 0 && label < A.K_out;
+  const float yl = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(yy), label_ok ? label : 0));
+  if (lane == 0) {
+    if (label_ok)
+      loss += (double)(logf(se) - (yl - m));
+    else
+      *A.err_flag = 1;
+  }
+  return ex / se - ((lane == label) ? 1.0f : 0.0f);
+}
+
 template <int QN, int LI>
 __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLds& S, int t, int b,
                                                    int cur, float (&v)[QN], float (&ad)[QN],
-                                                   float (&zt)[QN], double& loss, int label) {
+                                                   float (&zt)[QN], double& loss, int label,
+                                                   float& yk, float& dk) {
   const FwdLayer& Ly = A.L[LI];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const uint8_t* zprev = S.zc + (LI * 2 + cur) * S.npad;
   uint8_t* znow = S.zc + (LI * 2 + (cur ^ 1)) * S.npad;
   const uint8_t* inp;
@@ -127,6 +156,14 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   uint32_t* zring = S.zh + (LI == 0 ? 0 : A.L[0].n_pre);
   float* sy = S.sy + LI * A.K_out;
   const size_t row = (size_t)t * A.Bp + b;
+  // readout partial sums of this step and of the step before (by parity)
+  float* part = S.part + (LI * 2 + (t & 1)) * kFwdWaves * A.K_out;
+  const float* part_prev = S.part + (LI * 2 + ((t + 1) & 1)) * kFwdWaves * A.K_out;
+  // K_out <= 64: wave 0 takes the previous step's softmax while its first
+  // batch of drive loads is in flight, and stores delta with this step's
+  // stores; the block's last step is finished after the step loop
+  const bool defer = A.K_out <= kWave;
+  bool soft = defer && w == 0 && t > 0;
 
   // 1. presynaptic vector, its filter, ordered active lists
   const int rw = Ly.rows_per_wave;
@@ -185,12 +222,18 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
                        ? *(const float*)(rowp + tidoff + (uint32_t)q * kFwdThreads * 4u)
                        : 0.0f;
     }
+    if (soft) {
+      asm volatile("" ::: "memory");
+      dk = softmax_lanes(A, part_prev, yk, label, loss);
+      soft = false;
+    }
 #pragma unroll
     for (int u = 0; u < UB; ++u)
       if (k0 + u < total)
 #pragma unroll
         for (int q = 0; q < QN; ++q) I[q] += wv[u][q];
   }
+  if (soft) dk = softmax_lanes(A, part_prev, yk, label, loss);   // no active rows
   int n_spk = 0;
   float psv[QN];
   unsigned long long smask[QN];
@@ -244,7 +287,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       for (int u = 0; u < 16; ++u)
         if (s0 + u < n_spk) Y += wv[u];
     }
-    if (k < A.K_out) S.part[w * A.K_out + k] = Y;
+    if (k < A.K_out) part[w * A.K_out + k] = Y;
   }
 
   // Global stores of the step go last: a load waits for every store issued
@@ -266,6 +309,8 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       if (lane == 1 && w0 + 1 < A.W32) srow[w0 + 1] = (uint32_t)(smask[q] >> 32);
     }
   }
+  if (defer && w == 0 && t > 0 && lane < A.K_out)
+    Ly.deltaK[(row - A.Bp) * A.ldk + lane] = dk;
   // the pair words go out zgroup steps at a time (4 * zgroup bytes per row)
   if ((t & (A.zgroup - 1)) == A.zgroup - 1 || t == A.steps - 1) {
     uint32_t* zpk = Ly.z16 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * kChunk + ((t % kChunk) & ~(A.zgroup - 1));
@@ -283,12 +328,12 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   lds_barrier();
 
   // 4. readout, softmax cross-entropy (wave 0; the other waves go on)
-  if (w == 0) {
+  if (!defer && w == 0) {
     const bool label_ok = label >= 0 && label < A.K_out;
     float m = -INFINITY;
     for (int k = lane; k < A.K_out; k += kWave) {
       float Y = 0.0f;
-      for (int ww = 0; ww < kFwdWaves; ++ww) Y += S.part[ww * A.K_out + k];
+      for (int ww = 0; ww < kFwdWaves; ++ww) Y += part[ww * A.K_out + k];
       float yy = A.kappa * sy[k];
       yy = yy + Y;
       sy[k] = yy;
@@ -300,7 +345,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     se = wave_sum(se);
     if (lane == 0) {
       if (label_ok)
-        loss += log((double)se) - ((double)sy[label] - (double)m);
+        loss += (double)(logf(se) - (sy[label] - m));
       else
         *A.err_flag = 1;
     }
@@ -355,8 +400,8 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
   S.mrg = S.act + kFwdWaves * S.rwmax;         // [npre_max]
   S.spk = S.mrg + npre_max;                    // [waves][jlist]
   S.cnt = S.spk + kFwdWaves * A.jlist;         // [2 * waves + 2]
-  S.part = (float*)(S.cnt + 2 * kFwdWaves + 2);   // [waves][K_out]
-  S.sy = S.part + kFwdWaves * A.K_out;         // [n_layers][K_out]
+  S.part = (float*)(S.cnt + 2 * kFwdWaves + 2);   // [n_layers][2][waves][K_out]
+  S.sy = S.part + NL * 2 * kFwdWaves * A.K_out;   // [n_layers][K_out]
   S.szb = S.sy + NL * A.K_out;                 // [n_pre_0 + n_pre_1]
   const int npre_total = A.L[0].n_pre + (NL > 1 ? A.L[1].n_pre : 0);
   S.zh = (uint32_t*)(S.szb + npre_total);      // [zgroup][npre_total]
@@ -373,6 +418,13 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
   const int label = __builtin_amdgcn_readfirstlane(A.labels[b]);
   int cur = 0;
   lds_barrier();
+  // deferred softmax state (wave 0, lane k: class k)
+  const int lane = threadIdx.x & (kWave - 1);
+  float y0 = 0.0f, y1 = 0.0f, d0 = 0.0f, d1 = 0.0f;
+  if (lane < A.K_out) {
+    y0 = S.sy[lane];
+    if constexpr (NL > 1) y1 = S.sy[A.K_out + lane];
+  }
   for (int t = 0; t < A.steps; ++t) {
     if (t % kFwdXSteps == 0) {
       // stage the input spikes of the next kFwdXSteps steps (one round trip)
@@ -386,10 +438,30 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
       }
       lds_barrier();
     }
-    forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0, label);
-    if constexpr (NL > 1) forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1, label);
+    forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0, label, y0, d0);
+    if constexpr (NL > 1)
+      forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1, label, y1, d1);
     cur ^= 1;
   }
+  if (A.K_out <= kWave && threadIdx.x < kWave && A.steps > 0) {
+    // the last step's softmax (its partial sums are visible: every step ends
+    // with a barrier)
+    const int tl = A.steps - 1;
+    const size_t row = (size_t)tl * A.Bp + b;
+    d0 = softmax_lanes(A, S.part + (tl & 1) * kFwdWaves * A.K_out, y0, label, loss0);
+    if (lane < A.K_out) {
+      A.L[0].deltaK[row * A.ldk + lane] = d0;
+      S.sy[lane] = y0;
+    }
+    if constexpr (NL > 1) {
+      d1 = softmax_lanes(A, S.part + (2 + (tl & 1)) * kFwdWaves * A.K_out, y1, label, loss1);
+      if (lane < A.K_out) {
+        A.L[1].deltaK[row * A.ldk + lane] = d1;
+        S.sy[A.K_out + lane] = y1;
+      }
+    }
+  }
+  lds_barrier();
   forward_state<QN, 0>(A, S, b, false, v0, a0, zt0, cur);
   if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, false, v1, a1, zt1, cur);
   if (threadIdx.x == 0) {
