@@ -39,7 +39,10 @@
  * Streams: every call that takes a context enqueues work on the stream given
  * to eprop_init and returns without waiting, except eprop_status and
  * eprop_profile_end, which wait for that stream.  A context belongs to one
- * stream and one host thread at a time.
+ * stream and one host thread at a time.  Internally the forward and
+ * coefficient kernels run on two streams of the context's own, joined to the
+ * caller's stream by events: work enqueued on the caller's stream before a
+ * call happens before it, and work enqueued after a call sees its results.
  */
 #ifndef EPROP_H
 #define EPROP_H

@@ -230,8 +230,11 @@ struct eprop_ctx {
   int slot = 0;         // K-buffer slot the next block writes
   int last_slot = 0;    // slot of the last block
   bool slot_used[2] = {false, false};
-  hipStream_t fwd_stream = nullptr;   // internal stream of the forward kernel
-  hipEvent_t ev_entry = nullptr, ev_fwd[2] = {nullptr, nullptr}, ev_done[2] = {nullptr, nullptr};
+  // internal streams: the forward kernel, and the passes between it and the
+  // eligibility kernel (learning signal, readout gradient, coefficients)
+  hipStream_t fwd_stream = nullptr, coef_stream = nullptr;
+  hipEvent_t ev_entry = nullptr, ev_fwd[2] = {nullptr, nullptr}, ev_coef[2] = {nullptr, nullptr},
+             ev_done[2] = {nullptr, nullptr};
   bool alive = false;
   std::string err;
   // profiling of the eligibility kernel
@@ -300,6 +303,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   const eprop_config& c = P.cfg;
   hipStream_t s = ctx->stream;
   hipStream_t sf = ctx->fwd_stream;
+  hipStream_t sc = ctx->coef_stream;
   const int first = ctx->t == 0;
   const int sl = ctx->slot;
   int rc;
@@ -327,9 +331,12 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
   fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.zgroup = P.zgroup;
   if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
+  if ((rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
 
-  // On the forward stream, per layer: learning signal, readout gradient and
-  // the block coefficients of the eligibility recursion.
+  // On the coefficient stream, per layer: learning signal, readout gradient
+  // and the block coefficients of the eligibility recursion.  The forward of
+  // the next block (other slot) runs meanwhile.
+  if ((rc = check(ctx, hipStreamWaitEvent(sc, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
   const int rows = steps * P.Bp;
   const int kpad = (int)round_up(steps, 16);
   for (int l = 0; l < c.n_layers; ++l) {
@@ -339,7 +346,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     gl.A = L.deltaK[sl]; gl.Bm = L.WoutT; gl.C = L.LK[sl];
     gl.M = rows; gl.N = c.n_rec; gl.K = P.ldk; gl.lda = P.ldk; gl.ldb = P.ldk; gl.ldc = L.ldv;
     gl.splits = 1; gl.k_chunk = P.ldk; gl.split_stride = 0;
-    if ((rc = check(ctx, eprop::launch_gemm_nt(gl, sf), "learning-signal GEMM"))) return rc;
+    if ((rc = check(ctx, eprop::launch_gemm_nt(gl, sc), "learning-signal GEMM"))) return rc;
 
     // dW_out += sum over (t, b) of delta (x) ztilde, then fp64 accumulation
     eprop::GemmArgs g;
@@ -347,9 +354,9 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     g.M = c.n_out; g.N = c.n_rec; g.K = rows; g.lda = P.ldk; g.ldb = P.ldn; g.ldc = c.n_rec;
     choose_splits(g.M, g.N, g.K, P.out_splits, &g.splits, &g.k_chunk);
     g.split_stride = (size_t)c.n_out * c.n_rec;
-    if ((rc = check(ctx, eprop::launch_gemm_tn(g, sf), "readout gradient GEMM"))) return rc;
+    if ((rc = check(ctx, eprop::launch_gemm_tn(g, sc), "readout gradient GEMM"))) return rc;
     if ((rc = check(ctx, eprop::launch_accumulate(L.Cpart, g.splits, g.split_stride, c.n_out,
-                                                  c.n_rec, L.accout, L.ldj, first, sf),
+                                                  c.n_rec, L.accout, L.ldj, first, sc),
                     "readout gradient accumulation")))
       return rc;
 
@@ -361,11 +368,10 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(c.n_adaptive, eprop::kTile));
     ca.steps = steps; ca.kpad = kpad; ca.ldc = P.ldc;
     ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta;
-    if ((rc = check(ctx, eprop::launch_coef(ca, sf), "eligibility coefficient kernel"))) return rc;
-
+    if ((rc = check(ctx, eprop::launch_coef(ca, sc), "eligibility coefficient kernel"))) return rc;
   }
-  if ((rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
-  if ((rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
+  if ((rc = check(ctx, hipEventRecord(ctx->ev_coef[sl], sc), "event record"))) return rc;
+  if ((rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_coef[sl], 0), "stream wait"))) return rc;
 
   // On the caller's stream: the eligibility pass of every layer.
   for (int l = 0; l < c.n_layers; ++l) {
@@ -459,9 +465,13 @@ int eprop_init(const eprop_config* cfg, void* d_workspace, size_t ws_bytes,
   }
   int rc = check(ctx, hipStreamCreateWithFlags(&ctx->fwd_stream, hipStreamNonBlocking),
                  "stream create");
+  if (!rc) rc = check(ctx, hipStreamCreateWithFlags(&ctx->coef_stream, hipStreamNonBlocking),
+                      "stream create");
   if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_entry, hipEventDisableTiming), "event create");
   for (int k = 0; k < 2 && !rc; ++k) {
     rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_fwd[k], hipEventDisableTiming), "event create");
+    if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_coef[k], hipEventDisableTiming),
+                        "event create");
     if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_done[k], hipEventDisableTiming),
                         "event create");
   }
@@ -554,11 +564,13 @@ int eprop_status(eprop_ctx* ctx) {
 
 void eprop_destroy(eprop_ctx* ctx) {
   if (!ctx) return;
-  if (ctx->fwd_stream) {
-    (void)hipStreamSynchronize(ctx->fwd_stream);
-    (void)hipStreamDestroy(ctx->fwd_stream);
+  for (hipStream_t st : {ctx->fwd_stream, ctx->coef_stream}) {
+    if (!st) continue;
+    (void)hipStreamSynchronize(st);
+    (void)hipStreamDestroy(st);
   }
-  hipEvent_t own[] = {ctx->ev_entry, ctx->ev_fwd[0], ctx->ev_fwd[1], ctx->ev_done[0], ctx->ev_done[1]};
+  hipEvent_t own[] = {ctx->ev_entry, ctx->ev_fwd[0],  ctx->ev_fwd[1], ctx->ev_coef[0],
+                      ctx->ev_coef[1], ctx->ev_done[0], ctx->ev_done[1]};
   for (hipEvent_t e : own)
     if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
