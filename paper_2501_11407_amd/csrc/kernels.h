@@ -7,8 +7,9 @@
 //   psiK   [Kmax*Bp][ldv]  pseudo-derivative (ldv = n_rec rounded to 256)
 //   deltaK [rows][ldk]     readout error (softmax - onehot)
 //   ztK    [rows][ldn]     kappa-filtered spikes
-//   z16    [B][Kmax/16][ldi][16] filtered presynaptic vector as scaled fp16
-//                                 pairs, one 32-bit word per step (see below)
+//   z16    [B][Kmax/4][ldi][4] filtered presynaptic vector as scaled fp16
+//                                pairs, one 32-bit word per step (see below),
+//                                16 bytes per row and step quad
 // Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
 // psiK) and the readout gradient dW_out += deltaK^T * ztK; then the block
 // coefficients of the eligibility recursion and the eligibility kernel, which
@@ -40,7 +41,7 @@ struct FwdLayer {
   float* y;                      // state [B][K_out]
   double* lossacc;               // [B]
   float* psiK;                   // [rows][ldj]
-  uint32_t* z16;                 // [B][Kmax/16][ldi][16]
+  uint32_t* z16;                 // [B][Kmax/4][ldi][4]
   float zscale;
   float* deltaK; float* ztK;     // [rows][ldk], [rows][ldn]
   int n_inl, n_pre, rows_per_wave, ldi;
@@ -114,7 +115,7 @@ struct TraceArgs {
   float* epsa;     // [B][n_pre_pad / 64][n_jt_a][64 * 64]
   double* acc;     // [n_split][n_pre_pad][ldj] (row-major)
   size_t acc_stride;
-  const uint32_t* z16;                // [B][kKC][ldi][16], ldi = n_pre_pad
+  const uint32_t* z16;                // [B][kKQ][ldi][4], ldi = n_pre_pad
   const uint32_t* U; const uint32_t* V; const uint32_t* H; const float* S;   // as CoefArgs
   int B, n_pre_pad, n_post, ldj, n_adaptive, ldi, ldc, kpad, n_split;
   int n_jt, n_jt_a;   // tiles along j: all, and those holding adaptive neurons

@@ -293,8 +293,8 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // Global stores of the step go last: a load waits for every store issued
   // before it, so stores ahead of the drive and readout loads would lengthen
   // the step.  Per-step vectors: psi, ztilde, the spike words, and the
-  // filtered presynaptic values as scaled fp16 pairs ([b][t/16][i][16] words,
-  // step t % 16).
+  // filtered presynaptic values as scaled fp16 pairs ([b][t/4][i][4] words,
+  // step t % 4: a wave's group store covers 64 consecutive 16-byte records).
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
     const int j = q * kFwdThreads + tid;
@@ -313,10 +313,10 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     Ly.deltaK[(row - A.Bp) * A.ldk + lane] = dk;
   // the pair words go out zgroup steps at a time (4 * zgroup bytes per row)
   if ((t & (A.zgroup - 1)) == A.zgroup - 1 || t == A.steps - 1) {
-    uint32_t* zpk = Ly.z16 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * kChunk + ((t % kChunk) & ~(A.zgroup - 1));
+    uint32_t* zpk = Ly.z16 + ((size_t)b * kKQ + t / 4) * Ly.ldi * 4 + ((t & 3) & ~(A.zgroup - 1));
     const int np = S.npre_total;
     for (int i = i_beg + lane; i < i_end; i += kWave) {
-      uint32_t* d = zpk + (size_t)i * kChunk;
+      uint32_t* d = zpk + (size_t)i * 4;
       if (A.zgroup == 4)
         *(u32x4*)d = u32x4{zring[i], zring[np + i], zring[2 * np + i], zring[3 * np + i]};
       else if (A.zgroup == 2)
@@ -390,6 +390,9 @@ __device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S,
 template <int QN, int NL>
 __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))) void forward_kernel(FwdArgs A) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  // the forward is the sequential part of the step: its waves win instruction
+  // issue over the eligibility waves that share their compute units
+  __builtin_amdgcn_s_setprio(3);
   const int b = blockIdx.x;
   FwdLds S;
   S.rwmax = A.L[0].rows_per_wave;
@@ -817,11 +820,12 @@ struct TraceTile {
   __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
     char* slot = (char*)(sm + sl * kSlot);
     const int rw = 16 * w + (lane >> 2);
-    const uint32_t unit = (uint32_t)((lane & 3) ^ (lane >> 4)) * 16u;
-    const size_t zc = ((size_t)b * kKC + c) * a.ldi + i0 + rw;
+    const uint32_t q = (uint32_t)((lane & 3) ^ (lane >> 4));
+    const uint32_t unit = q * 16u;
+    const size_t zq = ((size_t)b * kKQ + 4 * c + q) * a.ldi + i0 + rw;   // step quad 4c + q
     const size_t cc = ((size_t)b * kKC + c) * a.ldc + j0 + rw;
     float* dst = (float*)(slot + w * 1024);
-    dma16((const float*)((const char*)a.z16 + zc * 64 + unit), dst);
+    dma16((const float*)((const char*)a.z16 + zq * 16), dst);
     dma16((const float*)((const char*)a.U + cc * 64 + unit), dst + kOpBytes / 4);
     dma16((const float*)((const char*)a.H + cc * 64 + unit), dst + 2 * kOpBytes / 4);
     if constexpr (ALIF)
