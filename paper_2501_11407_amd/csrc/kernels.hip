@@ -814,13 +814,13 @@ struct TraceTile {
   // Copies of chunk c of batch element b into ring slot sl.  Wave w copies
   // rows 16w .. 16w+15 of each operand (1 KiB: lane l takes 16 bytes of row
   // 16w + l/4); within a row the four 16-byte units are stored in the order
-  // u ^ ((row / 4) % 4), which keeps the MFMA operand reads free of bank
+  // u ^ ((row / 2) % 4), which keeps the MFMA operand reads free of bank
   // conflicts.  With chunk 0 also the scalars (planes w and w + 4) into
   // scalar buffer par.
   __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
     char* slot = (char*)(sm + sl * kSlot);
     const int rw = 16 * w + (lane >> 2);
-    const uint32_t q = (uint32_t)((lane & 3) ^ (lane >> 4));
+    const uint32_t q = (uint32_t)((lane & 3) ^ ((lane >> 3) & 3));
     const uint32_t unit = q * 16u;
     const size_t zq = ((size_t)b * kKQ + 4 * c + q) * a.ldi + i0 + rw;   // step quad 4c + q
     const size_t cc = ((size_t)b * kKC + c) * a.ldc + j0 + rw;
@@ -931,7 +931,7 @@ struct TraceTile {
         // k slots: A = X's words as they are; B = (z_hi, z_hi) per step, then
         // (z_lo, 0) with the same A: X_hi z_hi + X_lo z_hi + X_hi z_lo.
         const char* slot = (const char*)(sm + (n % kRing) * kSlot);
-        const int sw = (r >> 2) & 3;   // unit order of this lane's rows
+        const int sw = (r >> 1) & 3;   // unit order of this lane's rows
         const f16x8 zero8 = {};
         f16x8 bz1[2], bz2[2];
 #pragma unroll
