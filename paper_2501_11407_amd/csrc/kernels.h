@@ -25,7 +25,8 @@ namespace eprop {
 
 constexpr int kFwdThreads = 512;               // forward workgroup: one batch element
 constexpr int kFwdWaves = kFwdThreads / 64;
-constexpr int kFwdXSteps = 8;                  // input spikes staged in shared memory per load
+constexpr int kFwdXSteps = 8;                  // steps of input spikes staged in shared memory
+constexpr int kXRegs = 2;                      // input words (or bytes) per thread prefetched per step
 constexpr int kBlockSteps = 256;       // timesteps per block (Kmax)
 constexpr int kKQ = kBlockSteps / 4;   // step quads per block
 constexpr int kTile = 64;              // eligibility workgroup tile: 64 (i) x 64 (j)

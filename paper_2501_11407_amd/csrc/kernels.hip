@@ -18,16 +18,30 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
-__device__ inline float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+// Wave-wide reductions with DPP lane moves (no shared-memory round trip):
+// within quads, half-rows and rows of 16 lanes, then across the four rows
+// (row broadcasts of lanes 15 and 31); lane 63 ends with the result, which is
+// returned to every lane.  Every lane must be active.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, ROWS, 0xF, false));
 }
-
+template <typename Op>
+__device__ __forceinline__ float wave_reduce(float v, Op op) {
+  v = op(v, dpp_move<0xB1, 0xF>(v));    // quad_perm [1,0,3,2]
+  v = op(v, dpp_move<0x4E, 0xF>(v));    // quad_perm [2,3,0,1]
+  v = op(v, dpp_move<0x141, 0xF>(v));   // row_half_mirror
+  v = op(v, dpp_move<0x140, 0xF>(v));   // row_mirror
+  v = op(v, dpp_move<0x142, 0xA>(v));   // row_bcast:15 into rows 1 and 3
+  v = op(v, dpp_move<0x143, 0xC>(v));   // row_bcast:31 into rows 2 and 3
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ inline float wave_max(float v) {
+  return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
+}
 __device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  return wave_reduce(v, [](float a, float b) { return a + b; });
 }
 
 __device__ inline int lanes_below(unsigned long long m, int lane) {
@@ -106,7 +120,8 @@ struct FwdLds {
   uint32_t* zh;                  // [zgroup][npre_total]: pair words of the last zgroup steps
   int npre_total;
   uint8_t* zc;
-  uint8_t* xs;
+  uint8_t* xs;                   // [kFwdXSteps][n_in]: input spikes of steps t .. t+7, row t % 8
+  bool xwords;                   // rows 4-byte aligned: input rows copied as 32-bit words
   int rwmax, npad;
 };
 
@@ -205,6 +220,26 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // lanes, and each row's load is a scalar row base plus the lane offset.
   constexpr int UB = QN >= 32 ? 1 : 32 / QN;
   const int total = S.cnt[2 * kFwdWaves];
+  // Input spikes of step t+kFwdXSteps: loaded here, under the drive loads,
+  // and written after them into the staging row of step t, which this step's
+  // list has already read.
+  uint32_t xr[kXRegs];
+  const bool xpre = LI == 0 && t + kFwdXSteps < A.steps;
+  const uint8_t* xrow = A.x + ((size_t)(t + kFwdXSteps) * A.B + b) * A.n_in;
+  if constexpr (LI == 0) {
+    if (xpre) {
+#pragma unroll
+      for (int m = 0; m < kXRegs; ++m) {
+        const int k = tid + m * kFwdThreads;
+        xr[m] = 0;
+        if (S.xwords) {
+          if (k < (A.n_in >> 2)) xr[m] = ((const uint32_t*)xrow)[k];
+        } else if (k < A.n_in) {
+          xr[m] = xrow[k];
+        }
+      }
+    }
+  }
   const uint32_t tidoff = (uint32_t)tid * 4u;
   float I[QN];
 #pragma unroll
@@ -234,6 +269,26 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
         for (int q = 0; q < QN; ++q) I[q] += wv[u][q];
   }
   if (soft) dk = softmax_lanes(A, part_prev, yk, label, loss);   // no active rows
+  if constexpr (LI == 0) {
+    if (xpre) {
+      uint8_t* xs = S.xs + (t % kFwdXSteps) * A.n_in;
+#pragma unroll
+      for (int m = 0; m < kXRegs; ++m) {
+        const int k = tid + m * kFwdThreads;
+        if (S.xwords) {
+          if (k < (A.n_in >> 2)) ((uint32_t*)xs)[k] = xr[m];
+        } else if (k < A.n_in) {
+          xs[k] = (uint8_t)xr[m];
+        }
+      }
+      // inputs wider than the registers cover (rare): the rest directly
+      const int nk = S.xwords ? (A.n_in >> 2) : A.n_in;
+      for (int k = tid + kXRegs * kFwdThreads; k < nk; k += kFwdThreads) {
+        if (S.xwords) ((uint32_t*)xs)[k] = ((const uint32_t*)xrow)[k];
+        else xs[k] = xrow[k];
+      }
+    }
+  }
   int n_spk = 0;
   float psv[QN];
   unsigned long long smask[QN];
@@ -411,6 +466,7 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
   S.npre_total = npre_total;
   S.zc = (uint8_t*)(S.zh + A.zgroup * npre_total);   // [n_layers][2][npad]
   S.xs = S.zc + NL * 2 * S.npad;               // [kFwdXSteps][n_in]
+  S.xwords = (A.n_in & 3) == 0 && ((uintptr_t)A.x & 3) == 0;
 
   for (int e = threadIdx.x; e < A.zgroup * npre_total; e += kFwdThreads) S.zh[e] = 0u;
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
@@ -428,19 +484,14 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
     y0 = S.sy[lane];
     if constexpr (NL > 1) y1 = S.sy[A.K_out + lane];
   }
+  // input spikes of the first kFwdXSteps steps; each step then loads the
+  // row kFwdXSteps ahead
+  for (int tt = 0; tt < min(kFwdXSteps, A.steps); ++tt) {
+    const uint8_t* xrow = A.x + ((size_t)tt * A.B + b) * A.n_in;
+    for (int i = threadIdx.x; i < A.n_in; i += kFwdThreads) S.xs[tt * A.n_in + i] = xrow[i];
+  }
+  lds_barrier();
   for (int t = 0; t < A.steps; ++t) {
-    if (t % kFwdXSteps == 0) {
-      // stage the input spikes of the next kFwdXSteps steps (one round trip)
-      const int ns = min(kFwdXSteps, A.steps - t);
-#pragma unroll
-      for (int tt = 0; tt < kFwdXSteps; ++tt) {
-        if (tt < ns) {
-          const uint8_t* xrow = A.x + ((size_t)(t + tt) * A.B + b) * A.n_in;
-          for (int i = threadIdx.x; i < A.n_in; i += kFwdThreads) S.xs[tt * A.n_in + i] = xrow[i];
-        }
-      }
-      lds_barrier();
-    }
     forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0, label, y0, d0);
     if constexpr (NL > 1)
       forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1, label, y1, d1);
