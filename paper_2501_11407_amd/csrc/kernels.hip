@@ -17,6 +17,7 @@ namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
+constexpr int kSoftWave = kFwdWaves - 1;   // forward wave that runs the softmax
 
 // Wave-wide reductions with DPP lane moves (no shared-memory round trip):
 // within quads, half-rows and rows of 16 lanes, then across the four rows
@@ -112,7 +113,7 @@ __device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChu
 //        psi = (gamma/thr) * max(0, 1 - |x|/thr)
 //   3. each wave sums the readout weights of its spiking neurons for every
 //      class; ztilde = kappa*ztilde + z.
-//   4. wave 0: y = kappa*y + (sum of the waves' partial sums, in wave order),
+//   4. the last wave: y = kappa*y + (sum of the waves' partial sums, in wave order),
 //      softmax, delta = softmax - onehot(label), cross-entropy into the loss.
 // The learning signal L = W_out^T delta is one GEMM over the whole block.
 struct FwdLds {
@@ -125,21 +126,26 @@ struct FwdLds {
   int rwmax, npad;
 };
 
-// Softmax cross-entropy of one step for K_out <= 64, in wave 0: lane k holds
+// Softmax cross-entropy of one step for K_out <= 64, in one wave: lane k holds
 // class k's output y (updated here) and gets delta_k = softmax_k - onehot_k.
 // The waves' partial sums are added in wave order.
 __device__ __forceinline__ float softmax_lanes(const FwdArgs& A, const float* part, float& y,
                                                int label, double& loss) {
   const int lane = threadIdx.x & (kWave - 1);
   const bool in = lane < A.K_out;
+  // all partial sums read before any is used (lanes past K_out read class 0)
+  const int kc = in ? lane : 0;
+  float pw[kFwdWaves];
+#pragma unroll
+  for (int ww = 0; ww < kFwdWaves; ++ww) pw[ww] = part[ww * A.K_out + kc];
   float Y = 0.0f;
 #pragma unroll
-  for (int ww = 0; ww < kFwdWaves; ++ww) Y += in ? part[ww * A.K_out + lane] : 0.0f;
+  for (int ww = 0; ww < kFwdWaves; ++ww) Y += pw[ww];
   float yy = A.kappa * y;
   yy = yy + Y;
   if (in) y = yy;
   const float m = wave_max(in ? yy : -INFINITY);
-  const float ex = in ? expf(yy - m) : 0.0f;
+  const float ex = expf(in ? yy - m : -INFINITY);   // 0 past K_out
   const float se = wave_sum(ex);
   const bool label_ok = label >= 0 && label < A.K_out;
   const float yl = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(yy), label_ok ? label : 0));
@@ -174,11 +180,12 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // readout partial sums of this step and of the step before (by parity)
   float* part = S.part + (LI * 2 + (t & 1)) * kFwdWaves * A.K_out;
   const float* part_prev = S.part + (LI * 2 + ((t + 1) & 1)) * kFwdWaves * A.K_out;
-  // K_out <= 64: wave 0 takes the previous step's softmax while its first
-  // batch of drive loads is in flight, and stores delta with this step's
-  // stores; the block's last step is finished after the step loop
+  // K_out <= 64: the last wave, which holds the fewest presynaptic rows,
+  // takes the previous step's softmax while the others build their lists,
+  // and stores delta with this step's stores; the block's last step is
+  // finished after the step loop
   const bool defer = A.K_out <= kWave;
-  bool soft = defer && w == 0 && t > 0;
+  if (defer && w == kSoftWave && t > 0) dk = softmax_lanes(A, part_prev, yk, label, loss);
 
   // 1. presynaptic vector, its filter, ordered active lists
   const int rw = Ly.rows_per_wave;
@@ -257,18 +264,12 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
                        ? *(const float*)(rowp + tidoff + (uint32_t)q * kFwdThreads * 4u)
                        : 0.0f;
     }
-    if (soft) {
-      asm volatile("" ::: "memory");
-      dk = softmax_lanes(A, part_prev, yk, label, loss);
-      soft = false;
-    }
 #pragma unroll
     for (int u = 0; u < UB; ++u)
       if (k0 + u < total)
 #pragma unroll
         for (int q = 0; q < QN; ++q) I[q] += wv[u][q];
   }
-  if (soft) dk = softmax_lanes(A, part_prev, yk, label, loss);   // no active rows
   if constexpr (LI == 0) {
     if (xpre) {
       uint8_t* xs = S.xs + (t % kFwdXSteps) * A.n_in;
@@ -364,7 +365,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       if (lane == 1 && w0 + 1 < A.W32) srow[w0 + 1] = (uint32_t)(smask[q] >> 32);
     }
   }
-  if (defer && w == 0 && t > 0 && lane < A.K_out)
+  if (defer && w == kSoftWave && t > 0 && lane < A.K_out)
     Ly.deltaK[(row - A.Bp) * A.ldk + lane] = dk;
   // the pair words go out zgroup steps at a time (4 * zgroup bytes per row)
   if ((t & (A.zgroup - 1)) == A.zgroup - 1 || t == A.steps - 1) {
@@ -382,8 +383,8 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   }
   lds_barrier();
 
-  // 4. readout, softmax cross-entropy (wave 0; the other waves go on)
-  if (!defer && w == 0) {
+  // 4. readout, softmax cross-entropy (K_out > 64; the other waves go on)
+  if (!defer && w == kSoftWave) {
     const bool label_ok = label >= 0 && label < A.K_out;
     float m = -INFINITY;
     for (int k = lane; k < A.K_out; k += kWave) {
@@ -477,7 +478,7 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
   const int label = __builtin_amdgcn_readfirstlane(A.labels[b]);
   int cur = 0;
   lds_barrier();
-  // deferred softmax state (wave 0, lane k: class k)
+  // deferred softmax state (the softmax wave, lane k: class k)
   const int lane = threadIdx.x & (kWave - 1);
   float y0 = 0.0f, y1 = 0.0f, d0 = 0.0f, d1 = 0.0f;
   if (lane < A.K_out) {
@@ -497,7 +498,7 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
       forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1, label, y1, d1);
     cur ^= 1;
   }
-  if (A.K_out <= kWave && threadIdx.x < kWave && A.steps > 0) {
+  if (A.K_out <= kWave && (threadIdx.x >> 6) == kSoftWave && A.steps > 0) {
     // the last step's softmax (its partial sums are visible: every step ends
     // with a barrier)
     const int tl = A.steps - 1;
@@ -518,7 +519,7 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
   lds_barrier();
   forward_state<QN, 0>(A, S, b, false, v0, a0, zt0, cur);
   if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, false, v1, a1, zt1, cur);
-  if (threadIdx.x == 0) {
+  if (threadIdx.x == kSoftWave * kWave) {   // lane 0 of the softmax wave holds the loss
     A.L[0].lossacc[b] += loss0;
     if constexpr (NL > 1) A.L[1].lossacc[b] += loss1;
   }
