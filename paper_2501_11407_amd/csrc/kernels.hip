@@ -869,24 +869,35 @@ struct TraceTile {
   // u ^ ((row / 2) % 4), which keeps the MFMA operand reads free of bank
   // conflicts.  With chunk 0 also the scalars (planes w and w + 4) into
   // scalar buffer par.
+  // The copies are issued in two parts (P = 0: z and U; P = 1: H, V and the
+  // scalars), placed between MFMAs so that the vector-memory path works while
+  // the matrix cores do; the order of all copies is that of the full issue.
+  template <int P>
   __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
     char* slot = (char*)(sm + sl * kSlot);
     const int rw = 16 * w + (lane >> 2);
     const uint32_t q = (uint32_t)((lane & 3) ^ ((lane >> 3) & 3));
     const uint32_t unit = q * 16u;
-    const size_t zq = ((size_t)b * kKQ + 4 * c + q) * a.ldi + i0 + rw;   // step quad 4c + q
     const size_t cc = ((size_t)b * kKC + c) * a.ldc + j0 + rw;
     float* dst = (float*)(slot + w * 1024);
-    dma16((const float*)((const char*)a.z16 + zq * 16), dst);
-    dma16((const float*)((const char*)a.U + cc * 64 + unit), dst + kOpBytes / 4);
-    dma16((const float*)((const char*)a.H + cc * 64 + unit), dst + 2 * kOpBytes / 4);
-    if constexpr (ALIF)
-      dma16((const float*)((const char*)a.V + cc * 64 + unit), dst + 3 * kOpBytes / 4);
-    if (c == 0 && lane < 16) {
-      float* sb = sm + kRing * kSlot + par * kScal;
-      dma16(a.S + ((size_t)w * a.B + b) * a.ldc + j0 + lane * 4, sb + w * kTile);
-      dma16(a.S + ((size_t)(w + 4) * a.B + b) * a.ldc + j0 + lane * 4, sb + (w + 4) * kTile);
+    if constexpr (P == 0) {
+      const size_t zq = ((size_t)b * kKQ + 4 * c + q) * a.ldi + i0 + rw;   // step quad 4c + q
+      dma16((const float*)((const char*)a.z16 + zq * 16), dst);
+      dma16((const float*)((const char*)a.U + cc * 64 + unit), dst + kOpBytes / 4);
+    } else {
+      dma16((const float*)((const char*)a.H + cc * 64 + unit), dst + 2 * kOpBytes / 4);
+      if constexpr (ALIF)
+        dma16((const float*)((const char*)a.V + cc * 64 + unit), dst + 3 * kOpBytes / 4);
+      if (c == 0 && lane < 16) {
+        float* sb = sm + kRing * kSlot + par * kScal;
+        dma16(a.S + ((size_t)w * a.B + b) * a.ldc + j0 + lane * 4, sb + w * kTile);
+        dma16(a.S + ((size_t)(w + 4) * a.B + b) * a.ldc + j0 + lane * 4, sb + (w + 4) * kTile);
+      }
     }
+  }
+  __device__ __forceinline__ void issue_all(int b, int c, int sl, int par) const {
+    issue<0>(b, c, sl, par);
+    issue<1>(b, c, sl, par);
   }
 
   // block-start traces of batch element b into E/A
@@ -950,7 +961,7 @@ struct TraceTile {
       E[x >> 1][x & 1] = A[x >> 1][x & 1] = zero;
     }
 #pragma unroll
-    for (int c = 0; c < D; ++c) issue(split, c, c, 0);
+    for (int c = 0; c < D; ++c) issue_all(split, c, c, 0);
     for (int k = 0; k < nk; ++k) {
       const int b = split + k * a.n_split;
       const bool next = k + 1 < nk;
@@ -971,12 +982,15 @@ struct TraceTile {
           if constexpr (D == NCH) wg_barrier();
           __builtin_amdgcn_sched_barrier(0);
         }
+        // copies of chunk n + D (part P), placed inside the MFMA section
         constexpr int c2 = ch + D;
-        if constexpr (c2 < NCH)
-          issue(b, c2, (n + D) % kRing, k & 1);
-        else if (next)
-          issue(b + a.n_split, c2 - NCH, (n + D) % kRing, (k + 1) & 1);
-        if constexpr (ch == 0) load_traces(b, E, A);
+        auto issue_next = [&](auto pc) {
+          constexpr int P = decltype(pc)::value;
+          if constexpr (c2 < NCH)
+            issue<P>(b, c2, (n + D) % kRing, k & 1);
+          else if (next)
+            issue<P>(b + a.n_split, c2 - NCH, (n + D) % kRing, (k + 1) & 1);
+        };
 
         // Per output block and contraction X, two fp16 MFMAs (K = 32) over the
         // chunk's 16 steps.  Lane g holds steps 4g..4g+3 as (hi, lo) pairs of
@@ -1009,7 +1023,7 @@ struct TraceTile {
                         ? *(const f16x8*)(slot + (X + 1) * kOpBytes + cr * 64 + ((g ^ sw) << 4))
                         : zero8;
 #pragma unroll
-          for (int pass = 0; pass < 2; ++pass)
+          for (int pass = 0; pass < 2; ++pass) {
 #pragma unroll
             for (int bi = 0; bi < 2; ++bi) {
               const f16x8 bz = pass == 0 ? bz1[bi] : bz2[bi];
@@ -1018,6 +1032,18 @@ struct TraceTile {
               if constexpr (ALIF)
                 cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[2], bz, cV[bj][bi], 0, 0, 0);
             }
+            if (pass == 0) {
+              __builtin_amdgcn_sched_barrier(0);
+              if (bj == 0) {
+                issue_next(std::integral_constant<int, 0>{});
+              } else {
+                issue_next(std::integral_constant<int, 1>{});
+                // the element's block-start traces, after chunk 0's copies
+                if constexpr (ch == 0) load_traces(b, E, A);
+              }
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
       };
