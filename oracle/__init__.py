@@ -51,6 +51,13 @@ def load(path: str = LIB_PATH):
         ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p,
     ]
+    lib.oracle_eprop_run_fb.restype = ctypes.c_int
+    lib.oracle_eprop_run_fb.argtypes = [
+        ctypes.POINTER(OracleConfig), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p,
+    ]
     lib.oracle_state_bytes.restype = ctypes.c_size_t
     lib.oracle_state_bytes.argtypes = [ctypes.POINTER(OracleConfig), ctypes.c_int32]
     if path == LIB_PATH:
@@ -91,11 +98,13 @@ def run(shape, W: Sequence[np.ndarray], Wout: Sequence[np.ndarray], x: np.ndarra
         sample: Optional[np.ndarray] = None, want_spikes: bool = True, want_record: bool = False,
         fwd_fp32: bool = True, smooth: bool = False, reset: Optional[float] = None,
         spikes_out: Optional[np.ndarray] = None, lib_path: str = LIB_PATH,
-        **over) -> OracleResult:
+        feedback: Optional[Sequence[np.ndarray]] = None, **over) -> OracleResult:
     """Runs the oracle on batch elements [b_lo, b_hi).  ``sample`` is an int32
     array of (layer, j, i) rows; when given, only those synapses' gradients are
     computed (returned as dW[0] of length len(sample)).  ``spikes_out``, if
-    given, is the uint32 [T, L, B, ceil(n_rec/32)] record to write into."""
+    given, is the uint32 [T, L, B, ceil(n_rec/32)] record to write into.
+    ``feedback``: per layer the fixed matrix B [n_out, n_rec] of the learning
+    signal L = B^T delta (None: W_out)."""
     lib = load(lib_path)
     cfg = make_config(shape, fwd_fp32=fwd_fp32, smooth=smooth, reset=reset, **over)
     T = x.shape[0] if T is None else T
@@ -132,12 +141,19 @@ def run(shape, W: Sequence[np.ndarray], Wout: Sequence[np.ndarray], x: np.ndarra
         recs = {k: np.zeros((T, L, B, N)) for k in ("v", "a", "psi", "L", "z")}
         recs["y"] = np.zeros((T, L, B, K))
         rec = OracleRecord(*[_ptr(recs[k]) for k in ("v", "a", "psi", "L", "z", "y")])
-    rc = lib.oracle_eprop_run(ctypes.byref(cfg), ctypes.cast(Wp, ctypes.c_void_p),
-                              ctypes.cast(Wop, ctypes.c_void_p), _ptr(xc), T, _ptr(lab),
-                              b_lo, b_hi, smp_ptr, n_sample,
-                              _ptr(spikes) if spikes is not None else None,
-                              ctypes.cast(dWp, ctypes.c_void_p), ctypes.cast(dWop, ctypes.c_void_p),
-                              _ptr(loss), ctypes.byref(rec) if rec is not None else None)
+    Fbp = None
+    if feedback is not None:
+        Fbc = [np.ascontiguousarray(f, dtype=np.float32) for f in feedback]
+        assert len(Fbc) == L and all(f.shape == (K, N) for f in Fbc)
+        Fbp = (ctypes.c_void_p * L)(*[_ptr(f) for f in Fbc])
+    rc = lib.oracle_eprop_run_fb(ctypes.byref(cfg), ctypes.cast(Wp, ctypes.c_void_p),
+                                 ctypes.cast(Wop, ctypes.c_void_p),
+                                 ctypes.cast(Fbp, ctypes.c_void_p) if Fbp is not None else None,
+                                 _ptr(xc), T, _ptr(lab), b_lo, b_hi, smp_ptr, n_sample,
+                                 _ptr(spikes) if spikes is not None else None,
+                                 ctypes.cast(dWp, ctypes.c_void_p),
+                                 ctypes.cast(dWop, ctypes.c_void_p),
+                                 _ptr(loss), ctypes.byref(rec) if rec is not None else None)
     if rc != 0:
         raise ValueError(f"oracle_eprop_run returned {rc}")
     return OracleResult(dW=dW, dWout=dWout, loss=float(loss[0]), spikes=spikes, record=recs)

@@ -33,6 +33,10 @@
 //   * readout y^t = kappa*y^{t-1} + W_out z^t, no bias; learning signal
 //     L = W_out^T (softmax(y) - onehot(label)); the kappa filter of the readout
 //     moves onto the trace (ebar), which makes the forward sum exact;
+//   * optional fixed feedback: L = B^T (softmax(y) - onehot(label)) with a
+//     matrix B of W_out's shape in place of W_out (random feedback weights,
+//     the readout approximation that the source of Sec. III-B names and sets
+//     aside); only the learning signal changes;
 //   * two-layer stacks: layer 2 reads layer-1 spikes of the same step,
 //     gradient-stopped, and has its own readout and loss;
 //   * the recurrent-weight diagonal (no self-connections) gets gradient 0.
@@ -108,7 +112,7 @@ struct LayerState {
 
 template <typename R>
 int run(const oracle_config& c, const float* const* W, const float* const* Wout,
-        const uint8_t* x, int T, const int32_t* labels, int b_lo, int b_hi,
+        const float* const* Fb, const uint8_t* x, int T, const int32_t* labels, int b_lo, int b_hi,
         const Synapse* sample, int n_sample, uint32_t* spikes, double* const* dW,
         double* const* dWout, double* loss, const oracle_record* rec) {
   const int NL = c.n_layers, B = c.batch, N = c.n_rec, K = c.n_out, NA = c.n_adaptive;
@@ -167,6 +171,7 @@ int run(const oracle_config& c, const float* const* W, const float* const* Wout,
         LayerState<R>& s = st[l];
         const float* Wl = W[l];
         const float* Wo = Wout[l];
+        const float* Fo = (Fb && Fb[l]) ? Fb[l] : Wo;   // feedback matrix of the learning signal
 
         // Presynaptic vector p^t = [input^t ; z^{t-1}] and its alpha filter:
         // the eps^v component of G_t, since dv/dv = alpha and dv/dW_ji = p_i.
@@ -221,7 +226,7 @@ int run(const oracle_config& c, const float* const* W, const float* const* Wout,
         loss_sum += std::log(se) - (s.y[label] - m);
         for (int j = 0; j < N; ++j) {
           double Lj = 0.0;
-          for (int k = 0; k < K; ++k) Lj += (double)Wo[(size_t)k * N + j] * s.delta[k];
+          for (int k = 0; k < K; ++k) Lj += (double)Fo[(size_t)k * N + j] * s.delta[k];
           s.L[j] = Lj;
           s.ztil[j] = c.kappa * s.ztil[j] + s.z[j];
         }
@@ -339,11 +344,13 @@ size_t oracle_state_bytes(const oracle_config* c, int32_t n_sample) {
 //   spikes: NULL or [T][n_layers][batch][ceil(n_rec/32)], bit j%32 of word j/32
 //   dWout[l]: [n_out][n_rec];  loss: sum over b, t, layers of the cross-entropy
 // Returns 0, or -1 on an invalid argument.
-int oracle_eprop_run(const oracle_config* c, const float* const* W, const float* const* Wout,
-                     const uint8_t* x, int32_t T, const int32_t* labels, int32_t b_lo,
-                     int32_t b_hi, const int32_t* sample, int32_t n_sample, uint32_t* spikes,
-                     double* const* dW, double* const* dWout, double* loss,
-                     const oracle_record* rec) {
+//   Fb: NULL, or per layer NULL or the feedback matrix B [n_out][n_rec] fp32
+//       of the learning signal L = B^T delta (NULL: B = W_out).
+int oracle_eprop_run_fb(const oracle_config* c, const float* const* W, const float* const* Wout,
+                        const float* const* Fb, const uint8_t* x, int32_t T,
+                        const int32_t* labels, int32_t b_lo, int32_t b_hi, const int32_t* sample,
+                        int32_t n_sample, uint32_t* spikes, double* const* dW,
+                        double* const* dWout, double* loss, const oracle_record* rec) {
   if (!valid(c) || !W || !Wout || !x || !labels || !dW || !dWout || !loss || T < 0 ||
       b_lo < 0 || b_hi > c->batch || b_lo > b_hi || (n_sample >= 0 && !sample))
     return -1;
@@ -357,10 +364,20 @@ int oracle_eprop_run(const oracle_config* c, const float* const* W, const float*
     if (smp[q].j < 0 || smp[q].j >= c->n_rec || smp[q].i < 0 || smp[q].i >= n_pre) return -1;
   }
   if (c->fwd_fp32)
-    return run<float>(*c, W, Wout, x, T, labels, b_lo, b_hi, smp, n_sample, spikes, dW, dWout,
+    return run<float>(*c, W, Wout, Fb, x, T, labels, b_lo, b_hi, smp, n_sample, spikes, dW, dWout,
                       loss, rec);
-  return run<double>(*c, W, Wout, x, T, labels, b_lo, b_hi, smp, n_sample, spikes, dW, dWout,
+  return run<double>(*c, W, Wout, Fb, x, T, labels, b_lo, b_hi, smp, n_sample, spikes, dW, dWout,
                      loss, rec);
+}
+
+// The same with the learning signal through W_out (symmetric feedback).
+int oracle_eprop_run(const oracle_config* c, const float* const* W, const float* const* Wout,
+                     const uint8_t* x, int32_t T, const int32_t* labels, int32_t b_lo,
+                     int32_t b_hi, const int32_t* sample, int32_t n_sample, uint32_t* spikes,
+                     double* const* dW, double* const* dWout, double* loss,
+                     const oracle_record* rec) {
+  return oracle_eprop_run_fb(c, W, Wout, nullptr, x, T, labels, b_lo, b_hi, sample, n_sample,
+                             spikes, dW, dWout, loss, rec);
 }
 
 }  // extern "C"

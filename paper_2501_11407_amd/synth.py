@@ -132,6 +132,16 @@ def make_weights(shape: EpropShape, rng: np.random.Generator):
     return W, Wout
 
 
+def make_feedback(shape: EpropShape, seed: int) -> List[np.ndarray]:
+    """Fixed random feedback matrices B [K, N_rec] per layer for the
+    learning signal L = B^T delta: drawn like W_out (N(0, 1/N_rec), on the
+    weight grid) from their own generator."""
+    rng = np.random.Generator(np.random.PCG64(10_000 + seed))
+    return [np.ascontiguousarray(quantize(rng.normal(0.0, 1.0 / math.sqrt(shape.n_rec),
+                                                     size=(shape.n_out, shape.n_rec)), shape.n_rec))
+            for _ in range(shape.n_layers)]
+
+
 def make_workload(shape: EpropShape, seed: int, T: Optional[int] = None,
                   input_scale: float = 1.0) -> Workload:
     """Draw a workload with a fixed draw order: rates, then per layer W_in,

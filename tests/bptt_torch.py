@@ -35,11 +35,29 @@ class _Spike(torch.autograd.Function):
         return g * psi, None, None
 
 
-def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True):
+class _Readout(torch.autograd.Function):
+    """y = z W_out^T whose backward sends dy to z through a fixed feedback
+    matrix F [K, N] instead of W_out (F = W_out gives the ordinary product);
+    the gradient of W_out itself is the ordinary one."""
+
+    @staticmethod
+    def forward(ctx, z, wo, fb):
+        ctx.save_for_backward(z, fb)
+        return z @ wo.T
+
+    @staticmethod
+    def backward(ctx, g):
+        z, fb = ctx.saved_tensors
+        return g @ fb, g.T @ z, None
+
+
+def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedback=None):
     """Returns (dW list, dWout list, loss) as float64 numpy arrays.
 
     ``stop=False`` keeps every path (true surrogate gradient); it is only used
-    to show the gradient stops matter.
+    to show the gradient stops matter.  ``feedback``: per layer a matrix of
+    W_out's shape that carries the readout's gradient back to the spikes in
+    place of W_out (random-feedback learning signal).
     """
     T = x.shape[0] if T is None else T
     L, B, N = shape.n_layers, shape.batch, shape.n_rec
@@ -47,6 +65,7 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True):
     sg = (lambda v: v.detach()) if stop else (lambda v: v)
     Ws = [torch.tensor(np.asarray(w, dtype=np.float64), requires_grad=True) for w in W]
     Wos = [torch.tensor(np.asarray(w, dtype=np.float64), requires_grad=True) for w in Wout]
+    Fbs = None if feedback is None else [torch.tensor(np.asarray(f, dtype=np.float64)) for f in feedback]
     beta = torch.zeros(N, dtype=F64)
     beta[: shape.n_adaptive] = shape.beta
     lab = torch.tensor(np.asarray(labels, dtype=np.int64))
@@ -70,7 +89,8 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True):
             A = beta * al
             A = shape.thr + A
             z = _Spike.apply(vl - A, shape.gamma, shape.thr)
-            y[l] = shape.kappa * y[l] + z @ Wos[l].T
+            yz = z @ Wos[l].T if Fbs is None else _Readout.apply(z, Wos[l], Fbs[l])
+            y[l] = shape.kappa * y[l] + yz
             loss = loss + torch.nn.functional.cross_entropy(y[l], lab, reduction="sum")
             v[l], a[l] = vl, al
             z_now.append(z)

@@ -28,8 +28,11 @@ MUTANTS = [
     ("presyn_filter_kappa", "s.zbar[i] = c.alpha * s.zbar[i] + s.p[i];",
      "s.zbar[i] = c.kappa * s.zbar[i] + s.p[i];", 1),
     ("delta_sign", "- (k == label ? 1.0 : 0.0);", "+ (k == label ? 1.0 : 0.0);", 1),
-    ("learning_signal_transposed", "Lj += (double)Wo[(size_t)k * N + j] * s.delta[k];",
-     "Lj += (double)Wo[(size_t)j * K + k] * s.delta[k];", 1),
+    ("learning_signal_transposed", "Lj += (double)Fo[(size_t)k * N + j] * s.delta[k];",
+     "Lj += (double)Fo[(size_t)j * K + k] * s.delta[k];", 1),
+    ("feedback_ignored", "const float* Fo = (Fb && Fb[l]) ? Fb[l] : Wo;", "const float* Fo = Wo;", 1),
+    ("feedback_in_readout", "if (s.z[j] != 0.0) Y += (double)Wo[(size_t)k * N + j] * s.z[j];",
+     "if (s.z[j] != 0.0) Y += (double)Fo[(size_t)k * N + j] * s.z[j];", 1),
     ("surrogate_unclamped", "(u > 0.0 ? u : 0.0)", "u", 1),
     ("adaptation_path_dropped", "a = a + zp;", "a = a + R(0) * zp;", 1),
     ("reset_dropped", "v = v - reset * zp;", "v = v - R(0) * zp;", 1),

@@ -65,6 +65,48 @@ def test_oracle_equals_backprop_with_stop_gradients(name):
         assert rel_l2(r.dWout[l], dWout[l]) <= 1e-11
 
 
+FEEDBACK_CASES = ["ff_lif_b4_n32_t50", "rlif_ragged", "ralif_ragged", "ralif2_two_layers"]
+
+
+@pytest.mark.parametrize("name", FEEDBACK_CASES)
+def test_random_feedback_equals_backprop_with_feedback_readout(name):
+    # Fixed feedback B in the learning signal, L = B^T delta: e-prop with the
+    # stops equals reverse-mode autograd of the same network in which only
+    # the readout's backward edge to the spikes carries B instead of W_out.
+    shape, seed, scale = AUTOGRAD_CASES[name]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    fb = synth.make_feedback(shape, seed)
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False, feedback=fb)
+    dW, dWout, loss = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels, feedback=fb)
+    assert r.spikes.any()
+    assert abs(r.loss - loss) <= 1e-12 * abs(loss)
+    for l in range(shape.n_layers):
+        assert rel_l2(r.dW[l], dW[l]) <= 1e-11, (l, rel_l2(r.dW[l], dW[l]))
+        assert rel_l2(r.dWout[l], dWout[l]) <= 1e-11
+    # and it is a different gradient from the symmetric one
+    sym = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    assert rel_l2(r.dW[0], sym.dW[0]) > 1e-2
+
+
+def test_feedback_is_linear_and_leaves_the_forward_alone():
+    # dW = sum_t L ebar with L = B^T delta: linear in B; spikes, loss and the
+    # readout gradient do not depend on B; B = W_out is the symmetric case.
+    shape, seed, scale = AUTOGRAD_CASES["ralif_ragged"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    f1 = synth.make_feedback(shape, 1)[0]
+    f2 = synth.make_feedback(shape, 2)[0]
+    run = lambda fb: oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False,
+                                feedback=None if fb is None else [fb])
+    r1, r2, r12 = run(f1), run(f2), run(f1 + f2)   # sums of grid values stay exact in fp32
+    assert rel_l2(r12.dW[0], r1.dW[0] + r2.dW[0]) <= 1e-12
+    for r in (r2, r12):
+        assert np.array_equal(r.spikes, r1.spikes)
+        assert r.loss == r1.loss
+        assert np.array_equal(r.dWout[0], r1.dWout[0])
+    sym, same = run(None), run(wl.Wout[0])
+    assert np.array_equal(sym.dW[0], same.dW[0])
+
+
 def test_recurrence_breaks_exactness():
     # Without the stops the true surrogate gradient differs: the stops are real.
     shape, seed, scale = AUTOGRAD_CASES["ralif_ragged"]
