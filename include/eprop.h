@@ -158,6 +158,21 @@ int eprop_reset(eprop_ctx* ctx);
  */
 int eprop_status(eprop_ctx* ctx);
 
+/*
+ * Learning signal through fixed feedback matrices instead of the readout
+ * weights: L = B^T (softmax(y) - onehot(label)) per layer, the random-feedback
+ * alternative to the readout's gradient that the source of the paper's
+ * Sec. III-B names and sets aside.  Only the learning signal changes; the
+ * readout, the loss and the readout gradient still use W_out.
+ *   d_feedback: NULL (every layer back to B = W_out), or a host array of
+ *     n_layers device pointers, each NULL (that layer: B = W_out) or B fp32
+ *     [n_out][n_rec] row-major, the layout of W_out.
+ * The matrices are read here (queued on the context's stream) and again by
+ * every eprop_reset, must not be freed while set, and apply from the next
+ * step on.  Returns 0, EPROP_ESTATE on an unusable context.
+ */
+int eprop_set_feedback(eprop_ctx* ctx, const float* const* d_feedback);
+
 /* Frees the host-side context; the workspace and weights stay the caller's. */
 void eprop_destroy(eprop_ctx* ctx);
 

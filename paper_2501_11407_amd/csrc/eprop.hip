@@ -50,7 +50,8 @@ struct Layer {
   int rows_per_wave = 0;
   const float* W_src = nullptr;
   const float* Wout_src = nullptr;
-  float *Wt, *WoutT;                     // packed weights
+  const float* Fb_src = nullptr;         // feedback matrix of the learning signal (NULL: W_out)
+  float *Wt, *WoutT, *FbT;               // packed weights
   float *v, *a, *ztil, *zbar, *y;        // neuron, filter and readout state
   uint8_t* z;                            // spikes of the last step
   double* lossacc;                       // [B]
@@ -147,6 +148,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     const size_t np = L.n_pre, npp = L.n_pre_pad;
     L.Wt = (float*)take(sizeof(float) * np * L.ldw);
     L.WoutT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
+    L.FbT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.v = (float*)take(sizeof(float) * B * N);
     L.a = (float*)take(sizeof(float) * B * N);
     L.ztil = (float*)take(sizeof(float) * B * N);
@@ -264,10 +266,16 @@ int pack_weights(eprop_ctx* ctx) {
     int rc = check(ctx, eprop::launch_pack(L.W_src, c.n_rec, L.n_pre, L.Wt, L.ldw, L.n_pre, 1,
                                            ctx->stream), "weight packing");
     if (rc) return rc;
-    // WoutT[j][k] = Wout[k][j]: the B operand of the learning-signal GEMM
+    // WoutT[j][k] = Wout[k][j]: the readout, and the B operand of the
+    // learning-signal GEMM unless a feedback matrix is set (packed the same way)
     rc = check(ctx, eprop::launch_pack(L.Wout_src, c.n_out, c.n_rec, L.WoutT, ctx->plan.ldk,
                                        ctx->plan.ldn, 1, ctx->stream), "readout weight packing");
     if (rc) return rc;
+    if (L.Fb_src) {
+      rc = check(ctx, eprop::launch_pack(L.Fb_src, c.n_out, c.n_rec, L.FbT, ctx->plan.ldk,
+                                         ctx->plan.ldn, 1, ctx->stream), "feedback matrix packing");
+      if (rc) return rc;
+    }
   }
   return EPROP_OK;
 }
@@ -343,7 +351,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     Layer& L = ctx->plan.layers[l];
     // learning signal L[(t,b)][j] = sum_k delta[(t,b)][k] W_out[k][j]
     eprop::GemmArgs gl;
-    gl.A = L.deltaK[sl]; gl.Bm = L.WoutT; gl.C = L.LK[sl];
+    gl.A = L.deltaK[sl]; gl.Bm = L.Fb_src ? L.FbT : L.WoutT; gl.C = L.LK[sl];
     gl.M = rows; gl.N = c.n_rec; gl.K = P.ldk; gl.lda = P.ldk; gl.ldb = P.ldk; gl.ldc = L.ldv;
     gl.splits = 1; gl.k_chunk = P.ldk; gl.split_stride = 0;
     if ((rc = check(ctx, eprop::launch_gemm_nt(gl, sc), "learning-signal GEMM"))) return rc;
@@ -549,6 +557,13 @@ int eprop_reset(eprop_ctx* ctx) {
   int rc = pack_weights(ctx);
   if (!rc) rc = clear_state(ctx);
   return rc;
+}
+
+int eprop_set_feedback(eprop_ctx* ctx, const float* const* d_feedback) {
+  if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
+  for (int l = 0; l < ctx->plan.cfg.n_layers; ++l)
+    ctx->plan.layers[l].Fb_src = d_feedback ? d_feedback[l] : nullptr;
+  return pack_weights(ctx);
 }
 
 int eprop_status(eprop_ctx* ctx) {

@@ -22,8 +22,8 @@ EPROP_OK, EPROP_EINVAL, EPROP_ENOSPACE, EPROP_EDEVICE, EPROP_ESTATE = 0, -1, -2,
 # Every function the header declares, in declaration order.
 SYMBOLS = (
     "eprop_workspace_bytes", "eprop_init", "eprop_step", "eprop_run_sequence", "eprop_get_grads",
-    "eprop_reset", "eprop_status", "eprop_destroy", "eprop_last_error", "eprop_profile_begin",
-    "eprop_profile_end", "eprop_debug_buffer",
+    "eprop_reset", "eprop_status", "eprop_set_feedback", "eprop_destroy", "eprop_last_error",
+    "eprop_profile_begin", "eprop_profile_end", "eprop_debug_buffer",
 )
 
 
@@ -64,6 +64,7 @@ def load_library(path: str = LIB_PATH):
         "eprop_run_sequence": (ctypes.c_int, [vp, vp, i32, vp, vp]),
         "eprop_get_grads": (ctypes.c_int, [vp, vp, vp]),
         "eprop_reset": (ctypes.c_int, [vp]),
+        "eprop_set_feedback": (ctypes.c_int, [vp, vp]),
         "eprop_status": (ctypes.c_int, [vp]),
         "eprop_destroy": (None, [vp]),
         "eprop_last_error": (ctypes.c_char_p, [vp]),
@@ -137,6 +138,15 @@ def eprop_get_grads(ctx, grads: Sequence[torch.Tensor], loss: Optional[torch.Ten
 
 def eprop_reset(ctx):
     _check(load_library().eprop_reset(ctx), ctx)
+
+
+def eprop_set_feedback(ctx, feedback: Optional[Sequence[Optional[torch.Tensor]]]):
+    """feedback: None, or per layer None or a device fp32 [n_out, n_rec] tensor."""
+    arr = None
+    if feedback is not None:
+        arr = (ctypes.c_void_p * len(feedback))(*[_ptr(f) for f in feedback])
+    _check(load_library().eprop_set_feedback(ctx, ctypes.cast(arr, ctypes.c_void_p)
+                                             if arr is not None else None), ctx)
 
 
 def eprop_status(ctx) -> int:
@@ -236,6 +246,27 @@ class EpropContext:
 
     def reset(self):
         eprop_reset(self.ctx)
+
+    def set_feedback(self, feedback: Optional[Sequence]):
+        """Fixed feedback matrices B [n_out, n_rec] per layer for the learning
+        signal L = B^T delta (None, or None for a layer: W_out).  The tensors
+        are kept here for as long as they are set."""
+        s = self.shape
+        if feedback is None:
+            self.feedback = None
+        else:
+            if len(feedback) != s.n_layers:
+                raise ValueError(f"feedback needs {s.n_layers} entries")
+            self.feedback = []
+            for l, f in enumerate(feedback):
+                if f is None:
+                    self.feedback.append(None)
+                    continue
+                t = torch.as_tensor(f, dtype=torch.float32).to(self.device).contiguous()
+                if tuple(t.shape) != (s.n_out, s.n_rec):
+                    raise ValueError(f"feedback[{l}] must be {(s.n_out, s.n_rec)}, got {tuple(t.shape)}")
+                self.feedback.append(t)
+        eprop_set_feedback(self.ctx, self.feedback)
 
     def status(self) -> int:
         return eprop_status(self.ctx)

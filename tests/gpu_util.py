@@ -23,14 +23,17 @@ def to_dev(wl, T=None):
     return x, labels
 
 
-def gpu_run(wl, T=None, chunks=None, ctx=None):
+def gpu_run(wl, T=None, chunks=None, ctx=None, feedback=None):
     """Runs the HIP path over the workload; returns numpy results.
-    ``chunks``: split the sequence into run_sequence calls of these lengths."""
+    ``chunks``: split the sequence into run_sequence calls of these lengths.
+    ``feedback``: per-layer feedback matrices of the learning signal."""
     shape = wl.shape
     T = wl.x.shape[0] if T is None else T
     own = ctx is None
     if own:
         ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+    if feedback is not None:
+        ctx.set_feedback(feedback)
     x, labels = to_dev(wl, T)
     spikes = ctx.new_spike_buffer(T)
     chunks = chunks or [T]
@@ -73,11 +76,11 @@ def sample_synapses(shape, n_random=384, seed=0):
     return np.array(rows, dtype=np.int32)
 
 
-def check_against_oracle(wl, gpu, sample=None, T=None, tol=GRAD_TOL):
+def check_against_oracle(wl, gpu, sample=None, T=None, tol=GRAD_TOL, feedback=None):
     """Oracle on the same inputs; spikes must be identical, gradients within tol."""
     shape = wl.shape
     ref = oracle.run_sharded(shape, wl.W, wl.Wout, wl.x, wl.labels, T=T, sample=sample,
-                             workers=workers())
+                             workers=workers(), feedback=feedback)
     mism = first_spike_mismatch(gpu["spikes"], ref.spikes)
     assert mism is None, f"spike trains differ: {mism}"
     errs = {}

@@ -70,6 +70,52 @@ def test_ragged_shapes(name):
         assert ref.spikes.any()
 
 
+# ---------------------------------------------------------------- random feedback
+@pytest.mark.parametrize("name", ["rlif_ragged", "ralif_ragged_na13", "ralif2_two_layers",
+                                  "blocks_256_50"])
+def test_random_feedback_matches_oracle(name):
+    # learning signal L = B^T delta with fixed matrices B (two layers: the
+    # second layer keeps W_out, so both forms run in one context)
+    shape, seed, scale = RAGGED[name]
+    banner(f"random feedback {name} {shape}")
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    fb = synth.make_feedback(shape, seed)
+    if shape.n_layers == 2:
+        fb[1] = None
+    gpu = gpu_run(wl, feedback=fb)
+    ref_fb = [f if f is not None else wl.Wout[l] for l, f in enumerate(fb)]
+    errs, _ = check_against_oracle(wl, gpu, feedback=ref_fb)
+    banner(f"{name}: {errs}")
+
+
+def test_random_feedback_full_workload():
+    wl = synth.named_workload("rlif_b32_n256_t250")
+    fb = synth.make_feedback(wl.shape, 2)
+    banner("random feedback rlif_b32_n256_t250, every synapse")
+    gpu = gpu_run(wl, feedback=fb)
+    errs, _ = check_against_oracle(wl, gpu, feedback=fb)
+    banner(f"{errs}")
+
+
+def test_feedback_kept_over_reset_and_cleared():
+    shape, seed, scale = RAGGED["ralif_ragged_na13"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    fb = synth.make_feedback(shape, seed)
+    ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+    ctx.set_feedback(fb)
+    a = gpu_run(wl, ctx=ctx)
+    ctx.reset()
+    b = gpu_run(wl, ctx=ctx)                  # the feedback is read again by the reset
+    assert np.array_equal(a["dW"][0], b["dW"][0])
+    ctx.set_feedback(None)
+    ctx.reset()
+    c = gpu_run(wl, ctx=ctx)
+    ctx.close()
+    check_against_oracle(wl, c)               # back to the symmetric learning signal
+    check_against_oracle(wl, a, feedback=fb)
+    assert rel_l2(a["dW"][0], c["dW"][0]) > 1e-2
+
+
 def test_silent_input_gives_zero_gradient():
     shape = small(n_adaptive=7)
     wl = synth.make_workload(shape, 4, input_scale=0.0)
