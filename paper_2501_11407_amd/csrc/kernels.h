@@ -67,7 +67,8 @@ hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
 // NT: C_part[s][m][n] = sum_{k in split s} A[m][k] * Bm[n][k]
 // TN: C_part[s][m][n] = sum_{k in split s} A[k][m] * Bm[k][n]
 // fp32 MFMA.  Operands are zero padded: A and Bm provide round_up(M,32) and
-// round_up(N,32) rows (NT) or columns (TN), and K is a multiple of 16.
+// round_up(N,32) rows (NT) or columns (TN; the TN kernel reads A only up to
+// round_up(M,16) columns), and K is a multiple of 16.
 // Split s covers k in [s*k_chunk, min(K,(s+1)*k_chunk)).
 struct GemmArgs {
   const float* A;

@@ -580,52 +580,53 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
   }
 }
 
-// Same tiling with both operands stored k-major: lane (r, g) takes
-// A[k][m0 + r] and Bm[k][n0 + r] for its four k of every 16-k chunk.
+// Both operands stored k-major: lane (r, g) takes A[k][m] and Bm[k][n0 + r]
+// for its four k of every 16-k chunk.  A wave covers 16*MB rows of m (all of
+// them, M <= 16*MB) and 32 columns of n, so the large operand Bm is read once.
+template <int MB>
 __global__ __launch_bounds__(256) void gemm_tn_kernel(GemmArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int m0 = blockIdx.y * 32;
   const int n0 = (blockIdx.x * 4 + wave) * 32;
   if (n0 >= a.N) return;
   const int split = blockIdx.z;
   const int kb = split * a.k_chunk;
   const int ke = min(a.K, kb + a.k_chunk);
   const int r = lane & 15, g = lane >> 4;
-  f32x4 c00 = {0.f, 0.f, 0.f, 0.f}, c01 = c00, c10 = c00, c11 = c00;
-#pragma unroll 4
+  f32x4 c[MB][2];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) c[mb][0] = c[mb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
   for (int k = kb; k < ke; k += 16) {
-    f32x4 va0, va1, vb0, vb1;
+    f32x4 va[MB], vb0, vb1;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const size_t kk = (size_t)(k + 4 * g + q);
-      va0[q] = a.A[kk * a.lda + m0 + r];
-      va1[q] = a.A[kk * a.lda + m0 + 16 + r];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) va[mb][q] = a.A[kk * a.lda + 16 * mb + r];
       vb0[q] = a.Bm[kk * a.ldb + n0 + r];
       vb1[q] = a.Bm[kk * a.ldb + n0 + 16 + r];
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      c00 = __builtin_amdgcn_mfma_f32_16x16x4f32(va0[q], vb0[q], c00, 0, 0, 0);
-      c01 = __builtin_amdgcn_mfma_f32_16x16x4f32(va0[q], vb1[q], c01, 0, 0, 0);
-      c10 = __builtin_amdgcn_mfma_f32_16x16x4f32(va1[q], vb0[q], c10, 0, 0, 0);
-      c11 = __builtin_amdgcn_mfma_f32_16x16x4f32(va1[q], vb1[q], c11, 0, 0, 0);
-    }
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        c[mb][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(va[mb][q], vb0[q], c[mb][0], 0, 0, 0);
+        c[mb][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(va[mb][q], vb1[q], c[mb][1], 0, 0, 0);
+      }
   }
   float* out = a.C + (size_t)split * a.split_stride;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int mA = m0 + 4 * g + q, mB = mA + 16;
-    const int nA = n0 + r, nB = nA + 16;
-    if (mA < a.M) {
-      if (nA < a.N) out[(size_t)mA * a.ldc + nA] = c00[q];
-      if (nB < a.N) out[(size_t)mA * a.ldc + nB] = c01[q];
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int m = 16 * mb + 4 * g + q;
+      const int nA = n0 + r, nB = nA + 16;
+      if (m < a.M) {
+        if (nA < a.N) out[(size_t)m * a.ldc + nA] = c[mb][0][q];
+        if (nB < a.N) out[(size_t)m * a.ldc + nB] = c[mb][1][q];
+      }
     }
-    if (mB < a.M) {
-      if (nA < a.N) out[(size_t)mB * a.ldc + nA] = c10[q];
-      if (nB < a.N) out[(size_t)mB * a.ldc + nB] = c11[q];
-    }
-  }
 }
 
 // Split-K partials added into an fp64 accumulator in split order.
@@ -1193,8 +1194,24 @@ hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_gemm_tn(const GemmArgs& a, hipStream_t s) {
-  dim3 grid(cdiv(a.N, 128), cdiv(a.M, 32), a.splits);
-  gemm_tn_kernel<<<grid, 256, 0, s>>>(a);
+  // A provides round_up(M, 16) columns; larger M in groups of 64 rows
+  if (a.M > 64) {
+    for (int m0 = 0; m0 < a.M; m0 += 64) {
+      GemmArgs b = a;
+      b.A = a.A + m0;
+      b.C = a.C + (size_t)m0 * a.ldc;
+      b.M = std::min(64, a.M - m0);
+      hipError_t e = launch_gemm_tn(b, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  dim3 grid(cdiv(a.N, 128), 1, a.splits);
+  const int mb = (a.M + 15) / 16;
+  if (mb <= 1) gemm_tn_kernel<1><<<grid, 256, 0, s>>>(a);
+  else if (mb == 2) gemm_tn_kernel<2><<<grid, 256, 0, s>>>(a);
+  else if (mb == 3) gemm_tn_kernel<3><<<grid, 256, 0, s>>>(a);
+  else gemm_tn_kernel<4><<<grid, 256, 0, s>>>(a);
   return hipGetLastError();
 }
 
