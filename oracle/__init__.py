@@ -26,6 +26,7 @@ class OracleConfig(ctypes.Structure):
         ("thr", ctypes.c_double), ("beta", ctypes.c_double), ("gamma", ctypes.c_double),
         ("reset", ctypes.c_double),
         ("fwd_fp32", ctypes.c_int32), ("smooth", ctypes.c_int32),
+        ("reset_through", ctypes.c_int32),
     ]
 
 
@@ -79,6 +80,7 @@ def make_config(shape, fwd_fp32: bool = True, smooth: bool = False,
     c.thr, c.beta, c.gamma = shape.thr, shape.beta, shape.gamma
     c.reset = shape.thr if reset is None else reset
     c.fwd_fp32, c.smooth = int(fwd_fp32), int(smooth)
+    c.reset_through = int(getattr(shape, "reset_grad", 0))
     for k, v in over.items():
         setattr(c, k, v)
     return c

@@ -39,7 +39,13 @@
 //     aside); only the learning signal changes;
 //   * two-layer stacks: layer 2 reads layer-1 spikes of the same step,
 //     gradient-stopped, and has its own readout and loss;
-//   * the recurrent-weight diagonal (no self-connections) gets gradient 0.
+//   * the recurrent-weight diagonal (no self-connections) gets gradient 0;
+//   * optionally (reset_through) the reset path is kept in the gradient: the
+//     own spike z^{t-1} = H(v - A) then carries dv^t/dv^{t-1} = alpha -
+//     reset*psi^{t-1} and dv^t/da^{t-1} = reset*beta*psi^{t-1}, so the
+//     membrane component of G_t is a per-synapse eps^v (no longer the
+//     presynaptic filter zbar): one of the neuron-model variants the generic
+//     method of Sec. III-C covers.
 //
 // Precision: the neuron state (v, a, A, v-A) and the spike decision are
 // computed in the type R chosen by `fwd_fp32` (fp32 like the paper's runs,
@@ -67,6 +73,7 @@ typedef struct {
   double reset;        // amount subtracted from v after a spike
   int32_t fwd_fp32;    // 1: neuron state and spike decision in fp32, 0: fp64
   int32_t smooth;      // 1: z = S(v-A) with S' = psi (finite-difference checks)
+  int32_t reset_through;  // 1: the reset path (own spike -> own membrane) is kept
 } oracle_config;
 
 // Optional per-step records; each pointer may be NULL.
@@ -108,6 +115,7 @@ struct LayerState {
   std::vector<double> y, ztil;     // readout potential, kappa-filtered spikes
   std::vector<double> delta, L;    // dCE/dy, learning signal W_out^T delta
   std::vector<double> ebar, epsa;  // eligibility: kappa-filtered trace, eps^a
+  std::vector<double> epsv;        // per-synapse eps^v (reset_through; without the next input)
 };
 
 template <typename R>
@@ -139,12 +147,14 @@ int run(const oracle_config& c, const float* const* W, const float* const* Wout,
     if (all) {
       s.ebar.assign((size_t)N * s.n_pre, 0.0);
       s.epsa.assign((size_t)NA * s.n_pre, 0.0);
+      if (c.reset_through) s.epsv.assign((size_t)N * s.n_pre, 0.0);
     }
   }
-  std::vector<double> ebar_s, epsa_s;
+  std::vector<double> ebar_s, epsa_s, epsv_s;
   if (!all) {
     ebar_s.assign(n_sample, 0.0);
     epsa_s.assign(n_sample, 0.0);
+    epsv_s.assign(n_sample, 0.0);
   }
   std::vector<int> active;
 
@@ -161,9 +171,11 @@ int run(const oracle_config& c, const float* const* W, const float* const* Wout,
       std::fill(s.ztil.begin(), s.ztil.end(), 0.0);
       std::fill(s.ebar.begin(), s.ebar.end(), 0.0);
       std::fill(s.epsa.begin(), s.epsa.end(), 0.0);
+      std::fill(s.epsv.begin(), s.epsv.end(), 0.0);
     }
     std::fill(ebar_s.begin(), ebar_s.end(), 0.0);
     std::fill(epsa_s.begin(), epsa_s.end(), 0.0);
+    std::fill(epsv_s.begin(), epsv_s.end(), 0.0);
     const int label = labels[b];
 
     for (int t = 0; t < T; ++t) {
@@ -239,7 +251,38 @@ int run(const oracle_config& c, const float* const* W, const float* const* Wout,
         //   ebar   = kappa ebar + e                      readout filter moved onto e
         //   dW_ji += L_j ebar
         //   epsa   = psi_j zbar_i + (rho - beta_j psi_j) epsa   (eps^a at t+1)
-        if (all) {
+        // With the reset path kept, zbar_i is replaced by the per-synapse
+        //   epsv   = epsv + p_i                              (eps^v at t)
+        // and after the step
+        //   epsv   = (alpha - reset psi_j) epsv + reset beta_j psi_j epsa
+        //   epsa   = psi_j epsv + (rho - beta_j psi_j) epsa  (both with the values at t).
+        if (c.reset_through) {
+          for (int q = 0; q < (all ? N * s.n_pre : n_sample); ++q) {
+            int j, i;
+            if (all) {
+              j = q / s.n_pre;
+              i = q - j * s.n_pre;
+            } else {
+              if (sample[q].layer != l) continue;
+              j = sample[q].j;
+              i = sample[q].i;
+            }
+            const bool adaptive = j < NA;
+            const double bj = adaptive ? c.beta : 0.0;
+            const double pj = s.psi[j];
+            const size_t ji = (size_t)j * s.n_pre + i;
+            double& ev = all ? s.epsv[ji] : epsv_s[q];
+            double& eb = all ? s.ebar[ji] : ebar_s[q];
+            double* eap = adaptive ? (all ? &s.epsa[ji] : &epsa_s[q]) : nullptr;
+            const double ea = eap ? *eap : 0.0;
+            const double V = ev + s.p[i];
+            const double e = pj * (V - bj * ea);
+            eb = c.kappa * eb + e;
+            (all ? dW[l][ji] : dW[0][q]) += s.L[j] * eb;
+            ev = (c.alpha - c.reset * pj) * V + c.reset * bj * pj * ea;
+            if (eap) *eap = pj * V + (c.rho - bj * pj) * ea;
+          }
+        } else if (all) {
           for (int j = 0; j < N; ++j) {
             const bool adaptive = j < NA;
             const double bj = adaptive ? c.beta : 0.0;
@@ -329,9 +372,10 @@ size_t oracle_state_bytes(const oracle_config* c, int32_t n_sample) {
     const size_t N = c->n_rec, K = c->n_out;
     total += 2 * N * (c->fwd_fp32 ? sizeof(float) : sizeof(double));
     total += sizeof(double) * (2 * N + 2 * n_pre + N + 2 * K + N + K + N);
-    if (n_sample < 0) total += sizeof(double) * (N * n_pre + (size_t)c->n_adaptive * n_pre);
+    if (n_sample < 0)
+      total += sizeof(double) * ((c->reset_through ? 2 : 1) * N * n_pre + (size_t)c->n_adaptive * n_pre);
   }
-  if (n_sample >= 0) total += sizeof(double) * 2 * (size_t)n_sample;
+  if (n_sample >= 0) total += sizeof(double) * (c->reset_through ? 3 : 2) * (size_t)n_sample;
   return total;
 }
 

@@ -42,6 +42,8 @@ class EpropShape:
       the first layer in the same step.
     recurrent: 0 means the presynaptic vector is the input alone.
     n_adaptive: neurons j < n_adaptive have an adaptive threshold (ALIF).
+    reset_grad: 1 keeps the reset path (own spike -> own membrane) in the
+      gradient; 0 (default) stops it.
     Constants are fp32-representable; both implementations use these exact
     values.
     """
@@ -59,6 +61,7 @@ class EpropShape:
     thr: float = 1.0
     beta: float = f32(1.8)
     gamma: float = f32(0.3)
+    reset_grad: int = 0
     rate_lo: float = 0.005
     rate_hi: float = 0.05
     rate_const: Optional[float] = None  # one fixed rate for every channel

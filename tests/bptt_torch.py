@@ -5,8 +5,8 @@ forward pass in PyTorch and differentiated by backpropagation through time
 (the adjoint recursion, Eq. 6-7 of the paper) instead of the forward RTRL
 recursion of Eq. (5).  The three gradient stops of the method are
 ``detach()`` calls: the recurrent spikes (Sec. III-B, the stop_gradient
-footnote), the reset term, and in two-layer stacks the spikes passed from
-layer 1 to layer 2.  With these stops the forward recursion of e-prop and
+footnote), the reset term (kept when the shape has ``reset_grad=1``), and in
+two-layer stacks the spikes passed from layer 1 to layer 2.  With these stops the forward recursion of e-prop and
 backpropagation give the same gradient, which is what the paper checks in
 Table II for a feed-forward layer.
 
@@ -61,6 +61,7 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedbac
     """
     T = x.shape[0] if T is None else T
     L, B, N = shape.n_layers, shape.batch, shape.n_rec
+    keep_reset = bool(getattr(shape, "reset_grad", 0))   # the reset path kept in the gradient
     reset = shape.thr if reset is None else reset
     sg = (lambda v: v.detach()) if stop else (lambda v: v)
     Ws = [torch.tensor(np.asarray(w, dtype=np.float64), requires_grad=True) for w in W]
@@ -83,7 +84,7 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedbac
             I = p @ Ws[l].T
             vl = shape.alpha * v[l]
             vl = vl + I
-            vl = vl - reset * sg(zp[l])
+            vl = vl - reset * (zp[l] if keep_reset else sg(zp[l]))
             al = shape.rho * a[l]
             al = al + zp[l]                 # spike -> adaptation path is kept
             A = beta * al

@@ -44,6 +44,10 @@ MUTANTS = [
     ("diagonal_kept", "for (int j = 0; j < N; ++j) dW[l][(size_t)j * n_pre + n_in_l + j] = 0.0;",
      "", 1),
     ("threshold_adaptation_sign", "A = thr + A;", "A = thr - A;", 1),
+    ("reset_through_membrane_decay", "ev = (c.alpha - c.reset * pj) * V + c.reset * bj * pj * ea;",
+     "ev = c.alpha * V + c.reset * bj * pj * ea;", 1),
+    ("reset_through_coupling_dropped", "ev = (c.alpha - c.reset * pj) * V + c.reset * bj * pj * ea;",
+     "ev = (c.alpha - c.reset * pj) * V;", 1),
 ]
 
 

@@ -107,6 +107,45 @@ def test_feedback_is_linear_and_leaves_the_forward_alone():
     assert np.array_equal(sym.dW[0], same.dW[0])
 
 
+RESET_CASES = ["ff_lif_b4_n32_t50", "rlif_ragged", "ralif_ragged", "ralif_all_adaptive", "ff_alif",
+               "ralif2_two_layers"]
+
+
+@pytest.mark.parametrize("name", RESET_CASES)
+def test_reset_through_equals_backprop_with_reset_path(name):
+    # The reset path kept (reset_grad=1): the membrane eligibility becomes a
+    # per-synapse eps^v; the forward recursion must equal reverse-mode
+    # autograd of the network whose reset term is not detached.
+    shape, seed, scale = AUTOGRAD_CASES[name]
+    shape = shape.replace(reset_grad=1)
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    dW, dWout, loss = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels)
+    assert r.spikes.any()
+    assert abs(r.loss - loss) <= 1e-12 * abs(loss)
+    for l in range(shape.n_layers):
+        assert rel_l2(r.dW[l], dW[l]) <= 1e-11, (l, rel_l2(r.dW[l], dW[l]))
+        assert rel_l2(r.dWout[l], dWout[l]) <= 1e-11
+    # a different gradient from the default, reset-stopped one, with the same forward
+    stopped = oracle.run(shape.replace(reset_grad=0), wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    assert np.array_equal(r.spikes, stopped.spikes)
+    assert rel_l2(r.dW[0], stopped.dW[0]) > 1e-3
+
+
+def test_reset_through_samples_agree_with_full_run():
+    shape, seed, scale = AUTOGRAD_CASES["ralif_ragged"]
+    shape = shape.replace(reset_grad=1)
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    full = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    rng = np.random.default_rng(5)
+    smp = np.array([(0, int(rng.integers(shape.n_rec)), int(rng.integers(shape.n_pre(0))))
+                    for _ in range(60)] + [(0, 0, 0), (0, shape.n_rec - 1, shape.n_pre(0) - 1)],
+                   dtype=np.int32)
+    part = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False, sample=smp)
+    got = np.array([full.dW[0][j, i] for _, j, i in smp])
+    np.testing.assert_allclose(part.dW[0], got, rtol=1e-13, atol=1e-15)
+
+
 def test_recurrence_breaks_exactness():
     # Without the stops the true surrogate gradient differs: the stops are real.
     shape, seed, scale = AUTOGRAD_CASES["ralif_ragged"]
