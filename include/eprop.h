@@ -78,6 +78,10 @@ typedef struct {
   float thr;          /* threshold theta > 0, also the reset amount */
   float beta;         /* threshold adaptation strength of ALIF neurons */
   float gamma;        /* surrogate height */
+  int32_t reset_grad; /* 0: the reset path (own spike -> own membrane) is
+                         gradient-stopped like the recurrent spikes; 1: it is
+                         kept, so the membrane eligibility is per synapse
+                         (computed step by step, not in the blocked form) */
 } eprop_config;
 
 /*

@@ -69,6 +69,7 @@ struct Layer {
   int n_split = 1;                       // batch splits of the eligibility kernel
   size_t acc_stride = 0;                 // doubles between partial accumulators
   float *ebar, *epsa;                    // eligibility traces
+  float* epsv = nullptr;                 // reset_grad: per-synapse membrane eligibility
 };
 
 struct Plan {
@@ -105,6 +106,7 @@ bool valid_config(const eprop_config* c, std::string* why) {
     *why = "alpha must be in [0, 1) (the presynaptic filter must be bounded)";
     return false;
   }
+  if (c->reset_grad != 0 && c->reset_grad != 1) { *why = "reset_grad must be 0 or 1"; return false; }
   return true;
 }
 
@@ -173,8 +175,16 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     // traces tile by tile: all j tiles, and the tiles holding adaptive neurons
     const size_t ldc = round_up(N, eprop::kColPad);
     const size_t lda_t = round_up(c.n_adaptive, eprop::kTile);
-    L.ebar = (float*)take(sizeof(float) * B * npp * ldc);
-    L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * lda_t : 0);
+    if (c.reset_grad) {
+      // step-by-step eligibility: V, A, E as [B][n_pre_pad][ldj]
+      const size_t row = sizeof(float) * B * npp * L.ldj;
+      L.ebar = (float*)take(row);
+      L.epsa = (float*)take(row);
+      L.epsv = (float*)take(row);
+    } else {
+      L.ebar = (float*)take(sizeof(float) * B * npp * ldc);
+      L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * lda_t : 0);
+    }
   }
   for (Layer& L : plan->layers) {
     const size_t ldc = plan->ldc;
@@ -338,6 +348,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   fa.ldj = P.layers[0].ldv; fa.ldk = P.ldk; fa.ldn = P.ldn; fa.jlist = P.jlist;
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
   fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.zgroup = P.zgroup;
+  fa.reset_through = c.reset_grad;
   if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
   if ((rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
 
@@ -376,13 +387,27 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(c.n_adaptive, eprop::kTile));
     ca.steps = steps; ca.kpad = kpad; ca.ldc = P.ldc;
     ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta;
-    if ((rc = check(ctx, eprop::launch_coef(ca, sc), "eligibility coefficient kernel"))) return rc;
+    if (!c.reset_grad &&
+        (rc = check(ctx, eprop::launch_coef(ca, sc), "eligibility coefficient kernel")))
+      return rc;
   }
   if ((rc = check(ctx, hipEventRecord(ctx->ev_coef[sl], sc), "event record"))) return rc;
   if ((rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_coef[sl], 0), "stream wait"))) return rc;
 
   // On the caller's stream: the eligibility pass of every layer.
-  for (int l = 0; l < c.n_layers; ++l) {
+  for (int l = 0; l < c.n_layers && c.reset_grad; ++l) {
+    const Layer& L = P.layers[l];
+    eprop::TraceRtArgs ra;
+    ra.V = L.epsv; ra.A = L.epsa; ra.E = L.ebar;
+    ra.acc = L.acc; ra.acc_stride = L.acc_stride; ra.n_split = L.n_split;
+    ra.z16 = L.z16[sl]; ra.psiK = L.psiK[sl]; ra.LK = L.LK[sl]; ra.ldv = L.ldv; ra.Bp = P.Bp;
+    ra.B = c.batch; ra.n_pre_pad = L.n_pre_pad; ra.n_adaptive = c.n_adaptive; ra.ldj = L.ldj;
+    ra.ldi = L.n_pre_pad; ra.steps = steps;
+    ra.alpha = c.alpha; ra.rho = c.rho; ra.kappa = c.kappa; ra.beta = c.beta; ra.reset = c.thr;
+    ra.first = first;
+    if ((rc = check(ctx, eprop::launch_trace_rt(ra, s), "eligibility kernel"))) return rc;
+  }
+  for (int l = 0; l < c.n_layers && !c.reset_grad; ++l) {
     const Layer& L = P.layers[l];
     eprop::TraceArgs ta;
     ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.acc_stride = L.acc_stride;

@@ -60,6 +60,7 @@ struct FwdArgs {
   int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldk, ldn, jlist;  // ldj: row stride of psiK
   float alpha, rho, kappa, thr, beta, gamma_over_thr;
   int zgroup;                    // steps of pair words written together (1, 2 or 4)
+  int reset_through;             // 1: the pair words hold the binary p (1.0 or 0), not zbar
   size_t smem;
 };
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
@@ -126,6 +127,26 @@ struct TraceArgs {
   int first;       // 1: traces and accumulators start at zero (not read)
 };
 hipError_t launch_trace(const TraceArgs& a, hipStream_t s);
+
+// Eligibility pass with the reset path kept in the gradient: per synapse the
+// membrane eligibility V (per synapse, since its decay alpha - reset*psi_j
+// depends on j), the adaptation eligibility A and the kappa-filtered trace E
+// advance step by step through the block; each step
+//   V += p_i;  e = psi_j (V - beta_j A);  E = kappa E + e;  g += L_j E;
+//   (V, A) = ((alpha - reset psi_j) V + reset beta_j psi_j A,  psi_j V + (rho - beta_j psi_j) A).
+// One thread per (i, four consecutive j) and batch split; V, A, E fp32
+// [B][n_pre_pad][ldj]; g summed over the split's elements in fp32 and added
+// to acc as TraceArgs.
+struct TraceRtArgs {
+  float* V; float* A; float* E;
+  double* acc; size_t acc_stride; int n_split;
+  const uint32_t* z16;                 // p as fp16 words (hi half), layout of FwdLayer::z16
+  const float* psiK; const float* LK; int ldv, Bp;   // [t*Bp + b][ldv]
+  int B, n_pre_pad, n_adaptive, ldj, ldi, steps;
+  float alpha, rho, kappa, beta, reset;
+  int first;
+};
+hipError_t launch_trace_rt(const TraceRtArgs& a, hipStream_t s);
 
 // Gradient read-out: dW[j][i] = sum over splits s of acc[s][i][j] (in split
 // order; recurrent diagonal zeroed), dWout[k][j] = accout[k][j]; valid = 0

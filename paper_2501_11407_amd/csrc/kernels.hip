@@ -199,7 +199,8 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       on = sv != 0;
       const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
       szb[i] = zv;
-      zring[(t & (A.zgroup - 1)) * S.npre_total + i] = pair_word(zv * Ly.zscale);
+      zring[(t & (A.zgroup - 1)) * S.npre_total + i] =
+          pair_word(A.reset_through ? (on ? 1.0f : 0.0f) : zv * Ly.zscale);
     }
     const unsigned long long m = __ballot(on);
     if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
@@ -1107,6 +1108,49 @@ __global__ __launch_bounds__(256, 2) void trace_kernel(TraceArgs a) {
 
 // ---------------------------------------------------------------- gradient read-out
 // 32x32 tiles through shared memory: acc is [i][j], dW is [j][i].
+__global__ __launch_bounds__(256) void trace_rt_kernel(TraceRtArgs a) {
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int i = blockIdx.x * 4 + w;                      // presynaptic row (uniform)
+  const int j = (blockIdx.y * 64 + (threadIdx.x & 63)) * 4;
+  const int split = blockIdx.z;
+  if (i >= a.n_pre_pad || j >= a.ldj) return;            // no barriers in this kernel
+  float bt[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) bt[u] = (j + u < a.n_adaptive) ? a.beta : 0.0f;
+  const bool first = a.first != 0;
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  f32x4 G = zero;
+  for (int b = split; b < a.B; b += a.n_split) {
+    const size_t o = ((size_t)b * a.n_pre_pad + i) * a.ldj + j;
+    f32x4 V = first ? zero : *(const f32x4*)(a.V + o);
+    f32x4 Av = first ? zero : *(const f32x4*)(a.A + o);
+    f32x4 E = first ? zero : *(const f32x4*)(a.E + o);
+    const uint32_t* zb = a.z16 + (size_t)b * kKQ * a.ldi * 4 + (size_t)i * 4;
+    for (int s = 0; s < a.steps; ++s) {
+      const float p = (zb[(size_t)(s >> 2) * a.ldi * 4 + (s & 3)] & 0xFFFFu) ? 1.0f : 0.0f;
+      const size_t r = ((size_t)s * a.Bp + b) * a.ldv + j;
+      const f32x4 ps = *(const f32x4*)(a.psiK + r);
+      const f32x4 L = *(const f32x4*)(a.LK + r);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float v = V[u] + p;
+        const float e = ps[u] * (v - bt[u] * Av[u]);
+        E[u] = fmaf(a.kappa, E[u], e);
+        G[u] = fmaf(L[u], E[u], G[u]);
+        const float an = fmaf(ps[u], v, (a.rho - bt[u] * ps[u]) * Av[u]);
+        V[u] = fmaf(a.alpha - a.reset * ps[u], v, a.reset * bt[u] * ps[u] * Av[u]);
+        Av[u] = an;
+      }
+    }
+    *(f32x4*)(a.V + o) = V;
+    *(f32x4*)(a.A + o) = Av;
+    *(f32x4*)(a.E + o) = E;
+  }
+  double* p = a.acc + (size_t)split * a.acc_stride + (size_t)i * a.ldj + j;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) p[u] = (first ? 0.0 : p[u]) + (double)G[u];
+}
+
 __global__ __launch_bounds__(256) void grads_kernel(GradsArgs a) {
   __shared__ double tile[32][33];
   const int i0 = blockIdx.x * 32, j0 = blockIdx.y * 32;
@@ -1240,6 +1284,12 @@ hipError_t launch_trace(const TraceArgs& a, hipStream_t s) {
   }
   dim3 grid((a.n_pre_pad / kTile) * a.n_jt, a.n_split);
   trace_kernel<<<grid, 256, kTraceSmem, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_trace_rt(const TraceRtArgs& a, hipStream_t s) {
+  dim3 grid(a.n_pre_pad / 4, cdiv(a.ldj, 256), a.n_split);
+  trace_rt_kernel<<<grid, 256, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -34,6 +34,7 @@ class eprop_config(ctypes.Structure):
         ("n_adaptive", ctypes.c_int32),
         ("alpha", ctypes.c_float), ("rho", ctypes.c_float), ("kappa", ctypes.c_float),
         ("thr", ctypes.c_float), ("beta", ctypes.c_float), ("gamma", ctypes.c_float),
+        ("reset_grad", ctypes.c_int32),
     ]
 
 
@@ -85,7 +86,7 @@ def make_config(shape) -> eprop_config:
     """C config from an EpropShape (or any object with the same fields)."""
     return eprop_config(shape.n_layers, shape.batch, shape.n_in, shape.n_rec, shape.n_out,
                         shape.recurrent, shape.n_adaptive, shape.alpha, shape.rho, shape.kappa,
-                        shape.thr, shape.beta, shape.gamma)
+                        shape.thr, shape.beta, shape.gamma, int(getattr(shape, "reset_grad", 0)))
 
 
 def _ptr(t: Optional[torch.Tensor]):

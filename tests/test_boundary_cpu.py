@@ -60,7 +60,7 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
 @pytest.mark.parametrize("bad", [
     dict(n_layers=3), dict(n_layers=0), dict(batch=0), dict(n_in=0), dict(n_rec=0),
     dict(n_out=0), dict(n_adaptive=-1), dict(n_adaptive=30), dict(recurrent=2),
-    dict(thr=0.0), dict(alpha=float("nan")), dict(batch=70000),
+    dict(thr=0.0), dict(alpha=float("nan")), dict(batch=70000), dict(reset_grad=2),
 ])
 def test_invalid_configs_are_rejected_on_the_host(bad):
     shape = synth.EpropShape(batch=3, n_in=7, n_rec=29, n_out=5, T=10)

@@ -116,6 +116,31 @@ def test_feedback_kept_over_reset_and_cleared():
     assert rel_l2(a["dW"][0], c["dW"][0]) > 1e-2
 
 
+# ---------------------------------------------------------------- reset path kept
+@pytest.mark.parametrize("name", ["rlif_ragged", "ralif_ragged_na13", "ralif_all_adaptive", "ff_alif",
+                                  "ralif2_two_layers", "blocks_256_50", "single_step"])
+def test_reset_through_matches_oracle(name):
+    shape, seed, scale = RAGGED[name]
+    shape = shape.replace(reset_grad=1)
+    banner(f"reset path kept {name} {shape}")
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    for w in wl.W:
+        w *= W_SCALE.get(name, 1.0)
+    gpu = gpu_run(wl)
+    errs, ref = check_against_oracle(wl, gpu)
+    assert ref.spikes.any()
+    banner(f"{name}: {errs}")
+
+
+def test_reset_through_full_workload_and_split_calls():
+    wl = synth.named_workload("rlif_b32_n256_t250")
+    wl.shape = wl.shape.replace(reset_grad=1)
+    banner("reset path kept rlif_b32_n256_t250, every synapse, three calls")
+    gpu = gpu_run(wl, chunks=[100, 7, 143])
+    errs, _ = check_against_oracle(wl, gpu)
+    banner(f"{errs}")
+
+
 def test_silent_input_gives_zero_gradient():
     shape = small(n_adaptive=7)
     wl = synth.make_workload(shape, 4, input_scale=0.0)
