@@ -47,11 +47,17 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     every (i, j) read and written once; the first launch after a reset reads
     neither.  Per timestep covered, the operands read once: the filtered
     presynaptic vector [B, N_pre], the coefficients U, H [B, N] and V
-    [B, N_adaptive]; per launch the four scalars c, q, P, D [B, N]."""
+    [B, N_adaptive]; per launch the four scalars c, q, P, D [B, N].
+    With the reset path kept (reset_grad = 1): eps^v (every synapse) as a
+    third trace, the binary presynaptic vector in place of the filtered one,
+    a fourth coefficient row W [B, N], and nine scalars per (b, j)."""
     B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
     npre = shape.n_pre(layer)
-    trace = 4 * B * npre * (N + NA) + 8 * npre * N      # one direction
-    operands = steps * 4 * B * (npre + 2 * N + NA) + launches * 4 * 4 * B * N
+    rt = getattr(shape, "reset_grad", 0)
+    trace = 4 * B * npre * ((2 if rt else 1) * N + NA) + 8 * npre * N      # one direction
+    rows = (3 if rt else 2) * N + NA
+    scalars = 9 if rt else 4
+    operands = steps * 4 * B * (npre + rows) + launches * scalars * 4 * B * N
     return (2 * launches - first_launches) * trace + operands
 
 
@@ -59,10 +65,12 @@ def trace_flops(shape, layer: int, steps: int) -> int:
     """Algorithmic matrix operations of the eligibility kernel: per
     covered timestep and synapse, one multiply-add (2 operations) in each of
     the contractions over the block's steps -- C_U and C_H for every
-    synapse, C_V as well for synapses onto adaptive neurons."""
+    synapse, C_V as well for synapses onto adaptive neurons (and, with the
+    reset path kept, C_W for every synapse)."""
     B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
     npre = shape.n_pre(layer)
-    return steps * B * npre * 2 * (2 * N + NA)
+    rt = getattr(shape, "reset_grad", 0)
+    return steps * B * npre * 2 * ((3 if rt else 2) * N + NA)
 
 
 def source_digest() -> str:
@@ -149,6 +157,8 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--reset-grad", type=int, default=0, choices=(0, 1),
+                    help="1: the same workload with the reset path kept in the gradient")
     args = ap.parse_args()
     if args.summarize_counters:
         print(json.dumps(summarize_counters(*args.summarize_counters, args.copy_mib)))
@@ -164,7 +174,10 @@ def main():
     from paper_2501_11407_amd import eprop, synth
 
     wl = synth.named_workload(WORKLOAD)
+    if args.reset_grad:
+        wl.shape = wl.shape.replace(reset_grad=1)
     shape = wl.shape
+    workload = WORKLOAD + ("_reset_grad" if args.reset_grad else "")
     dev = torch.device("cuda:0")
     ctx = eprop.EpropContext(shape, wl.W, wl.Wout, device="cuda:0")
     x = torch.from_numpy(wl.x).to(dev)
@@ -206,7 +219,7 @@ def main():
     tflops = alg_flops / sec / 1e12
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": stored_traffic(shape),
+                "traffic": None if args.reset_grad else stored_traffic(shape),
                 "kernel": "trace_kernel", "avg_launch_us": round(trace_ms * 1e3 / n_timed, 2),
                 "steps_per_launch": round(timed_steps / n_timed, 2),
                 "alg_hbm_bytes_per_launch": round(alg_bytes / n_timed),
@@ -219,9 +232,10 @@ def main():
         "warmup": args.warmup, "ms_per_step": elapsed * 1e3 / args.steps,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded Bernoulli spike inputs, quantised Gaussian weights)",
-        "config": {"workload": WORKLOAD, "batch": shape.batch, "n_in": shape.n_in,
+        "config": {"workload": workload, "batch": shape.batch, "n_in": shape.n_in,
                    "n_rec": shape.n_rec, "n_adaptive": shape.n_adaptive, "n_out": shape.n_out,
-                   "T": shape.T, "layers": shape.n_layers, "parallelism": "single GPU"},
+                   "T": shape.T, "layers": shape.n_layers, "reset_grad": args.reset_grad,
+                   "parallelism": "single GPU"},
         "roofline": roofline,
     }
     if args.calibrate_copy:

@@ -61,7 +61,7 @@ struct Layer {
   // the filtered presynaptic values as scaled fp16 pairs, and the block
   // coefficients of the eligibility recursion (same two slots)
   uint32_t* z16[2];
-  uint32_t *coefU[2], *coefV[2], *coefH[2];
+  uint32_t *coefU[2], *coefV[2], *coefH[2], *coefW[2];
   float* coefS[2];
   float zscale = 1.0f;                   // power of two: zbar * zscale < 2^15
   float* Cpart;
@@ -175,16 +175,10 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     // traces tile by tile: all j tiles, and the tiles holding adaptive neurons
     const size_t ldc = round_up(N, eprop::kColPad);
     const size_t lda_t = round_up(c.n_adaptive, eprop::kTile);
-    if (c.reset_grad) {
-      // step-by-step eligibility: V, A, E as [B][n_pre_pad][ldj]
-      const size_t row = sizeof(float) * B * npp * L.ldj;
-      L.ebar = (float*)take(row);
-      L.epsa = (float*)take(row);
-      L.epsv = (float*)take(row);
-    } else {
-      L.ebar = (float*)take(sizeof(float) * B * npp * ldc);
-      L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * lda_t : 0);
-    }
+    L.ebar = (float*)take(sizeof(float) * B * npp * ldc);
+    L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * lda_t : 0);
+    // with the reset path kept, the membrane eligibility per synapse as well
+    L.epsv = c.reset_grad ? (float*)take(sizeof(float) * B * npp * ldc) : nullptr;
   }
   for (Layer& L : plan->layers) {
     const size_t ldc = plan->ldc;
@@ -194,7 +188,9 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
       L.coefU[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
       L.coefV[sl] = (uint32_t*)take(c.n_adaptive > 0 ? sizeof(uint32_t) * B * ldc * KM : 0);
       L.coefH[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
-      L.coefS[sl] = (float*)take(sizeof(float) * eprop::kScalarPlanes * B * ldc);
+      L.coefW[sl] = c.reset_grad ? (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM) : nullptr;
+      const int planes = c.reset_grad ? eprop::kScalarPlanesRT : eprop::kScalarPlanes;
+      L.coefS[sl] = (float*)take(sizeof(float) * planes * B * ldc);
     }
     // zbar <= 1/(1-alpha): the largest power of two that keeps it below 2^15
     {
@@ -386,33 +382,22 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ca.B = c.batch; ca.n_post = c.n_rec; ca.n_adaptive = c.n_adaptive;
     ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(c.n_adaptive, eprop::kTile));
     ca.steps = steps; ca.kpad = kpad; ca.ldc = P.ldc;
-    ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta;
-    if (!c.reset_grad &&
-        (rc = check(ctx, eprop::launch_coef(ca, sc), "eligibility coefficient kernel")))
-      return rc;
+    ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta; ca.alpha = c.alpha; ca.thr = c.thr;
+    ca.W = L.coefW[sl]; ca.reset_through = c.reset_grad;
+    if ((rc = check(ctx, eprop::launch_coef(ca, sc), "eligibility coefficient kernel"))) return rc;
   }
   if ((rc = check(ctx, hipEventRecord(ctx->ev_coef[sl], sc), "event record"))) return rc;
   if ((rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_coef[sl], 0), "stream wait"))) return rc;
 
   // On the caller's stream: the eligibility pass of every layer.
-  for (int l = 0; l < c.n_layers && c.reset_grad; ++l) {
-    const Layer& L = P.layers[l];
-    eprop::TraceRtArgs ra;
-    ra.V = L.epsv; ra.A = L.epsa; ra.E = L.ebar;
-    ra.acc = L.acc; ra.acc_stride = L.acc_stride; ra.n_split = L.n_split;
-    ra.z16 = L.z16[sl]; ra.psiK = L.psiK[sl]; ra.LK = L.LK[sl]; ra.ldv = L.ldv; ra.Bp = P.Bp;
-    ra.B = c.batch; ra.n_pre_pad = L.n_pre_pad; ra.n_adaptive = c.n_adaptive; ra.ldj = L.ldj;
-    ra.ldi = L.n_pre_pad; ra.steps = steps;
-    ra.alpha = c.alpha; ra.rho = c.rho; ra.kappa = c.kappa; ra.beta = c.beta; ra.reset = c.thr;
-    ra.first = first;
-    if ((rc = check(ctx, eprop::launch_trace_rt(ra, s), "eligibility kernel"))) return rc;
-  }
-  for (int l = 0; l < c.n_layers && !c.reset_grad; ++l) {
+  for (int l = 0; l < c.n_layers; ++l) {
     const Layer& L = P.layers[l];
     eprop::TraceArgs ta;
-    ta.ebar = L.ebar; ta.epsa = L.epsa; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
-    ta.n_split = L.n_split; ta.z16 = L.z16[sl]; ta.zinv = 1.0f / L.zscale;
+    ta.ebar = L.ebar; ta.epsa = L.epsa; ta.epsv = L.epsv; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
+    ta.n_split = L.n_split; ta.z16 = L.z16[sl];
+    ta.zinv = c.reset_grad ? 1.0f : 1.0f / L.zscale;
     ta.U = L.coefU[sl]; ta.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
+    ta.W = L.coefW[sl]; ta.reset_through = c.reset_grad;
     ta.S = L.coefS[sl];
     ta.B = c.batch; ta.n_pre_pad = L.n_pre_pad; ta.n_post = c.n_rec; ta.ldj = L.ldj;
     ta.n_adaptive = c.n_adaptive; ta.ldi = L.n_pre_pad;

@@ -98,12 +98,16 @@ constexpr int kScalarPlanes = 8;               // c, q, P, D, 1/sU, 1/sH, 1/sV, 
 // U, V, H as scaled fp16 pair words [B][kKC][ldc][16] (zero for steps <=
 // s < kpad; V written for j < n_vcols only, NULL when no neuron adapts), each
 // row with its own power-of-two scale, and S [8][B][ldc]: c, q, P, D and the
-// inverse scales of U, H, V.
+// inverse scales of U, H, V.  With reset_through the rows are those of the
+// recursion with the reset path kept (U = C_E, H = C_g, V = C_A, and W = C_V
+// for every j) and S has kScalarPlanesRT planes (see coef_rt_kernel).
+constexpr int kScalarPlanesRT = 16;
 struct CoefArgs {
   const float* psiK; const float* LK; int ldv, Bp;   // [t*Bp + b][ldv]
-  uint32_t* U; uint32_t* V; uint32_t* H; float* S;
+  uint32_t* U; uint32_t* V; uint32_t* H; uint32_t* W; float* S;
   int B, n_post, n_adaptive, n_vcols, steps, kpad, ldc;
-  float kappa, rho, beta;
+  float kappa, rho, beta, alpha, thr;
+  int reset_through;
 };
 hipError_t launch_coef(const CoefArgs& a, hipStream_t s);
 
@@ -116,37 +120,20 @@ hipError_t launch_coef(const CoefArgs& a, hipStream_t s);
 struct TraceArgs {
   float* ebar;     // [B][n_pre_pad / 64][n_jt][64 * 64]
   float* epsa;     // [B][n_pre_pad / 64][n_jt_a][64 * 64]
+  float* epsv;     // reset_through: [B][n_pre_pad / 64][n_jt][64 * 64]
   double* acc;     // [n_split][n_pre_pad][ldj] (row-major)
   size_t acc_stride;
   const uint32_t* z16;                // [B][kKQ][ldi][4], ldi = n_pre_pad
-  const uint32_t* U; const uint32_t* V; const uint32_t* H; const float* S;   // as CoefArgs
+  const uint32_t* U; const uint32_t* V; const uint32_t* H; const uint32_t* W;
+  const float* S;                     // as CoefArgs
   int B, n_pre_pad, n_post, ldj, n_adaptive, ldi, ldc, kpad, n_split;
   int n_jt, n_jt_a;   // tiles along j: all, and those holding adaptive neurons
   float kappa_K;   // kappa^steps
-  float zinv;      // 1 / zscale
+  float zinv;      // 1 / zscale (1 with reset_through: z16 holds the binary p)
   int first;       // 1: traces and accumulators start at zero (not read)
+  int reset_through;   // 1: the recursion with the reset path kept
 };
 hipError_t launch_trace(const TraceArgs& a, hipStream_t s);
-
-// Eligibility pass with the reset path kept in the gradient: per synapse the
-// membrane eligibility V (per synapse, since its decay alpha - reset*psi_j
-// depends on j), the adaptation eligibility A and the kappa-filtered trace E
-// advance step by step through the block; each step
-//   V += p_i;  e = psi_j (V - beta_j A);  E = kappa E + e;  g += L_j E;
-//   (V, A) = ((alpha - reset psi_j) V + reset beta_j psi_j A,  psi_j V + (rho - beta_j psi_j) A).
-// One thread per (i, four consecutive j) and batch split; V, A, E fp32
-// [B][n_pre_pad][ldj]; g summed over the split's elements in fp32 and added
-// to acc as TraceArgs.
-struct TraceRtArgs {
-  float* V; float* A; float* E;
-  double* acc; size_t acc_stride; int n_split;
-  const uint32_t* z16;                 // p as fp16 words (hi half), layout of FwdLayer::z16
-  const float* psiK; const float* LK; int ldv, Bp;   // [t*Bp + b][ldv]
-  int B, n_pre_pad, n_adaptive, ldj, ldi, steps;
-  float alpha, rho, kappa, beta, reset;
-  int first;
-};
-hipError_t launch_trace_rt(const TraceRtArgs& a, hipStream_t s);
 
 // Gradient read-out: dW[j][i] = sum over splits s of acc[s][i][j] (in split
 // order; recurrent diagonal zeroed), dWout[k][j] = accout[k][j]; valid = 0

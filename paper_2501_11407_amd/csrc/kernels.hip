@@ -748,18 +748,131 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
   a.S[6 * plane + so] = 1.0f / sV;
 }
 
+// Reset path kept in the gradient.  The membrane eligibility is then a
+// per-synapse state V whose input is the binary presynaptic value p_{i,s};
+// per step (v = V + p_s)
+//   e = psi_j (v - beta_j A);  E = kappa E + e;  g += L_j E;
+//   A = e + rho A;  V = alpha v - thr e,
+// the same recursion as psi v + (rho - beta psi) A and
+// (alpha - thr psi) v + thr beta psi A.  Over a block every output Y of
+// E_K, g, A_K, V_K is linear in the block-start (V0, A0, E0) and in the p_s.
+// The adjoint (lV, lA, lE) of Y with respect to the state before step s runs
+// backwards from the unit vector of Y (zero for g):
+//   tE = lE + [Y = g] L_s;  w = psi_s (lA + tE - thr lV);
+//   lV = alpha lV + w;  lA = rho lA - beta w;  lE = kappa tE.
+// p_s enters where V does, so Y's coefficient of p_s is lV after the update
+// at step s, and the block-start state enters with (lV, lA, lE) at s = 0.
+// Rows written: U = C_E, H = C_g, V = C_A (tiles holding adaptive neurons),
+// W = C_V, as scaled pairs like coef_kernel's; S holds 16 planes:
+//   0 gE  1 gA  2 gV  3 eA  4 eV  5 aA  6 aV  7 vA  8 vV
+//   9 1/sU  10 1/sH  11 1/sV  12 1/sW  (E0 reaches E_K as kappa^K only and
+//   reaches neither A_K nor V_K).
+struct Adjoint {
+  float v = 0.0f, a = 0.0f, e = 0.0f;
+  __device__ __forceinline__ void step(float ps, float Lg, float alpha, float rho, float kappa,
+                                       float bt, float thr) {
+    const float te = e + Lg;
+    const float w = ps * (a + te - thr * v);
+    v = fmaf(alpha, v, w);
+    a = fmaf(rho, a, -bt * w);
+    e = kappa * te;
+  }
+};
+
+__global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  const int b = blockIdx.y;
+  if (j >= a.n_post) return;
+  const float bt = (j < a.n_adaptive) ? a.beta : 0.0f;
+  const bool wv = a.V != nullptr && j < a.n_vcols;
+  const float* __restrict__ psiK = a.psiK;
+  const float* __restrict__ LK = a.LK;
+  auto load_chunk = [&](int c, float (&ps)[kChunk], float (&L)[kChunk]) {
+#pragma unroll
+    for (int e = 0; e < kChunk; ++e) {
+      const int s = kChunk * c + e;
+      ps[e] = 0.0f;
+      L[e] = 0.0f;
+      if (s < a.steps) {
+        const size_t row = ((size_t)s * a.Bp + b) * a.ldv + j;
+        ps[e] = psiK[row];
+        L[e] = LK[row];
+      }
+    }
+  };
+  // terminal adjoints: E_K, g, A_K, V_K
+  auto init = [](Adjoint (&y)[4]) {
+    y[0] = Adjoint{};
+    y[0].e = 1.0f;
+    y[1] = Adjoint{};
+    y[2] = Adjoint{};
+    y[2].a = 1.0f;
+    y[3] = Adjoint{};
+    y[3].v = 1.0f;
+  };
+  float mx[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  {
+    Adjoint y[4];
+    init(y);
+    for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
+      float ps[kChunk], L[kChunk];
+      load_chunk(c, ps, L);
+#pragma unroll
+      for (int e = kChunk - 1; e >= 0; --e) {
+        if (kChunk * c + e >= a.steps) continue;
+#pragma unroll
+        for (int o = 0; o < 4; ++o) {
+          y[o].step(ps[e], o == 1 ? L[e] : 0.0f, a.alpha, a.rho, a.kappa, bt, a.thr);
+          mx[o] = fmaxf(mx[o], fabsf(y[o].v));
+        }
+      }
+    }
+  }
+  float sc[4];
+#pragma unroll
+  for (int o = 0; o < 4; ++o) sc[o] = ldexpf(1.0f, pair_exponent(mx[o]));
+  const size_t rs = (size_t)a.ldc * kChunk;         // words between chunks
+  const size_t off = ((size_t)b * kKC * a.ldc + j) * kChunk;
+  Adjoint y[4];
+  init(y);
+  for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
+    float ps[kChunk], L[kChunk];
+    load_chunk(c, ps, L);
+    float x[4][kChunk];
+#pragma unroll
+    for (int e = kChunk - 1; e >= 0; --e) {
+      const bool live = kChunk * c + e < a.steps;
+#pragma unroll
+      for (int o = 0; o < 4; ++o) {
+        if (live) y[o].step(ps[e], o == 1 ? L[e] : 0.0f, a.alpha, a.rho, a.kappa, bt, a.thr);
+        x[o][e] = live ? y[o].v : 0.0f;
+      }
+    }
+    store_pairs(a.U + off + c * rs, x[0], sc[0]);
+    store_pairs(a.H + off + c * rs, x[1], sc[1]);
+    if (wv) store_pairs(a.V + off + c * rs, x[2], sc[2]);
+    store_pairs(a.W + off + c * rs, x[3], sc[3]);
+  }
+  const size_t so = (size_t)b * a.ldc + j, plane = (size_t)a.B * a.ldc;
+  const float s16[13] = {y[1].e, y[1].a, y[1].v, y[0].a, y[0].v, y[2].a, y[2].v, y[3].a, y[3].v,
+                         1.0f / sc[0], 1.0f / sc[1], 1.0f / sc[2], 1.0f / sc[3]};
+#pragma unroll
+  for (int k = 0; k < 13; ++k) a.S[k * plane + so] = s16[k];
+}
+
 // A workgroup of 4 waves owns a 64 (i) x 64 (j) tile of synapses and one
 // split of the batch; wave w computes the 32 x 32 sub-tile (w / 2, w % 2).
 // For each batch element b of the split:
 //  * MFMA contractions C_U, C_V, C_H = coef_b[j][s] x zbar_b[i][s] over the
-//    block's steps (v_mfma_f32_16x16x4f32, 2x2 blocks of 16x16 per wave),
-//    16 steps ("a chunk") at a time, operands read from shared memory;
+//    block's steps (v_mfma_f32_16x16x32_f16 on the scaled fp16 pairs, 2x2
+//    blocks of 16x16 per wave), 16 steps ("a chunk") at a time, operands
+//    read from shared memory;
 //  * then the elementwise update of the traces, each read once and written
 //    once (1 KiB contiguous per wave instruction), and of the gradient.
 // Operands stream through a ring of kRing chunk slots in shared memory:
 // zbar_b rows i and U, H (and V) rows j of the chunk's 16 steps are copied by
-// direct global-to-LDS loads (16 bytes per lane, no registers) kPrefetch
-// chunks ahead of the chunk being contracted, across batch elements.  The
+// direct global-to-LDS loads (16 bytes per lane, no registers) up to
+// kRing - 1 chunks ahead of the chunk being contracted, across batch elements.  The
 // block-start traces of a batch element (registers) and its scalars c, q, P,
 // D (shared memory, double-buffered) travel with its first chunk.
 // Waits: copies and loads complete in order, so a chunk's copies are waited
@@ -789,12 +902,8 @@ __device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, uint32_t off, f
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, kNonTemporal);
 }
 
-constexpr int kRing = 4;                              // chunk slots
-constexpr int kPrefetch = 3;                          // chunks copied ahead (< kRing)
+constexpr int kRing = 4;                              // chunk slots (reset-stopped)
 constexpr int kOpBytes = kTile * 64;                  // one operand of a chunk: 64 rows x 64 B
-constexpr int kSlot = 4 * kOpBytes / 4;               // floats per slot: z, U, H, V (16 KiB)
-constexpr int kScal = kScalarPlanes * kTile;          // floats of the scalars of 64 columns
-constexpr size_t kTraceSmem = sizeof(float) * (kRing * kSlot + 2 * kScal);
 constexpr uint32_t kSubTileBytes = 32 * 32 * 4;
 
 // s_waitcnt immediate that waits for vmcnt <= n only (gfx9 encoding)
@@ -818,14 +927,29 @@ __device__ __forceinline__ void dma16(const float* g, float* lds) {
   __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
 }
 
-template <bool ALIF, int NCH>
+// RT = false: the reset-stopped recursion (contractions U, H and, for tiles
+// holding adaptive neurons, V; traces ebar, epsa).  RT = true: the reset
+// path kept (coef_rt_kernel): contractions U = C_E, H = C_g, W = C_V and V =
+// C_A; traces ebar, epsv and epsa; the presynaptic operand is the binary p,
+// exact in fp16, so each contraction takes one MFMA pass.  Its five operand
+// slots use a ring of three chunks, which keeps two workgroups per compute
+// unit.
+template <bool ALIF, int NCH, bool RT>
 struct TraceTile {
+  static constexpr int RING = RT ? 3 : kRing;                 // chunk slots
+  static constexpr int PREF = RING - 1;                       // chunks copied ahead
+  static constexpr int NOP = RT ? 5 : 4;                      // operands per slot
+  static constexpr int SLOT = NOP * kOpBytes / 4;             // floats per slot
+  static constexpr int PLANES = RT ? kScalarPlanesRT : kScalarPlanes;
+  static constexpr int SCAL = PLANES * kTile;                 // floats of one scalar buffer
+  static constexpr size_t SMEM = sizeof(float) * (RING * SLOT + 2 * SCAL);
   // chunks in flight ahead; fewer than NCH so that a batch element's copies
   // never reach past the next element's first chunk
-  static constexpr int D = NCH == 1 ? 1 : (NCH - 1 < kPrefetch ? NCH - 1 : kPrefetch);
-  static constexpr int Q = ALIF ? 4 : 3;            // copies per wave per chunk
-  static constexpr int EA = ALIF ? 8 : 4;           // trace loads per wave per batch element
-  static constexpr int ops(int c) { return Q + (c == 0 ? 2 : 0); }   // + scalars with chunk 0
+  static constexpr int D = NCH == 1 ? 1 : (NCH - 1 < PREF ? NCH - 1 : PREF);
+  static constexpr int Q = 3 + (ALIF ? 1 : 0) + (RT ? 1 : 0);   // copies per wave per chunk
+  static constexpr int SC = PLANES / 4;                         // scalar copies per wave
+  static constexpr int EA = 4 * (1 + (ALIF ? 1 : 0) + (RT ? 1 : 0));   // trace loads per element
+  static constexpr int ops(int c) { return Q + (c == 0 ? SC : 0); }     // + scalars with chunk 0
   // Loads issued after those of chunk ch when it is waited for: the copies
   // of chunks ch+1 .. ch+D-1 (past the end of the batch element: the next
   // element's, if there is one), and the element's trace loads when they
@@ -856,27 +980,27 @@ struct TraceTile {
     wj = w & 1;
   }
 
-  __device__ __forceinline__ __amdgpu_buffer_rsrc_t ebar_rsrc(int b) const {
-    const size_t t = ((size_t)b * (a.n_pre_pad / kTile) + it) * a.n_jt + jt;
-    return make_rsrc((const char*)a.ebar + (t * 4 + w) * kSubTileBytes, kSubTileBytes);
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const float* base, int n_t, int b) const {
+    const size_t t = ((size_t)b * (a.n_pre_pad / kTile) + it) * n_t + jt;
+    return make_rsrc((const char*)base + (t * 4 + w) * kSubTileBytes, kSubTileBytes);
   }
-  __device__ __forceinline__ __amdgpu_buffer_rsrc_t epsa_rsrc(int b) const {
-    const size_t t = ((size_t)b * (a.n_pre_pad / kTile) + it) * a.n_jt_a + jt;
-    return make_rsrc((const char*)a.epsa + (t * 4 + w) * kSubTileBytes, kSubTileBytes);
-  }
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t ebar_rsrc(int b) const { return tile_rsrc(a.ebar, a.n_jt, b); }
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t epsa_rsrc(int b) const { return tile_rsrc(a.epsa, a.n_jt_a, b); }
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t epsv_rsrc(int b) const { return tile_rsrc(a.epsv, a.n_jt, b); }
 
   // Copies of chunk c of batch element b into ring slot sl.  Wave w copies
   // rows 16w .. 16w+15 of each operand (1 KiB: lane l takes 16 bytes of row
   // 16w + l/4); within a row the four 16-byte units are stored in the order
   // u ^ ((row / 2) % 4), which keeps the MFMA operand reads free of bank
-  // conflicts.  With chunk 0 also the scalars (planes w and w + 4) into
+  // conflicts.  With chunk 0 also the scalars (planes w, w + 4, ...) into
   // scalar buffer par.
-  // The copies are issued in two parts (P = 0: z and U; P = 1: H, V and the
-  // scalars), placed between MFMAs so that the vector-memory path works while
-  // the matrix cores do; the order of all copies is that of the full issue.
+  // The copies are issued in two parts (P = 0: z and U; P = 1: H, V, W and
+  // the scalars), placed between MFMAs so that the vector-memory path works
+  // while the matrix cores do; the order of all copies is that of the full
+  // issue.
   template <int P>
   __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
-    char* slot = (char*)(sm + sl * kSlot);
+    char* slot = (char*)(sm + sl * SLOT);
     const int rw = 16 * w + (lane >> 2);
     const uint32_t q = (uint32_t)((lane & 3) ^ ((lane >> 3) & 3));
     const uint32_t unit = q * 16u;
@@ -890,10 +1014,15 @@ struct TraceTile {
       dma16((const float*)((const char*)a.H + cc * 64 + unit), dst + 2 * kOpBytes / 4);
       if constexpr (ALIF)
         dma16((const float*)((const char*)a.V + cc * 64 + unit), dst + 3 * kOpBytes / 4);
+      if constexpr (RT)
+        dma16((const float*)((const char*)a.W + cc * 64 + unit), dst + 4 * kOpBytes / 4);
       if (c == 0 && lane < 16) {
-        float* sb = sm + kRing * kSlot + par * kScal;
-        dma16(a.S + ((size_t)w * a.B + b) * a.ldc + j0 + lane * 4, sb + w * kTile);
-        dma16(a.S + ((size_t)(w + 4) * a.B + b) * a.ldc + j0 + lane * 4, sb + (w + 4) * kTile);
+        float* sb = sm + RING * SLOT + par * SCAL;
+#pragma unroll
+        for (int m = 0; m < SC; ++m) {
+          const int pl = w + 4 * m;
+          dma16(a.S + ((size_t)pl * a.B + b) * a.ldc + j0 + lane * 4, sb + pl * kTile);
+        }
       }
     }
   }
@@ -902,8 +1031,9 @@ struct TraceTile {
     issue<1>(b, c, sl, par);
   }
 
-  // block-start traces of batch element b into E/A
-  __device__ __forceinline__ void load_traces(int b, f32x4 (&E)[2][2], f32x4 (&A)[2][2]) const {
+  // block-start traces of batch element b into E, A (and Vm)
+  __device__ __forceinline__ void load_traces(int b, f32x4 (&E)[2][2], f32x4 (&A)[2][2],
+                                              f32x4 (&Vm)[2][2]) const {
     const auto eR = ebar_rsrc(b);
 #pragma unroll
     for (int x = 0; x < 4; ++x) E[x >> 1][x & 1] = bload(eR, x * 1024u + lane * 16u);
@@ -912,42 +1042,80 @@ struct TraceTile {
 #pragma unroll
       for (int x = 0; x < 4; ++x) A[x >> 1][x & 1] = bload(aR, x * 1024u + lane * 16u);
     }
+    if constexpr (RT) {
+      const auto vR = epsv_rsrc(b);
+#pragma unroll
+      for (int x = 0; x < 4; ++x) Vm[x >> 1][x & 1] = bload(vR, x * 1024u + lane * 16u);
+    }
   }
 
   // traces and gradient of the k-th batch element from its contractions
   // (accumulated in the scaled units of the fp16 pairs)
   __device__ __forceinline__ void finish(int k, const f32x4 (&E)[2][2], const f32x4 (&A)[2][2],
-                                         const f32x4 (&cU)[2][2], const f32x4 (&cV)[2][2],
-                                         const f32x4 (&cH)[2][2], f32x4 (&gacc)[2][2]) const {
+                                         const f32x4 (&Vm)[2][2], const f32x4 (&cU)[2][2],
+                                         const f32x4 (&cV)[2][2], const f32x4 (&cH)[2][2],
+                                         const f32x4 (&cW)[2][2], f32x4 (&gacc)[2][2]) const {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     const int b = split + k * a.n_split;
-    const float* st = sm + kRing * kSlot + (k & 1) * kScal;   // c, q, P, D, 1/sU, 1/sH, 1/sV
+    const float* st = sm + RING * SLOT + (k & 1) * SCAL;
     const auto eR = ebar_rsrc(b);
     const auto aR = ALIF ? epsa_rsrc(b) : eR;
+    const auto vR = RT ? epsv_rsrc(b) : eR;
+    auto plane = [&](int p, int cj) { return *(const f32x4*)(st + p * kTile + cj); };
 #pragma unroll
     for (int bj = 0; bj < 2; ++bj) {
       const int cj = 32 * wj + 16 * bj + 4 * g;
-      const f32x4 c = *(const f32x4*)(st + cj), qq = *(const f32x4*)(st + kTile + cj);
-      const f32x4 P = ALIF ? *(const f32x4*)(st + 2 * kTile + cj) : zero;
-      const f32x4 Dd = ALIF ? *(const f32x4*)(st + 3 * kTile + cj) : zero;
-      const f32x4 fU = *(const f32x4*)(st + 4 * kTile + cj) * a.zinv;
-      const f32x4 fH = *(const f32x4*)(st + 5 * kTile + cj) * a.zinv;
-      const f32x4 fV = ALIF ? *(const f32x4*)(st + 6 * kTile + cj) * a.zinv : zero;
+      if constexpr (!RT) {
+        // c, q, P, D, 1/sU, 1/sH, 1/sV
+        const f32x4 c = plane(0, cj), qq = plane(1, cj);
+        const f32x4 P = ALIF ? plane(2, cj) : zero;
+        const f32x4 Dd = ALIF ? plane(3, cj) : zero;
+        const f32x4 fU = plane(4, cj) * a.zinv;
+        const f32x4 fH = plane(5, cj) * a.zinv;
+        const f32x4 fV = ALIF ? plane(6, cj) * a.zinv : zero;
 #pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-        const f32x4 e0 = first ? zero : E[bj][bi];
-        const f32x4 a0 = (first || !ALIF) ? zero : A[bj][bi];
-        f32x4 ek, ak, gk;
+        for (int bi = 0; bi < 2; ++bi) {
+          const f32x4 e0 = first ? zero : E[bj][bi];
+          const f32x4 a0 = (first || !ALIF) ? zero : A[bj][bi];
+          f32x4 ek, ak, gk;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], cU[bj][bi][q] * fU[q]));
-          gk[q] = fmaf(c[q], e0[q], fmaf(qq[q], a0[q], cH[bj][bi][q] * fH[q]));
-          ak[q] = fmaf(Dd[q], a0[q], cV[bj][bi][q] * fV[q]);
+          for (int q = 0; q < 4; ++q) {
+            ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], cU[bj][bi][q] * fU[q]));
+            gk[q] = fmaf(c[q], e0[q], fmaf(qq[q], a0[q], cH[bj][bi][q] * fH[q]));
+            ak[q] = fmaf(Dd[q], a0[q], cV[bj][bi][q] * fV[q]);
+          }
+          gacc[bj][bi] += gk;
+          const uint32_t o = (2 * bj + bi) * 1024u + lane * 16u;
+          bstore(eR, o, ek);
+          if constexpr (ALIF) bstore(aR, o, ak);
         }
-        gacc[bj][bi] += gk;
-        const uint32_t o = (2 * bj + bi) * 1024u + lane * 16u;
-        bstore(eR, o, ek);
-        if constexpr (ALIF) bstore(aR, o, ak);
+      } else {
+        // gE gA gV eA eV aA aV vA vV 1/sU 1/sH 1/sV 1/sW (coef_rt_kernel)
+        const f32x4 gE = plane(0, cj), gV = plane(2, cj), eV = plane(4, cj), vV = plane(8, cj);
+        const f32x4 gA = ALIF ? plane(1, cj) : zero, eA = ALIF ? plane(3, cj) : zero;
+        const f32x4 aA = ALIF ? plane(5, cj) : zero, aV = ALIF ? plane(6, cj) : zero;
+        const f32x4 vA = ALIF ? plane(7, cj) : zero;
+        const f32x4 fU = plane(9, cj), fH = plane(10, cj), fW = plane(12, cj);
+        const f32x4 fV = ALIF ? plane(11, cj) : zero;
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi) {
+          const f32x4 e0 = first ? zero : E[bj][bi];
+          const f32x4 v0 = first ? zero : Vm[bj][bi];
+          const f32x4 a0 = (first || !ALIF) ? zero : A[bj][bi];
+          f32x4 ek, ak, gk, vk;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            ek[q] = fmaf(a.kappa_K, e0[q], fmaf(eV[q], v0[q], fmaf(eA[q], a0[q], cU[bj][bi][q] * fU[q])));
+            gk[q] = fmaf(gE[q], e0[q], fmaf(gV[q], v0[q], fmaf(gA[q], a0[q], cH[bj][bi][q] * fH[q])));
+            vk[q] = fmaf(vV[q], v0[q], fmaf(vA[q], a0[q], cW[bj][bi][q] * fW[q]));
+            ak[q] = fmaf(aV[q], v0[q], fmaf(aA[q], a0[q], cV[bj][bi][q] * fV[q]));
+          }
+          gacc[bj][bi] += gk;
+          const uint32_t o = (2 * bj + bi) * 1024u + lane * 16u;
+          bstore(eR, o, ek);
+          bstore(vR, o, vk);
+          if constexpr (ALIF) bstore(aR, o, ak);
+        }
       }
     }
   }
@@ -955,12 +1123,12 @@ struct TraceTile {
   __device__ __forceinline__ void run() const {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     const int nk = (a.B - split + a.n_split - 1) / a.n_split;
-    f32x4 gacc[2][2], cU[2][2], cV[2][2], cH[2][2], E[2][2], A[2][2];
+    f32x4 gacc[2][2], cU[2][2], cV[2][2], cH[2][2], cW[2][2], E[2][2], A[2][2], Vm[2][2];
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
       gacc[x >> 1][x & 1] = zero;
-      cU[x >> 1][x & 1] = cV[x >> 1][x & 1] = cH[x >> 1][x & 1] = zero;
-      E[x >> 1][x & 1] = A[x >> 1][x & 1] = zero;
+      cU[x >> 1][x & 1] = cV[x >> 1][x & 1] = cH[x >> 1][x & 1] = cW[x >> 1][x & 1] = zero;
+      E[x >> 1][x & 1] = A[x >> 1][x & 1] = Vm[x >> 1][x & 1] = zero;
     }
 #pragma unroll
     for (int c = 0; c < D; ++c) issue_all(split, c, c, 0);
@@ -974,12 +1142,13 @@ struct TraceTile {
           __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, true)));
         else
           __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, false)));
-        wg_barrier();   // chunk n is in shared memory; slot (n - 1) % kRing is free
+        wg_barrier();   // chunk n is in shared memory; slot (n - 1) % RING is free
         if constexpr (ch == 0) {
           // element k-1 is finished now: its stores overlap this chunk's MFMAs
-          if (k > 0) finish(k - 1, E, A, cU, cV, cH, gacc);
+          if (k > 0) finish(k - 1, E, A, Vm, cU, cV, cH, cW, gacc);
 #pragma unroll
-          for (int x = 0; x < 4; ++x) cU[x >> 1][x & 1] = cV[x >> 1][x & 1] = cH[x >> 1][x & 1] = zero;
+          for (int x = 0; x < 4; ++x)
+            cU[x >> 1][x & 1] = cV[x >> 1][x & 1] = cH[x >> 1][x & 1] = cW[x >> 1][x & 1] = zero;
           // with D == NCH the next copies overwrite what finish() just read
           if constexpr (D == NCH) wg_barrier();
           __builtin_amdgcn_sched_barrier(0);
@@ -989,16 +1158,18 @@ struct TraceTile {
         auto issue_next = [&](auto pc) {
           constexpr int P = decltype(pc)::value;
           if constexpr (c2 < NCH)
-            issue<P>(b, c2, (n + D) % kRing, k & 1);
+            issue<P>(b, c2, (n + D) % RING, k & 1);
           else if (next)
-            issue<P>(b + a.n_split, c2 - NCH, (n + D) % kRing, (k + 1) & 1);
+            issue<P>(b + a.n_split, c2 - NCH, (n + D) % RING, (k + 1) & 1);
         };
 
-        // Per output block and contraction X, two fp16 MFMAs (K = 32) over the
+        // Per output block and contraction X, fp16 MFMAs (K = 32) over the
         // chunk's 16 steps.  Lane g holds steps 4g..4g+3 as (hi, lo) pairs of
         // k slots: A = X's words as they are; B = (z_hi, z_hi) per step, then
-        // (z_lo, 0) with the same A: X_hi z_hi + X_lo z_hi + X_hi z_lo.
-        const char* slot = (const char*)(sm + (n % kRing) * kSlot);
+        // (z_lo, 0) with the same A: X_hi z_hi + X_lo z_hi + X_hi z_lo.  With
+        // RT, z is the binary p (z_lo = 0) and the second pass is left out.
+        constexpr int NPASS = RT ? 1 : 2;
+        const char* slot = (const char*)(sm + (n % RING) * SLOT);
         const int sw = (r >> 1) & 3;   // unit order of this lane's rows
         const f16x8 zero8 = {};
         f16x8 bz1[2], bz2[2];
@@ -1018,14 +1189,14 @@ struct TraceTile {
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj) {
           const int cr = 32 * wj + 16 * bj + r;
-          f16x8 ax[3];
+          f16x8 ax[4];
 #pragma unroll
-          for (int X = 0; X < 3; ++X)
-            ax[X] = (X < 2 || ALIF)
+          for (int X = 0; X < 4; ++X)
+            ax[X] = ((X < 2) || (X == 2 && ALIF) || (X == 3 && RT))
                         ? *(const f16x8*)(slot + (X + 1) * kOpBytes + cr * 64 + ((g ^ sw) << 4))
                         : zero8;
 #pragma unroll
-          for (int pass = 0; pass < 2; ++pass) {
+          for (int pass = 0; pass < NPASS; ++pass) {
 #pragma unroll
             for (int bi = 0; bi < 2; ++bi) {
               const f16x8 bz = pass == 0 ? bz1[bi] : bz2[bi];
@@ -1033,6 +1204,8 @@ struct TraceTile {
               cH[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz, cH[bj][bi], 0, 0, 0);
               if constexpr (ALIF)
                 cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[2], bz, cV[bj][bi], 0, 0, 0);
+              if constexpr (RT)
+                cW[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[3], bz, cW[bj][bi], 0, 0, 0);
             }
             if (pass == 0) {
               __builtin_amdgcn_sched_barrier(0);
@@ -1041,7 +1214,7 @@ struct TraceTile {
               } else {
                 issue_next(std::integral_constant<int, 1>{});
                 // the element's block-start traces, after chunk 0's copies
-                if constexpr (ch == 0) load_traces(b, E, A);
+                if constexpr (ch == 0) load_traces(b, E, A, Vm);
               }
               __builtin_amdgcn_sched_barrier(0);
             }
@@ -1052,7 +1225,7 @@ struct TraceTile {
       for_each_index(chunk, std::make_integer_sequence<int, NCH>{});
     }
     __builtin_amdgcn_s_waitcnt(vm_wait(0));   // the last element's traces
-    finish(nk - 1, E, A, cU, cV, cH, gacc);
+    finish(nk - 1, E, A, Vm, cU, cV, cH, cW, gacc);
     // the split's fp64 accumulator (row-major [n_pre_pad][ldj])
     const int iw = i0 + 32 * wi, jw = j0 + 32 * wj;
     double* accp = a.acc + (size_t)split * a.acc_stride;
@@ -1070,87 +1243,27 @@ struct TraceTile {
   }
 };
 
-template <bool ALIF>
-__device__ __forceinline__ void trace_tile_n(const TraceArgs& a, float* sm, int it, int jt,
-                                             int split, bool first) {
-  static_assert(kBlockSteps == 256, "chunk dispatch assumes 256-step blocks");
-  switch (a.kpad >> 4) {
-    case 1: TraceTile<ALIF, 1>(a, sm, it, jt, split, first).run(); break;
-    case 2: TraceTile<ALIF, 2>(a, sm, it, jt, split, first).run(); break;
-    case 3: TraceTile<ALIF, 3>(a, sm, it, jt, split, first).run(); break;
-    case 4: TraceTile<ALIF, 4>(a, sm, it, jt, split, first).run(); break;
-    case 5: TraceTile<ALIF, 5>(a, sm, it, jt, split, first).run(); break;
-    case 6: TraceTile<ALIF, 6>(a, sm, it, jt, split, first).run(); break;
-    case 7: TraceTile<ALIF, 7>(a, sm, it, jt, split, first).run(); break;
-    case 8: TraceTile<ALIF, 8>(a, sm, it, jt, split, first).run(); break;
-    case 9: TraceTile<ALIF, 9>(a, sm, it, jt, split, first).run(); break;
-    case 10: TraceTile<ALIF, 10>(a, sm, it, jt, split, first).run(); break;
-    case 11: TraceTile<ALIF, 11>(a, sm, it, jt, split, first).run(); break;
-    case 12: TraceTile<ALIF, 12>(a, sm, it, jt, split, first).run(); break;
-    case 13: TraceTile<ALIF, 13>(a, sm, it, jt, split, first).run(); break;
-    case 14: TraceTile<ALIF, 14>(a, sm, it, jt, split, first).run(); break;
-    case 15: TraceTile<ALIF, 15>(a, sm, it, jt, split, first).run(); break;
-    default: TraceTile<ALIF, 16>(a, sm, it, jt, split, first).run(); break;
-  }
-}
-
 // blockIdx.x: tile in row-major order; blockIdx.y: batch split.  A tile
-// holding any adaptive neuron takes the three-contraction path.
+// holding any adaptive neuron takes the path with the adaptation trace.
+// One kernel per chunk count NCH = kpad / 16 (the host picks it), so that
+// each holds only its own two variants.
+template <bool RT, int NCH>
 __global__ __launch_bounds__(256, 2) void trace_kernel(TraceArgs a) {
   extern __shared__ __attribute__((aligned(16))) float trace_smem[];
   const int it = blockIdx.x / a.n_jt, jt = blockIdx.x - it * a.n_jt;
   const bool first = a.first != 0;
   if (jt < a.n_jt_a)
-    trace_tile_n<true>(a, trace_smem, it, jt, blockIdx.y, first);
+    TraceTile<true, NCH, RT>(a, trace_smem, it, jt, blockIdx.y, first).run();
   else
-    trace_tile_n<false>(a, trace_smem, it, jt, blockIdx.y, first);
+    TraceTile<false, NCH, RT>(a, trace_smem, it, jt, blockIdx.y, first).run();
+}
+// shared memory of the two variants (the same for every chunk count)
+constexpr size_t kTraceSmemOf(bool rt) {
+  return rt ? TraceTile<true, 16, true>::SMEM : TraceTile<true, 16, false>::SMEM;
 }
 
 // ---------------------------------------------------------------- gradient read-out
 // 32x32 tiles through shared memory: acc is [i][j], dW is [j][i].
-__global__ __launch_bounds__(256) void trace_rt_kernel(TraceRtArgs a) {
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int i = blockIdx.x * 4 + w;                      // presynaptic row (uniform)
-  const int j = (blockIdx.y * 64 + (threadIdx.x & 63)) * 4;
-  const int split = blockIdx.z;
-  if (i >= a.n_pre_pad || j >= a.ldj) return;            // no barriers in this kernel
-  float bt[4];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) bt[u] = (j + u < a.n_adaptive) ? a.beta : 0.0f;
-  const bool first = a.first != 0;
-  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-  f32x4 G = zero;
-  for (int b = split; b < a.B; b += a.n_split) {
-    const size_t o = ((size_t)b * a.n_pre_pad + i) * a.ldj + j;
-    f32x4 V = first ? zero : *(const f32x4*)(a.V + o);
-    f32x4 Av = first ? zero : *(const f32x4*)(a.A + o);
-    f32x4 E = first ? zero : *(const f32x4*)(a.E + o);
-    const uint32_t* zb = a.z16 + (size_t)b * kKQ * a.ldi * 4 + (size_t)i * 4;
-    for (int s = 0; s < a.steps; ++s) {
-      const float p = (zb[(size_t)(s >> 2) * a.ldi * 4 + (s & 3)] & 0xFFFFu) ? 1.0f : 0.0f;
-      const size_t r = ((size_t)s * a.Bp + b) * a.ldv + j;
-      const f32x4 ps = *(const f32x4*)(a.psiK + r);
-      const f32x4 L = *(const f32x4*)(a.LK + r);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float v = V[u] + p;
-        const float e = ps[u] * (v - bt[u] * Av[u]);
-        E[u] = fmaf(a.kappa, E[u], e);
-        G[u] = fmaf(L[u], E[u], G[u]);
-        const float an = fmaf(ps[u], v, (a.rho - bt[u] * ps[u]) * Av[u]);
-        V[u] = fmaf(a.alpha - a.reset * ps[u], v, a.reset * bt[u] * ps[u] * Av[u]);
-        Av[u] = an;
-      }
-    }
-    *(f32x4*)(a.V + o) = V;
-    *(f32x4*)(a.A + o) = Av;
-    *(f32x4*)(a.E + o) = E;
-  }
-  double* p = a.acc + (size_t)split * a.acc_stride + (size_t)i * a.ldj + j;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) p[u] = (first ? 0.0 : p[u]) + (double)G[u];
-}
-
 __global__ __launch_bounds__(256) void grads_kernel(GradsArgs a) {
   __shared__ double tile[32][33];
   const int i0 = blockIdx.x * 32, j0 = blockIdx.y * 32;
@@ -1268,29 +1381,41 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 
 hipError_t launch_coef(const CoefArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.n_post, 256), a.B);
-  coef_kernel<<<grid, 256, 0, s>>>(a);
+  if (a.reset_through)
+    coef_rt_kernel<<<grid, 256, 0, s>>>(a);
+  else
+    coef_kernel<<<grid, 256, 0, s>>>(a);
   return hipGetLastError();
 }
 
-hipError_t launch_trace(const TraceArgs& a, hipStream_t s) {
+template <bool RT, int NCH>
+hipError_t launch_trace_variant(const TraceArgs& a, hipStream_t s) {
   // more than 64 KiB of shared memory must be requested per kernel
+  constexpr size_t smem = kTraceSmemOf(RT);
   static bool granted = false;
   if (!granted) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&trace_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)kTraceSmem);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&trace_kernel<RT, NCH>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
     granted = true;
   }
   dim3 grid((a.n_pre_pad / kTile) * a.n_jt, a.n_split);
-  trace_kernel<<<grid, 256, kTraceSmem, s>>>(a);
+  trace_kernel<RT, NCH><<<grid, 256, smem, s>>>(a);
   return hipGetLastError();
 }
 
-hipError_t launch_trace_rt(const TraceRtArgs& a, hipStream_t s) {
-  dim3 grid(a.n_pre_pad / 4, cdiv(a.ldj, 256), a.n_split);
-  trace_rt_kernel<<<grid, 256, 0, s>>>(a);
-  return hipGetLastError();
+template <bool RT, int... I>
+hipError_t launch_trace_nch(const TraceArgs& a, hipStream_t s, std::integer_sequence<int, I...>) {
+  using Fn = hipError_t (*)(const TraceArgs&, hipStream_t);
+  static constexpr Fn table[] = {&launch_trace_variant<RT, I + 1>...};
+  return table[(a.kpad >> 4) - 1](a, s);
+}
+
+hipError_t launch_trace(const TraceArgs& a, hipStream_t s) {
+  static_assert(kKC == 16, "one kernel per chunk count of a 256-step block");
+  if (a.kpad < kChunk || a.kpad > kBlockSteps || a.kpad % kChunk != 0) return hipErrorInvalidValue;
+  const auto nch = std::make_integer_sequence<int, kKC>{};
+  return a.reset_through ? launch_trace_nch<true>(a, s, nch) : launch_trace_nch<false>(a, s, nch);
 }
 
 hipError_t launch_grads(const GradsArgs& a, hipStream_t s) {

@@ -98,3 +98,93 @@ def test_blocks_chain():
     assert e2 == pytest.approx(ref[0], rel=1e-12)
     assert a2 == pytest.approx(ref[1], rel=1e-12)
     assert g1 + g2 == pytest.approx(ref[2], rel=1e-12)
+
+
+# ---------------------------------------------------------------- reset path kept
+# With the reset's dependence on the membrane kept in the gradient, the
+# membrane eligibility V becomes a per-synapse state with the binary
+# presynaptic value p_s as its input.  Per step s (v = V + p_s):
+#     e = psi_s (v - beta A);  E = kappa E + e;  g += L_s E;
+#     A' = e + rho A;  V' = alpha v - thr e,
+# the same as (alpha - thr psi) v + thr beta psi A and psi v + (rho - beta psi) A.
+# Over a block each output Y in {V, A, E, g} is linear in the block-start
+# state and in the p_s.  The backward (adjoint) pass gives, per output, the
+# sensitivity (lV, lA, lE) to the state before step s; p_s enters where V
+# does, so its coefficient is lV at step s.
+def step_by_step_rt(V0, A0, E0, p, psi, L, kappa, rho, beta, alpha, thr):
+    V, A, E, g = V0, A0, E0, 0.0
+    for s in range(len(psi)):
+        v = V + p[s]
+        e = psi[s] * (v - beta * A)
+        E = kappa * E + e
+        g += L[s] * E
+        V, A = (alpha - thr * psi[s]) * v + thr * beta * psi[s] * A, psi[s] * v + (rho - beta * psi[s]) * A
+    return V, A, E, g
+
+
+def block_coefficients_rt(psi, L, kappa, rho, beta, alpha, thr):
+    """Per output Y: C_Y[s] (coefficient of p_s) and (lV, lA, lE) at s = 0."""
+    K = len(psi)
+    out = {}
+    for Y, term in (("V", (1.0, 0.0, 0.0)), ("A", (0.0, 1.0, 0.0)), ("E", (0.0, 0.0, 1.0)),
+                    ("g", (0.0, 0.0, 0.0))):
+        aV, aA, aE = term
+        C = np.zeros(K)
+        for s in range(K - 1, -1, -1):
+            tE = aE + (L[s] if Y == "g" else 0.0)
+            w = psi[s] * (aA + tE - thr * aV)
+            aV, aA, aE = alpha * aV + w, rho * aA - beta * w, kappa * tE
+            C[s] = aV
+        out[Y] = (C, (aV, aA, aE))
+    return out
+
+
+def block_form_rt(V0, A0, E0, p, psi, L, kappa, rho, beta, alpha, thr):
+    co = block_coefficients_rt(psi, L, kappa, rho, beta, alpha, thr)
+    res = []
+    for Y in ("V", "A", "E", "g"):
+        C, (lV, lA, lE) = co[Y]
+        res.append(p @ C + lV * V0 + lA * A0 + lE * E0)
+    return tuple(res)
+
+
+@pytest.mark.parametrize("beta", [0.0, 1.8])
+@pytest.mark.parametrize("K", [1, 2, 5, 16, 64, 256])
+def test_block_form_rt_equals_recursion(K, beta):
+    rng = np.random.default_rng(2000 * K + int(10 * beta))
+    kappa, rho, alpha, thr = np.exp(-1 / 20), np.exp(-1 / 200), np.exp(-1 / 20), 0.6
+    for _ in range(20):
+        p = (rng.random(K) < 0.3).astype(float)
+        psi = rng.uniform(0, 0.5, K) * (rng.random(K) < 0.6)
+        L = rng.normal(0, 1, K)
+        V0, A0, E0 = rng.normal(0, 3, 3)
+        ref = step_by_step_rt(V0, A0, E0, p, psi, L, kappa, rho, beta, alpha, thr)
+        got = block_form_rt(V0, A0, E0, p, psi, L, kappa, rho, beta, alpha, thr)
+        for r, x in zip(ref, got):
+            assert abs(r - x) <= 1e-11 * (1 + abs(r)), (K, beta, ref, got)
+
+
+def test_block_form_rt_structure():
+    # the coefficient of V0 is that of p_0; E0 reaches E only through kappa^K
+    # and never reaches V or A; with beta = 0 the adaptation eligibility
+    # reaches nothing else; thr = 0 gives the reset-stopped recursion
+    rng = np.random.default_rng(11)
+    K, kappa, rho, alpha = 40, np.exp(-1 / 20), np.exp(-1 / 200), np.exp(-1 / 20)
+    psi, L = rng.uniform(0, 0.5, K), rng.normal(0, 1, K)
+    co = block_coefficients_rt(psi, L, kappa, rho, 1.8, alpha, 0.6)
+    for Y in "VAEg":
+        C, (lV, lA, lE) = co[Y]
+        assert lV == C[0]
+    assert co["V"][1][2] == 0.0 and co["A"][1][2] == 0.0
+    assert co["E"][1][2] == pytest.approx(kappa ** K, rel=1e-13)
+    lif = block_coefficients_rt(psi, L, kappa, rho, 0.0, alpha, 0.6)
+    for Y in "VEg":
+        assert lif[Y][1][1] == 0.0
+    # thr = 0: E and g coefficients of p_s are those of zbar-based ones with
+    # zbar_s = sum_{r<=s} alpha^(s-r) p_r (the reset-stopped recursion above)
+    p = (rng.random(K) < 0.3).astype(float)
+    zbar = np.array([sum(alpha ** (s - r) * p[r] for r in range(s + 1)) for s in range(K)])
+    ref = step_by_step(0.0, 0.0, zbar, psi, L, kappa, rho, 1.8)
+    V, A, E, g = block_form_rt(0.0, 0.0, 0.0, p, psi, L, kappa, rho, 1.8, alpha, 0.0)
+    assert E == pytest.approx(ref[0], rel=1e-12) and A == pytest.approx(ref[1], rel=1e-12)
+    assert g == pytest.approx(ref[2], rel=1e-12)
