@@ -103,7 +103,7 @@ def summarize_counters(fetch_dir: str, write_dir: str, copy_mib: int) -> dict:
         for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             rows += list(csv.DictReader(open(f)))
         trace = [float(r["Counter_Value"]) for r in rows
-                 if r["Counter_Name"] == counter and "trace_kernel(" in r["Kernel_Name"]]
+                 if r["Counter_Name"] == counter and "::trace_kernel<" in r["Kernel_Name"]]
         copies = [r for r in rows if r["Counter_Name"] == counter and COPY_KERNEL in r["Kernel_Name"]]
         big = max(int(r["Grid_Size"]) for r in copies)      # the calibration copies, not small ones
         copy = [float(r["Counter_Value"]) for r in copies if int(r["Grid_Size"]) == big]

@@ -80,8 +80,9 @@ typedef struct {
   float gamma;        /* surrogate height */
   int32_t reset_grad; /* 0: the reset path (own spike -> own membrane) is
                          gradient-stopped like the recurrent spikes; 1: it is
-                         kept, so the membrane eligibility is per synapse
-                         (computed step by step, not in the blocked form) */
+                         kept (Eq. 5 with the reset's terms in the membrane
+                         row of H_I, Sec. III-C), so the membrane eligibility
+                         is a third per-synapse trace; other values: -1 */
 } eprop_config;
 
 /*

@@ -9,7 +9,9 @@
 //   ztK    [rows][ldn]     kappa-filtered spikes
 //   z16    [B][Kmax/4][ldi][4] filtered presynaptic vector as scaled fp16
 //                                pairs, one 32-bit word per step (see below),
-//                                16 bytes per row and step quad
+//                                16 bytes per row and step quad; with the
+//                                reset path kept, the binary presynaptic
+//                                vector (1.0 or 0) instead
 // Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
 // psiK) and the readout gradient dW_out += deltaK^T * ztK; then the block
 // coefficients of the eligibility recursion and the eligibility kernel, which
