@@ -51,6 +51,10 @@ RAGGED = {
     "single_step": (small(T=1, n_adaptive=13), 11, 8.0),
     "blocks_256_256_9": (small(n_adaptive=13, T=521, **DISTINCT), 12, 4.0),
     "blocks_256_50": (small(batch=6, n_adaptive=29, T=306, **DISTINCT), 13, 4.0),
+    # more classes than one wave's lanes (the readout's second path), up to
+    # the largest class count the library accepts
+    "classes_100": (small(batch=4, n_out=100, n_adaptive=13, **DISTINCT), 14, 4.0),
+    "classes_1024": (small(batch=2, n_in=20, n_rec=70, n_out=1024, T=20, n_adaptive=35), 15, 4.0),
 }
 # Weight multipliers (powers of two keep the 2**-14 grid): one step needs a
 # strong drive to spike.  Partial sums stay far below 2**10, so they are exact.
@@ -118,7 +122,8 @@ def test_feedback_kept_over_reset_and_cleared():
 
 # ---------------------------------------------------------------- reset path kept
 @pytest.mark.parametrize("name", ["rlif_ragged", "ralif_ragged_na13", "ralif_all_adaptive", "ff_alif",
-                                  "ralif2_two_layers", "blocks_256_50", "single_step"])
+                                  "ralif2_two_layers", "blocks_256_50", "single_step", "classes_100",
+                                  "blocks_256_256_9", "wide_1100"])
 def test_reset_through_matches_oracle(name):
     shape, seed, scale = RAGGED[name]
     shape = shape.replace(reset_grad=1)
