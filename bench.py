@@ -45,19 +45,21 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     Per launch: ebar (every synapse) and eps^a (synapses onto adaptive
     neurons) read once and written once, one fp64 gradient accumulator of
     every (i, j) read and written once; the first launch after a reset reads
-    neither.  Per timestep covered, the operands read once: the filtered
-    presynaptic vector [B, N_pre], the coefficients U, H [B, N] and V
-    [B, N_adaptive]; per launch the four scalars c, q, P, D [B, N].
-    With the reset path kept (reset_grad = 1): eps^v (every synapse) as a
-    third trace, the binary presynaptic vector in place of the filtered one,
-    a fourth coefficient row W [B, N], and nine scalars per (b, j)."""
+    neither.  Per timestep covered, the operands read once: the binary
+    presynaptic vector [B, N_pre] (one 4-byte pair word each), the
+    coefficients U, H [B, N] and V [B, N_adaptive]; per launch the seven
+    scalars c, q, P, D and the three block-start coefficients [B, N], and
+    the block-start filter [B, N_pre].  With the reset path kept
+    (reset_grad = 1): eps^v (every synapse) as a third trace, a fourth
+    coefficient row W [B, N], and nine scalars per (b, j)."""
     B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
     npre = shape.n_pre(layer)
     rt = getattr(shape, "reset_grad", 0)
     trace = 4 * B * npre * ((2 if rt else 1) * N + NA) + 8 * npre * N      # one direction
     rows = (3 if rt else 2) * N + NA
-    scalars = 9 if rt else 4
-    operands = steps * 4 * B * (npre + rows) + launches * scalars * 4 * B * N
+    scalars = 9 if rt else 7
+    operands = (steps * 4 * B * (npre + rows) + launches * scalars * 4 * B * N
+                + (0 if rt else launches * 4 * B * npre))
     return (2 * launches - first_launches) * trace + operands
 
 

@@ -63,7 +63,7 @@ struct Layer {
   uint32_t* z16[2];
   uint32_t *coefU[2], *coefV[2], *coefH[2], *coefW[2];
   float* coefS[2];
-  float zscale = 1.0f;                   // power of two: zbar * zscale < 2^15
+  float* zstart[2];                      // presynaptic filter at each block's start [B][ldi]
   float* Cpart;
   double *acc, *accout;                  // gradient accumulators (acc: n_split partials)
   int n_split = 1;                       // batch splits of the eligibility kernel
@@ -192,11 +192,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
       const int planes = c.reset_grad ? eprop::kScalarPlanesRT : eprop::kScalarPlanes;
       L.coefS[sl] = (float*)take(sizeof(float) * planes * B * ldc);
     }
-    // zbar <= 1/(1-alpha): the largest power of two that keeps it below 2^15
-    {
-      const double zmax = 1.0 / (1.0 - (double)c.alpha);
-      L.zscale = (float)std::ldexp(1.0, (int)std::floor(std::log2(32768.0 / zmax)));
-    }
+    for (int sl = 0; sl < 2; ++sl) L.zstart[sl] = (float*)take(sizeof(float) * B * L.n_pre_pad);
   }
   const size_t npad4 = round_up(N, 4);
   size_t npre_max = 0;
@@ -333,7 +329,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     const Layer& L = P.layers[std::min(l, c.n_layers - 1)];
     f.Wt = L.Wt; f.ldw = L.ldw; f.WoutT = L.WoutT;
     f.v = L.v; f.a = L.a; f.ztil = L.ztil; f.z = L.z; f.zbar = L.zbar; f.y = L.y;
-    f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.z16 = L.z16[sl]; f.zscale = L.zscale;
+    f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.z16 = L.z16[sl]; f.zstart = L.zstart[sl];
     f.deltaK = L.deltaK[sl]; f.ztK = L.ztK[sl];
     f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.rows_per_wave = L.rows_per_wave; f.ldi = L.n_pre_pad;
   }
@@ -344,7 +340,6 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   fa.ldj = P.layers[0].ldv; fa.ldk = P.ldk; fa.ldn = P.ldn; fa.jlist = P.jlist;
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
   fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.zgroup = P.zgroup;
-  fa.reset_through = c.reset_grad;
   if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
   if ((rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
 
@@ -395,7 +390,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     eprop::TraceArgs ta;
     ta.ebar = L.ebar; ta.epsa = L.epsa; ta.epsv = L.epsv; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
     ta.n_split = L.n_split; ta.z16 = L.z16[sl];
-    ta.zinv = c.reset_grad ? 1.0f : 1.0f / L.zscale;
+    ta.zstart = L.zstart[sl];
     ta.U = L.coefU[sl]; ta.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
     ta.W = L.coefW[sl]; ta.reset_through = c.reset_grad;
     ta.S = L.coefS[sl];

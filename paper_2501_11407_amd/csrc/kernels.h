@@ -7,11 +7,11 @@
 //   psiK   [Kmax*Bp][ldv]  pseudo-derivative (ldv = n_rec rounded to 256)
 //   deltaK [rows][ldk]     readout error (softmax - onehot)
 //   ztK    [rows][ldn]     kappa-filtered spikes
-//   z16    [B][Kmax/4][ldi][4] filtered presynaptic vector as scaled fp16
-//                                pairs, one 32-bit word per step (see below),
-//                                16 bytes per row and step quad; with the
-//                                reset path kept, the binary presynaptic
-//                                vector (1.0 or 0) instead
+//   z16    [B][Kmax/4][ldi][4] binary presynaptic vector as fp16 pair words
+//                                (1.0 or 0 in the low half, see below), one
+//                                32-bit word per step, 16 bytes per row and
+//                                step quad
+//   zstart [B][ldi]              presynaptic filter at the block's start
 // Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
 // psiK) and the readout gradient dW_out += deltaK^T * ztK; then the block
 // coefficients of the eligibility recursion and the eligibility kernel, which
@@ -45,7 +45,7 @@ struct FwdLayer {
   double* lossacc;               // [B]
   float* psiK;                   // [rows][ldj]
   uint32_t* z16;                 // [B][Kmax/4][ldi][4]
-  float zscale;
+  float* zstart;                 // [B][ldi]
   float* deltaK; float* ztK;     // [rows][ldk], [rows][ldn]
   int n_inl, n_pre, rows_per_wave, ldi;
 };
@@ -62,7 +62,6 @@ struct FwdArgs {
   int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldk, ldn, jlist;  // ldj: row stride of psiK
   float alpha, rho, kappa, thr, beta, gamma_over_thr;
   int zgroup;                    // steps of pair words written together (1, 2 or 4)
-  int reset_through;             // 1: the pair words hold the binary p (1.0 or 0), not zbar
   size_t smem;
 };
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
@@ -92,15 +91,17 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 // pairs: a value x (times a power-of-two scale 2^e) is hi = fp16(x 2^e) plus
 // lo = fp16(x 2^e - hi), together about 22 significant bits, in one 32-bit
 // word (hi in the low half).  Per 16-step chunk and row, 16 words (64 bytes).
+// The presynaptic operand is binary: hi = 1.0 or 0, lo = 0.
 constexpr int kChunk = 16;                     // steps per chunk
 constexpr int kKC = kBlockSteps / kChunk;      // chunks per block
-constexpr int kScalarPlanes = 8;               // c, q, P, D, 1/sU, 1/sH, 1/sV, unused
+constexpr int kScalarPlanes = 12;              // see coef_kernel
 
 // Block coefficients of the eligibility recursion, one thread per (b, j):
-// U, V, H as scaled fp16 pair words [B][kKC][ldc][16] (zero for steps <=
-// s < kpad; V written for j < n_vcols only, NULL when no neuron adapts), each
-// row with its own power-of-two scale, and S [8][B][ldc]: c, q, P, D and the
-// inverse scales of U, H, V.  With reset_through the rows are those of the
+// U', V', H' (against the binary presynaptic vector) as scaled fp16 pair
+// words [B][kKC][ldc][16] (zero for steps <= s < kpad; V' written for j <
+// n_vcols only, NULL when no neuron adapts), each row with its own
+// power-of-two scale, and S [kScalarPlanes][B][ldc] (see coef_kernel).  With
+// reset_through the rows are those of the
 // recursion with the reset path kept (U = C_E, H = C_g, V = C_A, and W = C_V
 // for every j) and S has kScalarPlanesRT planes (see coef_rt_kernel).
 constexpr int kScalarPlanesRT = 16;
@@ -126,12 +127,12 @@ struct TraceArgs {
   double* acc;     // [n_split][n_pre_pad][ldj] (row-major)
   size_t acc_stride;
   const uint32_t* z16;                // [B][kKQ][ldi][4], ldi = n_pre_pad
+  const float* zstart;                // [B][ldi] (reset-stopped form only)
   const uint32_t* U; const uint32_t* V; const uint32_t* H; const uint32_t* W;
   const float* S;                     // as CoefArgs
   int B, n_pre_pad, n_post, ldj, n_adaptive, ldi, ldc, kpad, n_split;
   int n_jt, n_jt_a;   // tiles along j: all, and those holding adaptive neurons
   float kappa_K;   // kappa^steps
-  float zinv;      // 1 / zscale (1 with reset_through: z16 holds the binary p)
   int first;       // 1: traces and accumulators start at zero (not read)
   int reset_through;   // 1: the recursion with the reset path kept
 };

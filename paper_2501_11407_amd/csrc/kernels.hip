@@ -80,6 +80,8 @@ __device__ __forceinline__ void split16(float x, _Float16& hi, _Float16& lo) {
   lo = (_Float16)(x - (float)hi);
 }
 
+constexpr uint32_t kPairOne = 0x3C00u;   // the pair word of 1.0: fp16 1.0 in the low half
+
 // scaled value -> one 32-bit word: hi in the low half, lo in the high half
 __device__ __forceinline__ uint32_t pair_word(float x) {
   _Float16 hi, lo;
@@ -199,8 +201,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       on = sv != 0;
       const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
       szb[i] = zv;
-      zring[(t & (A.zgroup - 1)) * S.npre_total + i] =
-          pair_word(A.reset_through ? (on ? 1.0f : 0.0f) : zv * Ly.zscale);
+      zring[(t & (A.zgroup - 1)) * S.npre_total + i] = on ? kPairOne : 0u;
     }
     const unsigned long long m = __ballot(on);
     if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
@@ -350,8 +351,8 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // Global stores of the step go last: a load waits for every store issued
   // before it, so stores ahead of the drive and readout loads would lengthen
   // the step.  Per-step vectors: psi, ztilde, the spike words, and the
-  // filtered presynaptic values as scaled fp16 pairs ([b][t/4][i][4] words,
-  // step t % 4: a wave's group store covers 64 consecutive 16-byte records).
+  // binary presynaptic values as pair words ([b][t/4][i][4] words, step
+  // t % 4: a wave's group store covers 64 consecutive 16-byte records).
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
     const int j = q * kFwdThreads + tid;
@@ -435,8 +436,14 @@ __device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S,
     }
   }
   for (int i = tid; i < Ly.n_pre; i += kFwdThreads) {
-    if (load) szb[i] = Ly.zbar[(size_t)b * Ly.n_pre + i];
-    else Ly.zbar[(size_t)b * Ly.n_pre + i] = szb[i];
+    if (load) {
+      // the filter at the block's start also goes to the eligibility pass
+      const float z = Ly.zbar[(size_t)b * Ly.n_pre + i];
+      szb[i] = z;
+      Ly.zstart[(size_t)b * Ly.ldi + i] = z;
+    } else {
+      Ly.zbar[(size_t)b * Ly.n_pre + i] = szb[i];
+    }
   }
   for (int k = tid; k < A.K_out; k += kFwdThreads) {
     if (load) sy[k] = Ly.y[(size_t)b * A.K_out + k];
@@ -653,15 +660,44 @@ __global__ __launch_bounds__(256) void accumulate_kernel(const float* part, int 
 //   ebar_K = kappa^K E0 + P_j A0 + sum_s zbar_{i,s} U_{j,s}
 //   epsa_K = D_j A0           + sum_s zbar_{i,s} V_{j,s}
 //   g     += c_j E0 + q_j A0  + sum_s zbar_{i,s} H_{j,s}
-// The sums over s are dense contractions (MFMA); the rest is elementwise.
 // Coefficients (d_s = rho - beta_j psi_s, M_s = sum_{t>=s} kappa^{t-s} L_t,
 // N_s = sum_{r>s} beta_j psi_r M_r prod_{s<u<r} d_u):
 //   H_s = psi_s (M_s - N_s),  c = kappa M_0,  q = -N_{-1},
 //   U_s, P: the same with L replaced by the unit vector at the block's last
 //   step,  V_s = psi_s prod_{u>s} d_u,  D = prod_u d_u.
 // For LIF neurons beta_j = 0: N = 0, the epsa terms vanish.
+// The filter is zbar_s = alpha^{s+1} Z + sum_{r<=s} alpha^{s-r} p_r (Z: its
+// value at the block's start, p: the binary presynaptic values), so each sum
+// is one over the binary p against the alpha-filtered coefficients
+//   X'_r = sum_{s>=r} alpha^{s-r} X_s = X_r + alpha X'_{r+1},
+// plus Z alpha X'_0.  p is exact in fp16, so each contraction takes one MFMA
+// pass.  Written: U', H', V' as scaled pairs, and S [12][B][ldc]:
+//   0 c  1 q  2 P  3 D  4 1/sU  5 1/sH  6 1/sV  7 alpha U'_0  8 alpha H'_0
+//   9 alpha V'_0  (10, 11 not written)
+// The sums over s are dense contractions (MFMA); the rest is elementwise.
 // Two passes of the backward recursion: the first finds each array's largest
 // magnitude (its scale), the second writes the scaled pairs chunk by chunk.
+struct CoefState {
+  float M = 0.0f, Mu = 0.0f, nx = 0.0f, nxu = 0.0f, Dsuf = 1.0f;   // backward recursion
+  float up = 0.0f, hp = 0.0f, vp = 0.0f;                          // alpha-filtered U, H, V
+  // step s (of `steps`); returns U'_s, H'_s, V'_s
+  __device__ __forceinline__ void step(const CoefArgs& a, int s, float ps, float L, float bt,
+                                       float& u, float& h, float& v) {
+    const float d = a.rho - bt * ps;
+    M = fmaf(a.kappa, M, L);
+    Mu = (s == a.steps - 1) ? 1.0f : a.kappa * Mu;
+    up = fmaf(a.alpha, up, ps * (Mu - nxu));
+    hp = fmaf(a.alpha, hp, ps * (M - nx));
+    vp = fmaf(a.alpha, vp, ps * Dsuf);
+    nx = fmaf(bt * ps, M, d * nx);
+    nxu = fmaf(bt * ps, Mu, d * nxu);
+    Dsuf = d * Dsuf;
+    u = up;
+    h = hp;
+    v = vp;
+  }
+};
+
 __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   const int b = blockIdx.y;
@@ -670,35 +706,34 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
   const bool wv = a.V != nullptr && j < a.n_vcols;
   const float* __restrict__ psiK = a.psiK;
   const float* __restrict__ LK = a.LK;
-  auto load = [&](int s, float& ps, float& L) {
-    const size_t row = ((size_t)s * a.Bp + b) * a.ldv + j;
-    ps = psiK[row];
-    L = LK[row];
+  auto load_chunk = [&](int c, float (&ps)[kChunk], float (&L)[kChunk]) {
+#pragma unroll
+    for (int e = 0; e < kChunk; ++e) {
+      const int s = kChunk * c + e;
+      ps[e] = 0.0f;
+      L[e] = 0.0f;
+      if (s < a.steps) {
+        const size_t row = ((size_t)s * a.Bp + b) * a.ldv + j;
+        ps[e] = psiK[row];
+        L[e] = LK[row];
+      }
+    }
   };
   float mU = 0.0f, mH = 0.0f, mV = 0.0f;
   {
-    float M = 0.0f, Mu = 0.0f, nx = 0.0f, nxu = 0.0f, Dsuf = 1.0f;
+    CoefState st;
     for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
       float ps[kChunk], L[kChunk];
-#pragma unroll
-      for (int e = 0; e < kChunk; ++e) {
-        ps[e] = 0.0f;
-        L[e] = 0.0f;
-        if (kChunk * c + e < a.steps) load(kChunk * c + e, ps[e], L[e]);
-      }
+      load_chunk(c, ps, L);
 #pragma unroll
       for (int e = kChunk - 1; e >= 0; --e) {
         const int s = kChunk * c + e;
         if (s >= a.steps) continue;
-        const float d = a.rho - bt * ps[e];
-        M = fmaf(a.kappa, M, L[e]);
-        Mu = (s == a.steps - 1) ? 1.0f : a.kappa * Mu;
-        mH = fmaxf(mH, fabsf(ps[e] * (M - nx)));
-        mU = fmaxf(mU, fabsf(ps[e] * (Mu - nxu)));
-        mV = fmaxf(mV, fabsf(ps[e] * Dsuf));
-        nx = fmaf(bt * ps[e], M, d * nx);
-        nxu = fmaf(bt * ps[e], Mu, d * nxu);
-        Dsuf = d * Dsuf;
+        float u, h, v;
+        st.step(a, s, ps[e], L[e], bt, u, h, v);
+        mU = fmaxf(mU, fabsf(u));
+        mH = fmaxf(mH, fabsf(h));
+        mV = fmaxf(mV, fabsf(v));
       }
     }
   }
@@ -706,16 +741,10 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
   const float sU = ldexpf(1.0f, eU), sH = ldexpf(1.0f, eH), sV = ldexpf(1.0f, eV);
   const size_t rs = (size_t)a.ldc * kChunk;         // words between chunks
   const size_t o = ((size_t)b * kKC * a.ldc + j) * kChunk;
-  float M = 0.0f, Mu = 0.0f, nx = 0.0f, nxu = 0.0f, Dsuf = 1.0f;
+  CoefState st;
   for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
     float ps[kChunk], L[kChunk];
-#pragma unroll
-    for (int e = 0; e < kChunk; ++e) {
-      const int s = kChunk * c + e;
-      ps[e] = 0.0f;
-      L[e] = 0.0f;
-      if (s < a.steps) load(s, ps[e], L[e]);
-    }
+    load_chunk(c, ps, L);
     float u[kChunk], v[kChunk], h[kChunk];
 #pragma unroll
     for (int e = kChunk - 1; e >= 0; --e) {
@@ -724,28 +753,17 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
         u[e] = v[e] = h[e] = 0.0f;
         continue;
       }
-      const float d = a.rho - bt * ps[e];
-      M = fmaf(a.kappa, M, L[e]);
-      Mu = (s == a.steps - 1) ? 1.0f : a.kappa * Mu;
-      h[e] = ps[e] * (M - nx);
-      u[e] = ps[e] * (Mu - nxu);
-      v[e] = ps[e] * Dsuf;
-      nx = fmaf(bt * ps[e], M, d * nx);
-      nxu = fmaf(bt * ps[e], Mu, d * nxu);
-      Dsuf = d * Dsuf;
+      st.step(a, s, ps[e], L[e], bt, u[e], h[e], v[e]);
     }
     store_pairs(a.U + o + c * rs, u, sU);
     store_pairs(a.H + o + c * rs, h, sH);
     if (wv) store_pairs(a.V + o + c * rs, v, sV);
   }
   const size_t so = (size_t)b * a.ldc + j, plane = (size_t)a.B * a.ldc;
-  a.S[so] = a.kappa * M;              // c
-  a.S[plane + so] = -nx;              // q
-  a.S[2 * plane + so] = -nxu;         // P
-  a.S[3 * plane + so] = Dsuf;         // D
-  a.S[4 * plane + so] = 1.0f / sU;    // inverse scales (exact powers of two)
-  a.S[5 * plane + so] = 1.0f / sH;
-  a.S[6 * plane + so] = 1.0f / sV;
+  const float out[10] = {a.kappa * st.M, -st.nx, -st.nxu, st.Dsuf, 1.0f / sU, 1.0f / sH, 1.0f / sV,
+                         a.alpha * st.up, a.alpha * st.hp, a.alpha * st.vp};
+#pragma unroll
+  for (int k = 0; k < 10; ++k) a.S[k * plane + so] = out[k];
 }
 
 // Reset path kept in the gradient.  The membrane eligibility is then a
@@ -863,18 +881,19 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
 // A workgroup of 4 waves owns a 64 (i) x 64 (j) tile of synapses and one
 // split of the batch; wave w computes the 32 x 32 sub-tile (w / 2, w % 2).
 // For each batch element b of the split:
-//  * MFMA contractions C_U, C_V, C_H = coef_b[j][s] x zbar_b[i][s] over the
+//  * MFMA contractions C_U, C_V, C_H = coef_b[j][s] x p_b[i][s] over the
 //    block's steps (v_mfma_f32_16x16x32_f16 on the scaled fp16 pairs, 2x2
 //    blocks of 16x16 per wave), 16 steps ("a chunk") at a time, operands
 //    read from shared memory;
 //  * then the elementwise update of the traces, each read once and written
 //    once (1 KiB contiguous per wave instruction), and of the gradient.
 // Operands stream through a ring of kRing chunk slots in shared memory:
-// zbar_b rows i and U, H (and V) rows j of the chunk's 16 steps are copied by
+// p_b rows i and U, H (and V) rows j of the chunk's 16 steps are copied by
 // direct global-to-LDS loads (16 bytes per lane, no registers) up to
 // kRing - 1 chunks ahead of the chunk being contracted, across batch elements.  The
-// block-start traces of a batch element (registers) and its scalars c, q, P,
-// D (shared memory, double-buffered) travel with its first chunk.
+// block-start traces of a batch element (registers) and its scalars
+// (shared memory, double-buffered; with the block-start filter of the
+// tile's rows) travel with its first chunk.
 // Waits: copies and loads complete in order, so a chunk's copies are waited
 // for with an exact vmcnt; trace stores (which may complete out of order with
 // respect to loads) are drained once per batch element, at its first chunk.
@@ -927,13 +946,13 @@ __device__ __forceinline__ void dma16(const float* g, float* lds) {
   __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
 }
 
-// RT = false: the reset-stopped recursion (contractions U, H and, for tiles
-// holding adaptive neurons, V; traces ebar, epsa).  RT = true: the reset
-// path kept (coef_rt_kernel): contractions U = C_E, H = C_g, W = C_V and V =
-// C_A; traces ebar, epsv and epsa; the presynaptic operand is the binary p,
-// exact in fp16, so each contraction takes one MFMA pass.  Its five operand
-// slots use a ring of three chunks, which keeps two workgroups per compute
-// unit.
+// RT = false: the reset-stopped recursion (contractions U', H' and, for
+// tiles holding adaptive neurons, V'; traces ebar, epsa; coef_kernel).  RT =
+// true: the reset path kept (coef_rt_kernel): contractions U = C_E, H = C_g,
+// W = C_V and V = C_A; traces ebar, epsv and epsa.  Either way the
+// presynaptic operand is the binary p, exact in fp16, so each contraction
+// takes one MFMA pass.  The five operand slots of RT use a ring of three
+// chunks, which keeps two workgroups per compute unit.
 template <bool ALIF, int NCH, bool RT>
 struct TraceTile {
   static constexpr int RING = RT ? 3 : kRing;                 // chunk slots
@@ -1021,7 +1040,12 @@ struct TraceTile {
 #pragma unroll
         for (int m = 0; m < SC; ++m) {
           const int pl = w + 4 * m;
-          dma16(a.S + ((size_t)pl * a.B + b) * a.ldc + j0 + lane * 4, sb + pl * kTile);
+          // the reset-stopped form's last plane: the filter at the block's
+          // start of the tile's 64 rows i
+          const float* src = (!RT && pl == PLANES - 1)
+                                 ? a.zstart + (size_t)b * a.ldi + i0 + lane * 4
+                                 : a.S + ((size_t)pl * a.B + b) * a.ldc + j0 + lane * 4;
+          dma16(src, sb + pl * kTile);
         }
       }
     }
@@ -1066,23 +1090,26 @@ struct TraceTile {
     for (int bj = 0; bj < 2; ++bj) {
       const int cj = 32 * wj + 16 * bj + 4 * g;
       if constexpr (!RT) {
-        // c, q, P, D, 1/sU, 1/sH, 1/sV
+        // c, q, P, D, 1/sU, 1/sH, 1/sV, alpha U'_0, alpha H'_0, alpha V'_0
+        // (coef_kernel); the block-start filter Z of row i in the last plane
         const f32x4 c = plane(0, cj), qq = plane(1, cj);
         const f32x4 P = ALIF ? plane(2, cj) : zero;
         const f32x4 Dd = ALIF ? plane(3, cj) : zero;
-        const f32x4 fU = plane(4, cj) * a.zinv;
-        const f32x4 fH = plane(5, cj) * a.zinv;
-        const f32x4 fV = ALIF ? plane(6, cj) * a.zinv : zero;
+        const f32x4 fU = plane(4, cj), fH = plane(5, cj);
+        const f32x4 fV = ALIF ? plane(6, cj) : zero;
+        const f32x4 zU = plane(7, cj), zH = plane(8, cj);
+        const f32x4 zV = ALIF ? plane(9, cj) : zero;
 #pragma unroll
         for (int bi = 0; bi < 2; ++bi) {
           const f32x4 e0 = first ? zero : E[bj][bi];
           const f32x4 a0 = (first || !ALIF) ? zero : A[bj][bi];
+          const float Z = st[(PLANES - 1) * kTile + 32 * wi + 16 * bi + r];
           f32x4 ek, ak, gk;
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], cU[bj][bi][q] * fU[q]));
-            gk[q] = fmaf(c[q], e0[q], fmaf(qq[q], a0[q], cH[bj][bi][q] * fH[q]));
-            ak[q] = fmaf(Dd[q], a0[q], cV[bj][bi][q] * fV[q]);
+            ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], fmaf(zU[q], Z, cU[bj][bi][q] * fU[q])));
+            gk[q] = fmaf(c[q], e0[q], fmaf(qq[q], a0[q], fmaf(zH[q], Z, cH[bj][bi][q] * fH[q])));
+            ak[q] = fmaf(Dd[q], a0[q], fmaf(zV[q], Z, cV[bj][bi][q] * fV[q]));
           }
           gacc[bj][bi] += gk;
           const uint32_t o = (2 * bj + bi) * 1024u + lane * 16u;
@@ -1163,28 +1190,22 @@ struct TraceTile {
             issue<P>(b + a.n_split, c2 - NCH, (n + D) % RING, (k + 1) & 1);
         };
 
-        // Per output block and contraction X, fp16 MFMAs (K = 32) over the
+        // Per output block and contraction X, one fp16 MFMA (K = 32) over the
         // chunk's 16 steps.  Lane g holds steps 4g..4g+3 as (hi, lo) pairs of
-        // k slots: A = X's words as they are; B = (z_hi, z_hi) per step, then
-        // (z_lo, 0) with the same A: X_hi z_hi + X_lo z_hi + X_hi z_lo.  With
-        // RT, z is the binary p (z_lo = 0) and the second pass is left out.
-        constexpr int NPASS = RT ? 1 : 2;
+        // k slots: A = X's words as they are; B = (p, p) per step, which sums
+        // X_hi p + X_lo p (p is the binary presynaptic value, exact in fp16).
         const char* slot = (const char*)(sm + (n % RING) * SLOT);
         const int sw = (r >> 1) & 3;   // unit order of this lane's rows
         const f16x8 zero8 = {};
-        f16x8 bz1[2], bz2[2];
+        f16x8 bz[2];
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
           const int zr = 32 * wi + 16 * x + r;
           const u32x4 zw = *(const u32x4*)(slot + zr * 64 + ((g ^ sw) << 4));
-          u32x4 w1, w2;
+          u32x4 w1;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            w1[e] = (zw[e] & 0xFFFFu) | (zw[e] << 16);
-            w2[e] = zw[e] >> 16;
-          }
-          bz1[x] = __builtin_bit_cast(f16x8, w1);
-          bz2[x] = __builtin_bit_cast(f16x8, w2);
+          for (int e = 0; e < 4; ++e) w1[e] = (zw[e] & 0xFFFFu) | (zw[e] << 16);
+          bz[x] = __builtin_bit_cast(f16x8, w1);
         }
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj) {
@@ -1196,28 +1217,21 @@ struct TraceTile {
                         ? *(const f16x8*)(slot + (X + 1) * kOpBytes + cr * 64 + ((g ^ sw) << 4))
                         : zero8;
 #pragma unroll
-          for (int pass = 0; pass < NPASS; ++pass) {
-#pragma unroll
-            for (int bi = 0; bi < 2; ++bi) {
-              const f16x8 bz = pass == 0 ? bz1[bi] : bz2[bi];
-              cU[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[0], bz, cU[bj][bi], 0, 0, 0);
-              cH[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz, cH[bj][bi], 0, 0, 0);
-              if constexpr (ALIF)
-                cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[2], bz, cV[bj][bi], 0, 0, 0);
-              if constexpr (RT)
-                cW[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[3], bz, cW[bj][bi], 0, 0, 0);
-            }
-            if (pass == 0) {
-              __builtin_amdgcn_sched_barrier(0);
-              if (bj == 0) {
-                issue_next(std::integral_constant<int, 0>{});
-              } else {
-                issue_next(std::integral_constant<int, 1>{});
-                // the element's block-start traces, after chunk 0's copies
-                if constexpr (ch == 0) load_traces(b, E, A, Vm);
-              }
-              __builtin_amdgcn_sched_barrier(0);
-            }
+          for (int bi = 0; bi < 2; ++bi) {
+            cU[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[0], bz[bi], cU[bj][bi], 0, 0, 0);
+            cH[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz[bi], cH[bj][bi], 0, 0, 0);
+            if constexpr (ALIF)
+              cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[2], bz[bi], cV[bj][bi], 0, 0, 0);
+            if constexpr (RT)
+              cW[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[3], bz[bi], cW[bj][bi], 0, 0, 0);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          if (bj == 0) {
+            issue_next(std::integral_constant<int, 0>{});
+          } else {
+            issue_next(std::integral_constant<int, 1>{});
+            // the element's block-start traces, after chunk 0's copies
+            if constexpr (ch == 0) load_traces(b, E, A, Vm);
           }
           __builtin_amdgcn_sched_barrier(0);
         }

@@ -188,3 +188,43 @@ def test_block_form_rt_structure():
     V, A, E, g = block_form_rt(0.0, 0.0, 0.0, p, psi, L, kappa, rho, 1.8, alpha, 0.0)
     assert E == pytest.approx(ref[0], rel=1e-12) and A == pytest.approx(ref[1], rel=1e-12)
     assert g == pytest.approx(ref[2], rel=1e-12)
+
+
+# ---------------------------------------------------------------- binary-input form
+# zbar_s = alpha^(s+1) Z + sum_{r<=s} alpha^(s-r) p_r, with Z the filter at the
+# block's start, so every contraction with zbar is one with the binary p
+# against the alpha-filtered coefficients X'_r = sum_{s>=r} alpha^(s-r) X_s
+# (a backward recursion X'_r = X_r + alpha X'_{r+1}) plus Z alpha X'_0.
+def primed(X, alpha):
+    out = np.zeros_like(X)
+    acc = 0.0
+    for r in range(len(X) - 1, -1, -1):
+        acc = X[r] + alpha * acc
+        out[r] = acc
+    return out
+
+
+@pytest.mark.parametrize("beta", [0.0, 1.8])
+@pytest.mark.parametrize("K", [1, 3, 16, 100, 256])
+def test_binary_input_form_equals_recursion(K, beta):
+    rng = np.random.default_rng(3000 * K + int(10 * beta))
+    kappa, rho, alpha = np.exp(-1 / 20), np.exp(-1 / 200), np.exp(-1 / 20)
+    for _ in range(10):
+        p = (rng.random(K) < 0.3).astype(float)
+        Z = rng.uniform(0, 5)
+        zbar = np.zeros(K)
+        z = Z
+        for s in range(K):
+            z = alpha * z + p[s]
+            zbar[s] = z
+        psi = rng.uniform(0, 0.3, K) * (rng.random(K) < 0.6)
+        L = rng.normal(0, 1, K)
+        E0, A0 = rng.normal(0, 3, 2)
+        ref = step_by_step(E0, A0, zbar, psi, L, kappa, rho, beta)
+        U, V, H, c, q, P, D = block_coefficients(psi, L, kappa, rho, beta)
+        Up, Vp, Hp = primed(U, alpha), primed(V, alpha), primed(H, alpha)
+        got = (kappa ** K * E0 + P * A0 + p @ Up + Z * alpha * Up[0],
+               D * A0 + p @ Vp + Z * alpha * Vp[0],
+               c * E0 + q * A0 + p @ Hp + Z * alpha * Hp[0])
+        for r, x in zip(ref, got):
+            assert abs(r - x) <= 1e-11 * (1 + abs(r)), (K, beta, ref, got)
