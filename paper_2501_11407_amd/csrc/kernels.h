@@ -94,7 +94,7 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 // The presynaptic operand is binary: hi = 1.0 or 0, lo = 0.
 constexpr int kChunk = 16;                     // steps per chunk
 constexpr int kKC = kBlockSteps / kChunk;      // chunks per block
-constexpr int kScalarPlanes = 12;              // see coef_kernel
+constexpr int kScalarPlanes = 8;               // see coef_kernel
 
 // Block coefficients of the eligibility recursion, one thread per (b, j):
 // U', V', H' (against the binary presynaptic vector) as scaled fp16 pair

@@ -671,9 +671,10 @@ __global__ __launch_bounds__(256) void accumulate_kernel(const float* part, int 
 // is one over the binary p against the alpha-filtered coefficients
 //   X'_r = sum_{s>=r} alpha^{s-r} X_s = X_r + alpha X'_{r+1},
 // plus Z alpha X'_0.  p is exact in fp16, so each contraction takes one MFMA
-// pass.  Written: U', H', V' as scaled pairs, and S [12][B][ldc]:
-//   0 c  1 q  2 P  3 D  4 1/sU  5 1/sH  6 1/sV  7 alpha U'_0  8 alpha H'_0
-//   9 alpha V'_0  (10, 11 not written)
+// pass.  Written: U', H', V' as scaled pairs, and S [8][B][ldc]:
+//   0 c  1 q  2 P  3 D  4 the scale exponents of U', H', V' (one byte each,
+//   biased by 128, in the bits of the float)  5 alpha U'_0  6 alpha H'_0
+//   7 alpha V'_0
 // The sums over s are dense contractions (MFMA); the rest is elementwise.
 // Two passes of the backward recursion: the first finds each array's largest
 // magnitude (its scale), the second writes the scaled pairs chunk by chunk.
@@ -760,10 +761,11 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
     if (wv) store_pairs(a.V + o + c * rs, v, sV);
   }
   const size_t so = (size_t)b * a.ldc + j, plane = (size_t)a.B * a.ldc;
-  const float out[10] = {a.kappa * st.M, -st.nx, -st.nxu, st.Dsuf, 1.0f / sU, 1.0f / sH, 1.0f / sV,
-                         a.alpha * st.up, a.alpha * st.hp, a.alpha * st.vp};
+  const uint32_t ex = (uint32_t)(eU + 128) | ((uint32_t)(eH + 128) << 8) | ((uint32_t)(eV + 128) << 16);
+  const float out[8] = {a.kappa * st.M, -st.nx, -st.nxu, st.Dsuf, __uint_as_float(ex),
+                        a.alpha * st.up, a.alpha * st.hp, a.alpha * st.vp};
 #pragma unroll
-  for (int k = 0; k < 10; ++k) a.S[k * plane + so] = out[k];
+  for (int k = 0; k < 8; ++k) a.S[k * plane + so] = out[k];
 }
 
 // Reset path kept in the gradient.  The membrane eligibility is then a
@@ -960,7 +962,9 @@ struct TraceTile {
   static constexpr int NOP = RT ? 5 : 4;                      // operands per slot
   static constexpr int SLOT = NOP * kOpBytes / 4;             // floats per slot
   static constexpr int PLANES = RT ? kScalarPlanesRT : kScalarPlanes;
-  static constexpr int SCAL = PLANES * kTile;                 // floats of one scalar buffer
+  // floats of one scalar buffer: the planes, and for the reset-stopped form
+  // the block-start filter of the tile's 64 rows after them
+  static constexpr int SCAL = (PLANES + (RT ? 0 : 1)) * kTile;
   static constexpr size_t SMEM = sizeof(float) * (RING * SLOT + 2 * SCAL);
   // chunks in flight ahead; fewer than NCH so that a batch element's copies
   // never reach past the next element's first chunk
@@ -1020,8 +1024,13 @@ struct TraceTile {
   template <int P>
   __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
     char* slot = (char*)(sm + sl * SLOT);
-    const int rw = 16 * w + (lane >> 2);
-    const uint32_t q = (uint32_t)((lane & 3) ^ ((lane >> 3) & 3));
+    // the lane's row and unit, recomputed here for every copy: the compiler
+    // may not keep the addresses of all the chunks live at once
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    asm volatile("" : "+s"(b));
+    const int rw = 16 * w + (ln >> 2);
+    const uint32_t q = (uint32_t)((ln & 3) ^ ((ln >> 3) & 3));
     const uint32_t unit = q * 16u;
     const size_t cc = ((size_t)b * kKC + c) * a.ldc + j0 + rw;
     float* dst = (float*)(slot + w * 1024);
@@ -1035,17 +1044,20 @@ struct TraceTile {
         dma16((const float*)((const char*)a.V + cc * 64 + unit), dst + 3 * kOpBytes / 4);
       if constexpr (RT)
         dma16((const float*)((const char*)a.W + cc * 64 + unit), dst + 4 * kOpBytes / 4);
-      if (c == 0 && lane < 16) {
+      if (c == 0) {
         float* sb = sm + RING * SLOT + par * SCAL;
 #pragma unroll
         for (int m = 0; m < SC; ++m) {
           const int pl = w + 4 * m;
-          // the reset-stopped form's last plane: the filter at the block's
-          // start of the tile's 64 rows i
-          const float* src = (!RT && pl == PLANES - 1)
-                                 ? a.zstart + (size_t)b * a.ldi + i0 + lane * 4
-                                 : a.S + ((size_t)pl * a.B + b) * a.ldc + j0 + lane * 4;
-          dma16(src, sb + pl * kTile);
+          // lanes 0-15: plane pl; with the last plane of the reset-stopped
+          // form, lanes 16-31 copy the filter at the block's start of the
+          // tile's 64 rows i into the place after it
+          const bool zs = !RT && pl == PLANES - 1;
+          if (lane < 16 || (zs && lane < 32)) {
+            const float* src = lane < 16 ? a.S + ((size_t)pl * a.B + b) * a.ldc + j0 + lane * 4
+                                         : a.zstart + (size_t)b * a.ldi + i0 + (lane - 16) * 4;
+            dma16(src, sb + pl * kTile);
+          }
         }
       }
     }
@@ -1090,31 +1102,47 @@ struct TraceTile {
     for (int bj = 0; bj < 2; ++bj) {
       const int cj = 32 * wj + 16 * bj + 4 * g;
       if constexpr (!RT) {
-        // c, q, P, D, 1/sU, 1/sH, 1/sV, alpha U'_0, alpha H'_0, alpha V'_0
-        // (coef_kernel); the block-start filter Z of row i in the last plane
-        const f32x4 c = plane(0, cj), qq = plane(1, cj);
-        const f32x4 P = ALIF ? plane(2, cj) : zero;
-        const f32x4 Dd = ALIF ? plane(3, cj) : zero;
-        const f32x4 fU = plane(4, cj), fH = plane(5, cj);
-        const f32x4 fV = ALIF ? plane(6, cj) : zero;
-        const f32x4 zU = plane(7, cj), zH = plane(8, cj);
-        const f32x4 zV = ALIF ? plane(9, cj) : zero;
+        // c, q, P, D, scale exponents, alpha U'_0, alpha H'_0, alpha V'_0
+        // (coef_kernel); the block-start filter Z of row i after them.  One
+        // output at a time, with the planes it needs, so that few registers
+        // are live beside the contractions.
+        // 2^-e from the biased exponent byte at bit `sh`
+        auto inv_scale = [&](int sh) {
+          const f32x4 ex = plane(4, cj);
+          f32x4 f;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            f[q] = __uint_as_float((uint32_t)(255 - (int)((__float_as_uint(ex[q]) >> sh) & 0xFF)) << 23);
+          return f;
+        };
 #pragma unroll
         for (int bi = 0; bi < 2; ++bi) {
           const f32x4 e0 = first ? zero : E[bj][bi];
           const f32x4 a0 = (first || !ALIF) ? zero : A[bj][bi];
-          const float Z = st[(PLANES - 1) * kTile + 32 * wi + 16 * bi + r];
-          f32x4 ek, ak, gk;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], fmaf(zU[q], Z, cU[bj][bi][q] * fU[q])));
-            gk[q] = fmaf(c[q], e0[q], fmaf(qq[q], a0[q], fmaf(zH[q], Z, cH[bj][bi][q] * fH[q])));
-            ak[q] = fmaf(Dd[q], a0[q], fmaf(zV[q], Z, cV[bj][bi][q] * fV[q]));
-          }
-          gacc[bj][bi] += gk;
+          const float Z = st[PLANES * kTile + 32 * wi + 16 * bi + r];
           const uint32_t o = (2 * bj + bi) * 1024u + lane * 16u;
-          bstore(eR, o, ek);
-          if constexpr (ALIF) bstore(aR, o, ak);
+          {
+            const f32x4 P = ALIF ? plane(2, cj) : zero, zU = plane(5, cj), fU = inv_scale(0);
+            f32x4 ek;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], fmaf(zU[q], Z, cU[bj][bi][q] * fU[q])));
+            bstore(eR, o, ek);
+          }
+          {
+            const f32x4 c = plane(0, cj), qq = plane(1, cj), zH = plane(6, cj), fH = inv_scale(8);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              gacc[bj][bi][q] += fmaf(c[q], e0[q], fmaf(qq[q], a0[q], fmaf(zH[q], Z, cH[bj][bi][q] * fH[q])));
+          }
+          if constexpr (ALIF) {
+            const f32x4 Dd = plane(3, cj), zV = plane(7, cj), fV = inv_scale(16);
+            f32x4 ak;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              ak[q] = fmaf(Dd[q], a0[q], fmaf(zV[q], Z, cV[bj][bi][q] * fV[q]));
+            bstore(aR, o, ak);
+          }
         }
       } else {
         // gE gA gV eA eV aA aV vA vV 1/sU 1/sH 1/sV 1/sW (coef_rt_kernel)
