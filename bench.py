@@ -46,8 +46,8 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     neurons) read once and written once, one fp64 gradient accumulator of
     every (i, j) read and written once; the first launch after a reset reads
     neither.  Per timestep covered, the operands read once: the binary
-    presynaptic vector [B, N_pre] (one 4-byte pair word each), the
-    coefficients U, H [B, N] and V [B, N_adaptive]; per launch the seven
+    presynaptic vector [B, N_pre] (one byte each), the coefficients U, H
+    [B, N] and V [B, N_adaptive] (4-byte pair words); per launch the seven
     scalars c, q, P, D and the three block-start coefficients [B, N], and
     the block-start filter [B, N_pre].  With the reset path kept
     (reset_grad = 1): eps^v (every synapse) as a third trace, a fourth
@@ -58,7 +58,7 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     trace = 4 * B * npre * ((2 if rt else 1) * N + NA) + 8 * npre * N      # one direction
     rows = (3 if rt else 2) * N + NA
     scalars = 9 if rt else 7
-    operands = (steps * 4 * B * (npre + rows) + launches * scalars * 4 * B * N
+    operands = (steps * B * (npre + 4 * rows) + launches * scalars * 4 * B * N
                 + (0 if rt else launches * 4 * B * npre))
     return (2 * launches - first_launches) * trace + operands
 

@@ -60,7 +60,7 @@ struct Layer {
   float *psiK[2], *LK[2], *deltaK[2], *ztK[2];
   // the filtered presynaptic values as scaled fp16 pairs, and the block
   // coefficients of the eligibility recursion (same two slots)
-  uint32_t* z16[2];
+  uint8_t* p8[2];
   uint32_t *coefU[2], *coefV[2], *coefH[2], *coefW[2];
   float* coefS[2];
   float* zstart[2];                      // presynaptic filter at each block's start [B][ldi]
@@ -184,7 +184,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     const size_t ldc = plan->ldc;
     for (int sl = 0; sl < 2; ++sl) {
       // a scaled fp16 pair per value: 4 bytes, as fp32
-      L.z16[sl] = (uint32_t*)take(sizeof(uint32_t) * B * L.n_pre_pad * KM);
+      L.p8[sl] = (uint8_t*)take((size_t)B * L.n_pre_pad * KM);
       L.coefU[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
       L.coefV[sl] = (uint32_t*)take(c.n_adaptive > 0 ? sizeof(uint32_t) * B * ldc * KM : 0);
       L.coefH[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
@@ -202,15 +202,16 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
                            sizeof(float) * ((size_t)2 * c.n_layers * eprop::kFwdWaves * K + (size_t)c.n_layers * K +
                                             npre_total) +
                            (size_t)c.n_layers * 2 * npad4 + (size_t)eprop::kFwdXSteps * c.n_in;
-  // pair words of the presynaptic filter are written 4 steps at a time when
-  // that keeps the forward's shared memory small enough for an eligibility
-  // workgroup to share its compute unit, else 2 or 1
-  plan->zgroup = 1;
-  for (int zg : {4, 2}) {
-    const size_t sm = smem_base + sizeof(uint32_t) * zg * npre_total;
-    if (sm <= (zg == 4 ? 96 : 160) * 1024) { plan->zgroup = zg; break; }
+  // the binary presynaptic bytes are written 16 steps at a time (one 16-byte
+  // record per row) when that keeps the forward's shared memory small enough
+  // for an eligibility workgroup to share its compute unit, else 8 or 4
+  // (16 bytes of alignment before them)
+  plan->zgroup = 4;
+  for (int zg : {16, 8}) {
+    const size_t sm = smem_base + 16 + (size_t)zg * npre_total;
+    if (sm <= 96 * 1024) { plan->zgroup = zg; break; }
   }
-  plan->smem = smem_base + sizeof(uint32_t) * plan->zgroup * npre_total;
+  plan->smem = smem_base + 16 + (size_t)plan->zgroup * npre_total;
   plan->bytes = round_up(off, 256);
 }
 
@@ -329,7 +330,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     const Layer& L = P.layers[std::min(l, c.n_layers - 1)];
     f.Wt = L.Wt; f.ldw = L.ldw; f.WoutT = L.WoutT;
     f.v = L.v; f.a = L.a; f.ztil = L.ztil; f.z = L.z; f.zbar = L.zbar; f.y = L.y;
-    f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.z16 = L.z16[sl]; f.zstart = L.zstart[sl];
+    f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.p8 = L.p8[sl]; f.zstart = L.zstart[sl];
     f.deltaK = L.deltaK[sl]; f.ztK = L.ztK[sl];
     f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.rows_per_wave = L.rows_per_wave; f.ldi = L.n_pre_pad;
   }
@@ -389,7 +390,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     const Layer& L = P.layers[l];
     eprop::TraceArgs ta;
     ta.ebar = L.ebar; ta.epsa = L.epsa; ta.epsv = L.epsv; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
-    ta.n_split = L.n_split; ta.z16 = L.z16[sl];
+    ta.n_split = L.n_split; ta.p8 = L.p8[sl];
     ta.zstart = L.zstart[sl];
     ta.U = L.coefU[sl]; ta.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
     ta.W = L.coefW[sl]; ta.reset_through = c.reset_grad;

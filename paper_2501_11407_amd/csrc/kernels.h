@@ -7,10 +7,9 @@
 //   psiK   [Kmax*Bp][ldv]  pseudo-derivative (ldv = n_rec rounded to 256)
 //   deltaK [rows][ldk]     readout error (softmax - onehot)
 //   ztK    [rows][ldn]     kappa-filtered spikes
-//   z16    [B][Kmax/4][ldi][4] binary presynaptic vector as fp16 pair words
-//                                (1.0 or 0 in the low half, see below), one
-//                                32-bit word per step, 16 bytes per row and
-//                                step quad
+//   p8     [B][Kmax/16][ldi][16] binary presynaptic vector, one byte (0 or 1)
+//                                per step: a 16-byte record per row and
+//                                16-step chunk
 //   zstart [B][ldi]              presynaptic filter at the block's start
 // Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
 // psiK) and the readout gradient dW_out += deltaK^T * ztK; then the block
@@ -30,7 +29,6 @@ constexpr int kFwdWaves = kFwdThreads / 64;
 constexpr int kFwdXSteps = 8;                  // steps of input spikes staged in shared memory
 constexpr int kXRegs = 2;                      // input words (or bytes) per thread prefetched per step
 constexpr int kBlockSteps = 256;       // timesteps per block (Kmax)
-constexpr int kKQ = kBlockSteps / 4;   // step quads per block
 constexpr int kTile = 64;              // eligibility workgroup tile: 64 (i) x 64 (j)
 constexpr int kRowPad = kTile;         // n_pre padded to the tile height (ldi)
 constexpr int kColPad = kTile;         // n_rec padded to the tile width (ldc)
@@ -44,7 +42,7 @@ struct FwdLayer {
   float* y;                      // state [B][K_out]
   double* lossacc;               // [B]
   float* psiK;                   // [rows][ldj]
-  uint32_t* z16;                 // [B][Kmax/4][ldi][4]
+  uint8_t* p8;                   // [B][Kmax/16][ldi][16]
   float* zstart;                 // [B][ldi]
   float* deltaK; float* ztK;     // [rows][ldk], [rows][ldn]
   int n_inl, n_pre, rows_per_wave, ldi;
@@ -61,7 +59,7 @@ struct FwdArgs {
   int W32;
   int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldk, ldn, jlist;  // ldj: row stride of psiK
   float alpha, rho, kappa, thr, beta, gamma_over_thr;
-  int zgroup;                    // steps of pair words written together (1, 2 or 4)
+  int zgroup;                    // steps of p bytes written together (4, 8 or 16)
   size_t smem;
 };
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
@@ -91,7 +89,7 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 // pairs: a value x (times a power-of-two scale 2^e) is hi = fp16(x 2^e) plus
 // lo = fp16(x 2^e - hi), together about 22 significant bits, in one 32-bit
 // word (hi in the low half).  Per 16-step chunk and row, 16 words (64 bytes).
-// The presynaptic operand is binary: hi = 1.0 or 0, lo = 0.
+// The presynaptic operand is binary (bytes, expanded to fp16 in the kernel).
 constexpr int kChunk = 16;                     // steps per chunk
 constexpr int kKC = kBlockSteps / kChunk;      // chunks per block
 constexpr int kScalarPlanes = 8;               // see coef_kernel
@@ -126,7 +124,7 @@ struct TraceArgs {
   float* epsv;     // reset_through: [B][n_pre_pad / 64][n_jt][64 * 64]
   double* acc;     // [n_split][n_pre_pad][ldj] (row-major)
   size_t acc_stride;
-  const uint32_t* z16;                // [B][kKQ][ldi][4], ldi = n_pre_pad
+  const uint8_t* p8;                  // [B][kKC][ldi][16], ldi = n_pre_pad
   const float* zstart;                // [B][ldi] (reset-stopped form only)
   const uint32_t* U; const uint32_t* V; const uint32_t* H; const uint32_t* W;
   const float* S;                     // as CoefArgs

@@ -80,7 +80,7 @@ __device__ __forceinline__ void split16(float x, _Float16& hi, _Float16& lo) {
   lo = (_Float16)(x - (float)hi);
 }
 
-constexpr uint32_t kPairOne = 0x3C00u;   // the pair word of 1.0: fp16 1.0 in the low half
+constexpr uint32_t kPairOne = 0x3C00u;   // fp16 1.0
 
 // scaled value -> one 32-bit word: hi in the low half, lo in the high half
 __device__ __forceinline__ uint32_t pair_word(float x) {
@@ -120,7 +120,7 @@ __device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChu
 // The learning signal L = W_out^T delta is one GEMM over the whole block.
 struct FwdLds {
   int* act; int* mrg; int* spk; int* cnt; float* part; float* sy; float* szb;
-  uint32_t* zh;                  // [zgroup][npre_total]: pair words of the last zgroup steps
+  uint8_t* zb;                   // [npre_total][zgroup]: p of the last zgroup steps
   int npre_total;
   uint8_t* zc;
   uint8_t* xs;                   // [kFwdXSteps][n_in]: input spikes of steps t .. t+7, row t % 8
@@ -176,7 +176,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   else
     inp = S.zc + ((LI - 1) * 2 + (cur ^ 1)) * S.npad;
   float* szb = S.szb + (LI == 0 ? 0 : A.L[0].n_pre);
-  uint32_t* zring = S.zh + (LI == 0 ? 0 : A.L[0].n_pre);
+  uint8_t* zring = S.zb + (LI == 0 ? 0 : A.L[0].n_pre) * A.zgroup;
   float* sy = S.sy + LI * A.K_out;
   const size_t row = (size_t)t * A.Bp + b;
   // readout partial sums of this step and of the step before (by parity)
@@ -201,7 +201,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       on = sv != 0;
       const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
       szb[i] = zv;
-      zring[(t & (A.zgroup - 1)) * S.npre_total + i] = on ? kPairOne : 0u;
+      zring[i * A.zgroup + (t & (A.zgroup - 1))] = on ? 1 : 0;
     }
     const unsigned long long m = __ballot(on);
     if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
@@ -369,18 +369,20 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   }
   if (defer && w == kSoftWave && t > 0 && lane < A.K_out)
     Ly.deltaK[(row - A.Bp) * A.ldk + lane] = dk;
-  // the pair words go out zgroup steps at a time (4 * zgroup bytes per row)
+  // the p bytes go out zgroup steps at a time into the row's 16-byte record
+  // of the chunk (bytes past the block's last step are ignored downstream)
   if ((t & (A.zgroup - 1)) == A.zgroup - 1 || t == A.steps - 1) {
-    uint32_t* zpk = Ly.z16 + ((size_t)b * kKQ + t / 4) * Ly.ldi * 4 + ((t & 3) & ~(A.zgroup - 1));
-    const int np = S.npre_total;
+    uint8_t* zpk = Ly.p8 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * 16 +
+                   ((t & (kChunk - 1)) & ~(A.zgroup - 1));
     for (int i = i_beg + lane; i < i_end; i += kWave) {
-      uint32_t* d = zpk + (size_t)i * 4;
-      if (A.zgroup == 4)
-        *(u32x4*)d = u32x4{zring[i], zring[np + i], zring[2 * np + i], zring[3 * np + i]};
-      else if (A.zgroup == 2)
-        *(uint2*)d = uint2{zring[i], zring[np + i]};
+      uint8_t* d = zpk + (size_t)i * 16;
+      const uint8_t* src = zring + i * A.zgroup;
+      if (A.zgroup == 16)
+        *(u32x4*)d = *(const u32x4*)src;
+      else if (A.zgroup == 8)
+        *(uint2*)d = *(const uint2*)src;
       else
-        *d = zring[i];
+        *(uint32_t*)d = *(const uint32_t*)src;
     }
   }
   lds_barrier();
@@ -471,13 +473,13 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
   S.sy = S.part + NL * 2 * kFwdWaves * A.K_out;   // [n_layers][K_out]
   S.szb = S.sy + NL * A.K_out;                 // [n_pre_0 + n_pre_1]
   const int npre_total = A.L[0].n_pre + (NL > 1 ? A.L[1].n_pre : 0);
-  S.zh = (uint32_t*)(S.szb + npre_total);      // [zgroup][npre_total]
+  S.zb = (uint8_t*)(((uintptr_t)(S.szb + npre_total) + 15) & ~(uintptr_t)15);   // [npre_total][zgroup]
   S.npre_total = npre_total;
-  S.zc = (uint8_t*)(S.zh + A.zgroup * npre_total);   // [n_layers][2][npad]
+  S.zc = S.zb + A.zgroup * npre_total;         // [n_layers][2][npad]
   S.xs = S.zc + NL * 2 * S.npad;               // [kFwdXSteps][n_in]
   S.xwords = (A.n_in & 3) == 0 && ((uintptr_t)A.x & 3) == 0;
 
-  for (int e = threadIdx.x; e < A.zgroup * npre_total; e += kFwdThreads) S.zh[e] = 0u;
+  for (int e = threadIdx.x; e < A.zgroup * npre_total; e += kFwdThreads) S.zb[e] = 0;
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
   forward_state<QN, 0>(A, S, b, true, v0, a0, zt0, 0);
   if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, true, v1, a1, zt1, 0);
@@ -925,6 +927,7 @@ __device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, uint32_t off, f
 
 constexpr int kRing = 4;                              // chunk slots (reset-stopped)
 constexpr int kOpBytes = kTile * 64;                  // one operand of a chunk: 64 rows x 64 B
+constexpr int kPBytes = kTile * 16;                   // the chunk's p bytes: 64 rows x 16 B
 constexpr uint32_t kSubTileBytes = 32 * 32 * 4;
 
 // s_waitcnt immediate that waits for vmcnt <= n only (gfx9 encoding)
@@ -959,8 +962,10 @@ template <bool ALIF, int NCH, bool RT>
 struct TraceTile {
   static constexpr int RING = RT ? 3 : kRing;                 // chunk slots
   static constexpr int PREF = RING - 1;                       // chunks copied ahead
-  static constexpr int NOP = RT ? 5 : 4;                      // operands per slot
-  static constexpr int SLOT = NOP * kOpBytes / 4;             // floats per slot
+  // a slot: the chunk's p bytes (64 rows x 16 B), then the coefficient
+  // operands U, H, V (and W) of 64 rows x 64 B each
+  static constexpr int NOP = RT ? 4 : 3;                      // coefficient operands
+  static constexpr int SLOT = (kPBytes + NOP * kOpBytes) / 4; // floats per slot
   static constexpr int PLANES = RT ? kScalarPlanesRT : kScalarPlanes;
   // floats of one scalar buffer: the planes, and for the reset-stopped form
   // the block-start filter of the tile's 64 rows after them
@@ -1033,17 +1038,20 @@ struct TraceTile {
     const uint32_t q = (uint32_t)((ln & 3) ^ ((ln >> 3) & 3));
     const uint32_t unit = q * 16u;
     const size_t cc = ((size_t)b * kKC + c) * a.ldc + j0 + rw;
-    float* dst = (float*)(slot + w * 1024);
+    float* dst = (float*)(slot + kPBytes + w * 1024);
     if constexpr (P == 0) {
-      const size_t zq = ((size_t)b * kKQ + 4 * c + q) * a.ldi + i0 + rw;   // step quad 4c + q
-      dma16((const float*)((const char*)a.z16 + zq * 16), dst);
-      dma16((const float*)((const char*)a.U + cc * 64 + unit), dst + kOpBytes / 4);
+      // p: rows 16w .. 16w+15, one 16-byte record each (lanes 0-15)
+      if (ln < 16) {
+        const size_t zr = ((size_t)b * kKC + c) * a.ldi + i0 + 16 * w + ln;
+        dma16((const float*)(a.p8 + zr * 16), (float*)(slot + w * 256));
+      }
+      dma16((const float*)((const char*)a.U + cc * 64 + unit), dst);
     } else {
-      dma16((const float*)((const char*)a.H + cc * 64 + unit), dst + 2 * kOpBytes / 4);
+      dma16((const float*)((const char*)a.H + cc * 64 + unit), dst + kOpBytes / 4);
       if constexpr (ALIF)
-        dma16((const float*)((const char*)a.V + cc * 64 + unit), dst + 3 * kOpBytes / 4);
+        dma16((const float*)((const char*)a.V + cc * 64 + unit), dst + 2 * kOpBytes / 4);
       if constexpr (RT)
-        dma16((const float*)((const char*)a.W + cc * 64 + unit), dst + 4 * kOpBytes / 4);
+        dma16((const float*)((const char*)a.W + cc * 64 + unit), dst + 3 * kOpBytes / 4);
       if (c == 0) {
         float* sb = sm + RING * SLOT + par * SCAL;
 #pragma unroll
@@ -1228,11 +1236,12 @@ struct TraceTile {
         f16x8 bz[2];
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
+          // steps 4g .. 4g+3 of row zr: four p bytes -> (p, p) fp16 pairs
           const int zr = 32 * wi + 16 * x + r;
-          const u32x4 zw = *(const u32x4*)(slot + zr * 64 + ((g ^ sw) << 4));
+          const uint32_t pb = *(const uint32_t*)(slot + zr * 16 + g * 4);
           u32x4 w1;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) w1[e] = (zw[e] & 0xFFFFu) | (zw[e] << 16);
+          for (int e = 0; e < 4; ++e) w1[e] = ((pb >> (8 * e)) & 1u) * (kPairOne | (kPairOne << 16));
           bz[x] = __builtin_bit_cast(f16x8, w1);
         }
 #pragma unroll
@@ -1242,7 +1251,7 @@ struct TraceTile {
 #pragma unroll
           for (int X = 0; X < 4; ++X)
             ax[X] = ((X < 2) || (X == 2 && ALIF) || (X == 3 && RT))
-                        ? *(const f16x8*)(slot + (X + 1) * kOpBytes + cr * 64 + ((g ^ sw) << 4))
+                        ? *(const f16x8*)(slot + kPBytes + X * kOpBytes + cr * 64 + ((g ^ sw) << 4))
                         : zero8;
 #pragma unroll
           for (int bi = 0; bi < 2; ++bi) {
