@@ -41,12 +41,18 @@ void choose_splits(int M, int N, int K, int max_splits, int* splits, int* k_chun
 // per-step vectors for this many steps, independent of the sequence length.
 using eprop::kBlockSteps;
 
+// Per-block buffers rotate through kSlots slots: the forward of block k may
+// start once the eligibility pass of block k - kSlots has released its slot,
+// so the forward runs up to kSlots - 1 blocks ahead of the eligibility work.
+constexpr int kSlots = 2;
+
 struct Layer {
   int n_inl = 0, n_pre = 0;
   int n_pre_pad = 0;   // n_pre rounded to the eligibility kernel's row group
   int ldj = 0;    // n_rec rounded to 4: row stride of traces and accumulators
   int ldv = 0;    // n_rec rounded to 256: row stride of psiK, LK
   int ldw = 0;    // n_rec rounded to the forward workgroup size: row stride of Wt
+  int16_t* W16 = nullptr;   // the drive weights times 2^14 as int16 (FwdLayer::W16)
   int rows_per_wave = 0;
   const float* W_src = nullptr;
   const float* Wout_src = nullptr;
@@ -57,13 +63,13 @@ struct Layer {
   double* lossacc;                       // [B]
   // per-block vectors, two slots: the forward of block k+1 fills one while
   // the eligibility pass of block k reads the other
-  float *psiK[2], *LK[2], *deltaK[2], *ztK[2];
+  float *psiK[kSlots], *LK[kSlots], *deltaK[kSlots], *ztK[kSlots];
   // the filtered presynaptic values as scaled fp16 pairs, and the block
   // coefficients of the eligibility recursion (same two slots)
-  uint8_t* p8[2];
-  uint32_t *coefU[2], *coefV[2], *coefH[2], *coefW[2];
-  float* coefS[2];
-  float* zstart[2];                      // presynaptic filter at each block's start [B][ldi]
+  uint8_t* p8[kSlots];
+  uint32_t *coefU[kSlots], *coefV[kSlots], *coefH[kSlots], *coefW[kSlots];
+  float* coefS[kSlots];
+  float* zstart[kSlots];                 // presynaptic filter at each block's start [B][ldi]
   float* Cpart;
   double *acc, *accout;                  // gradient accumulators (acc: n_split partials)
   int n_split = 1;                       // batch splits of the eligibility kernel
@@ -76,6 +82,7 @@ struct Plan {
   eprop_config cfg;
   std::vector<Layer> layers;
   int* err_flag = nullptr;
+  int* w16ok = nullptr;             // 1: the int16 drive weights are exact (launch_pack16)
   int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, ldc = 0, jlist = 0, out_splits = 1;
   size_t smem = 0;
   int zgroup = 1;
@@ -134,6 +141,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   }
   const size_t R = plan->rows;
   plan->err_flag = (int*)take(sizeof(int));
+  plan->w16ok = (int*)take(sizeof(int));
   int rwmax = 0;
   size_t npre_total = 0;
   for (int l = 0; l < c.n_layers; ++l) {
@@ -149,6 +157,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     npre_total += L.n_pre;
     const size_t np = L.n_pre, npp = L.n_pre_pad;
     L.Wt = (float*)take(sizeof(float) * np * L.ldw);
+    L.W16 = (int16_t*)take(sizeof(int16_t) * np * eprop::forward_qn(N) * eprop::kFwdThreads);
     L.WoutT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.FbT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.v = (float*)take(sizeof(float) * B * N);
@@ -158,7 +167,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.y = (float*)take(sizeof(float) * B * K);
     L.z = (uint8_t*)take(B * N);
     L.lossacc = (double*)take(sizeof(double) * B);
-    for (int sl = 0; sl < 2; ++sl) {
+    for (int sl = 0; sl < kSlots; ++sl) {
       L.psiK[sl] = (float*)take(sizeof(float) * R * L.ldv);
       L.LK[sl] = (float*)take(sizeof(float) * R * L.ldv);
       L.deltaK[sl] = (float*)take(sizeof(float) * R * plan->ldk);
@@ -182,7 +191,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   }
   for (Layer& L : plan->layers) {
     const size_t ldc = plan->ldc;
-    for (int sl = 0; sl < 2; ++sl) {
+    for (int sl = 0; sl < kSlots; ++sl) {
       // a scaled fp16 pair per value: 4 bytes, as fp32
       L.p8[sl] = (uint8_t*)take((size_t)B * L.n_pre_pad * KM);
       L.coefU[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
@@ -192,7 +201,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
       const int planes = c.reset_grad ? eprop::kScalarPlanesRT : eprop::kScalarPlanes;
       L.coefS[sl] = (float*)take(sizeof(float) * planes * B * ldc);
     }
-    for (int sl = 0; sl < 2; ++sl) L.zstart[sl] = (float*)take(sizeof(float) * B * L.n_pre_pad);
+    for (int sl = 0; sl < kSlots; ++sl) L.zstart[sl] = (float*)take(sizeof(float) * B * L.n_pre_pad);
   }
   const size_t npad4 = round_up(N, 4);
   size_t npre_max = 0;
@@ -234,12 +243,11 @@ struct eprop_ctx {
   int last_steps = 1;   // steps of the last block (where the last step's vectors sit)
   int slot = 0;         // K-buffer slot the next block writes
   int last_slot = 0;    // slot of the last block
-  bool slot_used[2] = {false, false};
+  bool slot_used[kSlots] = {};
   // internal streams: the forward kernel, and the passes between it and the
   // eligibility kernel (learning signal, readout gradient, coefficients)
   hipStream_t fwd_stream = nullptr, coef_stream = nullptr;
-  hipEvent_t ev_entry = nullptr, ev_fwd[2] = {nullptr, nullptr}, ev_coef[2] = {nullptr, nullptr},
-             ev_done[2] = {nullptr, nullptr};
+  hipEvent_t ev_entry = nullptr, ev_fwd[kSlots] = {}, ev_coef[kSlots] = {}, ev_done[kSlots] = {};
   bool alive = false;
   std::string err;
   // profiling of the eligibility kernel
@@ -263,7 +271,14 @@ int check(eprop_ctx* ctx, hipError_t e, const char* what) {
 
 int pack_weights(eprop_ctx* ctx) {
   const eprop_config& c = ctx->plan.cfg;
+  // the int16 drive weights are used when every layer's are exact
+  int rc0 = check(ctx, eprop::launch_set_flag(ctx->plan.w16ok, 1, ctx->stream), "weight packing");
+  if (rc0) return rc0;
   for (Layer& L : ctx->plan.layers) {
+    int rc16 = check(ctx, eprop::launch_pack16(L.W_src, c.n_rec, L.n_pre, L.W16,
+                                               eprop::forward_qn(c.n_rec), ctx->plan.w16ok,
+                                               ctx->stream), "weight packing");
+    if (rc16) return rc16;
     // drive weights transposed, Wt[i][j] = W[j][i], columns padded to the
     // forward workgroup size
     int rc = check(ctx, eprop::launch_pack(L.W_src, c.n_rec, L.n_pre, L.Wt, L.ldw, L.n_pre, 1,
@@ -318,8 +333,8 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   const int first = ctx->t == 0;
   const int sl = ctx->slot;
   int rc;
-  // The forward may overwrite this slot once the passes that read it two
-  // blocks ago are done.
+  // The forward may overwrite this slot once the passes that read it
+  // kSlots blocks ago are done.
   if (ctx->slot_used[sl] &&
       (rc = check(ctx, hipStreamWaitEvent(sf, ctx->ev_done[sl], 0), "stream wait")))
     return rc;
@@ -328,14 +343,14 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   for (int l = 0; l < 2; ++l) {
     eprop::FwdLayer& f = fa.L[l];
     const Layer& L = P.layers[std::min(l, c.n_layers - 1)];
-    f.Wt = L.Wt; f.ldw = L.ldw; f.WoutT = L.WoutT;
+    f.Wt = L.Wt; f.ldw = L.ldw; f.W16 = L.W16; f.WoutT = L.WoutT;
     f.v = L.v; f.a = L.a; f.ztil = L.ztil; f.z = L.z; f.zbar = L.zbar; f.y = L.y;
     f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.p8 = L.p8[sl]; f.zstart = L.zstart[sl];
     f.deltaK = L.deltaK[sl]; f.ztK = L.ztK[sl];
     f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.rows_per_wave = L.rows_per_wave; f.ldi = L.n_pre_pad;
   }
   fa.n_layers = c.n_layers; fa.x = x; fa.n_in = c.n_in; fa.labels = labels;
-  fa.err_flag = P.err_flag; fa.spikes = spikes; fa.W32 = (c.n_rec + 31) / 32;
+  fa.err_flag = P.err_flag; fa.w16ok = P.w16ok; fa.spikes = spikes; fa.W32 = (c.n_rec + 31) / 32;
   fa.B = c.batch; fa.Bp = P.Bp; fa.n_rec = c.n_rec; fa.K_out = c.n_out;
   fa.n_adaptive = c.n_adaptive; fa.Kmax = P.Kmax; fa.steps = steps;
   fa.ldj = P.layers[0].ldv; fa.ldk = P.ldk; fa.ldn = P.ldn; fa.jlist = P.jlist;
@@ -416,7 +431,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   if ((rc = check(ctx, hipEventRecord(ctx->ev_done[sl], s), "event record"))) return rc;
   ctx->slot_used[sl] = true;
   ctx->last_slot = sl;
-  ctx->slot ^= 1;
+  ctx->slot = (ctx->slot + 1) % kSlots;
   ctx->t += steps;
   ctx->last_steps = steps;
   return EPROP_OK;
@@ -482,7 +497,7 @@ int eprop_init(const eprop_config* cfg, void* d_workspace, size_t ws_bytes,
   if (!rc) rc = check(ctx, hipStreamCreateWithFlags(&ctx->coef_stream, hipStreamNonBlocking),
                       "stream create");
   if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_entry, hipEventDisableTiming), "event create");
-  for (int k = 0; k < 2 && !rc; ++k) {
+  for (int k = 0; k < kSlots && !rc; ++k) {
     rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_fwd[k], hipEventDisableTiming), "event create");
     if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_coef[k], hipEventDisableTiming),
                         "event create");
@@ -590,10 +605,10 @@ void eprop_destroy(eprop_ctx* ctx) {
     (void)hipStreamSynchronize(st);
     (void)hipStreamDestroy(st);
   }
-  hipEvent_t own[] = {ctx->ev_entry, ctx->ev_fwd[0],  ctx->ev_fwd[1], ctx->ev_coef[0],
-                      ctx->ev_coef[1], ctx->ev_done[0], ctx->ev_done[1]};
-  for (hipEvent_t e : own)
-    if (e) (void)hipEventDestroy(e);
+  if (ctx->ev_entry) (void)hipEventDestroy(ctx->ev_entry);
+  for (int k = 0; k < kSlots; ++k)
+    for (hipEvent_t e : {ctx->ev_fwd[k], ctx->ev_coef[k], ctx->ev_done[k]})
+      if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
   ctx->alive = false;
   delete ctx;
@@ -656,6 +671,7 @@ int eprop_debug_buffer(eprop_ctx* ctx, int32_t layer, int32_t which, const float
     case 2: *d_ptr = L.psiK[ctx->last_slot] + tl * L.ldv; *cols = c.n_rec; *ld = L.ldv; break;
     case 3: *d_ptr = L.LK[ctx->last_slot] + tl * L.ldv; *cols = c.n_rec; *ld = L.ldv; break;
     case 4: *d_ptr = L.y; *cols = c.n_out; *ld = c.n_out; break;
+    case 5: *d_ptr = reinterpret_cast<const float*>(ctx->plan.w16ok); *cols = 1; *ld = 1; break;
     default: return fail(ctx, EPROP_EINVAL, "unknown buffer");
   }
   return EPROP_OK;

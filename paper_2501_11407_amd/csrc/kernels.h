@@ -35,6 +35,10 @@ constexpr int kColPad = kTile;         // n_rec padded to the tile width (ldc)
 
 struct FwdLayer {
   const float* Wt; int ldw;      // transposed drive weights [n_pre][ldw]
+  // the same times 2^14 as int16, row stride 512 * QN, neuron q * 512 + t
+  // at t * QN + q (QN: neurons per forward thread, a power of two); used
+  // when *FwdArgs::w16ok (see launch_pack16)
+  const int16_t* W16;
   const float* WoutT;            // transposed readout weights [n_rec_pad][ldk]
   float* v; float* a; float* ztil;   // state [B][n_rec]
   uint8_t* z;                    // state: spikes of the last step [B][n_rec]
@@ -60,6 +64,7 @@ struct FwdArgs {
   int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldk, ldn, jlist;  // ldj: row stride of psiK
   float alpha, rho, kappa, thr, beta, gamma_over_thr;
   int zgroup;                    // steps of p bytes written together (4, 8 or 16)
+  const int* w16ok;              // 1: every layer's W16 is exact (drive summed as integers)
   size_t smem;
 };
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
@@ -153,5 +158,17 @@ hipError_t launch_loss(const double* lossacc, int B, int n_layers, size_t layer_
 // dst[c][r] = src[r][c] (transpose = 1); every other element of dst is zero.
 hipError_t launch_pack(const float* src, int rows, int cols, float* dst, int ldd, int dst_rows,
                        int transpose, hipStream_t s);
+
+// Drive weights W [n_rec][n_pre] (row-major) -> W16 as FwdLayer::W16 for
+// QN = the forward's neurons per thread.  Clears *ok unless every weight is
+// k 2^-14 with integer |k| <= min(32767, (2^24 - 1) / n_pre): then each
+// partial sum of a drive is an integer below 2^24 in units of 2^-14, exact
+// in fp32 in any order, and summing k as integers gives the fp32 sum bit for
+// bit.  *ok is set to 1 by launch_set_flag before the layers are packed.
+hipError_t launch_pack16(const float* W, int n_rec, int n_pre, int16_t* W16, int qn, int* ok,
+                         hipStream_t s);
+hipError_t launch_set_flag(int* flag, int value, hipStream_t s);
+// neurons per forward thread for n_rec neurons (a power of two, at most 16)
+int forward_qn(int n_rec);
 
 }  // namespace eprop

@@ -9,6 +9,8 @@
 
 #include <math.h>
 
+#include <algorithm>
+
 #include <utility>
 
 namespace eprop {
@@ -125,6 +127,7 @@ struct FwdLds {
   uint8_t* zc;
   uint8_t* xs;                   // [kFwdXSteps][n_in]: input spikes of steps t .. t+7, row t % 8
   bool xwords;                   // rows 4-byte aligned: input rows copied as 32-bit words
+  bool w16;                      // drive from the int16 weights (FwdLayer::W16)
   int rwmax, npad;
 };
 
@@ -253,7 +256,33 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   float I[QN];
 #pragma unroll
   for (int q = 0; q < QN; ++q) I[q] = 0.0f;
-  for (int k0 = 0; k0 < total; k0 += UB) {
+  if (S.w16) {
+    // integer weights k (w = k 2^-14): the thread's QN of a row in one load
+    // of 2 QN bytes; integer sums are exact in any order and equal the fp32
+    // sequential sum
+    constexpr int UB16 = QN == 1 ? 32 : 64 / QN;
+    typedef int16_t i16v __attribute__((ext_vector_type(QN)));
+    int isum[QN];
+#pragma unroll
+    for (int q = 0; q < QN; ++q) isum[q] = 0;
+    for (int k0 = 0; k0 < total; k0 += UB16) {
+      const int ent = S.mrg[min(k0 + (lane & (UB16 - 1)), total - 1)];
+      i16v wk[UB16];
+#pragma unroll
+      for (int u = 0; u < UB16; ++u) {
+        const int i = __builtin_amdgcn_readlane(ent, u);
+        wk[u] = *(const i16v*)(Ly.W16 + (size_t)i * (QN * kFwdThreads) + (size_t)tid * QN);
+      }
+#pragma unroll
+      for (int u = 0; u < UB16; ++u)
+        if (k0 + u < total)
+#pragma unroll
+          for (int q = 0; q < QN; ++q) isum[q] += (int)wk[u][q];
+    }
+#pragma unroll
+    for (int q = 0; q < QN; ++q) I[q] = (float)isum[q] * 0x1p-14f;
+  }
+  for (int k0 = 0; !S.w16 && k0 < total; k0 += UB) {
     const int ent = S.mrg[min(k0 + (lane & (UB - 1)), total - 1)];   // past the end: the last row
     float wv[UB][QN];
 #pragma unroll
@@ -478,6 +507,7 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
   S.zc = S.zb + A.zgroup * npre_total;         // [n_layers][2][npad]
   S.xs = S.zc + NL * 2 * S.npad;               // [kFwdXSteps][n_in]
   S.xwords = (A.n_in & 3) == 0 && ((uintptr_t)A.x & 3) == 0;
+  S.w16 = *A.w16ok != 0;
 
   for (int e = threadIdx.x; e < A.zgroup * npre_total; e += kFwdThreads) S.zb[e] = 0;
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
@@ -1353,6 +1383,22 @@ __global__ void loss_kernel(const double* lossacc, int B, int n_layers, size_t l
   *out = s;
 }
 
+__global__ __launch_bounds__(256) void pack16_kernel(const float* W, int n_rec, int n_pre,
+                                                     int16_t* W16, int qn, int lim, int* ok) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)n_rec * n_pre) return;
+  const int j = (int)(idx / n_pre), i = (int)(idx % n_pre);
+  const float k = W[idx] * 16384.0f;
+  const bool exact = k == rintf(k) && fabsf(k) <= (float)lim;
+  if (!exact) *ok = 0;   // every thread that finds one writes the same value
+  W16[(size_t)i * (qn * kFwdThreads) + (size_t)(j % kFwdThreads) * qn + j / kFwdThreads] =
+      exact ? (int16_t)k : (int16_t)0;
+}
+
+__global__ void set_flag_kernel(int* flag, int value) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) *flag = value;
+}
+
 __global__ __launch_bounds__(256) void pack_kernel(const float* src, int rows, int cols, float* dst,
                                                    int ldd, int dst_rows, int transpose) {
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -1480,6 +1526,26 @@ hipError_t launch_grads(const GradsArgs& a, hipStream_t s) {
 hipError_t launch_loss(const double* lossacc, int B, int n_layers, size_t layer_stride,
                        double* out, hipStream_t s) {
   loss_kernel<<<1, 64, 0, s>>>(lossacc, B, n_layers, layer_stride, out);
+  return hipGetLastError();
+}
+
+int forward_qn(int n_rec) {
+  const int qn = (n_rec + kFwdThreads - 1) / kFwdThreads;
+  int p = 1;
+  while (p < qn) p *= 2;
+  return p;
+}
+
+hipError_t launch_pack16(const float* W, int n_rec, int n_pre, int16_t* W16, int qn, int* ok,
+                         hipStream_t s) {
+  const long long n = (long long)n_rec * n_pre;
+  const int lim = (int)std::min<long long>(32767, ((1LL << 24) - 1) / std::max(1, n_pre));
+  pack16_kernel<<<cdiv(n, 256), 256, 0, s>>>(W, n_rec, n_pre, W16, qn, lim, ok);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_flag(int* flag, int value, hipStream_t s) {
+  set_flag_kernel<<<1, 64, 0, s>>>(flag, value);
   return hipGetLastError();
 }
 

@@ -286,6 +286,15 @@ class EpropContext:
         flat = self.workspace[off:off + 4 * rows * ld].view(torch.float32)
         return flat.view(rows, ld)[:, :cols].clone()
 
+    def integer_drive(self) -> bool:
+        """Whether the drive sums the weights as integers in units of 2**-14
+        (every weight on that grid and small enough), else fp32 in ascending
+        input order; both give the same result where the first applies."""
+        ptr, _, _ = eprop_debug_buffer(self.ctx, 0, 5)
+        off = ptr - self.workspace.data_ptr()
+        torch.cuda.synchronize(self.device)
+        return bool(self.workspace[off:off + 4].view(torch.int32).item())
+
     # -- helpers
     def new_spike_buffer(self, T: Optional[int] = None) -> torch.Tensor:
         w32 = (self.shape.n_rec + 31) // 32

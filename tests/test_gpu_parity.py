@@ -74,6 +74,70 @@ def test_ragged_shapes(name):
         assert ref.spikes.any()
 
 
+# ---------------------------------------------------------------- drive paths
+# Weights on the 2**-14 grid (within the integer bound) are summed as
+# integers; any other weights as fp32 in ascending input order, which the
+# oracle's sequential fp32 sums reproduce bit for bit.
+def _off_grid(wl, seed):
+    rng = np.random.default_rng(seed)
+    for w in wl.W:
+        m = rng.random(w.shape) < 0.3
+        w[m] = (w[m] * f32(1 + 2.0 ** -20)).astype(np.float32)   # no longer a multiple of 2**-14
+
+
+def test_grid_weights_take_the_integer_drive():
+    shape, seed, scale = RAGGED["ralif2_two_layers"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+    assert ctx.integer_drive()
+    ctx.close()
+
+
+@pytest.mark.parametrize("name", ["rlif_ragged", "ralif2_two_layers", "blocks_256_50", "wide_1100",
+                                  "classes_100"])
+def test_off_grid_weights_take_the_float_drive(name):
+    shape, seed, scale = RAGGED[name]
+    banner(f"off-grid weights {name} {shape}")
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    _off_grid(wl, seed)
+    ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+    assert not ctx.integer_drive()
+    gpu = gpu_run(wl, ctx=ctx)
+    ctx.close()
+    errs, ref = check_against_oracle(wl, gpu)
+    assert ref.spikes.any()
+
+
+def test_large_grid_weight_takes_the_float_drive():
+    # on the grid but past the integer bound: 4.0 is 2**16 units of 2**-14
+    shape, seed, scale = RAGGED["ralif_ragged_na13"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    wl.W[0][3, 5] = f32(4.0)
+    ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+    assert not ctx.integer_drive()
+    gpu = gpu_run(wl, ctx=ctx)
+    ctx.close()
+    check_against_oracle(wl, gpu)
+
+
+def test_drive_path_follows_the_weights_over_resets():
+    shape, seed, scale = RAGGED["ralif_ragged_na13"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+    assert ctx.integer_drive()
+    a = gpu_run(wl, ctx=ctx)
+    keep = ctx.weights[0].clone()
+    ctx.weights[0][0, 0] += 2.0 ** -20
+    ctx.reset()
+    assert not ctx.integer_drive()
+    ctx.weights[0].copy_(keep)
+    ctx.reset()
+    assert ctx.integer_drive()
+    b = gpu_run(wl, ctx=ctx)
+    ctx.close()
+    assert np.array_equal(a["spikes"], b["spikes"]) and np.array_equal(a["dW"][0], b["dW"][0])
+
+
 # ---------------------------------------------------------------- random feedback
 @pytest.mark.parametrize("name", ["rlif_ragged", "ralif_ragged_na13", "ralif2_two_layers",
                                   "blocks_256_50"])
