@@ -980,6 +980,10 @@ typedef __attribute__((address_space(3))) void lds_void;
 __device__ __forceinline__ void dma16(const float* g, float* lds) {
   __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
 }
+// Lane l copies 4 bytes from its own address g to lds + 4 l.
+__device__ __forceinline__ void dma4(const float* g, float* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 4, 0, 0);
+}
 
 // RT = false: the reset-stopped recursion (contractions U', H' and, for
 // tiles holding adaptive neurons, V'; traces ebar, epsa; coef_kernel).  RT =
@@ -1070,11 +1074,11 @@ struct TraceTile {
     const size_t cc = ((size_t)b * kKC + c) * a.ldc + j0 + rw;
     float* dst = (float*)(slot + kPBytes + w * 1024);
     if constexpr (P == 0) {
-      // p: rows 16w .. 16w+15, one 16-byte record each (lanes 0-15)
-      if (ln < 16) {
-        const size_t zr = ((size_t)b * kKC + c) * a.ldi + i0 + 16 * w + ln;
-        dma16((const float*)(a.p8 + zr * 16), (float*)(slot + w * 256));
-      }
+      // p of rows 16w .. 16w+15: lane l takes the 4 bytes of steps 4g..4g+3
+      // (g = l / 16) of row 16w + l % 16, stored at dword 16 g + l % 16 of
+      // the group, so the operand reads of a half-wave hit 32 banks
+      const size_t zr = ((size_t)b * kKC + c) * a.ldi + i0 + 16 * w + (ln & 15);
+      dma4((const float*)(a.p8 + zr * 16 + (ln >> 4) * 4), (float*)(slot + w * 256));
       dma16((const float*)((const char*)a.U + cc * 64 + unit), dst);
     } else {
       dma16((const float*)((const char*)a.H + cc * 64 + unit), dst + kOpBytes / 4);
@@ -1268,7 +1272,7 @@ struct TraceTile {
         for (int x = 0; x < 2; ++x) {
           // steps 4g .. 4g+3 of row zr: four p bytes -> (p, p) fp16 pairs
           const int zr = 32 * wi + 16 * x + r;
-          const uint32_t pb = *(const uint32_t*)(slot + zr * 16 + g * 4);
+          const uint32_t pb = *(const uint32_t*)(slot + (zr >> 4) * 256 + g * 64 + (zr & 15) * 4);
           u32x4 w1;
 #pragma unroll
           for (int e = 0; e < 4; ++e) w1[e] = ((pb >> (8 * e)) & 1u) * (kPairOne | (kPairOne << 16));
