@@ -7,9 +7,10 @@
 //   psiK   [Kmax*Bp][ldv]  pseudo-derivative (ldv = n_rec rounded to 256)
 //   deltaK [rows][ldk]     readout error (softmax - onehot)
 //   ztK    [rows][ldn]     kappa-filtered spikes
-//   p8     [B][Kmax/16][ldi][16] binary presynaptic vector, one byte (0 or 1)
-//                                per step: a 16-byte record per row and
-//                                16-step chunk
+//   p8     [B][Kmax/16][ldi][16] binary presynaptic vector, one byte per
+//                                step (0x3C, the high byte of fp16 1.0, or
+//                                0): a 16-byte record per row and 16-step
+//                                chunk
 //   zstart [B][ldi]              presynaptic filter at the block's start
 // Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
 // psiK) and the readout gradient dW_out += deltaK^T * ztK; then the block

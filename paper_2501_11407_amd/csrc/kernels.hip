@@ -82,7 +82,9 @@ __device__ __forceinline__ void split16(float x, _Float16& hi, _Float16& lo) {
   lo = (_Float16)(x - (float)hi);
 }
 
-constexpr uint32_t kPairOne = 0x3C00u;   // fp16 1.0
+// p as stored: the high byte of fp16 1.0 for a spike, 0 otherwise, so that a
+// byte permute places it in both halves of an fp16 pair (0x3C00 0x3C00)
+constexpr uint8_t kPByte = 0x3C;
 
 // scaled value -> one 32-bit word: hi in the low half, lo in the high half
 __device__ __forceinline__ uint32_t pair_word(float x) {
@@ -204,7 +206,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       on = sv != 0;
       const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
       szb[i] = zv;
-      zring[i * A.zgroup + (t & (A.zgroup - 1))] = on ? 1 : 0;
+      zring[i * A.zgroup + (t & (A.zgroup - 1))] = on ? kPByte : 0;
     }
     const unsigned long long m = __ballot(on);
     if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
@@ -1063,11 +1065,7 @@ struct TraceTile {
   template <int P>
   __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
     char* slot = (char*)(sm + sl * SLOT);
-    // the lane's row and unit, recomputed here for every copy: the compiler
-    // may not keep the addresses of all the chunks live at once
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-    asm volatile("" : "+s"(b));
+    const int ln = lane;
     const int rw = 16 * w + (ln >> 2);
     const uint32_t q = (uint32_t)((ln & 3) ^ ((ln >> 3) & 3));
     const uint32_t unit = q * 16u;
@@ -1270,12 +1268,14 @@ struct TraceTile {
         f16x8 bz[2];
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
-          // steps 4g .. 4g+3 of row zr: four p bytes -> (p, p) fp16 pairs
+          // steps 4g .. 4g+3 of row zr: four p bytes (0 or 0x3C) -> (p, p)
+          // fp16 pairs, byte e into bytes 1 and 3 of word e (0 elsewhere)
           const int zr = 32 * wi + 16 * x + r;
           const uint32_t pb = *(const uint32_t*)(slot + (zr >> 4) * 256 + g * 64 + (zr & 15) * 4);
           u32x4 w1;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) w1[e] = ((pb >> (8 * e)) & 1u) * (kPairOne | (kPairOne << 16));
+          for (int e = 0; e < 4; ++e)
+            w1[e] = __builtin_amdgcn_perm(0u, pb, (uint32_t)((e << 24) | (0x0C << 16) | (e << 8) | 0x0C));
           bz[x] = __builtin_bit_cast(f16x8, w1);
         }
 #pragma unroll
