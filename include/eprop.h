@@ -66,10 +66,10 @@ typedef struct eprop_ctx eprop_ctx; /* opaque, host-side */
 /* Network shape and constants.  All constants are used as given, in fp32. */
 typedef struct {
   int32_t n_layers;   /* 1, or 2 for a stack fed layer-1 spikes of the same step */
-  int32_t batch;      /* B >= 1 */
-  int32_t n_in;       /* inputs of layer 0 */
-  int32_t n_rec;      /* neurons per layer */
-  int32_t n_out;      /* readout classes K */
+  int32_t batch;      /* 1 <= B <= 65535 */
+  int32_t n_in;       /* inputs of layer 0, 1 .. 65536 */
+  int32_t n_rec;      /* neurons per layer, 1 .. 8192 */
+  int32_t n_out;      /* readout classes K, 1 .. 1024 */
   int32_t recurrent;  /* 1: presynaptic vector [in ; z^{t-1}], 0: in only */
   int32_t n_adaptive; /* neurons j < n_adaptive are ALIF (0 <= n_adaptive <= n_rec) */
   float alpha;        /* membrane decay exp(-dt/tau_m), Eq. (8a) */

@@ -98,7 +98,8 @@ bool valid_config(const eprop_config* c, std::string* why) {
   }
   if (c->batch > 65535) { *why = "batch must be <= 65535"; return false; }
   if (c->n_out > 1024) { *why = "n_out must be <= 1024"; return false; }
-  if (c->n_rec > 16384) { *why = "n_rec must be <= 16384"; return false; }
+  // the forward keeps at most 16 neurons per thread of its 512
+  if (c->n_rec > 16 * eprop::kFwdThreads) { *why = "n_rec must be <= 8192"; return false; }
   if (c->n_in > 65536) { *why = "n_in must be <= 65536"; return false; }
   if (c->recurrent != 0 && c->recurrent != 1) { *why = "recurrent must be 0 or 1"; return false; }
   if (c->n_adaptive < 0 || c->n_adaptive > c->n_rec) {

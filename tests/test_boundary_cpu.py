@@ -61,6 +61,7 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
     dict(n_layers=3), dict(n_layers=0), dict(batch=0), dict(n_in=0), dict(n_rec=0),
     dict(n_out=0), dict(n_adaptive=-1), dict(n_adaptive=30), dict(recurrent=2),
     dict(thr=0.0), dict(alpha=float("nan")), dict(batch=70000), dict(reset_grad=2),
+    dict(n_rec=8193, n_adaptive=0), dict(n_out=1025), dict(n_in=65537),
 ])
 def test_invalid_configs_are_rejected_on_the_host(bad):
     shape = synth.EpropShape(batch=3, n_in=7, n_rec=29, n_out=5, T=10)
@@ -109,3 +110,13 @@ def test_binding_refuses_to_run_without_a_gpu_or_library(monkeypatch):
     monkeypatch.setattr(eprop, "_lib", None)
     with pytest.raises(RuntimeError):
         eprop.load_library("/nonexistent/libeprop.so")
+
+
+def test_shape_past_the_forward_shared_memory_is_rejected():
+    # a recurrent layer of 8192 neurons needs more than 160 KiB of shared
+    # memory in the forward kernel: no workspace size, and a reason
+    shape = synth.EpropShape(batch=1, n_in=100, n_rec=8192, n_out=10, T=5, n_adaptive=0)
+    assert eprop.eprop_workspace_bytes(eprop.make_config(shape)) == 0
+    assert "shared memory" in eprop.eprop_last_error()
+    ff = shape.replace(recurrent=0)
+    assert eprop.eprop_workspace_bytes(eprop.make_config(ff)) > 0

@@ -74,6 +74,23 @@ def test_ragged_shapes(name):
         assert ref.spikes.any()
 
 
+# ---------------------------------------------------------------- large layers
+# 8 and 16 neurons per forward thread, up to the largest accepted layer (a
+# feed-forward layer of 8192); every spike compared, the gradient on sampled
+# synapses (with every index-range edge) and the readout gradient in full.
+@pytest.mark.parametrize("n_rec,n_in,rec", [(3000, 200, 1), (6000, 100, 1), (8192, 200, 0)])
+def test_large_layers(n_rec, n_in, rec):
+    shape = synth.EpropShape(batch=2, n_in=n_in, n_rec=n_rec, n_out=10, T=24, recurrent=rec,
+                             n_adaptive=n_rec // 2)
+    banner(f"large layer {shape}")
+    wl = synth.make_workload(shape, 20 + n_rec, input_scale=4.0)
+    gpu = gpu_run(wl)
+    smp = sample_synapses(shape, seed=n_rec)
+    errs, ref = check_against_oracle(wl, gpu, sample=smp)
+    assert ref.spikes.any()
+    banner(f"{n_rec}: {errs}")
+
+
 # ---------------------------------------------------------------- drive paths
 # Weights on the 2**-14 grid (within the integer bound) are summed as
 # integers; any other weights as fp32 in ascending input order, which the
