@@ -129,13 +129,13 @@ def summarize_counters(fetch_dir: str, write_dir: str, copy_mib: int) -> dict:
     return out
 
 
-def cpu_baseline(wl, seconds_hint: float = 15.0):
+def cpu_baseline(wl, name: str, seconds_hint: float = 15.0):
     """The oracle (one thread, fp64 traces) over every synapse and all T
     steps of the first n_b batch elements, n_b chosen so that the run takes
     about seconds_hint on this host."""
     import oracle
     shape = wl.shape
-    per_step = shape.n_pre(0) * shape.n_rec * shape.n_layers
+    per_step = shape.syn_per_step()
     t0 = time.perf_counter()
     oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, b_lo=0, b_hi=1, want_spikes=False)
     probe = time.perf_counter() - t0
@@ -145,7 +145,7 @@ def cpu_baseline(wl, seconds_hint: float = 15.0):
     dt = time.perf_counter() - t0
     return {"value": n_b * per_step * shape.T / dt, "unit": "syn-steps/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"batch elements 0..{n_b - 1} of {WORKLOAD} (of {shape.batch}), all "
+            "sample": f"batch elements 0..{n_b - 1} of {name} (of {shape.batch}), all "
                       f"{per_step} synapses, all {shape.T} timesteps: {dt:.1f} s on one thread "
                       f"(fp64 traces)"}
 
@@ -161,6 +161,8 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=1024)
     ap.add_argument("--reset-grad", type=int, default=0, choices=(0, 1),
                     help="1: the same workload with the reset path kept in the gradient")
+    ap.add_argument("--workload", default=WORKLOAD,
+                    help="another named synthetic workload (the headline is the default)")
     args = ap.parse_args()
     if args.summarize_counters:
         print(json.dumps(summarize_counters(*args.summarize_counters, args.copy_mib)))
@@ -175,11 +177,14 @@ def main():
 
     from paper_2501_11407_amd import eprop, synth
 
-    wl = synth.named_workload(WORKLOAD)
+    if args.workload not in synth.WORKLOADS:
+        print(f"unknown workload {args.workload}; one of {sorted(synth.WORKLOADS)}", file=sys.stderr)
+        sys.exit(2)
+    wl = synth.named_workload(args.workload)
     if args.reset_grad:
         wl.shape = wl.shape.replace(reset_grad=1)
     shape = wl.shape
-    workload = WORKLOAD + ("_reset_grad" if args.reset_grad else "")
+    workload = args.workload + ("_reset_grad" if args.reset_grad else "")
     dev = torch.device("cuda:0")
     ctx = eprop.EpropContext(shape, wl.W, wl.Wout, device="cuda:0")
     x = torch.from_numpy(wl.x).to(dev)
@@ -221,7 +226,7 @@ def main():
     tflops = alg_flops / sec / 1e12
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": None if args.reset_grad else stored_traffic(shape),
+                "traffic": None if (args.reset_grad or args.workload != WORKLOAD) else stored_traffic(shape),
                 "kernel": "trace_kernel", "avg_launch_us": round(trace_ms * 1e3 / n_timed, 2),
                 "steps_per_launch": round(timed_steps / n_timed, 2),
                 "alg_hbm_bytes_per_launch": round(alg_bytes / n_timed),
@@ -249,7 +254,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl)
+        line["cpu_baseline"] = cpu_baseline(wl, workload)
     ctx.close()
     print(json.dumps(line), flush=True)
 
