@@ -59,6 +59,11 @@ def load(path: str = LIB_PATH):
         ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p,
     ]
+    lib.oracle_eprop_run_online.restype = ctypes.c_int
+    lib.oracle_eprop_run_online.argtypes = [
+        ctypes.POINTER(OracleConfig), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_int32, ctypes.c_void_p, ctypes.c_double, ctypes.c_int32, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.oracle_state_bytes.restype = ctypes.c_size_t
     lib.oracle_state_bytes.argtypes = [ctypes.POINTER(OracleConfig), ctypes.c_int32]
     if path == LIB_PATH:
@@ -159,6 +164,46 @@ def run(shape, W: Sequence[np.ndarray], Wout: Sequence[np.ndarray], x: np.ndarra
     if rc != 0:
         raise ValueError(f"oracle_eprop_run returned {rc}")
     return OracleResult(dW=dW, dWout=dWout, loss=float(loss[0]), spikes=spikes, record=recs)
+
+
+@dataclass
+class OnlineResult:
+    dW: list            # per layer fp64 [n_rec, n_pre]: the gradient of the whole run
+    dWout: list         # per layer fp64 [n_out, n_rec]
+    loss: float
+    spikes: np.ndarray  # uint32 [T, L, B, ceil(n_rec/32)]
+    W: list             # per layer fp32: the drive weights in use at the end
+    Wout: list          # per layer fp32: the readout weights in use at the end
+
+
+def run_online(shape, W: Sequence[np.ndarray], Wout: Sequence[np.ndarray], x: np.ndarray,
+               labels: np.ndarray, lr: float, every: int, *, T: Optional[int] = None,
+               fwd_fp32: bool = True, lib_path: str = LIB_PATH, **over) -> OnlineResult:
+    """Every batch element, every synapse, with online weight application:
+    every ``every`` steps the weights in use become W0 - lr * (gradient so
+    far) on the 2**-14 grid (oracle_eprop_run_online)."""
+    lib = load(lib_path)
+    cfg = make_config(shape, fwd_fp32=fwd_fp32, **over)
+    T = x.shape[0] if T is None else T
+    L, N, K, B = shape.n_layers, shape.n_rec, shape.n_out, shape.batch
+    Wc = [np.ascontiguousarray(w, dtype=np.float32) for w in W]
+    Woc = [np.ascontiguousarray(w, dtype=np.float32) for w in Wout]
+    xc = np.ascontiguousarray(x, dtype=np.uint8)
+    lab = np.ascontiguousarray(labels, dtype=np.int32)
+    assert xc.shape[0] >= T and xc.shape[1] == B and xc.shape[2] == shape.n_in
+    dW = [np.zeros(w.shape, dtype=np.float64) for w in Wc]
+    dWout = [np.zeros((K, N), dtype=np.float64) for _ in range(L)]
+    Wf = [np.empty_like(w) for w in Wc]
+    Wof = [np.empty_like(w) for w in Woc]
+    loss = np.zeros(1, dtype=np.float64)
+    spikes = np.zeros((T, L, B, (N + 31) // 32), dtype=np.uint32)
+    arr = lambda xs: ctypes.cast((ctypes.c_void_p * len(xs))(*[_ptr(a) for a in xs]), ctypes.c_void_p)
+    rc = lib.oracle_eprop_run_online(ctypes.byref(cfg), arr(Wc), arr(Woc), _ptr(xc), T, _ptr(lab),
+                                     float(lr), int(every), _ptr(spikes), arr(dW), arr(dWout),
+                                     _ptr(loss), arr(Wf), arr(Wof))
+    if rc != 0:
+        raise ValueError(f"oracle_eprop_run_online returned {rc}")
+    return OnlineResult(dW=dW, dWout=dWout, loss=float(loss[0]), spikes=spikes, W=Wf, Wout=Wof)
 
 
 def state_bytes(shape, n_sample: int = -1, fwd_fp32: bool = True) -> int:

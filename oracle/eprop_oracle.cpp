@@ -118,17 +118,22 @@ struct LayerState {
   std::vector<double> epsv;        // per-synapse eps^v (reset_through; without the next input)
 };
 
+// The state of one batch element: neuron state, filters and traces of every
+// layer (and the traces of the sampled synapses).
 template <typename R>
-int run(const oracle_config& c, const float* const* W, const float* const* Wout,
-        const float* const* Fb, const uint8_t* x, int T, const int32_t* labels, int b_lo, int b_hi,
-        const Synapse* sample, int n_sample, uint32_t* spikes, double* const* dW,
-        double* const* dWout, double* loss, const oracle_record* rec) {
-  const int NL = c.n_layers, B = c.batch, N = c.n_rec, K = c.n_out, NA = c.n_adaptive;
-  const int W32 = (N + 31) / 32;
-  const bool all = n_sample < 0;
-  double loss_sum = 0.0;
+struct Seq {
+  std::vector<LayerState<R>> st;
+  std::vector<double> ebar_s, epsa_s, epsv_s;
+};
 
-  std::vector<LayerState<R>> st(NL);
+template <typename R>
+void seq_alloc(const oracle_config& c, bool all, int n_sample, Seq<R>& q) {
+  const int NL = c.n_layers, N = c.n_rec, K = c.n_out, NA = c.n_adaptive;
+  std::vector<LayerState<R>>& st = q.st;
+  std::vector<double>& ebar_s = q.ebar_s;
+  std::vector<double>& epsa_s = q.epsa_s;
+  std::vector<double>& epsv_s = q.epsv_s;
+  st.assign(NL, LayerState<R>());
   for (int l = 0; l < NL; ++l) {
     LayerState<R>& s = st[l];
     s.n_in_l = (l == 0) ? c.n_in : N;
@@ -150,192 +155,212 @@ int run(const oracle_config& c, const float* const* W, const float* const* Wout,
       if (c.reset_through) s.epsv.assign((size_t)N * s.n_pre, 0.0);
     }
   }
-  std::vector<double> ebar_s, epsa_s, epsv_s;
   if (!all) {
     ebar_s.assign(n_sample, 0.0);
     epsa_s.assign(n_sample, 0.0);
     epsv_s.assign(n_sample, 0.0);
   }
-  std::vector<int> active;
+}
 
-  for (int b = b_lo; b < b_hi; ++b) {
-    // A new sequence: every state, trace and filter starts at zero (G_0 = 0).
+// A new sequence: every state, trace and filter starts at zero (G_0 = 0).
+template <typename R>
+void seq_zero(const oracle_config& c, Seq<R>& q) {
+  const int NL = c.n_layers;
+  std::vector<LayerState<R>>& st = q.st;
+  for (int l = 0; l < NL; ++l) {
+    LayerState<R>& s = st[l];
+    std::fill(s.v.begin(), s.v.end(), R(0));
+    std::fill(s.a.begin(), s.a.end(), R(0));
+    std::fill(s.z.begin(), s.z.end(), 0.0);
+    std::fill(s.z_prev.begin(), s.z_prev.end(), 0.0);
+    std::fill(s.zbar.begin(), s.zbar.end(), 0.0);
+    std::fill(s.y.begin(), s.y.end(), 0.0);
+    std::fill(s.ztil.begin(), s.ztil.end(), 0.0);
+    std::fill(s.ebar.begin(), s.ebar.end(), 0.0);
+    std::fill(s.epsa.begin(), s.epsa.end(), 0.0);
+    std::fill(s.epsv.begin(), s.epsv.end(), 0.0);
+  }
+  std::fill(q.ebar_s.begin(), q.ebar_s.end(), 0.0);
+  std::fill(q.epsa_s.begin(), q.epsa_s.end(), 0.0);
+  std::fill(q.epsv_s.begin(), q.epsv_s.end(), 0.0);
+}
+
+// Steps t_lo .. t_hi-1 of batch element b from the state q, adding the
+// gradient into dW, dWout and the loss into loss_sum (in step order).
+template <typename R>
+void steps(const oracle_config& c, const float* const* W, const float* const* Wout,
+           const float* const* Fb, const uint8_t* x, int b, int label, int t_lo, int t_hi,
+           const Synapse* sample, int n_sample, uint32_t* spikes, double* const* dW,
+           double* const* dWout, double& loss_sum, const oracle_record* rec, Seq<R>& q,
+           std::vector<int>& active) {
+  const int NL = c.n_layers, B = c.batch, N = c.n_rec, K = c.n_out, NA = c.n_adaptive;
+  const int W32 = (N + 31) / 32;
+  const bool all = n_sample < 0;
+  std::vector<LayerState<R>>& st = q.st;
+  std::vector<double>& ebar_s = q.ebar_s;
+  std::vector<double>& epsa_s = q.epsa_s;
+  std::vector<double>& epsv_s = q.epsv_s;
+  for (int t = t_lo; t < t_hi; ++t) {
     for (int l = 0; l < NL; ++l) {
       LayerState<R>& s = st[l];
-      std::fill(s.v.begin(), s.v.end(), R(0));
-      std::fill(s.a.begin(), s.a.end(), R(0));
-      std::fill(s.z.begin(), s.z.end(), 0.0);
-      std::fill(s.z_prev.begin(), s.z_prev.end(), 0.0);
-      std::fill(s.zbar.begin(), s.zbar.end(), 0.0);
-      std::fill(s.y.begin(), s.y.end(), 0.0);
-      std::fill(s.ztil.begin(), s.ztil.end(), 0.0);
-      std::fill(s.ebar.begin(), s.ebar.end(), 0.0);
-      std::fill(s.epsa.begin(), s.epsa.end(), 0.0);
-      std::fill(s.epsv.begin(), s.epsv.end(), 0.0);
-    }
-    std::fill(ebar_s.begin(), ebar_s.end(), 0.0);
-    std::fill(epsa_s.begin(), epsa_s.end(), 0.0);
-    std::fill(epsv_s.begin(), epsv_s.end(), 0.0);
-    const int label = labels[b];
+      const float* Wl = W[l];
+      const float* Wo = Wout[l];
+      const float* Fo = (Fb && Fb[l]) ? Fb[l] : Wo;   // feedback matrix of the learning signal
 
-    for (int t = 0; t < T; ++t) {
-      for (int l = 0; l < NL; ++l) {
-        LayerState<R>& s = st[l];
-        const float* Wl = W[l];
-        const float* Wo = Wout[l];
-        const float* Fo = (Fb && Fb[l]) ? Fb[l] : Wo;   // feedback matrix of the learning signal
+      // Presynaptic vector p^t = [input^t ; z^{t-1}] and its alpha filter:
+      // the eps^v component of G_t, since dv/dv = alpha and dv/dW_ji = p_i.
+      for (int i = 0; i < s.n_in_l; ++i)
+        s.p[i] = (l == 0) ? (x[((size_t)t * B + b) * c.n_in + i] ? 1.0 : 0.0) : st[l - 1].z[i];
+      if (c.recurrent)
+        for (int j = 0; j < N; ++j) s.p[s.n_in_l + j] = s.z_prev[j];
+      for (int i = 0; i < s.n_pre; ++i) s.zbar[i] = c.alpha * s.zbar[i] + s.p[i];
 
-        // Presynaptic vector p^t = [input^t ; z^{t-1}] and its alpha filter:
-        // the eps^v component of G_t, since dv/dv = alpha and dv/dW_ji = p_i.
-        for (int i = 0; i < s.n_in_l; ++i)
-          s.p[i] = (l == 0) ? (x[((size_t)t * B + b) * c.n_in + i] ? 1.0 : 0.0) : st[l - 1].z[i];
-        if (c.recurrent)
-          for (int j = 0; j < N; ++j) s.p[s.n_in_l + j] = s.z_prev[j];
-        for (int i = 0; i < s.n_pre; ++i) s.zbar[i] = c.alpha * s.zbar[i] + s.p[i];
+      // Drive I_j = sum_i W_ji p_i.  Terms with p_i = 0 add nothing, so only
+      // the nonzero entries are visited, in ascending i.
+      active.clear();
+      for (int i = 0; i < s.n_pre; ++i)
+        if (s.p[i] != 0.0) active.push_back(i);
 
-        // Drive I_j = sum_i W_ji p_i.  Terms with p_i = 0 add nothing, so only
-        // the nonzero entries are visited, in ascending i.
-        active.clear();
-        for (int i = 0; i < s.n_pre; ++i)
-          if (s.p[i] != 0.0) active.push_back(i);
+      // Neuron step, Eq. (8) with reset and adaptation, in precision R.
+      const R alpha = (R)c.alpha, rho = (R)c.rho, thr = (R)c.thr, reset = (R)c.reset;
+      for (int j = 0; j < N; ++j) {
+        R I = 0;
+        for (int i : active) I = I + (R)Wl[(size_t)j * s.n_pre + i] * (R)s.p[i];
+        const R zp = (R)s.z_prev[j];
+        R v = alpha * s.v[j];
+        v = v + I;
+        v = v - reset * zp;
+        R a = rho * s.a[j];
+        a = a + zp;
+        const R bj = (j < NA) ? (R)c.beta : R(0);
+        R A = bj * a;
+        A = thr + A;
+        const R xj = v - A;
+        s.v[j] = v;
+        s.a[j] = a;
+        const double xd = (double)xj;
+        s.z[j] = c.smooth ? smooth_spike(xd, c.thr, c.gamma) : (xj > R(0) ? 1.0 : 0.0);
+        const double u = 1.0 - std::fabs(xd) / c.thr;
+        s.psi[j] = (c.gamma / c.thr) * (u > 0.0 ? u : 0.0);
+      }
 
-        // Neuron step, Eq. (8) with reset and adaptation, in precision R.
-        const R alpha = (R)c.alpha, rho = (R)c.rho, thr = (R)c.thr, reset = (R)c.reset;
-        for (int j = 0; j < N; ++j) {
-          R I = 0;
-          for (int i : active) I = I + (R)Wl[(size_t)j * s.n_pre + i] * (R)s.p[i];
-          const R zp = (R)s.z_prev[j];
-          R v = alpha * s.v[j];
-          v = v + I;
-          v = v - reset * zp;
-          R a = rho * s.a[j];
-          a = a + zp;
-          const R bj = (j < NA) ? (R)c.beta : R(0);
-          R A = bj * a;
-          A = thr + A;
-          const R xj = v - A;
-          s.v[j] = v;
-          s.a[j] = a;
-          const double xd = (double)xj;
-          s.z[j] = c.smooth ? smooth_spike(xd, c.thr, c.gamma) : (xj > R(0) ? 1.0 : 0.0);
-          const double u = 1.0 - std::fabs(xd) / c.thr;
-          s.psi[j] = (c.gamma / c.thr) * (u > 0.0 ? u : 0.0);
-        }
+      // Leaky readout, softmax cross-entropy, learning signal, readout gradient.
+      for (int k = 0; k < K; ++k) {
+        double Y = 0.0;
+        for (int j = 0; j < N; ++j)
+          if (s.z[j] != 0.0) Y += (double)Wo[(size_t)k * N + j] * s.z[j];
+        s.y[k] = c.kappa * s.y[k] + Y;
+      }
+      double m = s.y[0];
+      for (int k = 1; k < K; ++k) m = s.y[k] > m ? s.y[k] : m;
+      double se = 0.0;
+      for (int k = 0; k < K; ++k) se += std::exp(s.y[k] - m);
+      for (int k = 0; k < K; ++k)
+        s.delta[k] = std::exp(s.y[k] - m) / se - (k == label ? 1.0 : 0.0);
+      loss_sum += std::log(se) - (s.y[label] - m);
+      for (int j = 0; j < N; ++j) {
+        double Lj = 0.0;
+        for (int k = 0; k < K; ++k) Lj += (double)Fo[(size_t)k * N + j] * s.delta[k];
+        s.L[j] = Lj;
+        s.ztil[j] = c.kappa * s.ztil[j] + s.z[j];
+      }
+      for (int k = 0; k < K; ++k)
+        for (int j = 0; j < N; ++j) dWout[l][(size_t)k * N + j] += s.delta[k] * s.ztil[j];
 
-        // Leaky readout, softmax cross-entropy, learning signal, readout gradient.
-        for (int k = 0; k < K; ++k) {
-          double Y = 0.0;
-          for (int j = 0; j < N; ++j)
-            if (s.z[j] != 0.0) Y += (double)Wo[(size_t)k * N + j] * s.z[j];
-          s.y[k] = c.kappa * s.y[k] + Y;
-        }
-        double m = s.y[0];
-        for (int k = 1; k < K; ++k) m = s.y[k] > m ? s.y[k] : m;
-        double se = 0.0;
-        for (int k = 0; k < K; ++k) se += std::exp(s.y[k] - m);
-        for (int k = 0; k < K; ++k)
-          s.delta[k] = std::exp(s.y[k] - m) / se - (k == label ? 1.0 : 0.0);
-        loss_sum += std::log(se) - (s.y[label] - m);
-        for (int j = 0; j < N; ++j) {
-          double Lj = 0.0;
-          for (int k = 0; k < K; ++k) Lj += (double)Fo[(size_t)k * N + j] * s.delta[k];
-          s.L[j] = Lj;
-          s.ztil[j] = c.kappa * s.ztil[j] + s.z[j];
-        }
-        for (int k = 0; k < K; ++k)
-          for (int j = 0; j < N; ++j) dWout[l][(size_t)k * N + j] += s.delta[k] * s.ztil[j];
-
-        // Eligibility vectors and gradient accumulation (Eq. 5 with diagonal H,
-        // then Eq. 3).  For synapse (j,i):
-        //   e      = psi_j (zbar_i - beta_j epsa_ji)     dz_j^t/dW_ji
-        //   ebar   = kappa ebar + e                      readout filter moved onto e
-        //   dW_ji += L_j ebar
-        //   epsa   = psi_j zbar_i + (rho - beta_j psi_j) epsa   (eps^a at t+1)
-        // With the reset path kept, zbar_i is replaced by the per-synapse
-        //   epsv   = epsv + p_i                              (eps^v at t)
-        // and after the step
-        //   epsv   = (alpha - reset psi_j) epsv + reset beta_j psi_j epsa
-        //   epsa   = psi_j epsv + (rho - beta_j psi_j) epsa  (both with the values at t).
-        if (c.reset_through) {
-          for (int q = 0; q < (all ? N * s.n_pre : n_sample); ++q) {
-            int j, i;
-            if (all) {
-              j = q / s.n_pre;
-              i = q - j * s.n_pre;
-            } else {
-              if (sample[q].layer != l) continue;
-              j = sample[q].j;
-              i = sample[q].i;
-            }
-            const bool adaptive = j < NA;
-            const double bj = adaptive ? c.beta : 0.0;
-            const double pj = s.psi[j];
-            const size_t ji = (size_t)j * s.n_pre + i;
-            double& ev = all ? s.epsv[ji] : epsv_s[q];
-            double& eb = all ? s.ebar[ji] : ebar_s[q];
-            double* eap = adaptive ? (all ? &s.epsa[ji] : &epsa_s[q]) : nullptr;
-            const double ea = eap ? *eap : 0.0;
-            const double V = ev + s.p[i];
-            const double e = pj * (V - bj * ea);
-            eb = c.kappa * eb + e;
-            (all ? dW[l][ji] : dW[0][q]) += s.L[j] * eb;
-            ev = (c.alpha - c.reset * pj) * V + c.reset * bj * pj * ea;
-            if (eap) *eap = pj * V + (c.rho - bj * pj) * ea;
-          }
-        } else if (all) {
-          for (int j = 0; j < N; ++j) {
-            const bool adaptive = j < NA;
-            const double bj = adaptive ? c.beta : 0.0;
-            const double pj = s.psi[j], Lj = s.L[j];
-            for (int i = 0; i < s.n_pre; ++i) {
-              const size_t ji = (size_t)j * s.n_pre + i;
-              const double ea = adaptive ? s.epsa[ji] : 0.0;
-              const double e = pj * (s.zbar[i] - bj * ea);
-              s.ebar[ji] = c.kappa * s.ebar[ji] + e;
-              dW[l][ji] += Lj * s.ebar[ji];
-              if (adaptive) s.epsa[ji] = pj * s.zbar[i] + (c.rho - bj * pj) * ea;
-            }
-          }
-        } else {
-          for (int q = 0; q < n_sample; ++q) {
+      // Eligibility vectors and gradient accumulation (Eq. 5 with diagonal H,
+      // then Eq. 3).  For synapse (j,i):
+      //   e      = psi_j (zbar_i - beta_j epsa_ji)     dz_j^t/dW_ji
+      //   ebar   = kappa ebar + e                      readout filter moved onto e
+      //   dW_ji += L_j ebar
+      //   epsa   = psi_j zbar_i + (rho - beta_j psi_j) epsa   (eps^a at t+1)
+      // With the reset path kept, zbar_i is replaced by the per-synapse
+      //   epsv   = epsv + p_i                              (eps^v at t)
+      // and after the step
+      //   epsv   = (alpha - reset psi_j) epsv + reset beta_j psi_j epsa
+      //   epsa   = psi_j epsv + (rho - beta_j psi_j) epsa  (both with the values at t).
+      if (c.reset_through) {
+        for (int q = 0; q < (all ? N * s.n_pre : n_sample); ++q) {
+          int j, i;
+          if (all) {
+            j = q / s.n_pre;
+            i = q - j * s.n_pre;
+          } else {
             if (sample[q].layer != l) continue;
-            const int j = sample[q].j, i = sample[q].i;
-            const bool adaptive = j < NA;
-            const double bj = adaptive ? c.beta : 0.0;
-            const double pj = s.psi[j];
-            const double ea = adaptive ? epsa_s[q] : 0.0;
+            j = sample[q].j;
+            i = sample[q].i;
+          }
+          const bool adaptive = j < NA;
+          const double bj = adaptive ? c.beta : 0.0;
+          const double pj = s.psi[j];
+          const size_t ji = (size_t)j * s.n_pre + i;
+          double& ev = all ? s.epsv[ji] : epsv_s[q];
+          double& eb = all ? s.ebar[ji] : ebar_s[q];
+          double* eap = adaptive ? (all ? &s.epsa[ji] : &epsa_s[q]) : nullptr;
+          const double ea = eap ? *eap : 0.0;
+          const double V = ev + s.p[i];
+          const double e = pj * (V - bj * ea);
+          eb = c.kappa * eb + e;
+          (all ? dW[l][ji] : dW[0][q]) += s.L[j] * eb;
+          ev = (c.alpha - c.reset * pj) * V + c.reset * bj * pj * ea;
+          if (eap) *eap = pj * V + (c.rho - bj * pj) * ea;
+        }
+      } else if (all) {
+        for (int j = 0; j < N; ++j) {
+          const bool adaptive = j < NA;
+          const double bj = adaptive ? c.beta : 0.0;
+          const double pj = s.psi[j], Lj = s.L[j];
+          for (int i = 0; i < s.n_pre; ++i) {
+            const size_t ji = (size_t)j * s.n_pre + i;
+            const double ea = adaptive ? s.epsa[ji] : 0.0;
             const double e = pj * (s.zbar[i] - bj * ea);
-            ebar_s[q] = c.kappa * ebar_s[q] + e;
-            dW[0][q] += s.L[j] * ebar_s[q];
-            if (adaptive) epsa_s[q] = pj * s.zbar[i] + (c.rho - bj * pj) * ea;
+            s.ebar[ji] = c.kappa * s.ebar[ji] + e;
+            dW[l][ji] += Lj * s.ebar[ji];
+            if (adaptive) s.epsa[ji] = pj * s.zbar[i] + (c.rho - bj * pj) * ea;
           }
         }
-
-        if (spikes) {
-          uint32_t* row = spikes + (((size_t)t * NL + l) * B + b) * W32;
-          for (int w = 0; w < W32; ++w) row[w] = 0;
-          for (int j = 0; j < N; ++j)
-            if (s.z[j] > 0.0) row[j / 32] |= 1u << (j % 32);
-        }
-        if (rec) {
-          const size_t o = (((size_t)t * NL + l) * B + b) * N;
-          for (int j = 0; j < N; ++j) {
-            if (rec->v) rec->v[o + j] = (double)s.v[j];
-            if (rec->a) rec->a[o + j] = (double)s.a[j];
-            if (rec->psi) rec->psi[o + j] = s.psi[j];
-            if (rec->L) rec->L[o + j] = s.L[j];
-            if (rec->z) rec->z[o + j] = s.z[j];
-          }
-          if (rec->y)
-            for (int k = 0; k < K; ++k)
-              rec->y[(((size_t)t * NL + l) * B + b) * K + k] = s.y[k];
+      } else {
+        for (int q = 0; q < n_sample; ++q) {
+          if (sample[q].layer != l) continue;
+          const int j = sample[q].j, i = sample[q].i;
+          const bool adaptive = j < NA;
+          const double bj = adaptive ? c.beta : 0.0;
+          const double pj = s.psi[j];
+          const double ea = adaptive ? epsa_s[q] : 0.0;
+          const double e = pj * (s.zbar[i] - bj * ea);
+          ebar_s[q] = c.kappa * ebar_s[q] + e;
+          dW[0][q] += s.L[j] * ebar_s[q];
+          if (adaptive) epsa_s[q] = pj * s.zbar[i] + (c.rho - bj * pj) * ea;
         }
       }
-      for (int l = 0; l < NL; ++l) st[l].z_prev = st[l].z;
-    }
-  }
 
-  // No self-connections: the recurrent diagonal is not a parameter.
+      if (spikes) {
+        uint32_t* row = spikes + (((size_t)t * NL + l) * B + b) * W32;
+        for (int w = 0; w < W32; ++w) row[w] = 0;
+        for (int j = 0; j < N; ++j)
+          if (s.z[j] > 0.0) row[j / 32] |= 1u << (j % 32);
+      }
+      if (rec) {
+        const size_t o = (((size_t)t * NL + l) * B + b) * N;
+        for (int j = 0; j < N; ++j) {
+          if (rec->v) rec->v[o + j] = (double)s.v[j];
+          if (rec->a) rec->a[o + j] = (double)s.a[j];
+          if (rec->psi) rec->psi[o + j] = s.psi[j];
+          if (rec->L) rec->L[o + j] = s.L[j];
+          if (rec->z) rec->z[o + j] = s.z[j];
+        }
+        if (rec->y)
+          for (int k = 0; k < K; ++k)
+            rec->y[(((size_t)t * NL + l) * B + b) * K + k] = s.y[k];
+      }
+    }
+    for (int l = 0; l < NL; ++l) st[l].z_prev = st[l].z;
+  }
+}
+
+// No self-connections: the recurrent diagonal is not a parameter.
+void zero_diagonal(const oracle_config& c, bool all, const Synapse* sample, int n_sample,
+                   double* const* dW) {
+  const int NL = c.n_layers, N = c.n_rec;
   if (all && c.recurrent)
     for (int l = 0; l < NL; ++l) {
       const int n_in_l = (l == 0) ? c.n_in : N;
@@ -347,7 +372,78 @@ int run(const oracle_config& c, const float* const* W, const float* const* Wout,
       const int n_in_l = (sample[q].layer == 0) ? c.n_in : N;
       if (c.recurrent && sample[q].i == n_in_l + sample[q].j) dW[0][q] = 0.0;
     }
+}
+
+template <typename R>
+int run(const oracle_config& c, const float* const* W, const float* const* Wout,
+        const float* const* Fb, const uint8_t* x, int T, const int32_t* labels, int b_lo, int b_hi,
+        const Synapse* sample, int n_sample, uint32_t* spikes, double* const* dW,
+        double* const* dWout, double* loss, const oracle_record* rec) {
+  const bool all = n_sample < 0;
+  double loss_sum = 0.0;
+  Seq<R> q;
+  seq_alloc(c, all, n_sample, q);
+  std::vector<int> active;
+  for (int b = b_lo; b < b_hi; ++b) {
+    seq_zero(c, q);
+    steps(c, W, Wout, Fb, x, b, labels[b], 0, T, sample, n_sample, spikes, dW, dWout, loss_sum, rec,
+          q, active);
+  }
+  zero_diagonal(c, all, sample, n_sample, dW);
   *loss += loss_sum;
+  return 0;
+}
+
+// Online weight application: the gradient is available at every step
+// (Sec. III-A), so the weights may change within the sequence.  Every `every`
+// steps from the start, once every batch element has run them, the drive and
+// readout weights in use become W0 - lr * G rounded to the nearest multiple
+// of 2^-14 (ties to even), G being the gradient accumulated so far over all
+// elements and steps; the recurrent diagonal keeps its W0 value.  All batch
+// elements advance together, block by block, so each keeps its own state.
+float on_grid(double v) { return (float)(std::nearbyint(v * 16384.0) / 16384.0); }
+
+template <typename R>
+int run_online(const oracle_config& c, const float* const* W0, const float* const* Wout0,
+               const uint8_t* x, int T, const int32_t* labels, double lr, int every,
+               uint32_t* spikes, double* const* dW, double* const* dWout, double* loss,
+               float* const* Wcur, float* const* Woutcur) {
+  const int NL = c.n_layers, B = c.batch, N = c.n_rec, K = c.n_out;
+  for (int l = 0; l < NL; ++l) {
+    const size_t n_pre = (size_t)((l == 0) ? c.n_in : N) + (c.recurrent ? N : 0);
+    std::memcpy(Wcur[l], W0[l], sizeof(float) * N * n_pre);
+    std::memcpy(Woutcur[l], Wout0[l], sizeof(float) * (size_t)K * N);
+  }
+  std::vector<Seq<R>> qs(B);
+  for (Seq<R>& q : qs) {
+    seq_alloc(c, true, -1, q);
+    seq_zero(c, q);
+  }
+  std::vector<double> loss_b(B, 0.0);
+  std::vector<int> active;
+  for (int t0 = 0; t0 < T; t0 += every) {
+    const int t1 = t0 + every < T ? t0 + every : T;
+    for (int b = 0; b < B; ++b)
+      steps(c, Wcur, Woutcur, nullptr, x, b, labels[b], t0, t1, nullptr, -1, spikes, dW, dWout,
+            loss_b[b], nullptr, qs[b], active);
+    if (t1 == T) break;
+    for (int l = 0; l < NL; ++l) {
+      const int n_in_l = (l == 0) ? c.n_in : N;
+      const int n_pre = n_in_l + (c.recurrent ? N : 0);
+      for (int j = 0; j < N; ++j)
+        for (int i = 0; i < n_pre; ++i) {
+          if (c.recurrent && i == n_in_l + j) continue;
+          const size_t ji = (size_t)j * n_pre + i;
+          Wcur[l][ji] = on_grid((double)W0[l][ji] - lr * dW[l][ji]);
+        }
+      for (size_t kj = 0; kj < (size_t)K * N; ++kj)
+        Woutcur[l][kj] = on_grid((double)Wout0[l][kj] - lr * dWout[l][kj]);
+    }
+  }
+  zero_diagonal(c, true, nullptr, -1, dW);
+  double total = 0.0;
+  for (int b = 0; b < B; ++b) total += loss_b[b];
+  *loss += total;
   return 0;
 }
 
@@ -412,6 +508,27 @@ int oracle_eprop_run_fb(const oracle_config* c, const float* const* W, const flo
                       loss, rec);
   return run<double>(*c, W, Wout, Fb, x, T, labels, b_lo, b_hi, smp, n_sample, spikes, dW, dWout,
                      loss, rec);
+}
+
+// Every batch element over T steps with online weight application every
+// `every` steps (see run_online): dW, dWout (zeroed by the caller) receive the
+// gradient of the whole run, W_final[l], Wout_final[l] (layouts of W, Wout)
+// the weights in use at its end.  Spikes as oracle_eprop_run_fb.
+int oracle_eprop_run_online(const oracle_config* c, const float* const* W,
+                            const float* const* Wout, const uint8_t* x, int32_t T,
+                            const int32_t* labels, double lr, int32_t every, uint32_t* spikes,
+                            double* const* dW, double* const* dWout, double* loss,
+                            float* const* W_final, float* const* Wout_final) {
+  if (!valid(c) || !W || !Wout || !x || !labels || !dW || !dWout || !loss || !W_final ||
+      !Wout_final || T < 0 || every < 1)
+    return -1;
+  for (int b = 0; b < c->batch; ++b)
+    if (labels[b] < 0 || labels[b] >= c->n_out) return -1;
+  if (c->fwd_fp32)
+    return run_online<float>(*c, W, Wout, x, T, labels, lr, every, spikes, dW, dWout, loss, W_final,
+                             Wout_final);
+  return run_online<double>(*c, W, Wout, x, T, labels, lr, every, spikes, dW, dWout, loss, W_final,
+                            Wout_final);
 }
 
 // The same with the learning signal through W_out (symmetric feedback).

@@ -51,13 +51,22 @@ class _Readout(torch.autograd.Function):
         return g @ fb, g.T @ z, None
 
 
-def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedback=None):
+def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedback=None,
+               schedule=None):
     """Returns (dW list, dWout list, loss) as float64 numpy arrays.
 
     ``stop=False`` keeps every path (true surrogate gradient); it is only used
     to show the gradient stops matter.  ``feedback``: per layer a matrix of
     W_out's shape that carries the readout's gradient back to the spikes in
-    place of W_out (random-feedback learning signal).
+    place of W_out (random-feedback learning signal).  ``schedule``: a list
+    of (t_start, W list, Wout list) in increasing t_start; from step t_start
+    on, the network uses those values in place of W, Wout.  The gradient is
+    still taken with respect to W and W_out: each use adds its derivative,
+    which is what a forward recursion accumulates while the weights change.
+    With a schedule the learning signal is e-prop's online one: the error at
+    step t reaches the spikes of steps s <= t through the readout weights in
+    use at step t (kappa^(t-s) W_out(t)^T delta_t), not those in use at s;
+    the readout value and its gradient stay exact.
     """
     T = x.shape[0] if T is None else T
     L, B, N = shape.n_layers, shape.batch, shape.n_rec
@@ -75,13 +84,25 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedbac
     a = [torch.zeros(B, N, dtype=F64) for _ in range(L)]
     zp = [torch.zeros(B, N, dtype=F64) for _ in range(L)]
     y = [torch.zeros(B, shape.n_out, dtype=F64) for _ in range(L)]
+    zh = [torch.zeros(B, N, dtype=F64) for _ in range(L)]   # kappa-filtered spikes (schedule)
     loss = torch.zeros((), dtype=F64)
+    sched = [(t0, [torch.tensor(np.asarray(w, dtype=np.float64)) for w in Wv],
+              [torch.tensor(np.asarray(w, dtype=np.float64)) for w in Wov])
+             for t0, Wv, Wov in (schedule or [])]
     for t in range(T):
         z_now = []
+        cur = [e for e in sched if e[0] <= t]
+        if cur:
+            # the values in use at this step; the derivative still flows to W, W_out
+            _, Wv, Wov = cur[-1]
+            Wuse = [w + (wv - w).detach() for w, wv in zip(Ws, Wv)]
+            Wouse = [w + (wv - w).detach() for w, wv in zip(Wos, Wov)]
+        else:
+            Wuse, Wouse = Ws, Wos
         for l in range(L):
             inp = xs[t] if l == 0 else sg(z_now[l - 1])
             p = torch.cat([inp, sg(zp[l])], dim=1) if shape.recurrent else inp
-            I = p @ Ws[l].T
+            I = p @ Wuse[l].T
             vl = shape.alpha * v[l]
             vl = vl + I
             vl = vl - reset * (zp[l] if keep_reset else sg(zp[l]))
@@ -90,9 +111,17 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedbac
             A = beta * al
             A = shape.thr + A
             z = _Spike.apply(vl - A, shape.gamma, shape.thr)
-            yz = z @ Wos[l].T if Fbs is None else _Readout.apply(z, Wos[l], Fbs[l])
-            y[l] = shape.kappa * y[l] + yz
-            loss = loss + torch.nn.functional.cross_entropy(y[l], lab, reduction="sum")
+            if schedule is None:
+                yz = z @ Wouse[l].T if Fbs is None else _Readout.apply(z, Wouse[l], Fbs[l])
+                y[l] = shape.kappa * y[l] + yz
+                logits = y[l]
+            else:
+                # value: the exact leaky readout (gradient to W_out only); the
+                # spikes' gradient: filtered spikes through today's W_out
+                y[l] = shape.kappa * y[l] + z.detach() @ Wouse[l].T
+                zh[l] = shape.kappa * zh[l] + z
+                logits = y[l] + (zh[l] - zh[l].detach()) @ Wouse[l].detach().T
+            loss = loss + torch.nn.functional.cross_entropy(logits, lab, reduction="sum")
             v[l], a[l] = vl, al
             z_now.append(z)
         zp = z_now

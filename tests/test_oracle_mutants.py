@@ -48,6 +48,10 @@ MUTANTS = [
      "ev = c.alpha * V + c.reset * bj * pj * ea;", 1),
     ("reset_through_coupling_dropped", "ev = (c.alpha - c.reset * pj) * V + c.reset * bj * pj * ea;",
      "ev = (c.alpha - c.reset * pj) * V;", 1),
+    ("online_update_from_current_weights", "Wcur[l][ji] = on_grid((double)W0[l][ji] - lr * dW[l][ji]);",
+     "Wcur[l][ji] = on_grid((double)Wcur[l][ji] - lr * dW[l][ji]);", 1),
+    ("online_readout_not_updated", "Woutcur[l][kj] = on_grid((double)Wout0[l][kj] - lr * dWout[l][kj]);",
+     "Woutcur[l][kj] = Wout0[l][kj];", 1),
 ]
 
 

@@ -107,6 +107,64 @@ def test_feedback_is_linear_and_leaves_the_forward_alone():
     assert np.array_equal(sym.dW[0], same.dW[0])
 
 
+# ---------------------------------------------------------------- online weight application
+def online_schedule(shape, wl, lr, every, T):
+    """The weights in use after each block of ``every`` steps, built from
+    reverse-mode gradients of the prefix: W0 - lr * G on the 2**-14 grid
+    (ties to even).  Also returns the smallest distance, in grid units, of a
+    value from a rounding tie (the decisions are robust when it is large)."""
+    sched, margin = [], np.inf
+    for t1 in range(every, T, every):
+        dW, dWout, _ = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels, T=t1, schedule=sched)
+        Wn, Won = [], []
+        for W0, G, out in ((wl.W, dW, Wn), (wl.Wout, dWout, Won)):
+            for l in range(shape.n_layers):
+                v = (np.asarray(W0[l], np.float64) - lr * G[l]) * 16384.0
+                margin = min(margin, float(np.min(np.abs(np.abs(v - np.floor(v)) - 0.5))))
+                out.append((np.rint(v) / 16384.0).astype(np.float32))
+        sched.append((t1, Wn, Won))
+    return sched, margin
+
+
+ONLINE_CASES = ["rlif_ragged", "ralif_ragged", "ff_alif", "ralif2_two_layers"]
+
+
+@pytest.mark.parametrize("name", ONLINE_CASES)
+def test_online_weights_equal_backprop_with_the_same_schedule(name):
+    # Weights applied every 10 steps: the oracle's forward recursion with
+    # changing weights must give the gradient that reverse-mode autograd
+    # gives for the same weight schedule, and end on the same weights.
+    shape, seed, scale = AUTOGRAD_CASES[name]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    lr, every = 2.0 ** -8, 10
+    sched, margin = online_schedule(shape, wl, lr, every, shape.T)
+    assert margin > 1e-6
+    r = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, lr, every, fwd_fp32=False)
+    dW, dWout, loss = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels, schedule=sched)
+    assert abs(r.loss - loss) <= 1e-12 * abs(loss)
+    for l in range(shape.n_layers):
+        assert rel_l2(r.dW[l], dW[l]) <= 1e-11, (l, rel_l2(r.dW[l], dW[l]))
+        assert rel_l2(r.dWout[l], dWout[l]) <= 1e-11
+        assert np.array_equal(r.W[l], sched[-1][1][l]) and np.array_equal(r.Wout[l], sched[-1][2][l])
+    # the weights moved, and the run differs from one without updates
+    assert any(not np.array_equal(r.W[l], wl.W[l]) for l in range(shape.n_layers))
+    plain = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    assert rel_l2(r.dW[0], plain.dW[0]) > 1e-3
+
+
+def test_online_without_a_change_is_the_plain_run():
+    # lr = 0, or blocks as long as the sequence: the plain run (up to the
+    # order of the gradient sums over batch elements and steps)
+    shape, seed, scale = AUTOGRAD_CASES["ralif_ragged"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    plain = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels)
+    for lr, every in ((0.0, 7), (2.0 ** -8, shape.T), (2.0 ** -8, 10 * shape.T)):
+        r = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, lr, every)
+        assert np.array_equal(r.spikes, plain.spikes)
+        assert rel_l2(r.dW[0], plain.dW[0]) <= 1e-13 and abs(r.loss - plain.loss) <= 1e-12 * plain.loss
+        assert np.array_equal(r.W[0], wl.W[0])
+
+
 RESET_CASES = ["ff_lif_b4_n32_t50", "rlif_ragged", "ralif_ragged", "ralif_all_adaptive", "ff_alif",
                "ralif2_two_layers"]
 
