@@ -178,6 +178,31 @@ int eprop_status(eprop_ctx* ctx);
  */
 int eprop_set_feedback(eprop_ctx* ctx, const float* const* d_feedback);
 
+/*
+ * Online weight application: the gradient is available at every step
+ * (Sec. III-A), so the weights may change during the sequence.  Before the
+ * step that follows every `every` steps counted from the last reset, the drive
+ * and readout weights in use become W0 - lr * G rounded to the nearest
+ * multiple of 2^-14 (ties to even; the grid keeps the drive's sums exact),
+ * where W0 are the weights read at init or reset and G the gradient
+ * accumulated since that reset (what eprop_get_grads would return); the
+ * recurrent diagonal keeps W0.  The learning signal then uses the readout
+ * weights in use at its step.  No update follows the last step run, and the
+ * caller's weight buffers are not written (eprop_get_weights reads the ones in
+ * use).  every = 0 (the default) or lr = 0 turns it off; it applies from the
+ * next step on and is kept over resets.  The blocks of eprop_run_sequence
+ * end at the update steps, and the forward of the block after an update waits
+ * for it.  Returns 0, EPROP_EINVAL (every < 0 or lr not finite), EPROP_ESTATE.
+ */
+int eprop_set_online(eprop_ctx* ctx, float lr, int32_t every);
+
+/*
+ * The weights in use (after any online updates), queued on the context's
+ * stream: d_weights as eprop_init's (device pointers, layouts of W and W_out),
+ * written, not read.  Returns 0, EPROP_EINVAL on a NULL pointer, EPROP_ESTATE.
+ */
+int eprop_get_weights(eprop_ctx* ctx, float* const* d_weights);
+
 /* Frees the host-side context; the workspace and weights stay the caller's. */
 void eprop_destroy(eprop_ctx* ctx);
 

@@ -249,6 +249,12 @@ struct eprop_ctx {
   // eligibility kernel (learning signal, readout gradient, coefficients)
   hipStream_t fwd_stream = nullptr, coef_stream = nullptr;
   hipEvent_t ev_entry = nullptr, ev_fwd[kSlots] = {}, ev_coef[kSlots] = {}, ev_done[kSlots] = {};
+  // online weight application (eprop_set_online): every `online_every` steps
+  // since the reset, before the next step runs
+  float online_lr = 0.0f;
+  int online_every = 0;
+  long long online_applied = -1;   // step count of the last update
+  hipEvent_t ev_update = nullptr;
   bool alive = false;
   std::string err;
   // profiling of the eligibility kernel
@@ -320,6 +326,32 @@ int clear_state(eprop_ctx* ctx) {
     rc = check(ctx, e, "reset");
   }
   ctx->t = 0;
+  ctx->online_applied = -1;
+  return rc;
+}
+
+// The weights in use become W0 - lr * G on the 2^-14 grid (G: the gradient
+// so far), on the caller's stream after the last eligibility pass; the next
+// forward waits for it.
+int apply_online(eprop_ctx* ctx) {
+  const Plan& P = ctx->plan;
+  const eprop_config& c = P.cfg;
+  hipStream_t s = ctx->stream;
+  int rc = check(ctx, eprop::launch_set_flag(P.w16ok, 1, s), "online weight update");
+  for (int l = 0; l < c.n_layers && !rc; ++l) {
+    const Layer& L = P.layers[l];
+    eprop::OnlineArgs a;
+    a.W0 = L.W_src; a.Wout0 = L.Wout_src;
+    a.acc = L.acc; a.ldj = L.ldj; a.n_split = L.n_split; a.acc_stride = L.acc_stride;
+    a.accout = L.accout; a.ld_acc = L.ldj;
+    a.Wt = L.Wt; a.ldw = L.ldw; a.W16 = L.W16; a.qn = eprop::forward_qn(c.n_rec); a.ok = P.w16ok;
+    a.WoutT = L.WoutT; a.ldk = P.ldk;
+    a.n_rec = c.n_rec; a.n_pre = L.n_pre; a.n_inl = L.n_inl; a.recurrent = c.recurrent; a.K = c.n_out;
+    a.lr = (double)ctx->online_lr;
+    rc = check(ctx, eprop::launch_online_update(a, s), "online weight update");
+  }
+  if (!rc) rc = check(ctx, hipEventRecord(ctx->ev_update, s), "event record");
+  if (!rc) rc = check(ctx, hipStreamWaitEvent(ctx->fwd_stream, ctx->ev_update, 0), "stream wait");
   return rc;
 }
 
@@ -334,6 +366,11 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   const int first = ctx->t == 0;
   const int sl = ctx->slot;
   int rc;
+  if (ctx->online_every > 0 && ctx->t > 0 && ctx->t % ctx->online_every == 0 &&
+      ctx->online_applied != ctx->t) {
+    if ((rc = apply_online(ctx))) return rc;
+    ctx->online_applied = ctx->t;
+  }
   // The forward may overwrite this slot once the passes that read it
   // kSlots blocks ago are done.
   if (ctx->slot_used[sl] &&
@@ -498,6 +535,7 @@ int eprop_init(const eprop_config* cfg, void* d_workspace, size_t ws_bytes,
   if (!rc) rc = check(ctx, hipStreamCreateWithFlags(&ctx->coef_stream, hipStreamNonBlocking),
                       "stream create");
   if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_entry, hipEventDisableTiming), "event create");
+  if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_update, hipEventDisableTiming), "event create");
   for (int k = 0; k < kSlots && !rc; ++k) {
     rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_fwd[k], hipEventDisableTiming), "event create");
     if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_coef[k], hipEventDisableTiming),
@@ -538,7 +576,9 @@ int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int3
   int rc0 = join_forward_stream(ctx);
   if (rc0) return rc0;
   for (int32_t t = 0; t < T;) {
-    const int steps = std::min<int32_t>(ctx->plan.Kmax, T - t);
+    int steps = std::min<int32_t>(ctx->plan.Kmax, T - t);
+    if (ctx->online_every > 0)   // blocks end where the weights change
+      steps = (int)std::min<long long>(steps, ctx->online_every - ctx->t % ctx->online_every);
     int rc = do_block(ctx, d_x + t * x_step, steps, d_labels,
                       d_spikes ? d_spikes + t * s_step : nullptr);
     if (rc) return rc;
@@ -588,6 +628,31 @@ int eprop_set_feedback(eprop_ctx* ctx, const float* const* d_feedback) {
   return pack_weights(ctx);
 }
 
+int eprop_set_online(eprop_ctx* ctx, float lr, int32_t every) {
+  if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
+  if (every < 0 || !std::isfinite(lr)) return fail(ctx, EPROP_EINVAL, "every must be >= 0 and lr finite");
+  ctx->online_lr = lr;
+  ctx->online_every = every;
+  return EPROP_OK;
+}
+
+int eprop_get_weights(eprop_ctx* ctx, float* const* d_weights) {
+  if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
+  if (!d_weights) return fail(ctx, EPROP_EINVAL, "weights is NULL");
+  const eprop_config& c = ctx->plan.cfg;
+  for (int k = 0; k < 2 * c.n_layers; ++k)
+    if (!d_weights[k]) return fail(ctx, EPROP_EINVAL, "a weight pointer is NULL");
+  for (int l = 0; l < c.n_layers; ++l) {
+    const Layer& L = ctx->plan.layers[l];
+    int rc = check(ctx, eprop::launch_unpack_weights(L.Wt, L.ldw, L.WoutT, ctx->plan.ldk, c.n_rec,
+                                                     L.n_pre, c.n_out, d_weights[2 * l],
+                                                     d_weights[2 * l + 1], ctx->stream),
+                   "weight read-out");
+    if (rc) return rc;
+  }
+  return EPROP_OK;
+}
+
 int eprop_status(eprop_ctx* ctx) {
   if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
   int flag = 0;
@@ -607,6 +672,7 @@ void eprop_destroy(eprop_ctx* ctx) {
     (void)hipStreamDestroy(st);
   }
   if (ctx->ev_entry) (void)hipEventDestroy(ctx->ev_entry);
+  if (ctx->ev_update) (void)hipEventDestroy(ctx->ev_update);
   for (int k = 0; k < kSlots; ++k)
     for (hipEvent_t e : {ctx->ev_fwd[k], ctx->ev_coef[k], ctx->ev_done[k]})
       if (e) (void)hipEventDestroy(e);

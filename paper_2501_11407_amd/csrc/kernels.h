@@ -169,6 +169,27 @@ hipError_t launch_pack(const float* src, int rows, int cols, float* dst, int ldd
 hipError_t launch_pack16(const float* W, int n_rec, int n_pre, int16_t* W16, int qn, int* ok,
                          hipStream_t s);
 hipError_t launch_set_flag(int* flag, int value, hipStream_t s);
+
+// Online weight application for one layer: the weights in use become
+// W0 - lr * G rounded to the nearest multiple of 2^-14 (ties to even), G the
+// gradient accumulated so far (acc summed over its splits in split order,
+// accout); the recurrent diagonal keeps W0.  Writes Wt (transposed fp32), W16
+// (as launch_pack16, clearing *ok where a weight has no exact int16 form) and
+// WoutT [n_rec][ldk].
+struct OnlineArgs {
+  const float* W0; const float* Wout0;      // the caller's W [n_rec][n_pre], W_out [K][n_rec]
+  const double* acc; int ldj, n_split; size_t acc_stride;
+  const double* accout; int ld_acc;
+  float* Wt; int ldw; int16_t* W16; int qn; int* ok;
+  float* WoutT; int ldk;
+  int n_rec, n_pre, n_inl, recurrent, K;
+  double lr;
+};
+hipError_t launch_online_update(const OnlineArgs& a, hipStream_t s);
+// The weights in use back in the caller's layouts: W [n_rec][n_pre] from Wt,
+// W_out [K][n_rec] from WoutT.
+hipError_t launch_unpack_weights(const float* Wt, int ldw, const float* WoutT, int ldk, int n_rec,
+                                 int n_pre, int K, float* W, float* Wout, hipStream_t s);
 // neurons per forward thread for n_rec neurons (a power of two, at most 16)
 int forward_qn(int n_rec);
 

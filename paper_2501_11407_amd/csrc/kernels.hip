@@ -1399,6 +1399,53 @@ __global__ __launch_bounds__(256) void pack16_kernel(const float* W, int n_rec, 
       exact ? (int16_t)k : (int16_t)0;
 }
 
+// Weights on the 2^-14 grid: rint(x 2^14) 2^-14 in fp64 (ties to even).
+__device__ __forceinline__ float on_grid(double x) { return (float)(rint(x * 16384.0) / 16384.0); }
+
+// One thread per (i, j), j fastest (coalesced over the accumulators and Wt).
+__global__ __launch_bounds__(256) void online_w_kernel(OnlineArgs a, int lim) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)a.n_rec * a.n_pre) return;
+  const int i = (int)(idx / a.n_rec), j = (int)(idx % a.n_rec);
+  const float w0 = a.W0[(size_t)j * a.n_pre + i];
+  float wn = w0;
+  if (!(a.recurrent && i == a.n_inl + j)) {
+    double g = 0.0;
+    for (int sp = 0; sp < a.n_split; ++sp) g += a.acc[sp * a.acc_stride + (size_t)i * a.ldj + j];
+    wn = on_grid((double)w0 - a.lr * g);
+  }
+  a.Wt[(size_t)i * a.ldw + j] = wn;
+  const float k = wn * 16384.0f;
+  const bool exact = k == rintf(k) && fabsf(k) <= (float)lim;
+  if (!exact) *a.ok = 0;   // every thread that finds one writes the same value
+  a.W16[(size_t)i * (a.qn * kFwdThreads) + (size_t)(j % kFwdThreads) * a.qn + j / kFwdThreads] =
+      exact ? (int16_t)k : (int16_t)0;
+}
+
+// One thread per (j, k): WoutT[j][k].
+__global__ __launch_bounds__(256) void online_wout_kernel(OnlineArgs a) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)a.n_rec * a.K) return;
+  const int j = (int)(idx / a.K), k = (int)(idx % a.K);
+  const double g = a.accout[(size_t)k * a.ld_acc + j];
+  a.WoutT[(size_t)j * a.ldk + k] = on_grid((double)a.Wout0[(size_t)k * a.n_rec + j] - a.lr * g);
+}
+
+__global__ __launch_bounds__(256) void unpack_kernel(const float* Wt, int ldw, const float* WoutT,
+                                                     int ldk, int n_rec, int n_pre, int K, float* W,
+                                                     float* Wout) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long nw = (long long)n_rec * n_pre;
+  if (idx < nw) {
+    const int j = (int)(idx / n_pre), i = (int)(idx % n_pre);
+    W[idx] = Wt[(size_t)i * ldw + j];
+  } else if (idx < nw + (long long)K * n_rec) {
+    const long long r = idx - nw;
+    const int k = (int)(r / n_rec), j = (int)(r % n_rec);
+    Wout[r] = WoutT[(size_t)j * ldk + k];
+  }
+}
+
 __global__ void set_flag_kernel(int* flag, int value) {
   if (threadIdx.x == 0 && blockIdx.x == 0) *flag = value;
 }
@@ -1545,6 +1592,22 @@ hipError_t launch_pack16(const float* W, int n_rec, int n_pre, int16_t* W16, int
   const long long n = (long long)n_rec * n_pre;
   const int lim = (int)std::min<long long>(32767, ((1LL << 24) - 1) / std::max(1, n_pre));
   pack16_kernel<<<cdiv(n, 256), 256, 0, s>>>(W, n_rec, n_pre, W16, qn, lim, ok);
+  return hipGetLastError();
+}
+
+hipError_t launch_online_update(const OnlineArgs& a, hipStream_t s) {
+  const int lim = (int)std::min<long long>(32767, ((1LL << 24) - 1) / std::max(1, a.n_pre));
+  online_w_kernel<<<cdiv((long long)a.n_rec * a.n_pre, 256), 256, 0, s>>>(a, lim);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  online_wout_kernel<<<cdiv((long long)a.n_rec * a.K, 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpack_weights(const float* Wt, int ldw, const float* WoutT, int ldk, int n_rec,
+                                 int n_pre, int K, float* W, float* Wout, hipStream_t s) {
+  const long long n = (long long)n_rec * n_pre + (long long)K * n_rec;
+  unpack_kernel<<<cdiv(n, 256), 256, 0, s>>>(Wt, ldw, WoutT, ldk, n_rec, n_pre, K, W, Wout);
   return hipGetLastError();
 }
 

@@ -22,7 +22,8 @@ EPROP_OK, EPROP_EINVAL, EPROP_ENOSPACE, EPROP_EDEVICE, EPROP_ESTATE = 0, -1, -2,
 # Every function the header declares, in declaration order.
 SYMBOLS = (
     "eprop_workspace_bytes", "eprop_init", "eprop_step", "eprop_run_sequence", "eprop_get_grads",
-    "eprop_reset", "eprop_status", "eprop_set_feedback", "eprop_destroy", "eprop_last_error",
+    "eprop_reset", "eprop_status", "eprop_set_feedback", "eprop_set_online", "eprop_get_weights",
+    "eprop_destroy", "eprop_last_error",
     "eprop_profile_begin", "eprop_profile_end", "eprop_debug_buffer",
 )
 
@@ -66,6 +67,8 @@ def load_library(path: str = LIB_PATH):
         "eprop_get_grads": (ctypes.c_int, [vp, vp, vp]),
         "eprop_reset": (ctypes.c_int, [vp]),
         "eprop_set_feedback": (ctypes.c_int, [vp, vp]),
+        "eprop_set_online": (ctypes.c_int, [vp, ctypes.c_float, i32]),
+        "eprop_get_weights": (ctypes.c_int, [vp, vp]),
         "eprop_status": (ctypes.c_int, [vp]),
         "eprop_destroy": (None, [vp]),
         "eprop_last_error": (ctypes.c_char_p, [vp]),
@@ -148,6 +151,16 @@ def eprop_set_feedback(ctx, feedback: Optional[Sequence[Optional[torch.Tensor]]]
         arr = (ctypes.c_void_p * len(feedback))(*[_ptr(f) for f in feedback])
     _check(load_library().eprop_set_feedback(ctx, ctypes.cast(arr, ctypes.c_void_p)
                                              if arr is not None else None), ctx)
+
+
+def eprop_set_online(ctx, lr: float, every: int):
+    _check(load_library().eprop_set_online(ctx, float(lr), int(every)), ctx)
+
+
+def eprop_get_weights(ctx, weights: Sequence[torch.Tensor]):
+    """weights: per layer W then W_out, device fp32 tensors (written)."""
+    arr = (ctypes.c_void_p * len(weights))(*[_ptr(w) for w in weights])
+    _check(load_library().eprop_get_weights(ctx, ctypes.cast(arr, ctypes.c_void_p)), ctx)
 
 
 def eprop_status(ctx) -> int:
@@ -268,6 +281,21 @@ class EpropContext:
                     raise ValueError(f"feedback[{l}] must be {(s.n_out, s.n_rec)}, got {tuple(t.shape)}")
                 self.feedback.append(t)
         eprop_set_feedback(self.ctx, self.feedback)
+
+    def set_online(self, lr: float, every: int):
+        """Online weight application: every ``every`` steps since the reset
+        the weights in use become W0 - lr * G on the 2**-14 grid (0: off)."""
+        eprop_set_online(self.ctx, lr, every)
+
+    def get_weights(self):
+        """The weights in use: (W list, W_out list) as new device tensors."""
+        s = self.shape
+        W = [torch.empty(s.n_rec, s.n_pre(l), dtype=torch.float32, device=self.device)
+             for l in range(s.n_layers)]
+        Wo = [torch.empty(s.n_out, s.n_rec, dtype=torch.float32, device=self.device)
+              for _ in range(s.n_layers)]
+        eprop_get_weights(self.ctx, [t for l in range(s.n_layers) for t in (W[l], Wo[l])])
+        return W, Wo
 
     def status(self) -> int:
         return eprop_status(self.ctx)

@@ -155,6 +155,78 @@ def test_drive_path_follows_the_weights_over_resets():
     assert np.array_equal(a["spikes"], b["spikes"]) and np.array_equal(a["dW"][0], b["dW"][0])
 
 
+# ---------------------------------------------------------------- online weight application
+# Every `every` steps the weights in use become W0 - lr * G on the 2**-14 grid.
+# Rounding turns the gradient into weights, so the GPU (fp32 traces) and the
+# oracle (fp64) agree on every weight only if no value lies near a rounding
+# tie: the cases are seeds whose oracle values keep a margin well above the
+# GPU's gradient error (about 1e-5 grid units at lr = 2**-12); the test
+# asserts that margin from the oracle alone.
+ONLINE = {
+    "rlif": (small(**DISTINCT), 35, 10),
+    "ralif": (small(n_adaptive=13, T=60, **DISTINCT), 38, 10),
+    "ff_alif": (small(recurrent=0, n_adaptive=11, **DISTINCT), 30, 10),
+    "ralif2": (small(batch=2, n_in=21, n_rec=19, n_out=4, T=60, n_layers=2, n_adaptive=9,
+                     **DISTINCT), 31, 10),
+    "blocks_300": (small(batch=2, n_in=15, n_rec=20, n_out=3, n_adaptive=10, T=300, **DISTINCT), 30,
+                   100),
+}
+ONLINE_LR = 2.0 ** -12
+
+
+def _online_margin(shape, wl, lr, every):
+    m = np.inf
+    for t1 in range(every, wl.x.shape[0], every):
+        r = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, lr, every, T=t1)
+        for l in range(shape.n_layers):
+            for W0, G in ((wl.W[l], r.dW[l]), (wl.Wout[l], r.dWout[l])):
+                v = (W0.astype(np.float64) - lr * G) * 16384.0
+                m = min(m, float(np.min(np.abs(np.abs(v - np.floor(v)) - 0.5))))
+    return m
+
+
+@pytest.mark.parametrize("name", list(ONLINE))
+def test_online_weights_match_oracle(name):
+    shape, seed, every = ONLINE[name]
+    banner(f"online weights {name} {shape} every {every}")
+    wl = synth.make_workload(shape, seed, input_scale=4.0)
+    assert _online_margin(shape, wl, ONLINE_LR, every) > 1e-4
+    ref = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, ONLINE_LR, every)
+    for chunks in (None, [7, shape.T - 7]):
+        ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+        ctx.set_online(ONLINE_LR, every)
+        gpu = gpu_run(wl, ctx=ctx, chunks=chunks)
+        Wg, Wog = ctx.get_weights()
+        torch.cuda.synchronize()
+        ctx.close()
+        mism = first_spike_mismatch(gpu["spikes"], ref.spikes)
+        assert mism is None, f"spike trains differ: {mism}"
+        for l in range(shape.n_layers):
+            assert np.array_equal(Wg[l].cpu().numpy(), ref.W[l]), f"layer {l} weights differ"
+            assert np.array_equal(Wog[l].cpu().numpy(), ref.Wout[l])
+            assert rel_l2(gpu["dW"][l], ref.dW[l]) <= 1e-4
+            assert rel_l2(gpu["dWout"][l], ref.dWout[l]) <= 1e-4
+        assert abs(gpu["loss"] - ref.loss) <= 1e-4 * abs(ref.loss)
+        assert any(not np.array_equal(ref.W[l], wl.W[l]) for l in range(shape.n_layers))
+
+
+def test_online_off_and_reset_give_the_plain_run():
+    shape, seed, every = ONLINE["rlif"]
+    wl = synth.make_workload(shape, seed, input_scale=4.0)
+    plain = gpu_run(wl)
+    ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+    ctx.set_online(ONLINE_LR, every)
+    gpu_run(wl, ctx=ctx)
+    ctx.set_online(0.0, 0)
+    ctx.reset()                              # back to W0, updates off
+    b = gpu_run(wl, ctx=ctx)
+    Wg, _ = ctx.get_weights()
+    torch.cuda.synchronize()
+    ctx.close()
+    assert np.array_equal(b["spikes"], plain["spikes"]) and np.array_equal(b["dW"][0], plain["dW"][0])
+    assert np.array_equal(Wg[0].cpu().numpy(), wl.W[0])
+
+
 # ---------------------------------------------------------------- random feedback
 @pytest.mark.parametrize("name", ["rlif_ragged", "ralif_ragged_na13", "ralif2_two_layers",
                                   "blocks_256_50"])
