@@ -161,6 +161,9 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=1024)
     ap.add_argument("--reset-grad", type=int, default=0, choices=(0, 1),
                     help="1: the same workload with the reset path kept in the gradient")
+    ap.add_argument("--online-every", type=int, default=0, metavar="K",
+                    help="online weight application every K steps (learning rate --online-lr)")
+    ap.add_argument("--online-lr", type=float, default=2.0 ** -12)
     ap.add_argument("--workload", default=WORKLOAD,
                     help="another named synthetic workload (the headline is the default)")
     args = ap.parse_args()
@@ -184,9 +187,12 @@ def main():
     if args.reset_grad:
         wl.shape = wl.shape.replace(reset_grad=1)
     shape = wl.shape
-    workload = args.workload + ("_reset_grad" if args.reset_grad else "")
+    workload = args.workload + ("_reset_grad" if args.reset_grad else "") + \
+        (f"_online{args.online_every}" if args.online_every else "")
     dev = torch.device("cuda:0")
     ctx = eprop.EpropContext(shape, wl.W, wl.Wout, device="cuda:0")
+    if args.online_every:
+        ctx.set_online(args.online_lr, args.online_every)
     x = torch.from_numpy(wl.x).to(dev)
     labels = torch.from_numpy(wl.labels).to(dev)
 
@@ -226,7 +232,8 @@ def main():
     tflops = alg_flops / sec / 1e12
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": None if (args.reset_grad or args.workload != WORKLOAD) else stored_traffic(shape),
+                "traffic": (None if (args.reset_grad or args.online_every or args.workload != WORKLOAD)
+                            else stored_traffic(shape)),
                 "kernel": "trace_kernel", "avg_launch_us": round(trace_ms * 1e3 / n_timed, 2),
                 "steps_per_launch": round(timed_steps / n_timed, 2),
                 "alg_hbm_bytes_per_launch": round(alg_bytes / n_timed),
