@@ -61,11 +61,11 @@ struct Layer {
   float *v, *a, *ztil, *zbar, *y;        // neuron, filter and readout state
   uint8_t* z;                            // spikes of the last step
   double* lossacc;                       // [B]
-  // per-block vectors, two slots: the forward of block k+1 fills one while
-  // the eligibility pass of block k reads the other
+  // per-block vectors in kSlots slots: the forward of block k+1 fills one
+  // while the eligibility pass of block k reads another
   float *psiK[kSlots], *LK[kSlots], *deltaK[kSlots], *ztK[kSlots];
-  // the filtered presynaptic values as scaled fp16 pairs, and the block
-  // coefficients of the eligibility recursion (same two slots)
+  // the binary presynaptic values (one byte per step), and the block
+  // coefficients of the eligibility recursion as scaled fp16 pairs
   uint8_t* p8[kSlots];
   uint32_t *coefU[kSlots], *coefV[kSlots], *coefH[kSlots], *coefW[kSlots];
   float* coefS[kSlots];
@@ -193,7 +193,8 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   for (Layer& L : plan->layers) {
     const size_t ldc = plan->ldc;
     for (int sl = 0; sl < kSlots; ++sl) {
-      // a scaled fp16 pair per value: 4 bytes, as fp32
+      // p: one byte per row and step; coefficients: a scaled fp16 pair per
+      // value (4 bytes)
       L.p8[sl] = (uint8_t*)take((size_t)B * L.n_pre_pad * KM);
       L.coefU[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
       L.coefV[sl] = (uint32_t*)take(c.n_adaptive > 0 ? sizeof(uint32_t) * B * ldc * KM : 0);

@@ -381,9 +381,8 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
 
   // Global stores of the step go last: a load waits for every store issued
   // before it, so stores ahead of the drive and readout loads would lengthen
-  // the step.  Per-step vectors: psi, ztilde, the spike words, and the
-  // binary presynaptic values as pair words ([b][t/4][i][4] words, step
-  // t % 4: a wave's group store covers 64 consecutive 16-byte records).
+  // the step.  Per-step vectors: psi, ztilde, the spike words, and (every
+  // zgroup steps) the binary presynaptic bytes ([b][t/16][i][16]).
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
     const int j = q * kFwdThreads + tid;
