@@ -991,11 +991,11 @@ __device__ __forceinline__ void dma4(const float* g, float* lds) {
 // true: the reset path kept (coef_rt_kernel): contractions U = C_E, H = C_g,
 // W = C_V and V = C_A; traces ebar, epsv and epsa.  Either way the
 // presynaptic operand is the binary p, exact in fp16, so each contraction
-// takes one MFMA pass.  The five operand slots of RT use a ring of three
-// chunks, which keeps two workgroups per compute unit.
+// takes one MFMA pass.  With the p bytes (1 KiB per chunk) even the four
+// coefficient operands of RT fit a ring of four chunks twice per compute unit.
 template <bool ALIF, int NCH, bool RT>
 struct TraceTile {
-  static constexpr int RING = RT ? 3 : kRing;                 // chunk slots
+  static constexpr int RING = kRing;                          // chunk slots
   static constexpr int PREF = RING - 1;                       // chunks copied ahead
   // a slot: the chunk's p bytes (64 rows x 16 B), then the coefficient
   // operands U, H, V (and W) of 64 rows x 64 B each
