@@ -170,6 +170,7 @@ ONLINE = {
                      **DISTINCT), 31, 10),
     "blocks_300": (small(batch=2, n_in=15, n_rec=20, n_out=3, n_adaptive=10, T=300, **DISTINCT), 30,
                    100),
+    "reset_path_kept": (small(n_adaptive=13, **DISTINCT).replace(reset_grad=1), 46, 10),
 }
 ONLINE_LR = 2.0 ** -12
 
