@@ -135,7 +135,7 @@ def cpu_baseline(wl, name: str, seconds_hint: float = 15.0):
     about seconds_hint on this host."""
     import oracle
     shape = wl.shape
-    per_step = shape.syn_per_step()
+    per_step = shape.syn_per_step() // shape.batch     # synapses of one batch element, all layers
     t0 = time.perf_counter()
     oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, b_lo=0, b_hi=1, want_spikes=False)
     probe = time.perf_counter() - t0
