@@ -291,6 +291,19 @@ def test_reset_through_matches_oracle(name):
     banner(f"{name}: {errs}")
 
 
+@pytest.mark.parametrize("name", ["ralif_ragged_na13", "ralif2_two_layers"])
+def test_reset_through_with_random_feedback(name):
+    # both variants at once: the learning signal through B, the reset path kept
+    shape, seed, scale = RAGGED[name]
+    shape = shape.replace(reset_grad=1)
+    banner(f"reset path kept with random feedback {name}")
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    fb = synth.make_feedback(shape, seed)
+    gpu = gpu_run(wl, feedback=fb)
+    errs, ref = check_against_oracle(wl, gpu, feedback=fb)
+    assert ref.spikes.any()
+
+
 def test_reset_through_full_workload_and_split_calls():
     wl = synth.named_workload("rlif_b32_n256_t250")
     wl.shape = wl.shape.replace(reset_grad=1)
