@@ -1043,9 +1043,10 @@ struct TraceTile {
     wj = w & 1;
   }
 
-  __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const float* base, int n_t, int b) const {
+  __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const float* base, int n_t, int b,
+                                                             uint32_t bytes = kSubTileBytes) const {
     const size_t t = ((size_t)b * (a.n_pre_pad / kTile) + it) * n_t + jt;
-    return make_rsrc((const char*)base + (t * 4 + w) * kSubTileBytes, kSubTileBytes);
+    return make_rsrc((const char*)base + (t * 4 + w) * kSubTileBytes, bytes);
   }
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t ebar_rsrc(int b) const { return tile_rsrc(a.ebar, a.n_jt, b); }
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t epsa_rsrc(int b) const { return tile_rsrc(a.epsa, a.n_jt_a, b); }
@@ -1106,19 +1107,23 @@ struct TraceTile {
     issue<1>(b, c, sl, par);
   }
 
-  // block-start traces of batch element b into E, A (and Vm)
+  // block-start traces of batch element b into E, A (and Vm).  In the first
+  // block after a reset they are zero: the loads then get an empty range, so
+  // they read zero without touching memory and still count as issued loads
+  // (the waits above count them).
   __device__ __forceinline__ void load_traces(int b, f32x4 (&E)[2][2], f32x4 (&A)[2][2],
                                               f32x4 (&Vm)[2][2]) const {
-    const auto eR = ebar_rsrc(b);
+    const uint32_t range = first ? 0u : kSubTileBytes;
+    const auto eR = tile_rsrc(a.ebar, a.n_jt, b, range);
 #pragma unroll
     for (int x = 0; x < 4; ++x) E[x >> 1][x & 1] = bload(eR, x * 1024u + lane * 16u);
     if constexpr (ALIF) {
-      const auto aR = epsa_rsrc(b);
+      const auto aR = tile_rsrc(a.epsa, a.n_jt_a, b, range);
 #pragma unroll
       for (int x = 0; x < 4; ++x) A[x >> 1][x & 1] = bload(aR, x * 1024u + lane * 16u);
     }
     if constexpr (RT) {
-      const auto vR = epsv_rsrc(b);
+      const auto vR = tile_rsrc(a.epsv, a.n_jt, b, range);
 #pragma unroll
       for (int x = 0; x < 4; ++x) Vm[x >> 1][x & 1] = bload(vR, x * 1024u + lane * 16u);
     }
