@@ -1231,6 +1231,7 @@ struct TraceTile {
     }
 #pragma unroll
     for (int c = 0; c < D; ++c) issue_all(split, c, c, 0);
+#pragma nounroll
     for (int k = 0; k < nk; ++k) {
       const int b = split + k * a.n_split;
       const bool next = k + 1 < nk;
