@@ -291,6 +291,24 @@ def test_reset_through_matches_oracle(name):
     banner(f"{name}: {errs}")
 
 
+# The eligibility kernel exists once per count of 16-step chunks in a block.
+# Fed in calls of these lengths, each call is one block of 5, 6, ..., 15
+# chunks (the last chunk partial), after the counts the other cases reach.
+EVERY_CHUNK_COUNT = [65, 81, 97, 113, 129, 145, 161, 177, 193, 209, 240]
+
+
+@pytest.mark.parametrize("reset_grad", [0, 1])
+def test_every_chunk_count(reset_grad):
+    shape = small(n_rec=70, n_adaptive=13, T=sum(EVERY_CHUNK_COUNT), reset_grad=reset_grad,
+                  **DISTINCT)
+    banner(f"every chunk count, reset_grad={reset_grad}, {shape}")
+    wl = synth.make_workload(shape, 21, input_scale=4.0)
+    gpu = gpu_run(wl, chunks=EVERY_CHUNK_COUNT)
+    errs, ref = check_against_oracle(wl, gpu)
+    assert ref.spikes.any()
+    banner(f"every chunk count: {errs}")
+
+
 @pytest.mark.parametrize("name", ["ralif_ragged_na13", "ralif2_two_layers"])
 def test_reset_through_with_random_feedback(name):
     # both variants at once: the learning signal through B, the reset path kept
