@@ -292,9 +292,10 @@ def test_reset_through_matches_oracle(name):
 
 
 # The eligibility kernel exists once per count of 16-step chunks in a block.
-# Fed in calls of these lengths, each call is one block of 5, 6, ..., 15
-# chunks (the last chunk partial), after the counts the other cases reach.
-EVERY_CHUNK_COUNT = [65, 81, 97, 113, 129, 145, 161, 177, 193, 209, 240]
+# Fed in calls of these lengths, each call is one block of 1, 2, ..., 15
+# chunks (the last chunk partial but for the first); 16 chunks come with
+# every longer sequence.
+EVERY_CHUNK_COUNT = [1, 17, 33, 49, 65, 81, 97, 113, 129, 145, 161, 177, 193, 209, 240]
 
 
 @pytest.mark.parametrize("reset_grad", [0, 1])
