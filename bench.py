@@ -166,6 +166,8 @@ def main():
     ap.add_argument("--online-lr", type=float, default=2.0 ** -12)
     ap.add_argument("--workload", default=WORKLOAD,
                     help="another named synthetic workload (the headline is the default)")
+    ap.add_argument("--batch", type=int, default=0, metavar="B",
+                    help="the named workload with another batch size (same seed and recipe)")
     args = ap.parse_args()
     if args.summarize_counters:
         print(json.dumps(summarize_counters(*args.summarize_counters, args.copy_mib)))
@@ -183,11 +185,16 @@ def main():
     if args.workload not in synth.WORKLOADS:
         print(f"unknown workload {args.workload}; one of {sorted(synth.WORKLOADS)}", file=sys.stderr)
         sys.exit(2)
-    wl = synth.named_workload(args.workload)
+    if args.batch:
+        wl = synth.make_workload(synth.WORKLOADS[args.workload].replace(batch=args.batch),
+                                 synth.WORKLOAD_SEED[args.workload])
+    else:
+        wl = synth.named_workload(args.workload)
     if args.reset_grad:
         wl.shape = wl.shape.replace(reset_grad=1)
     shape = wl.shape
-    workload = args.workload + ("_reset_grad" if args.reset_grad else "") + \
+    workload = args.workload + (f"_batch{args.batch}" if args.batch else "") + \
+        ("_reset_grad" if args.reset_grad else "") + \
         (f"_online{args.online_every}" if args.online_every else "")
     dev = torch.device("cuda:0")
     ctx = eprop.EpropContext(shape, wl.W, wl.Wout, device="cuda:0")
@@ -232,7 +239,7 @@ def main():
     tflops = alg_flops / sec / 1e12
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": (None if (args.reset_grad or args.online_every or args.workload != WORKLOAD)
+                "traffic": (None if (args.reset_grad or args.online_every or args.batch or args.workload != WORKLOAD)
                             else stored_traffic(shape)),
                 "kernel": "trace_kernel", "avg_launch_us": round(trace_ms * 1e3 / n_timed, 2),
                 "steps_per_launch": round(timed_steps / n_timed, 2),
