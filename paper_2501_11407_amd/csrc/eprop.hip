@@ -176,10 +176,17 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     }
     L.Cpart = (float*)take(sizeof(float) * plan->out_splits * K * N);
     // batch splits of the eligibility kernel: about 2048 workgroups (four
-    // rounds of two per compute unit), at most 8 and at most one per element
+    // rounds of two per compute unit; at most 8 splits for that), and enough
+    // splits that a workgroup walks at most about 26 batch elements (the row
+    // tiles that share a coefficient chunk drift apart in L2 over longer
+    // walks); at most 32, one per element, and 2 GiB of fp64 partials
     const size_t tiles = (npp / eprop::kTile) * ((N + eprop::kTile - 1) / eprop::kTile);
-    L.n_split = (int)std::max<size_t>(1, std::min<size_t>({8, B, (2048 + tiles - 1) / tiles}));
     L.acc_stride = npp * L.ldj;
+    const size_t by_tiles = std::min<size_t>(8, (2048 + tiles - 1) / tiles);
+    const size_t by_batch = (B + 25) / 26;
+    const size_t by_memory = std::max<size_t>(1, ((size_t)2 << 30) / (sizeof(double) * L.acc_stride));
+    L.n_split = (int)std::max<size_t>(
+        1, std::min<size_t>({std::max(by_tiles, by_batch), 32, B, by_memory}));
     L.acc = (double*)take(sizeof(double) * L.n_split * L.acc_stride);
     L.accout = (double*)take(sizeof(double) * K * L.ldj);
     // traces tile by tile: all j tiles, and the tiles holding adaptive neurons
