@@ -63,6 +63,26 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     return (2 * launches - first_launches) * trace + operands
 
 
+BYTE_MODEL = ("block: per launch (one block of up to 256 steps), every trace read once and "
+              "written once (4 B x B x N_pre x (N_post + N_adaptive) each way; the first launch "
+              "after a reset reads none), the fp64 gradient accumulator read and written once "
+              "(8 B x N_pre x N_post each way), the operands of the block's steps read once "
+              "(B x N_pre bytes of presynaptic spikes and 4 B x B x (2 N_post + N_adaptive) of "
+              "coefficient pairs per step, plus 7 scalars per (b, j) and the block-start filter "
+              "per launch)")
+
+
+def per_step_model_bytes(shape, layer: int) -> int:
+    """Bytes per timestep if every trace made a round trip at every step:
+    per synapse 8 B of ebar, 8 B of eps^a onto adaptive neurons, and per
+    (i, j) the fp64 accumulator read and written and W read (12 B over the
+    batch)."""
+    B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
+    npre = shape.n_pre(layer)
+    rt = getattr(shape, "reset_grad", 0)     # eps^v as a third trace
+    return 8 * B * npre * ((2 if rt else 1) * N + NA) + 12 * npre * N
+
+
 def trace_flops(shape, layer: int, steps: int) -> int:
     """Algorithmic matrix operations of the eligibility kernel: per
     covered timestep and synapse, one multiply-add (2 operations) in each of
@@ -129,25 +149,64 @@ def summarize_counters(fetch_dir: str, write_dir: str, copy_mib: int) -> dict:
     return out
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(wl, name: str, seconds_hint: float = 15.0):
     """The oracle (one thread, fp64 traces) over every synapse and all T
     steps of the first n_b batch elements, n_b chosen so that the run takes
-    about seconds_hint on this host."""
+    about seconds_hint on this host.  The process is pinned to one core for
+    the measurement (the first core it may run on) and unpinned afterwards."""
     import oracle
     shape = wl.shape
     per_step = shape.syn_per_step() // shape.batch     # synapses of one batch element, all layers
-    t0 = time.perf_counter()
-    oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, b_lo=0, b_hi=1, want_spikes=False)
-    probe = time.perf_counter() - t0
-    n_b = int(min(shape.batch, max(1, round(seconds_hint / max(probe, 1e-6)))))
-    t0 = time.perf_counter()
-    oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, b_lo=0, b_hi=n_b, want_spikes=False)
-    dt = time.perf_counter() - t0
+    allowed = sorted(os.sched_getaffinity(0))
+    core = allowed[0]
+    os.sched_setaffinity(0, {core})
+    try:
+        t0 = time.perf_counter()
+        oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, b_lo=0, b_hi=1, want_spikes=False)
+        probe = time.perf_counter() - t0
+        n_b = int(min(shape.batch, max(1, round(seconds_hint / max(probe, 1e-6)))))
+        t0 = time.perf_counter()
+        oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, b_lo=0, b_hi=n_b, want_spikes=False)
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, set(allowed))
     return {"value": n_b * per_step * shape.T / dt, "unit": "syn-steps/s", "cores": 1,
-            "kind": "oracle",
+            "kind": "oracle", "pinned_core": core, "cpu_model": cpu_model(),
+            "nproc": os.cpu_count(), "cores_allowed": len(allowed),
             "sample": f"batch elements 0..{n_b - 1} of {name} (of {shape.batch}), all "
                       f"{per_step} synapses, all {shape.T} timesteps: {dt:.1f} s on one thread "
-                      f"(fp64 traces)"}
+                      f"pinned to core {core} (fp64 traces)"}
+
+
+def copy_ceiling_gbs(torch, dev, mib: int = 1024, reps: int = 5) -> float:
+    """Measured HBM ceiling: a device-to-device copy of `mib` MiB (read once
+    and written once), bytes moved per second, best of `reps`, HIP events on
+    the current stream."""
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    best = float("inf")
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        e1.synchronize()
+        best = min(best, e0.elapsed_time(e1) * 1e-3)
+    del src, dst
+    return 2 * n / best / 1e9
 
 
 def main():
@@ -237,8 +296,17 @@ def main():
     # HBM; the matrix rate is reported beside it.
     achieved = alg_bytes / sec / 1e9
     tflops = alg_flops / sec / 1e12
+    copy_gbs = copy_ceiling_gbs(torch, dev)
+    # the same launches priced with the per-step byte model (every trace read
+    # and written at every timestep): what an unblocked kernel would move
+    per_step_bytes = sum(per_step_model_bytes(shape, l) for l in range(shape.n_layers)) * args.steps * shape.T
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "byte_model": BYTE_MODEL,
+                "copy_ceiling_gbs": round(copy_gbs, 1),
+                "frac_of_copy_ceiling": round(achieved / copy_gbs, 4),
+                "per_step_model_bytes_per_launch": round(per_step_bytes / n_timed),
+                "per_step_model_gbs": round(per_step_bytes / sec / 1e9, 1),
                 "traffic": (None if (args.reset_grad or args.online_every or args.batch or args.workload != WORKLOAD)
                             else stored_traffic(shape)),
                 "kernel": "trace_kernel", "avg_launch_us": round(trace_ms * 1e3 / n_timed, 2),
@@ -251,7 +319,12 @@ def main():
         "metric": "synapse-timestep e-prop updates/sec (B*N_pre*N_post*T/s) + % HBM peak",
         "value": value, "unit": "syn-steps/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": elapsed * 1e3 / args.steps,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32 (contraction operands f16 hi/lo pairs)",
+        "precision": "fp32 neuron state, traces and per-launch sums; fp64 gradient accumulators; "
+                     "the eligibility contractions take their coefficient operands as scaled "
+                     "fp16 hi/lo pairs (about 22 significant bits) against the exact binary "
+                     "presynaptic values, with fp32 accumulation",
         "data": "synthetic (seeded Bernoulli spike inputs, quantised Gaussian weights)",
         "config": {"workload": workload, "batch": shape.batch, "n_in": shape.n_in,
                    "n_rec": shape.n_rec, "n_adaptive": shape.n_adaptive, "n_out": shape.n_out,

@@ -102,7 +102,8 @@ size_t eprop_workspace_bytes(const eprop_config* cfg);
  *   The weights are read here and again by every eprop_reset, and must not be
  *   freed before eprop_destroy.
  *   hip_stream: a hipStream_t (NULL = the null stream).
- * State, traces and accumulators start at zero.  On success *out is the new
+ * State, traces and accumulators start at zero (the recursion of Eq. (5)
+ * starts from G_0 = 0, Sec. III-A).  On success *out is the new
  * context and 0 is returned; on failure *out is NULL and the reason is in
  * eprop_last_error(NULL).
  */
@@ -152,7 +153,9 @@ int eprop_get_grads(eprop_ctx* ctx, float* const* d_grads, double* d_loss);
 
 /*
  * Starts a new sequence: zeroes neuron state, filters, eligibility vectors,
- * gradient and loss accumulators, and re-reads the weights.
+ * gradient and loss accumulators (G_0 = 0 and h_0 = 0 at the start of the
+ * recursion of Eq. (1) and (5), Sec. III-A), and re-reads the weights and
+ * any feedback matrices.
  */
 int eprop_reset(eprop_ctx* ctx);
 
@@ -174,7 +177,10 @@ int eprop_status(eprop_ctx* ctx);
  *     [n_out][n_rec] row-major, the layout of W_out.
  * The matrices are read here (queued on the context's stream) and again by
  * every eprop_reset, must not be freed while set, and apply from the next
- * step on.  Returns 0, EPROP_ESTATE on an unusable context.
+ * step on.  Nothing else is read or rewritten: the weights in use (with
+ * online application, the updated ones) stay as they are.  With online
+ * application the matrices keep their values while W and W_out change.
+ * Returns 0, EPROP_ESTATE on an unusable context.
  */
 int eprop_set_feedback(eprop_ctx* ctx, const float* const* d_feedback);
 
@@ -189,7 +195,8 @@ int eprop_set_feedback(eprop_ctx* ctx, const float* const* d_feedback);
  * recurrent diagonal keeps W0.  The learning signal then uses the readout
  * weights in use at its step.  No update follows the last step run, and the
  * caller's weight buffers are not written (eprop_get_weights reads the ones in
- * use).  every = 0 (the default) or lr = 0 turns it off; it applies from the
+ * use).  Feedback matrices set by eprop_set_feedback are not weights: they
+ * keep their values.  every = 0 (the default) or lr = 0 turns it off; it applies from the
  * next step on and is kept over resets.  The blocks of eprop_run_sequence
  * end at the update steps, and the forward of the block after an update waits
  * for it.  Returns 0, EPROP_EINVAL (every < 0 or lr not finite), EPROP_ESTATE.

@@ -64,6 +64,12 @@ def load(path: str = LIB_PATH):
         ctypes.POINTER(OracleConfig), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_int32, ctypes.c_void_p, ctypes.c_double, ctypes.c_int32, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.oracle_eprop_run_online_fb.restype = ctypes.c_int
+    lib.oracle_eprop_run_online_fb.argtypes = [
+        ctypes.POINTER(OracleConfig), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_double, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p]
     lib.oracle_state_bytes.restype = ctypes.c_size_t
     lib.oracle_state_bytes.argtypes = [ctypes.POINTER(OracleConfig), ctypes.c_int32]
     if path == LIB_PATH:
@@ -178,10 +184,13 @@ class OnlineResult:
 
 def run_online(shape, W: Sequence[np.ndarray], Wout: Sequence[np.ndarray], x: np.ndarray,
                labels: np.ndarray, lr: float, every: int, *, T: Optional[int] = None,
-               fwd_fp32: bool = True, lib_path: str = LIB_PATH, **over) -> OnlineResult:
+               fwd_fp32: bool = True, lib_path: str = LIB_PATH,
+               feedback: Optional[Sequence[np.ndarray]] = None, **over) -> OnlineResult:
     """Every batch element, every synapse, with online weight application:
     every ``every`` steps the weights in use become W0 - lr * (gradient so
-    far) on the 2**-14 grid (oracle_eprop_run_online)."""
+    far) on the 2**-14 grid (oracle_eprop_run_online_fb).  ``feedback``: per
+    layer a fixed matrix B of the learning signal (None: the readout weights
+    in use); it does not change with the weights."""
     lib = load(lib_path)
     cfg = make_config(shape, fwd_fp32=fwd_fp32, **over)
     T = x.shape[0] if T is None else T
@@ -198,9 +207,16 @@ def run_online(shape, W: Sequence[np.ndarray], Wout: Sequence[np.ndarray], x: np
     loss = np.zeros(1, dtype=np.float64)
     spikes = np.zeros((T, L, B, (N + 31) // 32), dtype=np.uint32)
     arr = lambda xs: ctypes.cast((ctypes.c_void_p * len(xs))(*[_ptr(a) for a in xs]), ctypes.c_void_p)
-    rc = lib.oracle_eprop_run_online(ctypes.byref(cfg), arr(Wc), arr(Woc), _ptr(xc), T, _ptr(lab),
-                                     float(lr), int(every), _ptr(spikes), arr(dW), arr(dWout),
-                                     _ptr(loss), arr(Wf), arr(Wof))
+    fbp = None
+    if feedback is not None:
+        # a None entry: that layer's learning signal through its readout weights in use
+        Fbc = [None if f is None else np.ascontiguousarray(f, dtype=np.float32) for f in feedback]
+        assert len(Fbc) == L and all(f is None or f.shape == (K, N) for f in Fbc)
+        fbp = ctypes.cast((ctypes.c_void_p * L)(*[None if f is None else _ptr(f) for f in Fbc]),
+                          ctypes.c_void_p)
+    rc = lib.oracle_eprop_run_online_fb(ctypes.byref(cfg), arr(Wc), arr(Woc), fbp, _ptr(xc), T,
+                                        _ptr(lab), float(lr), int(every), _ptr(spikes), arr(dW),
+                                        arr(dWout), _ptr(loss), arr(Wf), arr(Wof))
     if rc != 0:
         raise ValueError(f"oracle_eprop_run_online returned {rc}")
     return OnlineResult(dW=dW, dWout=dWout, loss=float(loss[0]), spikes=spikes, W=Wf, Wout=Wof)

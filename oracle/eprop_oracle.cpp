@@ -401,11 +401,14 @@ int run(const oracle_config& c, const float* const* W, const float* const* Wout,
 // of 2^-14 (ties to even), G being the gradient accumulated so far over all
 // elements and steps; the recurrent diagonal keeps its W0 value.  All batch
 // elements advance together, block by block, so each keeps its own state.
+// Fixed feedback matrices (Fb, as in steps()) are not weights of the network:
+// they keep their values while W and W_out change.
 float on_grid(double v) { return (float)(std::nearbyint(v * 16384.0) / 16384.0); }
 
 template <typename R>
 int run_online(const oracle_config& c, const float* const* W0, const float* const* Wout0,
-               const uint8_t* x, int T, const int32_t* labels, double lr, int every,
+               const float* const* Fb, const uint8_t* x, int T, const int32_t* labels, double lr,
+               int every,
                uint32_t* spikes, double* const* dW, double* const* dWout, double* loss,
                float* const* Wcur, float* const* Woutcur) {
   const int NL = c.n_layers, B = c.batch, N = c.n_rec, K = c.n_out;
@@ -424,7 +427,7 @@ int run_online(const oracle_config& c, const float* const* W0, const float* cons
   for (int t0 = 0; t0 < T; t0 += every) {
     const int t1 = t0 + every < T ? t0 + every : T;
     for (int b = 0; b < B; ++b)
-      steps(c, Wcur, Woutcur, nullptr, x, b, labels[b], t0, t1, nullptr, -1, spikes, dW, dWout,
+      steps(c, Wcur, Woutcur, Fb, x, b, labels[b], t0, t1, nullptr, -1, spikes, dW, dWout,
             loss_b[b], nullptr, qs[b], active);
     if (t1 == T) break;
     for (int l = 0; l < NL; ++l) {
@@ -513,22 +516,33 @@ int oracle_eprop_run_fb(const oracle_config* c, const float* const* W, const flo
 // Every batch element over T steps with online weight application every
 // `every` steps (see run_online): dW, dWout (zeroed by the caller) receive the
 // gradient of the whole run, W_final[l], Wout_final[l] (layouts of W, Wout)
-// the weights in use at its end.  Spikes as oracle_eprop_run_fb.
-int oracle_eprop_run_online(const oracle_config* c, const float* const* W,
-                            const float* const* Wout, const uint8_t* x, int32_t T,
-                            const int32_t* labels, double lr, int32_t every, uint32_t* spikes,
-                            double* const* dW, double* const* dWout, double* loss,
-                            float* const* W_final, float* const* Wout_final) {
+// the weights in use at its end.  Spikes as oracle_eprop_run_fb; Fb as
+// oracle_eprop_run_fb (NULL: the learning signal through the readout weights
+// in use).
+int oracle_eprop_run_online_fb(const oracle_config* c, const float* const* W,
+                               const float* const* Wout, const float* const* Fb, const uint8_t* x,
+                               int32_t T, const int32_t* labels, double lr, int32_t every,
+                               uint32_t* spikes, double* const* dW, double* const* dWout,
+                               double* loss, float* const* W_final, float* const* Wout_final) {
   if (!valid(c) || !W || !Wout || !x || !labels || !dW || !dWout || !loss || !W_final ||
       !Wout_final || T < 0 || every < 1)
     return -1;
   for (int b = 0; b < c->batch; ++b)
     if (labels[b] < 0 || labels[b] >= c->n_out) return -1;
   if (c->fwd_fp32)
-    return run_online<float>(*c, W, Wout, x, T, labels, lr, every, spikes, dW, dWout, loss, W_final,
-                             Wout_final);
-  return run_online<double>(*c, W, Wout, x, T, labels, lr, every, spikes, dW, dWout, loss, W_final,
-                            Wout_final);
+    return run_online<float>(*c, W, Wout, Fb, x, T, labels, lr, every, spikes, dW, dWout, loss,
+                             W_final, Wout_final);
+  return run_online<double>(*c, W, Wout, Fb, x, T, labels, lr, every, spikes, dW, dWout, loss,
+                            W_final, Wout_final);
+}
+
+int oracle_eprop_run_online(const oracle_config* c, const float* const* W,
+                            const float* const* Wout, const uint8_t* x, int32_t T,
+                            const int32_t* labels, double lr, int32_t every, uint32_t* spikes,
+                            double* const* dW, double* const* dWout, double* loss,
+                            float* const* W_final, float* const* Wout_final) {
+  return oracle_eprop_run_online_fb(c, W, Wout, nullptr, x, T, labels, lr, every, spikes, dW, dWout,
+                                    loss, W_final, Wout_final);
 }
 
 // The same with the learning signal through W_out (symmetric feedback).

@@ -304,11 +304,19 @@ int pack_weights(eprop_ctx* ctx) {
     rc = check(ctx, eprop::launch_pack(L.Wout_src, c.n_out, c.n_rec, L.WoutT, ctx->plan.ldk,
                                        ctx->plan.ldn, 1, ctx->stream), "readout weight packing");
     if (rc) return rc;
-    if (L.Fb_src) {
-      rc = check(ctx, eprop::launch_pack(L.Fb_src, c.n_out, c.n_rec, L.FbT, ctx->plan.ldk,
-                                         ctx->plan.ldn, 1, ctx->stream), "feedback matrix packing");
-      if (rc) return rc;
-    }
+  }
+  return EPROP_OK;
+}
+
+// FbT[j][k] = B[k][j] for every layer with a feedback matrix set; nothing
+// else is rewritten (the weights in use stay what they are).
+int pack_feedback(eprop_ctx* ctx) {
+  const eprop_config& c = ctx->plan.cfg;
+  for (Layer& L : ctx->plan.layers) {
+    if (!L.Fb_src) continue;
+    int rc = check(ctx, eprop::launch_pack(L.Fb_src, c.n_out, c.n_rec, L.FbT, ctx->plan.ldk,
+                                           ctx->plan.ldn, 1, ctx->stream), "feedback matrix packing");
+    if (rc) return rc;
   }
   return EPROP_OK;
 }
@@ -625,6 +633,7 @@ int eprop_get_grads(eprop_ctx* ctx, float* const* d_grads, double* d_loss) {
 int eprop_reset(eprop_ctx* ctx) {
   if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
   int rc = pack_weights(ctx);
+  if (!rc) rc = pack_feedback(ctx);
   if (!rc) rc = clear_state(ctx);
   return rc;
 }
@@ -633,7 +642,11 @@ int eprop_set_feedback(eprop_ctx* ctx, const float* const* d_feedback) {
   if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
   for (int l = 0; l < ctx->plan.cfg.n_layers; ++l)
     ctx->plan.layers[l].Fb_src = d_feedback ? d_feedback[l] : nullptr;
-  return pack_weights(ctx);
+  // Queued after the work already enqueued: the blocks of earlier calls
+  // (whose learning-signal GEMMs read the old matrices) run before the
+  // repacking, because the coefficient stream is joined to the caller's
+  // stream by every block's eligibility pass.
+  return pack_feedback(ctx);
 }
 
 int eprop_set_online(eprop_ctx* ctx, float lr, int32_t every) {

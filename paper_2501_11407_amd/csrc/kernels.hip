@@ -10,7 +10,7 @@
 #include <math.h>
 
 #include <algorithm>
-
+#include <mutex>
 #include <utility>
 
 namespace eprop {
@@ -1472,17 +1472,27 @@ __global__ __launch_bounds__(256) void pack_kernel(const float* src, int rows, i
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
+// gfx950 gives a workgroup up to the whole 160 KiB of shared memory, but
+// more than 64 KiB must be requested per kernel.  Each kernel is granted its
+// largest size once per process (std::call_once: contexts may launch from
+// several host threads), and every launch checks the outcome.
+constexpr int kMaxSmem = 160 * 1024;
+template <auto Kernel>   // one instance (and one flag) per kernel
+hipError_t grant_smem(int bytes) {
+  static std::once_flag once;
+  static hipError_t result = hipSuccess;
+  std::call_once(once, [bytes] {
+    result = hipFuncSetAttribute(reinterpret_cast<const void*>(Kernel),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  });
+  return result;
+}
+
 template <int QN, int NL>
 hipError_t launch_forward_qn(const FwdArgs& a, hipStream_t s) {
-  // gfx950 gives a workgroup up to the whole 160 KiB of shared memory, but
-  // more than 64 KiB must be requested per kernel.
-  static size_t granted = 64 * 1024;
-  if (a.smem > granted) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&forward_kernel<QN, NL>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.smem);
-    if (e != hipSuccess) return e;
-    granted = a.smem;
-  }
+  if (a.smem > (size_t)kMaxSmem) return hipErrorInvalidValue;
+  hipError_t e = grant_smem<&forward_kernel<QN, NL>>(kMaxSmem);
+  if (e != hipSuccess) return e;
   forward_kernel<QN, NL><<<a.B, kFwdThreads, a.smem, s>>>(a);
   return hipGetLastError();
 }
@@ -1545,13 +1555,8 @@ template <bool RT, int NCH>
 hipError_t launch_trace_variant(const TraceArgs& a, hipStream_t s) {
   // more than 64 KiB of shared memory must be requested per kernel
   constexpr size_t smem = kTraceSmemOf(RT);
-  static bool granted = false;
-  if (!granted) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&trace_kernel<RT, NCH>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (e != hipSuccess) return e;
-    granted = true;
-  }
+  hipError_t e = grant_smem<&trace_kernel<RT, NCH>>((int)smem);
+  if (e != hipSuccess) return e;
   dim3 grid((a.n_pre_pad / kTile) * a.n_jt, a.n_split);
   trace_kernel<RT, NCH><<<grid, 256, smem, s>>>(a);
   return hipGetLastError();

@@ -66,7 +66,8 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedbac
     With a schedule the learning signal is e-prop's online one: the error at
     step t reaches the spikes of steps s <= t through the readout weights in
     use at step t (kappa^(t-s) W_out(t)^T delta_t), not those in use at s;
-    the readout value and its gradient stay exact.
+    the readout value and its gradient stay exact.  With both, the feedback
+    matrices take the place of W_out(t) in that signal and do not change.
     """
     T = x.shape[0] if T is None else T
     L, B, N = shape.n_layers, shape.batch, shape.n_rec
@@ -75,7 +76,9 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedbac
     sg = (lambda v: v.detach()) if stop else (lambda v: v)
     Ws = [torch.tensor(np.asarray(w, dtype=np.float64), requires_grad=True) for w in W]
     Wos = [torch.tensor(np.asarray(w, dtype=np.float64), requires_grad=True) for w in Wout]
-    Fbs = None if feedback is None else [torch.tensor(np.asarray(f, dtype=np.float64)) for f in feedback]
+    # a None entry: that layer's learning signal through its own readout weights
+    Fbs = None if feedback is None else [None if f is None else torch.tensor(np.asarray(f, dtype=np.float64))
+                                         for f in feedback]
     beta = torch.zeros(N, dtype=F64)
     beta[: shape.n_adaptive] = shape.beta
     lab = torch.tensor(np.asarray(labels, dtype=np.int64))
@@ -112,7 +115,7 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedbac
             A = shape.thr + A
             z = _Spike.apply(vl - A, shape.gamma, shape.thr)
             if schedule is None:
-                yz = z @ Wouse[l].T if Fbs is None else _Readout.apply(z, Wouse[l], Fbs[l])
+                yz = z @ Wouse[l].T if Fbs is None or Fbs[l] is None else _Readout.apply(z, Wouse[l], Fbs[l])
                 y[l] = shape.kappa * y[l] + yz
                 logits = y[l]
             else:
@@ -120,7 +123,8 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedbac
                 # spikes' gradient: filtered spikes through today's W_out
                 y[l] = shape.kappa * y[l] + z.detach() @ Wouse[l].T
                 zh[l] = shape.kappa * zh[l] + z
-                logits = y[l] + (zh[l] - zh[l].detach()) @ Wouse[l].detach().T
+                back = Wouse[l].detach() if Fbs is None or Fbs[l] is None else Fbs[l]   # fixed feedback
+                logits = y[l] + (zh[l] - zh[l].detach()) @ back.T
             loss = loss + torch.nn.functional.cross_entropy(logits, lab, reduction="sum")
             v[l], a[l] = vl, al
             z_now.append(z)

@@ -76,6 +76,21 @@ def sample_synapses(shape, n_random=384, seed=0):
     return np.array(rows, dtype=np.int32)
 
 
+def sample_every_tile(shape, tile=64, seed=0):
+    """One random synapse inside every tile x tile block of (i, j) of every
+    layer, plus the index-range edges of sample_synapses."""
+    rng = np.random.default_rng(seed)
+    rows = [tuple(r) for r in sample_synapses(shape, n_random=0)]
+    for l in range(shape.n_layers):
+        n_pre = shape.n_pre(l)
+        for i0 in range(0, n_pre, tile):
+            for j0 in range(0, shape.n_rec, tile):
+                i = int(rng.integers(i0, min(i0 + tile, n_pre)))
+                j = int(rng.integers(j0, min(j0 + tile, shape.n_rec)))
+                rows.append((l, j, i))
+    return np.array(rows, dtype=np.int32)
+
+
 def check_against_oracle(wl, gpu, sample=None, T=None, tol=GRAD_TOL, feedback=None):
     """Oracle on the same inputs; spikes must be identical, gradients within tol."""
     shape = wl.shape

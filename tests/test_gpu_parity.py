@@ -13,8 +13,8 @@ import torch
 import oracle
 from paper_2501_11407_amd import eprop, synth
 from tests.bptt_torch import rel_l2
-from tests.gpu_util import (check_against_oracle, first_spike_mismatch, gpu_run, sample_synapses,
-                            to_dev, workers)
+from tests.gpu_util import (check_against_oracle, first_spike_mismatch, gpu_run, sample_every_tile,
+                            sample_synapses, to_dev, workers)
 
 pytestmark = pytest.mark.gpu
 f32 = synth.f32
@@ -211,6 +211,67 @@ def test_online_weights_match_oracle(name):
         assert any(not np.array_equal(ref.W[l], wl.W[l]) for l in range(shape.n_layers))
 
 
+ONLINE_FB = {
+    "rlif": ONLINE["rlif"],
+    "ralif": ONLINE["ralif"],
+    "ralif2": ONLINE["ralif2"],
+}
+
+
+def _online_margin_fb(shape, wl, lr, every, fb):
+    m = np.inf
+    for t1 in range(every, wl.x.shape[0], every):
+        r = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, lr, every, T=t1, feedback=fb)
+        for l in range(shape.n_layers):
+            for W0, G in ((wl.W[l], r.dW[l]), (wl.Wout[l], r.dWout[l])):
+                v = (W0.astype(np.float64) - lr * G) * 16384.0
+                m = min(m, float(np.min(np.abs(np.abs(v - np.floor(v)) - 0.5))))
+    return m
+
+
+@pytest.mark.parametrize("name", list(ONLINE_FB))
+def test_online_weights_with_feedback_match_oracle(name):
+    # Online weight application with fixed feedback matrices (two layers:
+    # on layer 1 only).  The matrices stay while W and W_out change.  Split
+    # calls set the same matrices again between the calls, after an update:
+    # that must not touch the weights in use.
+    shape, seed, every = ONLINE_FB[name]
+    banner(f"online weights with feedback {name} {shape} every {every}")
+    wl = synth.make_workload(shape, seed, input_scale=4.0)
+    fb = synth.make_feedback(shape, seed)
+    if shape.n_layers == 2:
+        fb[1] = None
+    assert _online_margin_fb(shape, wl, ONLINE_LR, every, fb) > 1e-4
+    ref = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, ONLINE_LR, every, feedback=fb)
+    sym = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, ONLINE_LR, every)
+    assert rel_l2(ref.dW[0], sym.dW[0]) > 1e-2
+    for split in (None, 15):
+        ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+        ctx.set_online(ONLINE_LR, every)
+        ctx.set_feedback(fb)
+        x, labels = to_dev(wl)
+        spikes = ctx.new_spike_buffer(shape.T)
+        if split is None:
+            ctx.run_sequence(x, labels, spikes)
+        else:
+            ctx.run_sequence(x[:split], labels, spikes[:split])
+            ctx.set_feedback(fb)
+            ctx.run_sequence(x[split:], labels, spikes[split:])
+        dW, dWout, loss = ctx.get_grads()
+        Wg, Wog = ctx.get_weights()
+        torch.cuda.synchronize()
+        assert ctx.status() == 0
+        ctx.close()
+        mism = first_spike_mismatch(spikes.cpu().numpy().view(np.uint32), ref.spikes)
+        assert mism is None, f"spike trains differ: {mism}"
+        for l in range(shape.n_layers):
+            assert np.array_equal(Wg[l].cpu().numpy(), ref.W[l]), f"layer {l} weights differ"
+            assert np.array_equal(Wog[l].cpu().numpy(), ref.Wout[l])
+            assert rel_l2(dW[l].cpu().numpy(), ref.dW[l]) <= 1e-4
+            assert rel_l2(dWout[l].cpu().numpy(), ref.dWout[l]) <= 1e-4
+        assert abs(float(loss.cpu()) - ref.loss) <= 1e-4 * abs(ref.loss)
+
+
 def test_online_off_and_reset_give_the_plain_run():
     shape, seed, every = ONLINE["rlif"]
     wl = synth.make_workload(shape, seed, input_scale=4.0)
@@ -351,17 +412,87 @@ def test_named_workload_all_synapses(name):
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("name", ["ralif_b64_n512_t500", "ralif_b128_n1024_t1000",
-                                  "ralif2_b256_n2048_t2000"])
-def test_named_workload_sampled_synapses(name):
-    # Full size; every spike compared, the gradient on sampled synapses (the
-    # oracle computes those one by one), the readout gradient in full.
-    banner(f"workload {name}, sampled synapses")
+@pytest.mark.parametrize("name", ["ralif_b64_n512_t500", "ralif_b128_n1024_t1000"])
+def test_named_workload_every_synapse_full_size(name):
+    # Full size, every spike and every synapse's gradient (the oracle in
+    # single-threaded batch shards on the host's cores).
+    banner(f"workload {name}, every synapse")
     wl = synth.named_workload(name)
     gpu = gpu_run(wl)
-    smp = sample_synapses(wl.shape)
+    errs, _ = check_against_oracle(wl, gpu)
+    banner(f"{name}: {errs}")
+
+
+@pytest.mark.timeout(900)
+def test_two_layer_workload_every_tile_sampled():
+    # Two layers of 2048, B=256, T=2000: every spike, the readout gradients in
+    # full, and one synapse in every 64 x 64 block of (i, j) of both layers
+    # (3424 blocks) plus the index-range edges, which the oracle computes one
+    # by one.
+    name = "ralif2_b256_n2048_t2000"
+    banner(f"workload {name}, one synapse per 64x64 block")
+    wl = synth.named_workload(name)
+    gpu = gpu_run(wl)
+    smp = sample_every_tile(wl.shape)
+    assert len(smp) > 3400
     errs, _ = check_against_oracle(wl, gpu, sample=smp)
     banner(f"{name}: {errs}")
+
+
+@pytest.mark.parametrize("reset_grad", [0, 1])
+def test_large_batch_uneven_splits(reset_grad):
+    # B = 233: the eligibility kernel's batch split count comes from the
+    # batch (9 splits of 26 or 25 elements), every synapse compared.
+    shape = synth.EpropShape(batch=233, n_in=24, n_rec=40, n_out=5, T=40, n_adaptive=20,
+                             reset_grad=reset_grad, **DISTINCT)
+    banner(f"large batch {shape}")
+    wl = synth.make_workload(shape, 233, input_scale=4.0)
+    gpu = gpu_run(wl)
+    errs, ref = check_against_oracle(wl, gpu)
+    assert ref.spikes.any()
+    banner(f"B=233: {errs}")
+
+
+def adversarial_range_workload(reset_grad=0):
+    """Mostly inhibitory inputs with a few strong excitatory channels (the
+    pseudo-derivative is zero for most steps of most neurons) and a readout
+    that becomes confident in the one label, so that the learning signal of a
+    neuron spans many decades within a 256-step block."""
+    shape = synth.EpropShape(batch=4, n_in=40, n_rec=48, n_out=3, T=300, n_adaptive=24,
+                             reset_grad=reset_grad, **DISTINCT)
+    wl = synth.make_workload(shape, 77, input_scale=6.0)
+    rng = np.random.default_rng(5)
+    w_in = rng.normal(-0.35, 0.25, size=(shape.n_rec, shape.n_in))
+    exc = rng.random(shape.n_in) < 0.25
+    w_in[:, exc] = rng.normal(0.9, 0.2, size=(shape.n_rec, int(exc.sum())))
+    wl.W[0][:, :shape.n_in] = synth.quantize(w_in, 8)
+    wl.labels[:] = 0
+    wl.Wout[0][:] = -0.125
+    wl.Wout[0][0] = 0.25
+    return wl
+
+
+@pytest.mark.parametrize("reset_grad", [0, 1])
+def test_adversarial_dynamic_range(reset_grad):
+    # The contraction operands are scaled fp16 pairs with one scale per
+    # (batch element, neuron) row and block: small entries of a row with a
+    # wide range keep only the row's absolute precision.  Here the learning
+    # signal of every row spans >= 8 decades within each block and the
+    # pseudo-derivative is zero for most steps (both checked on the oracle's
+    # record); the gradients must still meet the parity bar.
+    wl = adversarial_range_workload(reset_grad)
+    shape = wl.shape
+    banner(f"adversarial dynamic range, reset_grad={reset_grad}")
+    rec = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, want_record=True).record
+    assert (rec["psi"] == 0).mean() > 0.75
+    for t0, t1 in ((0, 256), (256, shape.T)):
+        a = np.abs(rec["L"][t0:t1, 0])
+        lo = np.where(a > 0, a, np.inf).min(0)
+        assert np.all(a.max(0) / lo >= 1e8)
+    gpu = gpu_run(wl)
+    errs, ref = check_against_oracle(wl, gpu)
+    assert ref.spikes.any()
+    banner(f"adversarial range: {errs}")
 
 
 def test_intermediate_state_matches_oracle_record():

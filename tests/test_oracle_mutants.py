@@ -50,6 +50,7 @@ MUTANTS = [
      "ev = (c.alpha - c.reset * pj) * V;", 1),
     ("online_update_from_current_weights", "Wcur[l][ji] = on_grid((double)W0[l][ji] - lr * dW[l][ji]);",
      "Wcur[l][ji] = on_grid((double)Wcur[l][ji] - lr * dW[l][ji]);", 1),
+    ("online_feedback_ignored", "steps(c, Wcur, Woutcur, Fb, x,", "steps(c, Wcur, Woutcur, nullptr, x,", 1),
     ("online_readout_not_updated", "Woutcur[l][kj] = on_grid((double)Wout0[l][kj] - lr * dWout[l][kj]);",
      "Woutcur[l][kj] = Wout0[l][kj];", 1),
 ]

@@ -48,6 +48,8 @@ AUTOGRAD_CASES = {
     "rlif_b32_n256_t250": (synth.WORKLOADS["rlif_b32_n256_t250"], 2, 1.0),
     # The recurrent-ALIF shape (700 in, 512 neurons, 204 adaptive) with B=6, T=120.
     "ralif_n512_b6_t120": (synth.WORKLOADS["ralif_b64_n512_t500"].replace(batch=6, T=120), 3, 1.0),
+    # The bench shape (700 in, 1024 neurons, 512 adaptive, 35 classes) with B=3, T=150.
+    "ralif_n1024_b3_t150": (synth.WORKLOADS["ralif_b128_n1024_t1000"].replace(batch=3, T=150), 4, 1.0),
 }
 
 
@@ -152,6 +154,55 @@ def test_online_weights_equal_backprop_with_the_same_schedule(name):
     assert rel_l2(r.dW[0], plain.dW[0]) > 1e-3
 
 
+def online_schedule_fb(shape, wl, lr, every, T, fb):
+    """online_schedule with fixed feedback matrices in the learning signal."""
+    sched, margin = [], np.inf
+    for t1 in range(every, T, every):
+        dW, dWout, _ = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels, T=t1, schedule=sched,
+                                  feedback=fb)
+        Wn, Won = [], []
+        for W0, G, out in ((wl.W, dW, Wn), (wl.Wout, dWout, Won)):
+            for l in range(shape.n_layers):
+                v = (np.asarray(W0[l], np.float64) - lr * G[l]) * 16384.0
+                margin = min(margin, float(np.min(np.abs(np.abs(v - np.floor(v)) - 0.5))))
+                out.append((np.rint(v) / 16384.0).astype(np.float32))
+        sched.append((t1, Wn, Won))
+    return sched, margin
+
+
+@pytest.mark.parametrize("name", ["rlif_ragged", "ralif_ragged", "ralif2_two_layers"])
+def test_online_weights_with_feedback_equal_backprop(name):
+    # Online weight application with fixed feedback matrices in the learning
+    # signal (the two-layer case: feedback on layer 1 only, layer 2 through
+    # its readout weights in use).  The matrices are not weights: they keep
+    # their values while W and W_out change.  Reverse-mode autograd with the
+    # same schedule and the same fixed matrices must agree.
+    shape, seed, scale = AUTOGRAD_CASES[name]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    fb = synth.make_feedback(shape, seed)
+    if shape.n_layers == 2:
+        fb[1] = None
+    lr, every = 2.0 ** -8, 10
+    sched, margin = online_schedule_fb(shape, wl, lr, every, shape.T, fb)
+    assert margin > 1e-6
+    r = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, lr, every, fwd_fp32=False,
+                          feedback=fb)
+    dW, dWout, loss = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels, schedule=sched, feedback=fb)
+    assert r.spikes.any()
+    assert abs(r.loss - loss) <= 1e-12 * abs(loss)
+    for l in range(shape.n_layers):
+        assert rel_l2(r.dW[l], dW[l]) <= 1e-11, (l, rel_l2(r.dW[l], dW[l]))
+        assert rel_l2(r.dWout[l], dWout[l]) <= 1e-11
+        assert np.array_equal(r.W[l], sched[-1][1][l]) and np.array_equal(r.Wout[l], sched[-1][2][l])
+    # the feedback matters: a different run from the online one without it
+    sym = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, lr, every, fwd_fp32=False)
+    assert rel_l2(r.dW[0], sym.dW[0]) > 1e-2
+    # feedback equal to W_out0 is not the symmetric online run: the matrices stay fixed
+    same0 = oracle.run_online(shape, wl.W, wl.Wout, wl.x, wl.labels, lr, every, fwd_fp32=False,
+                              feedback=[w.copy() for w in wl.Wout])
+    assert rel_l2(same0.dW[0], sym.dW[0]) > 1e-9
+
+
 def test_online_without_a_change_is_the_plain_run():
     # lr = 0, or blocks as long as the sequence: the plain run (up to the
     # order of the gradient sums over batch elements and steps)
@@ -211,6 +262,59 @@ def test_recurrence_breaks_exactness():
     r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
     dW, _, _ = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels, stop=False)
     assert rel_l2(r.dW[0], dW[0]) > 1e-3
+
+
+def test_without_recurrent_weights_equals_feedforward_backprop():
+    # W_rec = 0 in the recurrent LIF workload (B=32, 700 in, 256 neurons,
+    # T=250): the recurrent spikes then have no influence on the dynamics,
+    # so the stop on them cuts nothing and the input-weight gradient must be
+    # plain backpropagation through time of the feed-forward layer (with the
+    # reset stopped, as always).
+    shape = synth.WORKLOADS["rlif_b32_n256_t250"]
+    wl = synth.make_workload(shape, 2)
+    W = [wl.W[0].copy()]
+    W[0][:, shape.n_in:] = 0.0
+    r = oracle.run(shape, W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    ff = shape.replace(recurrent=0)
+    dW, dWout, loss = bptt_grads(ff, [np.ascontiguousarray(W[0][:, :shape.n_in])], wl.Wout, wl.x,
+                                 wl.labels)
+    assert r.spikes.any()
+    assert abs(r.loss - loss) <= 1e-12 * abs(loss)
+    assert rel_l2(r.dW[0][:, :shape.n_in], dW[0]) <= 1e-11
+    assert rel_l2(r.dWout[0], dWout[0]) <= 1e-11
+    # the recurrent columns carry a gradient of their own (dE/dW_rec at 0)
+    assert np.abs(r.dW[0][:, shape.n_in:]).max() > 0
+
+
+@pytest.mark.parametrize("recurrent", [0, 1])
+def test_zero_readout_leak_makes_the_filtered_trace_the_trace(recurrent):
+    # kappa = 0: the readout has no memory, the filtered trace is the trace
+    # itself (ebar = e), and for LIF neurons e = psi_j zbar_i, so
+    # dW_ji = sum_b sum_t L_j psi_j zbar_i with zbar the alpha-filtered
+    # presynaptic vector, built here from the inputs and the recorded spikes.
+    shape = small(T=60, recurrent=recurrent, kappa=0.0, alpha=DISTINCT["alpha"])
+    wl = synth.make_workload(shape, 21, input_scale=4.0)
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False, want_record=True)
+    psi, L, z = r.record["psi"][:, 0], r.record["L"][:, 0], r.record["z"][:, 0]
+    assert z.any()
+    dW = np.zeros((shape.n_rec, shape.n_pre(0)))
+    zbar = np.zeros((shape.batch, shape.n_pre(0)))
+    zprev = np.zeros((shape.batch, shape.n_rec))
+    for t in range(shape.T):
+        p = wl.x[t].astype(np.float64)
+        if recurrent:
+            p = np.concatenate([p, zprev], axis=1)
+        zbar = shape.alpha * zbar + p
+        dW += (L[t] * psi[t]).T @ zbar
+        zprev = z[t]
+    if recurrent:
+        idx = np.arange(shape.n_rec)
+        dW[idx, shape.n_in + idx] = 0.0
+    assert rel_l2(r.dW[0], dW) <= 1e-12
+    # and kappa matters: the default readout leak gives another gradient
+    r2 = oracle.run(shape.replace(kappa=DISTINCT["kappa"]), wl.W, wl.Wout, wl.x, wl.labels,
+                    fwd_fp32=False)
+    assert rel_l2(r2.dW[0], r.dW[0]) > 1e-3
 
 
 def test_fp32_and_fp64_forward_agree():
