@@ -214,6 +214,31 @@ int eprop_get_weights(eprop_ctx* ctx, float* const* d_weights);
 void eprop_destroy(eprop_ctx* ctx);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid it): one whole sequence
+ * without a caller workspace, creating no streams or events.  Equivalent to
+ * eprop_init + eprop_run_sequence(d_x, T, d_labels, d_spikes) +
+ * eprop_get_grads(d_grads, d_loss) + eprop_destroy, with the same kernels and
+ * results, all queued on hip_stream (one stream: the forward of a block does
+ * not overlap the eligibility pass of the one before).  Arguments as for
+ * those calls; the weights are read on the stream.
+ * The workspace is the library's static scratch, EPROP_STATIC_SCRATCH_BYTES
+ * of device memory that every GPU the library runs on holds from the first
+ * use of the library until the process ends; shapes whose
+ * eprop_workspace_bytes exceeds it return EPROP_ENOSPACE (before any device
+ * call).  The device is the one current on the calling thread, which must be
+ * the stream's.  Every call on one GPU uses that GPU's one scratch array:
+ * calls that overlap on a GPU (queued on different streams without ordering,
+ * or from several host threads) race; calls queued on one stream do not.
+ * Each call clears what it needs itself.  Errors: eprop_last_error(NULL).
+ */
+#define EPROP_STATIC_SCRATCH_BYTES (160u << 20)
+int eprop_sequence_static(const eprop_config* cfg, const float* const* d_weights,
+                          const uint8_t* d_x, int32_t T, const int32_t* d_labels,
+                          uint32_t* d_spikes, float* const* d_grads, double* d_loss,
+                          void* hip_stream);
+
+/*
  * Message of the last failure on ctx, or of the last failed eprop_init /
  * workspace query of this thread when ctx is NULL.  Never NULL.
  */

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -78,9 +79,25 @@ struct Layer {
   float* epsv = nullptr;                 // reset_grad: per-synapse membrane eligibility
 };
 
+// At most two layers, held in place (a plan allocates nothing).
+struct Layers {
+  Layer l[2];
+  int n = 0;
+  void assign(int count, const Layer& v) {
+    n = count;
+    for (int k = 0; k < 2; ++k) l[k] = v;
+  }
+  Layer& operator[](int k) { return l[k]; }
+  const Layer& operator[](int k) const { return l[k]; }
+  Layer* begin() { return l; }
+  Layer* end() { return l + n; }
+  const Layer* begin() const { return l; }
+  const Layer* end() const { return l + n; }
+};
+
 struct Plan {
   eprop_config cfg;
-  std::vector<Layer> layers;
+  Layers layers;
   int* err_flag = nullptr;
   int* w16ok = nullptr;             // 1: the int16 drive weights are exact (launch_pack16)
   int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, ldc = 0, jlist = 0, out_splits = 1;
@@ -257,6 +274,9 @@ struct eprop_ctx {
   // eligibility kernel (learning signal, readout gradient, coefficients)
   hipStream_t fwd_stream = nullptr, coef_stream = nullptr;
   hipEvent_t ev_entry = nullptr, ev_fwd[kSlots] = {}, ev_coef[kSlots] = {}, ev_done[kSlots] = {};
+  // every kernel on the caller's stream, in issue order, with no streams or
+  // events of the context's own (the entry point that allocates nothing)
+  bool single_stream = false;
   // online weight application (eprop_set_online): every `online_every` steps
   // since the reset, before the next step runs
   float online_lr = 0.0f;
@@ -328,17 +348,18 @@ int clear_state(eprop_ctx* ctx) {
   const eprop_config& c = ctx->plan.cfg;
   const size_t B = c.batch, N = c.n_rec, K = c.n_out;
   hipStream_t s = ctx->stream;
-  int rc = check(ctx, hipMemsetAsync(ctx->plan.err_flag, 0, sizeof(int), s), "reset");
+  // a fill kernel rather than memset nodes, so that a caller may capture it
+  int rc = check(ctx, eprop::launch_zero(ctx->plan.err_flag, sizeof(int), s), "reset");
   for (Layer& L : ctx->plan.layers) {
     if (rc) return rc;
     hipError_t e = hipSuccess;
-    e = e ? e : hipMemsetAsync(L.v, 0, sizeof(float) * B * N, s);
-    e = e ? e : hipMemsetAsync(L.a, 0, sizeof(float) * B * N, s);
-    e = e ? e : hipMemsetAsync(L.ztil, 0, sizeof(float) * B * N, s);
-    e = e ? e : hipMemsetAsync(L.zbar, 0, sizeof(float) * B * L.n_pre, s);
-    e = e ? e : hipMemsetAsync(L.y, 0, sizeof(float) * B * K, s);
-    e = e ? e : hipMemsetAsync(L.z, 0, B * N, s);
-    e = e ? e : hipMemsetAsync(L.lossacc, 0, sizeof(double) * B, s);
+    e = e ? e : eprop::launch_zero(L.v, sizeof(float) * B * N, s);
+    e = e ? e : eprop::launch_zero(L.a, sizeof(float) * B * N, s);
+    e = e ? e : eprop::launch_zero(L.ztil, sizeof(float) * B * N, s);
+    e = e ? e : eprop::launch_zero(L.zbar, sizeof(float) * B * L.n_pre, s);
+    e = e ? e : eprop::launch_zero(L.y, sizeof(float) * B * K, s);
+    e = e ? e : eprop::launch_zero(L.z, B * N, s);
+    e = e ? e : eprop::launch_zero(L.lossacc, sizeof(double) * B, s);
     rc = check(ctx, e, "reset");
   }
   ctx->t = 0;
@@ -366,6 +387,7 @@ int apply_online(eprop_ctx* ctx) {
     a.lr = (double)ctx->online_lr;
     rc = check(ctx, eprop::launch_online_update(a, s), "online weight update");
   }
+  if (ctx->single_stream) return rc;
   if (!rc) rc = check(ctx, hipEventRecord(ctx->ev_update, s), "event record");
   if (!rc) rc = check(ctx, hipStreamWaitEvent(ctx->fwd_stream, ctx->ev_update, 0), "stream wait");
   return rc;
@@ -388,8 +410,9 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ctx->online_applied = ctx->t;
   }
   // The forward may overwrite this slot once the passes that read it
-  // kSlots blocks ago are done.
-  if (ctx->slot_used[sl] &&
+  // kSlots blocks ago are done.  (On one stream, issue order says so.)
+  const bool ev = !ctx->single_stream;
+  if (ev && ctx->slot_used[sl] &&
       (rc = check(ctx, hipStreamWaitEvent(sf, ctx->ev_done[sl], 0), "stream wait")))
     return rc;
 
@@ -411,12 +434,12 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
   fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.zgroup = P.zgroup;
   if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
-  if ((rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
+  if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
 
   // On the coefficient stream, per layer: learning signal, readout gradient
   // and the block coefficients of the eligibility recursion.  The forward of
   // the next block (other slot) runs meanwhile.
-  if ((rc = check(ctx, hipStreamWaitEvent(sc, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
+  if (ev && (rc = check(ctx, hipStreamWaitEvent(sc, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
   const int rows = steps * P.Bp;
   const int kpad = (int)round_up(steps, 16);
   for (int l = 0; l < c.n_layers; ++l) {
@@ -451,8 +474,8 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ca.W = L.coefW[sl]; ca.reset_through = c.reset_grad;
     if ((rc = check(ctx, eprop::launch_coef(ca, sc), "eligibility coefficient kernel"))) return rc;
   }
-  if ((rc = check(ctx, hipEventRecord(ctx->ev_coef[sl], sc), "event record"))) return rc;
-  if ((rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_coef[sl], 0), "stream wait"))) return rc;
+  if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_coef[sl], sc), "event record"))) return rc;
+  if (ev && (rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_coef[sl], 0), "stream wait"))) return rc;
 
   // On the caller's stream: the eligibility pass of every layer.
   for (int l = 0; l < c.n_layers; ++l) {
@@ -482,7 +505,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
       ctx->prof_n++;
     }
   }
-  if ((rc = check(ctx, hipEventRecord(ctx->ev_done[sl], s), "event record"))) return rc;
+  if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_done[sl], s), "event record"))) return rc;
   ctx->slot_used[sl] = true;
   ctx->last_slot = sl;
   ctx->slot = (ctx->slot + 1) % kSlots;
@@ -496,9 +519,100 @@ bool usable(const eprop_ctx* ctx) { return ctx && ctx->alive; }
 // Work queued on the caller's stream before this call (inputs, a reset, new
 // weights) happens before the forward kernels of this call.
 int join_forward_stream(eprop_ctx* ctx) {
+  if (ctx->single_stream) return EPROP_OK;
   int rc = check(ctx, hipEventRecord(ctx->ev_entry, ctx->stream), "event record");
   if (!rc) rc = check(ctx, hipStreamWaitEvent(ctx->fwd_stream, ctx->ev_entry, 0), "stream wait");
   return rc;
+}
+
+// Argument checks shared by eprop_init and eprop_sequence_static (errors
+// reported through eprop_last_error(NULL)).
+int check_init_args(const eprop_config* cfg, const void* d_workspace, size_t ws_bytes,
+                    const float* const* d_weights) {
+  std::string why;
+  if (!valid_config(cfg, &why)) return fail(nullptr, EPROP_EINVAL, why);
+  if (!d_workspace || !d_weights) return fail(nullptr, EPROP_EINVAL, "workspace or weights is NULL");
+  if (((uintptr_t)d_workspace) % 256 != 0)
+    return fail(nullptr, EPROP_EINVAL, "workspace must be 256-byte aligned");
+  for (int k = 0; k < 2 * cfg->n_layers; ++k)
+    if (!d_weights[k]) return fail(nullptr, EPROP_EINVAL, "a weight pointer is NULL");
+  Plan probe;
+  make_plan(*cfg, nullptr, &probe);
+  if (!plan_fits(probe, &why)) return fail(nullptr, EPROP_EINVAL, why);
+  if (ws_bytes < probe.bytes)
+    return fail(nullptr, EPROP_ENOSPACE,
+                "workspace too small: need " + std::to_string(probe.bytes) + " bytes");
+  return EPROP_OK;
+}
+
+// Lays the context out in the workspace and queues the clear, the weight
+// packing and the state reset.  With single_stream the context creates no
+// streams or events: every kernel goes to the caller's stream in issue order.
+int setup_ctx(eprop_ctx* ctx, const eprop_config* cfg, char* ws, size_t ws_bytes,
+              const float* const* d_weights, hipStream_t stream, bool single_stream) {
+  ctx->ws = ws;
+  ctx->ws_bytes = ws_bytes;
+  ctx->stream = stream;
+  ctx->single_stream = single_stream;
+  make_plan(*cfg, ctx->ws, &ctx->plan);
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    ctx->plan.layers[l].W_src = d_weights[2 * l];
+    ctx->plan.layers[l].Wout_src = d_weights[2 * l + 1];
+  }
+  int rc = EPROP_OK;
+  if (single_stream) {
+    ctx->fwd_stream = ctx->coef_stream = stream;
+  } else {
+    rc = check(ctx, hipStreamCreateWithFlags(&ctx->fwd_stream, hipStreamNonBlocking), "stream create");
+    if (!rc) rc = check(ctx, hipStreamCreateWithFlags(&ctx->coef_stream, hipStreamNonBlocking),
+                        "stream create");
+    if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_entry, hipEventDisableTiming), "event create");
+    if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_update, hipEventDisableTiming), "event create");
+    for (int k = 0; k < kSlots && !rc; ++k) {
+      rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_fwd[k], hipEventDisableTiming), "event create");
+      if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_coef[k], hipEventDisableTiming),
+                          "event create");
+      if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_done[k], hipEventDisableTiming),
+                          "event create");
+    }
+  }
+  // Padding of every buffer must read as zero; clear the whole layout once.
+  if (!rc) rc = check(ctx, eprop::launch_zero(ctx->ws, ctx->plan.bytes, ctx->stream), "workspace clear");
+  if (!rc) rc = pack_weights(ctx);
+  if (!rc) rc = clear_state(ctx);
+  if (!rc) ctx->alive = true;
+  return rc;
+}
+
+// ---------------------------------------------------------------- static scratch
+// Device memory of eprop_sequence_static: a file-scope array that every GPU
+// the library runs on holds (its own copy) until the process ends.  Host code
+// never passes the array's name to a kernel: its device address, per device,
+// comes from hipGetSymbolAddress on the first call on that device.
+constexpr size_t kScratchBytes = (size_t)EPROP_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch array's address on the current device (set up once per device).
+int scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(nullptr, EPROP_EDEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(nullptr, EPROP_EDEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(nullptr, EPROP_EDEVICE,
+                  std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return EPROP_OK;
 }
 
 }  // namespace
@@ -524,53 +638,47 @@ int eprop_init(const eprop_config* cfg, void* d_workspace, size_t ws_bytes,
                const float* const* d_weights, void* hip_stream, eprop_ctx** out) {
   if (!out) return fail(nullptr, EPROP_EINVAL, "out is NULL");
   *out = nullptr;
-  std::string why;
-  if (!valid_config(cfg, &why)) return fail(nullptr, EPROP_EINVAL, why);
-  if (!d_workspace || !d_weights) return fail(nullptr, EPROP_EINVAL, "workspace or weights is NULL");
-  if (((uintptr_t)d_workspace) % 256 != 0)
-    return fail(nullptr, EPROP_EINVAL, "workspace must be 256-byte aligned");
-  for (int k = 0; k < 2 * cfg->n_layers; ++k)
-    if (!d_weights[k]) return fail(nullptr, EPROP_EINVAL, "a weight pointer is NULL");
-  Plan probe;
-  make_plan(*cfg, nullptr, &probe);
-  if (!plan_fits(probe, &why)) return fail(nullptr, EPROP_EINVAL, why);
-  if (ws_bytes < probe.bytes)
-    return fail(nullptr, EPROP_ENOSPACE,
-                "workspace too small: need " + std::to_string(probe.bytes) + " bytes");
+  int rc = check_init_args(cfg, d_workspace, ws_bytes, d_weights);
+  if (rc) return rc;
   eprop_ctx* ctx = new eprop_ctx();
-  ctx->ws = (char*)d_workspace;
-  ctx->ws_bytes = ws_bytes;
-  ctx->stream = (hipStream_t)hip_stream;
-  make_plan(*cfg, ctx->ws, &ctx->plan);
-  for (int l = 0; l < cfg->n_layers; ++l) {
-    ctx->plan.layers[l].W_src = d_weights[2 * l];
-    ctx->plan.layers[l].Wout_src = d_weights[2 * l + 1];
-  }
-  int rc = check(ctx, hipStreamCreateWithFlags(&ctx->fwd_stream, hipStreamNonBlocking),
-                 "stream create");
-  if (!rc) rc = check(ctx, hipStreamCreateWithFlags(&ctx->coef_stream, hipStreamNonBlocking),
-                      "stream create");
-  if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_entry, hipEventDisableTiming), "event create");
-  if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_update, hipEventDisableTiming), "event create");
-  for (int k = 0; k < kSlots && !rc; ++k) {
-    rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_fwd[k], hipEventDisableTiming), "event create");
-    if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_coef[k], hipEventDisableTiming),
-                        "event create");
-    if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_done[k], hipEventDisableTiming),
-                        "event create");
-  }
-  // Padding of every buffer must read as zero; clear the whole layout once.
-  if (!rc) rc = check(ctx, hipMemsetAsync(ctx->ws, 0, ctx->plan.bytes, ctx->stream), "workspace clear");
-  if (!rc) rc = pack_weights(ctx);
-  if (!rc) rc = clear_state(ctx);
+  rc = setup_ctx(ctx, cfg, (char*)d_workspace, ws_bytes, d_weights, (hipStream_t)hip_stream, false);
   if (rc) {
     g_last_error = ctx->err;
     eprop_destroy(ctx);
     return rc;
   }
-  ctx->alive = true;
   *out = ctx;
   return EPROP_OK;
+}
+
+int eprop_sequence_static(const eprop_config* cfg, const float* const* d_weights, const uint8_t* d_x,
+                          int32_t T, const int32_t* d_labels, uint32_t* d_spikes,
+                          float* const* d_grads, double* d_loss, void* hip_stream) {
+  if (!d_x || !d_labels || !d_grads) return fail(nullptr, EPROP_EINVAL, "x, labels or grads is NULL");
+  if (T < 1) return fail(nullptr, EPROP_EINVAL, "T must be >= 1");
+  std::string why;
+  if (!valid_config(cfg, &why)) return fail(nullptr, EPROP_EINVAL, why);
+  for (int k = 0; k < 2 * cfg->n_layers; ++k)
+    if (!d_grads[k]) return fail(nullptr, EPROP_EINVAL, "a gradient pointer is NULL");
+  // the size check comes before any device call
+  const size_t need = eprop_workspace_bytes(cfg);
+  if (need == 0) return fail(nullptr, EPROP_EINVAL, g_last_error);
+  if (need > kScratchBytes)
+    return fail(nullptr, EPROP_ENOSPACE,
+                "shape needs " + std::to_string(need) + " bytes of workspace; the static scratch holds " +
+                    std::to_string(kScratchBytes));
+  void* ws = nullptr;
+  int rc = scratch_address(&ws);
+  if (rc) return rc;
+  rc = check_init_args(cfg, ws, kScratchBytes, d_weights);
+  if (rc) return rc;
+  eprop_ctx ctx;   // host-side bookkeeping only, on this stack frame
+  rc = setup_ctx(&ctx, cfg, (char*)ws, kScratchBytes, d_weights, (hipStream_t)hip_stream, true);
+  if (!rc) rc = eprop_run_sequence(&ctx, d_x, T, d_labels, d_spikes);
+  if (!rc) rc = eprop_get_grads(&ctx, d_grads, d_loss);
+  if (rc) g_last_error = ctx.err;
+  ctx.alive = false;
+  return rc;
 }
 
 int eprop_step(eprop_ctx* ctx, const uint8_t* d_x_t, const int32_t* d_labels, uint32_t* d_spikes_t) {
@@ -688,7 +796,7 @@ int eprop_status(eprop_ctx* ctx) {
 void eprop_destroy(eprop_ctx* ctx) {
   if (!ctx) return;
   for (hipStream_t st : {ctx->fwd_stream, ctx->coef_stream}) {
-    if (!st) continue;
+    if (!st || ctx->single_stream) continue;   // the caller's stream is not ours
     (void)hipStreamSynchronize(st);
     (void)hipStreamDestroy(st);
   }

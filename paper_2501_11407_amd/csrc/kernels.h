@@ -169,6 +169,8 @@ hipError_t launch_pack(const float* src, int rows, int cols, float* dst, int ldd
 hipError_t launch_pack16(const float* W, int n_rec, int n_pre, int16_t* W16, int qn, int* ok,
                          hipStream_t s);
 hipError_t launch_set_flag(int* flag, int value, hipStream_t s);
+// Zeroes `bytes` bytes at `p` (a fill kernel, not a memset node).
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 
 // Online weight application for one layer: the weights in use become
 // W0 - lr * G rounded to the nearest multiple of 2^-14 (ties to even), G the

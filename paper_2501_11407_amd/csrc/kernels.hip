@@ -1455,6 +1455,20 @@ __global__ void set_flag_kernel(int* flag, int value) {
   if (threadIdx.x == 0 && blockIdx.x == 0) *flag = value;
 }
 
+// 16-byte stores over the aligned body, byte stores over the ragged ends;
+// grid-stride, so any grid size covers the range.
+__global__ __launch_bounds__(256) void zero_kernel(unsigned char* p, size_t bytes) {
+  const size_t head = min(bytes, (size_t)((16 - ((uintptr_t)p & 15)) & 15));
+  const size_t nvec = (bytes - head) / 16;
+  const size_t tail0 = head + nvec * 16;
+  const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t nth = (size_t)gridDim.x * blockDim.x;
+  u32x4* body = (u32x4*)(p + head);
+  for (size_t k = tid; k < nvec; k += nth) body[k] = u32x4{0u, 0u, 0u, 0u};
+  if (tid < head) p[tid] = 0;
+  if (tid < bytes - tail0) p[tail0 + tid] = 0;
+}
+
 __global__ __launch_bounds__(256) void pack_kernel(const float* src, int rows, int cols, float* dst,
                                                    int ldd, int dst_rows, int transpose) {
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -1623,6 +1637,13 @@ hipError_t launch_unpack_weights(const float* Wt, int ldw, const float* WoutT, i
 
 hipError_t launch_set_flag(int* flag, int value, hipStream_t s) {
   set_flag_kernel<<<1, 64, 0, s>>>(flag, value);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  const long long blocks = std::min<long long>(8192, std::max<long long>(1, cdiv((long long)(bytes / 16), 256)));
+  zero_kernel<<<(int)blocks, 256, 0, s>>>((unsigned char*)p, bytes);
   return hipGetLastError();
 }
 

@@ -23,7 +23,7 @@ EPROP_OK, EPROP_EINVAL, EPROP_ENOSPACE, EPROP_EDEVICE, EPROP_ESTATE = 0, -1, -2,
 SYMBOLS = (
     "eprop_workspace_bytes", "eprop_init", "eprop_step", "eprop_run_sequence", "eprop_get_grads",
     "eprop_reset", "eprop_status", "eprop_set_feedback", "eprop_set_online", "eprop_get_weights",
-    "eprop_destroy", "eprop_last_error",
+    "eprop_destroy", "eprop_sequence_static", "eprop_last_error",
     "eprop_profile_begin", "eprop_profile_end", "eprop_debug_buffer",
 )
 
@@ -71,6 +71,7 @@ def load_library(path: str = LIB_PATH):
         "eprop_get_weights": (ctypes.c_int, [vp, vp]),
         "eprop_status": (ctypes.c_int, [vp]),
         "eprop_destroy": (None, [vp]),
+        "eprop_sequence_static": (ctypes.c_int, [cfgp, vp, vp, i32, vp, vp, vp, vp, vp]),
         "eprop_last_error": (ctypes.c_char_p, [vp]),
         "eprop_profile_begin": (ctypes.c_int, [vp, i32]),
         "eprop_profile_end": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double),
@@ -169,6 +170,22 @@ def eprop_status(ctx) -> int:
 
 def eprop_destroy(ctx):
     load_library().eprop_destroy(ctx)
+
+
+STATIC_SCRATCH_BYTES = 160 << 20      # EPROP_STATIC_SCRATCH_BYTES
+
+
+def eprop_sequence_static(cfg: eprop_config, weights: Sequence[torch.Tensor], x: torch.Tensor, T: int,
+                          labels: torch.Tensor, spikes: Optional[torch.Tensor],
+                          grads: Sequence[torch.Tensor], loss: Optional[torch.Tensor] = None,
+                          stream: Optional[torch.cuda.Stream] = None):
+    """One sequence in the library's static scratch (no caller workspace):
+    weights [W_0, Wout_0, ...] and grads [dW_0, dWout_0, ...] device fp32."""
+    s = (stream or torch.cuda.current_stream()).cuda_stream
+    rc = load_library().eprop_sequence_static(ctypes.byref(cfg), _ptr_array(weights), _ptr(x), int(T),
+                                              _ptr(labels), _ptr(spikes), _ptr_array(grads), _ptr(loss),
+                                              ctypes.c_void_p(s))
+    _check(rc)
 
 
 def eprop_profile_begin(ctx, max_launches: int):

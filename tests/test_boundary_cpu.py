@@ -120,3 +120,23 @@ def test_shape_past_the_forward_shared_memory_is_rejected():
     assert "shared memory" in eprop.eprop_last_error()
     ff = shape.replace(recurrent=0)
     assert eprop.eprop_workspace_bytes(eprop.make_config(ff)) > 0
+
+
+def test_static_entry_rejects_shapes_past_its_scratch_before_any_device_call():
+    # the bench workload needs ~3 GB of workspace, more than the static scratch
+    shape = synth.WORKLOADS["ralif_b128_n1024_t1000"]
+    cfg = eprop.make_config(shape)
+    assert eprop.eprop_workspace_bytes(cfg) > eprop.STATIC_SCRATCH_BYTES
+    lib = eprop.load_library()
+    w = (ctypes.c_void_p * 2)(256, 256)
+    g = (ctypes.c_void_p * 2)(256, 256)
+    rc = lib.eprop_sequence_static(ctypes.byref(cfg), w, ctypes.c_void_p(256), 10, ctypes.c_void_p(256),
+                                   None, g, None, None)
+    assert rc == eprop.EPROP_ENOSPACE
+    assert "static scratch" in eprop.eprop_last_error()
+    assert lib.eprop_sequence_static(ctypes.byref(cfg), w, None, 10, ctypes.c_void_p(256), None, g,
+                                     None, None) == eprop.EPROP_EINVAL
+    # the size the header states
+    hdr = open(HEADER).read()
+    assert "#define EPROP_STATIC_SCRATCH_BYTES (160u << 20)" in hdr
+    assert eprop.STATIC_SCRATCH_BYTES == 160 << 20
