@@ -197,7 +197,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     // splits that a workgroup walks at most about 26 batch elements (the row
     // tiles that share a coefficient chunk drift apart in L2 over longer
     // walks); at most 32, one per element, and 2 GiB of fp64 partials
-    const size_t tiles = (npp / eprop::kTile) * ((N + eprop::kTile - 1) / eprop::kTile);
+    const size_t tiles = (npp / eprop::kTileI) * ((N + eprop::kTileJ - 1) / eprop::kTileJ);
     L.acc_stride = npp * L.ldj;
     const size_t by_tiles = std::min<size_t>(8, (2048 + tiles - 1) / tiles);
     const size_t by_batch = (B + 25) / 26;
@@ -208,7 +208,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.accout = (double*)take(sizeof(double) * K * L.ldj);
     // traces tile by tile: all j tiles, and the tiles holding adaptive neurons
     const size_t ldc = round_up(N, eprop::kColPad);
-    const size_t lda_t = round_up(c.n_adaptive, eprop::kTile);
+    const size_t lda_t = round_up(c.n_adaptive, eprop::kTileJ);
     L.ebar = (float*)take(sizeof(float) * B * npp * ldc);
     L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * lda_t : 0);
     // with the reset path kept, the membrane eligibility per synapse as well
@@ -232,7 +232,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   const size_t npad4 = round_up(N, 4);
   size_t npre_max = 0;
   for (const Layer& L : plan->layers) npre_max = std::max<size_t>(npre_max, L.n_pre);
-  const size_t smem_base = sizeof(int) * (eprop::kFwdWaves * ((size_t)rwmax + (size_t)plan->jlist) +
+  const size_t smem_base = sizeof(int) * (eprop::kFwdWaves * ((size_t)rwmax + (size_t)c.n_layers * plan->jlist) +
                                           npre_max + 2 * eprop::kFwdWaves + 2) +
                            sizeof(float) * ((size_t)2 * c.n_layers * eprop::kFwdWaves * K + (size_t)c.n_layers * K +
                                             npre_total) +
@@ -468,7 +468,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ca.U = L.coefU[sl]; ca.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ca.H = L.coefH[sl];
     ca.S = L.coefS[sl];
     ca.B = c.batch; ca.n_post = c.n_rec; ca.n_adaptive = c.n_adaptive;
-    ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(c.n_adaptive, eprop::kTile));
+    ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(c.n_adaptive, eprop::kTileJ));
     ca.steps = steps; ca.kpad = kpad; ca.ldc = P.ldc;
     ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta; ca.alpha = c.alpha; ca.thr = c.thr;
     ca.W = L.coefW[sl]; ca.reset_through = c.reset_grad;
@@ -487,10 +487,10 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ta.U = L.coefU[sl]; ta.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
     ta.W = L.coefW[sl]; ta.reset_through = c.reset_grad;
     ta.S = L.coefS[sl];
-    ta.B = c.batch; ta.n_pre_pad = L.n_pre_pad; ta.n_post = c.n_rec; ta.ldj = L.ldj;
+    ta.B = c.batch; ta.n_pre = L.n_pre; ta.n_pre_pad = L.n_pre_pad; ta.n_post = c.n_rec; ta.ldj = L.ldj;
     ta.n_adaptive = c.n_adaptive; ta.ldi = L.n_pre_pad;
-    ta.n_jt = (c.n_rec + eprop::kTile - 1) / eprop::kTile;
-    ta.n_jt_a = (c.n_adaptive + eprop::kTile - 1) / eprop::kTile;
+    ta.n_jt = (c.n_rec + eprop::kTileJ - 1) / eprop::kTileJ;
+    ta.n_jt_a = (c.n_adaptive + eprop::kTileJ - 1) / eprop::kTileJ;
     ta.ldc = P.ldc; ta.kpad = kpad;
     ta.kappa_K = (float)std::pow((double)c.kappa, (double)steps);
     ta.first = first;

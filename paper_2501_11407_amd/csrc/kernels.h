@@ -7,10 +7,10 @@
 //   psiK   [Kmax*Bp][ldv]  pseudo-derivative (ldv = n_rec rounded to 256)
 //   deltaK [rows][ldk]     readout error (softmax - onehot)
 //   ztK    [rows][ldn]     kappa-filtered spikes
-//   p8     [B][Kmax/16][ldi][16] binary presynaptic vector, one byte per
-//                                step (0x3C, the high byte of fp16 1.0, or
-//                                0): a 16-byte record per row and 16-step
-//                                chunk
+//   p8     [B][Kmax/16][ldi/16][4][16][4] binary presynaptic vector, one
+//                                byte per step (0x3C, the high byte of fp16
+//                                1.0, or 0); per 16-step chunk and 16-row
+//                                group, the four 4-step quads of its rows
 //   zstart [B][ldi]              presynaptic filter at the block's start
 // Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
 // psiK) and the readout gradient dW_out += deltaK^T * ztK; then the block
@@ -30,9 +30,10 @@ constexpr int kFwdWaves = kFwdThreads / 64;
 constexpr int kFwdXSteps = 8;                  // steps of input spikes staged in shared memory
 constexpr int kXRegs = 2;                      // input words (or bytes) per thread prefetched per step
 constexpr int kBlockSteps = 256;       // timesteps per block (Kmax)
-constexpr int kTile = 64;              // eligibility workgroup tile: 64 (i) x 64 (j)
-constexpr int kRowPad = kTile;         // n_pre padded to the tile height (ldi)
-constexpr int kColPad = kTile;         // n_rec padded to the tile width (ldc)
+constexpr int kTileI = 256;            // eligibility workgroup tile: 256 (i) x 16 (j)
+constexpr int kTileJ = 16;
+constexpr int kRowPad = kTileI;        // n_pre padded to the tile height (ldi)
+constexpr int kColPad = kTileJ;        // n_rec padded to the tile width (ldc)
 
 struct FwdLayer {
   const float* Wt; int ldw;      // transposed drive weights [n_pre][ldw]
@@ -47,7 +48,7 @@ struct FwdLayer {
   float* y;                      // state [B][K_out]
   double* lossacc;               // [B]
   float* psiK;                   // [rows][ldj]
-  uint8_t* p8;                   // [B][Kmax/16][ldi][16]
+  uint8_t* p8;                   // [B][Kmax/16][ldi/16][4][16][4]
   float* zstart;                 // [B][ldi]
   float* deltaK; float* ztK;     // [rows][ldk], [rows][ldn]
   int n_inl, n_pre, rows_per_wave, ldi;
@@ -119,22 +120,22 @@ struct CoefArgs {
 hipError_t launch_coef(const CoefArgs& a, hipStream_t s);
 
 
-// The traces are stored tile by tile: for batch element b and 64 x 64 tile
-// (it, jt), 16 KiB holding the four 32 x 32 wave sub-tiles, each as four
-// 16 x 16 blocks (bj, bi) of 64 lanes x 4 floats, in the order the kernel's
-// lanes hold them (see trace_kernel).  epsa covers the n_jt_a tiles that hold
+// The traces are stored tile by tile: for batch element b and 256 x 16 tile
+// (it, jt), 16 KiB holding the four 64 x 16 wave sub-tiles, each as four
+// 16 x 16 blocks bi of 64 lanes x 4 floats, in the order the kernel's lanes
+// hold them (see trace_kernel).  epsa covers the n_jt_a tiles that hold
 // adaptive neurons.
 struct TraceArgs {
-  float* ebar;     // [B][n_pre_pad / 64][n_jt][64 * 64]
-  float* epsa;     // [B][n_pre_pad / 64][n_jt_a][64 * 64]
-  float* epsv;     // reset_through: [B][n_pre_pad / 64][n_jt][64 * 64]
+  float* ebar;     // [B][n_pre_pad / 256][n_jt][256 * 16]
+  float* epsa;     // [B][n_pre_pad / 256][n_jt_a][256 * 16]
+  float* epsv;     // reset_through: [B][n_pre_pad / 256][n_jt][256 * 16]
   double* acc;     // [n_split][n_pre_pad][ldj] (row-major)
   size_t acc_stride;
-  const uint8_t* p8;                  // [B][kKC][ldi][16], ldi = n_pre_pad
+  const uint8_t* p8;                  // [B][kKC][ldi/16][4][16][4], ldi = n_pre_pad
   const float* zstart;                // [B][ldi] (reset-stopped form only)
   const uint32_t* U; const uint32_t* V; const uint32_t* H; const uint32_t* W;
   const float* S;                     // as CoefArgs
-  int B, n_pre_pad, n_post, ldj, n_adaptive, ldi, ldc, kpad, n_split;
+  int B, n_pre, n_pre_pad, n_post, ldj, n_adaptive, ldi, ldc, kpad, n_split;
   int n_jt, n_jt_a;   // tiles along j: all, and those holding adaptive neurons
   float kappa_K;   // kappa^steps
   int first;       // 1: traces and accumulators start at zero (not read)

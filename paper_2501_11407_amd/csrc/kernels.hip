@@ -165,11 +165,56 @@ __device__ __forceinline__ float softmax_lanes(const FwdArgs& A, const float* pa
   return ex / se - ((lane == label) ? 1.0f : 0.0f);
 }
 
+// Readout partial sums of the spikes of one step in one wave, K_out <= 64
+// (lane k: class k): the rows of the transposed readout weights of the
+// wave's spiking neurons (their list in spk), up to kReadoutRows loaded
+// together, added in list order.
+constexpr int kReadoutRows = 8;
+struct ReadoutRows {
+  float wv[kReadoutRows];
+  int n;
+};
+__device__ __forceinline__ void readout_issue(const FwdArgs& A, const float* WoutT, const int* spk,
+                                              int n_spk, ReadoutRows& R) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t koff = (uint32_t)min(lane, A.K_out - 1) * 4u;
+  R.n = min(n_spk, kReadoutRows);
+  const int ent = spk[min(lane & (kReadoutRows - 1), max(n_spk - 1, 0))];
+#pragma unroll
+  for (int u = 0; u < kReadoutRows; ++u) {
+    const int j = __builtin_amdgcn_readlane(ent, u);
+    R.wv[u] = u < R.n ? *(const float*)((const char*)(WoutT + (size_t)j * A.ldk) + koff) : 0.0f;
+  }
+}
+__device__ __forceinline__ float readout_sum(const FwdArgs& A, const float* WoutT, const int* spk,
+                                             int n_spk, const ReadoutRows& R) {
+  const int lane = threadIdx.x & (kWave - 1);
+  float Y = 0.0f;
+#pragma unroll
+  for (int u = 0; u < kReadoutRows; ++u)
+    if (u < R.n) Y += R.wv[u];
+  // more spikes in the wave (rare): the rest in further rounds
+  const uint32_t koff = (uint32_t)min(lane, A.K_out - 1) * 4u;
+  for (int s0 = kReadoutRows; s0 < n_spk; s0 += 16) {
+    const int ent = spk[min(s0 + (lane & 15), n_spk - 1)];
+    float wv[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int j = __builtin_amdgcn_readlane(ent, u);
+      wv[u] = *(const float*)((const char*)(WoutT + (size_t)j * A.ldk) + koff);
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (s0 + u < n_spk) Y += wv[u];
+  }
+  return Y;
+}
+
 template <int QN, int LI>
 __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLds& S, int t, int b,
                                                    int cur, float (&v)[QN], float (&ad)[QN],
                                                    float (&zt)[QN], double& loss, int label,
-                                                   float& yk, float& dk) {
+                                                   float& yk, float& dk, int& nspk_prev) {
   const FwdLayer& Ly = A.L[LI];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
@@ -183,16 +228,18 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   float* szb = S.szb + (LI == 0 ? 0 : A.L[0].n_pre);
   uint8_t* zring = S.zb + (LI == 0 ? 0 : A.L[0].n_pre) * A.zgroup;
   float* sy = S.sy + LI * A.K_out;
+  int* spk = S.spk + LI * kFwdWaves * A.jlist + w * A.jlist;   // this wave's spike list
   const size_t row = (size_t)t * A.Bp + b;
-  // readout partial sums of this step and of the step before (by parity)
+  // readout partial sums by step parity
   float* part = S.part + (LI * 2 + (t & 1)) * kFwdWaves * A.K_out;
-  const float* part_prev = S.part + (LI * 2 + ((t + 1) & 1)) * kFwdWaves * A.K_out;
-  // K_out <= 64: the last wave, which holds the fewest presynaptic rows,
-  // takes the previous step's softmax while the others build their lists,
-  // and stores delta with this step's stores; the block's last step is
+  // K_out <= 64: the readout of a step's spikes is loaded together with the
+  // next step's drive (its partial sums go to part of that step's parity),
+  // and the last wave, which holds the fewest presynaptic rows, takes the
+  // softmax of the step two back while the others build their lists, and
+  // stores delta with this step's stores; the block's last two steps are
   // finished after the step loop
   const bool defer = A.K_out <= kWave;
-  if (defer && w == kSoftWave && t > 0) dk = softmax_lanes(A, part_prev, yk, label, loss);
+  if (defer && w == kSoftWave && t > 1) dk = softmax_lanes(A, part, yk, label, loss);
 
   // 1. presynaptic vector, its filter, ordered active lists
   const int rw = Ly.rows_per_wave;
@@ -254,6 +301,9 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       }
     }
   }
+  // the readout rows of the previous step's spikes, loaded with the drive rows
+  ReadoutRows rr;
+  if (defer) readout_issue(A, Ly.WoutT, spk, nspk_prev, rr);
   const uint32_t tidoff = (uint32_t)tid * 4u;
   float I[QN];
 #pragma unroll
@@ -323,6 +373,11 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       }
     }
   }
+  if (defer && t > 0) {
+    const float Y = readout_sum(A, Ly.WoutT, spk, nspk_prev, rr);
+    float* part_prev = S.part + (LI * 2 + ((t - 1) & 1)) * kFwdWaves * A.K_out;
+    if (lane < A.K_out) part_prev[w * A.K_out + lane] = Y;
+  }
   int n_spk = 0;
   float psv[QN];
   unsigned long long smask[QN];
@@ -354,18 +409,19 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     }
     const unsigned long long m = __ballot(z);
     smask[q] = m;
-    if (z) S.spk[w * A.jlist + n_spk + lanes_below(m, lane)] = j;
+    if (z) spk[n_spk + lanes_below(m, lane)] = j;
     n_spk += __popcll(m);
   }
+  nspk_prev = n_spk;
 
-  // 3. this wave's share of the readout: rows of the transposed readout
-  // weights of its spiking neurons, read coalesced over the classes
-  for (int kb = 0; kb < A.K_out; kb += kWave) {
+  // 3. (K_out > 64) this wave's share of the readout: rows of the transposed
+  // readout weights of its spiking neurons, read coalesced over the classes
+  for (int kb = 0; !defer && kb < A.K_out; kb += kWave) {
     const int k = kb + lane;
     const uint32_t koff = (uint32_t)min(k, A.K_out - 1) * 4u;
     float Y = 0.0f;
     for (int s0 = 0; s0 < n_spk; s0 += 16) {
-      const int ent = S.spk[w * A.jlist + min(s0 + (lane & 15), n_spk - 1)];
+      const int ent = spk[min(s0 + (lane & 15), n_spk - 1)];
       float wv[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
@@ -387,32 +443,29 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   for (int q = 0; q < QN; ++q) {
     const int j = q * kFwdThreads + tid;
     if (j < A.n_rec) {
-      Ly.psiK[row * A.ldj + j] = psv[q];
-      Ly.ztK[row * A.ldn + j] = zt[q];
+      __builtin_nontemporal_store(psv[q], Ly.psiK + row * A.ldj + j);
+      __builtin_nontemporal_store(zt[q], Ly.ztK + row * A.ldn + j);
     }
     if (A.spikes) {
       const int w0 = (q * kFwdThreads + w * kWave) >> 5;
       uint32_t* srow = A.spikes + (((size_t)t * A.n_layers + LI) * A.B + b) * A.W32;
-      if (lane == 0 && w0 < A.W32) srow[w0] = (uint32_t)smask[q];
-      if (lane == 1 && w0 + 1 < A.W32) srow[w0 + 1] = (uint32_t)(smask[q] >> 32);
+      if (lane == 0 && w0 < A.W32) __builtin_nontemporal_store((uint32_t)smask[q], srow + w0);
+      if (lane == 1 && w0 + 1 < A.W32) __builtin_nontemporal_store((uint32_t)(smask[q] >> 32), srow + w0 + 1);
     }
   }
-  if (defer && w == kSoftWave && t > 0 && lane < A.K_out)
-    Ly.deltaK[(row - A.Bp) * A.ldk + lane] = dk;
-  // the p bytes go out zgroup steps at a time into the row's 16-byte record
-  // of the chunk (bytes past the block's last step are ignored downstream)
+  if (defer && w == kSoftWave && t > 1 && lane < A.K_out)
+    __builtin_nontemporal_store(dk, Ly.deltaK + (row - 2 * A.Bp) * A.ldk + lane);
+  // the p bytes go out zgroup steps at a time, as 4-step quads into the
+  // chunk's [16-row group][quad][row][4] layout (bytes past the block's last
+  // step are ignored downstream)
   if ((t & (A.zgroup - 1)) == A.zgroup - 1 || t == A.steps - 1) {
-    uint8_t* zpk = Ly.p8 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * 16 +
-                   ((t & (kChunk - 1)) & ~(A.zgroup - 1));
+    uint8_t* cb = Ly.p8 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * 16;
+    const int q0 = ((t & (kChunk - 1)) & ~(A.zgroup - 1)) >> 2;
     for (int i = i_beg + lane; i < i_end; i += kWave) {
-      uint8_t* d = zpk + (size_t)i * 16;
-      const uint8_t* src = zring + i * A.zgroup;
-      if (A.zgroup == 16)
-        *(u32x4*)d = *(const u32x4*)src;
-      else if (A.zgroup == 8)
-        *(uint2*)d = *(const uint2*)src;
-      else
-        *(uint32_t*)d = *(const uint32_t*)src;
+      uint8_t* d = cb + (size_t)(i >> 4) * 256 + (i & 15) * 4;
+      const uint32_t* src = (const uint32_t*)(zring + i * A.zgroup);
+      for (int q = 0; q < (A.zgroup >> 2); ++q)
+        __builtin_nontemporal_store(src[q], (uint32_t*)(d + (q0 + q) * 64));
     }
   }
   lds_barrier();
@@ -483,8 +536,12 @@ __device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S,
   }
 }
 
+// Four waves per SIMD (128 registers) for one layer of at most two neurons
+// per thread; three (168) for two layers or four neurons per thread and
+// more, so that those do not spill up to four.  Either way an eligibility
+// workgroup fits beside the forward on its compute unit.
 template <int QN, int NL>
-__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))) void forward_kernel(FwdArgs A) {
+__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu((QN >= 4 || NL > 1) ? 3 : 4))) void forward_kernel(FwdArgs A) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   // the forward is the sequential part of the step: its waves win instruction
   // issue over the eligibility waves that share their compute units
@@ -497,8 +554,8 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
   const int npre_max = max(A.L[0].n_pre, NL > 1 ? A.L[1].n_pre : 0);
   S.act = (int*)smem;                          // [waves][rwmax]
   S.mrg = S.act + kFwdWaves * S.rwmax;         // [npre_max]
-  S.spk = S.mrg + npre_max;                    // [waves][jlist]
-  S.cnt = S.spk + kFwdWaves * A.jlist;         // [2 * waves + 2]
+  S.spk = S.mrg + npre_max;                    // [n_layers][waves][jlist]
+  S.cnt = S.spk + NL * kFwdWaves * A.jlist;    // [2 * waves + 2]
   S.part = (float*)(S.cnt + 2 * kFwdWaves + 2);   // [n_layers][2][waves][K_out]
   S.sy = S.part + NL * 2 * kFwdWaves * A.K_out;   // [n_layers][K_out]
   S.szb = S.sy + NL * A.K_out;                 // [n_pre_0 + n_pre_1]
@@ -533,27 +590,43 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(4))
     for (int i = threadIdx.x; i < A.n_in; i += kFwdThreads) S.xs[tt * A.n_in + i] = xrow[i];
   }
   lds_barrier();
+  int ns0 = 0, ns1 = 0;   // spikes of the previous step in this wave, per layer
   for (int t = 0; t < A.steps; ++t) {
-    forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0, label, y0, d0);
+    forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0, label, y0, d0, ns0);
     if constexpr (NL > 1)
-      forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1, label, y1, d1);
+      forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1, label, y1, d1, ns1);
     cur ^= 1;
   }
-  if (A.K_out <= kWave && (threadIdx.x >> 6) == kSoftWave && A.steps > 0) {
-    // the last step's softmax (its partial sums are visible: every step ends
-    // with a barrier)
+  if (A.K_out <= kWave && A.steps > 0) {
+    // the readout of the last step's spikes, then the softmax of the last
+    // two steps (every step ends with a barrier, so the partial sums of the
+    // step before the last are visible)
     const int tl = A.steps - 1;
-    const size_t row = (size_t)tl * A.Bp + b;
-    d0 = softmax_lanes(A, S.part + (tl & 1) * kFwdWaves * A.K_out, y0, label, loss0);
-    if (lane < A.K_out) {
-      A.L[0].deltaK[row * A.ldk + lane] = d0;
-      S.sy[lane] = y0;
-    }
-    if constexpr (NL > 1) {
-      d1 = softmax_lanes(A, S.part + (2 + (tl & 1)) * kFwdWaves * A.K_out, y1, label, loss1);
+    const int w = threadIdx.x >> 6;
+    auto last_readout = [&](int li, int ns) {
+      const float* WoutT = li == 0 ? A.L[0].WoutT : A.L[1].WoutT;
+      const int* spk = S.spk + li * kFwdWaves * A.jlist + w * A.jlist;
+      ReadoutRows rr;
+      readout_issue(A, WoutT, spk, ns, rr);
+      const float Y = readout_sum(A, WoutT, spk, ns, rr);
+      if (lane < A.K_out) S.part[((li * 2 + (tl & 1)) * kFwdWaves + w) * A.K_out + lane] = Y;
+    };
+    last_readout(0, ns0);
+    if constexpr (NL > 1) last_readout(1, ns1);
+    lds_barrier();
+    if (w == kSoftWave) {
+      for (int ts = max(tl - 1, 0); ts <= tl; ++ts) {
+        const size_t row = (size_t)ts * A.Bp + b;
+        d0 = softmax_lanes(A, S.part + (ts & 1) * kFwdWaves * A.K_out, y0, label, loss0);
+        if (lane < A.K_out) __builtin_nontemporal_store(d0, A.L[0].deltaK + row * A.ldk + lane);
+        if constexpr (NL > 1) {
+          d1 = softmax_lanes(A, S.part + (2 + (ts & 1)) * kFwdWaves * A.K_out, y1, label, loss1);
+          if (lane < A.K_out) __builtin_nontemporal_store(d1, A.L[1].deltaK + row * A.ldk + lane);
+        }
+      }
       if (lane < A.K_out) {
-        A.L[1].deltaK[row * A.ldk + lane] = d1;
-        S.sy[A.K_out + lane] = y1;
+        S.sy[lane] = y0;
+        if constexpr (NL > 1) S.sy[A.K_out + lane] = y1;
       }
     }
   }
@@ -913,33 +986,40 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
   for (int k = 0; k < 13; ++k) a.S[k * plane + so] = s16[k];
 }
 
-// A workgroup of 4 waves owns a 64 (i) x 64 (j) tile of synapses and one
-// split of the batch; wave w computes the 32 x 32 sub-tile (w / 2, w % 2).
+// A workgroup of 4 waves owns a 256 (i) x 16 (j) tile of synapses and one
+// split of the batch; wave w computes the 64 x 16 sub-tile of rows
+// 64 w .. 64 w + 63.  Tall tiles let one shared-memory copy of a chunk of
+// coefficient rows (which depend on j) serve 256 presynaptic rows, and all
+// four waves read the same coefficient operand.
 // For each batch element b of the split:
 //  * MFMA contractions C_U, C_V, C_H = coef_b[j][s] x p_b[i][s] over the
-//    block's steps (v_mfma_f32_16x16x32_f16 on the scaled fp16 pairs, 2x2
-//    blocks of 16x16 per wave), 16 steps ("a chunk") at a time, operands
-//    read from shared memory;
+//    block's steps (v_mfma_f32_16x16x32_f16 on the scaled fp16 pairs, four
+//    16x16 blocks per wave stacked along i), 16 steps ("a chunk") at a time,
+//    operands read from shared memory;
 //  * then the elementwise update of the traces, each read once and written
 //    once (1 KiB contiguous per wave instruction), and of the gradient.
 // Operands stream through a ring of kRing chunk slots in shared memory:
-// p_b rows i and U, H (and V) rows j of the chunk's 16 steps are copied by
-// direct global-to-LDS loads (16 bytes per lane, no registers) up to
-// kRing - 1 chunks ahead of the chunk being contracted, across batch elements.  The
-// block-start traces of a batch element (registers) and its scalars
-// (shared memory, double-buffered; with the block-start filter of the
+// the p_b bytes of the tile's 256 rows (one contiguous 4 KiB run, a wave
+// copies its own 64 rows) and the U, H (and V, W) rows of its 16 columns
+// (one contiguous 1 KiB run each, copied by waves 0, 1 (2, 3)) of the
+// chunk's 16 steps are copied by direct buffer-to-LDS loads (16 bytes per
+// lane, no registers, the chunk's position in a scalar offset) up to
+// kRing - 1 chunks ahead of the chunk being contracted, across batch
+// elements.  The block-start traces of a batch element (registers) and its
+// scalars (shared memory, double-buffered; with the block-start filter of the
 // tile's rows) travel with its first chunk.
 // Waits: copies and loads complete in order, so a chunk's copies are waited
 // for with an exact vmcnt; trace stores (which may complete out of order with
-// respect to loads) are drained once per batch element, at its first chunk.
+// respect to loads) are drained once per batch element, at its second chunk.
 // The workgroup barrier carries no memory fence (a fence would drain every
 // copy in flight); shared-memory hazards are ordered by the waits and the
 // barrier alone.
-// Lane (r, g) of block (bj, bi) holds the 4 columns j = jw + 16 bj + 4 g ..+3
-// of row i = iw + 16 bi + r; the traces of a wave sub-tile are stored in
-// exactly this order (block (bj, bi) at (2 bj + bi) KiB, lane l at 16 l
-// bytes).  The gradient of the batch elements of one launch is summed in
-// fp32 per lane and added to the split's fp64 accumulator at the end.
+// Lane (r, g) of block bi holds the 4 columns j = j0 + 4 g ..+3 of row
+// i = i0 + 64 w + 16 bi + r; the traces of a wave sub-tile are stored in
+// exactly this order (block bi at bi KiB, lane l at 16 l bytes).  A wave whose
+// 64 rows are all padding (past n_pre) reads and writes no traces.  The
+// gradient of the batch elements of one launch is summed in fp32 per lane and
+// added to the split's fp64 accumulator at the end.
 // Buffer access: a wave-uniform base with a byte range (accesses outside it
 // read zero and write nothing) and a 32-bit per-lane byte offset.  The trace
 // streams use the non-temporal cache policy (bit 1 of the policy operand):
@@ -956,10 +1036,12 @@ __device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, uint32_t off, f
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, kNonTemporal);
 }
 
-constexpr int kRing = 4;                              // chunk slots (reset-stopped)
-constexpr int kOpBytes = kTile * 64;                  // one operand of a chunk: 64 rows x 64 B
-constexpr int kPBytes = kTile * 16;                   // the chunk's p bytes: 64 rows x 16 B
-constexpr uint32_t kSubTileBytes = 32 * 32 * 4;
+constexpr int kRing = 4;                              // chunk slots
+constexpr int kOpBytes = kTileJ * 64;                 // one coefficient operand of a chunk: 16 rows x 64 B
+constexpr int kPBytes = kTileI * 16;                  // the chunk's p records: 256 rows x 16 B
+constexpr int kWaveRows = kTileI / 4;                 // rows of a wave sub-tile
+constexpr uint32_t kSubTileBytes = kWaveRows * kTileJ * 4;   // a wave's traces of one array (4 KiB)
+constexpr int kScalWave = 256;                        // floats of one wave's scalar copy (64 lanes x 16 B)
 
 // s_waitcnt immediate that waits for vmcnt <= n only (gfx9 encoding)
 constexpr int vm_wait(int n) { return (n & 0xF) | ((n >> 4) << 14) | 0x70 | 0xF00; }
@@ -978,12 +1060,14 @@ __device__ __forceinline__ void for_each_index(F&& f, std::integer_sequence<int,
 
 typedef __attribute__((address_space(3))) void lds_void;
 // Lane l copies 16 bytes from its own address g to lds + 16 l.
-__device__ __forceinline__ void dma16(const float* g, float* lds) {
+__device__ __forceinline__ void dma16(const void* g, void* lds) {
   __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
 }
-// Lane l copies 4 bytes from its own address g to lds + 4 l.
-__device__ __forceinline__ void dma4(const float* g, float* lds) {
-  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 4, 0, 0);
+// Lane l copies 16 bytes at byte voff + soff of the buffer r to lds + 16 l
+// (soff: a wave-uniform offset, so stepping through chunks costs no vector
+// instructions).
+__device__ __forceinline__ void dma16b(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, void* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds, 16, voff, soff, 0, 0);
 }
 
 // RT = false: the reset-stopped recursion (contractions U', H' and, for
@@ -991,113 +1075,113 @@ __device__ __forceinline__ void dma4(const float* g, float* lds) {
 // true: the reset path kept (coef_rt_kernel): contractions U = C_E, H = C_g,
 // W = C_V and V = C_A; traces ebar, epsv and epsa.  Either way the
 // presynaptic operand is the binary p, exact in fp16, so each contraction
-// takes one MFMA pass.  With the p bytes (1 KiB per chunk) even the four
-// coefficient operands of RT fit a ring of four chunks twice per compute unit.
+// takes one MFMA pass.
 template <bool ALIF, int NCH, bool RT>
 struct TraceTile {
   static constexpr int RING = kRing;                          // chunk slots
   static constexpr int PREF = RING - 1;                       // chunks copied ahead
-  // a slot: the chunk's p bytes (64 rows x 16 B), then the coefficient
-  // operands U, H, V (and W) of 64 rows x 64 B each
-  static constexpr int NOP = RT ? 4 : 3;                      // coefficient operands
-  static constexpr int SLOT = (kPBytes + NOP * kOpBytes) / 4; // floats per slot
+  // a slot: the chunk's p records (256 rows x 16 B), then the coefficient
+  // operands U, H, V (and W) of 16 rows x 64 B each (V's place is kept in
+  // tiles without adaptive neurons)
+  static constexpr int NOPS = RT ? 4 : 3;
+  static constexpr int SLOT = (kPBytes + NOPS * kOpBytes) / 4;   // floats per slot
   static constexpr int PLANES = RT ? kScalarPlanesRT : kScalarPlanes;
-  // floats of one scalar buffer: the planes, and for the reset-stopped form
-  // the block-start filter of the tile's 64 rows after them
-  static constexpr int SCAL = (PLANES + (RT ? 0 : 1)) * kTile;
+  static constexpr int PPW = PLANES / 4;                      // planes copied per wave
+  // one scalar buffer: per wave kScalWave floats = its PPW planes of the 16
+  // columns, then (reset-stopped form) the block-start filter of its 64 rows
+  static constexpr int SCAL = 4 * kScalWave;
+  static constexpr int ZOFF = 64;                             // filter offset in a wave's part
+  static_assert(PPW * kTileJ <= ZOFF, "planes overlap the filter");
   static constexpr size_t SMEM = sizeof(float) * (RING * SLOT + 2 * SCAL);
   // chunks in flight ahead; fewer than NCH so that a batch element's copies
   // never reach past the next element's first chunk
   static constexpr int D = NCH == 1 ? 1 : (NCH - 1 < PREF ? NCH - 1 : PREF);
-  static constexpr int Q = 3 + (ALIF ? 1 : 0) + (RT ? 1 : 0);   // copies per wave per chunk
-  static constexpr int SC = PLANES / 4;                         // scalar copies per wave
+  // Copies per wave per chunk: its p rows, and one coefficient operand for
+  // the copying waves (wave X copies operand X: U, H, and V / W when present).
+  static constexpr bool has_op(int X) { return X < 2 || (X == 2 && ALIF) || (X == 3 && RT); }
+  static constexpr int SC = 1;                                  // scalar copies per wave
   static constexpr int EA = 4 * (1 + (ALIF ? 1 : 0) + (RT ? 1 : 0));   // trace loads per element
-  static constexpr int ops(int c) { return Q + (c == 0 ? SC : 0); }     // + scalars with chunk 0
+  static constexpr int ops(int c, bool cp) { return 1 + (cp ? 1 : 0) + (c == 0 ? SC : 0); }
   // Loads issued after those of chunk ch when it is waited for: the copies
   // of chunks ch+1 .. ch+D-1 (past the end of the batch element: the next
   // element's, if there is one), and the element's trace loads when they
   // were issued in between (at chunk 0, after that chunk's copies).  Loads
   // complete in order, so at most that many outstanding operations means
   // chunk ch has landed, whatever stores are still in flight.
-  static constexpr int pending(int ch, bool next) {
+  static constexpr int pending(int ch, bool next, bool cp) {
     int n = (ch >= 1 && ch <= D) ? EA : 0;
-    for (int m = ch + 1; m <= ch + D - 1; ++m) n += m < NCH ? ops(m) : (next ? ops(m - NCH) : 0);
+    for (int m = ch + 1; m <= ch + D - 1; ++m)
+      n += m < NCH ? ops(m, cp) : (next ? ops(m - NCH, cp) : 0);
     return n;
   }
-  static_assert(pending(1, true) <= 63, "vmcnt range");
+  static_assert(pending(1, true, true) <= 63, "vmcnt range");
 
   const TraceArgs& a;
   float* sm;
-  int i0, j0, it, jt, split, lane, r, g, w, wi, wj;
-  bool first;
+  int i0, j0, it, jt, split, lane, r, g, w;
+  bool first, live, copier;
+  uint32_t pvoff, cvoff;          // this lane's byte offsets in the p and coefficient copies
 
   __device__ __forceinline__ TraceTile(const TraceArgs& a_, float* sm_, int it_, int jt_, int split_,
                                        bool first_)
-      : a(a_), sm(sm_), i0(it_ * kTile), j0(jt_ * kTile), it(it_), jt(jt_), split(split_),
+      : a(a_), sm(sm_), i0(it_ * kTileI), j0(jt_ * kTileJ), it(it_), jt(jt_), split(split_),
         first(first_) {
     lane = threadIdx.x & 63;
     r = lane & 15;
     g = lane >> 4;
     w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index, uniform
-    wi = w >> 1;
-    wj = w & 1;
+    live = i0 + kWaveRows * w < a.n_pre;                    // the wave holds a real row
+    copier = (w < 2) || (w == 2 && ALIF) || (w == 3 && RT);
+    // p: the records of rows i0 + 64 w .. +63 are one contiguous 1 KiB run;
+    // coefficients: lane l takes row l / 4 of the 16 columns, 16-byte unit
+    // (l % 4) ^ ((row / 2) % 4) (see issue)
+    pvoff = (uint32_t)(i0 + kWaveRows * w) * 16u + (uint32_t)lane * 16u;
+    const int row = lane >> 2;
+    cvoff = (uint32_t)(j0 + row) * 64u + (uint32_t)((lane & 3) ^ ((row >> 1) & 3)) * 16u;
   }
 
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const float* base, int n_t, int b,
-                                                             uint32_t bytes = kSubTileBytes) const {
-    const size_t t = ((size_t)b * (a.n_pre_pad / kTile) + it) * n_t + jt;
-    return make_rsrc((const char*)base + (t * 4 + w) * kSubTileBytes, bytes);
+                                                             uint32_t bytes) const {
+    const size_t t = ((size_t)b * (a.n_pre_pad / kTileI) + it) * n_t + jt;
+    return make_rsrc((const char*)base + (t * 4 + w) * kSubTileBytes, live ? bytes : 0u);
   }
-  __device__ __forceinline__ __amdgpu_buffer_rsrc_t ebar_rsrc(int b) const { return tile_rsrc(a.ebar, a.n_jt, b); }
-  __device__ __forceinline__ __amdgpu_buffer_rsrc_t epsa_rsrc(int b) const { return tile_rsrc(a.epsa, a.n_jt_a, b); }
-  __device__ __forceinline__ __amdgpu_buffer_rsrc_t epsv_rsrc(int b) const { return tile_rsrc(a.epsv, a.n_jt, b); }
 
-  // Copies of chunk c of batch element b into ring slot sl.  Wave w copies
-  // rows 16w .. 16w+15 of each operand (1 KiB: lane l takes 16 bytes of row
-  // 16w + l/4); within a row the four 16-byte units are stored in the order
-  // u ^ ((row / 2) % 4), which keeps the MFMA operand reads free of bank
-  // conflicts.  With chunk 0 also the scalars (planes w, w + 4, ...) into
-  // scalar buffer par.
-  // The copies are issued in two parts (P = 0: z and U; P = 1: H, V, W and
-  // the scalars), placed between MFMAs so that the vector-memory path works
-  // while the matrix cores do; the order of all copies is that of the full
-  // issue.
+  // Copies of chunk c of batch element b into ring slot sl: wave w copies
+  // the p bytes of its 64 rows (stored by the forward as [16-row group][step
+  // quad][row][4 steps], so that the operand reads below are free of bank
+  // conflicts), and wave X the 16 rows of coefficient operand X (lane l: row
+  // l / 4, its 16-byte unit u = (l % 4) ^ ((row / 2) % 4) stored at position
+  // l % 4, which keeps the MFMA operand reads free of bank conflicts).  With
+  // chunk 0 also the scalars (planes PPW w .. PPW w + PPW - 1 of the 16
+  // columns, and the block-start filter of the wave's rows) into scalar
+  // buffer par.  The copies are issued in two parts (P = 0: p; P = 1: the
+  // coefficient operand and the scalars), placed between MFMAs so that the
+  // vector-memory path works while the matrix cores do; the order of all
+  // copies is that of the full issue.
   template <int P>
   __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
     char* slot = (char*)(sm + sl * SLOT);
-    const int ln = lane;
-    const int rw = 16 * w + (ln >> 2);
-    const uint32_t q = (uint32_t)((ln & 3) ^ ((ln >> 3) & 3));
-    const uint32_t unit = q * 16u;
-    const size_t cc = ((size_t)b * kKC + c) * a.ldc + j0 + rw;
-    float* dst = (float*)(slot + kPBytes + w * 1024);
     if constexpr (P == 0) {
-      // p of rows 16w .. 16w+15: lane l takes the 4 bytes of steps 4g..4g+3
-      // (g = l / 16) of row 16w + l % 16, stored at dword 16 g + l % 16 of
-      // the group, so the operand reads of a half-wave hit 32 banks
-      const size_t zr = ((size_t)b * kKC + c) * a.ldi + i0 + 16 * w + (ln & 15);
-      dma4((const float*)(a.p8 + zr * 16 + (ln >> 4) * 4), (float*)(slot + w * 256));
-      dma16((const float*)((const char*)a.U + cc * 64 + unit), dst);
+      const uint32_t estride = (uint32_t)(kKC * a.ldi * 16);         // bytes of one element
+      const auto pr = make_rsrc(a.p8 + (size_t)b * estride, estride);
+      dma16b(pr, pvoff, (uint32_t)(c * a.ldi * 16), slot + kWaveRows * w * 16);
     } else {
-      dma16((const float*)((const char*)a.H + cc * 64 + unit), dst + kOpBytes / 4);
-      if constexpr (ALIF)
-        dma16((const float*)((const char*)a.V + cc * 64 + unit), dst + 2 * kOpBytes / 4);
-      if constexpr (RT)
-        dma16((const float*)((const char*)a.W + cc * 64 + unit), dst + 3 * kOpBytes / 4);
+      if (copier) {
+        const uint32_t estride = (uint32_t)(kKC * a.ldc * 64);       // bytes of one element
+        const uint32_t* X = w == 0 ? a.U : w == 1 ? a.H : w == 2 ? a.V : a.W;
+        const auto cr = make_rsrc((const char*)X + (size_t)b * estride, estride);
+        dma16b(cr, cvoff, (uint32_t)(c * a.ldc * 64), slot + kPBytes + w * kOpBytes);
+      }
       if (c == 0) {
-        float* sb = sm + RING * SLOT + par * SCAL;
-#pragma unroll
-        for (int m = 0; m < SC; ++m) {
-          const int pl = w + 4 * m;
-          // lanes 0-15: plane pl; with the last plane of the reset-stopped
-          // form, lanes 16-31 copy the filter at the block's start of the
-          // tile's 64 rows i into the place after it
-          const bool zs = !RT && pl == PLANES - 1;
-          if (lane < 16 || (zs && lane < 32)) {
-            const float* src = lane < 16 ? a.S + ((size_t)pl * a.B + b) * a.ldc + j0 + lane * 4
-                                         : a.zstart + (size_t)b * a.ldi + i0 + (lane - 16) * 4;
-            dma16(src, sb + pl * kTile);
-          }
+        float* sb = sm + RING * SLOT + par * SCAL + w * kScalWave;
+        // lanes 0 .. 4 PPW - 1: plane PPW w + l / 4, columns 4 (l % 4) .. +3;
+        // lanes 16-31 (reset-stopped form): the filter of rows 64 w + 4 (l - 16) .. +3
+        const bool zs = !RT && lane >= 16 && lane < 32;
+        if (lane < 4 * PPW || zs) {
+          const float* src = lane < 16
+              ? a.S + ((size_t)(PPW * w + (lane >> 2)) * a.B + b) * a.ldc + j0 + (lane & 3) * 4
+              : a.zstart + (size_t)b * a.ldi + i0 + kWaveRows * w + (lane - 16) * 4;
+          dma16(src, sb);
         }
       }
     }
@@ -1108,113 +1192,112 @@ struct TraceTile {
   }
 
   // block-start traces of batch element b into E, A (and Vm).  In the first
-  // block after a reset they are zero: the loads then get an empty range, so
-  // they read zero without touching memory and still count as issued loads
-  // (the waits above count them).
-  __device__ __forceinline__ void load_traces(int b, f32x4 (&E)[2][2], f32x4 (&A)[2][2],
-                                              f32x4 (&Vm)[2][2]) const {
+  // block after a reset (and for a wave of padding rows) they are zero: the
+  // loads then get an empty range, so they read zero without touching memory
+  // and still count as issued loads (the waits above count them).
+  __device__ __forceinline__ void load_traces(int b, f32x4 (&E)[4], f32x4 (&A)[4], f32x4 (&Vm)[4]) const {
     const uint32_t range = first ? 0u : kSubTileBytes;
     const auto eR = tile_rsrc(a.ebar, a.n_jt, b, range);
 #pragma unroll
-    for (int x = 0; x < 4; ++x) E[x >> 1][x & 1] = bload(eR, x * 1024u + lane * 16u);
+    for (int x = 0; x < 4; ++x) E[x] = bload(eR, x * 1024u + lane * 16u);
     if constexpr (ALIF) {
       const auto aR = tile_rsrc(a.epsa, a.n_jt_a, b, range);
 #pragma unroll
-      for (int x = 0; x < 4; ++x) A[x >> 1][x & 1] = bload(aR, x * 1024u + lane * 16u);
+      for (int x = 0; x < 4; ++x) A[x] = bload(aR, x * 1024u + lane * 16u);
     }
     if constexpr (RT) {
       const auto vR = tile_rsrc(a.epsv, a.n_jt, b, range);
 #pragma unroll
-      for (int x = 0; x < 4; ++x) Vm[x >> 1][x & 1] = bload(vR, x * 1024u + lane * 16u);
+      for (int x = 0; x < 4; ++x) Vm[x] = bload(vR, x * 1024u + lane * 16u);
     }
   }
 
   // traces and gradient of the k-th batch element from its contractions
   // (accumulated in the scaled units of the fp16 pairs)
-  __device__ __forceinline__ void finish(int k, const f32x4 (&E)[2][2], const f32x4 (&A)[2][2],
-                                         const f32x4 (&Vm)[2][2], const f32x4 (&cU)[2][2],
-                                         const f32x4 (&cV)[2][2], const f32x4 (&cH)[2][2],
-                                         const f32x4 (&cW)[2][2], f32x4 (&gacc)[2][2]) const {
+  __device__ __forceinline__ void finish(int k, const f32x4 (&E)[4], const f32x4 (&A)[4],
+                                         const f32x4 (&Vm)[4], const f32x4 (&cU)[4],
+                                         const f32x4 (&cV)[4], const f32x4 (&cH)[4],
+                                         const f32x4 (&cW)[4], f32x4 (&gacc)[4]) const {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     const int b = split + k * a.n_split;
     const float* st = sm + RING * SLOT + (k & 1) * SCAL;
-    const auto eR = ebar_rsrc(b);
-    const auto aR = ALIF ? epsa_rsrc(b) : eR;
-    const auto vR = RT ? epsv_rsrc(b) : eR;
-    auto plane = [&](int p, int cj) { return *(const f32x4*)(st + p * kTile + cj); };
+    const auto eR = tile_rsrc(a.ebar, a.n_jt, b, kSubTileBytes);
+    const auto aR = ALIF ? tile_rsrc(a.epsa, a.n_jt_a, b, kSubTileBytes) : eR;
+    const auto vR = RT ? tile_rsrc(a.epsv, a.n_jt, b, kSubTileBytes) : eR;
+    const int cj = 4 * g;
+    auto plane = [&](int p) {
+      return *(const f32x4*)(st + (p / PPW) * kScalWave + (p % PPW) * kTileJ + cj);
+    };
+    if constexpr (!RT) {
+      // c, q, P, D, scale exponents, alpha U'_0, alpha H'_0, alpha V'_0
+      // (coef_kernel); the block-start filter Z of row i after them.  One
+      // output at a time, with the planes it needs, so that few registers
+      // are live beside the contractions.
+      // 2^-e from the biased exponent byte at bit `sh`
+      auto inv_scale = [&](int sh) {
+        const f32x4 ex = plane(4);
+        f32x4 f;
 #pragma unroll
-    for (int bj = 0; bj < 2; ++bj) {
-      const int cj = 32 * wj + 16 * bj + 4 * g;
-      if constexpr (!RT) {
-        // c, q, P, D, scale exponents, alpha U'_0, alpha H'_0, alpha V'_0
-        // (coef_kernel); the block-start filter Z of row i after them.  One
-        // output at a time, with the planes it needs, so that few registers
-        // are live beside the contractions.
-        // 2^-e from the biased exponent byte at bit `sh`
-        auto inv_scale = [&](int sh) {
-          const f32x4 ex = plane(4, cj);
-          f32x4 f;
+        for (int q = 0; q < 4; ++q)
+          f[q] = __uint_as_float((uint32_t)(255 - (int)((__float_as_uint(ex[q]) >> sh) & 0xFF)) << 23);
+        return f;
+      };
+      const float* zrow = st + w * kScalWave + ZOFF;
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi) {
+        const f32x4 e0 = first ? zero : E[bi];
+        const f32x4 a0 = (first || !ALIF) ? zero : A[bi];
+        const float Z = zrow[16 * bi + r];
+        const uint32_t o = bi * 1024u + lane * 16u;
+        {
+          const f32x4 P = ALIF ? plane(2) : zero, zU = plane(5), fU = inv_scale(0);
+          f32x4 ek;
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            f[q] = __uint_as_float((uint32_t)(255 - (int)((__float_as_uint(ex[q]) >> sh) & 0xFF)) << 23);
-          return f;
-        };
-#pragma unroll
-        for (int bi = 0; bi < 2; ++bi) {
-          const f32x4 e0 = first ? zero : E[bj][bi];
-          const f32x4 a0 = (first || !ALIF) ? zero : A[bj][bi];
-          const float Z = st[PLANES * kTile + 32 * wi + 16 * bi + r];
-          const uint32_t o = (2 * bj + bi) * 1024u + lane * 16u;
-          {
-            const f32x4 P = ALIF ? plane(2, cj) : zero, zU = plane(5, cj), fU = inv_scale(0);
-            f32x4 ek;
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], fmaf(zU[q], Z, cU[bj][bi][q] * fU[q])));
-            bstore(eR, o, ek);
-          }
-          {
-            const f32x4 c = plane(0, cj), qq = plane(1, cj), zH = plane(6, cj), fH = inv_scale(8);
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              gacc[bj][bi][q] += fmaf(c[q], e0[q], fmaf(qq[q], a0[q], fmaf(zH[q], Z, cH[bj][bi][q] * fH[q])));
-          }
-          if constexpr (ALIF) {
-            const f32x4 Dd = plane(3, cj), zV = plane(7, cj), fV = inv_scale(16);
-            f32x4 ak;
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              ak[q] = fmaf(Dd[q], a0[q], fmaf(zV[q], Z, cV[bj][bi][q] * fV[q]));
-            bstore(aR, o, ak);
-          }
-        }
-      } else {
-        // gE gA gV eA eV aA aV vA vV 1/sU 1/sH 1/sV 1/sW (coef_rt_kernel)
-        const f32x4 gE = plane(0, cj), gV = plane(2, cj), eV = plane(4, cj), vV = plane(8, cj);
-        const f32x4 gA = ALIF ? plane(1, cj) : zero, eA = ALIF ? plane(3, cj) : zero;
-        const f32x4 aA = ALIF ? plane(5, cj) : zero, aV = ALIF ? plane(6, cj) : zero;
-        const f32x4 vA = ALIF ? plane(7, cj) : zero;
-        const f32x4 fU = plane(9, cj), fH = plane(10, cj), fW = plane(12, cj);
-        const f32x4 fV = ALIF ? plane(11, cj) : zero;
-#pragma unroll
-        for (int bi = 0; bi < 2; ++bi) {
-          const f32x4 e0 = first ? zero : E[bj][bi];
-          const f32x4 v0 = first ? zero : Vm[bj][bi];
-          const f32x4 a0 = (first || !ALIF) ? zero : A[bj][bi];
-          f32x4 ek, ak, gk, vk;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            ek[q] = fmaf(a.kappa_K, e0[q], fmaf(eV[q], v0[q], fmaf(eA[q], a0[q], cU[bj][bi][q] * fU[q])));
-            gk[q] = fmaf(gE[q], e0[q], fmaf(gV[q], v0[q], fmaf(gA[q], a0[q], cH[bj][bi][q] * fH[q])));
-            vk[q] = fmaf(vV[q], v0[q], fmaf(vA[q], a0[q], cW[bj][bi][q] * fW[q]));
-            ak[q] = fmaf(aV[q], v0[q], fmaf(aA[q], a0[q], cV[bj][bi][q] * fV[q]));
-          }
-          gacc[bj][bi] += gk;
-          const uint32_t o = (2 * bj + bi) * 1024u + lane * 16u;
+            ek[q] = fmaf(a.kappa_K, e0[q], fmaf(P[q], a0[q], fmaf(zU[q], Z, cU[bi][q] * fU[q])));
           bstore(eR, o, ek);
-          bstore(vR, o, vk);
-          if constexpr (ALIF) bstore(aR, o, ak);
         }
+        {
+          const f32x4 c = plane(0), qq = plane(1), zH = plane(6), fH = inv_scale(8);
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            gacc[bi][q] += fmaf(c[q], e0[q], fmaf(qq[q], a0[q], fmaf(zH[q], Z, cH[bi][q] * fH[q])));
+        }
+        if constexpr (ALIF) {
+          const f32x4 Dd = plane(3), zV = plane(7), fV = inv_scale(16);
+          f32x4 ak;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            ak[q] = fmaf(Dd[q], a0[q], fmaf(zV[q], Z, cV[bi][q] * fV[q]));
+          bstore(aR, o, ak);
+        }
+      }
+    } else {
+      // gE gA gV eA eV aA aV vA vV 1/sU 1/sH 1/sV 1/sW (coef_rt_kernel)
+      const f32x4 gE = plane(0), gV = plane(2), eV = plane(4), vV = plane(8);
+      const f32x4 gA = ALIF ? plane(1) : zero, eA = ALIF ? plane(3) : zero;
+      const f32x4 aA = ALIF ? plane(5) : zero, aV = ALIF ? plane(6) : zero;
+      const f32x4 vA = ALIF ? plane(7) : zero;
+      const f32x4 fU = plane(9), fH = plane(10), fW = plane(12);
+      const f32x4 fV = ALIF ? plane(11) : zero;
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi) {
+        const f32x4 e0 = first ? zero : E[bi];
+        const f32x4 v0 = first ? zero : Vm[bi];
+        const f32x4 a0 = (first || !ALIF) ? zero : A[bi];
+        f32x4 ek, ak, gk, vk;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          ek[q] = fmaf(a.kappa_K, e0[q], fmaf(eV[q], v0[q], fmaf(eA[q], a0[q], cU[bi][q] * fU[q])));
+          gk[q] = fmaf(gE[q], e0[q], fmaf(gV[q], v0[q], fmaf(gA[q], a0[q], cH[bi][q] * fH[q])));
+          vk[q] = fmaf(vV[q], v0[q], fmaf(vA[q], a0[q], cW[bi][q] * fW[q]));
+          ak[q] = fmaf(aV[q], v0[q], fmaf(aA[q], a0[q], cV[bi][q] * fV[q]));
+        }
+        gacc[bi] += gk;
+        const uint32_t o = bi * 1024u + lane * 16u;
+        bstore(eR, o, ek);
+        bstore(vR, o, vk);
+        if constexpr (ALIF) bstore(aR, o, ak);
       }
     }
   }
@@ -1222,12 +1305,12 @@ struct TraceTile {
   __device__ __forceinline__ void run() const {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     const int nk = (a.B - split + a.n_split - 1) / a.n_split;
-    f32x4 gacc[2][2], cU[2][2], cV[2][2], cH[2][2], cW[2][2], E[2][2], A[2][2], Vm[2][2];
+    f32x4 gacc[4], cU[4], cV[4], cH[4], cW[4], E[4], A[4], Vm[4];
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
-      gacc[x >> 1][x & 1] = zero;
-      cU[x >> 1][x & 1] = cV[x >> 1][x & 1] = cH[x >> 1][x & 1] = cW[x >> 1][x & 1] = zero;
-      E[x >> 1][x & 1] = A[x >> 1][x & 1] = Vm[x >> 1][x & 1] = zero;
+      gacc[x] = zero;
+      cU[x] = cV[x] = cH[x] = cW[x] = zero;
+      E[x] = A[x] = Vm[x] = zero;
     }
 #pragma unroll
     for (int c = 0; c < D; ++c) issue_all(split, c, c, 0);
@@ -1238,17 +1321,23 @@ struct TraceTile {
       auto chunk = [&](auto chc) {
         constexpr int ch = decltype(chc)::value;
         const int n = k * NCH + ch;
-        if (next)
-          __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, true)));
-        else
-          __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, false)));
+        if (copier) {
+          if (next)
+            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, true, true)));
+          else
+            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, false, true)));
+        } else {
+          if (next)
+            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, true, false)));
+          else
+            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, false, false)));
+        }
         wg_barrier();   // chunk n is in shared memory; slot (n - 1) % RING is free
         if constexpr (ch == 0) {
           // element k-1 is finished now: its stores overlap this chunk's MFMAs
           if (k > 0) finish(k - 1, E, A, Vm, cU, cV, cH, cW, gacc);
 #pragma unroll
-          for (int x = 0; x < 4; ++x)
-            cU[x >> 1][x & 1] = cV[x >> 1][x & 1] = cH[x >> 1][x & 1] = cW[x >> 1][x & 1] = zero;
+          for (int x = 0; x < 4; ++x) cU[x] = cV[x] = cH[x] = cW[x] = zero;
           // with D == NCH the next copies overwrite what finish() just read
           if constexpr (D == NCH) wg_barrier();
           __builtin_amdgcn_sched_barrier(0);
@@ -1265,80 +1354,79 @@ struct TraceTile {
 
         // Per output block and contraction X, one fp16 MFMA (K = 32) over the
         // chunk's 16 steps.  Lane g holds steps 4g..4g+3 as (hi, lo) pairs of
-        // k slots: A = X's words as they are; B = (p, p) per step, which sums
-        // X_hi p + X_lo p (p is the binary presynaptic value, exact in fp16).
+        // k slots: A = X's words as they are (row r of the 16 columns, the
+        // same for every wave); B = (p, p) per step, which sums X_hi p +
+        // X_lo p (p is the binary presynaptic value, exact in fp16).
         const char* slot = (const char*)(sm + (n % RING) * SLOT);
-        const int sw = (r >> 1) & 3;   // unit order of this lane's rows
+        const int sw = (r >> 1) & 3;   // unit order of this lane's row
         const f16x8 zero8 = {};
-        f16x8 bz[2];
+        f16x8 ax[4];
 #pragma unroll
-        for (int x = 0; x < 2; ++x) {
-          // steps 4g .. 4g+3 of row zr: four p bytes (0 or 0x3C) -> (p, p)
-          // fp16 pairs, byte e into bytes 1 and 3 of word e (0 elsewhere)
-          const int zr = 32 * wi + 16 * x + r;
-          const uint32_t pb = *(const uint32_t*)(slot + (zr >> 4) * 256 + g * 64 + (zr & 15) * 4);
+        for (int X = 0; X < 4; ++X)
+          ax[X] = ((X < 2) || (X == 2 && ALIF) || (X == 3 && RT))
+                      ? *(const f16x8*)(slot + kPBytes + X * kOpBytes + r * 64 + ((g ^ sw) << 4))
+                      : zero8;
+#pragma unroll
+        for (int bi = 0; bi < 4; ++bi) {
+          // steps 4g .. 4g+3 of row r of group zg: four p bytes (0 or 0x3C)
+          // -> (p, p) fp16 pairs, byte e into bytes 1 and 3 of word e (0
+          // elsewhere); a half-wave reads 32 consecutive words
+          const int zg = 4 * w + bi;
+          const uint32_t pb = *(const uint32_t*)(slot + zg * 256 + g * 64 + r * 4);
           u32x4 w1;
 #pragma unroll
           for (int e = 0; e < 4; ++e)
             w1[e] = __builtin_amdgcn_perm(0u, pb, (uint32_t)((e << 24) | (0x0C << 16) | (e << 8) | 0x0C));
-          bz[x] = __builtin_bit_cast(f16x8, w1);
-        }
-#pragma unroll
-        for (int bj = 0; bj < 2; ++bj) {
-          const int cr = 32 * wj + 16 * bj + r;
-          f16x8 ax[4];
-#pragma unroll
-          for (int X = 0; X < 4; ++X)
-            ax[X] = ((X < 2) || (X == 2 && ALIF) || (X == 3 && RT))
-                        ? *(const f16x8*)(slot + kPBytes + X * kOpBytes + cr * 64 + ((g ^ sw) << 4))
-                        : zero8;
-#pragma unroll
-          for (int bi = 0; bi < 2; ++bi) {
-            cU[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[0], bz[bi], cU[bj][bi], 0, 0, 0);
-            cH[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz[bi], cH[bj][bi], 0, 0, 0);
-            if constexpr (ALIF)
-              cV[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[2], bz[bi], cV[bj][bi], 0, 0, 0);
-            if constexpr (RT)
-              cW[bj][bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[3], bz[bi], cW[bj][bi], 0, 0, 0);
-          }
-          __builtin_amdgcn_sched_barrier(0);
-          if (bj == 0) {
+          const f16x8 bz = __builtin_bit_cast(f16x8, w1);
+          cU[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[0], bz, cU[bi], 0, 0, 0);
+          cH[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz, cH[bi], 0, 0, 0);
+          if constexpr (ALIF)
+            cV[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[2], bz, cV[bi], 0, 0, 0);
+          if constexpr (RT)
+            cW[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[3], bz, cW[bi], 0, 0, 0);
+          if (bi == 1) {
+            __builtin_amdgcn_sched_barrier(0);
             issue_next(std::integral_constant<int, 0>{});
-          } else {
+            __builtin_amdgcn_sched_barrier(0);
+          } else if (bi == 3) {
+            __builtin_amdgcn_sched_barrier(0);
             issue_next(std::integral_constant<int, 1>{});
             // the element's block-start traces, after chunk 0's copies
             if constexpr (ch == 0) load_traces(b, E, A, Vm);
+            __builtin_amdgcn_sched_barrier(0);
           }
-          __builtin_amdgcn_sched_barrier(0);
         }
       };
       for_each_index(chunk, std::make_integer_sequence<int, NCH>{});
     }
     __builtin_amdgcn_s_waitcnt(vm_wait(0));   // the last element's traces
     finish(nk - 1, E, A, Vm, cU, cV, cH, cW, gacc);
-    // the split's fp64 accumulator (row-major [n_pre_pad][ldj])
-    const int iw = i0 + 32 * wi, jw = j0 + 32 * wj;
+    // the split's fp64 accumulator (row-major [n_pre_pad][ldj]); rows past
+    // n_pre and columns past n_post are not written
+    const int jb = j0 + 4 * g;
+    if (!live || jb >= a.n_post) return;
     double* accp = a.acc + (size_t)split * a.acc_stride;
 #pragma unroll
-    for (int bj = 0; bj < 2; ++bj) {
-      const int jb = jw + 16 * bj + 4 * g;
-      if (jb >= a.n_post) continue;
+    for (int bi = 0; bi < 4; ++bi) {
+      const int i = i0 + kWaveRows * w + 16 * bi + r;
+      if (i >= a.n_pre) continue;
+      double* p = accp + (size_t)i * a.ldj + jb;
 #pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-        double* p = accp + (size_t)(iw + 16 * bi + r) * a.ldj + jb;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) p[q] = (first ? 0.0 : p[q]) + (double)gacc[bj][bi][q];
-      }
+      for (int q = 0; q < 4; ++q) p[q] = (first ? 0.0 : p[q]) + (double)gacc[bi][q];
     }
   }
 };
 
-// blockIdx.x: tile in row-major order; blockIdx.y: batch split.  A tile
-// holding any adaptive neuron takes the path with the adaptation trace.
-// One kernel per chunk count NCH = kpad / 16 (the host picks it), so that
-// each holds only its own two variants.
+// blockIdx.x: tile in row-major order (it, jt); blockIdx.y: batch split.  A
+// tile holding any adaptive neuron takes the path with the adaptation trace.
+// With a multiple of 8 column tiles, the row tiles of one column tile (which
+// share its coefficient chunks) land on one XCD (workgroups go round-robin
+// over the eight).  One kernel per chunk count NCH = kpad / 16 (the host picks
+// it), so that each holds only its own two variants.
+// Three workgroups per compute unit for the reset-stopped form (its
+// variants fit 168 registers), two with the reset path kept.
 template <bool RT, int NCH>
-__global__ __launch_bounds__(256, 2) void trace_kernel(TraceArgs a) {
+__global__ __launch_bounds__(256, RT ? 2 : 3) void trace_kernel(TraceArgs a) {
   extern __shared__ __attribute__((aligned(16))) float trace_smem[];
   const int it = blockIdx.x / a.n_jt, jt = blockIdx.x - it * a.n_jt;
   const bool first = a.first != 0;
@@ -1571,7 +1659,7 @@ hipError_t launch_trace_variant(const TraceArgs& a, hipStream_t s) {
   constexpr size_t smem = kTraceSmemOf(RT);
   hipError_t e = grant_smem<&trace_kernel<RT, NCH>>((int)smem);
   if (e != hipSuccess) return e;
-  dim3 grid((a.n_pre_pad / kTile) * a.n_jt, a.n_split);
+  dim3 grid((a.n_pre_pad / kTileI) * a.n_jt, a.n_split);
   trace_kernel<RT, NCH><<<grid, 256, smem, s>>>(a);
   return hipGetLastError();
 }
