@@ -27,6 +27,8 @@ class OracleConfig(ctypes.Structure):
         ("reset", ctypes.c_double),
         ("fwd_fp32", ctypes.c_int32), ("smooth", ctypes.c_int32),
         ("reset_through", ctypes.c_int32),
+        ("model", ctypes.c_int32), ("alpha_d", ctypes.c_double), ("coupling", ctypes.c_double),
+        ("bap", ctypes.c_double),
     ]
 
 
@@ -92,6 +94,10 @@ def make_config(shape, fwd_fp32: bool = True, smooth: bool = False,
     c.reset = shape.thr if reset is None else reset
     c.fwd_fp32, c.smooth = int(fwd_fp32), int(smooth)
     c.reset_through = int(getattr(shape, "reset_grad", 0))
+    c.model = int(getattr(shape, "neuron_model", 0))
+    c.alpha_d = float(getattr(shape, "alpha_d", 0.0))
+    c.coupling = float(getattr(shape, "coupling", 0.0))
+    c.bap = float(getattr(shape, "bap", 0.0))
     for k, v in over.items():
         setattr(c, k, v)
     return c

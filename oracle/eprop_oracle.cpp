@@ -46,6 +46,20 @@
 //     membrane component of G_t is a per-synapse eps^v (no longer the
 //     presynaptic filter zbar): one of the neuron-model variants the generic
 //     method of Sec. III-C covers.
+//   * optionally (model = 1) a two-compartment neuron instead: a dendrite d
+//     that receives the synaptic drive and the neuron's own last spike (a
+//     backpropagating spike of strength q, kept in the gradient), and a soma
+//     s driven by the dendrite's previous value through a coupling g and
+//     reset by subtraction:
+//       d^t = alpha_d d^{t-1} + I^t + q z^{t-1}
+//       s^t = alpha s^{t-1} + g d^{t-1} - reset z^{t-1}
+//       z^t = H(s^t - thr),  psi^t = (gamma/thr) max(0, 1 - |s^t - thr|/thr)
+//     Its neuron-on-itself Jacobian is a full 2x2 block per neuron,
+//     H_I^t = [[alpha - reset*psi^{t-1} (reset kept only), g],
+//              [q psi^{t-1}, alpha_d]]  over (s, d),
+//     and F_t = dh^t/dW_ji = (0, p_i^t): the block-diagonal case of the
+//     footnote in Sec. III-C with a state-dependent off-diagonal, so both
+//     components of the eligibility vector are per-synapse state.
 //
 // Precision: the neuron state (v, a, A, v-A) and the spike decision are
 // computed in the type R chosen by `fwd_fp32` (fp32 like the paper's runs,
@@ -74,6 +88,10 @@ typedef struct {
   int32_t fwd_fp32;    // 1: neuron state and spike decision in fp32, 0: fp64
   int32_t smooth;      // 1: z = S(v-A) with S' = psi (finite-difference checks)
   int32_t reset_through;  // 1: the reset path (own spike -> own membrane) is kept
+  int32_t model;       // 0: LIF/ALIF, 1: two-compartment neuron (soma s, dendrite d)
+  double alpha_d;      // model 1: dendritic decay
+  double coupling;     // model 1: dendrite -> soma coupling g
+  double bap;          // model 1: own spike -> dendrite (backpropagating spike) q
 } oracle_config;
 
 // Optional per-step records; each pointer may be NULL.
@@ -116,6 +134,9 @@ struct LayerState {
   std::vector<double> delta, L;    // dCE/dy, learning signal W_out^T delta
   std::vector<double> ebar, epsa;  // eligibility: kappa-filtered trace, eps^a
   std::vector<double> epsv;        // per-synapse eps^v (reset_through; without the next input)
+  // two-compartment neuron: per-synapse eligibility vector (eps_s, eps_d) of
+  // the last step, and the pseudo-derivative of the last step per neuron
+  std::vector<double> eps_s, eps_d, psi_prev;
 };
 
 // The state of one batch element: neuron state, filters and traces of every
@@ -153,7 +174,12 @@ void seq_alloc(const oracle_config& c, bool all, int n_sample, Seq<R>& q) {
       s.ebar.assign((size_t)N * s.n_pre, 0.0);
       s.epsa.assign((size_t)NA * s.n_pre, 0.0);
       if (c.reset_through) s.epsv.assign((size_t)N * s.n_pre, 0.0);
+      if (c.model == 1) {
+        s.eps_s.assign((size_t)N * s.n_pre, 0.0);
+        s.eps_d.assign((size_t)N * s.n_pre, 0.0);
+      }
     }
+    s.psi_prev.assign(N, 0.0);
   }
   if (!all) {
     ebar_s.assign(n_sample, 0.0);
@@ -161,6 +187,7 @@ void seq_alloc(const oracle_config& c, bool all, int n_sample, Seq<R>& q) {
     epsv_s.assign(n_sample, 0.0);
   }
 }
+
 
 // A new sequence: every state, trace and filter starts at zero (G_0 = 0).
 template <typename R>
@@ -179,6 +206,9 @@ void seq_zero(const oracle_config& c, Seq<R>& q) {
     std::fill(s.ebar.begin(), s.ebar.end(), 0.0);
     std::fill(s.epsa.begin(), s.epsa.end(), 0.0);
     std::fill(s.epsv.begin(), s.epsv.end(), 0.0);
+    std::fill(s.eps_s.begin(), s.eps_s.end(), 0.0);
+    std::fill(s.eps_d.begin(), s.eps_d.end(), 0.0);
+    std::fill(s.psi_prev.begin(), s.psi_prev.end(), 0.0);
   }
   std::fill(q.ebar_s.begin(), q.ebar_s.end(), 0.0);
   std::fill(q.epsa_s.begin(), q.epsa_s.end(), 0.0);
@@ -227,6 +257,19 @@ void steps(const oracle_config& c, const float* const* W, const float* const* Wo
         R I = 0;
         for (int i : active) I = I + (R)Wl[(size_t)j * s.n_pre + i] * (R)s.p[i];
         const R zp = (R)s.z_prev[j];
+        R xj;
+        if (c.model == 1) {
+          // two-compartment neuron: v holds the soma s, a the dendrite d
+          R d = (R)c.alpha_d * s.a[j];
+          d = d + I;
+          d = d + (R)c.bap * zp;
+          R sm = alpha * s.v[j];
+          sm = sm + (R)c.coupling * s.a[j];
+          sm = sm - reset * zp;
+          xj = sm - thr;
+          s.v[j] = sm;
+          s.a[j] = d;
+        } else {
         R v = alpha * s.v[j];
         v = v + I;
         v = v - reset * zp;
@@ -235,9 +278,10 @@ void steps(const oracle_config& c, const float* const* W, const float* const* Wo
         const R bj = (j < NA) ? (R)c.beta : R(0);
         R A = bj * a;
         A = thr + A;
-        const R xj = v - A;
+        xj = v - A;
         s.v[j] = v;
         s.a[j] = a;
+        }
         const double xd = (double)xj;
         s.z[j] = c.smooth ? smooth_spike(xd, c.thr, c.gamma) : (xj > R(0) ? 1.0 : 0.0);
         const double u = 1.0 - std::fabs(xd) / c.thr;
@@ -278,7 +322,38 @@ void steps(const oracle_config& c, const float* const* W, const float* const* Wo
       // and after the step
       //   epsv   = (alpha - reset psi_j) epsv + reset beta_j psi_j epsa
       //   epsa   = psi_j epsv + (rho - beta_j psi_j) epsa  (both with the values at t).
-      if (c.reset_through) {
+      if (c.model == 1) {
+        // Eq. (5) with the 2x2 block H_I^t of each neuron (psi of the last
+        // step in its second row, and in its first with the reset kept) and
+        // F_t = (0, p_i): eps^t = H_I^t eps^{t-1} + F_t, then
+        // e = dz^t/dW_ji = psi^t eps_s^t (z depends on the soma only).
+        for (int q = 0; q < (all ? N * s.n_pre : n_sample); ++q) {
+          int j, i;
+          if (all) {
+            j = q / s.n_pre;
+            i = q - j * s.n_pre;
+          } else {
+            if (sample[q].layer != l) continue;
+            j = sample[q].j;
+            i = sample[q].i;
+          }
+          const double pp = s.psi_prev[j];
+          const double h11 = c.alpha - (c.reset_through ? c.reset * pp : 0.0);
+          const double h12 = c.coupling, h21 = c.bap * pp, h22 = c.alpha_d;
+          const size_t ji = (size_t)j * s.n_pre + i;
+          double& es = all ? s.eps_s[ji] : epsv_s[q];
+          double& ed = all ? s.eps_d[ji] : epsa_s[q];
+          double& eb = all ? s.ebar[ji] : ebar_s[q];
+          const double es_new = h11 * es + h12 * ed;
+          const double ed_new = h21 * es + h22 * ed + s.p[i];
+          es = es_new;
+          ed = ed_new;
+          const double e = s.psi[j] * es;
+          eb = c.kappa * eb + e;
+          (all ? dW[l][ji] : dW[0][q]) += s.L[j] * eb;
+        }
+        for (int j = 0; j < N; ++j) s.psi_prev[j] = s.psi[j];
+      } else if (c.reset_through) {
         for (int q = 0; q < (all ? N * s.n_pre : n_sample); ++q) {
           int j, i;
           if (all) {
@@ -453,7 +528,7 @@ int run_online(const oracle_config& c, const float* const* W0, const float* cons
 bool valid(const oracle_config* c) {
   return c && (c->n_layers == 1 || c->n_layers == 2) && c->batch > 0 && c->n_in > 0 &&
          c->n_rec > 0 && c->n_out > 0 && c->n_adaptive >= 0 && c->n_adaptive <= c->n_rec &&
-         c->thr > 0.0;
+         c->thr > 0.0 && (c->model == 0 || (c->model == 1 && c->n_adaptive == 0));
 }
 
 }  // namespace
@@ -471,10 +546,12 @@ size_t oracle_state_bytes(const oracle_config* c, int32_t n_sample) {
     const size_t N = c->n_rec, K = c->n_out;
     total += 2 * N * (c->fwd_fp32 ? sizeof(float) : sizeof(double));
     total += sizeof(double) * (2 * N + 2 * n_pre + N + 2 * K + N + K + N);
+    total += sizeof(double) * N;   // last pseudo-derivative
     if (n_sample < 0)
-      total += sizeof(double) * ((c->reset_through ? 2 : 1) * N * n_pre + (size_t)c->n_adaptive * n_pre);
+      total += sizeof(double) * ((c->model == 1 ? 3 : c->reset_through ? 2 : 1) * N * n_pre +
+                                 (size_t)c->n_adaptive * n_pre);
   }
-  if (n_sample >= 0) total += sizeof(double) * (c->reset_through ? 3 : 2) * (size_t)n_sample;
+  if (n_sample >= 0) total += sizeof(double) * (c->reset_through || c->model == 1 ? 3 : 2) * (size_t)n_sample;
   return total;
 }
 

@@ -44,6 +44,10 @@ class EpropShape:
     n_adaptive: neurons j < n_adaptive have an adaptive threshold (ALIF).
     reset_grad: 1 keeps the reset path (own spike -> own membrane) in the
       gradient; 0 (default) stops it.
+    neuron_model: 0 LIF/ALIF; 1 a two-compartment neuron (a dendrite with
+      decay alpha_d receiving the drive and the own spike times bap, a soma
+      with decay alpha driven by the dendrite times coupling); n_adaptive
+      must be 0 then.
     Constants are fp32-representable; both implementations use these exact
     values.
     """
@@ -62,6 +66,10 @@ class EpropShape:
     beta: float = f32(1.8)
     gamma: float = f32(0.3)
     reset_grad: int = 0
+    neuron_model: int = 0
+    alpha_d: float = f32(math.exp(-1.0 / 10.0))
+    coupling: float = f32(0.5)
+    bap: float = f32(-0.5)
     rate_lo: float = 0.005
     rate_hi: float = 0.05
     rate_const: Optional[float] = None  # one fixed rate for every channel

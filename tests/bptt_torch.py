@@ -106,14 +106,25 @@ def bptt_grads(shape, W, Wout, x, labels, T=None, reset=None, stop=True, feedbac
             inp = xs[t] if l == 0 else sg(z_now[l - 1])
             p = torch.cat([inp, sg(zp[l])], dim=1) if shape.recurrent else inp
             I = p @ Wuse[l].T
-            vl = shape.alpha * v[l]
-            vl = vl + I
-            vl = vl - reset * (zp[l] if keep_reset else sg(zp[l]))
-            al = shape.rho * a[l]
-            al = al + zp[l]                 # spike -> adaptation path is kept
-            A = beta * al
-            A = shape.thr + A
-            z = _Spike.apply(vl - A, shape.gamma, shape.thr)
+            if getattr(shape, "neuron_model", 0) == 1:
+                # two-compartment neuron: v is the soma, a the dendrite; the
+                # own spike reaches the dendrite (kept) and resets the soma
+                al = shape.alpha_d * a[l]
+                al = al + I
+                al = al + shape.bap * zp[l]
+                vl = shape.alpha * v[l]
+                vl = vl + shape.coupling * a[l]
+                vl = vl - reset * (zp[l] if keep_reset else sg(zp[l]))
+                z = _Spike.apply(vl - shape.thr, shape.gamma, shape.thr)
+            else:
+                vl = shape.alpha * v[l]
+                vl = vl + I
+                vl = vl - reset * (zp[l] if keep_reset else sg(zp[l]))
+                al = shape.rho * a[l]
+                al = al + zp[l]                 # spike -> adaptation path is kept
+                A = beta * al
+                A = shape.thr + A
+                z = _Spike.apply(vl - A, shape.gamma, shape.thr)
             if schedule is None:
                 yz = z @ Wouse[l].T if Fbs is None or Fbs[l] is None else _Readout.apply(z, Wouse[l], Fbs[l])
                 y[l] = shape.kappa * y[l] + yz

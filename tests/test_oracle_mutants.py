@@ -50,6 +50,13 @@ MUTANTS = [
      "ev = (c.alpha - c.reset * pj) * V;", 1),
     ("online_update_from_current_weights", "Wcur[l][ji] = on_grid((double)W0[l][ji] - lr * dW[l][ji]);",
      "Wcur[l][ji] = on_grid((double)Wcur[l][ji] - lr * dW[l][ji]);", 1),
+    ("two_compartment_feedback_dropped", "h21 = c.bap * pp", "h21 = 0.0 * pp", 1),
+    ("two_compartment_coupling_transposed", "const double ed_new = h21 * es + h22 * ed + s.p[i];",
+     "const double ed_new = h12 * es + h22 * ed + s.p[i];", 1),
+    ("two_compartment_current_psi_in_jacobian", "const double pp = s.psi_prev[j];",
+     "const double pp = s.psi[j];", 1),
+    ("two_compartment_soma_reads_new_dendrite", "sm = sm + (R)c.coupling * s.a[j];",
+     "sm = sm + (R)c.coupling * d;", 1),
     ("online_feedback_ignored", "steps(c, Wcur, Woutcur, Fb, x,", "steps(c, Wcur, Woutcur, nullptr, x,", 1),
     ("online_readout_not_updated", "Woutcur[l][kj] = on_grid((double)Wout0[l][kj] - lr * dWout[l][kj]);",
      "Woutcur[l][kj] = Wout0[l][kj];", 1),

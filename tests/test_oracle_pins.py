@@ -241,6 +241,63 @@ def test_reset_through_equals_backprop_with_reset_path(name):
     assert rel_l2(r.dW[0], stopped.dW[0]) > 1e-3
 
 
+# ---------------------------------------------------------------- two-compartment neuron
+TWO_COMP = dict(neuron_model=1, n_adaptive=0)
+TWO_COMP_CASES = {
+    "tc_ff": (small(T=70, recurrent=0, **TWO_COMP, **DISTINCT), 6, 4.0),
+    "tc_recurrent": (small(T=90, **TWO_COMP, **DISTINCT), 3, 4.0),
+    "tc_two_layers": (small(batch=2, n_in=21, n_rec=19, n_out=4, T=80, n_layers=2, **TWO_COMP,
+                            **DISTINCT), 4, 4.0),
+    "tc_positive_q": (small(T=60, bap=0.25, coupling=0.75, **TWO_COMP, **DISTINCT), 8, 4.0),
+}
+
+
+@pytest.mark.parametrize("reset_grad", [0, 1])
+@pytest.mark.parametrize("name", list(TWO_COMP_CASES))
+def test_two_compartment_equals_backprop(name, reset_grad):
+    # A soma-dendrite neuron whose own spike feeds its dendrite: the
+    # neuron-on-itself Jacobian is a full 2x2 block with the pseudo-
+    # derivative off the diagonal.  The forward recursion with that block
+    # must equal reverse-mode autograd of the network with the same stops.
+    shape, seed, scale = TWO_COMP_CASES[name]
+    shape = shape.replace(reset_grad=reset_grad)
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    dW, dWout, loss = bptt_grads(shape, wl.W, wl.Wout, wl.x, wl.labels)
+    assert r.spikes.any()
+    assert abs(r.loss - loss) <= 1e-12 * abs(loss)
+    for l in range(shape.n_layers):
+        assert np.abs(dW[l]).max() > 0
+        assert rel_l2(r.dW[l], dW[l]) <= 1e-11, (l, rel_l2(r.dW[l], dW[l]))
+        assert rel_l2(r.dWout[l], dWout[l]) <= 1e-11
+
+
+def test_two_compartment_is_its_own_model():
+    # Different spikes from the LIF neuron on the same inputs; with no
+    # coupling the soma never sees the drive: no spikes and no gradient.
+    shape, seed, scale = TWO_COMP_CASES["tc_recurrent"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    r = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    plain = oracle.run(shape.replace(neuron_model=0), wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    assert not np.array_equal(r.spikes, plain.spikes)
+    r0 = oracle.run(shape.replace(coupling=0.0), wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    assert not r0.spikes.any() and not r0.dW[0].any()
+
+
+def test_two_compartment_samples_agree_with_full_run():
+    shape, seed, scale = TWO_COMP_CASES["tc_recurrent"]
+    shape = shape.replace(reset_grad=1)
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    full = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False)
+    rng = np.random.default_rng(6)
+    smp = np.array([(0, int(rng.integers(shape.n_rec)), int(rng.integers(shape.n_pre(0))))
+                    for _ in range(60)] + [(0, 0, 0), (0, shape.n_rec - 1, shape.n_pre(0) - 1)],
+                   dtype=np.int32)
+    part = oracle.run(shape, wl.W, wl.Wout, wl.x, wl.labels, fwd_fp32=False, sample=smp)
+    got = np.array([full.dW[0][j, i] for _, j, i in smp])
+    np.testing.assert_allclose(part.dW[0], got, rtol=1e-13, atol=1e-15)
+
+
 def test_reset_through_samples_agree_with_full_run():
     shape, seed, scale = AUTOGRAD_CASES["ralif_ragged"]
     shape = shape.replace(reset_grad=1)
