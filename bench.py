@@ -40,6 +40,15 @@ COUNTERS = os.path.join(ROOT, "profiles", "trace_kernel_counters.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2501_11407_amd", "csrc", "kernels.hip")
 
 
+def dims(shape):
+    """(B, N, neurons with a second per-synapse state component, three-trace
+    recursion): the reset path kept, or the two-compartment neuron (whose
+    soma and dendrite eligibilities are both per-synapse)."""
+    model = getattr(shape, "neuron_model", 0)
+    rt = 1 if (getattr(shape, "reset_grad", 0) or model == 1) else 0
+    return shape.batch, shape.n_rec, (shape.n_rec if model == 1 else shape.n_adaptive), rt
+
+
 def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: int) -> int:
     """Algorithmic HBM bytes of eligibility-kernel launches on one layer.
     Per launch: ebar (every synapse) and eps^a (synapses onto adaptive
@@ -52,9 +61,8 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     the block-start filter [B, N_pre].  With the reset path kept
     (reset_grad = 1): eps^v (every synapse) as a third trace, a fourth
     coefficient row W [B, N], and nine scalars per (b, j)."""
-    B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
+    B, N, NA, rt = dims(shape)
     npre = shape.n_pre(layer)
-    rt = getattr(shape, "reset_grad", 0)
     trace = 4 * B * npre * ((2 if rt else 1) * N + NA) + 8 * npre * N      # one direction
     rows = (3 if rt else 2) * N + NA
     scalars = 9 if rt else 7
@@ -77,9 +85,8 @@ def per_step_model_bytes(shape, layer: int) -> int:
     per synapse 8 B of ebar, 8 B of eps^a onto adaptive neurons, and per
     (i, j) the fp64 accumulator read and written and W read (12 B over the
     batch)."""
-    B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
+    B, N, NA, rt = dims(shape)
     npre = shape.n_pre(layer)
-    rt = getattr(shape, "reset_grad", 0)     # eps^v as a third trace
     return 8 * B * npre * ((2 if rt else 1) * N + NA) + 12 * npre * N
 
 
@@ -89,9 +96,8 @@ def trace_flops(shape, layer: int, steps: int) -> int:
     the contractions over the block's steps -- C_U and C_H for every
     synapse, C_V as well for synapses onto adaptive neurons (and, with the
     reset path kept, C_W for every synapse)."""
-    B, N, NA = shape.batch, shape.n_rec, shape.n_adaptive
+    B, N, NA, rt = dims(shape)
     npre = shape.n_pre(layer)
-    rt = getattr(shape, "reset_grad", 0)
     return steps * B * npre * 2 * ((3 if rt else 2) * N + NA)
 
 
@@ -220,6 +226,8 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=1024)
     ap.add_argument("--reset-grad", type=int, default=0, choices=(0, 1),
                     help="1: the same workload with the reset path kept in the gradient")
+    ap.add_argument("--neuron-model", type=int, default=0, choices=(0, 1),
+                    help="1: the same workload with two-compartment neurons (no adaptive ones)")
     ap.add_argument("--online-every", type=int, default=0, metavar="K",
                     help="online weight application every K steps (learning rate --online-lr)")
     ap.add_argument("--online-lr", type=float, default=2.0 ** -12)
@@ -251,9 +259,12 @@ def main():
         wl = synth.named_workload(args.workload)
     if args.reset_grad:
         wl.shape = wl.shape.replace(reset_grad=1)
+    if args.neuron_model:
+        wl.shape = wl.shape.replace(neuron_model=1, n_adaptive=0)
     shape = wl.shape
     workload = args.workload + (f"_batch{args.batch}" if args.batch else "") + \
         ("_reset_grad" if args.reset_grad else "") + \
+        ("_two_compartment" if args.neuron_model else "") + \
         (f"_online{args.online_every}" if args.online_every else "")
     dev = torch.device("cuda:0")
     ctx = eprop.EpropContext(shape, wl.W, wl.Wout, device="cuda:0")
@@ -307,7 +318,8 @@ def main():
                 "frac_of_copy_ceiling": round(achieved / copy_gbs, 4),
                 "per_step_model_bytes_per_launch": round(per_step_bytes / n_timed),
                 "per_step_model_gbs": round(per_step_bytes / sec / 1e9, 1),
-                "traffic": (None if (args.reset_grad or args.online_every or args.batch or args.workload != WORKLOAD)
+                "traffic": (None if (args.reset_grad or args.neuron_model or args.online_every or args.batch
+                                     or args.workload != WORKLOAD)
                             else stored_traffic(shape)),
                 "kernel": "trace_kernel", "avg_launch_us": round(trace_ms * 1e3 / n_timed, 2),
                 "steps_per_launch": round(timed_steps / n_timed, 2),
@@ -329,6 +341,7 @@ def main():
         "config": {"workload": workload, "batch": shape.batch, "n_in": shape.n_in,
                    "n_rec": shape.n_rec, "n_adaptive": shape.n_adaptive, "n_out": shape.n_out,
                    "T": shape.T, "layers": shape.n_layers, "reset_grad": args.reset_grad,
+                   "neuron_model": args.neuron_model,
                    "parallelism": "single GPU"},
         "roofline": roofline,
     }

@@ -83,7 +83,33 @@ typedef struct {
                          kept (Eq. 5 with the reset's terms in the membrane
                          row of H_I, Sec. III-C), so the membrane eligibility
                          is a third per-synapse trace; other values: -1 */
+  int32_t neuron_model; /* 0: LIF/ALIF as above.  1: a two-compartment
+                         neuron (n_adaptive must be 0; rho and beta unused):
+                           d^t = alpha_d d^{t-1} + sum_i W_ji p^t_i + bap z^{t-1}
+                           s^t = alpha s^{t-1} + coupling d^{t-1} - thr z^{t-1}
+                           z^t = [s^t - thr > 0], psi from s^t - thr as above;
+                         the own spike's path into the dendrite is kept in
+                         the gradient (the soma reset follows reset_grad), so
+                         H_I is a full 2x2 block per neuron (footnote of
+                         Sec. III-C) and both eligibility components are
+                         per-synapse traces */
+  float alpha_d;      /* neuron_model 1: dendritic decay */
+  float coupling;     /* neuron_model 1: dendrite -> soma coupling */
+  float bap;          /* neuron_model 1: own spike -> dendrite */
 } eprop_config;
+
+/*
+ * The neuron model's step, h^t = A h^{t-1} + b I^t + r z^{t-1} with the spike
+ * argument u = c . h - thr, differentiated on the host by forward-mode dual
+ * numbers (the automatic derivation of H_I and F_t of Sec. III-C for models
+ * whose step is linear in the state): out[0..9] = A00 A01 A10 A11 b0 b1 r0 r1
+ * c0 c1 for neurons j < n_adaptive (cls = 1) or the others (cls = 0), with
+ * r the own-spike terms that stay in the gradient (the reset of component 0
+ * only when reset_grad = 1), so that H_I^t = A + psi^{t-1} r c^T and
+ * F_t = b p^t.  Host only.  Returns 0, or EPROP_EINVAL (invalid config, a
+ * step that is not linear in its state).
+ */
+int eprop_neuron_coefficients(const eprop_config* cfg, int32_t cls, float* out);
 
 /*
  * Bytes of device workspace a context with this shape needs; 0 if the

@@ -79,6 +79,12 @@ struct Layer {
   float* epsv = nullptr;                 // reset_grad: per-synapse membrane eligibility
 };
 
+// A neuron step linear in its state: h = A h_prev + b I + r z_prev, spike
+// argument c . h - thr (see derive_neuron).
+struct NeuronCoef {
+  double A[2][2], b[2], r[2], c[2];
+};
+
 // At most two layers, held in place (a plan allocates nothing).
 struct Layers {
   Layer l[2];
@@ -98,6 +104,10 @@ struct Layers {
 struct Plan {
   eprop_config cfg;
   Layers layers;
+  // three-trace recursion (reset path kept, or the two-compartment neuron),
+  // and the neurons whose second state component has per-synapse traces
+  int rt = 0, na2 = 0;
+  NeuronCoef gen{};                 // two-compartment neuron: derived step
   int* err_flag = nullptr;
   int* w16ok = nullptr;             // 1: the int16 drive weights are exact (launch_pack16)
   int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, ldc = 0, jlist = 0, out_splits = 1;
@@ -132,6 +142,83 @@ bool valid_config(const eprop_config* c, std::string* why) {
     return false;
   }
   if (c->reset_grad != 0 && c->reset_grad != 1) { *why = "reset_grad must be 0 or 1"; return false; }
+  if (c->neuron_model != 0 && c->neuron_model != 1) { *why = "neuron_model must be 0 or 1"; return false; }
+  if (c->neuron_model == 1) {
+    if (c->n_adaptive != 0) { *why = "the two-compartment neuron has no adaptive threshold (n_adaptive 0)"; return false; }
+    const float k2[] = {c->alpha_d, c->coupling, c->bap};
+    for (float v : k2)
+      if (!std::isfinite(v)) { *why = "constants must be finite"; return false; }
+  }
+  return true;
+}
+
+// ---------------------------------------------------------------- neuron models
+// Forward-mode dual numbers: a value and its derivative along one direction.
+struct Dual {
+  double v = 0.0, d = 0.0;
+};
+Dual operator+(Dual a, Dual b) { return {a.v + b.v, a.d + b.d}; }
+Dual operator-(Dual a, Dual b) { return {a.v - b.v, a.d - b.d}; }
+Dual operator*(Dual a, Dual b) { return {a.v * b.v, a.d * b.v + a.v * b.d}; }
+Dual konst(double x) { return {x, 0.0}; }
+
+// The neuron models' step over a scalar type T, as the forward kernel and
+// the paper's Eq. (8) write them: state h (component 0: the membrane or soma,
+// the one the reset acts on), drive I, last spike zp -> new state, and the
+// spike argument u(h) (spike iff u > 0).  cls 1: adaptive neurons.
+template <typename T>
+void model_step(const eprop_config& c, int cls, const T (&h)[2], T I, T zp, T (&out)[2]) {
+  const T thr = konst(c.thr);
+  if (c.neuron_model == 1) {   // soma s = h0, dendrite d = h1
+    out[1] = konst(c.alpha_d) * h[1] + I + konst(c.bap) * zp;
+    out[0] = konst(c.alpha) * h[0] + konst(c.coupling) * h[1] - thr * zp;
+  } else {                     // membrane v = h0, adaptation a = h1
+    out[0] = konst(c.alpha) * h[0] + I - thr * zp;
+    out[1] = konst(c.rho) * h[1] + zp;
+  }
+}
+template <typename T>
+T model_arg(const eprop_config& c, int cls, const T (&h)[2]) {
+  if (c.neuron_model == 1) return h[0] - konst(c.thr);
+  const double beta = cls == 1 ? c.beta : 0.0;
+  return h[0] - (konst(c.thr) + konst(beta) * h[1]);
+}
+
+// Coefficients of a step that is linear in (h, I, zp): A = dh/dh_prev,
+// b = dh/dI, r = dh/dzp (the own-spike paths; the reset of component 0 is
+// gradient-stopped unless reset_grad), c = du/dh, each column one dual pass.
+// The derivatives are taken at two different points and must agree (else
+// the step is not linear and the block form does not apply).
+bool derive_neuron(const eprop_config& cfg, int cls, NeuronCoef* out) {
+  const double pts[2][4] = {{0.3, -0.2, 0.7, 1.0}, {-1.1, 0.45, -0.3, 0.0}};
+  NeuronCoef k[2];
+  for (int p = 0; p < 2; ++p) {
+    for (int dir = 0; dir < 4; ++dir) {   // h0, h1, I, zp
+      Dual h[2] = {{pts[p][0], dir == 0 ? 1.0 : 0.0}, {pts[p][1], dir == 1 ? 1.0 : 0.0}};
+      Dual I{pts[p][2], dir == 2 ? 1.0 : 0.0}, zp{pts[p][3], dir == 3 ? 1.0 : 0.0};
+      Dual o[2];
+      model_step(cfg, cls, h, I, zp, o);
+      for (int m = 0; m < 2; ++m) {
+        if (dir < 2) k[p].A[m][dir] = o[m].d;
+        else if (dir == 2) k[p].b[m] = o[m].d;
+        else k[p].r[m] = o[m].d;
+      }
+    }
+    for (int dir = 0; dir < 2; ++dir) {
+      Dual h[2] = {{pts[p][0], dir == 0 ? 1.0 : 0.0}, {pts[p][1], dir == 1 ? 1.0 : 0.0}};
+      k[p].c[dir] = model_arg(cfg, cls, h).d;
+    }
+  }
+  // the same derivatives at both points (== treats the two zeros as one)
+  const double* k0 = &k[0].A[0][0];
+  const double* k1 = &k[1].A[0][0];
+  constexpr int nk = sizeof(NeuronCoef) / sizeof(double);
+  for (int q = 0; q < nk; ++q)
+    if (!(k0[q] == k1[q])) return false;
+  *out = k[0];
+  double* o = &out->A[0][0];
+  for (int q = 0; q < nk; ++q) o[q] = o[q] + 0.0;   // -0 -> +0
+  if (!cfg.reset_grad) out->r[0] = 0.0;   // the reset stays gradient-stopped
   return true;
 }
 
@@ -139,6 +226,9 @@ bool valid_config(const eprop_config* c, std::string* why) {
 void make_plan(const eprop_config& c, char* base, Plan* plan) {
   plan->cfg = c;
   plan->layers.assign(c.n_layers, Layer());
+  plan->rt = (c.reset_grad || c.neuron_model == 1) ? 1 : 0;
+  plan->na2 = c.neuron_model == 1 ? c.n_rec : c.n_adaptive;
+  if (c.neuron_model == 1) derive_neuron(c, 0, &plan->gen);
   size_t off = 0;
   auto take = [&](size_t bytes) -> char* {
     off = round_up(off, 256);
@@ -208,11 +298,12 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.accout = (double*)take(sizeof(double) * K * L.ldj);
     // traces tile by tile: all j tiles, and the tiles holding adaptive neurons
     const size_t ldc = round_up(N, eprop::kColPad);
-    const size_t lda_t = round_up(c.n_adaptive, eprop::kTileJ);
+    const size_t lda_t = round_up(plan->na2, eprop::kTileJ);
     L.ebar = (float*)take(sizeof(float) * B * npp * ldc);
-    L.epsa = (float*)take(c.n_adaptive > 0 ? sizeof(float) * B * npp * lda_t : 0);
-    // with the reset path kept, the membrane eligibility per synapse as well
-    L.epsv = c.reset_grad ? (float*)take(sizeof(float) * B * npp * ldc) : nullptr;
+    L.epsa = (float*)take(plan->na2 > 0 ? sizeof(float) * B * npp * lda_t : 0);
+    // with the reset path kept (or two compartments), the first state
+    // component's eligibility per synapse as well
+    L.epsv = plan->rt ? (float*)take(sizeof(float) * B * npp * ldc) : nullptr;
   }
   for (Layer& L : plan->layers) {
     const size_t ldc = plan->ldc;
@@ -221,10 +312,10 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
       // value (4 bytes)
       L.p8[sl] = (uint8_t*)take((size_t)B * L.n_pre_pad * KM);
       L.coefU[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
-      L.coefV[sl] = (uint32_t*)take(c.n_adaptive > 0 ? sizeof(uint32_t) * B * ldc * KM : 0);
+      L.coefV[sl] = (uint32_t*)take(plan->na2 > 0 ? sizeof(uint32_t) * B * ldc * KM : 0);
       L.coefH[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
-      L.coefW[sl] = c.reset_grad ? (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM) : nullptr;
-      const int planes = c.reset_grad ? eprop::kScalarPlanesRT : eprop::kScalarPlanes;
+      L.coefW[sl] = plan->rt ? (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM) : nullptr;
+      const int planes = plan->rt ? eprop::kScalarPlanesRT : eprop::kScalarPlanes;
       L.coefS[sl] = (float*)take(sizeof(float) * planes * B * ldc);
     }
     for (int sl = 0; sl < kSlots; ++sl) L.zstart[sl] = (float*)take(sizeof(float) * B * L.n_pre_pad);
@@ -433,6 +524,21 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   fa.ldj = P.layers[0].ldv; fa.ldk = P.ldk; fa.ldn = P.ldn; fa.jlist = P.jlist;
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
   fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.zgroup = P.zgroup;
+  fa.model = c.neuron_model;
+  for (int m = 0; m < 2; ++m) {
+    fa.mA[m][0] = (float)P.gen.A[m][0]; fa.mA[m][1] = (float)P.gen.A[m][1];
+    fa.mb[m] = (float)P.gen.b[m]; fa.mc[m] = (float)P.gen.c[m];
+  }
+  // the forward uses the full own-spike terms (the reset included)
+  {
+    NeuronCoef full{};
+    if (c.neuron_model == 1) {
+      eprop_config cf = c;
+      cf.reset_grad = 1;
+      derive_neuron(cf, 0, &full);
+    }
+    fa.mr[0] = (float)full.r[0]; fa.mr[1] = (float)full.r[1];
+  }
   if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
   if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
 
@@ -465,13 +571,18 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
 
     eprop::CoefArgs ca;
     ca.psiK = L.psiK[sl]; ca.LK = L.LK[sl]; ca.ldv = L.ldv; ca.Bp = P.Bp;
-    ca.U = L.coefU[sl]; ca.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ca.H = L.coefH[sl];
+    ca.U = L.coefU[sl]; ca.V = P.na2 > 0 ? L.coefV[sl] : nullptr; ca.H = L.coefH[sl];
     ca.S = L.coefS[sl];
     ca.B = c.batch; ca.n_post = c.n_rec; ca.n_adaptive = c.n_adaptive;
-    ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(c.n_adaptive, eprop::kTileJ));
+    ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(P.na2, eprop::kTileJ));
     ca.steps = steps; ca.kpad = kpad; ca.ldc = P.ldc;
     ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta; ca.alpha = c.alpha; ca.thr = c.thr;
-    ca.W = L.coefW[sl]; ca.reset_through = c.reset_grad;
+    ca.W = L.coefW[sl]; ca.reset_through = P.rt;
+    ca.model = c.neuron_model;
+    for (int m = 0; m < 2; ++m) {
+      ca.gA[m][0] = (float)P.gen.A[m][0]; ca.gA[m][1] = (float)P.gen.A[m][1];
+      ca.gb[m] = (float)P.gen.b[m]; ca.gr[m] = (float)P.gen.r[m]; ca.gc[m] = (float)P.gen.c[m];
+    }
     if ((rc = check(ctx, eprop::launch_coef(ca, sc), "eligibility coefficient kernel"))) return rc;
   }
   if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_coef[sl], sc), "event record"))) return rc;
@@ -484,13 +595,13 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ta.ebar = L.ebar; ta.epsa = L.epsa; ta.epsv = L.epsv; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
     ta.n_split = L.n_split; ta.p8 = L.p8[sl];
     ta.zstart = L.zstart[sl];
-    ta.U = L.coefU[sl]; ta.V = c.n_adaptive > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
-    ta.W = L.coefW[sl]; ta.reset_through = c.reset_grad;
+    ta.U = L.coefU[sl]; ta.V = P.na2 > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
+    ta.W = L.coefW[sl]; ta.reset_through = P.rt;
     ta.S = L.coefS[sl];
     ta.B = c.batch; ta.n_pre = L.n_pre; ta.n_pre_pad = L.n_pre_pad; ta.n_post = c.n_rec; ta.ldj = L.ldj;
-    ta.n_adaptive = c.n_adaptive; ta.ldi = L.n_pre_pad;
+    ta.n_adaptive = P.na2; ta.ldi = L.n_pre_pad;
     ta.n_jt = (c.n_rec + eprop::kTileJ - 1) / eprop::kTileJ;
-    ta.n_jt_a = (c.n_adaptive + eprop::kTileJ - 1) / eprop::kTileJ;
+    ta.n_jt_a = (P.na2 + eprop::kTileJ - 1) / eprop::kTileJ;
     ta.ldc = P.ldc; ta.kpad = kpad;
     ta.kappa_K = (float)std::pow((double)c.kappa, (double)steps);
     ta.first = first;
@@ -618,6 +729,18 @@ int scratch_address(void** out) {
 }  // namespace
 
 extern "C" {
+
+int eprop_neuron_coefficients(const eprop_config* cfg, int32_t cls, float* out) {
+  std::string why;
+  if (!valid_config(cfg, &why)) return fail(nullptr, EPROP_EINVAL, why);
+  if (!out || (cls != 0 && cls != 1)) return fail(nullptr, EPROP_EINVAL, "out is NULL or cls not 0/1");
+  NeuronCoef k;
+  if (!derive_neuron(*cfg, cls, &k)) return fail(nullptr, EPROP_EINVAL, "neuron step is not linear in its state");
+  const double v[10] = {k.A[0][0], k.A[0][1], k.A[1][0], k.A[1][1], k.b[0], k.b[1],
+                        k.r[0], k.r[1], k.c[0], k.c[1]};
+  for (int q = 0; q < 10; ++q) out[q] = (float)v[q];
+  return EPROP_OK;
+}
 
 size_t eprop_workspace_bytes(const eprop_config* cfg) {
   std::string why;

@@ -66,6 +66,11 @@ struct FwdArgs {
   int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldk, ldn, jlist;  // ldj: row stride of psiK
   float alpha, rho, kappa, thr, beta, gamma_over_thr;
   int zgroup;                    // steps of p bytes written together (4, 8 or 16)
+  // neuron_model 1: h = A h_prev + b I + r z_prev, spike argument
+  // u = c . h - thr (the two-compartment neuron, coefficients derived on the
+  // host; v holds h0, a holds h1)
+  int model;
+  float mA[2][2], mb[2], mr[2], mc[2];
   const int* w16ok;              // 1: every layer's W16 is exact (drive summed as integers)
   size_t smem;
 };
@@ -116,6 +121,10 @@ struct CoefArgs {
   int B, n_post, n_adaptive, n_vcols, steps, kpad, ldc;
   float kappa, rho, beta, alpha, thr;
   int reset_through;
+  // model 1: the generic adjoint pass (coef_gen_kernel) of a step with
+  // H_I = A + psi_prev r c^T, F = b p, e = psi c . eps
+  int model;
+  float gA[2][2], gb[2], gr[2], gc[2];
 };
 hipError_t launch_coef(const CoefArgs& a, hipStream_t s);
 

@@ -388,6 +388,25 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     psv[q] = 0.0f;
     if (j < A.n_rec) {
       const float zp = zprev[j] ? 1.0f : 0.0f;
+      float x;
+      if (A.model == 1) {
+        // a step linear in its two state components with host-derived
+        // coefficients (the two-compartment neuron: h0 soma, h1 dendrite),
+        // each component summed in the order A h_prev, b I, r z_prev
+        float h1 = A.mA[1][0] * v[q];
+        h1 = h1 + A.mA[1][1] * ad[q];
+        h1 = h1 + A.mb[1] * I[q];
+        h1 = h1 + A.mr[1] * zp;
+        float h0 = A.mA[0][0] * v[q];
+        h0 = h0 + A.mA[0][1] * ad[q];
+        h0 = h0 + A.mb[0] * I[q];
+        h0 = h0 + A.mr[0] * zp;
+        float u = A.mc[0] * h0;
+        u = u + A.mc[1] * h1;
+        x = u - A.thr;
+        v[q] = h0;
+        ad[q] = h1;
+      } else {
       float vv = A.alpha * v[q];
       vv = vv + I[q];
       vv = vv - A.thr * zp;
@@ -396,9 +415,10 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       const float bj = (j < A.n_adaptive) ? A.beta : 0.0f;
       float th = bj * aa;
       th = A.thr + th;
-      const float x = vv - th;
+      x = vv - th;
       v[q] = vv;
       ad[q] = aa;
+      }
       z = x > 0.0f;
       znow[j] = z ? 1 : 0;
       const float u = 1.0f - fabsf(x) / A.thr;
@@ -895,16 +915,43 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
 //   reaches neither A_K nor V_K).
 struct Adjoint {
   float v = 0.0f, a = 0.0f, e = 0.0f;
-  __device__ __forceinline__ void step(float ps, float Lg, float alpha, float rho, float kappa,
-                                       float bt, float thr) {
+  __device__ __forceinline__ void step(const CoefArgs& A, float ps, float Lg, float bt) {
     const float te = e + Lg;
-    const float w = ps * (a + te - thr * v);
-    v = fmaf(alpha, v, w);
-    a = fmaf(rho, a, -bt * w);
-    e = kappa * te;
+    const float w = ps * (a + te - A.thr * v);
+    v = fmaf(A.alpha, v, w);
+    a = fmaf(A.rho, a, -bt * w);
+    e = A.kappa * te;
   }
+  __device__ __forceinline__ float coef(const CoefArgs&) const { return v; }
 };
 
+// The same adjoint for any neuron step that is linear in its two state
+// components (coefficients derived on the host): with the stored state
+// sigma = H_I eps before the next input, per step
+//   eps = sigma + b p;  e = psi (c . eps);  E = kappa E + e;  g += L E;
+//   sigma' = A eps + r e,
+// the adjoint of an output runs backwards as
+//   tE = lE + [Y = g] L;  le = tE + r . l;  w = psi le;
+//   l' = A^T l + c w;  lE = kappa tE,
+// and p's coefficient is b . l' (v: component 0, a: component 1).  With
+// A = diag(alpha, rho), b = (1, 0), r = (-thr, 1), c = (1, -beta) it is the
+// reset-kept LIF/ALIF recursion above.
+struct GenAdjoint {
+  float v = 0.0f, a = 0.0f, e = 0.0f;
+  __device__ __forceinline__ void step(const CoefArgs& A, float ps, float Lg, float) {
+    const float te = e + Lg;
+    const float le = fmaf(A.gr[1], a, fmaf(A.gr[0], v, te));
+    const float w = ps * le;
+    const float nv = fmaf(A.gc[0], w, fmaf(A.gA[1][0], a, A.gA[0][0] * v));
+    const float na = fmaf(A.gc[1], w, fmaf(A.gA[1][1], a, A.gA[0][1] * v));
+    v = nv;
+    a = na;
+    e = A.kappa * te;
+  }
+  __device__ __forceinline__ float coef(const CoefArgs& A) const { return fmaf(A.gb[1], a, A.gb[0] * v); }
+};
+
+template <typename Adj>
 __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   const int b = blockIdx.y;
@@ -927,18 +974,18 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
     }
   };
   // terminal adjoints: E_K, g, A_K, V_K
-  auto init = [](Adjoint (&y)[4]) {
-    y[0] = Adjoint{};
+  auto init = [](Adj (&y)[4]) {
+    y[0] = Adj{};
     y[0].e = 1.0f;
-    y[1] = Adjoint{};
-    y[2] = Adjoint{};
+    y[1] = Adj{};
+    y[2] = Adj{};
     y[2].a = 1.0f;
-    y[3] = Adjoint{};
+    y[3] = Adj{};
     y[3].v = 1.0f;
   };
   float mx[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   {
-    Adjoint y[4];
+    Adj y[4];
     init(y);
     for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
       float ps[kChunk], L[kChunk];
@@ -948,8 +995,8 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
         if (kChunk * c + e >= a.steps) continue;
 #pragma unroll
         for (int o = 0; o < 4; ++o) {
-          y[o].step(ps[e], o == 1 ? L[e] : 0.0f, a.alpha, a.rho, a.kappa, bt, a.thr);
-          mx[o] = fmaxf(mx[o], fabsf(y[o].v));
+          y[o].step(a, ps[e], o == 1 ? L[e] : 0.0f, bt);
+          mx[o] = fmaxf(mx[o], fabsf(y[o].coef(a)));
         }
       }
     }
@@ -959,7 +1006,7 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
   for (int o = 0; o < 4; ++o) sc[o] = ldexpf(1.0f, pair_exponent(mx[o]));
   const size_t rs = (size_t)a.ldc * kChunk;         // words between chunks
   const size_t off = ((size_t)b * kKC * a.ldc + j) * kChunk;
-  Adjoint y[4];
+  Adj y[4];
   init(y);
   for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
     float ps[kChunk], L[kChunk];
@@ -970,8 +1017,8 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
       const bool live = kChunk * c + e < a.steps;
 #pragma unroll
       for (int o = 0; o < 4; ++o) {
-        if (live) y[o].step(ps[e], o == 1 ? L[e] : 0.0f, a.alpha, a.rho, a.kappa, bt, a.thr);
-        x[o][e] = live ? y[o].v : 0.0f;
+        if (live) y[o].step(a, ps[e], o == 1 ? L[e] : 0.0f, bt);
+        x[o][e] = live ? y[o].coef(a) : 0.0f;
       }
     }
     store_pairs(a.U + off + c * rs, x[0], sc[0]);
@@ -1646,8 +1693,10 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 
 hipError_t launch_coef(const CoefArgs& a, hipStream_t s) {
   dim3 grid(cdiv(a.n_post, 256), a.B);
-  if (a.reset_through)
-    coef_rt_kernel<<<grid, 256, 0, s>>>(a);
+  if (a.model == 1)
+    coef_rt_kernel<GenAdjoint><<<grid, 256, 0, s>>>(a);
+  else if (a.reset_through)
+    coef_rt_kernel<Adjoint><<<grid, 256, 0, s>>>(a);
   else
     coef_kernel<<<grid, 256, 0, s>>>(a);
   return hipGetLastError();

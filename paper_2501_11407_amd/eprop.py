@@ -21,7 +21,7 @@ EPROP_OK, EPROP_EINVAL, EPROP_ENOSPACE, EPROP_EDEVICE, EPROP_ESTATE = 0, -1, -2,
 
 # Every function the header declares, in declaration order.
 SYMBOLS = (
-    "eprop_workspace_bytes", "eprop_init", "eprop_step", "eprop_run_sequence", "eprop_get_grads",
+    "eprop_neuron_coefficients", "eprop_workspace_bytes", "eprop_init", "eprop_step", "eprop_run_sequence", "eprop_get_grads",
     "eprop_reset", "eprop_status", "eprop_set_feedback", "eprop_set_online", "eprop_get_weights",
     "eprop_destroy", "eprop_sequence_static", "eprop_last_error",
     "eprop_profile_begin", "eprop_profile_end", "eprop_debug_buffer",
@@ -36,6 +36,8 @@ class eprop_config(ctypes.Structure):
         ("alpha", ctypes.c_float), ("rho", ctypes.c_float), ("kappa", ctypes.c_float),
         ("thr", ctypes.c_float), ("beta", ctypes.c_float), ("gamma", ctypes.c_float),
         ("reset_grad", ctypes.c_int32),
+        ("neuron_model", ctypes.c_int32), ("alpha_d", ctypes.c_float), ("coupling", ctypes.c_float),
+        ("bap", ctypes.c_float),
     ]
 
 
@@ -60,6 +62,7 @@ def load_library(path: str = LIB_PATH):
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     cfgp = ctypes.POINTER(eprop_config)
     sig = {
+        "eprop_neuron_coefficients": (ctypes.c_int, [cfgp, i32, ctypes.POINTER(ctypes.c_float)]),
         "eprop_workspace_bytes": (ctypes.c_size_t, [cfgp]),
         "eprop_init": (ctypes.c_int, [cfgp, vp, ctypes.c_size_t, vp, vp, ctypes.POINTER(vp)]),
         "eprop_step": (ctypes.c_int, [vp, vp, vp, vp]),
@@ -90,7 +93,18 @@ def make_config(shape) -> eprop_config:
     """C config from an EpropShape (or any object with the same fields)."""
     return eprop_config(shape.n_layers, shape.batch, shape.n_in, shape.n_rec, shape.n_out,
                         shape.recurrent, shape.n_adaptive, shape.alpha, shape.rho, shape.kappa,
-                        shape.thr, shape.beta, shape.gamma, int(getattr(shape, "reset_grad", 0)))
+                        shape.thr, shape.beta, shape.gamma, int(getattr(shape, "reset_grad", 0)),
+                        int(getattr(shape, "neuron_model", 0)), float(getattr(shape, "alpha_d", 0.0)),
+                        float(getattr(shape, "coupling", 0.0)), float(getattr(shape, "bap", 0.0)))
+
+
+def eprop_neuron_coefficients(cfg: eprop_config, cls: int):
+    """(A [2x2], b [2], r [2], c [2]) of the configured neuron model, derived
+    by the library on the host."""
+    out = (ctypes.c_float * 10)()
+    _check(load_library().eprop_neuron_coefficients(ctypes.byref(cfg), int(cls), out))
+    v = list(out)
+    return [[v[0], v[1]], [v[2], v[3]]], v[4:6], v[6:8], v[8:10]
 
 
 def _ptr(t: Optional[torch.Tensor]):

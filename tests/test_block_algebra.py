@@ -228,3 +228,76 @@ def test_binary_input_form_equals_recursion(K, beta):
                c * E0 + q * A0 + p @ Hp + Z * alpha * Hp[0])
         for r, x in zip(ref, got):
             assert abs(r - x) <= 1e-11 * (1 + abs(r)), (K, beta, ref, got)
+
+
+# ---------------------------------------------------------------- any linear two-component neuron
+# A neuron step linear in its state, h = A h_prev + b I + r z_prev with the
+# spike argument c . h - thr, has the per-synapse recursion (sigma: the
+# stored eligibility before the next input, H_I = A + psi_prev r c^T, F = b p)
+#     eps = sigma + b p_s;  e = psi_s (c . eps);  E = kappa E + e;  g += L_s E;
+#     sigma' = A eps + r e.
+# The adjoint pass of the eligibility kernel's coefficients is generic in
+# (A, b, r, c); with A = diag(alpha, rho), b = (1, 0), r = (-thr, 1),
+# c = (1, -beta) it is the reset-kept recursion above, and the two-compartment
+# neuron has A = [[alpha, g], [0, alpha_d]], b = (0, 1), r = (0 or -thr, q),
+# c = (1, 0).
+def step_by_step_gen(S0, E0, p, psi, L, kappa, A, b, r, c):
+    S, E, g = np.array(S0, float), E0, 0.0
+    for s in range(len(psi)):
+        eps = S + b * p[s]
+        e = psi[s] * (c @ eps)
+        E = kappa * E + e
+        g += L[s] * E
+        S = A @ eps + r * e
+    return S[0], S[1], E, g
+
+
+def block_form_gen(S0, E0, p, psi, L, kappa, A, b, r, c):
+    K = len(psi)
+    res = []
+    for Y in ("S0", "S1", "E", "g"):
+        l = np.array([1.0 if Y == "S0" else 0.0, 1.0 if Y == "S1" else 0.0])
+        lE = 1.0 if Y == "E" else 0.0
+        C = np.zeros(K)
+        for s in range(K - 1, -1, -1):
+            tE = lE + (L[s] if Y == "g" else 0.0)
+            le = tE + r @ l
+            w = psi[s] * le
+            l = A.T @ l + c * w
+            lE = kappa * tE
+            C[s] = b @ l
+        res.append(p @ C + l @ np.asarray(S0) + lE * E0)
+    return tuple(res)
+
+
+@pytest.mark.parametrize("K", [1, 3, 16, 100, 256])
+def test_generic_block_form_equals_recursion(K):
+    rng = np.random.default_rng(77 + K)
+    kappa = np.exp(-1 / 20)
+    for _ in range(10):
+        A = rng.normal(0, 0.5, (2, 2)) + np.diag([0.5, 0.5])
+        b, r, c = rng.normal(0, 1, 2), rng.normal(0, 1, 2), rng.normal(0, 1, 2)
+        p = (rng.random(K) < 0.3).astype(float)
+        psi = rng.uniform(0, 0.5, K) * (rng.random(K) < 0.6)
+        L = rng.normal(0, 1, K)
+        S0, E0 = rng.normal(0, 3, 2), rng.normal(0, 3)
+        ref = step_by_step_gen(S0, E0, p, psi, L, kappa, A, b, r, c)
+        got = block_form_gen(S0, E0, p, psi, L, kappa, A, b, r, c)
+        scale = 1 + max(abs(x) for x in ref)
+        for x, y in zip(ref, got):
+            assert abs(x - y) <= 1e-10 * scale, (K, ref, got)
+
+
+def test_generic_form_reduces_to_the_reset_kept_recursion():
+    rng = np.random.default_rng(5)
+    K, kappa, rho, alpha, thr, beta = 40, np.exp(-1 / 20), np.exp(-1 / 200), np.exp(-1 / 20), 0.6, 1.8
+    A, b = np.diag([alpha, rho]), np.array([1.0, 0.0])
+    r, c = np.array([-thr, 1.0]), np.array([1.0, -beta])
+    p = (rng.random(K) < 0.3).astype(float)
+    psi = rng.uniform(0, 0.5, K)
+    L = rng.normal(0, 1, K)
+    V0, A0, E0 = rng.normal(0, 3, 3)
+    ref = step_by_step_rt(V0, A0, E0, p, psi, L, kappa, rho, beta, alpha, thr)
+    got = step_by_step_gen([V0, A0], E0, p, psi, L, kappa, A, b, r, c)
+    for x, y in zip(ref, got):
+        assert abs(x - y) <= 1e-12 * (1 + abs(x))

@@ -4,6 +4,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 from paper_2501_11407_amd import eprop, synth
@@ -140,3 +141,52 @@ def test_static_entry_rejects_shapes_past_its_scratch_before_any_device_call():
     hdr = open(HEADER).read()
     assert "#define EPROP_STATIC_SCRATCH_BYTES (160u << 20)" in hdr
     assert eprop.STATIC_SCRATCH_BYTES == 160 << 20
+
+
+def _coef(shape, cls):
+    A, b, r, c = eprop.eprop_neuron_coefficients(eprop.make_config(shape), cls)
+    return np.array(A), np.array(b), np.array(r), np.array(c)
+
+
+def test_derived_neuron_coefficients():
+    # The library derives A, b, r, c of the neuron step by dual numbers; they
+    # must be the ones read off the model's equations (Eq. 8 with an adaptive
+    # threshold; the two-compartment neuron of the header), with the reset's
+    # own-spike term only when the reset path is kept.  H_I = A + psi r c^T is
+    # then the 2x2 block [[alpha, 0], [psi, rho - beta psi]] of an ALIF neuron.
+    f = np.float32
+    s = synth.EpropShape(batch=1, n_in=3, n_rec=4, n_out=2, T=1, n_adaptive=2)
+    A, b, r, c = _coef(s, 1)
+    np.testing.assert_array_equal(A, np.diag([f(s.alpha), f(s.rho)]))
+    np.testing.assert_array_equal(b, [1, 0])
+    np.testing.assert_array_equal(r, [0, 1])
+    np.testing.assert_array_equal(c, [1, -f(s.beta)])
+    psi = 0.25
+    H = A + psi * np.outer(r, c)
+    np.testing.assert_allclose(H, [[f(s.alpha), 0], [psi, f(s.rho) - f(s.beta) * psi]], rtol=1e-7)
+    _, _, _, c0 = _coef(s, 0)
+    np.testing.assert_array_equal(c0, [1, 0])                 # LIF: no adaptive threshold
+    _, _, rk, _ = _coef(s.replace(reset_grad=1), 1)
+    np.testing.assert_array_equal(rk, [-1, 1])                # the reset kept: -thr
+    t = synth.EpropShape(batch=1, n_in=3, n_rec=4, n_out=2, T=1, neuron_model=1)
+    A, b, r, c = _coef(t, 0)
+    np.testing.assert_array_equal(A, [[f(t.alpha), f(t.coupling)], [0, f(t.alpha_d)]])
+    np.testing.assert_array_equal(b, [0, 1])
+    np.testing.assert_array_equal(r, [0, f(t.bap)])
+    np.testing.assert_array_equal(c, [1, 0])
+    _, _, rk, _ = _coef(t.replace(reset_grad=1), 0)
+    np.testing.assert_array_equal(rk, [-1, f(t.bap)])
+
+
+def test_two_compartment_config_checks():
+    t = synth.EpropShape(batch=1, n_in=3, n_rec=4, n_out=2, T=1, neuron_model=1, n_adaptive=1)
+    assert eprop.eprop_workspace_bytes(eprop.make_config(t)) == 0
+    assert "adaptive" in eprop.eprop_last_error()
+    cfg = eprop.make_config(t.replace(n_adaptive=0))
+    cfg.neuron_model = 2
+    assert eprop.eprop_workspace_bytes(cfg) == 0
+    # two state components per synapse: about three trace arrays
+    u = synth.EpropShape(batch=4, n_in=300, n_rec=256, n_out=5, T=1, neuron_model=1)
+    lif = eprop.eprop_workspace_bytes(eprop.make_config(u.replace(neuron_model=0)))
+    two = eprop.eprop_workspace_bytes(eprop.make_config(u))
+    assert two > lif + 2 * 4 * u.batch * u.n_pre(0) * u.n_rec * 0.9

@@ -393,6 +393,91 @@ def test_reset_through_full_workload_and_split_calls():
     banner(f"{errs}")
 
 
+# ---------------------------------------------------------------- two-compartment neuron
+# A soma-dendrite neuron whose own spike feeds its dendrite: the forward takes
+# the step with the coefficients the library derives on the host, the
+# eligibility recursion has a full 2x2 Jacobian block per neuron (generic
+# adjoint coefficient pass, three traces per synapse).
+TC = dict(neuron_model=1, n_adaptive=0)
+TWO_COMP = {
+    "tc_ragged": (small(**TC, **DISTINCT), 2, 4.0),
+    "tc_ff": (small(recurrent=0, **TC, **DISTINCT), 6, 4.0),
+    "tc_two_layers": (small(batch=5, n_in=21, n_rec=45, n_out=4, n_layers=2, **TC, **DISTINCT), 4, 4.0),
+    "tc_blocks_256_50": (small(batch=6, T=306, **TC, **DISTINCT), 13, 4.0),
+    "tc_wide_1100": (small(batch=2, n_in=50, n_rec=1100, n_out=7, T=12, **TC), 9, 4.0),
+    "tc_positive_feedback": (small(bap=0.25, coupling=0.75, **TC, **DISTINCT), 8, 4.0),
+    "tc_classes_100": (small(batch=4, n_out=100, **TC, **DISTINCT), 14, 4.0),
+}
+
+
+@pytest.mark.parametrize("reset_grad", [0, 1])
+@pytest.mark.parametrize("name", list(TWO_COMP))
+def test_two_compartment_matches_oracle(name, reset_grad):
+    shape, seed, scale = TWO_COMP[name]
+    shape = shape.replace(reset_grad=reset_grad)
+    banner(f"two-compartment {name} {shape}")
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    gpu = gpu_run(wl)
+    errs, ref = check_against_oracle(wl, gpu)
+    assert ref.spikes.any()
+    banner(f"{name}: {errs}")
+
+
+def test_two_compartment_full_workload_split_calls_and_state():
+    # the recurrent workload's shape (B=32, 700 inputs, 256 neurons, T=250)
+    # with two-compartment neurons, every synapse, over three calls; the soma
+    # and dendrite state bit for bit
+    wl = synth.make_workload(synth.WORKLOADS["rlif_b32_n256_t250"].replace(neuron_model=1), 2)
+    banner("two-compartment rlif_b32_n256_t250 shape, every synapse, three calls")
+    ctx = eprop.EpropContext(wl.shape, wl.W, wl.Wout)
+    gpu = gpu_run(wl, chunks=[100, 7, 143], ctx=ctx)
+    errs, _ = check_against_oracle(wl, gpu)
+    T = 33
+    ref = oracle.run(wl.shape, wl.W, wl.Wout, wl.x, wl.labels, T=T, b_hi=wl.shape.batch,
+                     want_record=True)
+    ctx.reset()
+    x, labels = to_dev(wl, T)
+    ctx.run_sequence(x, labels)
+    torch.cuda.synchronize()
+    assert np.array_equal(ctx.debug("v", 0).cpu().numpy(), ref.record["v"][T - 1, 0].astype(np.float32))
+    assert np.array_equal(ctx.debug("a", 0).cpu().numpy(), ref.record["a"][T - 1, 0].astype(np.float32))
+    ctx.close()
+    banner(f"{errs}")
+
+
+@pytest.mark.parametrize("reset_grad", [0, 1])
+def test_two_compartment_every_chunk_count(reset_grad):
+    shape = small(n_rec=70, T=sum(EVERY_CHUNK_COUNT), reset_grad=reset_grad, **TC, **DISTINCT)
+    banner(f"two-compartment every chunk count, reset_grad={reset_grad}")
+    wl = synth.make_workload(shape, 21, input_scale=4.0)
+    gpu = gpu_run(wl, chunks=EVERY_CHUNK_COUNT)
+    errs, ref = check_against_oracle(wl, gpu)
+    assert ref.spikes.any()
+
+
+def test_two_compartment_with_feedback_and_online_weights():
+    # the two variants of the learning-signal row on the new neuron
+    shape, seed, scale = TWO_COMP["tc_ragged"]
+    wl = synth.make_workload(shape, seed, input_scale=scale)
+    fb = synth.make_feedback(shape, seed)
+    gpu = gpu_run(wl, feedback=fb)
+    check_against_oracle(wl, gpu, feedback=fb)
+    sh2 = small(n_adaptive=0, neuron_model=1, T=60, **DISTINCT)
+    wl2 = synth.make_workload(sh2, 41, input_scale=4.0)
+    every = 10
+    assert _online_margin(sh2, wl2, ONLINE_LR, every) > 1e-4
+    ref = oracle.run_online(sh2, wl2.W, wl2.Wout, wl2.x, wl2.labels, ONLINE_LR, every)
+    ctx = eprop.EpropContext(sh2, wl2.W, wl2.Wout)
+    ctx.set_online(ONLINE_LR, every)
+    g2 = gpu_run(wl2, ctx=ctx, chunks=[7, sh2.T - 7])
+    Wg, Wog = ctx.get_weights()
+    torch.cuda.synchronize()
+    ctx.close()
+    assert first_spike_mismatch(g2["spikes"], ref.spikes) is None
+    assert np.array_equal(Wg[0].cpu().numpy(), ref.W[0]) and np.array_equal(Wog[0].cpu().numpy(), ref.Wout[0])
+    assert rel_l2(g2["dW"][0], ref.dW[0]) <= 1e-4
+
+
 def test_silent_input_gives_zero_gradient():
     shape = small(n_adaptive=7)
     wl = synth.make_workload(shape, 4, input_scale=0.0)
