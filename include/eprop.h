@@ -286,11 +286,13 @@ int eprop_profile_end(eprop_ctx* ctx, double* total_ms, int32_t* n_launches, int
  * layer `layer` as left by the last step, for checking intermediate values.
  *   which: 0 = v, 1 = a, 2 = psi, 3 = L (learning signal), 4 = y (readout)
  *   fp32, rows = B, row stride *ld elements, *cols valid columns.
- *   which = 5: one int32 (rows = cols = ld = 1, any layer), 1 when the drive
- *   sums the weights as integers in units of 2^-14 (every weight is such a
- *   multiple, small enough that each partial sum is exact in fp32: the same
- *   result as the fp32 sum), 0 when it sums fp32 weights in ascending input
- *   order; valid once the work queued by init or reset has run.
+ *   which = 5: two int32 (rows = 1, cols = ld = 2, any layer): [0] is 1 when
+ *   every drive weight is k 2^-14 with integer |k| <= 32767, [1] the largest
+ *   |k|.  Then every step with at most 2^24 / [1] active presynaptic inputs
+ *   sums the weights as integers (each partial sum is then exact in fp32:
+ *   the same result as the fp32 sum); other steps, and all steps when [0] is
+ *   0, sum fp32 weights in ascending input order.  Valid once the work queued
+ *   by init, reset or an online update has run.
  */
 int eprop_debug_buffer(eprop_ctx* ctx, int32_t layer, int32_t which, const float** d_ptr,
                        int64_t* cols, int64_t* ld);

@@ -109,7 +109,7 @@ struct Plan {
   int rt = 0, na2 = 0;
   NeuronCoef gen{};                 // two-compartment neuron: derived step
   int* err_flag = nullptr;
-  int* w16ok = nullptr;             // 1: the int16 drive weights are exact (launch_pack16)
+  int* w16ok = nullptr;             // [2]: the int16 drive weights are exact, their largest |k| (launch_pack16)
   int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, ldc = 0, jlist = 0, out_splits = 1;
   size_t smem = 0;
   int zgroup = 1;
@@ -249,7 +249,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   }
   const size_t R = plan->rows;
   plan->err_flag = (int*)take(sizeof(int));
-  plan->w16ok = (int*)take(sizeof(int));
+  plan->w16ok = (int*)take(2 * sizeof(int));
   int rwmax = 0;
   size_t npre_total = 0;
   for (int l = 0; l < c.n_layers; ++l) {
@@ -990,7 +990,7 @@ int eprop_debug_buffer(eprop_ctx* ctx, int32_t layer, int32_t which, const float
     case 2: *d_ptr = L.psiK[ctx->last_slot] + tl * L.ldv; *cols = c.n_rec; *ld = L.ldv; break;
     case 3: *d_ptr = L.LK[ctx->last_slot] + tl * L.ldv; *cols = c.n_rec; *ld = L.ldv; break;
     case 4: *d_ptr = L.y; *cols = c.n_out; *ld = c.n_out; break;
-    case 5: *d_ptr = reinterpret_cast<const float*>(ctx->plan.w16ok); *cols = 1; *ld = 1; break;
+    case 5: *d_ptr = reinterpret_cast<const float*>(ctx->plan.w16ok); *cols = 2; *ld = 2; break;
     default: return fail(ctx, EPROP_EINVAL, "unknown buffer");
   }
   return EPROP_OK;

@@ -71,7 +71,7 @@ struct FwdArgs {
   // host; v holds h0, a holds h1)
   int model;
   float mA[2][2], mb[2], mr[2], mc[2];
-  const int* w16ok;              // 1: every layer's W16 is exact (drive summed as integers)
+  const int* w16ok;              // [0]: every layer's W16 is exact, [1]: their largest |k|
   size_t smem;
 };
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
@@ -171,11 +171,13 @@ hipError_t launch_pack(const float* src, int rows, int cols, float* dst, int ldd
                        int transpose, hipStream_t s);
 
 // Drive weights W [n_rec][n_pre] (row-major) -> W16 as FwdLayer::W16 for
-// QN = the forward's neurons per thread.  Clears *ok unless every weight is
-// k 2^-14 with integer |k| <= min(32767, (2^24 - 1) / n_pre): then each
-// partial sum of a drive is an integer below 2^24 in units of 2^-14, exact
-// in fp32 in any order, and summing k as integers gives the fp32 sum bit for
-// bit.  *ok is set to 1 by launch_set_flag before the layers are packed.
+// QN = the forward's neurons per thread.  ok[0] is cleared unless every
+// weight is k 2^-14 with integer |k| <= 32767, and ok[1] becomes the largest
+// |k| seen (atomic max).  A drive over at most 2^24 / max|k| active rows then
+// has every partial sum an integer of at most 2^24 units in any order, exact
+// in fp32, and summing k as integers gives the fp32 sequential sum bit for
+// bit; the forward decides this per step.  launch_set_flag sets ok[0] = value
+// and ok[1] = 0 before the layers are packed.
 hipError_t launch_pack16(const float* W, int n_rec, int n_pre, int16_t* W16, int qn, int* ok,
                          hipStream_t s);
 hipError_t launch_set_flag(int* flag, int value, hipStream_t s);

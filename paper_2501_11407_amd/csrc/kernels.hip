@@ -129,7 +129,8 @@ struct FwdLds {
   uint8_t* zc;
   uint8_t* xs;                   // [kFwdXSteps][n_in]: input spikes of steps t .. t+7, row t % 8
   bool xwords;                   // rows 4-byte aligned: input rows copied as 32-bit words
-  bool w16;                      // drive from the int16 weights (FwdLayer::W16)
+  bool w16;                      // the int16 weights are exact (FwdLayer::W16)
+  int w16max;                    // their largest |k|
   int rwmax, npad;
 };
 
@@ -308,10 +309,13 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   float I[QN];
 #pragma unroll
   for (int q = 0; q < QN; ++q) I[q] = 0.0f;
-  if (S.w16) {
-    // integer weights k (w = k 2^-14): the thread's QN of a row in one load
-    // of 2 QN bytes; integer sums are exact in any order and equal the fp32
-    // sequential sum
+  // integer weights k (w = k 2^-14, |k| <= 32767): with at most 2^24 / max|k|
+  // active rows every partial sum in any order is an integer of at most
+  // 2^24 units, exact in fp32, so the integer sum equals the fp32
+  // sequential sum; decided per step from the step's active rows
+  const bool w16 = S.w16 && (long long)total * S.w16max <= (1ll << 24);
+  if (w16) {
+    // the thread's QN of a row in one load of 2 QN bytes
     constexpr int UB16 = QN == 1 ? 32 : 64 / QN;
     typedef int16_t i16v __attribute__((ext_vector_type(QN)));
     int isum[QN];
@@ -334,7 +338,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
 #pragma unroll
     for (int q = 0; q < QN; ++q) I[q] = (float)isum[q] * 0x1p-14f;
   }
-  for (int k0 = 0; !S.w16 && k0 < total; k0 += UB) {
+  for (int k0 = 0; !w16 && k0 < total; k0 += UB) {
     const int ent = S.mrg[min(k0 + (lane & (UB - 1)), total - 1)];   // past the end: the last row
     float wv[UB][QN];
 #pragma unroll
@@ -585,7 +589,8 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu((QN
   S.zc = S.zb + A.zgroup * npre_total;         // [n_layers][2][npad]
   S.xs = S.zc + NL * 2 * S.npad;               // [kFwdXSteps][n_in]
   S.xwords = (A.n_in & 3) == 0 && ((uintptr_t)A.x & 3) == 0;
-  S.w16 = *A.w16ok != 0;
+  S.w16 = A.w16ok[0] != 0;
+  S.w16max = A.w16ok[1];
 
   for (int e = threadIdx.x; e < A.zgroup * npre_total; e += kFwdThreads) S.zb[e] = 0;
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
@@ -1527,39 +1532,65 @@ __global__ void loss_kernel(const double* lossacc, int B, int n_layers, size_t l
   *out = s;
 }
 
+// Workgroups of the weight-packing kernels: a fixed grid walks the weights,
+// so that the largest |k| takes one global atomic per workgroup.
+constexpr int kPackBlocks = 1024;
+
+// The largest |k| of a workgroup's exact weights (kmax: the thread's) into
+// ok[1]: a maximum in shared memory, then one global atomic per workgroup
+// (the result does not depend on the order).
+__device__ __forceinline__ void max_k(int* ok, int kmax) {
+  __shared__ int smax;
+  if (threadIdx.x == 0) smax = 0;
+  __syncthreads();
+  if (kmax > 0) atomicMax(&smax, kmax);
+  __syncthreads();
+  if (threadIdx.x == 0 && smax > 0) atomicMax(ok + 1, smax);
+}
+
 __global__ __launch_bounds__(256) void pack16_kernel(const float* W, int n_rec, int n_pre,
-                                                     int16_t* W16, int qn, int lim, int* ok) {
-  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long long)n_rec * n_pre) return;
-  const int j = (int)(idx / n_pre), i = (int)(idx % n_pre);
-  const float k = W[idx] * 16384.0f;
-  const bool exact = k == rintf(k) && fabsf(k) <= (float)lim;
-  if (!exact) *ok = 0;   // every thread that finds one writes the same value
-  W16[(size_t)i * (qn * kFwdThreads) + (size_t)(j % kFwdThreads) * qn + j / kFwdThreads] =
-      exact ? (int16_t)k : (int16_t)0;
+                                                     int16_t* W16, int qn, int* ok) {
+  const long long n = (long long)n_rec * n_pre;
+  int kmax = 0;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < n;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const float k = W[idx] * 16384.0f;
+    const bool exact = k == rintf(k) && fabsf(k) <= 32767.0f;
+    if (!exact) ok[0] = 0;   // every thread that finds one writes the same value
+    else kmax = max(kmax, (int)fabsf(k));
+    const int j = (int)(idx / n_pre), i = (int)(idx % n_pre);
+    W16[(size_t)i * (qn * kFwdThreads) + (size_t)(j % kFwdThreads) * qn + j / kFwdThreads] =
+        exact ? (int16_t)k : (int16_t)0;
+  }
+  max_k(ok, kmax);
 }
 
 // Weights on the 2^-14 grid: rint(x 2^14) 2^-14 in fp64 (ties to even).
 __device__ __forceinline__ float on_grid(double x) { return (float)(rint(x * 16384.0) / 16384.0); }
 
 // One thread per (i, j), j fastest (coalesced over the accumulators and Wt).
-__global__ __launch_bounds__(256) void online_w_kernel(OnlineArgs a, int lim) {
-  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long long)a.n_rec * a.n_pre) return;
-  const int i = (int)(idx / a.n_rec), j = (int)(idx % a.n_rec);
-  const float w0 = a.W0[(size_t)j * a.n_pre + i];
-  float wn = w0;
-  if (!(a.recurrent && i == a.n_inl + j)) {
-    double g = 0.0;
-    for (int sp = 0; sp < a.n_split; ++sp) g += a.acc[sp * a.acc_stride + (size_t)i * a.ldj + j];
-    wn = on_grid((double)w0 - a.lr * g);
+__global__ __launch_bounds__(256) void online_w_kernel(OnlineArgs a) {
+  const long long n = (long long)a.n_rec * a.n_pre;
+  int kmax = 0;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < n;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int i = (int)(idx / a.n_rec), j = (int)(idx % a.n_rec);
+    const float w0 = a.W0[(size_t)j * a.n_pre + i];
+    float wn = w0;
+    if (!(a.recurrent && i == a.n_inl + j)) {
+      double g = 0.0;
+      for (int sp = 0; sp < a.n_split; ++sp) g += a.acc[sp * a.acc_stride + (size_t)i * a.ldj + j];
+      wn = on_grid((double)w0 - a.lr * g);
+    }
+    a.Wt[(size_t)i * a.ldw + j] = wn;
+    const float k = wn * 16384.0f;
+    const bool exact = k == rintf(k) && fabsf(k) <= 32767.0f;
+    if (!exact) a.ok[0] = 0;   // every thread that finds one writes the same value
+    else kmax = max(kmax, (int)fabsf(k));
+    a.W16[(size_t)i * (a.qn * kFwdThreads) + (size_t)(j % kFwdThreads) * a.qn + j / kFwdThreads] =
+        exact ? (int16_t)k : (int16_t)0;
   }
-  a.Wt[(size_t)i * a.ldw + j] = wn;
-  const float k = wn * 16384.0f;
-  const bool exact = k == rintf(k) && fabsf(k) <= (float)lim;
-  if (!exact) *a.ok = 0;   // every thread that finds one writes the same value
-  a.W16[(size_t)i * (a.qn * kFwdThreads) + (size_t)(j % kFwdThreads) * a.qn + j / kFwdThreads] =
-      exact ? (int16_t)k : (int16_t)0;
+  max_k(a.ok, kmax);
 }
 
 // One thread per (j, k): WoutT[j][k].
@@ -1587,7 +1618,10 @@ __global__ __launch_bounds__(256) void unpack_kernel(const float* Wt, int ldw, c
 }
 
 __global__ void set_flag_kernel(int* flag, int value) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) *flag = value;
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    flag[0] = value;
+    flag[1] = 0;
+  }
 }
 
 // 16-byte stores over the aligned body, byte stores over the ragged ends;
@@ -1751,14 +1785,12 @@ int forward_qn(int n_rec) {
 hipError_t launch_pack16(const float* W, int n_rec, int n_pre, int16_t* W16, int qn, int* ok,
                          hipStream_t s) {
   const long long n = (long long)n_rec * n_pre;
-  const int lim = (int)std::min<long long>(32767, ((1LL << 24) - 1) / std::max(1, n_pre));
-  pack16_kernel<<<cdiv(n, 256), 256, 0, s>>>(W, n_rec, n_pre, W16, qn, lim, ok);
+  pack16_kernel<<<std::min(kPackBlocks, cdiv(n, 256)), 256, 0, s>>>(W, n_rec, n_pre, W16, qn, ok);
   return hipGetLastError();
 }
 
 hipError_t launch_online_update(const OnlineArgs& a, hipStream_t s) {
-  const int lim = (int)std::min<long long>(32767, ((1LL << 24) - 1) / std::max(1, a.n_pre));
-  online_w_kernel<<<cdiv((long long)a.n_rec * a.n_pre, 256), 256, 0, s>>>(a, lim);
+  online_w_kernel<<<std::min(kPackBlocks, cdiv((long long)a.n_rec * a.n_pre, 256)), 256, 0, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   online_wout_kernel<<<cdiv((long long)a.n_rec * a.K, 256), 256, 0, s>>>(a);

@@ -346,13 +346,19 @@ class EpropContext:
         return flat.view(rows, ld)[:, :cols].clone()
 
     def integer_drive(self) -> bool:
-        """Whether the drive sums the weights as integers in units of 2**-14
-        (every weight on that grid and small enough), else fp32 in ascending
-        input order; both give the same result where the first applies."""
+        """Whether every drive weight is an int16 multiple of 2**-14, so that
+        steps with few enough active inputs sum them as integers (else fp32 in
+        ascending input order; both give the same result where the first
+        applies)."""
+        return self.integer_weights()[0]
+
+    def integer_weights(self):
+        """(every weight an int16 multiple of 2**-14, the largest |k|)."""
         ptr, _, _ = eprop_debug_buffer(self.ctx, 0, 5)
         off = ptr - self.workspace.data_ptr()
         torch.cuda.synchronize(self.device)
-        return bool(self.workspace[off:off + 4].view(torch.int32).item())
+        v = self.workspace[off:off + 8].view(torch.int32).cpu().tolist()
+        return bool(v[0]), int(v[1])
 
     # -- helpers
     def new_spike_buffer(self, T: Optional[int] = None) -> torch.Tensor:

@@ -137,6 +137,29 @@ def test_large_grid_weight_takes_the_float_drive():
     check_against_oracle(wl, gpu)
 
 
+def test_integer_drive_decided_per_step():
+    # int16 weights up to |k| = 32767 (2.0): steps with more than 512 active
+    # inputs take the fp32 drive, the others the integer drive; both must give
+    # the oracle's sequential fp32 sums bit for bit
+    shape = small(batch=2, n_in=1000, n_rec=40, n_out=3, T=30, n_adaptive=20, **DISTINCT)
+    wl = synth.make_workload(shape, 61)
+    rng = np.random.default_rng(61)
+    k = rng.integers(-32767, 32768, size=wl.W[0].shape)
+    k[0, 0] = 32767
+    wl.W[0][:] = (k * 2.0 ** -14).astype(np.float32)
+    wl.x[:] = 0
+    for t in range(shape.T):
+        rate = 0.6 if t % 3 == 0 else 0.01
+        wl.x[t] = rng.random((shape.batch, shape.n_in)) < rate
+    ctx = eprop.EpropContext(shape, wl.W, wl.Wout)
+    assert ctx.integer_weights() == (True, 32767)
+    gpu = gpu_run(wl, ctx=ctx)
+    ctx.close()
+    errs, ref = check_against_oracle(wl, gpu)
+    assert ref.spikes.any()
+    assert wl.x[0].sum(axis=1).max() > 512 and wl.x[1].sum(axis=1).max() < 512
+
+
 def test_drive_path_follows_the_weights_over_resets():
     shape, seed, scale = RAGGED["ralif_ragged_na13"]
     wl = synth.make_workload(shape, seed, input_scale=scale)

@@ -1,10 +1,11 @@
 """The integer drive's exactness argument, checked on the CPU.
 
-When every weight is k 2^-14 with integer |k| <= min(32767, (2^24 - 1) / N_pre),
-every partial sum of a drive is an integer below 2^24 in units of 2^-14, so
-the fp32 sum in ascending input order (what the fp32 drive and the oracle
-compute) is exact and equals the integer sum of the k times 2^-14.  The GPU
-relies on this to sum int16 weights as integers in any order.
+When every weight is k 2^-14 with integer |k| <= 32767 and a step has n active
+inputs with n max|k| <= 2^24, every partial sum of its drive is an integer of
+at most 2^24 in units of 2^-14, so the fp32 sum in ascending input order (what
+the fp32 drive and the oracle compute) is exact and equals the integer sum of
+the k times 2^-14.  The GPU relies on this to sum int16 weights as integers in
+any order at such steps (and takes the fp32 drive at the others).
 """
 import numpy as np
 import pytest
@@ -42,3 +43,17 @@ def test_past_the_bound_the_orders_can_differ():
     w = (k * 2.0 ** -14).astype(np.float32)
     sums = {float(fp32_sequential(w[rng.permutation(len(w))])) for _ in range(10)}
     assert len(sums) > 1
+
+
+@pytest.mark.parametrize("maxk", [32767, 4866, 100])
+def test_bound_in_active_rows(maxk):
+    # n active rows with n * maxk <= 2^24: exact in any order, at the bound too
+    rng = np.random.default_rng(maxk)
+    n = (2 ** 24) // maxk
+    for trial in range(6):
+        k = rng.integers(-maxk, maxk + 1, size=n)
+        if trial == 0:
+            k[:] = maxk
+        w = (k * 2.0 ** -14).astype(np.float32)
+        order = rng.permutation(n)
+        assert fp32_sequential(w[order]) == np.float32(int(k.sum()) * 2.0 ** -14)
