@@ -321,10 +321,8 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     for (int sl = 0; sl < kSlots; ++sl) L.zstart[sl] = (float*)take(sizeof(float) * B * L.n_pre_pad);
   }
   const size_t npad4 = round_up(N, 4);
-  size_t npre_max = 0;
-  for (const Layer& L : plan->layers) npre_max = std::max<size_t>(npre_max, L.n_pre);
   const size_t smem_base = sizeof(int) * (eprop::kFwdWaves * ((size_t)rwmax + (size_t)c.n_layers * plan->jlist) +
-                                          npre_max + 2 * eprop::kFwdWaves + 2) +
+                                          2 * eprop::kFwdWaves + 2) +
                            sizeof(float) * ((size_t)2 * c.n_layers * eprop::kFwdWaves * K + (size_t)c.n_layers * K +
                                             npre_total) +
                            (size_t)c.n_layers * 2 * npad4 + (size_t)eprop::kFwdXSteps * c.n_in;

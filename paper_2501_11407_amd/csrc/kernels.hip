@@ -123,7 +123,7 @@ __device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChu
 //      softmax, delta = softmax - onehot(label), cross-entropy into the loss.
 // The learning signal L = W_out^T delta is one GEMM over the whole block.
 struct FwdLds {
-  int* act; int* mrg; int* spk; int* cnt; float* part; float* sy; float* szb;
+  int* act; int* spk; int* cnt; float* part; float* sy; float* szb;
   uint8_t* zb;                   // [npre_total][zgroup]: p of the last zgroup steps
   int npre_total;
   uint8_t* zc;
@@ -242,9 +242,11 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   const bool defer = A.K_out <= kWave;
   if (defer && w == kSoftWave && t > 1) dk = softmax_lanes(A, part, yk, label, loss);
 
-  // 1. presynaptic vector, its filter, ordered active lists
+  // 1. presynaptic vector: each wave lists the indices of its contiguous
+  // slice of p that are 1, in ascending order, and keeps the step's p bytes
   const int rw = Ly.rows_per_wave;
   const int i_beg = w * rw, i_end = min(Ly.n_pre, i_beg + rw);
+  const int zslot = t & (A.zgroup - 1);
   int n_act = 0;
   for (int base = i_beg; base < i_end; base += kWave) {
     const int i = base + lane;
@@ -252,9 +254,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     if (i < i_end) {
       const uint8_t sv = (i < Ly.n_inl) ? inp[i] : zprev[i - Ly.n_inl];
       on = sv != 0;
-      const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
-      szb[i] = zv;
-      zring[i * A.zgroup + (t & (A.zgroup - 1))] = on ? kPByte : 0;
+      zring[i * A.zgroup + zslot] = on ? kPByte : 0;
     }
     const unsigned long long m = __ballot(on);
     if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
@@ -262,18 +262,41 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   }
   if (lane == 0) S.cnt[w] = n_act;
   lds_barrier();
+  // The waves' lists in wave order are the ascending list of active rows:
+  // every lane holds the counts, and entry e lies in the last wave whose
+  // list starts at or before e (such a wave is never empty).
+  int offs[kFwdWaves];
+  int total = 0;
   {
-    // offset of this wave's list: the counts of the waves before it (one
-    // LDS read, then lane reads without waits)
     const int cl = (lane < kFwdWaves) ? S.cnt[lane] : 0;
-    int off = 0;
 #pragma unroll
-    for (int ww = 0; ww < kFwdWaves; ++ww)
-      if (ww < w) off += __builtin_amdgcn_readlane(cl, ww);
-    for (int k = lane; k < n_act; k += kWave) S.mrg[off + k] = S.act[w * S.rwmax + k];
-    if (w == kFwdWaves - 1 && lane == 0) S.cnt[2 * kFwdWaves] = off + n_act;
+    for (int ww = 0; ww < kFwdWaves; ++ww) {
+      offs[ww] = total;
+      total += __builtin_amdgcn_readlane(cl, ww);
+    }
   }
-  lds_barrier();
+  auto list_entry = [&](int e) {
+    int ww = 0, o = 0;
+#pragma unroll
+    for (int v = 1; v < kFwdWaves; ++v)
+      if (e >= offs[v]) {
+        ww = v;
+        o = offs[v];
+      }
+    return S.act[ww * S.rwmax + (e - o)];
+  };
+  // The presynaptic filter of the wave's rows, off the critical path: done
+  // while the drive's loads are in flight (from the p bytes kept above).
+  bool filtered = false;
+  auto filter_rows = [&]() {
+    if (filtered) return;
+    filtered = true;
+    for (int i = i_beg + lane; i < i_end; i += kWave) {
+      const bool on = zring[i * A.zgroup + zslot] != 0;
+      const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
+      szb[i] = zv;
+    }
+  };
 
   // 2. drive and neuron step.  Rows of Wt are padded to a multiple of the
   // workgroup size; chunks q with q*kFwdThreads >= n_rec are skipped (QN is
@@ -281,7 +304,6 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // lane u reads list entry k0 + u, every wave takes the entries from its
   // lanes, and each row's load is a scalar row base plus the lane offset.
   constexpr int UB = QN >= 32 ? 1 : 32 / QN;
-  const int total = S.cnt[2 * kFwdWaves];
   // Input spikes of step t+kFwdXSteps: loaded here, under the drive loads,
   // and written after them into the staging row of step t, which this step's
   // list has already read.
@@ -322,13 +344,16 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
 #pragma unroll
     for (int q = 0; q < QN; ++q) isum[q] = 0;
     for (int k0 = 0; k0 < total; k0 += UB16) {
-      const int ent = S.mrg[min(k0 + (lane & (UB16 - 1)), total - 1)];
+      const int ent = list_entry(min(k0 + (lane & (UB16 - 1)), total - 1));
       i16v wk[UB16];
 #pragma unroll
       for (int u = 0; u < UB16; ++u) {
         const int i = __builtin_amdgcn_readlane(ent, u);
         wk[u] = *(const i16v*)(Ly.W16 + (size_t)i * (QN * kFwdThreads) + (size_t)tid * QN);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      filter_rows();
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < UB16; ++u)
         if (k0 + u < total)
@@ -339,7 +364,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     for (int q = 0; q < QN; ++q) I[q] = (float)isum[q] * 0x1p-14f;
   }
   for (int k0 = 0; !w16 && k0 < total; k0 += UB) {
-    const int ent = S.mrg[min(k0 + (lane & (UB - 1)), total - 1)];   // past the end: the last row
+    const int ent = list_entry(min(k0 + (lane & (UB - 1)), total - 1));   // past the end: the last row
     float wv[UB][QN];
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
@@ -351,12 +376,16 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
                        ? *(const float*)(rowp + tidoff + (uint32_t)q * kFwdThreads * 4u)
                        : 0.0f;
     }
+    __builtin_amdgcn_sched_barrier(0);
+    filter_rows();
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < UB; ++u)
       if (k0 + u < total)
 #pragma unroll
         for (int q = 0; q < QN; ++q) I[q] += wv[u][q];
   }
+  filter_rows();   // (no active row this step)
   if constexpr (LI == 0) {
     if (xpre) {
       uint8_t* xs = S.xs + (t % kFwdXSteps) * A.n_in;
@@ -575,10 +604,8 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu((QN
   S.rwmax = A.L[0].rows_per_wave;
   if constexpr (NL > 1) S.rwmax = max(S.rwmax, A.L[1].rows_per_wave);
   S.npad = (A.n_rec + 3) & ~3;
-  const int npre_max = max(A.L[0].n_pre, NL > 1 ? A.L[1].n_pre : 0);
   S.act = (int*)smem;                          // [waves][rwmax]
-  S.mrg = S.act + kFwdWaves * S.rwmax;         // [npre_max]
-  S.spk = S.mrg + npre_max;                    // [n_layers][waves][jlist]
+  S.spk = S.act + kFwdWaves * S.rwmax;         // [n_layers][waves][jlist]
   S.cnt = S.spk + NL * kFwdWaves * A.jlist;    // [2 * waves + 2]
   S.part = (float*)(S.cnt + 2 * kFwdWaves + 2);   // [n_layers][2][waves][K_out]
   S.sy = S.part + NL * 2 * kFwdWaves * A.K_out;   // [n_layers][K_out]
