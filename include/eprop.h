@@ -258,7 +258,7 @@ void eprop_destroy(eprop_ctx* ctx);
  * or from several host threads) race; calls queued on one stream do not.
  * Each call clears what it needs itself.  Errors: eprop_last_error(NULL).
  */
-#define EPROP_STATIC_SCRATCH_BYTES (160u << 20)
+#define EPROP_STATIC_SCRATCH_BYTES (256u << 20)
 int eprop_sequence_static(const eprop_config* cfg, const float* const* d_weights,
                           const uint8_t* d_x, int32_t T, const int32_t* d_labels,
                           uint32_t* d_spikes, float* const* d_grads, double* d_loss,

@@ -42,19 +42,21 @@ void choose_splits(int M, int N, int K, int max_splits, int* splits, int* k_chun
 // per-step vectors for this many steps, independent of the sequence length.
 using eprop::kBlockSteps;
 
-// Per-block buffers rotate through kSlots slots: the forward of block k may
-// start once the eligibility pass of block k - kSlots has released its slot,
-// so the forward runs up to kSlots - 1 blocks ahead of the eligibility work.
-constexpr int kSlots = 2;
+// Per-block buffers rotate through the plan's slots (kSlots, or one on a
+// single stream): the forward of block k may start once the eligibility pass
+// of block k - kSlots has released its slot.  With three, the forward, the
+// passes between it and the eligibility kernel, and the eligibility kernel
+// of three consecutive blocks run at once, and a block costs the longest of
+// the three rather than the sum of two of them.
+constexpr int kSlots = 3;
 
 struct Layer {
   int n_inl = 0, n_pre = 0;
   int n_pre_pad = 0;   // n_pre rounded to the eligibility kernel's row group
   int ldj = 0;    // n_rec rounded to 4: row stride of traces and accumulators
   int ldv = 0;    // n_rec rounded to 256: row stride of psiK, LK
-  int ldw = 0;    // n_rec rounded to the forward workgroup size: row stride of Wt
+  int ldw = 0;    // 512 QN (forward positions): row stride of Wt
   int16_t* W16 = nullptr;   // the drive weights times 2^14 as int16 (FwdLayer::W16)
-  int rows_per_wave = 0;
   const float* W_src = nullptr;
   const float* Wout_src = nullptr;
   const float* Fb_src = nullptr;         // feedback matrix of the learning signal (NULL: W_out)
@@ -62,7 +64,7 @@ struct Layer {
   float *v, *a, *ztil, *zbar, *y;        // neuron, filter and readout state
   uint8_t* z;                            // spikes of the last step
   double* lossacc;                       // [B]
-  // per-block vectors in kSlots slots: the forward of block k+1 fills one
+  // per-block vectors in up to kSlots slots: the forward of block k+1 fills one
   // while the eligibility pass of block k reads another
   float *psiK[kSlots], *LK[kSlots], *deltaK[kSlots], *ztK[kSlots];
   // the binary presynaptic values (one byte per step), and the block
@@ -107,11 +109,18 @@ struct Plan {
   // three-trace recursion (reset path kept, or the two-compartment neuron),
   // and the neurons whose second state component has per-synapse traces
   int rt = 0, na2 = 0;
+  int slots = kSlots;               // per-block buffer sets in use
   NeuronCoef gen{};                 // two-compartment neuron: derived step
   int* err_flag = nullptr;
   int* w16ok = nullptr;             // [2]: the int16 drive weights are exact, their largest |k| (launch_pack16)
+  // the first layer's input drive of a block and its active-input counts
+  // (launch_input_drive), in two buffers: the next block's may be computed
+  // while the forward of the current one reads the other
+  float* Iin[2] = {};
+  int* nin[2] = {};
   int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, ldc = 0, jlist = 0, out_splits = 1;
   size_t smem = 0;
+  int svc = 0;                      // the forward's service wave (FwdArgs::svc)
   int zgroup = 1;
   size_t bytes = 0;
 };
@@ -222,9 +231,11 @@ bool derive_neuron(const eprop_config& cfg, int cls, NeuronCoef* out) {
   return true;
 }
 
-// Lays the workspace out (base == nullptr: sizing only).
-void make_plan(const eprop_config& c, char* base, Plan* plan) {
+// Lays the workspace out (base == nullptr: sizing only) with `slots` sets of
+// per-block buffers.
+void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots) {
   plan->cfg = c;
+  plan->slots = slots;
   plan->layers.assign(c.n_layers, Layer());
   plan->rt = (c.reset_grad || c.neuron_model == 1) ? 1 : 0;
   plan->na2 = c.neuron_model == 1 ? c.n_rec : c.n_adaptive;
@@ -242,7 +253,8 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   plan->ldk = (int)round_up(K, 32);
   plan->ldn = (int)round_up(N, 32);
   plan->ldc = (int)round_up(N, eprop::kColPad);
-  plan->jlist = (int)(round_up(N, eprop::kFwdThreads) / eprop::kFwdThreads * 64);
+  const int qn = eprop::forward_qn((int)N);
+  plan->jlist = qn * 64;   // a wave's neurons
   {
     int dummy;
     choose_splits(c.n_out, c.n_rec, (int)(KM * plan->Bp), kMaxOutSplits, &plan->out_splits, &dummy);
@@ -250,8 +262,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
   const size_t R = plan->rows;
   plan->err_flag = (int*)take(sizeof(int));
   plan->w16ok = (int*)take(2 * sizeof(int));
-  int rwmax = 0;
-  size_t npre_total = 0;
+  size_t fwd_rows = 0;   // rows whose filter the forward keeps: recurrent rows of layer 1, all of layer 2
   for (int l = 0; l < c.n_layers; ++l) {
     Layer& L = plan->layers[l];
     L.n_inl = (l == 0) ? c.n_in : c.n_rec;
@@ -259,13 +270,11 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.n_pre_pad = (int)round_up(L.n_pre, eprop::kRowPad);
     L.ldj = (int)round_up(N, 4);
     L.ldv = (int)round_up(N, 256);
-    L.ldw = (int)round_up(N, eprop::kFwdThreads);
-    L.rows_per_wave = (int)round_up((L.n_pre + eprop::kFwdWaves - 1) / eprop::kFwdWaves, 64);
-    rwmax = std::max(rwmax, L.rows_per_wave);
-    npre_total += L.n_pre;
+    L.ldw = qn * eprop::kFwdThreads;
+    fwd_rows += (size_t)(l == 0 ? L.n_pre - L.n_inl : L.n_pre);
     const size_t np = L.n_pre, npp = L.n_pre_pad;
     L.Wt = (float*)take(sizeof(float) * np * L.ldw);
-    L.W16 = (int16_t*)take(sizeof(int16_t) * np * eprop::forward_qn(N) * eprop::kFwdThreads);
+    L.W16 = (int16_t*)take(sizeof(int16_t) * np * L.ldw);
     L.WoutT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.FbT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.v = (float*)take(sizeof(float) * B * N);
@@ -275,7 +284,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     L.y = (float*)take(sizeof(float) * B * K);
     L.z = (uint8_t*)take(B * N);
     L.lossacc = (double*)take(sizeof(double) * B);
-    for (int sl = 0; sl < kSlots; ++sl) {
+    for (int sl = 0; sl < slots; ++sl) {
       L.psiK[sl] = (float*)take(sizeof(float) * R * L.ldv);
       L.LK[sl] = (float*)take(sizeof(float) * R * L.ldv);
       L.deltaK[sl] = (float*)take(sizeof(float) * R * plan->ldk);
@@ -305,9 +314,13 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
     // component's eligibility per synapse as well
     L.epsv = plan->rt ? (float*)take(sizeof(float) * B * npp * ldc) : nullptr;
   }
+  for (int k = 0; k < 2; ++k) {
+    plan->Iin[k] = (float*)take(sizeof(float) * KM * B * qn * eprop::kFwdThreads);
+    plan->nin[k] = (int*)take(sizeof(int) * KM * B);
+  }
   for (Layer& L : plan->layers) {
     const size_t ldc = plan->ldc;
-    for (int sl = 0; sl < kSlots; ++sl) {
+    for (int sl = 0; sl < slots; ++sl) {
       // p: one byte per row and step; coefficients: a scaled fp16 pair per
       // value (4 bytes)
       L.p8[sl] = (uint8_t*)take((size_t)B * L.n_pre_pad * KM);
@@ -318,24 +331,30 @@ void make_plan(const eprop_config& c, char* base, Plan* plan) {
       const int planes = plan->rt ? eprop::kScalarPlanesRT : eprop::kScalarPlanes;
       L.coefS[sl] = (float*)take(sizeof(float) * planes * B * ldc);
     }
-    for (int sl = 0; sl < kSlots; ++sl) L.zstart[sl] = (float*)take(sizeof(float) * B * L.n_pre_pad);
+    for (int sl = 0; sl < slots; ++sl) L.zstart[sl] = (float*)take(sizeof(float) * B * L.n_pre_pad);
   }
-  const size_t npad4 = round_up(N, 4);
-  const size_t smem_base = sizeof(int) * (eprop::kFwdWaves * ((size_t)rwmax + (size_t)c.n_layers * plan->jlist) +
-                                          2 * eprop::kFwdWaves + 2) +
-                           sizeof(float) * ((size_t)2 * c.n_layers * eprop::kFwdWaves * K + (size_t)c.n_layers * K +
-                                            npre_total) +
-                           (size_t)c.n_layers * 2 * npad4 + (size_t)eprop::kFwdXSteps * c.n_in;
-  // the binary presynaptic bytes are written 16 steps at a time (one 16-byte
-  // record per row) when that keeps the forward's shared memory small enough
-  // for an eligibility workgroup to share its compute unit, else 8 or 4
+  // the forward's shared memory (FwdLds): spike lists and their lengths by
+  // step parity, the block's input counts, readout partial sums and outputs,
+  // the filter of its rows, their p bytes, the spike bytes
+  const size_t npad4 = round_up(N, 4), NL = c.n_layers, W = eprop::kFwdWaves;
+  const size_t smem_base = sizeof(int) * (NL * 2 * W * plan->jlist + NL * 2 * W + KM) +
+                           sizeof(float) * (NL * 2 * W * K + NL * K + fwd_rows) + NL * 2 * npad4;
+  // the forward's service wave and its input-drive ring (three steps of 512
+  // QN floats) where that fits beside an eligibility workgroup, and the binary
+  // presynaptic bytes written 16 steps at a time (one 16-byte record per row)
+  // when that keeps the forward's shared memory small enough, else 8 or 4
   // (16 bytes of alignment before them)
+  const size_t ring = (size_t)3 * qn * eprop::kFwdThreads * sizeof(float);
+  auto fwd_smem = [&](int zg, int svc) {
+    return smem_base + (svc ? ring : 0) + 16 + (size_t)zg * fwd_rows;
+  };
+  constexpr size_t kShareSmem = 96 * 1024;   // leaves an eligibility workgroup room on the CU
+  plan->svc = qn <= 2 || (qn == 4 && fwd_smem(4, 1) <= kShareSmem);
   plan->zgroup = 4;
   for (int zg : {16, 8}) {
-    const size_t sm = smem_base + 16 + (size_t)zg * npre_total;
-    if (sm <= 96 * 1024) { plan->zgroup = zg; break; }
+    if (fwd_smem(zg, plan->svc) <= kShareSmem) { plan->zgroup = zg; break; }
   }
-  plan->smem = smem_base + 16 + (size_t)plan->zgroup * npre_total;
+  plan->smem = fwd_smem(plan->zgroup, plan->svc);
   plan->bytes = round_up(off, 256);
 }
 
@@ -372,6 +391,16 @@ struct eprop_ctx {
   int online_every = 0;
   long long online_applied = -1;   // step count of the last update
   hipEvent_t ev_update = nullptr;
+  // the first layer's input drive of the next block of a sequence, computed
+  // on in_stream while the forward of the current block runs: ev_pre is
+  // recorded on the forward stream before that forward (the weights, the
+  // inputs and the other buffer are then ready), ev_in[k] when buffer k is
+  // filled; in_buf is the buffer the next block reads, in_ready whether it
+  // has been filled for it
+  hipStream_t in_stream = nullptr;
+  hipEvent_t ev_pre = nullptr, ev_in[2] = {};
+  int in_buf = 0;
+  bool in_ready = false;
   bool alive = false;
   std::string err;
   // profiling of the eligibility kernel
@@ -482,9 +511,17 @@ int apply_online(eprop_ctx* ctx) {
   return rc;
 }
 
+// An online weight update falls before the step t steps after the reset.
+bool online_due(const eprop_ctx* ctx, long long t) {
+  return ctx->online_every > 0 && t > 0 && t % ctx->online_every == 0 && ctx->online_applied != t;
+}
+
 // `steps` (1..Kmax) consecutive timesteps: forward of every layer, readout
-// gradient, eligibility traces and gradient accumulation.
-int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels, uint32_t* spikes) {
+// gradient, eligibility traces and gradient accumulation.  x_next (NULL:
+// none) and steps_next: the block that follows in the same call, whose
+// input drive may be computed meanwhile.
+int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels, uint32_t* spikes,
+             const uint8_t* x_next, int steps_next) {
   const Plan& P = ctx->plan;
   const eprop_config& c = P.cfg;
   hipStream_t s = ctx->stream;
@@ -493,8 +530,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   const int first = ctx->t == 0;
   const int sl = ctx->slot;
   int rc;
-  if (ctx->online_every > 0 && ctx->t > 0 && ctx->t % ctx->online_every == 0 &&
-      ctx->online_applied != ctx->t) {
+  if (online_due(ctx, ctx->t)) {
     if ((rc = apply_online(ctx))) return rc;
     ctx->online_applied = ctx->t;
   }
@@ -513,15 +549,33 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     f.v = L.v; f.a = L.a; f.ztil = L.ztil; f.z = L.z; f.zbar = L.zbar; f.y = L.y;
     f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.p8 = L.p8[sl]; f.zstart = L.zstart[sl];
     f.deltaK = L.deltaK[sl]; f.ztK = L.ztK[sl];
-    f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.rows_per_wave = L.rows_per_wave; f.ldi = L.n_pre_pad;
+    f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.ldi = L.n_pre_pad;
   }
-  fa.n_layers = c.n_layers; fa.x = x; fa.n_in = c.n_in; fa.labels = labels;
+  // the first layer's input rows: their drive before the forward (already
+  // computed on the input stream, or now on the forward stream); their
+  // filter and p bytes on the coefficient stream (below)
+  const Layer& L0 = P.layers[0];
+  const int ib = ctx->in_buf;
+  eprop::InputArgs ia;
+  ia.x = x; ia.n_in = c.n_in; ia.B = c.batch; ia.steps = steps;
+  ia.Wt = L0.Wt; ia.ldw = L0.ldw; ia.W16 = L0.W16; ia.qn = eprop::forward_qn(c.n_rec); ia.w16ok = P.w16ok;
+  ia.Iin = P.Iin[ib]; ia.nin = P.nin[ib];
+  ia.zbar = L0.zbar; ia.n_pre = L0.n_pre; ia.zstart = L0.zstart[sl]; ia.p8 = L0.p8[sl];
+  ia.ldi = L0.n_pre_pad; ia.alpha = c.alpha;
+  if (ctx->in_ready) {
+    ctx->in_ready = false;
+    if ((rc = check(ctx, hipStreamWaitEvent(sf, ctx->ev_in[ib], 0), "stream wait"))) return rc;
+  } else if ((rc = check(ctx, eprop::launch_input_drive(ia, sf), "input drive kernel"))) {
+    return rc;
+  }
+  fa.Iin = P.Iin[ib]; fa.nin = P.nin[ib];
+  fa.n_layers = c.n_layers; fa.labels = labels;
   fa.err_flag = P.err_flag; fa.w16ok = P.w16ok; fa.spikes = spikes; fa.W32 = (c.n_rec + 31) / 32;
   fa.B = c.batch; fa.Bp = P.Bp; fa.n_rec = c.n_rec; fa.K_out = c.n_out;
   fa.n_adaptive = c.n_adaptive; fa.Kmax = P.Kmax; fa.steps = steps;
   fa.ldj = P.layers[0].ldv; fa.ldk = P.ldk; fa.ldn = P.ldn; fa.jlist = P.jlist;
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
-  fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.zgroup = P.zgroup;
+  fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.zgroup = P.zgroup; fa.svc = P.svc;
   fa.model = c.neuron_model;
   for (int m = 0; m < 2; ++m) {
     fa.mA[m][0] = (float)P.gen.A[m][0]; fa.mA[m][1] = (float)P.gen.A[m][1];
@@ -537,13 +591,30 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     }
     fa.mr[0] = (float)full.r[0]; fa.mr[1] = (float)full.r[1];
   }
+  // the next block's input drive into the other buffer, while this forward
+  // runs (not when the weights change before the next block)
+  const bool pre = ev && x_next && steps_next > 0 && !online_due(ctx, ctx->t + steps);
+  if (pre) {
+    eprop::InputArgs nx = ia;
+    nx.x = x_next; nx.steps = steps_next; nx.Iin = P.Iin[ib ^ 1]; nx.nin = P.nin[ib ^ 1];
+    if ((rc = check(ctx, hipEventRecord(ctx->ev_pre, sf), "event record")) ||
+        (rc = check(ctx, hipStreamWaitEvent(ctx->in_stream, ctx->ev_pre, 0), "stream wait")) ||
+        (rc = check(ctx, eprop::launch_input_drive(nx, ctx->in_stream), "input drive kernel")) ||
+        (rc = check(ctx, hipEventRecord(ctx->ev_in[ib ^ 1], ctx->in_stream), "event record")))
+      return rc;
+  }
   if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
   if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
+  if (pre) {
+    ctx->in_buf = ib ^ 1;
+    ctx->in_ready = true;
+  }
 
   // On the coefficient stream, per layer: learning signal, readout gradient
   // and the block coefficients of the eligibility recursion.  The forward of
   // the next block (other slot) runs meanwhile.
   if (ev && (rc = check(ctx, hipStreamWaitEvent(sc, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
+  if ((rc = check(ctx, eprop::launch_input_filter(ia, sc), "input filter kernel"))) return rc;
   const int rows = steps * P.Bp;
   const int kpad = (int)round_up(steps, 16);
   for (int l = 0; l < c.n_layers; ++l) {
@@ -617,7 +688,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_done[sl], s), "event record"))) return rc;
   ctx->slot_used[sl] = true;
   ctx->last_slot = sl;
-  ctx->slot = (ctx->slot + 1) % kSlots;
+  ctx->slot = (ctx->slot + 1) % P.slots;
   ctx->t += steps;
   ctx->last_steps = steps;
   return EPROP_OK;
@@ -628,6 +699,7 @@ bool usable(const eprop_ctx* ctx) { return ctx && ctx->alive; }
 // Work queued on the caller's stream before this call (inputs, a reset, new
 // weights) happens before the forward kernels of this call.
 int join_forward_stream(eprop_ctx* ctx) {
+  ctx->in_ready = false;   // an input drive is only computed ahead within a call
   if (ctx->single_stream) return EPROP_OK;
   int rc = check(ctx, hipEventRecord(ctx->ev_entry, ctx->stream), "event record");
   if (!rc) rc = check(ctx, hipStreamWaitEvent(ctx->fwd_stream, ctx->ev_entry, 0), "stream wait");
@@ -663,7 +735,7 @@ int setup_ctx(eprop_ctx* ctx, const eprop_config* cfg, char* ws, size_t ws_bytes
   ctx->ws_bytes = ws_bytes;
   ctx->stream = stream;
   ctx->single_stream = single_stream;
-  make_plan(*cfg, ctx->ws, &ctx->plan);
+  make_plan(*cfg, ctx->ws, &ctx->plan, single_stream ? 1 : kSlots);
   for (int l = 0; l < cfg->n_layers; ++l) {
     ctx->plan.layers[l].W_src = d_weights[2 * l];
     ctx->plan.layers[l].Wout_src = d_weights[2 * l + 1];
@@ -677,6 +749,10 @@ int setup_ctx(eprop_ctx* ctx, const eprop_config* cfg, char* ws, size_t ws_bytes
                         "stream create");
     if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_entry, hipEventDisableTiming), "event create");
     if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_update, hipEventDisableTiming), "event create");
+    if (!rc) rc = check(ctx, hipStreamCreateWithFlags(&ctx->in_stream, hipStreamNonBlocking), "stream create");
+    if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_pre, hipEventDisableTiming), "event create");
+    for (int k = 0; k < 2 && !rc; ++k)
+      rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_in[k], hipEventDisableTiming), "event create");
     for (int k = 0; k < kSlots && !rc; ++k) {
       rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_fwd[k], hipEventDisableTiming), "event create");
       if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_coef[k], hipEventDisableTiming),
@@ -807,7 +883,7 @@ int eprop_step(eprop_ctx* ctx, const uint8_t* d_x_t, const int32_t* d_labels, ui
   if (!d_x_t || !d_labels) return fail(ctx, EPROP_EINVAL, "x or labels is NULL");
   int rc = join_forward_stream(ctx);
   if (rc) return rc;
-  return do_block(ctx, d_x_t, 1, d_labels, d_spikes_t);
+  return do_block(ctx, d_x_t, 1, d_labels, d_spikes_t, nullptr, 0);
 }
 
 int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int32_t* d_labels,
@@ -820,14 +896,22 @@ int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int3
   const size_t s_step = (size_t)c.n_layers * c.batch * ((c.n_rec + 31) / 32);
   int rc0 = join_forward_stream(ctx);
   if (rc0) return rc0;
-  for (int32_t t = 0; t < T;) {
+  // blocks of up to Kmax steps that end where the weights change
+  auto block_steps = [&](int32_t t, long long t_ctx) {
     int steps = std::min<int32_t>(ctx->plan.Kmax, T - t);
-    if (ctx->online_every > 0)   // blocks end where the weights change
-      steps = (int)std::min<long long>(steps, ctx->online_every - ctx->t % ctx->online_every);
+    if (ctx->online_every > 0)
+      steps = (int)std::min<long long>(steps, ctx->online_every - t_ctx % ctx->online_every);
+    return steps;
+  };
+  for (int32_t t = 0; t < T;) {
+    const int steps = block_steps(t, ctx->t);
+    const int32_t tn = t + steps;
+    const int steps_next = tn < T ? block_steps(tn, ctx->t + steps) : 0;
     int rc = do_block(ctx, d_x + t * x_step, steps, d_labels,
-                      d_spikes ? d_spikes + t * s_step : nullptr);
+                      d_spikes ? d_spikes + t * s_step : nullptr,
+                      steps_next > 0 ? d_x + tn * x_step : nullptr, steps_next);
     if (rc) return rc;
-    t += steps;
+    t = tn;
   }
   return EPROP_OK;
 }
@@ -916,13 +1000,15 @@ int eprop_status(eprop_ctx* ctx) {
 
 void eprop_destroy(eprop_ctx* ctx) {
   if (!ctx) return;
-  for (hipStream_t st : {ctx->fwd_stream, ctx->coef_stream}) {
+  for (hipStream_t st : {ctx->fwd_stream, ctx->coef_stream, ctx->in_stream}) {
     if (!st || ctx->single_stream) continue;   // the caller's stream is not ours
     (void)hipStreamSynchronize(st);
     (void)hipStreamDestroy(st);
   }
   if (ctx->ev_entry) (void)hipEventDestroy(ctx->ev_entry);
   if (ctx->ev_update) (void)hipEventDestroy(ctx->ev_update);
+  for (hipEvent_t e : {ctx->ev_pre, ctx->ev_in[0], ctx->ev_in[1]})
+    if (e) (void)hipEventDestroy(e);
   for (int k = 0; k < kSlots; ++k)
     for (hipEvent_t e : {ctx->ev_fwd[k], ctx->ev_coef[k], ctx->ev_done[k]})
       if (e) (void)hipEventDestroy(e);

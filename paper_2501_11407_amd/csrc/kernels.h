@@ -27,18 +27,24 @@ namespace eprop {
 
 constexpr int kFwdThreads = 512;               // forward workgroup: one batch element
 constexpr int kFwdWaves = kFwdThreads / 64;
-constexpr int kFwdXSteps = 8;                  // steps of input spikes staged in shared memory
-constexpr int kXRegs = 2;                      // input words (or bytes) per thread prefetched per step
 constexpr int kBlockSteps = 256;       // timesteps per block (Kmax)
 constexpr int kTileI = 256;            // eligibility workgroup tile: 256 (i) x 16 (j)
 constexpr int kTileJ = 16;
 constexpr int kRowPad = kTileI;        // n_pre padded to the tile height (ldi)
 constexpr int kColPad = kTileJ;        // n_rec padded to the tile width (ldc)
 
+// Forward thread 64 w + l (wave w, lane l) holds the QN neurons
+// 64 QN w + 64 q + l, q < QN (QN: neurons per thread, a power of two); the
+// int16 drive weights and the input drive store neuron j at position
+// tid QN + q of a row of 512 QN, so that a thread reads its QN in one load.
+__host__ __device__ inline int fwd_position(int j, int qn) {
+  const int w = j / (64 * qn), q = (j / 64) % qn, l = j % 64;
+  return (64 * w + l) * qn + q;
+}
+
 struct FwdLayer {
-  const float* Wt; int ldw;      // transposed drive weights [n_pre][ldw]
-  // the same times 2^14 as int16, row stride 512 * QN, neuron q * 512 + t
-  // at t * QN + q (QN: neurons per forward thread, a power of two); used
+  const float* Wt; int ldw;      // transposed drive weights [n_pre][ldw], ldw = 512 QN
+  // the same times 2^14 as int16 [n_pre][512 QN] at forward positions; used
   // when *FwdArgs::w16ok (see launch_pack16)
   const int16_t* W16;
   const float* WoutT;            // transposed readout weights [n_rec_pad][ldk]
@@ -51,14 +57,17 @@ struct FwdLayer {
   uint8_t* p8;                   // [B][Kmax/16][ldi/16][4][16][4]
   float* zstart;                 // [B][ldi]
   float* deltaK; float* ztK;     // [rows][ldk], [rows][ldn]
-  int n_inl, n_pre, rows_per_wave, ldi;
+  int n_inl, n_pre, ldi;
 };
 
+// The forward handles the p bytes, filter and zstart of the recurrent rows
+// (and of every row of a second layer); the first layer's input rows, and
+// the input part of its drive, come from the input kernels below.
 struct FwdArgs {
   FwdLayer L[2];
   int n_layers;
-  const uint8_t* x;              // [steps][B][n_in]
-  int n_in;
+  const float* Iin;              // first layer's input drive [steps][B][512 QN] (launch_input_drive)
+  const int* nin;                // [steps][B]: its number of active inputs
   const int32_t* labels;
   int* err_flag;
   uint32_t* spikes;              // NULL or [steps][n_layers][B][W32]
@@ -72,9 +81,29 @@ struct FwdArgs {
   int model;
   float mA[2][2], mb[2], mr[2], mc[2];
   const int* w16ok;              // [0]: every layer's W16 is exact, [1]: their largest |k|
+  // 1: a ninth (service) wave stages the input drive in shared memory (a
+  // ring of three steps, 6 KiB per neuron per thread, at the start of smem);
+  // required for QN <= 2, allowed for QN == 4, not for more
+  int svc;
   size_t smem;
 };
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
+
+// The first layer's input rows over a block of `steps` steps, x [steps][B][n_in]:
+// launch_input_drive writes Iin[t][b][512 qn] (forward positions), the sum of
+// the drive weights over the step's active inputs in ascending order in fp32
+// from 0 (rows from W16 when *w16ok, else Wt), and nin[t][b], their number;
+// launch_input_filter advances zbar [B][n_pre] of the input rows over the
+// steps (their value at the start into zstart [B][ldi]) and writes their p
+// bytes into p8 as the forward does for its rows.
+struct InputArgs {
+  const uint8_t* x; int n_in, B, steps;
+  const float* Wt; int ldw; const int16_t* W16; int qn; const int* w16ok;
+  float* Iin; int* nin;
+  float* zbar; int n_pre; float* zstart; uint8_t* p8; int ldi; float alpha;
+};
+hipError_t launch_input_drive(const InputArgs& a, hipStream_t s);
+hipError_t launch_input_filter(const InputArgs& a, hipStream_t s);
 
 // NT: C_part[s][m][n] = sum_{k in split s} A[m][k] * Bm[n][k]
 // TN: C_part[s][m][n] = sum_{k in split s} A[k][m] * Bm[k][n]

@@ -105,34 +105,53 @@ __device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChu
 
 // ---------------------------------------------------------------- forward
 // One workgroup per batch element runs `steps` timesteps of every layer; the
-// neuron state of the threads' neurons stays in registers, the filtered
-// presynaptic vector and the readout in shared memory.  Per step and layer:
-//   1. p = [in ; z_prev]; zbar = alpha*zbar + p; each wave lists the indices
-//      of its contiguous slice of p that are 1, in ascending order, and the
-//      lists are merged into one ascending list.
-//   2. drive I_j = sum of W_ji over the listed i, added in ascending i (the
-//      order of a plain sequential sum; the rows are loaded a batch at a
-//      time), then the neuron step with one rounding per operation:
+// neuron state stays in registers, the presynaptic filter of the rows the
+// workgroup handles and the readout in shared memory.  Thread 64 w + l (wave
+// w, lane l) holds the QN neurons 64 QN w + 64 q + l, q < QN (fwd_neuron): a
+// wave owns a contiguous range of neurons, its spike list, built by ballots
+// in ascending q, is ascending, and the waves' lists in wave order are the
+// ascending list of the layer's spikes.  Per step and layer:
+//   1. the active rows of p = [in ; z_prev] in ascending order: for the
+//      first layer, the previous step's spike lists (its input rows enter
+//      through the input drive, below); for a second layer, the first
+//      layer's lists of this step and then its own of the previous step.
+//   2. drive I_j: the first layer starts from its input drive, the sum of
+//      W_ji over the step's active inputs in ascending i (input_drive_kernel;
+//      it does not depend on the network state), a second layer from 0; the
+//      listed rows are added in ascending i, so that I is the plain
+//      sequential sum over the active rows.  While the rows' loads are in
+//      flight: the filter zbar = alpha*zbar + p of the rows the workgroup
+//      handles (recurrent rows, and every row of a second layer; the first
+//      layer's input rows are input_filter_kernel's) and their p bytes.  Then
+//      the neuron step with one rounding per operation:
 //        v = alpha*v; v = v + I; v = v - thr*z_prev
 //        a = rho*a;   a = a + z_prev
 //        A = beta_j*a; A = thr + A;  x = v - A;  z = x > 0
 //        psi = (gamma/thr) * max(0, 1 - |x|/thr)
 //   3. each wave sums the readout weights of its spiking neurons for every
 //      class; ztilde = kappa*ztilde + z.
-//   4. the last wave: y = kappa*y + (sum of the waves' partial sums, in wave order),
-//      softmax, delta = softmax - onehot(label), cross-entropy into the loss.
+//   4. one wave: y = kappa*y + (sum of the waves' partial sums, in wave
+//      order), softmax, delta = softmax - onehot(label), cross-entropy.
 // The learning signal L = W_out^T delta is one GEMM over the whole block.
 struct FwdLds {
-  int* act; int* spk; int* cnt; float* part; float* sy; float* szb;
-  uint8_t* zb;                   // [npre_total][zgroup]: p of the last zgroup steps
-  int npre_total;
-  uint8_t* zc;
-  uint8_t* xs;                   // [kFwdXSteps][n_in]: input spikes of steps t .. t+7, row t % 8
-  bool xwords;                   // rows 4-byte aligned: input rows copied as 32-bit words
+  float* iring;                  // SVC: [3][512 QN] input drive of steps t, t+1, t+2 (slot t % 3)
+  int* spk;                      // [n_layers][2][waves][jlist]: spike lists by step parity
+  int* cnt;                      // [n_layers][2][waves]: their lengths
+  int* nin;                      // [steps]: active inputs of the first layer per step
+  float* part; float* sy;
+  float* szb;                    // filter of the rows the workgroup handles
+  uint8_t* zb;                   // [rows][zgroup]: their p bytes of the last zgroup steps
+  uint8_t* zc;                   // [n_layers][2][npad]: spikes of this and the previous step
   bool w16;                      // the int16 weights are exact (FwdLayer::W16)
   int w16max;                    // their largest |k|
-  int rwmax, npad;
+  int npad;
+  int rows0;                     // rows handled in the first layer: its recurrent rows
 };
+
+template <int QN>
+__device__ __forceinline__ int fwd_neuron(int tid, int q) {
+  return (tid >> 6) * (kWave * QN) + q * kWave + (tid & (kWave - 1));
+}
 
 // Softmax cross-entropy of one step for K_out <= 64, in one wave: lane k holds
 // class k's output y (updated here) and gets delta_k = softmax_k - onehot_k.
@@ -211,145 +230,173 @@ __device__ __forceinline__ float readout_sum(const FwdArgs& A, const float* Wout
   return Y;
 }
 
+// The spike list of a wave (parity par) from the spike bytes of its
+// neurons, for the block's first step; returns its length.
 template <int QN, int LI>
+__device__ __forceinline__ int wave_list_from_bytes(const FwdArgs& A, const FwdLds& S, int par,
+                                                    const uint8_t* zc) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int* spk = S.spk + ((LI * 2 + par) * kFwdWaves + w) * A.jlist;
+  int n = 0;
+#pragma unroll
+  for (int q = 0; q < QN; ++q) {
+    const int j = fwd_neuron<QN>(tid, q);
+    const bool z = j < A.n_rec && zc[j] != 0;
+    const unsigned long long m = __ballot(z);
+    if (z) spk[n + lanes_below(m, lane)] = j;
+    n += __popcll(m);
+  }
+  if (lane == 0) S.cnt[(LI * 2 + par) * kFwdWaves + w] = n;
+  return n;
+}
+
+// SOFTWIN: the softmax runs while the drive's loads are in flight (else at
+// the step's start, which needs fewer registers at the loads).  SVC: the
+// input drive comes from the shared-memory ring the service wave fills
+// (else each thread loads the next step's itself).
+template <int QN, int LI, bool SOFTWIN, bool SVC>
 __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLds& S, int t, int b,
                                                    int cur, float (&v)[QN], float (&ad)[QN],
                                                    float (&zt)[QN], double& loss, int label,
-                                                   float& yk, float& dk, int& nspk_prev) {
+                                                   float& yk, float& dk, int& nspk_prev,
+                                                   float (&iin)[QN]) {
   const FwdLayer& Ly = A.L[LI];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const uint8_t* zprev = S.zc + (LI * 2 + cur) * S.npad;
   uint8_t* znow = S.zc + (LI * 2 + (cur ^ 1)) * S.npad;
-  const uint8_t* inp;
-  if constexpr (LI == 0)
-    inp = S.xs + (t % kFwdXSteps) * A.n_in;      // staged input spikes of this step
-  else
-    inp = S.zc + ((LI - 1) * 2 + (cur ^ 1)) * S.npad;
-  float* szb = S.szb + (LI == 0 ? 0 : A.L[0].n_pre);
-  uint8_t* zring = S.zb + (LI == 0 ? 0 : A.L[0].n_pre) * A.zgroup;
+  // a second layer's input: the first layer's spikes of this step
+  const uint8_t* inp = S.zc + (cur ^ 1) * S.npad;
+  const bool recurrent = Ly.n_pre > Ly.n_inl;
+  const int ridx = LI == 0 ? 0 : S.rows0;      // first filter row of this layer
+  float* szb = S.szb + ridx;
+  uint8_t* zring = S.zb + ridx * A.zgroup;
   float* sy = S.sy + LI * A.K_out;
-  int* spk = S.spk + LI * kFwdWaves * A.jlist + w * A.jlist;   // this wave's spike list
+  const int pc = t & 1, pp = pc ^ 1;           // parity of this and the previous step
+  int* spk_now = S.spk + ((LI * 2 + pc) * kFwdWaves + w) * A.jlist;
+  const int* spk_prev = S.spk + ((LI * 2 + pp) * kFwdWaves + w) * A.jlist;
   const size_t row = (size_t)t * A.Bp + b;
   // readout partial sums by step parity
-  float* part = S.part + (LI * 2 + (t & 1)) * kFwdWaves * A.K_out;
+  float* part = S.part + (LI * 2 + pc) * kFwdWaves * A.K_out;
   // K_out <= 64: the readout of a step's spikes is loaded together with the
   // next step's drive (its partial sums go to part of that step's parity),
-  // and the last wave, which holds the fewest presynaptic rows, takes the
-  // softmax of the step two back while the others build their lists, and
-  // stores delta with this step's stores; the block's last two steps are
-  // finished after the step loop
+  // and the last wave takes the softmax of the step two back and stores
+  // delta with this step's stores; the block's last two steps are finished
+  // after the step loop
   const bool defer = A.K_out <= kWave;
-  if (defer && w == kSoftWave && t > 1) dk = softmax_lanes(A, part, yk, label, loss);
+  if (!SOFTWIN && defer && w == kSoftWave && t > 1) dk = softmax_lanes(A, part, yk, label, loss);
 
-  // 1. presynaptic vector: each wave lists the indices of its contiguous
-  // slice of p that are 1, in ascending order, and keeps the step's p bytes
-  const int rw = Ly.rows_per_wave;
-  const int i_beg = w * rw, i_end = min(Ly.n_pre, i_beg + rw);
-  const int zslot = t & (A.zgroup - 1);
-  int n_act = 0;
-  for (int base = i_beg; base < i_end; base += kWave) {
-    const int i = base + lane;
-    bool on = false;
-    if (i < i_end) {
-      const uint8_t sv = (i < Ly.n_inl) ? inp[i] : zprev[i - Ly.n_inl];
-      on = sv != 0;
-      zring[i * A.zgroup + zslot] = on ? kPByte : 0;
-    }
-    const unsigned long long m = __ballot(on);
-    if (on) S.act[w * S.rwmax + n_act + lanes_below(m, lane)] = i;
-    n_act += __popcll(m);
-  }
-  if (lane == 0) S.cnt[w] = n_act;
-  lds_barrier();
-  // The waves' lists in wave order are the ascending list of active rows:
-  // every lane holds the counts, and entry e lies in the last wave whose
-  // list starts at or before e (such a wave is never empty).
-  int offs[kFwdWaves];
+  // 1. the active rows: segments of spike lists (LDS int offsets), each with
+  // the row index of its neuron 0
+  constexpr int NSEG = LI == 0 ? kFwdWaves : 2 * kFwdWaves;
+  int offs[NSEG];
   int total = 0;
   {
-    const int cl = (lane < kFwdWaves) ? S.cnt[lane] : 0;
+    const int* c0 = S.cnt + (LI == 0 ? (0 * 2 + pp) : (0 * 2 + pc)) * kFwdWaves;
+    const int* c1 = S.cnt + (1 * 2 + pp) * kFwdWaves;
+    // the first segments: a second layer's inputs, or the first layer's
+    // recurrent rows (none in a feed-forward layer)
+    int cl = 0;
+    if (lane < kFwdWaves && (LI == 1 || recurrent)) cl = c0[lane];
+    else if (LI == 1 && recurrent && lane >= kFwdWaves && lane < 2 * kFwdWaves) cl = c1[lane - kFwdWaves];
 #pragma unroll
-    for (int ww = 0; ww < kFwdWaves; ++ww) {
-      offs[ww] = total;
-      total += __builtin_amdgcn_readlane(cl, ww);
+    for (int s = 0; s < NSEG; ++s) {
+      offs[s] = total;
+      total += __builtin_amdgcn_readlane(cl, s);
     }
   }
+  const int seg0 = (LI == 0 ? (0 * 2 + pp) : (0 * 2 + pc)) * kFwdWaves * A.jlist;
+  const int seg1 = (1 * 2 + pp) * kFwdWaves * A.jlist;
+  const int roff0 = LI == 0 ? Ly.n_inl : 0;    // row of neuron 0 in the first segments
   auto list_entry = [&](int e) {
-    int ww = 0, o = 0;
+    int s = 0, o = 0;
 #pragma unroll
-    for (int v = 1; v < kFwdWaves; ++v)
-      if (e >= offs[v]) {
-        ww = v;
-        o = offs[v];
+    for (int u = 1; u < NSEG; ++u)
+      if (e >= offs[u]) {
+        s = u;
+        o = offs[u];
       }
-    return S.act[ww * S.rwmax + (e - o)];
+    const bool hi = LI == 1 && s >= kFwdWaves;
+    const int base = hi ? seg1 + (s - kFwdWaves) * A.jlist : seg0 + s * A.jlist;
+    return S.spk[base + (e - o)] + (hi ? A.n_rec : roff0);
   };
-  // The presynaptic filter of the wave's rows, off the critical path: done
-  // while the drive's loads are in flight (from the p bytes kept above).
+  // the rows this wave filters: those of its neurons
+  const int jlo = w * (kWave * QN), jhi = min(A.n_rec, jlo + kWave * QN);
+  const int zslot = t & (A.zgroup - 1);
+  auto filter_one = [&](int idx, uint8_t pv) {
+    const bool on = pv != 0;
+    zring[idx * A.zgroup + zslot] = on ? kPByte : 0;
+    szb[idx] = A.alpha * szb[idx] + (on ? 1.0f : 0.0f);
+  };
+  // The presynaptic filter and the next step's input drive, off the
+  // critical path: issued while the drive's loads are in flight.
+  float inext[QN];
+#pragma unroll
+  for (int q = 0; q < QN; ++q) inext[q] = 0.0f;
   bool filtered = false;
   auto filter_rows = [&]() {
     if (filtered) return;
     filtered = true;
-    for (int i = i_beg + lane; i < i_end; i += kWave) {
-      const bool on = zring[i * A.zgroup + zslot] != 0;
-      const float zv = A.alpha * szb[i] + (on ? 1.0f : 0.0f);
-      szb[i] = zv;
+    if (SOFTWIN && defer && w == kSoftWave && t > 1) dk = softmax_lanes(A, part, yk, label, loss);
+    if constexpr (LI == 0 && !SVC) {
+      if (t + 1 < A.steps) {
+        typedef float fqv __attribute__((ext_vector_type(QN)));
+        const fqv nv = *(const fqv*)(A.Iin + ((size_t)(t + 1) * A.B + b) * (QN * kFwdThreads) +
+                                     (size_t)tid * QN);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) inext[q] = nv[q];
+      }
+    }
+    for (int j = jlo + lane; j < jhi; j += kWave) {
+      if (LI == 0) {
+        if (recurrent) filter_one(j, zprev[j]);
+      } else {
+        filter_one(j, inp[j]);
+        if (recurrent) filter_one(A.n_rec + j, zprev[j]);
+      }
     }
   };
 
-  // 2. drive and neuron step.  Rows of Wt are padded to a multiple of the
-  // workgroup size; chunks q with q*kFwdThreads >= n_rec are skipped (QN is
-  // rounded up to a power of two).  UB rows are loaded before any is added:
-  // lane u reads list entry k0 + u, every wave takes the entries from its
-  // lanes, and each row's load is a scalar row base plus the lane offset.
-  constexpr int UB = QN >= 32 ? 1 : 32 / QN;
-  // Input spikes of step t+kFwdXSteps: loaded here, under the drive loads,
-  // and written after them into the staging row of step t, which this step's
-  // list has already read.
-  uint32_t xr[kXRegs];
-  const bool xpre = LI == 0 && t + kFwdXSteps < A.steps;
-  const uint8_t* xrow = A.x + ((size_t)(t + kFwdXSteps) * A.B + b) * A.n_in;
-  if constexpr (LI == 0) {
-    if (xpre) {
-#pragma unroll
-      for (int m = 0; m < kXRegs; ++m) {
-        const int k = tid + m * kFwdThreads;
-        xr[m] = 0;
-        if (S.xwords) {
-          if (k < (A.n_in >> 2)) xr[m] = ((const uint32_t*)xrow)[k];
-        } else if (k < A.n_in) {
-          xr[m] = xrow[k];
-        }
-      }
-    }
-  }
+  // 2. drive and neuron step.  UB rows are loaded before any is added: lane
+  // u reads list entry k0 + u, every wave takes the entries from its lanes,
+  // and each row's load is a scalar row base plus the lane offset.
+  constexpr int UB = QN >= 16 ? 1 : 16 / QN;
   // the readout rows of the previous step's spikes, loaded with the drive rows
   ReadoutRows rr;
-  if (defer) readout_issue(A, Ly.WoutT, spk, nspk_prev, rr);
-  const uint32_t tidoff = (uint32_t)tid * 4u;
+  if (defer && t > 0) readout_issue(A, Ly.WoutT, spk_prev, nspk_prev, rr);
   float I[QN];
+  if constexpr (LI == 0 && SVC) {
+    typedef float fqv __attribute__((ext_vector_type(QN)));
+    const fqv rv = *(const fqv*)(S.iring + (t % 3) * (QN * kFwdThreads) + tid * QN);
 #pragma unroll
-  for (int q = 0; q < QN; ++q) I[q] = 0.0f;
+    for (int q = 0; q < QN; ++q) I[q] = rv[q];
+  } else {
+#pragma unroll
+    for (int q = 0; q < QN; ++q) I[q] = LI == 0 ? iin[q] : 0.0f;
+  }
   // integer weights k (w = k 2^-14, |k| <= 32767): with at most 2^24 / max|k|
   // active rows every partial sum in any order is an integer of at most
-  // 2^24 units, exact in fp32, so the integer sum equals the fp32
-  // sequential sum; decided per step from the step's active rows
-  const bool w16 = S.w16 && (long long)total * S.w16max <= (1ll << 24);
+  // 2^24 units, exact in fp32, so the integer sum plus the (then exact)
+  // input drive equals the fp32 sequential sum; decided per step from the
+  // step's active rows, inputs included
+  const int all_rows = total + (LI == 0 ? S.nin[t] : 0);
+  const bool w16 = S.w16 && (long long)all_rows * S.w16max <= (1ll << 24);
   if (w16) {
     // the thread's QN of a row in one load of 2 QN bytes
-    constexpr int UB16 = QN == 1 ? 32 : 64 / QN;
+    constexpr int UB16 = QN <= 2 ? 16 : 32 / QN;
     typedef int16_t i16v __attribute__((ext_vector_type(QN)));
     int isum[QN];
 #pragma unroll
     for (int q = 0; q < QN; ++q) isum[q] = 0;
     for (int k0 = 0; k0 < total; k0 += UB16) {
       const int ent = list_entry(min(k0 + (lane & (UB16 - 1)), total - 1));
+      const int nb = min(UB16, total - k0);   // rows of this batch (wave-uniform)
       i16v wk[UB16];
 #pragma unroll
       for (int u = 0; u < UB16; ++u) {
         const int i = __builtin_amdgcn_readlane(ent, u);
-        wk[u] = *(const i16v*)(Ly.W16 + (size_t)i * (QN * kFwdThreads) + (size_t)tid * QN);
+        if (u < nb) wk[u] = *(const i16v*)(Ly.W16 + (size_t)i * (QN * kFwdThreads) + (size_t)tid * QN);
       }
       __builtin_amdgcn_sched_barrier(0);
       filter_rows();
@@ -361,20 +408,19 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
           for (int q = 0; q < QN; ++q) isum[q] += (int)wk[u][q];
     }
 #pragma unroll
-    for (int q = 0; q < QN; ++q) I[q] = (float)isum[q] * 0x1p-14f;
+    for (int q = 0; q < QN; ++q) I[q] = I[q] + (float)isum[q] * 0x1p-14f;
   }
   for (int k0 = 0; !w16 && k0 < total; k0 += UB) {
-    const int ent = list_entry(min(k0 + (lane & (UB - 1)), total - 1));   // past the end: the last row
+    const int ent = list_entry(min(k0 + (lane & (UB - 1)), total - 1));
+    const int nb = min(UB, total - k0);   // rows of this batch (wave-uniform)
     float wv[UB][QN];
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int i = __builtin_amdgcn_readlane(ent, u);
-      const char* rowp = (const char*)(Ly.Wt + (size_t)i * Ly.ldw);
+      const float* rowp = Ly.Wt + (size_t)i * Ly.ldw;
+      if (u < nb)
 #pragma unroll
-      for (int q = 0; q < QN; ++q)
-        wv[u][q] = (q == 0 || q * kFwdThreads < A.n_rec)
-                       ? *(const float*)(rowp + tidoff + (uint32_t)q * kFwdThreads * 4u)
-                       : 0.0f;
+        for (int q = 0; q < QN; ++q) wv[u][q] = rowp[fwd_neuron<QN>(tid, q)];
     }
     __builtin_amdgcn_sched_barrier(0);
     filter_rows();
@@ -386,29 +432,9 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
         for (int q = 0; q < QN; ++q) I[q] += wv[u][q];
   }
   filter_rows();   // (no active row this step)
-  if constexpr (LI == 0) {
-    if (xpre) {
-      uint8_t* xs = S.xs + (t % kFwdXSteps) * A.n_in;
-#pragma unroll
-      for (int m = 0; m < kXRegs; ++m) {
-        const int k = tid + m * kFwdThreads;
-        if (S.xwords) {
-          if (k < (A.n_in >> 2)) ((uint32_t*)xs)[k] = xr[m];
-        } else if (k < A.n_in) {
-          xs[k] = (uint8_t)xr[m];
-        }
-      }
-      // inputs wider than the registers cover (rare): the rest directly
-      const int nk = S.xwords ? (A.n_in >> 2) : A.n_in;
-      for (int k = tid + kXRegs * kFwdThreads; k < nk; k += kFwdThreads) {
-        if (S.xwords) ((uint32_t*)xs)[k] = ((const uint32_t*)xrow)[k];
-        else xs[k] = xrow[k];
-      }
-    }
-  }
   if (defer && t > 0) {
-    const float Y = readout_sum(A, Ly.WoutT, spk, nspk_prev, rr);
-    float* part_prev = S.part + (LI * 2 + ((t - 1) & 1)) * kFwdWaves * A.K_out;
+    const float Y = readout_sum(A, Ly.WoutT, spk_prev, nspk_prev, rr);
+    float* part_prev = S.part + (LI * 2 + pp) * kFwdWaves * A.K_out;
     if (lane < A.K_out) part_prev[w * A.K_out + lane] = Y;
   }
   int n_spk = 0;
@@ -416,7 +442,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   unsigned long long smask[QN];
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
-    const int j = q * kFwdThreads + tid;
+    const int j = fwd_neuron<QN>(tid, q);
     bool z = false;
     psv[q] = 0.0f;
     if (j < A.n_rec) {
@@ -440,17 +466,17 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
         v[q] = h0;
         ad[q] = h1;
       } else {
-      float vv = A.alpha * v[q];
-      vv = vv + I[q];
-      vv = vv - A.thr * zp;
-      float aa = A.rho * ad[q];
-      aa = aa + zp;
-      const float bj = (j < A.n_adaptive) ? A.beta : 0.0f;
-      float th = bj * aa;
-      th = A.thr + th;
-      x = vv - th;
-      v[q] = vv;
-      ad[q] = aa;
+        float vv = A.alpha * v[q];
+        vv = vv + I[q];
+        vv = vv - A.thr * zp;
+        float aa = A.rho * ad[q];
+        aa = aa + zp;
+        const float bj = (j < A.n_adaptive) ? A.beta : 0.0f;
+        float th = bj * aa;
+        th = A.thr + th;
+        x = vv - th;
+        v[q] = vv;
+        ad[q] = aa;
       }
       z = x > 0.0f;
       znow[j] = z ? 1 : 0;
@@ -462,10 +488,15 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     }
     const unsigned long long m = __ballot(z);
     smask[q] = m;
-    if (z) spk[n_spk + lanes_below(m, lane)] = j;
+    if (z) spk_now[n_spk + lanes_below(m, lane)] = j;
     n_spk += __popcll(m);
   }
+  if (lane == 0) S.cnt[(LI * 2 + pc) * kFwdWaves + w] = n_spk;
   nspk_prev = n_spk;
+  if constexpr (LI == 0 && !SVC) {
+#pragma unroll
+    for (int q = 0; q < QN; ++q) iin[q] = inext[q];
+  }
 
   // 3. (K_out > 64) this wave's share of the readout: rows of the transposed
   // readout weights of its spiking neurons, read coalesced over the classes
@@ -474,7 +505,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     const uint32_t koff = (uint32_t)min(k, A.K_out - 1) * 4u;
     float Y = 0.0f;
     for (int s0 = 0; s0 < n_spk; s0 += 16) {
-      const int ent = spk[min(s0 + (lane & 15), n_spk - 1)];
+      const int ent = spk_now[min(s0 + (lane & 15), n_spk - 1)];
       float wv[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
@@ -494,13 +525,13 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // zgroup steps) the binary presynaptic bytes ([b][t/16][i][16]).
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
-    const int j = q * kFwdThreads + tid;
+    const int j = fwd_neuron<QN>(tid, q);
     if (j < A.n_rec) {
       __builtin_nontemporal_store(psv[q], Ly.psiK + row * A.ldj + j);
       __builtin_nontemporal_store(zt[q], Ly.ztK + row * A.ldn + j);
     }
     if (A.spikes) {
-      const int w0 = (q * kFwdThreads + w * kWave) >> 5;
+      const int w0 = (w * (kWave * QN) + q * kWave) >> 5;
       uint32_t* srow = A.spikes + (((size_t)t * A.n_layers + LI) * A.B + b) * A.W32;
       if (lane == 0 && w0 < A.W32) __builtin_nontemporal_store((uint32_t)smask[q], srow + w0);
       if (lane == 1 && w0 + 1 < A.W32) __builtin_nontemporal_store((uint32_t)(smask[q] >> 32), srow + w0 + 1);
@@ -514,11 +545,19 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   if ((t & (A.zgroup - 1)) == A.zgroup - 1 || t == A.steps - 1) {
     uint8_t* cb = Ly.p8 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * 16;
     const int q0 = ((t & (kChunk - 1)) & ~(A.zgroup - 1)) >> 2;
-    for (int i = i_beg + lane; i < i_end; i += kWave) {
+    auto flush = [&](int idx, int i) {
       uint8_t* d = cb + (size_t)(i >> 4) * 256 + (i & 15) * 4;
-      const uint32_t* src = (const uint32_t*)(zring + i * A.zgroup);
+      const uint32_t* src = (const uint32_t*)(zring + idx * A.zgroup);
       for (int q = 0; q < (A.zgroup >> 2); ++q)
         __builtin_nontemporal_store(src[q], (uint32_t*)(d + (q0 + q) * 64));
+    };
+    for (int j = jlo + lane; j < jhi; j += kWave) {
+      if (LI == 0) {
+        if (recurrent) flush(j, Ly.n_inl + j);
+      } else {
+        flush(j, j);
+        if (recurrent) flush(A.n_rec + j, A.n_rec + j);
+      }
     }
   }
   lds_barrier();
@@ -552,18 +591,20 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   }
 }
 
+// The state of one layer in (load) or out.  The filter rows are those the
+// workgroup handles (ridx.. in shared memory, presynaptic rows i0.. of the
+// layer); on load the filter also goes to zstart for the eligibility pass.
 template <int QN, int LI>
 __device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S, int b, bool load,
                                               float (&v)[QN], float (&ad)[QN], float (&zt)[QN],
                                               int cur) {
   const FwdLayer& Ly = A.L[LI];
   const int tid = threadIdx.x;
-  float* szb = S.szb + (LI == 0 ? 0 : A.L[0].n_pre);
   float* sy = S.sy + LI * A.K_out;
   uint8_t* zc = S.zc + (LI * 2 + cur) * S.npad;
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
-    const int j = q * kFwdThreads + tid;
+    const int j = fwd_neuron<QN>(tid, q);
     if (j < A.n_rec) {
       const size_t o = (size_t)b * A.n_rec + j;
       if (load) {
@@ -573,14 +614,17 @@ __device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S,
       }
     }
   }
-  for (int i = tid; i < Ly.n_pre; i += kFwdThreads) {
+  const int ridx = LI == 0 ? 0 : S.rows0;
+  const int i0 = LI == 0 ? Ly.n_inl : 0;
+  const int nrows = Ly.n_pre - i0;
+  for (int r = tid; r < nrows; r += kFwdThreads) {
+    const int i = i0 + r;
     if (load) {
-      // the filter at the block's start also goes to the eligibility pass
       const float z = Ly.zbar[(size_t)b * Ly.n_pre + i];
-      szb[i] = z;
+      S.szb[ridx + r] = z;
       Ly.zstart[(size_t)b * Ly.ldi + i] = z;
     } else {
-      Ly.zbar[(size_t)b * Ly.n_pre + i] = szb[i];
+      Ly.zbar[(size_t)b * Ly.n_pre + i] = S.szb[ridx + r];
     }
   }
   for (int k = tid; k < A.K_out; k += kFwdThreads) {
@@ -589,44 +633,103 @@ __device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S,
   }
 }
 
+// The service wave (SVC): a ninth wave that owns no neurons.  During step t
+// it writes the input drive of step t + 2 into ring slot (t + 2) % 3 (read by
+// the other waves at step t + 2; its last reader, step t - 1, is past the
+// barrier) from registers loaded during step t - 1, then loads step t + 3's.
+// Its global loads are its own: the vector-memory counter is per wave, so the
+// other waves' waits for their drive rows never include them.  It takes part
+// in every barrier of the workgroup.
+template <int QN, int NL>
+__device__ __forceinline__ void forward_service_wave(const FwdArgs& A, const FwdLds& S, int b) {
+  constexpr int NV = QN * kFwdThreads / (4 * kWave);   // 16-byte vectors per lane and step
+  const int l = threadIdx.x & (kWave - 1);
+  f32x4 R[NV];
+  auto load = [&](int tt) {
+    const float* src = A.Iin + ((size_t)tt * A.B + b) * (QN * kFwdThreads);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) R[k] = *(const f32x4*)(src + k * 4 * kWave + 4 * l);
+  };
+  auto put = [&](int slot) {
+    float* d = S.iring + slot * (QN * kFwdThreads);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) *(f32x4*)(d + k * 4 * kWave + 4 * l) = R[k];
+  };
+  for (int tt = 0; tt < min(2, A.steps); ++tt) {
+    load(tt);
+    put(tt);
+  }
+  if (A.steps > 2) load(2);
+  lds_barrier();                                   // the others' barrier before the step loop
+  for (int t = 0; t < A.steps; ++t) {
+    if (t + 2 < A.steps) {
+      put((t + 2) % 3);
+      if (t + 3 < A.steps) load(t + 3);
+    }
+    for (int li = 0; li < NL; ++li) lds_barrier();   // one per layer step
+  }
+  if (A.K_out <= kWave && A.steps > 0) lds_barrier();   // the last readout
+  lds_barrier();                                   // before the state goes out
+}
+
 // Four waves per SIMD (128 registers) for one layer of at most two neurons
 // per thread; three (168) for two layers or four neurons per thread and
 // more, so that those do not spill up to four.  Either way an eligibility
 // workgroup fits beside the forward on its compute unit.
-template <int QN, int NL>
-__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu((QN >= 4 || NL > 1) ? 3 : 4))) void forward_kernel(FwdArgs A) {
+template <int QN, int NL, bool SVC>
+__global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__((amdgpu_waves_per_eu((QN >= 4 || NL > 1) ? 3 : 4))) void forward_kernel(FwdArgs A) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   // the forward is the sequential part of the step: its waves win instruction
   // issue over the eligibility waves that share their compute units
   __builtin_amdgcn_s_setprio(3);
   const int b = blockIdx.x;
   FwdLds S;
-  S.rwmax = A.L[0].rows_per_wave;
-  if constexpr (NL > 1) S.rwmax = max(S.rwmax, A.L[1].rows_per_wave);
   S.npad = (A.n_rec + 3) & ~3;
-  S.act = (int*)smem;                          // [waves][rwmax]
-  S.spk = S.act + kFwdWaves * S.rwmax;         // [n_layers][waves][jlist]
-  S.cnt = S.spk + NL * kFwdWaves * A.jlist;    // [2 * waves + 2]
-  S.part = (float*)(S.cnt + 2 * kFwdWaves + 2);   // [n_layers][2][waves][K_out]
-  S.sy = S.part + NL * 2 * kFwdWaves * A.K_out;   // [n_layers][K_out]
-  S.szb = S.sy + NL * A.K_out;                 // [n_pre_0 + n_pre_1]
-  const int npre_total = A.L[0].n_pre + (NL > 1 ? A.L[1].n_pre : 0);
-  S.zb = (uint8_t*)(((uintptr_t)(S.szb + npre_total) + 15) & ~(uintptr_t)15);   // [npre_total][zgroup]
-  S.npre_total = npre_total;
-  S.zc = S.zb + A.zgroup * npre_total;         // [n_layers][2][npad]
-  S.xs = S.zc + NL * 2 * S.npad;               // [kFwdXSteps][n_in]
-  S.xwords = (A.n_in & 3) == 0 && ((uintptr_t)A.x & 3) == 0;
+  S.rows0 = A.L[0].n_pre - A.L[0].n_inl;
+  const int rows = S.rows0 + (NL > 1 ? A.L[1].n_pre : 0);
+  S.iring = (float*)smem;                          // SVC: [3][512 QN]
+  S.spk = (int*)(S.iring + (SVC ? 3 * QN * kFwdThreads : 0));   // [NL][2][waves][jlist]
+  S.cnt = S.spk + NL * 2 * kFwdWaves * A.jlist;    // [NL][2][waves]
+  S.nin = S.cnt + NL * 2 * kFwdWaves;              // [Kmax]
+  S.part = (float*)(S.nin + A.Kmax);               // [NL][2][waves][K_out]
+  S.sy = S.part + NL * 2 * kFwdWaves * A.K_out;    // [NL][K_out]
+  S.szb = S.sy + NL * A.K_out;                     // [rows]
+  // 16-byte aligned by an offset from smem: an integer round trip of the
+  // pointer would lose its address space (generic accesses wait for the
+  // step's global loads as well)
+  const size_t zb_off = (((unsigned char*)(S.szb + rows) - smem) + 15) & ~(size_t)15;
+  S.zb = smem + zb_off;                            // [rows][zgroup]
+  S.zc = S.zb + A.zgroup * rows;                   // [NL][2][npad]
   S.w16 = A.w16ok[0] != 0;
   S.w16max = A.w16ok[1];
+  if constexpr (SVC) {
+    if (threadIdx.x >= kFwdThreads) {
+      forward_service_wave<QN, NL>(A, S, b);
+      return;
+    }
+  }
 
-  for (int e = threadIdx.x; e < A.zgroup * npre_total; e += kFwdThreads) S.zb[e] = 0;
+  for (int e = threadIdx.x; e < A.zgroup * rows; e += kFwdThreads) S.zb[e] = 0;
+  for (int e = threadIdx.x; e < A.steps; e += kFwdThreads) S.nin[e] = A.nin[(size_t)e * A.B + b];
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
   forward_state<QN, 0>(A, S, b, true, v0, a0, zt0, 0);
   if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, true, v1, a1, zt1, 0);
+  // the spike lists of the step before the block (parity 1), from the
+  // spike bytes each thread has just loaded for its own neurons
+  wave_list_from_bytes<QN, 0>(A, S, 1, S.zc);
+  if constexpr (NL > 1) wave_list_from_bytes<QN, 1>(A, S, 1, S.zc + 2 * S.npad);
   double loss0 = 0.0, loss1 = 0.0;
   // loaded once: a global load inside the step would wait for the step's stores
   const int label = __builtin_amdgcn_readfirstlane(A.labels[b]);
   int cur = 0;
+  // the first step's input drive (with the service wave: in the ring)
+  float iin[QN];
+  if constexpr (!SVC) {
+    typedef float fqv __attribute__((ext_vector_type(QN)));
+    const fqv nv = *(const fqv*)(A.Iin + (size_t)b * (QN * kFwdThreads) + (size_t)threadIdx.x * QN);
+#pragma unroll
+    for (int q = 0; q < QN; ++q) iin[q] = nv[q];
+  }
   lds_barrier();
   // deferred softmax state (the softmax wave, lane k: class k)
   const int lane = threadIdx.x & (kWave - 1);
@@ -635,18 +738,17 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu((QN
     y0 = S.sy[lane];
     if constexpr (NL > 1) y1 = S.sy[A.K_out + lane];
   }
-  // input spikes of the first kFwdXSteps steps; each step then loads the
-  // row kFwdXSteps ahead
-  for (int tt = 0; tt < min(kFwdXSteps, A.steps); ++tt) {
-    const uint8_t* xrow = A.x + ((size_t)tt * A.B + b) * A.n_in;
-    for (int i = threadIdx.x; i < A.n_in; i += kFwdThreads) S.xs[tt * A.n_in + i] = xrow[i];
-  }
-  lds_barrier();
-  int ns0 = 0, ns1 = 0;   // spikes of the previous step in this wave, per layer
+  // spikes of the previous step in this wave whose readout is still to be
+  // summed, per layer (none at the block's start)
+  int ns0 = 0, ns1 = 0;
+  float unused[QN];
   for (int t = 0; t < A.steps; ++t) {
-    forward_layer_step<QN, 0>(A, S, t, b, cur, v0, a0, zt0, loss0, label, y0, d0, ns0);
+    // two layers of four neurons per thread and more: the softmax at the
+    // step's start (no spills)
+    constexpr bool SW = NL == 1 || QN < 4;
+    forward_layer_step<QN, 0, SW, SVC>(A, S, t, b, cur, v0, a0, zt0, loss0, label, y0, d0, ns0, iin);
     if constexpr (NL > 1)
-      forward_layer_step<QN, 1>(A, S, t, b, cur, v1, a1, zt1, loss1, label, y1, d1, ns1);
+      forward_layer_step<QN, 1, SW, SVC>(A, S, t, b, cur, v1, a1, zt1, loss1, label, y1, d1, ns1, unused);
     cur ^= 1;
   }
   if (A.K_out <= kWave && A.steps > 0) {
@@ -657,7 +759,7 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu((QN
     const int w = threadIdx.x >> 6;
     auto last_readout = [&](int li, int ns) {
       const float* WoutT = li == 0 ? A.L[0].WoutT : A.L[1].WoutT;
-      const int* spk = S.spk + li * kFwdWaves * A.jlist + w * A.jlist;
+      const int* spk = S.spk + ((li * 2 + (tl & 1)) * kFwdWaves + w) * A.jlist;
       ReadoutRows rr;
       readout_issue(A, WoutT, spk, ns, rr);
       const float Y = readout_sum(A, WoutT, spk, ns, rr);
@@ -689,6 +791,225 @@ __global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu((QN
     A.L[0].lossacc[b] += loss0;
     if constexpr (NL > 1) A.L[1].lossacc[b] += loss1;
   }
+}
+
+// ---------------------------------------------------------------- input drive and filter
+// The rows listed in lst[0, n) (ascending input indices) added to acc in
+// that order, U rows loaded before any is added: int16 rows kept packed
+// until the add (exact: the same values as Wt), fp32 rows from Wt at the
+// lane's neurons jof.
+template <int PW, bool W16>
+__device__ __forceinline__ void add_input_rows(const InputArgs& a, const int* lst, int n, int p0,
+                                               const int (&jof)[PW], float (&acc)[PW]) {
+  constexpr int U = W16 ? 8 : 4;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int qnp = a.qn * kFwdThreads;
+  for (int k0 = 0; k0 < n; k0 += U) {
+    const int ent = lst[min(k0 + (lane & (U - 1)), n - 1)];
+    const int nb = min(U, n - k0);   // rows of this batch (wave-uniform)
+    if constexpr (W16) {
+      typedef int16_t i16p __attribute__((ext_vector_type(PW)));
+      i16p k[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = __builtin_amdgcn_readlane(ent, u);
+        if (u < nb) k[u] = *(const i16p*)(a.W16 + (size_t)r * qnp + p0);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (u < nb)
+#pragma unroll
+          for (int e = 0; e < PW; ++e) acc[e] = acc[e] + (float)k[u][e] * 0x1p-14f;
+    } else {
+      float wr[U][PW];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = __builtin_amdgcn_readlane(ent, u);
+        if (u < nb)
+#pragma unroll
+          for (int e = 0; e < PW; ++e) wr[u][e] = a.Wt[(size_t)r * a.ldw + jof[e]];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (u < nb)
+#pragma unroll
+          for (int e = 0; e < PW; ++e) acc[e] = acc[e] + wr[u][e];
+    }
+  }
+}
+
+// The first layer's input part of the drive for every step of a block, one
+// wave per (step, batch element) and slice of 64 PW forward positions: the
+// active inputs in ascending order, listed in shared memory (up to kInList
+// at a time), their rows added in that order in fp32 starting from 0, the
+// prefix of the forward's sequential sum.  Rows come from W16 (exact: the
+// same values) when *w16ok, else from Wt.  Also the number of active
+// inputs.  Input rows whose length is a multiple of 4 are read as 32-bit
+// words, 1024 inputs per round trip (lane l holds inputs 4 l .. 4 l + 3 of
+// each 256); other rows as bytes, 512 per round trip.
+constexpr int kInPW = 8;     // forward positions per lane
+constexpr int kInList = 256; // list entries per wave
+__global__ __launch_bounds__(256) void input_drive_kernel(InputArgs a) {
+  constexpr int PW = kInPW;
+  __shared__ int lists[4][kInList];
+  const int lane = threadIdx.x & (kWave - 1);
+  int* lst = lists[threadIdx.x >> 6];
+  const int wv = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int qsh = __builtin_ctz(a.qn);                // qn is a power of two
+  const int slices = a.qn;                            // 512 qn / (64 PW)
+  const int pair = wv >> qsh;
+  if (pair >= a.steps * a.B) return;                  // the whole wave (no barriers below)
+  const int sl = wv & (slices - 1);
+  const int t = pair / a.B, b = pair - t * a.B;
+  const uint8_t* xr = a.x + ((size_t)t * a.B + b) * a.n_in;
+  const int p0 = (sl * kWave + lane) * PW;            // the lane's first position
+  const bool w16 = a.w16ok[0] != 0;
+  // the neurons of the lane's positions (position tid*QN + q holds neuron
+  // 64 QN (tid / 64) + 64 q + tid % 64), for rows of Wt
+  int jof[PW];
+#pragma unroll
+  for (int e = 0; e < PW; ++e) {
+    const int p = p0 + e, tid = p >> qsh, q = p & (a.qn - 1);
+    jof[e] = ((tid >> 6) << (6 + qsh)) + q * kWave + (tid & (kWave - 1));
+  }
+  float acc[PW];
+#pragma unroll
+  for (int e = 0; e < PW; ++e) acc[e] = 0.0f;
+  auto flush = [&](int n) {
+    if (w16) add_input_rows<PW, true>(a, lst, n, p0, jof, acc);
+    else add_input_rows<PW, false>(a, lst, n, p0, jof, acc);
+  };
+  int cnt = 0, n = 0;   // active inputs so far; entries in the list
+  const bool words = (a.n_in & 3) == 0 && ((uintptr_t)a.x & 3) == 0;
+  if (words) {
+    constexpr int G = 4;   // words per lane loaded together
+    const int nw = a.n_in >> 2;
+    const uint32_t* xw = (const uint32_t*)xr;
+    for (int base = 0; base < nw; base += kWave * G) {
+      uint32_t xv[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int k = base + g * kWave + lane;
+        xv[g] = k < nw ? xw[k] : 0u;
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        unsigned long long m[4];
+        int below = 0, c = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          m[k] = __ballot(((xv[g] >> (8 * k)) & 0xFFu) != 0);
+          below += lanes_below(m[k], lane);
+          c += __popcll(m[k]);
+        }
+        if (n + c > kInList) {   // the list is full: add its rows first
+          flush(n);
+          n = 0;
+        }
+        int own = 0;
+        const int i0 = 4 * (base + g * kWave + lane);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if ((xv[g] >> (8 * k)) & 0xFFu) lst[n + below + own++] = i0 + k;
+        n += c;
+        cnt += c;
+      }
+    }
+  } else {
+    constexpr int G = 8;   // bytes per lane loaded together
+    for (int base = 0; base < a.n_in; base += kWave * G) {
+      uint8_t xv[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int i = base + g * kWave + lane;
+        xv[g] = i < a.n_in ? xr[i] : 0;
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const bool on = xv[g] != 0;
+        const unsigned long long m = __ballot(on);
+        const int c = __popcll(m);
+        if (n + c > kInList) {
+          flush(n);
+          n = 0;
+        }
+        if (on) lst[n + lanes_below(m, lane)] = base + g * kWave + lane;
+        n += c;
+        cnt += c;
+      }
+    }
+  }
+  if (n > 0) flush(n);
+  float* o = a.Iin + ((size_t)t * a.B + b) * (a.qn * kFwdThreads) + p0;
+#pragma unroll
+  for (int e = 0; e < PW; e += 4) *(f32x4*)(o + e) = f32x4{acc[e], acc[e + 1], acc[e + 2], acc[e + 3]};
+  if (sl == 0 && lane == 0) a.nin[(size_t)t * a.B + b] = cnt;
+}
+
+// The first layer's input rows: their filter zbar over the block's steps
+// (zstart: its value at the block's start) and their p bytes, the same
+// recursion as the forward's filter rows.  One thread per four consecutive
+// inputs and batch element (32-bit words of x when rows allow, else bytes),
+// the inputs of a 16-step chunk loaded per round trip (32-bit offsets from
+// the block's x); the four inputs' words of a 4-step quad are adjacent in p8
+// (one 16-byte store).
+__global__ __launch_bounds__(256) void input_filter_kernel(InputArgs a) {
+  const int g = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;   // inputs 4 g .. 4 g + 3
+  const int i0 = 4 * g;
+  if (i0 >= a.n_in) return;
+  const int ni = min(4, a.n_in - i0);
+  const bool words = (a.n_in & 3) == 0 && ((uintptr_t)a.x & 3) == 0;
+  const uint32_t stride = (uint32_t)a.B * (uint32_t)a.n_in;   // bytes per step
+  float z[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    z[k] = k < ni ? a.zbar[(size_t)b * a.n_pre + i0 + k] : 0.0f;
+    if (k < ni) a.zstart[(size_t)b * a.ldi + i0 + k] = z[k];
+  }
+  // the quad words of inputs i0.. (16-row group i0 >> 4, rows i0 & 15 ..)
+  uint8_t* pb = a.p8 + (size_t)b * kKC * a.ldi * 16 + (size_t)(i0 >> 4) * 256 + (i0 & 15) * 4;
+  for (int t0 = 0; t0 < a.steps; t0 += kChunk) {
+    uint32_t xv[kChunk];   // byte k: input i0 + k at step t0 + u
+    uint32_t off = (uint32_t)t0 * stride + (uint32_t)b * a.n_in + i0;
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u, off += stride) {
+      xv[u] = 0;
+      if (t0 + u < a.steps) {
+        if (words) {
+          xv[u] = *(const uint32_t*)(a.x + off);
+        } else {
+          for (int k = 0; k < ni; ++k) xv[u] |= (uint32_t)a.x[off + k] << (8 * k);
+        }
+      }
+    }
+    uint8_t* cb = pb + (size_t)(t0 / kChunk) * a.ldi * 16;
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int tq = t0 + 4 * q4;   // the quad's first step
+      if (tq >= a.steps) break;
+      uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4) {
+        if (tq + s4 < a.steps) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const bool on = ((xv[4 * q4 + s4] >> (8 * k)) & 0xFFu) != 0;
+            w[k] |= (uint32_t)(on ? kPByte : 0) << (8 * s4);
+            z[k] = a.alpha * z[k] + (on ? 1.0f : 0.0f);
+          }
+        }
+      }
+      uint8_t* d = cb + q4 * 64;
+      if (ni == 4 && (i0 & 15) <= 12) {
+        __builtin_nontemporal_store(u32x4{w[0], w[1], w[2], w[3]}, (u32x4*)d);
+      } else {
+        for (int k = 0; k < ni; ++k) __builtin_nontemporal_store(w[k], (uint32_t*)(d + 4 * k));
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    if (k < ni) a.zbar[(size_t)b * a.n_pre + i0 + k] = z[k];
 }
 
 // ---------------------------------------------------------------- MFMA GEMM
@@ -1586,7 +1907,7 @@ __global__ __launch_bounds__(256) void pack16_kernel(const float* W, int n_rec, 
     if (!exact) ok[0] = 0;   // every thread that finds one writes the same value
     else kmax = max(kmax, (int)fabsf(k));
     const int j = (int)(idx / n_pre), i = (int)(idx % n_pre);
-    W16[(size_t)i * (qn * kFwdThreads) + (size_t)(j % kFwdThreads) * qn + j / kFwdThreads] =
+    W16[(size_t)i * (qn * kFwdThreads) + fwd_position(j, qn)] =
         exact ? (int16_t)k : (int16_t)0;
   }
   max_k(ok, kmax);
@@ -1614,7 +1935,7 @@ __global__ __launch_bounds__(256) void online_w_kernel(OnlineArgs a) {
     const bool exact = k == rintf(k) && fabsf(k) <= 32767.0f;
     if (!exact) a.ok[0] = 0;   // every thread that finds one writes the same value
     else kmax = max(kmax, (int)fabsf(k));
-    a.W16[(size_t)i * (a.qn * kFwdThreads) + (size_t)(j % kFwdThreads) * a.qn + j / kFwdThreads] =
+    a.W16[(size_t)i * (a.qn * kFwdThreads) + fwd_position(j, a.qn)] =
         exact ? (int16_t)k : (int16_t)0;
   }
   max_k(a.ok, kmax);
@@ -1698,23 +2019,53 @@ hipError_t grant_smem(int bytes) {
   return result;
 }
 
-template <int QN, int NL>
+template <int QN, int NL, bool SVC>
 hipError_t launch_forward_qn(const FwdArgs& a, hipStream_t s) {
   if (a.smem > (size_t)kMaxSmem) return hipErrorInvalidValue;
-  hipError_t e = grant_smem<&forward_kernel<QN, NL>>(kMaxSmem);
+  hipError_t e = grant_smem<&forward_kernel<QN, NL, SVC>>(kMaxSmem);
   if (e != hipSuccess) return e;
-  forward_kernel<QN, NL><<<a.B, kFwdThreads, a.smem, s>>>(a);
+  forward_kernel<QN, NL, SVC><<<a.B, SVC ? kFwdThreads + 64 : kFwdThreads, a.smem, s>>>(a);
   return hipGetLastError();
 }
 
+template <int QN, int NL>
+hipError_t launch_forward_svc(const FwdArgs& a, hipStream_t s) {
+  if constexpr (QN <= 4) {
+    if (a.svc) return launch_forward_qn<QN, NL, true>(a, s);
+  }
+  if constexpr (QN >= 4) return launch_forward_qn<QN, NL, false>(a, s);
+  return hipErrorInvalidValue;   // at most two neurons per thread: always with the service wave
+}
+
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s) {
-  const int qn = (a.n_rec + kFwdThreads - 1) / kFwdThreads;
-  if (qn <= 1) return a.n_layers > 1 ? launch_forward_qn<1, 2>(a, s) : launch_forward_qn<1, 1>(a, s);
-  if (qn <= 2) return a.n_layers > 1 ? launch_forward_qn<2, 2>(a, s) : launch_forward_qn<2, 1>(a, s);
-  if (qn <= 4) return a.n_layers > 1 ? launch_forward_qn<4, 2>(a, s) : launch_forward_qn<4, 1>(a, s);
-  if (qn <= 8) return a.n_layers > 1 ? launch_forward_qn<8, 2>(a, s) : launch_forward_qn<8, 1>(a, s);
-  if (qn <= 16) return a.n_layers > 1 ? launch_forward_qn<16, 2>(a, s) : launch_forward_qn<16, 1>(a, s);
-  return hipErrorInvalidValue;
+  const int qn = forward_qn(a.n_rec);
+  if (a.svc && qn > 4) return hipErrorInvalidValue;
+  const bool two = a.n_layers > 1;
+  switch (qn) {
+    case 1: return two ? launch_forward_svc<1, 2>(a, s) : launch_forward_svc<1, 1>(a, s);
+    case 2: return two ? launch_forward_svc<2, 2>(a, s) : launch_forward_svc<2, 1>(a, s);
+    case 4: return two ? launch_forward_svc<4, 2>(a, s) : launch_forward_svc<4, 1>(a, s);
+    case 8: return two ? launch_forward_svc<8, 2>(a, s) : launch_forward_svc<8, 1>(a, s);
+    case 16: return two ? launch_forward_svc<16, 2>(a, s) : launch_forward_svc<16, 1>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_input_drive(const InputArgs& a, hipStream_t s) {
+  if (a.steps <= 0 || a.n_in <= 0) return hipSuccess;
+  // one wave per (step, batch element) and slice of 64 kInPW positions
+  static_assert(kFwdThreads / (64 * kInPW) == 1, "a slice per neuron per thread");
+  const long long waves = (long long)a.steps * a.B * a.qn;
+  if (waves >= (1ll << 31) || (a.qn & (a.qn - 1)) != 0) return hipErrorInvalidValue;
+  input_drive_kernel<<<cdiv(waves, 4), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_input_filter(const InputArgs& a, hipStream_t s) {
+  if (a.steps <= 0 || a.n_in <= 0) return hipSuccess;
+  dim3 grid(cdiv(cdiv(a.n_in, 4), 256), a.B);
+  input_filter_kernel<<<grid, 256, 0, s>>>(a);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s) {

@@ -186,7 +186,7 @@ def eprop_destroy(ctx):
     load_library().eprop_destroy(ctx)
 
 
-STATIC_SCRATCH_BYTES = 160 << 20      # EPROP_STATIC_SCRATCH_BYTES
+STATIC_SCRATCH_BYTES = 256 << 20      # EPROP_STATIC_SCRATCH_BYTES
 
 
 def eprop_sequence_static(cfg: eprop_config, weights: Sequence[torch.Tensor], x: torch.Tensor, T: int,

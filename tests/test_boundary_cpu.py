@@ -36,21 +36,30 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
         n = eprop.eprop_workspace_bytes(eprop.make_config(shape))
         traces = sum(4 * shape.batch * shape.n_pre(l) * (shape.n_rec + shape.n_adaptive)
                      for l in range(shape.n_layers))
-        # per-step vectors for two blocks of at most 256 steps (one being
-        # written by the forward pass while the other is read; the filtered
+        # per-step vectors for three blocks of at most 256 steps (the forward
+        # writes one while the passes after it read the others; the filtered
         # presynaptic vector twice: fp32 and as fp16 pairs), plus one
         # block's eligibility coefficients per layer and slot (three per neuron
         # and step)
+        slots = 3
         bp = -(-shape.batch // 16) * 16
         nv = -(-shape.n_rec // 256) * 256
         per_step = sum(4 * (2 * bp * nv + 2 * (shape.n_pre(l) + 63) * shape.batch
                             + (shape.n_out + 32 + shape.n_rec + 32) * bp)
                        for l in range(shape.n_layers))
         coef = 4 * 3 * shape.batch * (shape.n_rec + 63)
-        # at most 8 fp64 partial gradient accumulators (batch splits) per layer
-        partial = sum(8 * 8 * (shape.n_pre(l) + 63) * shape.n_rec for l in range(shape.n_layers))
-        assert traces <= n <= (traces * 1.05 + 2 * 256 * per_step + 2 * shape.n_layers * 256 * coef
-                               + partial + (16 << 20)), \
+        # fp64 partial gradient accumulators: up to 8 batch splits per layer,
+        # more for large batches (a split walks at most about 26 elements)
+        splits = max(8, -(-shape.batch // 26))
+        partial = sum(splits * 8 * (shape.n_pre(l) + 63) * shape.n_rec for l in range(shape.n_layers))
+        # the first layer's input drive of two blocks, at 512 positions per
+        # neuron per forward thread
+        qn = 1
+        while qn * 512 < shape.n_rec:
+            qn *= 2
+        indrive = 2 * 256 * shape.batch * (512 * qn + 1) * 4
+        assert traces <= n <= (traces * 1.05 + slots * 256 * per_step + slots * shape.n_layers * 256 * coef
+                               + partial + indrive + (16 << 20)), \
             (name, n, traces)
     # the same shape with any T needs the same workspace: T is not an input
     s = synth.WORKLOADS["ralif_b64_n512_t500"]
@@ -114,13 +123,14 @@ def test_binding_refuses_to_run_without_a_gpu_or_library(monkeypatch):
 
 
 def test_shape_past_the_forward_shared_memory_is_rejected():
-    # a recurrent layer of 8192 neurons needs more than 160 KiB of shared
-    # memory in the forward kernel: no workspace size, and a reason
-    shape = synth.EpropShape(batch=1, n_in=100, n_rec=8192, n_out=10, T=5, n_adaptive=0)
+    # two recurrent layers of 8192 neurons need more than 160 KiB of shared
+    # memory in the forward kernel (spike lists of 16 neurons per thread in
+    # two layers): no workspace size, and a reason; one such layer fits
+    shape = synth.EpropShape(batch=1, n_in=100, n_rec=8192, n_out=10, T=5, n_adaptive=0, n_layers=2)
     assert eprop.eprop_workspace_bytes(eprop.make_config(shape)) == 0
     assert "shared memory" in eprop.eprop_last_error()
-    ff = shape.replace(recurrent=0)
-    assert eprop.eprop_workspace_bytes(eprop.make_config(ff)) > 0
+    one = shape.replace(n_layers=1)
+    assert eprop.eprop_workspace_bytes(eprop.make_config(one)) > 0
 
 
 def test_static_entry_rejects_shapes_past_its_scratch_before_any_device_call():
@@ -139,8 +149,8 @@ def test_static_entry_rejects_shapes_past_its_scratch_before_any_device_call():
                                      None, None) == eprop.EPROP_EINVAL
     # the size the header states
     hdr = open(HEADER).read()
-    assert "#define EPROP_STATIC_SCRATCH_BYTES (160u << 20)" in hdr
-    assert eprop.STATIC_SCRATCH_BYTES == 160 << 20
+    assert "#define EPROP_STATIC_SCRATCH_BYTES (256u << 20)" in hdr
+    assert eprop.STATIC_SCRATCH_BYTES == 256 << 20
 
 
 def _coef(shape, cls):

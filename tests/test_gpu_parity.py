@@ -75,10 +75,10 @@ def test_ragged_shapes(name):
 
 
 # ---------------------------------------------------------------- large layers
-# 8 and 16 neurons per forward thread, up to the largest accepted layer (a
-# feed-forward layer of 8192); every spike compared, the gradient on sampled
-# synapses (with every index-range edge) and the readout gradient in full.
-@pytest.mark.parametrize("n_rec,n_in,rec", [(3000, 200, 1), (6000, 100, 1), (8192, 200, 0)])
+# 8 and 16 neurons per forward thread, up to the largest accepted layer
+# (8192 neurons, recurrent or not); every spike compared, the gradient on
+# sampled synapses (with every index-range edge) and the readout gradient in full.
+@pytest.mark.parametrize("n_rec,n_in,rec", [(3000, 200, 1), (6000, 100, 1), (8192, 200, 0), (8192, 200, 1)])
 def test_large_layers(n_rec, n_in, rec):
     shape = synth.EpropShape(batch=2, n_in=n_in, n_rec=n_rec, n_out=10, T=24, recurrent=rec,
                              n_adaptive=n_rec // 2)
