@@ -69,7 +69,7 @@ struct Layer {
   float *psiK[kSlots], *LK[kSlots], *deltaK[kSlots], *ztK[kSlots];
   // the binary presynaptic values (one byte per step), and the block
   // coefficients of the eligibility recursion as scaled fp16 pairs
-  uint8_t* p8[kSlots];
+  uint16_t* pbits[kSlots];
   uint32_t *coefU[kSlots], *coefV[kSlots], *coefH[kSlots], *coefW[kSlots];
   float* coefS[kSlots];
   float* zstart[kSlots];                 // presynaptic filter at each block's start [B][ldi]
@@ -121,7 +121,6 @@ struct Plan {
   int Kmax = kBlockSteps, Bp = 0, rows = 0, ldk = 0, ldn = 0, ldc = 0, jlist = 0, out_splits = 1;
   size_t smem = 0;
   int svc = 0;                      // the forward's service wave (FwdArgs::svc)
-  int zgroup = 1;
   size_t bytes = 0;
 };
 
@@ -323,7 +322,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
     for (int sl = 0; sl < slots; ++sl) {
       // p: one byte per row and step; coefficients: a scaled fp16 pair per
       // value (4 bytes)
-      L.p8[sl] = (uint8_t*)take((size_t)B * L.n_pre_pad * KM);
+      L.pbits[sl] = (uint16_t*)take(sizeof(uint16_t) * B * L.n_pre_pad * (KM / eprop::kChunk));
       L.coefU[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
       L.coefV[sl] = (uint32_t*)take(plan->na2 > 0 ? sizeof(uint32_t) * B * ldc * KM : 0);
       L.coefH[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
@@ -340,21 +339,12 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
   const size_t smem_base = sizeof(int) * (NL * 2 * W * plan->jlist + NL * 2 * W + KM) +
                            sizeof(float) * (NL * 2 * W * K + NL * K + fwd_rows) + NL * 2 * npad4;
   // the forward's service wave and its input-drive ring (three steps of 512
-  // QN floats) where that fits beside an eligibility workgroup, and the binary
-  // presynaptic bytes written 16 steps at a time (one 16-byte record per row)
-  // when that keeps the forward's shared memory small enough, else 8 or 4
-  // (16 bytes of alignment before them)
+  // QN floats) where that fits beside an eligibility workgroup
   const size_t ring = (size_t)3 * qn * eprop::kFwdThreads * sizeof(float);
-  auto fwd_smem = [&](int zg, int svc) {
-    return smem_base + (svc ? ring : 0) + 16 + (size_t)zg * fwd_rows;
-  };
+  const size_t fwd_smem = smem_base + sizeof(uint32_t) * fwd_rows;   // and the rows' p bits
   constexpr size_t kShareSmem = 96 * 1024;   // leaves an eligibility workgroup room on the CU
-  plan->svc = qn <= 2 || (qn == 4 && fwd_smem(4, 1) <= kShareSmem);
-  plan->zgroup = 4;
-  for (int zg : {16, 8}) {
-    if (fwd_smem(zg, plan->svc) <= kShareSmem) { plan->zgroup = zg; break; }
-  }
-  plan->smem = fwd_smem(plan->zgroup, plan->svc);
+  plan->svc = qn <= 2 || (qn == 4 && fwd_smem + ring <= kShareSmem);
+  plan->smem = fwd_smem + (plan->svc ? ring : 0);
   plan->bytes = round_up(off, 256);
 }
 
@@ -547,7 +537,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     const Layer& L = P.layers[std::min(l, c.n_layers - 1)];
     f.Wt = L.Wt; f.ldw = L.ldw; f.W16 = L.W16; f.WoutT = L.WoutT;
     f.v = L.v; f.a = L.a; f.ztil = L.ztil; f.z = L.z; f.zbar = L.zbar; f.y = L.y;
-    f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.p8 = L.p8[sl]; f.zstart = L.zstart[sl];
+    f.lossacc = L.lossacc; f.psiK = L.psiK[sl]; f.pbits = L.pbits[sl]; f.zstart = L.zstart[sl];
     f.deltaK = L.deltaK[sl]; f.ztK = L.ztK[sl];
     f.n_inl = L.n_inl; f.n_pre = L.n_pre; f.ldi = L.n_pre_pad;
   }
@@ -560,7 +550,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   ia.x = x; ia.n_in = c.n_in; ia.B = c.batch; ia.steps = steps;
   ia.Wt = L0.Wt; ia.ldw = L0.ldw; ia.W16 = L0.W16; ia.qn = eprop::forward_qn(c.n_rec); ia.w16ok = P.w16ok;
   ia.Iin = P.Iin[ib]; ia.nin = P.nin[ib];
-  ia.zbar = L0.zbar; ia.n_pre = L0.n_pre; ia.zstart = L0.zstart[sl]; ia.p8 = L0.p8[sl];
+  ia.zbar = L0.zbar; ia.n_pre = L0.n_pre; ia.zstart = L0.zstart[sl]; ia.pbits = L0.pbits[sl];
   ia.ldi = L0.n_pre_pad; ia.alpha = c.alpha;
   if (ctx->in_ready) {
     ctx->in_ready = false;
@@ -575,7 +565,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   fa.n_adaptive = c.n_adaptive; fa.Kmax = P.Kmax; fa.steps = steps;
   fa.ldj = P.layers[0].ldv; fa.ldk = P.ldk; fa.ldn = P.ldn; fa.jlist = P.jlist;
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
-  fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.zgroup = P.zgroup; fa.svc = P.svc;
+  fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.svc = P.svc;
   fa.model = c.neuron_model;
   for (int m = 0; m < 2; ++m) {
     fa.mA[m][0] = (float)P.gen.A[m][0]; fa.mA[m][1] = (float)P.gen.A[m][1];
@@ -662,7 +652,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     const Layer& L = P.layers[l];
     eprop::TraceArgs ta;
     ta.ebar = L.ebar; ta.epsa = L.epsa; ta.epsv = L.epsv; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
-    ta.n_split = L.n_split; ta.p8 = L.p8[sl];
+    ta.n_split = L.n_split; ta.pbits = L.pbits[sl];
     ta.zstart = L.zstart[sl];
     ta.U = L.coefU[sl]; ta.V = P.na2 > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
     ta.W = L.coefW[sl]; ta.reset_through = P.rt;

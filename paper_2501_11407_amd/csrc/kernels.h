@@ -7,10 +7,9 @@
 //   psiK   [Kmax*Bp][ldv]  pseudo-derivative (ldv = n_rec rounded to 256)
 //   deltaK [rows][ldk]     readout error (softmax - onehot)
 //   ztK    [rows][ldn]     kappa-filtered spikes
-//   p8     [B][Kmax/16][ldi/16][4][16][4] binary presynaptic vector, one
-//                                byte per step (0x3C, the high byte of fp16
-//                                1.0, or 0); per 16-step chunk and 16-row
-//                                group, the four 4-step quads of its rows
+//   pbits  [B][Kmax/16][ldi]     binary presynaptic vector: per 16-step
+//                                chunk and row, one 16-bit word (bit s: step
+//                                16 c + s)
 //   zstart [B][ldi]              presynaptic filter at the block's start
 // Two MFMA GEMMs follow: the learning signal LK = deltaK * W_out (rows as
 // psiK) and the readout gradient dW_out += deltaK^T * ztK; then the block
@@ -54,7 +53,7 @@ struct FwdLayer {
   float* y;                      // state [B][K_out]
   double* lossacc;               // [B]
   float* psiK;                   // [rows][ldj]
-  uint8_t* p8;                   // [B][Kmax/16][ldi/16][4][16][4]
+  uint16_t* pbits;               // [B][Kmax/16][ldi]
   float* zstart;                 // [B][ldi]
   float* deltaK; float* ztK;     // [rows][ldk], [rows][ldn]
   int n_inl, n_pre, ldi;
@@ -74,7 +73,6 @@ struct FwdArgs {
   int W32;
   int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldk, ldn, jlist;  // ldj: row stride of psiK
   float alpha, rho, kappa, thr, beta, gamma_over_thr;
-  int zgroup;                    // steps of p bytes written together (4, 8 or 16)
   // neuron_model 1: h = A h_prev + b I + r z_prev, spike argument
   // u = c . h - thr (the two-compartment neuron, coefficients derived on the
   // host; v holds h0, a holds h1)
@@ -95,12 +93,12 @@ hipError_t launch_forward(const FwdArgs& a, hipStream_t s);
 // from 0 (rows from W16 when *w16ok, else Wt), and nin[t][b], their number;
 // launch_input_filter advances zbar [B][n_pre] of the input rows over the
 // steps (their value at the start into zstart [B][ldi]) and writes their p
-// bytes into p8 as the forward does for its rows.
+// bits into pbits as the forward does for its rows.
 struct InputArgs {
   const uint8_t* x; int n_in, B, steps;
   const float* Wt; int ldw; const int16_t* W16; int qn; const int* w16ok;
   float* Iin; int* nin;
-  float* zbar; int n_pre; float* zstart; uint8_t* p8; int ldi; float alpha;
+  float* zbar; int n_pre; float* zstart; uint16_t* pbits; int ldi; float alpha;
 };
 hipError_t launch_input_drive(const InputArgs& a, hipStream_t s);
 hipError_t launch_input_filter(const InputArgs& a, hipStream_t s);
@@ -169,7 +167,7 @@ struct TraceArgs {
   float* epsv;     // reset_through: [B][n_pre_pad / 256][n_jt][256 * 16]
   double* acc;     // [n_split][n_pre_pad][ldj] (row-major)
   size_t acc_stride;
-  const uint8_t* p8;                  // [B][kKC][ldi/16][4][16][4], ldi = n_pre_pad
+  const uint16_t* pbits;              // [B][kKC][ldi], ldi = n_pre_pad
   const float* zstart;                // [B][ldi] (reset-stopped form only)
   const uint32_t* U; const uint32_t* V; const uint32_t* H; const uint32_t* W;
   const float* S;                     // as CoefArgs

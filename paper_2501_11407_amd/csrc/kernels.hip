@@ -82,10 +82,6 @@ __device__ __forceinline__ void split16(float x, _Float16& hi, _Float16& lo) {
   lo = (_Float16)(x - (float)hi);
 }
 
-// p as stored: the high byte of fp16 1.0 for a spike, 0 otherwise, so that a
-// byte permute places it in both halves of an fp16 pair (0x3C00 0x3C00)
-constexpr uint8_t kPByte = 0x3C;
-
 // scaled value -> one 32-bit word: hi in the low half, lo in the high half
 __device__ __forceinline__ uint32_t pair_word(float x) {
   _Float16 hi, lo;
@@ -140,7 +136,7 @@ struct FwdLds {
   int* nin;                      // [steps]: active inputs of the first layer per step
   float* part; float* sy;
   float* szb;                    // filter of the rows the workgroup handles
-  uint8_t* zb;                   // [rows][zgroup]: their p bytes of the last zgroup steps
+  uint32_t* zbits;               // [rows]: their p bits of the current 16-step chunk (bit t % 16)
   uint8_t* zc;                   // [n_layers][2][npad]: spikes of this and the previous step
   bool w16;                      // the int16 weights are exact (FwdLayer::W16)
   int w16max;                    // their largest |k|
@@ -271,7 +267,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   const bool recurrent = Ly.n_pre > Ly.n_inl;
   const int ridx = LI == 0 ? 0 : S.rows0;      // first filter row of this layer
   float* szb = S.szb + ridx;
-  uint8_t* zring = S.zb + ridx * A.zgroup;
+  uint32_t* zbits = S.zbits + ridx;
   float* sy = S.sy + LI * A.K_out;
   const int pc = t & 1, pp = pc ^ 1;           // parity of this and the previous step
   int* spk_now = S.spk + ((LI * 2 + pc) * kFwdWaves + w) * A.jlist;
@@ -323,10 +319,10 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   };
   // the rows this wave filters: those of its neurons
   const int jlo = w * (kWave * QN), jhi = min(A.n_rec, jlo + kWave * QN);
-  const int zslot = t & (A.zgroup - 1);
+  const int zslot = t & (kChunk - 1);
   auto filter_one = [&](int idx, uint8_t pv) {
     const bool on = pv != 0;
-    zring[idx * A.zgroup + zslot] = on ? kPByte : 0;
+    if (on) zbits[idx] |= 1u << zslot;   // the lane owns the row
     szb[idx] = A.alpha * szb[idx] + (on ? 1.0f : 0.0f);
   };
   // The presynaptic filter and the next step's input drive, off the
@@ -522,7 +518,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // Global stores of the step go last: a load waits for every store issued
   // before it, so stores ahead of the drive and readout loads would lengthen
   // the step.  Per-step vectors: psi, ztilde, the spike words, and (every
-  // zgroup steps) the binary presynaptic bytes ([b][t/16][i][16]).
+  // 16 steps) the binary presynaptic bits ([b][t/16][i]).
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
     const int j = fwd_neuron<QN>(tid, q);
@@ -539,17 +535,14 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   }
   if (defer && w == kSoftWave && t > 1 && lane < A.K_out)
     __builtin_nontemporal_store(dk, Ly.deltaK + (row - 2 * A.Bp) * A.ldk + lane);
-  // the p bytes go out zgroup steps at a time, as 4-step quads into the
-  // chunk's [16-row group][quad][row][4] layout (bytes past the block's last
-  // step are ignored downstream)
-  if ((t & (A.zgroup - 1)) == A.zgroup - 1 || t == A.steps - 1) {
-    uint8_t* cb = Ly.p8 + ((size_t)b * kKC + t / kChunk) * Ly.ldi * 16;
-    const int q0 = ((t & (kChunk - 1)) & ~(A.zgroup - 1)) >> 2;
+  // the p bits of a chunk go out at its last step (or the block's), one
+  // 16-bit word per row, and the row's bits start over (bits past the
+  // block's last step are zero)
+  if ((t & (kChunk - 1)) == kChunk - 1 || t == A.steps - 1) {
+    uint16_t* cb = Ly.pbits + ((size_t)b * kKC + t / kChunk) * Ly.ldi;
     auto flush = [&](int idx, int i) {
-      uint8_t* d = cb + (size_t)(i >> 4) * 256 + (i & 15) * 4;
-      const uint32_t* src = (const uint32_t*)(zring + idx * A.zgroup);
-      for (int q = 0; q < (A.zgroup >> 2); ++q)
-        __builtin_nontemporal_store(src[q], (uint32_t*)(d + (q0 + q) * 64));
+      __builtin_nontemporal_store((uint16_t)zbits[idx], cb + i);
+      zbits[idx] = 0u;
     };
     for (int j = jlo + lane; j < jhi; j += kWave) {
       if (LI == 0) {
@@ -694,12 +687,8 @@ __global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__
   S.part = (float*)(S.nin + A.Kmax);               // [NL][2][waves][K_out]
   S.sy = S.part + NL * 2 * kFwdWaves * A.K_out;    // [NL][K_out]
   S.szb = S.sy + NL * A.K_out;                     // [rows]
-  // 16-byte aligned by an offset from smem: an integer round trip of the
-  // pointer would lose its address space (generic accesses wait for the
-  // step's global loads as well)
-  const size_t zb_off = (((unsigned char*)(S.szb + rows) - smem) + 15) & ~(size_t)15;
-  S.zb = smem + zb_off;                            // [rows][zgroup]
-  S.zc = S.zb + A.zgroup * rows;                   // [NL][2][npad]
+  S.zbits = (uint32_t*)(S.szb + rows);             // [rows]
+  S.zc = (uint8_t*)(S.zbits + rows);               // [NL][2][npad]
   S.w16 = A.w16ok[0] != 0;
   S.w16max = A.w16ok[1];
   if constexpr (SVC) {
@@ -709,7 +698,7 @@ __global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__
     }
   }
 
-  for (int e = threadIdx.x; e < A.zgroup * rows; e += kFwdThreads) S.zb[e] = 0;
+  for (int e = threadIdx.x; e < rows; e += kFwdThreads) S.zbits[e] = 0u;
   for (int e = threadIdx.x; e < A.steps; e += kFwdThreads) S.nin[e] = A.nin[(size_t)e * A.B + b];
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
   forward_state<QN, 0>(A, S, b, true, v0, a0, zt0, 0);
@@ -947,12 +936,12 @@ __global__ __launch_bounds__(256) void input_drive_kernel(InputArgs a) {
 }
 
 // The first layer's input rows: their filter zbar over the block's steps
-// (zstart: its value at the block's start) and their p bytes, the same
+// (zstart: its value at the block's start) and their p bits, the same
 // recursion as the forward's filter rows.  One thread per four consecutive
 // inputs and batch element (32-bit words of x when rows allow, else bytes),
 // the inputs of a 16-step chunk loaded per round trip (32-bit offsets from
-// the block's x); the four inputs' words of a 4-step quad are adjacent in p8
-// (one 16-byte store).
+// the block's x); the four inputs' 16-bit words of a chunk are adjacent (one
+// 8-byte store).
 __global__ __launch_bounds__(256) void input_filter_kernel(InputArgs a) {
   const int g = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;   // inputs 4 g .. 4 g + 3
   const int i0 = 4 * g;
@@ -966,8 +955,6 @@ __global__ __launch_bounds__(256) void input_filter_kernel(InputArgs a) {
     z[k] = k < ni ? a.zbar[(size_t)b * a.n_pre + i0 + k] : 0.0f;
     if (k < ni) a.zstart[(size_t)b * a.ldi + i0 + k] = z[k];
   }
-  // the quad words of inputs i0.. (16-row group i0 >> 4, rows i0 & 15 ..)
-  uint8_t* pb = a.p8 + (size_t)b * kKC * a.ldi * 16 + (size_t)(i0 >> 4) * 256 + (i0 & 15) * 4;
   for (int t0 = 0; t0 < a.steps; t0 += kChunk) {
     uint32_t xv[kChunk];   // byte k: input i0 + k at step t0 + u
     uint32_t off = (uint32_t)t0 * stride + (uint32_t)b * a.n_in + i0;
@@ -982,29 +969,25 @@ __global__ __launch_bounds__(256) void input_filter_kernel(InputArgs a) {
         }
       }
     }
-    uint8_t* cb = pb + (size_t)(t0 / kChunk) * a.ldi * 16;
+    uint32_t m[4] = {0u, 0u, 0u, 0u};   // the chunk's bits of each input
 #pragma unroll
-    for (int q4 = 0; q4 < 4; ++q4) {
-      const int tq = t0 + 4 * q4;   // the quad's first step
-      if (tq >= a.steps) break;
-      uint32_t w[4] = {0u, 0u, 0u, 0u};
+    for (int u = 0; u < kChunk; ++u) {
+      if (t0 + u < a.steps) {
 #pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4) {
-        if (tq + s4 < a.steps) {
-#pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const bool on = ((xv[4 * q4 + s4] >> (8 * k)) & 0xFFu) != 0;
-            w[k] |= (uint32_t)(on ? kPByte : 0) << (8 * s4);
-            z[k] = a.alpha * z[k] + (on ? 1.0f : 0.0f);
-          }
+        for (int k = 0; k < 4; ++k) {
+          const bool on = ((xv[u] >> (8 * k)) & 0xFFu) != 0;
+          m[k] |= (on ? 1u : 0u) << u;
+          z[k] = a.alpha * z[k] + (on ? 1.0f : 0.0f);
         }
       }
-      uint8_t* d = cb + q4 * 64;
-      if (ni == 4 && (i0 & 15) <= 12) {
-        __builtin_nontemporal_store(u32x4{w[0], w[1], w[2], w[3]}, (u32x4*)d);
-      } else {
-        for (int k = 0; k < ni; ++k) __builtin_nontemporal_store(w[k], (uint32_t*)(d + 4 * k));
-      }
+    }
+    uint16_t* d = a.pbits + ((size_t)b * kKC + t0 / kChunk) * a.ldi + i0;
+    if (ni == 4) {
+      __builtin_nontemporal_store((unsigned long long)m[0] | ((unsigned long long)m[1] << 16) |
+                                      ((unsigned long long)m[2] << 32) | ((unsigned long long)m[3] << 48),
+                                  (unsigned long long*)d);
+    } else {
+      for (int k = 0; k < ni; ++k) __builtin_nontemporal_store((uint16_t)m[k], d + k);
     }
   }
 #pragma unroll
@@ -1438,7 +1421,7 @@ __device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, uint32_t off, f
 
 constexpr int kRing = 4;                              // chunk slots
 constexpr int kOpBytes = kTileJ * 64;                 // one coefficient operand of a chunk: 16 rows x 64 B
-constexpr int kPBytes = kTileI * 16;                  // the chunk's p records: 256 rows x 16 B
+constexpr int kPBytes = kTileI * 2;                   // the chunk's p bits: 256 rows x 16 bits
 constexpr int kWaveRows = kTileI / 4;                 // rows of a wave sub-tile
 constexpr uint32_t kSubTileBytes = kWaveRows * kTileJ * 4;   // a wave's traces of one array (4 KiB)
 constexpr int kScalWave = 256;                        // floats of one wave's scalar copy (64 lanes x 16 B)
@@ -1532,10 +1515,10 @@ struct TraceTile {
     w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index, uniform
     live = i0 + kWaveRows * w < a.n_pre;                    // the wave holds a real row
     copier = (w < 2) || (w == 2 && ALIF) || (w == 3 && RT);
-    // p: the records of rows i0 + 64 w .. +63 are one contiguous 1 KiB run;
+    // p: the bits of rows i0 + 64 w .. +63 are one contiguous 128-byte run;
     // coefficients: lane l takes row l / 4 of the 16 columns, 16-byte unit
     // (l % 4) ^ ((row / 2) % 4) (see issue)
-    pvoff = (uint32_t)(i0 + kWaveRows * w) * 16u + (uint32_t)lane * 16u;
+    pvoff = (uint32_t)(i0 + kWaveRows * w) * 2u + (uint32_t)(lane & 7) * 16u;
     const int row = lane >> 2;
     cvoff = (uint32_t)(j0 + row) * 64u + (uint32_t)((lane & 3) ^ ((row >> 1) & 3)) * 16u;
   }
@@ -1562,9 +1545,10 @@ struct TraceTile {
   __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
     char* slot = (char*)(sm + sl * SLOT);
     if constexpr (P == 0) {
-      const uint32_t estride = (uint32_t)(kKC * a.ldi * 16);         // bytes of one element
-      const auto pr = make_rsrc(a.p8 + (size_t)b * estride, estride);
-      dma16b(pr, pvoff, (uint32_t)(c * a.ldi * 16), slot + kWaveRows * w * 16);
+      const uint32_t estride = (uint32_t)(kKC * a.ldi * 2);          // bytes of one element
+      const auto pr = make_rsrc((const char*)a.pbits + (size_t)b * estride, estride);
+      // the wave's 64 rows: 128 bytes, lanes 0-7 (one instruction per wave)
+      if (lane < 8) dma16b(pr, pvoff, (uint32_t)(c * a.ldi * 2), slot + kWaveRows * w * 2);
     } else {
       if (copier) {
         const uint32_t estride = (uint32_t)(kKC * a.ldc * 64);       // bytes of one element
@@ -1768,15 +1752,13 @@ struct TraceTile {
                       : zero8;
 #pragma unroll
         for (int bi = 0; bi < 4; ++bi) {
-          // steps 4g .. 4g+3 of row r of group zg: four p bytes (0 or 0x3C)
-          // -> (p, p) fp16 pairs, byte e into bytes 1 and 3 of word e (0
-          // elsewhere); a half-wave reads 32 consecutive words
-          const int zg = 4 * w + bi;
-          const uint32_t pb = *(const uint32_t*)(slot + zg * 256 + g * 64 + r * 4);
+          // steps 4g .. 4g+3 of row 16 bi + r of the wave: four p bits ->
+          // (p, p) fp16 pairs (1.0 = 0x3C00 in both halves of word e); the
+          // 16 rows' words are 32 consecutive bytes, read by every g alike
+          const uint32_t pb = (uint32_t)*(const uint16_t*)(slot + (kWaveRows * w + 16 * bi + r) * 2) >> (4 * g);
           u32x4 w1;
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            w1[e] = __builtin_amdgcn_perm(0u, pb, (uint32_t)((e << 24) | (0x0C << 16) | (e << 8) | 0x0C));
+          for (int e = 0; e < 4; ++e) w1[e] = ((pb >> e) & 1u) ? 0x3C003C00u : 0u;
           const f16x8 bz = __builtin_bit_cast(f16x8, w1);
           cU[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[0], bz, cU[bi], 0, 0, 0);
           cH[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz, cH[bi], 0, 0, 0);
