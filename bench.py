@@ -55,7 +55,7 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     neurons) read once and written once, one fp64 gradient accumulator of
     every (i, j) read and written once; the first launch after a reset reads
     neither.  Per timestep covered, the operands read once: the binary
-    presynaptic vector [B, N_pre] (one byte each), the coefficients U, H
+    presynaptic vector [B, N_pre] (one bit each), the coefficients U, H
     [B, N] and V [B, N_adaptive] (4-byte pair words); per launch the seven
     scalars c, q, P, D and the three block-start coefficients [B, N], and
     the block-start filter [B, N_pre].  With the reset path kept
@@ -66,16 +66,16 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     trace = 4 * B * npre * ((2 if rt else 1) * N + NA) + 8 * npre * N      # one direction
     rows = (3 if rt else 2) * N + NA
     scalars = 9 if rt else 7
-    operands = (steps * B * (npre + 4 * rows) + launches * scalars * 4 * B * N
+    operands = (steps * B * (npre / 8 + 4 * rows) + launches * scalars * 4 * B * N
                 + (0 if rt else launches * 4 * B * npre))
-    return (2 * launches - first_launches) * trace + operands
+    return int((2 * launches - first_launches) * trace + operands)
 
 
 BYTE_MODEL = ("block: per launch (one block of up to 256 steps), every trace read once and "
               "written once (4 B x B x N_pre x (N_post + N_adaptive) each way; the first launch "
               "after a reset reads none), the fp64 gradient accumulator read and written once "
               "(8 B x N_pre x N_post each way), the operands of the block's steps read once "
-              "(B x N_pre bytes of presynaptic spikes and 4 B x B x (2 N_post + N_adaptive) of "
+              "(B x N_pre bits of presynaptic spikes and 4 B x B x (2 N_post + N_adaptive) of "
               "coefficient pairs per step, plus 7 scalars per (b, j) and the block-start filter "
               "per launch)")
 
