@@ -320,8 +320,8 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
   for (Layer& L : plan->layers) {
     const size_t ldc = plan->ldc;
     for (int sl = 0; sl < slots; ++sl) {
-      // p: one byte per row and step; coefficients: a scaled fp16 pair per
-      // value (4 bytes)
+      // p: one bit per row and step (a 16-bit word per row and 16-step
+      // chunk); coefficients: a scaled fp16 pair per value (4 bytes)
       L.pbits[sl] = (uint16_t*)take(sizeof(uint16_t) * B * L.n_pre_pad * (KM / eprop::kChunk));
       L.coefU[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
       L.coefV[sl] = (uint32_t*)take(plan->na2 > 0 ? sizeof(uint32_t) * B * ldc * KM : 0);

@@ -1475,7 +1475,10 @@ struct TraceTile {
   static constexpr int SCAL = 4 * kScalWave;
   static constexpr int ZOFF = 64;                             // filter offset in a wave's part
   static_assert(PPW * kTileJ <= ZOFF, "planes overlap the filter");
-  static constexpr size_t SMEM = sizeof(float) * (RING * SLOT + 2 * SCAL);
+  // the (p, p) expansion table after the scalar buffers: entry n (16 bytes)
+  // holds the four pair words of the 4-bit p pattern n
+  static constexpr int TBL = RING * SLOT + 2 * SCAL;           // float offset of the table
+  static constexpr size_t SMEM = sizeof(float) * (TBL + 64);
   // chunks in flight ahead; fewer than NCH so that a batch element's copies
   // never reach past the next element's first chunk
   static constexpr int D = NCH == 1 ? 1 : (NCH - 1 < PREF ? NCH - 1 : PREF);
@@ -1504,6 +1507,7 @@ struct TraceTile {
   int i0, j0, it, jt, split, lane, r, g, w;
   bool first, live, copier;
   uint32_t pvoff, cvoff;          // this lane's byte offsets in the p and coefficient copies
+  const char* opbase;             // the coefficient operand this wave copies (copier waves)
 
   __device__ __forceinline__ TraceTile(const TraceArgs& a_, float* sm_, int it_, int jt_, int split_,
                                        bool first_)
@@ -1521,6 +1525,7 @@ struct TraceTile {
     pvoff = (uint32_t)(i0 + kWaveRows * w) * 2u + (uint32_t)(lane & 7) * 16u;
     const int row = lane >> 2;
     cvoff = (uint32_t)(j0 + row) * 64u + (uint32_t)((lane & 3) ^ ((row >> 1) & 3)) * 16u;
+    opbase = (const char*)(w == 0 ? a.U : w == 1 ? a.H : w == 2 ? a.V : a.W);
   }
 
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const float* base, int n_t, int b,
@@ -1542,7 +1547,8 @@ struct TraceTile {
   // vector-memory path works while the matrix cores do; the order of all
   // copies is that of the full issue.
   template <int P>
-  __device__ __forceinline__ void issue(int b, int c, int sl, int par) const {
+  __device__ __forceinline__ void issue(int b_, int c, int sl, int par) const {
+    const int b = __builtin_amdgcn_readfirstlane(b_);   // wave-uniform: scalar address arithmetic
     char* slot = (char*)(sm + sl * SLOT);
     if constexpr (P == 0) {
       const uint32_t estride = (uint32_t)(kKC * a.ldi * 2);          // bytes of one element
@@ -1552,8 +1558,7 @@ struct TraceTile {
     } else {
       if (copier) {
         const uint32_t estride = (uint32_t)(kKC * a.ldc * 64);       // bytes of one element
-        const uint32_t* X = w == 0 ? a.U : w == 1 ? a.H : w == 2 ? a.V : a.W;
-        const auto cr = make_rsrc((const char*)X + (size_t)b * estride, estride);
+        const auto cr = make_rsrc(opbase + (size_t)b * estride, estride);
         dma16b(cr, cvoff, (uint32_t)(c * a.ldc * 64), slot + kPBytes + w * kOpBytes);
       }
       if (c == 0) {
@@ -1688,6 +1693,10 @@ struct TraceTile {
 
   __device__ __forceinline__ void run() const {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    // the expansion table (word e of entry n: pair word of bit e of n)
+    if (threadIdx.x < 64)
+      ((uint32_t*)sm)[TBL + threadIdx.x] = ((threadIdx.x >> 2) >> (threadIdx.x & 3)) & 1u ? 0x3C003C00u : 0u;
+    __syncthreads();
     const int nk = (a.B - split + a.n_split - 1) / a.n_split;
     f32x4 gacc[4], cU[4], cV[4], cH[4], cW[4], E[4], A[4], Vm[4];
 #pragma unroll
@@ -1744,22 +1753,27 @@ struct TraceTile {
         const char* slot = (const char*)(sm + (n % RING) * SLOT);
         const int sw = (r >> 1) & 3;   // unit order of this lane's row
         const f16x8 zero8 = {};
+        // the chunk's shared-memory reads in two round trips: the
+        // coefficient operands and the p words of the four row blocks, then
+        // the expansion table.  Steps 4g .. 4g+3 of row 16 bi + r of the
+        // wave: four p bits -> (p, p) fp16 pairs (1.0 = 0x3C00 in both
+        // halves of word e); the 16 rows' words are 32 consecutive bytes,
+        // read by every g alike.
         f16x8 ax[4];
 #pragma unroll
         for (int X = 0; X < 4; ++X)
           ax[X] = ((X < 2) || (X == 2 && ALIF) || (X == 3 && RT))
                       ? *(const f16x8*)(slot + kPBytes + X * kOpBytes + r * 64 + ((g ^ sw) << 4))
                       : zero8;
+        uint32_t pw[4];
+#pragma unroll
+        for (int bi = 0; bi < 4; ++bi) pw[bi] = *(const uint16_t*)(slot + (kWaveRows * w + 16 * bi + r) * 2);
+        f16x8 bzs[4];
+#pragma unroll
+        for (int bi = 0; bi < 4; ++bi) bzs[bi] = *(const f16x8*)(sm + TBL + 4 * ((pw[bi] >> (4 * g)) & 15u));
 #pragma unroll
         for (int bi = 0; bi < 4; ++bi) {
-          // steps 4g .. 4g+3 of row 16 bi + r of the wave: four p bits ->
-          // (p, p) fp16 pairs (1.0 = 0x3C00 in both halves of word e); the
-          // 16 rows' words are 32 consecutive bytes, read by every g alike
-          const uint32_t pb = (uint32_t)*(const uint16_t*)(slot + (kWaveRows * w + 16 * bi + r) * 2) >> (4 * g);
-          u32x4 w1;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) w1[e] = ((pb >> e) & 1u) ? 0x3C003C00u : 0u;
-          const f16x8 bz = __builtin_bit_cast(f16x8, w1);
+          const f16x8 bz = bzs[bi];
           cU[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[0], bz, cU[bi], 0, 0, 0);
           cH[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz, cH[bi], 0, 0, 0);
           if constexpr (ALIF)
@@ -1799,23 +1813,33 @@ struct TraceTile {
   }
 };
 
-// blockIdx.x: tile in row-major order (it, jt); blockIdx.y: batch split.  A
-// tile holding any adaptive neuron takes the path with the adaptation trace.
-// With a multiple of 8 column tiles, the row tiles of one column tile (which
-// share its coefficient chunks) land on one XCD (workgroups go round-robin
-// over the eight).  One kernel per chunk count NCH = kpad / 16 (the host picks
-// it), so that each holds only its own two variants.
+// Workgroup order: a group is one column tile jt of one batch split; its row
+// tiles (which read the same coefficient chunks of the same batch elements)
+// are consecutive workgroups of one XCD.  Workgroups go round-robin over the
+// eight XCDs, so workgroup L belongs to XCD L % 8 and is the (L / 8)-th of
+// that XCD; group G = 8 g + x is the g-th group of XCD x.  Dispatched one
+// after the other on one XCD, the row tiles of a group start together and,
+// being of one kind (a tile holding any adaptive neuron takes the path with
+// the adaptation trace), advance together, so each coefficient chunk is
+// fetched into that XCD's L2 once for all of them.  Workgroups past the last
+// group exit at once.  One kernel per chunk count NCH = kpad / 16 (the host
+// picks it), so that each holds only its own two variants.
 // Three workgroups per compute unit for the reset-stopped form (its
 // variants fit 168 registers), two with the reset path kept.
 template <bool RT, int NCH>
 __global__ __launch_bounds__(256, RT ? 2 : 3) void trace_kernel(TraceArgs a) {
   extern __shared__ __attribute__((aligned(16))) float trace_smem[];
-  const int it = blockIdx.x / a.n_jt, jt = blockIdx.x - it * a.n_jt;
+  const int n_it = a.n_pre_pad / kTileI;
+  const int L = blockIdx.x, x = L & 7, pos = L >> 3;
+  const int gl = pos / n_it, it = pos - gl * n_it;
+  const int G = gl * 8 + x;
+  if (G >= a.n_jt * a.n_split) return;
+  const int split = G / a.n_jt, jt = G - split * a.n_jt;
   const bool first = a.first != 0;
   if (jt < a.n_jt_a)
-    TraceTile<true, NCH, RT>(a, trace_smem, it, jt, blockIdx.y, first).run();
+    TraceTile<true, NCH, RT>(a, trace_smem, it, jt, split, first).run();
   else
-    TraceTile<false, NCH, RT>(a, trace_smem, it, jt, blockIdx.y, first).run();
+    TraceTile<false, NCH, RT>(a, trace_smem, it, jt, split, first).run();
 }
 // shared memory of the two variants (the same for every chunk count)
 constexpr size_t kTraceSmemOf(bool rt) {
@@ -2102,8 +2126,10 @@ hipError_t launch_trace_variant(const TraceArgs& a, hipStream_t s) {
   constexpr size_t smem = kTraceSmemOf(RT);
   hipError_t e = grant_smem<&trace_kernel<RT, NCH>>((int)smem);
   if (e != hipSuccess) return e;
-  dim3 grid((a.n_pre_pad / kTileI) * a.n_jt, a.n_split);
-  trace_kernel<RT, NCH><<<grid, 256, smem, s>>>(a);
+  // eight XCDs times the groups per XCD times the row tiles of a group
+  const long long wgs = 8ll * cdiv(a.n_jt * a.n_split, 8) * (a.n_pre_pad / kTileI);
+  if (wgs > 0x7fffffffll) return hipErrorInvalidValue;
+  trace_kernel<RT, NCH><<<dim3((unsigned)wgs), 256, smem, s>>>(a);
   return hipGetLastError();
 }
 
