@@ -70,7 +70,7 @@ struct Layer {
   // the binary presynaptic values (one byte per step), and the block
   // coefficients of the eligibility recursion as scaled fp16 pairs
   uint16_t* pbits[kSlots];
-  uint32_t *coefU[kSlots], *coefV[kSlots], *coefH[kSlots], *coefW[kSlots];
+  uint32_t* coefO[kSlots];        // the coefficient operands, tile-major (OpLayout)
   float* coefS[kSlots];
   float* zstart[kSlots];                 // presynaptic filter at each block's start [B][ldi]
   float* Cpart;
@@ -109,6 +109,7 @@ struct Plan {
   // three-trace recursion (reset path kept, or the two-compartment neuron),
   // and the neurons whose second state component has per-synapse traces
   int rt = 0, na2 = 0;
+  eprop::OpLayout ol{};             // coefficient operands, tile-major
   int slots = kSlots;               // per-block buffer sets in use
   NeuronCoef gen{};                 // two-compartment neuron: derived step
   int* err_flag = nullptr;
@@ -252,6 +253,13 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
   plan->ldk = (int)round_up(K, 32);
   plan->ldn = (int)round_up(N, 32);
   plan->ldc = (int)round_up(N, eprop::kColPad);
+  {
+    const int n_jt = (int)((N + eprop::kTileJ - 1) / eprop::kTileJ);
+    plan->ol.n_jt_a = (plan->na2 + eprop::kTileJ - 1) / eprop::kTileJ;
+    plan->ol.nxa = 3 + plan->rt;      // U, H, V (, W)
+    plan->ol.nxl = 2 + plan->rt;      // U, H (, W)
+    plan->ol.cw = 256 * (plan->ol.n_jt_a * plan->ol.nxa + (n_jt - plan->ol.n_jt_a) * plan->ol.nxl);
+  }
   const int qn = eprop::forward_qn((int)N);
   plan->jlist = qn * 64;   // a wave's neurons
   {
@@ -323,10 +331,7 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
       // p: one bit per row and step (a 16-bit word per row and 16-step
       // chunk); coefficients: a scaled fp16 pair per value (4 bytes)
       L.pbits[sl] = (uint16_t*)take(sizeof(uint16_t) * B * L.n_pre_pad * (KM / eprop::kChunk));
-      L.coefU[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
-      L.coefV[sl] = (uint32_t*)take(plan->na2 > 0 ? sizeof(uint32_t) * B * ldc * KM : 0);
-      L.coefH[sl] = (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM);
-      L.coefW[sl] = plan->rt ? (uint32_t*)take(sizeof(uint32_t) * B * ldc * KM) : nullptr;
+      L.coefO[sl] = (uint32_t*)take(sizeof(uint32_t) * B * (KM / eprop::kChunk) * plan->ol.cw);
       const int planes = plan->rt ? eprop::kScalarPlanesRT : eprop::kScalarPlanes;
       L.coefS[sl] = (float*)take(sizeof(float) * planes * B * ldc);
     }
@@ -630,13 +635,12 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
 
     eprop::CoefArgs ca;
     ca.psiK = L.psiK[sl]; ca.LK = L.LK[sl]; ca.ldv = L.ldv; ca.Bp = P.Bp;
-    ca.U = L.coefU[sl]; ca.V = P.na2 > 0 ? L.coefV[sl] : nullptr; ca.H = L.coefH[sl];
+    ca.O = L.coefO[sl]; ca.ol = P.ol;
     ca.S = L.coefS[sl];
     ca.B = c.batch; ca.n_post = c.n_rec; ca.n_adaptive = c.n_adaptive;
-    ca.n_vcols = std::min<int>(c.n_rec, (int)round_up(P.na2, eprop::kTileJ));
     ca.steps = steps; ca.kpad = kpad; ca.ldc = P.ldc;
     ca.kappa = c.kappa; ca.rho = c.rho; ca.beta = c.beta; ca.alpha = c.alpha; ca.thr = c.thr;
-    ca.W = L.coefW[sl]; ca.reset_through = P.rt;
+    ca.reset_through = P.rt;
     ca.model = c.neuron_model;
     for (int m = 0; m < 2; ++m) {
       ca.gA[m][0] = (float)P.gen.A[m][0]; ca.gA[m][1] = (float)P.gen.A[m][1];
@@ -654,8 +658,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ta.ebar = L.ebar; ta.epsa = L.epsa; ta.epsv = L.epsv; ta.acc = L.acc; ta.acc_stride = L.acc_stride;
     ta.n_split = L.n_split; ta.pbits = L.pbits[sl];
     ta.zstart = L.zstart[sl];
-    ta.U = L.coefU[sl]; ta.V = P.na2 > 0 ? L.coefV[sl] : nullptr; ta.H = L.coefH[sl];
-    ta.W = L.coefW[sl]; ta.reset_through = P.rt;
+    ta.O = L.coefO[sl]; ta.ol = P.ol; ta.reset_through = P.rt;
     ta.S = L.coefS[sl];
     ta.B = c.batch; ta.n_pre = L.n_pre; ta.n_pre_pad = L.n_pre_pad; ta.n_post = c.n_rec; ta.ldj = L.ldj;
     ta.n_adaptive = P.na2; ta.ldi = L.n_pre_pad;

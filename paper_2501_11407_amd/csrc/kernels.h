@@ -128,15 +128,31 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 // pairs: a value x (times a power-of-two scale 2^e) is hi = fp16(x 2^e) plus
 // lo = fp16(x 2^e - hi), together about 22 significant bits, in one 32-bit
 // word (hi in the low half).  Per 16-step chunk and row, 16 words (64 bytes).
-// The presynaptic operand is binary (bytes, expanded to fp16 in the kernel).
+// The presynaptic operand is binary (bits, expanded to fp16 in the kernel).
 constexpr int kChunk = 16;                     // steps per chunk
 constexpr int kKC = kBlockSteps / kChunk;      // chunks per block
 constexpr int kScalarPlanes = 8;               // see coef_kernel
 
+// Coefficient operands, tile-major: per batch element and chunk, the column
+// tiles of kTileJ columns in order, and per tile its operands one after the
+// other (U, H, then V in tiles holding adaptive neurons, then W with the
+// reset path kept), each 16 rows (the tile's columns) of 16 pair words (the
+// chunk's steps), 1 KiB.  The tiles holding adaptive neurons come first.
+// One eligibility workgroup's operands of a chunk are one contiguous run.
+struct OpLayout {
+  int n_jt_a;        // tiles holding adaptive neurons
+  int nxa, nxl;      // operands per tile with and without adaptive neurons
+  int cw;            // words per chunk: 256 (n_jt_a nxa + (n_jt - n_jt_a) nxl)
+  // first word of tile jt within a chunk
+  __host__ __device__ int tile(int jt) const {
+    return 256 * (jt < n_jt_a ? jt * nxa : n_jt_a * nxa + (jt - n_jt_a) * nxl);
+  }
+};
+
 // Block coefficients of the eligibility recursion, one thread per (b, j):
 // U', V', H' (against the binary presynaptic vector) as scaled fp16 pair
-// words [B][kKC][ldc][16] (zero for steps <= s < kpad; V' written for j <
-// n_vcols only, NULL when no neuron adapts), each row with its own
+// words in O [B][kKC][ol.cw] (OpLayout; zero for steps <= s < kpad; V' in
+// the tiles holding adaptive neurons only), each row with its own
 // power-of-two scale, and S [kScalarPlanes][B][ldc] (see coef_kernel).  With
 // reset_through the rows are those of the
 // recursion with the reset path kept (U = C_E, H = C_g, V = C_A, and W = C_V
@@ -144,8 +160,8 @@ constexpr int kScalarPlanes = 8;               // see coef_kernel
 constexpr int kScalarPlanesRT = 16;
 struct CoefArgs {
   const float* psiK; const float* LK; int ldv, Bp;   // [t*Bp + b][ldv]
-  uint32_t* U; uint32_t* V; uint32_t* H; uint32_t* W; float* S;
-  int B, n_post, n_adaptive, n_vcols, steps, kpad, ldc;
+  uint32_t* O; OpLayout ol; float* S;
+  int B, n_post, n_adaptive, steps, kpad, ldc;
   float kappa, rho, beta, alpha, thr;
   int reset_through;
   // model 1: the generic adjoint pass (coef_gen_kernel) of a step with
@@ -169,7 +185,7 @@ struct TraceArgs {
   size_t acc_stride;
   const uint16_t* pbits;              // [B][kKC][ldi], ldi = n_pre_pad
   const float* zstart;                // [B][ldi] (reset-stopped form only)
-  const uint32_t* U; const uint32_t* V; const uint32_t* H; const uint32_t* W;
+  const uint32_t* O; OpLayout ol;     // as CoefArgs
   const float* S;                     // as CoefArgs
   int B, n_pre, n_pre_pad, n_post, ldj, n_adaptive, ldi, ldc, kpad, n_split;
   int n_jt, n_jt_a;   // tiles along j: all, and those holding adaptive neurons

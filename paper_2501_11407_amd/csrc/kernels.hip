@@ -1166,7 +1166,8 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
   const int b = blockIdx.y;
   if (j >= a.n_post) return;
   const float bt = (j < a.n_adaptive) ? a.beta : 0.0f;
-  const bool wv = a.V != nullptr && j < a.n_vcols;
+  const int jt = j / kTileJ;
+  const bool wv = jt < a.ol.n_jt_a;   // a tile holding adaptive neurons: V' too
   const float* __restrict__ psiK = a.psiK;
   const float* __restrict__ LK = a.LK;
   auto load_chunk = [&](int c, float (&ps)[kChunk], float (&L)[kChunk]) {
@@ -1202,8 +1203,8 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
   }
   const int eU = pair_exponent(mU), eH = pair_exponent(mH), eV = pair_exponent(mV);
   const float sU = ldexpf(1.0f, eU), sH = ldexpf(1.0f, eH), sV = ldexpf(1.0f, eV);
-  const size_t rs = (size_t)a.ldc * kChunk;         // words between chunks
-  const size_t o = ((size_t)b * kKC * a.ldc + j) * kChunk;
+  const size_t rs = (size_t)a.ol.cw;                // words between chunks
+  uint32_t* o = a.O + (size_t)b * kKC * a.ol.cw + a.ol.tile(jt) + (j % kTileJ) * kChunk;
   CoefState st;
   for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
     float ps[kChunk], L[kChunk];
@@ -1218,9 +1219,10 @@ __global__ __launch_bounds__(256) void coef_kernel(CoefArgs a) {
       }
       st.step(a, s, ps[e], L[e], bt, u[e], h[e], v[e]);
     }
-    store_pairs(a.U + o + c * rs, u, sU);
-    store_pairs(a.H + o + c * rs, h, sH);
-    if (wv) store_pairs(a.V + o + c * rs, v, sV);
+    // the tile's operands U, H (, V) one after the other, 1 KiB each
+    store_pairs(o + c * rs, u, sU);
+    store_pairs(o + c * rs + 256, h, sH);
+    if (wv) store_pairs(o + c * rs + 512, v, sV);
   }
   const size_t so = (size_t)b * a.ldc + j, plane = (size_t)a.B * a.ldc;
   const uint32_t ex = (uint32_t)(eU + 128) | ((uint32_t)(eH + 128) << 8) | ((uint32_t)(eV + 128) << 16);
@@ -1293,7 +1295,8 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
   const int b = blockIdx.y;
   if (j >= a.n_post) return;
   const float bt = (j < a.n_adaptive) ? a.beta : 0.0f;
-  const bool wv = a.V != nullptr && j < a.n_vcols;
+  const int jt = j / kTileJ;
+  const bool wv = jt < a.ol.n_jt_a;   // a tile holding adaptive neurons: V' too
   const float* __restrict__ psiK = a.psiK;
   const float* __restrict__ LK = a.LK;
   auto load_chunk = [&](int c, float (&ps)[kChunk], float (&L)[kChunk]) {
@@ -1340,8 +1343,8 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
   float sc[4];
 #pragma unroll
   for (int o = 0; o < 4; ++o) sc[o] = ldexpf(1.0f, pair_exponent(mx[o]));
-  const size_t rs = (size_t)a.ldc * kChunk;         // words between chunks
-  const size_t off = ((size_t)b * kKC * a.ldc + j) * kChunk;
+  const size_t rs = (size_t)a.ol.cw;                // words between chunks
+  uint32_t* o = a.O + (size_t)b * kKC * a.ol.cw + a.ol.tile(jt) + (j % kTileJ) * kChunk;
   Adj y[4];
   init(y);
   for (int c = a.kpad / kChunk - 1; c >= 0; --c) {
@@ -1357,10 +1360,11 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
         x[o][e] = live ? y[o].coef(a) : 0.0f;
       }
     }
-    store_pairs(a.U + off + c * rs, x[0], sc[0]);
-    store_pairs(a.H + off + c * rs, x[1], sc[1]);
-    if (wv) store_pairs(a.V + off + c * rs, x[2], sc[2]);
-    store_pairs(a.W + off + c * rs, x[3], sc[3]);
+    // the tile's operands U, H (, V), W one after the other, 1 KiB each
+    store_pairs(o + c * rs, x[0], sc[0]);
+    store_pairs(o + c * rs + 256, x[1], sc[1]);
+    if (wv) store_pairs(o + c * rs + 512, x[2], sc[2]);
+    store_pairs(o + c * rs + (wv ? 768 : 512), x[3], sc[3]);
   }
   const size_t so = (size_t)b * a.ldc + j, plane = (size_t)a.B * a.ldc;
   const float s16[13] = {y[1].e, y[1].a, y[1].v, y[0].a, y[0].v, y[2].a, y[2].v, y[3].a, y[3].v,
@@ -1419,7 +1423,7 @@ __device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, uint32_t off, f
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, kNonTemporal);
 }
 
-constexpr int kRing = 4;                              // chunk slots
+constexpr int kRing = 4;                              // slots of two chunks
 constexpr int kOpBytes = kTileJ * 64;                 // one coefficient operand of a chunk: 16 rows x 64 B
 constexpr int kPBytes = kTileI * 2;                   // the chunk's p bits: 256 rows x 16 bits
 constexpr int kWaveRows = kTileI / 4;                 // rows of a wave sub-tile
@@ -1461,13 +1465,19 @@ __device__ __forceinline__ void dma16b(__amdgpu_buffer_rsrc_t r, uint32_t voff, 
 // takes one MFMA pass.
 template <bool ALIF, int NCH, bool RT>
 struct TraceTile {
-  static constexpr int RING = kRing;                          // chunk slots
-  static constexpr int PREF = RING - 1;                       // chunks copied ahead
-  // a slot: the chunk's p records (256 rows x 16 B), then the coefficient
-  // operands U, H, V (and W) of 16 rows x 64 B each (V's place is kept in
-  // tiles without adaptive neurons)
+  // The chunks of a batch element are taken two at a time ("pairs", 32
+  // steps; the last pair of an odd chunk count holds one): one wait, one
+  // barrier and one batch of shared-memory reads per pair.
+  static constexpr int NS = (NCH + 1) / 2;                    // pairs per batch element
+  static constexpr int in_pair(int s) { return 2 * s + 1 < NCH ? 2 : 1; }   // chunks of pair s
+  static constexpr int RING = kRing;                          // pair slots
+  static constexpr int PREF = RING - 1;                       // pairs copied ahead
+  // half a slot: a chunk's p bits (256 rows x 16 bits), then the
+  // coefficient operands U, H, V (and W) of 16 rows x 64 B each (V's place is
+  // kept in tiles without adaptive neurons)
   static constexpr int NOPS = RT ? 4 : 3;
-  static constexpr int SLOT = (kPBytes + NOPS * kOpBytes) / 4;   // floats per slot
+  static constexpr int HSLOT = kPBytes + NOPS * kOpBytes;     // bytes per chunk
+  static constexpr int SLOT = 2 * HSLOT / 4;                  // floats per slot
   static constexpr int PLANES = RT ? kScalarPlanesRT : kScalarPlanes;
   static constexpr int PPW = PLANES / 4;                      // planes copied per wave
   // one scalar buffer: per wave kScalWave floats = its PPW planes of the 16
@@ -1475,29 +1485,34 @@ struct TraceTile {
   static constexpr int SCAL = 4 * kScalWave;
   static constexpr int ZOFF = 64;                             // filter offset in a wave's part
   static_assert(PPW * kTileJ <= ZOFF, "planes overlap the filter");
-  // the (p, p) expansion table after the scalar buffers: entry n (16 bytes)
-  // holds the four pair words of the 4-bit p pattern n
-  static constexpr int TBL = RING * SLOT + 2 * SCAL;           // float offset of the table
-  static constexpr size_t SMEM = sizeof(float) * (TBL + 64);
-  // chunks in flight ahead; fewer than NCH so that a batch element's copies
-  // never reach past the next element's first chunk
-  static constexpr int D = NCH == 1 ? 1 : (NCH - 1 < PREF ? NCH - 1 : PREF);
+  static constexpr size_t SMEM = sizeof(float) * (RING * SLOT + 2 * SCAL);
+  // pairs in flight ahead; fewer than NS so that a batch element's copies
+  // never reach past the next element's first pair
+  static constexpr int D = NS == 1 ? 1 : (NS - 1 < PREF ? NS - 1 : PREF);
   // Copies per wave per chunk: its p rows, and one coefficient operand for
   // the copying waves (wave X copies operand X: U, H, and V / W when present).
-  static constexpr bool has_op(int X) { return X < 2 || (X == 2 && ALIF) || (X == 3 && RT); }
   static constexpr int SC = 1;                                  // scalar copies per wave
   static constexpr int EA = 4 * (1 + (ALIF ? 1 : 0) + (RT ? 1 : 0));   // trace loads per element
-  static constexpr int ops(int c, bool cp) { return 1 + (cp ? 1 : 0) + (c == 0 ? SC : 0); }
-  // Loads issued after those of chunk ch when it is waited for: the copies
-  // of chunks ch+1 .. ch+D-1 (past the end of the batch element: the next
+  static constexpr int ops(int s, bool cp) { return in_pair(s) * (1 + (cp ? 1 : 0)) + (s == 0 ? SC : 0); }
+  // The block-start traces are loaded one 16 x 16 block bi of each trace per
+  // pair over the element's first four pairs (all at pair 0 with fewer
+  // pairs), after that pair's copies: spread out, the loads of a batch element
+  // do not arrive at the memory system at once, and the copies issued after
+  // them (which complete in order behind them) are not held up by a burst.
+  static constexpr int NT = EA / 4;                              // traces per element
+  static constexpr bool spread = NS >= 4;
+  static constexpr int tl(int s) { return spread ? (s < 4 ? NT : 0) : (s == 0 ? EA : 0); }
+  // Loads issued after those of pair s when it is waited for: the copies of
+  // pairs s+1 .. s+D-1 (past the end of the batch element: the next
   // element's, if there is one), and the element's trace loads when they
-  // were issued in between (at chunk 0, after that chunk's copies).  Loads
+  // were issued in between (at pair 0, after that pair's copies).  Loads
   // complete in order, so at most that many outstanding operations means
-  // chunk ch has landed, whatever stores are still in flight.
-  static constexpr int pending(int ch, bool next, bool cp) {
-    int n = (ch >= 1 && ch <= D) ? EA : 0;
-    for (int m = ch + 1; m <= ch + D - 1; ++m)
-      n += m < NCH ? ops(m, cp) : (next ? ops(m - NCH, cp) : 0);
+  // pair s has landed, whatever stores are still in flight.
+  static constexpr int pending(int ps, bool next, bool cp) {
+    int n = 0;
+    for (int i = ps - D; i < ps; ++i) n += i >= 0 ? tl(i) : 0;
+    for (int m = ps + 1; m <= ps + D - 1; ++m)
+      n += m < NS ? ops(m, cp) : (next ? ops(m - NS, cp) : 0);
     return n;
   }
   static_assert(pending(1, true, true) <= 63, "vmcnt range");
@@ -1524,8 +1539,9 @@ struct TraceTile {
     // (l % 4) ^ ((row / 2) % 4) (see issue)
     pvoff = (uint32_t)(i0 + kWaveRows * w) * 2u + (uint32_t)(lane & 7) * 16u;
     const int row = lane >> 2;
-    cvoff = (uint32_t)(j0 + row) * 64u + (uint32_t)((lane & 3) ^ ((row >> 1) & 3)) * 16u;
-    opbase = (const char*)(w == 0 ? a.U : w == 1 ? a.H : w == 2 ? a.V : a.W);
+    cvoff = (uint32_t)row * 64u + (uint32_t)((lane & 3) ^ ((row >> 1) & 3)) * 16u;
+    // operand w of the tile (U, H, V, W; W follows H where the tile has no V)
+    opbase = (const char*)(a.O + a.ol.tile(jt_)) + (w == 3 && !ALIF ? 2 : w) * kOpBytes;
   }
 
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const float* base, int n_t, int b,
@@ -1546,20 +1562,31 @@ struct TraceTile {
   // coefficient operand and the scalars), placed between MFMAs so that the
   // vector-memory path works while the matrix cores do; the order of all
   // copies is that of the full issue.
-  template <int P>
+  template <int P, int NC>
   __device__ __forceinline__ void issue(int b_, int c, int sl, int par) const {
     const int b = __builtin_amdgcn_readfirstlane(b_);   // wave-uniform: scalar address arithmetic
     char* slot = (char*)(sm + sl * SLOT);
     if constexpr (P == 0) {
       const uint32_t estride = (uint32_t)(kKC * a.ldi * 2);          // bytes of one element
       const auto pr = make_rsrc((const char*)a.pbits + (size_t)b * estride, estride);
-      // the wave's 64 rows: 128 bytes, lanes 0-7 (one instruction per wave)
-      if (lane < 8) dma16b(pr, pvoff, (uint32_t)(c * a.ldi * 2), slot + kWaveRows * w * 2);
+      // the chunk offsets computed here (kept out of scalar registers
+      // across the loop)
+      uint32_t cs = (uint32_t)(a.ldi * 2);
+      asm volatile("" : "+s"(cs));
+      // the wave's 64 rows: 128 bytes, lanes 0-7 (one instruction per wave
+      // and chunk)
+#pragma unroll
+      for (int h = 0; h < NC; ++h)
+        if (lane < 8) dma16b(pr, pvoff, (uint32_t)(c + h) * cs, slot + h * HSLOT + kWaveRows * w * 2);
     } else {
       if (copier) {
-        const uint32_t estride = (uint32_t)(kKC * a.ldc * 64);       // bytes of one element
+        const uint32_t estride = (uint32_t)(kKC * a.ol.cw * 4);      // bytes of one element
         const auto cr = make_rsrc(opbase + (size_t)b * estride, estride);
-        dma16b(cr, cvoff, (uint32_t)(c * a.ldc * 64), slot + kPBytes + w * kOpBytes);
+        uint32_t cs = (uint32_t)(a.ol.cw * 4);
+        asm volatile("" : "+s"(cs));
+#pragma unroll
+        for (int h = 0; h < NC; ++h)
+          dma16b(cr, cvoff, (uint32_t)(c + h) * cs, slot + h * HSLOT + kPBytes + w * kOpBytes);
       }
       if (c == 0) {
         float* sb = sm + RING * SLOT + par * SCAL + w * kScalWave;
@@ -1575,29 +1602,36 @@ struct TraceTile {
       }
     }
   }
-  __device__ __forceinline__ void issue_all(int b, int c, int sl, int par) const {
-    issue<0>(b, c, sl, par);
-    issue<1>(b, c, sl, par);
+  // all copies of pair PS (chunks 2 PS and 2 PS + 1 when there is one)
+  template <int PS>
+  __device__ __forceinline__ void issue_all(int b, std::integral_constant<int, PS>, int sl, int par) const {
+    issue<0, in_pair(PS)>(b, 2 * PS, sl, par);
+    issue<1, in_pair(PS)>(b, 2 * PS, sl, par);
   }
 
   // block-start traces of batch element b into E, A (and Vm).  In the first
   // block after a reset (and for a wave of padding rows) they are zero: the
   // loads then get an empty range, so they read zero without touching memory
   // and still count as issued loads (the waits above count them).
-  __device__ __forceinline__ void load_traces(int b, f32x4 (&E)[4], f32x4 (&A)[4], f32x4 (&Vm)[4]) const {
+  // blocks x0 .. x1 - 1 of each
+  __device__ __forceinline__ void load_traces(int b, int x0, int x1, f32x4 (&E)[4], f32x4 (&A)[4],
+                                              f32x4 (&Vm)[4]) const {
     const uint32_t range = first ? 0u : kSubTileBytes;
     const auto eR = tile_rsrc(a.ebar, a.n_jt, b, range);
 #pragma unroll
-    for (int x = 0; x < 4; ++x) E[x] = bload(eR, x * 1024u + lane * 16u);
+    for (int x = 0; x < 4; ++x)
+      if (x >= x0 && x < x1) E[x] = bload(eR, x * 1024u + lane * 16u);
     if constexpr (ALIF) {
       const auto aR = tile_rsrc(a.epsa, a.n_jt_a, b, range);
 #pragma unroll
-      for (int x = 0; x < 4; ++x) A[x] = bload(aR, x * 1024u + lane * 16u);
+      for (int x = 0; x < 4; ++x)
+        if (x >= x0 && x < x1) A[x] = bload(aR, x * 1024u + lane * 16u);
     }
     if constexpr (RT) {
       const auto vR = tile_rsrc(a.epsv, a.n_jt, b, range);
 #pragma unroll
-      for (int x = 0; x < 4; ++x) Vm[x] = bload(vR, x * 1024u + lane * 16u);
+      for (int x = 0; x < 4; ++x)
+        if (x >= x0 && x < x1) Vm[x] = bload(vR, x * 1024u + lane * 16u);
     }
   }
 
@@ -1693,10 +1727,6 @@ struct TraceTile {
 
   __device__ __forceinline__ void run() const {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-    // the expansion table (word e of entry n: pair word of bit e of n)
-    if (threadIdx.x < 64)
-      ((uint32_t*)sm)[TBL + threadIdx.x] = ((threadIdx.x >> 2) >> (threadIdx.x & 3)) & 1u ? 0x3C003C00u : 0u;
-    __syncthreads();
     const int nk = (a.B - split + a.n_split - 1) / a.n_split;
     f32x4 gacc[4], cU[4], cV[4], cH[4], cW[4], E[4], A[4], Vm[4];
 #pragma unroll
@@ -1705,98 +1735,108 @@ struct TraceTile {
       cU[x] = cV[x] = cH[x] = cW[x] = zero;
       E[x] = A[x] = Vm[x] = zero;
     }
-#pragma unroll
-    for (int c = 0; c < D; ++c) issue_all(split, c, c, 0);
+    for_each_index([&](auto pc) { issue_all(split, pc, decltype(pc)::value, 0); },
+                   std::make_integer_sequence<int, D>{});
 #pragma nounroll
     for (int k = 0; k < nk; ++k) {
       const int b = split + k * a.n_split;
       const bool next = k + 1 < nk;
-      auto chunk = [&](auto chc) {
-        constexpr int ch = decltype(chc)::value;
-        const int n = k * NCH + ch;
+      auto pair = [&](auto psc) {
+        constexpr int ps = decltype(psc)::value;
+        constexpr int NC = in_pair(ps);
+        const int n = k * NS + ps;
         if (copier) {
           if (next)
-            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, true, true)));
+            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ps, true, true)));
           else
-            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, false, true)));
+            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ps, false, true)));
         } else {
           if (next)
-            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, true, false)));
+            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ps, true, false)));
           else
-            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ch, false, false)));
+            __builtin_amdgcn_s_waitcnt(vm_wait(pending(ps, false, false)));
         }
-        wg_barrier();   // chunk n is in shared memory; slot (n - 1) % RING is free
-        if constexpr (ch == 0) {
-          // element k-1 is finished now: its stores overlap this chunk's MFMAs
-          if (k > 0) finish(k - 1, E, A, Vm, cU, cV, cH, cW, gacc);
-#pragma unroll
-          for (int x = 0; x < 4; ++x) cU[x] = cV[x] = cH[x] = cW[x] = zero;
-          // with D == NCH the next copies overwrite what finish() just read
-          if constexpr (D == NCH) wg_barrier();
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        // copies of chunk n + D (part P), placed inside the MFMA section
-        constexpr int c2 = ch + D;
+        wg_barrier();   // pair n is in shared memory; slot (n - 1) % RING is free
+        // copies of pair n + D (part P), placed inside the MFMA section
+        constexpr int s2 = ps + D;
         auto issue_next = [&](auto pc) {
           constexpr int P = decltype(pc)::value;
-          if constexpr (c2 < NCH)
-            issue<P>(b, c2, (n + D) % RING, k & 1);
+          if constexpr (s2 < NS)
+            issue<P, in_pair(s2 < NS ? s2 : 0)>(b, 2 * s2, (n + D) % RING, k & 1);
           else if (next)
-            issue<P>(b + a.n_split, c2 - NCH, (n + D) % RING, (k + 1) & 1);
+            issue<P, in_pair(s2 - NS >= 0 ? s2 - NS : 0)>(b + a.n_split, 2 * (s2 - NS), (n + D) % RING,
+                                                          (k + 1) & 1);
         };
 
-        // Per output block and contraction X, one fp16 MFMA (K = 32) over the
-        // chunk's 16 steps.  Lane g holds steps 4g..4g+3 as (hi, lo) pairs of
-        // k slots: A = X's words as they are (row r of the 16 columns, the
+        // Per output block and contraction X, one fp16 MFMA (K = 32) per
+        // chunk of 16 steps.  Lane g holds steps 4g..4g+3 as (hi, lo) pairs
+        // of k slots: A = X's words as they are (row r of the 16 columns, the
         // same for every wave); B = (p, p) per step, which sums X_hi p +
         // X_lo p (p is the binary presynaptic value, exact in fp16).
         const char* slot = (const char*)(sm + (n % RING) * SLOT);
         const int sw = (r >> 1) & 3;   // unit order of this lane's row
         const f16x8 zero8 = {};
-        // the chunk's shared-memory reads in two round trips: the
-        // coefficient operands and the p words of the four row blocks, then
-        // the expansion table.  Steps 4g .. 4g+3 of row 16 bi + r of the
-        // wave: four p bits -> (p, p) fp16 pairs (1.0 = 0x3C00 in both
-        // halves of word e); the 16 rows' words are 32 consecutive bytes,
-        // read by every g alike.
-        f16x8 ax[4];
+        // the pair's shared-memory reads in one batch: the coefficient
+        // operands and the p words of the four row blocks of both chunks
+        f16x8 ax[2][4];
+        uint32_t pw[2][4];
 #pragma unroll
-        for (int X = 0; X < 4; ++X)
-          ax[X] = ((X < 2) || (X == 2 && ALIF) || (X == 3 && RT))
-                      ? *(const f16x8*)(slot + kPBytes + X * kOpBytes + r * 64 + ((g ^ sw) << 4))
-                      : zero8;
-        uint32_t pw[4];
+        for (int h = 0; h < NC; ++h) {
 #pragma unroll
-        for (int bi = 0; bi < 4; ++bi) pw[bi] = *(const uint16_t*)(slot + (kWaveRows * w + 16 * bi + r) * 2);
-        f16x8 bzs[4];
+          for (int X = 0; X < 4; ++X)
+            ax[h][X] = ((X < 2) || (X == 2 && ALIF) || (X == 3 && RT))
+                           ? *(const f16x8*)(slot + h * HSLOT + kPBytes + X * kOpBytes + r * 64 + ((g ^ sw) << 4))
+                           : zero8;
 #pragma unroll
-        for (int bi = 0; bi < 4; ++bi) bzs[bi] = *(const f16x8*)(sm + TBL + 4 * ((pw[bi] >> (4 * g)) & 15u));
+          for (int bi = 0; bi < 4; ++bi)
+            pw[h][bi] = *(const uint16_t*)(slot + h * HSLOT + (kWaveRows * w + 16 * bi + r) * 2);
+        }
 #pragma unroll
-        for (int bi = 0; bi < 4; ++bi) {
-          const f16x8 bz = bzs[bi];
-          cU[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[0], bz, cU[bi], 0, 0, 0);
-          cH[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz, cH[bi], 0, 0, 0);
-          if constexpr (ALIF)
-            cV[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[2], bz, cV[bi], 0, 0, 0);
-          if constexpr (RT)
-            cW[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[3], bz, cW[bi], 0, 0, 0);
-          if (bi == 1) {
-            __builtin_amdgcn_sched_barrier(0);
-            issue_next(std::integral_constant<int, 0>{});
-            __builtin_amdgcn_sched_barrier(0);
-          } else if (bi == 3) {
-            __builtin_amdgcn_sched_barrier(0);
-            issue_next(std::integral_constant<int, 1>{});
-            // the element's block-start traces, after chunk 0's copies
-            if constexpr (ch == 0) load_traces(b, E, A, Vm);
-            __builtin_amdgcn_sched_barrier(0);
+        for (int h = 0; h < NC; ++h) {
+#pragma unroll
+          for (int bi = 0; bi < 4; ++bi) {
+            // steps 4g .. 4g+3 of row 16 bi + r of the wave: four p bits ->
+            // (p, p) fp16 pairs (1.0 = 0x3C00 in both halves of word e); the
+            // 16 rows' words are 32 consecutive bytes, read by every g alike
+            const uint32_t pb = pw[h][bi] >> (4 * g);
+            u32x4 w1;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w1[e] = ((pb >> e) & 1u) ? 0x3C003C00u : 0u;
+            const f16x8 bz = __builtin_bit_cast(f16x8, w1);
+            cU[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][0], bz, cU[bi], 0, 0, 0);
+            cH[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][1], bz, cH[bi], 0, 0, 0);
+            if constexpr (ALIF)
+              cV[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][2], bz, cV[bi], 0, 0, 0);
+            if constexpr (RT)
+              cW[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][3], bz, cW[bi], 0, 0, 0);
+            if (h == 0 && bi == 1) {
+              __builtin_amdgcn_sched_barrier(0);
+              issue_next(std::integral_constant<int, 0>{});
+              __builtin_amdgcn_sched_barrier(0);
+            } else if (h == 0 && bi == 3) {
+              __builtin_amdgcn_sched_barrier(0);
+              issue_next(std::integral_constant<int, 1>{});
+              // the element's block-start traces, after pair 0's copies
+              if constexpr (spread && ps < 4)
+                load_traces(b, ps, ps + 1, E, A, Vm);
+              else if constexpr (!spread && ps == 0)
+                load_traces(b, 0, 4, E, A, Vm);
+              __builtin_amdgcn_sched_barrier(0);
+            }
           }
         }
       };
-      for_each_index(chunk, std::make_integer_sequence<int, NCH>{});
+      for_each_index(pair, std::make_integer_sequence<int, NS>{});
+      // The element's traces and gradient.  Its block-start traces were
+      // loaded in this iteration (at pair 0), so the compiler's wait for them
+      // counts only the loads issued since (no drain of the copies in flight
+      // ahead); its scalars arrived with pair 0.  The scalar buffer of this
+      // element's parity is next written with the copies of element k + 2's
+      // first pair, after at least one more barrier.
+      finish(k, E, A, Vm, cU, cV, cH, cW, gacc);
+#pragma unroll
+      for (int x = 0; x < 4; ++x) cU[x] = cV[x] = cH[x] = cW[x] = zero;
     }
-    __builtin_amdgcn_s_waitcnt(vm_wait(0));   // the last element's traces
-    finish(nk - 1, E, A, Vm, cU, cV, cH, cW, gacc);
     // the split's fp64 accumulator (row-major [n_pre_pad][ldj]); rows past
     // n_pre and columns past n_post are not written
     const int jb = j0 + 4 * g;
