@@ -281,7 +281,9 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
     fwd_rows += (size_t)(l == 0 ? L.n_pre - L.n_inl : L.n_pre);
     const size_t np = L.n_pre, npp = L.n_pre_pad;
     L.Wt = (float*)take(sizeof(float) * np * L.ldw);
-    L.W16 = (int16_t*)take(sizeof(int16_t) * np * L.ldw);
+    // one more row, of zeros: the forward's drive loads of a batch's entries
+    // past the active list read it
+    L.W16 = (int16_t*)take(sizeof(int16_t) * (np + 1) * L.ldw);
     L.WoutT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.FbT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.v = (float*)take(sizeof(float) * B * N);
@@ -426,6 +428,9 @@ int pack_weights(eprop_ctx* ctx) {
     int rc16 = check(ctx, eprop::launch_pack16(L.W_src, c.n_rec, L.n_pre, L.W16,
                                                eprop::forward_qn(c.n_rec), ctx->plan.w16ok,
                                                ctx->stream), "weight packing");
+    if (rc16) return rc16;
+    rc16 = check(ctx, eprop::launch_zero((unsigned char*)(L.W16 + (size_t)L.n_pre * L.ldw),
+                                         sizeof(int16_t) * L.ldw, ctx->stream), "weight packing");
     if (rc16) return rc16;
     // drive weights transposed, Wt[i][j] = W[j][i], columns padded to the
     // forward workgroup size

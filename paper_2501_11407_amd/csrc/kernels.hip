@@ -247,6 +247,12 @@ __device__ __forceinline__ int wave_list_from_bytes(const FwdArgs& A, const FwdL
   return n;
 }
 
+// A buffer resource over [base, base + bytes): loads past the range read
+// zero and stores past it write nothing.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+
 // SOFTWIN: the softmax runs while the drive's loads are in flight (else at
 // the step's start, which needs fewer registers at the loads).  SVC: the
 // input drive comes from the shared-memory ring the service wave fills
@@ -385,23 +391,29 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     int isum[QN];
 #pragma unroll
     for (int q = 0; q < QN; ++q) isum[q] = 0;
+    // A batch's entries past the list get row n_pre, a row of zeros after
+    // the layer's rows, so every load and every add is unconditional (no
+    // branch per row) and the integer sum is unchanged.  Each load is the
+    // row base plus a 32-bit per-lane offset.
+    const char* w16 = (const char*)Ly.W16;
+    const uint32_t voff = (uint32_t)tid * (QN * 2);
     for (int k0 = 0; k0 < total; k0 += UB16) {
-      const int ent = list_entry(min(k0 + (lane & (UB16 - 1)), total - 1));
-      const int nb = min(UB16, total - k0);   // rows of this batch (wave-uniform)
+      const int e = k0 + (lane & (UB16 - 1));
+      const int le = list_entry(min(e, total - 1));
+      const int ent = e < total ? le : Ly.n_pre;
       i16v wk[UB16];
 #pragma unroll
       for (int u = 0; u < UB16; ++u) {
-        const int i = __builtin_amdgcn_readlane(ent, u);
-        if (u < nb) wk[u] = *(const i16v*)(Ly.W16 + (size_t)i * (QN * kFwdThreads) + (size_t)tid * QN);
+        const uint32_t i = (uint32_t)__builtin_amdgcn_readlane(ent, u);
+        wk[u] = *(const i16v*)(w16 + (voff + i * (uint32_t)(QN * kFwdThreads * 2)));
       }
       __builtin_amdgcn_sched_barrier(0);
       filter_rows();
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < UB16; ++u)
-        if (k0 + u < total)
 #pragma unroll
-          for (int q = 0; q < QN; ++q) isum[q] += (int)wk[u][q];
+        for (int q = 0; q < QN; ++q) isum[q] += (int)wk[u][q];
     }
 #pragma unroll
     for (int q = 0; q < QN; ++q) I[q] = I[q] + (float)isum[q] * 0x1p-14f;
@@ -1412,9 +1424,6 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
 // streams use the non-temporal cache policy (bit 1 of the policy operand):
 // each trace is touched once per block, and keeping it out of the caches
 // leaves room for the operand tiles that neighbouring workgroups reuse.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
-}
 constexpr int kNonTemporal = 2;
 __device__ __forceinline__ f32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal));
