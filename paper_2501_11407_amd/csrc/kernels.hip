@@ -283,11 +283,13 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   float* part = S.part + (LI * 2 + pc) * kFwdWaves * A.K_out;
   // K_out <= 64: the readout of a step's spikes is loaded together with the
   // next step's drive (its partial sums go to part of that step's parity),
-  // and the last wave takes the softmax of the step two back and stores
-  // delta with this step's stores; the block's last two steps are finished
-  // after the step loop
+  // and the softmax of the step two back is taken during this step, by the
+  // service wave where there is one (SVC), else by the last wave, which
+  // stores delta with this step's stores; the block's last two steps are
+  // finished after the step loop
   const bool defer = A.K_out <= kWave;
-  if (!SOFTWIN && defer && w == kSoftWave && t > 1) dk = softmax_lanes(A, part, yk, label, loss);
+  constexpr bool SOFTHERE = !SVC;   // this wave group takes the deferred softmax
+  if (SOFTHERE && !SOFTWIN && defer && w == kSoftWave && t > 1) dk = softmax_lanes(A, part, yk, label, loss);
 
   // 1. the active rows: segments of spike lists (LDS int offsets), each with
   // the row index of its neuron 0
@@ -340,7 +342,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   auto filter_rows = [&]() {
     if (filtered) return;
     filtered = true;
-    if (SOFTWIN && defer && w == kSoftWave && t > 1) dk = softmax_lanes(A, part, yk, label, loss);
+    if (SOFTHERE && SOFTWIN && defer && w == kSoftWave && t > 1) dk = softmax_lanes(A, part, yk, label, loss);
     if constexpr (LI == 0 && !SVC) {
       if (t + 1 < A.steps) {
         typedef float fqv __attribute__((ext_vector_type(QN)));
@@ -545,7 +547,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
       if (lane == 1 && w0 + 1 < A.W32) __builtin_nontemporal_store((uint32_t)(smask[q] >> 32), srow + w0 + 1);
     }
   }
-  if (defer && w == kSoftWave && t > 1 && lane < A.K_out)
+  if (SOFTHERE && defer && w == kSoftWave && t > 1 && lane < A.K_out)
     __builtin_nontemporal_store(dk, Ly.deltaK + (row - 2 * A.Bp) * A.ldk + lane);
   // the p bits of a chunk go out at its last step (or the block's), one
   // 16-bit word per row, and the row's bits start over (bits past the
@@ -665,15 +667,49 @@ __device__ __forceinline__ void forward_service_wave(const FwdArgs& A, const Fwd
     put(tt);
   }
   if (A.steps > 2) load(2);
+  // K_out <= 64: the deferred softmax (lane k: class k), off the compute
+  // waves' path: during step t, that of step t - 2 of every layer (its
+  // partial sums are complete since the end of step t - 1 and are next
+  // overwritten in step t + 1), delta stored for that step; y (the readout
+  // filter) in registers from the block's start to its end; the loss added
+  // to the batch element's sum at the end
+  const bool defer = A.K_out <= kWave;
+  const int label = __builtin_amdgcn_readfirstlane(A.labels[b]);
+  float y[NL];
+  double loss[NL];
   lds_barrier();                                   // the others' barrier before the step loop
+#pragma unroll
+  for (int li = 0; li < NL; ++li) {
+    y[li] = l < A.K_out ? S.sy[li * A.K_out + l] : 0.0f;
+    loss[li] = 0.0;
+  }
+  auto softmax_step = [&](int ts) {
+#pragma unroll
+    for (int li = 0; li < NL; ++li) {
+      const float d = softmax_lanes(A, S.part + (li * 2 + (ts & 1)) * kFwdWaves * A.K_out, y[li], label,
+                                    loss[li]);
+      if (l < A.K_out)
+        __builtin_nontemporal_store(d, A.L[li].deltaK + ((size_t)ts * A.Bp + b) * A.ldk + l);
+    }
+  };
   for (int t = 0; t < A.steps; ++t) {
     if (t + 2 < A.steps) {
       put((t + 2) % 3);
       if (t + 3 < A.steps) load(t + 3);
     }
+    if (defer && t > 1) softmax_step(t - 2);
     for (int li = 0; li < NL; ++li) lds_barrier();   // one per layer step
   }
-  if (A.K_out <= kWave && A.steps > 0) lds_barrier();   // the last readout
+  if (defer && A.steps > 0) {
+    lds_barrier();                                 // the last readout
+    for (int ts = max(A.steps - 2, 0); ts < A.steps; ++ts) softmax_step(ts);
+    if (l < A.K_out)
+#pragma unroll
+      for (int li = 0; li < NL; ++li) S.sy[li * A.K_out + l] = y[li];
+    if (l == 0)
+#pragma unroll
+      for (int li = 0; li < NL; ++li) A.L[li].lossacc[b] += loss[li];
+  }
   lds_barrier();                                   // before the state goes out
 }
 
@@ -769,7 +805,7 @@ __global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__
     last_readout(0, ns0);
     if constexpr (NL > 1) last_readout(1, ns1);
     lds_barrier();
-    if (w == kSoftWave) {
+    if (!SVC && w == kSoftWave) {
       for (int ts = max(tl - 1, 0); ts <= tl; ++ts) {
         const size_t row = (size_t)ts * A.Bp + b;
         d0 = softmax_lanes(A, S.part + (ts & 1) * kFwdWaves * A.K_out, y0, label, loss0);
@@ -788,7 +824,9 @@ __global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__
   lds_barrier();
   forward_state<QN, 0>(A, S, b, false, v0, a0, zt0, cur);
   if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, false, v1, a1, zt1, cur);
-  if (threadIdx.x == kSoftWave * kWave) {   // lane 0 of the softmax wave holds the loss
+  // lane 0 of the softmax wave holds the loss (with the deferred softmax in
+  // the service wave: that wave's, added there)
+  if (threadIdx.x == kSoftWave * kWave && (!SVC || A.K_out > kWave)) {
     A.L[0].lossacc[b] += loss0;
     if constexpr (NL > 1) A.L[1].lossacc[b] += loss1;
   }
