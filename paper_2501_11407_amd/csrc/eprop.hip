@@ -269,7 +269,6 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
   const size_t R = plan->rows;
   plan->err_flag = (int*)take(sizeof(int));
   plan->w16ok = (int*)take(2 * sizeof(int));
-  size_t fwd_rows = 0;   // rows whose filter the forward keeps: recurrent rows of layer 1, all of layer 2
   for (int l = 0; l < c.n_layers; ++l) {
     Layer& L = plan->layers[l];
     L.n_inl = (l == 0) ? c.n_in : c.n_rec;
@@ -278,7 +277,6 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
     L.ldj = (int)round_up(N, 4);
     L.ldv = (int)round_up(N, 256);
     L.ldw = qn * eprop::kFwdThreads;
-    fwd_rows += (size_t)(l == 0 ? L.n_pre - L.n_inl : L.n_pre);
     const size_t np = L.n_pre, npp = L.n_pre_pad;
     L.Wt = (float*)take(sizeof(float) * np * L.ldw);
     // one more row, of zeros: the forward's drive loads of a batch's entries
@@ -340,17 +338,17 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
     for (int sl = 0; sl < slots; ++sl) L.zstart[sl] = (float*)take(sizeof(float) * B * L.n_pre_pad);
   }
   // the forward's shared memory (FwdLds): spike lists and their lengths by
-  // step parity, the block's input counts, readout partial sums and outputs,
-  // the filter of its rows, their p bytes, the spike bytes
-  const size_t npad4 = round_up(N, 4), NL = c.n_layers, W = eprop::kFwdWaves;
+  // step parity, the block's input counts, readout partial sums and outputs
+  // (the filter of the rows and the spikes are in registers)
+  const size_t NL = c.n_layers, W = eprop::kFwdWaves;
   const size_t smem_base = sizeof(int) * (NL * 2 * W * plan->jlist + NL * 2 * W + KM) +
-                           sizeof(float) * (NL * 2 * W * K + NL * K + fwd_rows) + NL * 2 * npad4;
+                           sizeof(float) * (NL * 2 * W * K + NL * K);
   // the forward's service wave and its input-drive ring (three steps of 512
   // QN floats) where that fits beside an eligibility workgroup
   const size_t ring = (size_t)3 * qn * eprop::kFwdThreads * sizeof(float);
-  const size_t fwd_smem = smem_base + sizeof(uint32_t) * fwd_rows;   // and the rows' p bits
-  constexpr size_t kShareSmem = 96 * 1024;   // leaves an eligibility workgroup room on the CU
-  plan->svc = qn <= 2 || (qn == 4 && fwd_smem + ring <= kShareSmem);
+  const size_t fwd_smem = smem_base;
+  // with up to four neurons per thread (the spike lists of at most 64 KiB)
+  plan->svc = qn <= 4;
   plan->smem = fwd_smem + (plan->svc ? ring : 0);
   plan->bytes = round_up(off, 256);
 }
@@ -575,7 +573,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   fa.n_adaptive = c.n_adaptive; fa.Kmax = P.Kmax; fa.steps = steps;
   fa.ldj = P.layers[0].ldv; fa.ldk = P.ldk; fa.ldn = P.ldn; fa.jlist = P.jlist;
   fa.alpha = c.alpha; fa.rho = c.rho; fa.kappa = c.kappa; fa.thr = c.thr; fa.beta = c.beta;
-  fa.gamma_over_thr = c.gamma / c.thr; fa.smem = P.smem; fa.svc = P.svc;
+  fa.gamma_over_thr = c.gamma / c.thr; fa.inv_thr = 1.0f / c.thr; fa.smem = P.smem; fa.svc = P.svc;
   fa.model = c.neuron_model;
   for (int m = 0; m < 2; ++m) {
     fa.mA[m][0] = (float)P.gen.A[m][0]; fa.mA[m][1] = (float)P.gen.A[m][1];

@@ -73,6 +73,7 @@ struct FwdArgs {
   int W32;
   int B, Bp, n_rec, K_out, n_adaptive, Kmax, steps, ldj, ldk, ldn, jlist;  // ldj: row stride of psiK
   float alpha, rho, kappa, thr, beta, gamma_over_thr;
+  float inv_thr;                 // 1/thr (exact for a power-of-two threshold)
   // neuron_model 1: h = A h_prev + b I + r z_prev, spike argument
   // u = c . h - thr (the two-compartment neuron, coefficients derived on the
   // host; v holds h0, a holds h1)

@@ -135,13 +135,22 @@ struct FwdLds {
   int* cnt;                      // [n_layers][2][waves]: their lengths
   int* nin;                      // [steps]: active inputs of the first layer per step
   float* part; float* sy;
-  float* szb;                    // filter of the rows the workgroup handles
-  uint32_t* zbits;               // [rows]: their p bits of the current 16-step chunk (bit t % 16)
-  uint8_t* zc;                   // [n_layers][2][npad]: spikes of this and the previous step
   bool w16;                      // the int16 weights are exact (FwdLayer::W16)
   int w16max;                    // their largest |k|
-  int npad;
-  int rows0;                     // rows handled in the first layer: its recurrent rows
+};
+
+// Per thread and layer, in registers: the spikes of the thread's neurons at
+// the last step, and the filter (zbar) and current 16-step chunk's p bits
+// (bit t % 16) of the presynaptic rows the thread owns: the recurrent rows
+// of its neurons (slot q; a second layer's: slot QN + q) and, in a second
+// layer, the input rows of the first layer's neurons it holds (slot q).  Every
+// row the forward filters is owned this way, so the filter needs no shared
+// memory.
+template <int QN>
+struct FwdRows {
+  float zb[2 * QN];
+  uint32_t bits[2 * QN];
+  bool z[QN];
 };
 
 template <int QN>
@@ -226,11 +235,11 @@ __device__ __forceinline__ float readout_sum(const FwdArgs& A, const float* Wout
   return Y;
 }
 
-// The spike list of a wave (parity par) from the spike bytes of its
-// neurons, for the block's first step; returns its length.
+// The spike list of a wave (parity par) from its neurons' spikes, for the
+// block's first step; returns its length.
 template <int QN, int LI>
-__device__ __forceinline__ int wave_list_from_bytes(const FwdArgs& A, const FwdLds& S, int par,
-                                                    const uint8_t* zc) {
+__device__ __forceinline__ int wave_list_from_regs(const FwdArgs& A, const FwdLds& S, int par,
+                                                   const FwdRows<QN>& R) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   int* spk = S.spk + ((LI * 2 + par) * kFwdWaves + w) * A.jlist;
@@ -238,7 +247,7 @@ __device__ __forceinline__ int wave_list_from_bytes(const FwdArgs& A, const FwdL
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
     const int j = fwd_neuron<QN>(tid, q);
-    const bool z = j < A.n_rec && zc[j] != 0;
+    const bool z = j < A.n_rec && R.z[q];
     const unsigned long long m = __ballot(z);
     if (z) spk[n + lanes_below(m, lane)] = j;
     n += __popcll(m);
@@ -257,23 +266,19 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 // the step's start, which needs fewer registers at the loads).  SVC: the
 // input drive comes from the shared-memory ring the service wave fills
 // (else each thread loads the next step's itself).
+// R: this layer's rows and spikes; R0: the first layer's (a second layer's
+// input: its spikes of this step).
 template <int QN, int LI, bool SOFTWIN, bool SVC>
 __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLds& S, int t, int b,
-                                                   int cur, float (&v)[QN], float (&ad)[QN],
+                                                   float (&v)[QN], float (&ad)[QN],
                                                    float (&zt)[QN], double& loss, int label,
                                                    float& yk, float& dk, int& nspk_prev,
-                                                   float (&iin)[QN]) {
+                                                   float (&iin)[QN], FwdRows<QN>& R,
+                                                   const FwdRows<QN>& R0) {
   const FwdLayer& Ly = A.L[LI];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
-  const uint8_t* zprev = S.zc + (LI * 2 + cur) * S.npad;
-  uint8_t* znow = S.zc + (LI * 2 + (cur ^ 1)) * S.npad;
-  // a second layer's input: the first layer's spikes of this step
-  const uint8_t* inp = S.zc + (cur ^ 1) * S.npad;
   const bool recurrent = Ly.n_pre > Ly.n_inl;
-  const int ridx = LI == 0 ? 0 : S.rows0;      // first filter row of this layer
-  float* szb = S.szb + ridx;
-  uint32_t* zbits = S.zbits + ridx;
   float* sy = S.sy + LI * A.K_out;
   const int pc = t & 1, pp = pc ^ 1;           // parity of this and the previous step
   int* spk_now = S.spk + ((LI * 2 + pc) * kFwdWaves + w) * A.jlist;
@@ -325,13 +330,10 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     const int base = hi ? seg1 + (s - kFwdWaves) * A.jlist : seg0 + s * A.jlist;
     return S.spk[base + (e - o)] + (hi ? A.n_rec : roff0);
   };
-  // the rows this wave filters: those of its neurons
-  const int jlo = w * (kWave * QN), jhi = min(A.n_rec, jlo + kWave * QN);
   const int zslot = t & (kChunk - 1);
-  auto filter_one = [&](int idx, uint8_t pv) {
-    const bool on = pv != 0;
-    if (on) zbits[idx] |= 1u << zslot;   // the lane owns the row
-    szb[idx] = A.alpha * szb[idx] + (on ? 1.0f : 0.0f);
+  auto filter_one = [&](int k, bool on) {
+    if (on) R.bits[k] |= 1u << zslot;
+    R.zb[k] = A.alpha * R.zb[k] + (on ? 1.0f : 0.0f);
   };
   // The presynaptic filter and the next step's input drive, off the
   // critical path: issued while the drive's loads are in flight.
@@ -352,12 +354,14 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
         for (int q = 0; q < QN; ++q) inext[q] = nv[q];
       }
     }
-    for (int j = jlo + lane; j < jhi; j += kWave) {
+#pragma unroll
+    for (int q = 0; q < QN; ++q) {
+      if (fwd_neuron<QN>(tid, q) >= A.n_rec) continue;
       if (LI == 0) {
-        if (recurrent) filter_one(j, zprev[j]);
+        if (recurrent) filter_one(q, R.z[q]);
       } else {
-        filter_one(j, inp[j]);
-        if (recurrent) filter_one(A.n_rec + j, zprev[j]);
+        filter_one(q, R0.z[q]);
+        if (recurrent) filter_one(QN + q, R.z[q]);
       }
     }
   };
@@ -456,7 +460,7 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
     bool z = false;
     psv[q] = 0.0f;
     if (j < A.n_rec) {
-      const float zp = zprev[j] ? 1.0f : 0.0f;
+      const float zp = R.z[q] ? 1.0f : 0.0f;
       float x;
       if (A.model == 1) {
         // a step linear in its two state components with host-derived
@@ -489,8 +493,11 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
         ad[q] = aa;
       }
       z = x > 0.0f;
-      znow[j] = z ? 1 : 0;
-      const float u = 1.0f - fabsf(x) / A.thr;
+      R.z[q] = z;
+      // |x|/thr as a product with 1/thr (the same value for a power-of-two
+      // threshold; within a rounding of it otherwise, and psi only enters
+      // the gradient)
+      const float u = 1.0f - fabsf(x) * A.inv_thr;
       psv[q] = A.gamma_over_thr * fmaxf(u, 0.0f);
       float zz = A.kappa * zt[q];
       zz = zz + (z ? 1.0f : 0.0f);
@@ -554,16 +561,19 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
   // block's last step are zero)
   if ((t & (kChunk - 1)) == kChunk - 1 || t == A.steps - 1) {
     uint16_t* cb = Ly.pbits + ((size_t)b * kKC + t / kChunk) * Ly.ldi;
-    auto flush = [&](int idx, int i) {
-      __builtin_nontemporal_store((uint16_t)zbits[idx], cb + i);
-      zbits[idx] = 0u;
+    auto flush = [&](int k, int i) {
+      __builtin_nontemporal_store((uint16_t)R.bits[k], cb + i);
+      R.bits[k] = 0u;
     };
-    for (int j = jlo + lane; j < jhi; j += kWave) {
+#pragma unroll
+    for (int q = 0; q < QN; ++q) {
+      const int j = fwd_neuron<QN>(tid, q);
+      if (j >= A.n_rec) continue;
       if (LI == 0) {
-        if (recurrent) flush(j, Ly.n_inl + j);
+        if (recurrent) flush(q, Ly.n_inl + j);
       } else {
-        flush(j, j);
-        if (recurrent) flush(A.n_rec + j, A.n_rec + j);
+        flush(q, j);
+        if (recurrent) flush(QN + q, A.n_rec + j);
       }
     }
   }
@@ -604,34 +614,38 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
 template <int QN, int LI>
 __device__ __forceinline__ void forward_state(const FwdArgs& A, const FwdLds& S, int b, bool load,
                                               float (&v)[QN], float (&ad)[QN], float (&zt)[QN],
-                                              int cur) {
+                                              FwdRows<QN>& R) {
   const FwdLayer& Ly = A.L[LI];
   const int tid = threadIdx.x;
   float* sy = S.sy + LI * A.K_out;
-  uint8_t* zc = S.zc + (LI * 2 + cur) * S.npad;
+  const bool recurrent = Ly.n_pre > Ly.n_inl;
+  // the filter of row i (load: also the block-start filter zstart)
+  auto row = [&](int k, int i) {
+    float* zb = Ly.zbar + (size_t)b * Ly.n_pre + i;
+    if (load) {
+      R.zb[k] = *zb;
+      R.bits[k] = 0u;
+      Ly.zstart[(size_t)b * Ly.ldi + i] = R.zb[k];
+    } else {
+      *zb = R.zb[k];
+    }
+  };
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
     const int j = fwd_neuron<QN>(tid, q);
     if (j < A.n_rec) {
       const size_t o = (size_t)b * A.n_rec + j;
       if (load) {
-        v[q] = Ly.v[o]; ad[q] = Ly.a[o]; zt[q] = Ly.ztil[o]; zc[j] = Ly.z[o];
+        v[q] = Ly.v[o]; ad[q] = Ly.a[o]; zt[q] = Ly.ztil[o]; R.z[q] = Ly.z[o] != 0;
       } else {
-        Ly.v[o] = v[q]; Ly.a[o] = ad[q]; Ly.ztil[o] = zt[q]; Ly.z[o] = zc[j];
+        Ly.v[o] = v[q]; Ly.a[o] = ad[q]; Ly.ztil[o] = zt[q]; Ly.z[o] = R.z[q] ? 1 : 0;
       }
-    }
-  }
-  const int ridx = LI == 0 ? 0 : S.rows0;
-  const int i0 = LI == 0 ? Ly.n_inl : 0;
-  const int nrows = Ly.n_pre - i0;
-  for (int r = tid; r < nrows; r += kFwdThreads) {
-    const int i = i0 + r;
-    if (load) {
-      const float z = Ly.zbar[(size_t)b * Ly.n_pre + i];
-      S.szb[ridx + r] = z;
-      Ly.zstart[(size_t)b * Ly.ldi + i] = z;
-    } else {
-      Ly.zbar[(size_t)b * Ly.n_pre + i] = S.szb[ridx + r];
+      if (LI == 0) {
+        if (recurrent) row(q, Ly.n_inl + j);
+      } else {
+        row(q, j);
+        if (recurrent) row(QN + q, A.n_rec + j);
+      }
     }
   }
   for (int k = tid; k < A.K_out; k += kFwdThreads) {
@@ -725,18 +739,12 @@ __global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__
   __builtin_amdgcn_s_setprio(3);
   const int b = blockIdx.x;
   FwdLds S;
-  S.npad = (A.n_rec + 3) & ~3;
-  S.rows0 = A.L[0].n_pre - A.L[0].n_inl;
-  const int rows = S.rows0 + (NL > 1 ? A.L[1].n_pre : 0);
   S.iring = (float*)smem;                          // SVC: [3][512 QN]
   S.spk = (int*)(S.iring + (SVC ? 3 * QN * kFwdThreads : 0));   // [NL][2][waves][jlist]
   S.cnt = S.spk + NL * 2 * kFwdWaves * A.jlist;    // [NL][2][waves]
   S.nin = S.cnt + NL * 2 * kFwdWaves;              // [Kmax]
   S.part = (float*)(S.nin + A.Kmax);               // [NL][2][waves][K_out]
   S.sy = S.part + NL * 2 * kFwdWaves * A.K_out;    // [NL][K_out]
-  S.szb = S.sy + NL * A.K_out;                     // [rows]
-  S.zbits = (uint32_t*)(S.szb + rows);             // [rows]
-  S.zc = (uint8_t*)(S.zbits + rows);               // [NL][2][npad]
   S.w16 = A.w16ok[0] != 0;
   S.w16max = A.w16ok[1];
   if constexpr (SVC) {
@@ -746,19 +754,18 @@ __global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__
     }
   }
 
-  for (int e = threadIdx.x; e < rows; e += kFwdThreads) S.zbits[e] = 0u;
   for (int e = threadIdx.x; e < A.steps; e += kFwdThreads) S.nin[e] = A.nin[(size_t)e * A.B + b];
   float v0[QN], a0[QN], zt0[QN], v1[QN], a1[QN], zt1[QN];
-  forward_state<QN, 0>(A, S, b, true, v0, a0, zt0, 0);
-  if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, true, v1, a1, zt1, 0);
+  FwdRows<QN> R0, R1;
+  forward_state<QN, 0>(A, S, b, true, v0, a0, zt0, R0);
+  if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, true, v1, a1, zt1, R1);
   // the spike lists of the step before the block (parity 1), from the
-  // spike bytes each thread has just loaded for its own neurons
-  wave_list_from_bytes<QN, 0>(A, S, 1, S.zc);
-  if constexpr (NL > 1) wave_list_from_bytes<QN, 1>(A, S, 1, S.zc + 2 * S.npad);
+  // spikes each thread has just loaded for its own neurons
+  wave_list_from_regs<QN, 0>(A, S, 1, R0);
+  if constexpr (NL > 1) wave_list_from_regs<QN, 1>(A, S, 1, R1);
   double loss0 = 0.0, loss1 = 0.0;
   // loaded once: a global load inside the step would wait for the step's stores
   const int label = __builtin_amdgcn_readfirstlane(A.labels[b]);
-  int cur = 0;
   // the first step's input drive (with the service wave: in the ring)
   float iin[QN];
   if constexpr (!SVC) {
@@ -783,10 +790,9 @@ __global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__
     // two layers of four neurons per thread and more: the softmax at the
     // step's start (no spills)
     constexpr bool SW = NL == 1 || QN < 4;
-    forward_layer_step<QN, 0, SW, SVC>(A, S, t, b, cur, v0, a0, zt0, loss0, label, y0, d0, ns0, iin);
+    forward_layer_step<QN, 0, SW, SVC>(A, S, t, b, v0, a0, zt0, loss0, label, y0, d0, ns0, iin, R0, R0);
     if constexpr (NL > 1)
-      forward_layer_step<QN, 1, SW, SVC>(A, S, t, b, cur, v1, a1, zt1, loss1, label, y1, d1, ns1, unused);
-    cur ^= 1;
+      forward_layer_step<QN, 1, SW, SVC>(A, S, t, b, v1, a1, zt1, loss1, label, y1, d1, ns1, unused, R1, R0);
   }
   if (A.K_out <= kWave && A.steps > 0) {
     // the readout of the last step's spikes, then the softmax of the last
@@ -822,8 +828,8 @@ __global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__
     }
   }
   lds_barrier();
-  forward_state<QN, 0>(A, S, b, false, v0, a0, zt0, cur);
-  if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, false, v1, a1, zt1, cur);
+  forward_state<QN, 0>(A, S, b, false, v0, a0, zt0, R0);
+  if constexpr (NL > 1) forward_state<QN, 1>(A, S, b, false, v1, a1, zt1, R1);
   // lane 0 of the softmax wave holds the loss (with the deferred softmax in
   // the service wave: that wave's, added there)
   if (threadIdx.x == kSoftWave * kWave && (!SVC || A.K_out > kWave)) {
@@ -2123,11 +2129,12 @@ hipError_t launch_forward_qn(const FwdArgs& a, hipStream_t s) {
 
 template <int QN, int NL>
 hipError_t launch_forward_svc(const FwdArgs& a, hipStream_t s) {
-  if constexpr (QN <= 4) {
-    if (a.svc) return launch_forward_qn<QN, NL, true>(a, s);
-  }
-  if constexpr (QN >= 4) return launch_forward_qn<QN, NL, false>(a, s);
-  return hipErrorInvalidValue;   // at most two neurons per thread: always with the service wave
+  // up to four neurons per thread: always with the service wave (its ring
+  // fits); more: without
+  if constexpr (QN <= 4)
+    return a.svc ? launch_forward_qn<QN, NL, true>(a, s) : hipErrorInvalidValue;
+  else
+    return a.svc ? hipErrorInvalidValue : launch_forward_qn<QN, NL, false>(a, s);
 }
 
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s) {

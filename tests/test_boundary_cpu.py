@@ -123,14 +123,16 @@ def test_binding_refuses_to_run_without_a_gpu_or_library(monkeypatch):
 
 
 def test_shape_past_the_forward_shared_memory_is_rejected():
-    # two recurrent layers of 8192 neurons need more than 160 KiB of shared
-    # memory in the forward kernel (spike lists of 16 neurons per thread in
-    # two layers): no workspace size, and a reason; one such layer fits
-    shape = synth.EpropShape(batch=1, n_in=100, n_rec=8192, n_out=10, T=5, n_adaptive=0, n_layers=2)
+    # two recurrent layers of 8192 neurons with 1024 classes need more than
+    # 160 KiB of shared memory in the forward kernel (the spike lists of 16
+    # neurons per thread and the readout partial sums of 1024 classes, per
+    # layer, by step parity): no workspace size, and a reason; with 10
+    # classes, or one such layer, it fits
+    shape = synth.EpropShape(batch=1, n_in=100, n_rec=8192, n_out=1024, T=5, n_adaptive=0, n_layers=2)
     assert eprop.eprop_workspace_bytes(eprop.make_config(shape)) == 0
     assert "shared memory" in eprop.eprop_last_error()
-    one = shape.replace(n_layers=1)
-    assert eprop.eprop_workspace_bytes(eprop.make_config(one)) > 0
+    assert eprop.eprop_workspace_bytes(eprop.make_config(shape.replace(n_out=10))) > 0
+    assert eprop.eprop_workspace_bytes(eprop.make_config(shape.replace(n_layers=1))) > 0
 
 
 def test_static_entry_rejects_shapes_past_its_scratch_before_any_device_call():
