@@ -278,9 +278,9 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
     L.ldv = (int)round_up(N, 256);
     L.ldw = qn * eprop::kFwdThreads;
     const size_t np = L.n_pre, npp = L.n_pre_pad;
-    L.Wt = (float*)take(sizeof(float) * np * L.ldw);
-    // one more row, of zeros: the forward's drive loads of a batch's entries
-    // past the active list read it
+    // one more row each, of zeros: the forward's drive loads of a batch's
+    // entries past the active list read it
+    L.Wt = (float*)take(sizeof(float) * (np + 1) * L.ldw);
     L.W16 = (int16_t*)take(sizeof(int16_t) * (np + 1) * L.ldw);
     L.WoutT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
     L.FbT = (float*)take(sizeof(float) * plan->ldn * plan->ldk);
@@ -429,6 +429,9 @@ int pack_weights(eprop_ctx* ctx) {
     if (rc16) return rc16;
     rc16 = check(ctx, eprop::launch_zero((unsigned char*)(L.W16 + (size_t)L.n_pre * L.ldw),
                                          sizeof(int16_t) * L.ldw, ctx->stream), "weight packing");
+    if (!rc16)
+      rc16 = check(ctx, eprop::launch_zero((unsigned char*)(L.Wt + (size_t)L.n_pre * L.ldw),
+                                           sizeof(float) * L.ldw, ctx->stream), "weight packing");
     if (rc16) return rc16;
     // drive weights transposed, Wt[i][j] = W[j][i], columns padded to the
     // forward workgroup size

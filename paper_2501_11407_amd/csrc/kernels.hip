@@ -424,26 +424,30 @@ __device__ __forceinline__ void forward_layer_step(const FwdArgs& A, const FwdLd
 #pragma unroll
     for (int q = 0; q < QN; ++q) I[q] = I[q] + (float)isum[q] * 0x1p-14f;
   }
+  // fp32 rows: the same scheme (entries past the list read the zero row
+  // n_pre); the zeros are added after every listed row, to a sum that is
+  // never -0 (it starts at +0 and a sum of opposite values rounds to +0), so
+  // the sum's bits are those of the listed rows' sequential sum
+  const char* wt = (const char*)Ly.Wt;
   for (int k0 = 0; !w16 && k0 < total; k0 += UB) {
-    const int ent = list_entry(min(k0 + (lane & (UB - 1)), total - 1));
-    const int nb = min(UB, total - k0);   // rows of this batch (wave-uniform)
+    const int e = k0 + (lane & (UB - 1));
+    const int le = list_entry(min(e, total - 1));
+    const int ent = e < total ? le : Ly.n_pre;
     float wv[UB][QN];
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      const int i = __builtin_amdgcn_readlane(ent, u);
-      const float* rowp = Ly.Wt + (size_t)i * Ly.ldw;
-      if (u < nb)
+      const uint32_t i = (uint32_t)__builtin_amdgcn_readlane(ent, u);
 #pragma unroll
-        for (int q = 0; q < QN; ++q) wv[u][q] = rowp[fwd_neuron<QN>(tid, q)];
+      for (int q = 0; q < QN; ++q)
+        wv[u][q] = *(const float*)(wt + (i * (uint32_t)Ly.ldw + (uint32_t)fwd_neuron<QN>(tid, q)) * 4u);
     }
     __builtin_amdgcn_sched_barrier(0);
     filter_rows();
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < UB; ++u)
-      if (k0 + u < total)
 #pragma unroll
-        for (int q = 0; q < QN; ++q) I[q] += wv[u][q];
+      for (int q = 0; q < QN; ++q) I[q] += wv[u][q];
   }
   filter_rows();   // (no active row this step)
   if (defer && t > 0) {
