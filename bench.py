@@ -71,7 +71,7 @@ def trace_bytes(shape, layer: int, launches: int, first_launches: int, steps: in
     return int((2 * launches - first_launches) * trace + operands)
 
 
-BYTE_MODEL = ("block: per launch (one block of up to 256 steps), every trace read once and "
+BYTE_MODEL = ("block: per launch (one block of up to 512 steps), every trace read once and "
               "written once (4 B x B x N_pre x (N_post + N_adaptive) each way; the first launch "
               "after a reset reads none), the fp64 gradient accumulator read and written once "
               "(8 B x N_pre x N_post each way), the operands of the block's steps read once "

@@ -166,6 +166,40 @@ int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int3
                        uint32_t* d_spikes);
 
 /*
+ * How eprop_run_sequence splits a call into blocks (eprop_set_block_split).
+ * The steps up to the next weight change (or the end of the call) form one
+ * block when they number at most 256, else blocks of equal length (within a
+ * step), at least two and each at most 512 steps, the block limit.  With
+ * EPROP_SPLIT_AUTO (the default) a run of more than 512 steps may instead
+ * start with a short block followed by blocks of twice its length, one block
+ * more than the equal split, when a rough cost model of the shape says that
+ * starting the first eligibility pass earlier saves more than the added trace
+ * round trip costs.  EPROP_SPLIT_EQUAL always takes the equal split.
+ */
+#define EPROP_SPLIT_AUTO 0
+#define EPROP_SPLIT_EQUAL 1
+
+/*
+ * Sets the split mode of the context's later eprop_run_sequence calls (kept
+ * over resets).  The split changes only the order of floating-point
+ * summation in the gradients.  Returns 0, EPROP_EINVAL (unknown mode),
+ * EPROP_ESTATE.
+ */
+int eprop_set_block_split(eprop_ctx* ctx, int32_t mode);
+
+/*
+ * The block lengths eprop_run_sequence uses for a call of T steps that starts
+ * t0 steps after the last reset, with online application every `online_every`
+ * steps (0: none), for the shape `cfg` and split `mode`.  Host only: touches
+ * no device and no context.  Writes min(count, max_blocks) lengths to
+ * `lengths` (host int32; may be NULL when max_blocks is 0) and returns the
+ * count of blocks, or EPROP_EINVAL (invalid config or mode, T < 1, t0 < 0,
+ * online_every < 0, max_blocks < 0, or lengths NULL with max_blocks > 0).
+ */
+int eprop_block_lengths(const eprop_config* cfg, int32_t T, int64_t t0, int32_t online_every,
+                        int32_t mode, int32_t* lengths, int32_t max_blocks);
+
+/*
  * Writes the gradient accumulated since the last reset, summed over batch
  * elements and steps:
  *   d_grads: host array of 2*n_layers device pointers, per layer l:

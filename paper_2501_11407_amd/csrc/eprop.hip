@@ -384,6 +384,7 @@ struct eprop_ctx {
   // since the reset, before the next step runs
   float online_lr = 0.0f;
   int online_every = 0;
+  int split_mode = EPROP_SPLIT_AUTO;   // eprop_set_block_split
   long long online_applied = -1;   // step count of the last update
   hipEvent_t ev_update = nullptr;
   // the first layer's input drive of the next block of a sequence, computed
@@ -885,6 +886,90 @@ int eprop_step(eprop_ctx* ctx, const uint8_t* d_x_t, const int32_t* d_labels, ui
   return do_block(ctx, d_x_t, 1, d_labels, d_spikes_t, nullptr, 0);
 }
 
+namespace {
+
+// Rough costs that decide the block split, in microseconds on MI355X: one
+// round trip of every layer's per-synapse traces through HBM at about half
+// its peak bandwidth (the fixed part of an eligibility pass), and one
+// timestep of the forward pass of every layer with the learning-signal and
+// coefficient passes that follow it.
+struct SplitCost {
+  double round_trip_us = 0, step_us = 0;
+};
+
+SplitCost split_cost(const Plan& P) {
+  const eprop_config& c = P.cfg;
+  SplitCost k;
+  const double per_syn = 1.0 + (double)P.na2 / c.n_rec + P.rt;   // traces per synapse
+  for (const Layer& L : P.layers)
+    k.round_trip_us += (double)c.batch * L.n_pre * c.n_rec * per_syn * 8.0 / 4.0e6;
+  k.step_us = c.n_layers * (2.5 + (double)c.batch * c.n_rec * 32.0 / 4.0e6);
+  return k;
+}
+
+// Blocks of up to Kmax steps that end where the weights change.  The steps
+// up to the next change (or the end of the call), a segment, form one block
+// when they are at most Kmax / 2, else blocks of equal length (within a
+// step), at least two, so that the forward pass of the second block runs
+// beside the eligibility pass of the first.  A segment longer than Kmax may
+// instead start with a short block followed by k blocks of twice its length
+// (k the smallest count that keeps those at most Kmax), when that adds one
+// block to the equal split: the first eligibility pass then starts that many
+// forward steps earlier, which pays when the steps saved cost more than the
+// added trace round trip.
+struct Split {
+  int32_t seg_end = 0;   // end of the current segment (call-local step)
+  int blk = 0;           // length of its blocks after the first
+};
+
+int next_block(int32_t t, int32_t T, long long t_ctx, int32_t every, int mode,
+               const SplitCost& cost, Split& sp) {
+  if (t < sp.seg_end) return std::min(sp.blk, sp.seg_end - t);
+  long long seg = T - t;
+  if (every > 0) seg = std::min<long long>(seg, every - t_ctx % every);
+  sp.seg_end = (int32_t)(t + seg);
+  const long long K = kBlockSteps;
+  long long first = seg, blk = seg;
+  if (seg > K / 2) {
+    const long long nb = std::max<long long>(2, (seg + K - 1) / K);
+    first = blk = (seg + nb - 1) / nb;
+    if (seg > K) {
+      const long long k = (2 * seg - K + 2 * K - 1) / (2 * K);
+      const long long short_first = (seg + 2 * k) / (2 * k + 1);
+      if (mode == EPROP_SPLIT_AUTO && k == nb &&
+          (double)(first - short_first) * cost.step_us > cost.round_trip_us) {
+        first = short_first;
+        blk = (seg - short_first + k - 1) / k;
+      }
+    }
+  }
+  sp.blk = (int)blk;
+  return (int)first;
+}
+
+}  // namespace
+
+int eprop_block_lengths(const eprop_config* cfg, int32_t T, int64_t t0, int32_t online_every,
+                        int32_t mode, int32_t* lengths, int32_t max_blocks) {
+  std::string why;
+  if (!valid_config(cfg, &why)) return fail(nullptr, EPROP_EINVAL, why);
+  if (T < 1 || t0 < 0 || online_every < 0 || max_blocks < 0 || (max_blocks > 0 && !lengths) ||
+      (mode != EPROP_SPLIT_AUTO && mode != EPROP_SPLIT_EQUAL))
+    return fail(nullptr, EPROP_EINVAL, "T must be >= 1, t0, online_every and max_blocks >= 0, "
+                                       "lengths not NULL when max_blocks > 0, mode a split mode");
+  Plan probe;
+  make_plan(*cfg, nullptr, &probe);
+  const SplitCost cost = split_cost(probe);
+  Split sp;
+  int32_t n = 0;
+  for (int32_t t = 0; t < T; ++n) {
+    const int steps = next_block(t, T, t0 + t, online_every, mode, cost, sp);
+    if (n < max_blocks) lengths[n] = steps;
+    t += steps;
+  }
+  return n;
+}
+
 int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int32_t* d_labels,
                        uint32_t* d_spikes) {
   if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
@@ -895,17 +980,14 @@ int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int3
   const size_t s_step = (size_t)c.n_layers * c.batch * ((c.n_rec + 31) / 32);
   int rc0 = join_forward_stream(ctx);
   if (rc0) return rc0;
-  // blocks of up to Kmax steps that end where the weights change
-  auto block_steps = [&](int32_t t, long long t_ctx) {
-    int steps = std::min<int32_t>(ctx->plan.Kmax, T - t);
-    if (ctx->online_every > 0)
-      steps = (int)std::min<long long>(steps, ctx->online_every - t_ctx % ctx->online_every);
-    return steps;
-  };
+  const SplitCost cost = split_cost(ctx->plan);
+  Split sp;
   for (int32_t t = 0; t < T;) {
-    const int steps = block_steps(t, ctx->t);
+    const int steps = next_block(t, T, ctx->t, ctx->online_every, ctx->split_mode, cost, sp);
     const int32_t tn = t + steps;
-    const int steps_next = tn < T ? block_steps(tn, ctx->t + steps) : 0;
+    Split sp_next = sp;
+    const int steps_next =
+        tn < T ? next_block(tn, T, ctx->t + steps, ctx->online_every, ctx->split_mode, cost, sp_next) : 0;
     int rc = do_block(ctx, d_x + t * x_step, steps, d_labels,
                       d_spikes ? d_spikes + t * s_step : nullptr,
                       steps_next > 0 ? d_x + tn * x_step : nullptr, steps_next);
@@ -966,6 +1048,14 @@ int eprop_set_online(eprop_ctx* ctx, float lr, int32_t every) {
   if (every < 0 || !std::isfinite(lr)) return fail(ctx, EPROP_EINVAL, "every must be >= 0 and lr finite");
   ctx->online_lr = lr;
   ctx->online_every = every;
+  return EPROP_OK;
+}
+
+int eprop_set_block_split(eprop_ctx* ctx, int32_t mode) {
+  if (!usable(ctx)) return fail(ctx, EPROP_ESTATE, "context not initialised");
+  if (mode != EPROP_SPLIT_AUTO && mode != EPROP_SPLIT_EQUAL)
+    return fail(ctx, EPROP_EINVAL, "mode must be EPROP_SPLIT_AUTO or EPROP_SPLIT_EQUAL");
+  ctx->split_mode = mode;
   return EPROP_OK;
 }
 

@@ -26,7 +26,7 @@ namespace eprop {
 
 constexpr int kFwdThreads = 512;               // forward workgroup: one batch element
 constexpr int kFwdWaves = kFwdThreads / 64;
-constexpr int kBlockSteps = 256;       // timesteps per block (Kmax)
+constexpr int kBlockSteps = 512;       // timesteps per block (Kmax)
 constexpr int kTileI = 256;            // eligibility workgroup tile: 256 (i) x 16 (j)
 constexpr int kTileJ = 16;
 constexpr int kRowPad = kTileI;        // n_pre padded to the tile height (ldi)

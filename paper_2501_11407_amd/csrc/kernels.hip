@@ -2239,7 +2239,7 @@ hipError_t launch_trace_nch(const TraceArgs& a, hipStream_t s, std::integer_sequ
 }
 
 hipError_t launch_trace(const TraceArgs& a, hipStream_t s) {
-  static_assert(kKC == 16, "one kernel per chunk count of a 256-step block");
+  // one kernel per chunk count of a block (kKC of them)
   if (a.kpad < kChunk || a.kpad > kBlockSteps || a.kpad % kChunk != 0) return hipErrorInvalidValue;
   const auto nch = std::make_integer_sequence<int, kKC>{};
   return a.reset_through ? launch_trace_nch<true>(a, s, nch) : launch_trace_nch<false>(a, s, nch);

@@ -18,10 +18,12 @@ LIB_PATH = os.environ.get("EPROP_LIB") or \
     os.path.join(os.path.dirname(os.path.abspath(__file__)), "libeprop.so")
 
 EPROP_OK, EPROP_EINVAL, EPROP_ENOSPACE, EPROP_EDEVICE, EPROP_ESTATE = 0, -1, -2, -3, -4
+EPROP_SPLIT_AUTO, EPROP_SPLIT_EQUAL = 0, 1
 
 # Every function the header declares, in declaration order.
 SYMBOLS = (
-    "eprop_neuron_coefficients", "eprop_workspace_bytes", "eprop_init", "eprop_step", "eprop_run_sequence", "eprop_get_grads",
+    "eprop_neuron_coefficients", "eprop_workspace_bytes", "eprop_init", "eprop_step", "eprop_run_sequence",
+    "eprop_set_block_split", "eprop_block_lengths", "eprop_get_grads",
     "eprop_reset", "eprop_status", "eprop_set_feedback", "eprop_set_online", "eprop_get_weights",
     "eprop_destroy", "eprop_sequence_static", "eprop_last_error",
     "eprop_profile_begin", "eprop_profile_end", "eprop_debug_buffer",
@@ -67,6 +69,8 @@ def load_library(path: str = LIB_PATH):
         "eprop_init": (ctypes.c_int, [cfgp, vp, ctypes.c_size_t, vp, vp, ctypes.POINTER(vp)]),
         "eprop_step": (ctypes.c_int, [vp, vp, vp, vp]),
         "eprop_run_sequence": (ctypes.c_int, [vp, vp, i32, vp, vp]),
+        "eprop_set_block_split": (ctypes.c_int, [vp, i32]),
+        "eprop_block_lengths": (ctypes.c_int, [cfgp, i32, i64, i32, i32, ctypes.POINTER(i32), i32]),
         "eprop_get_grads": (ctypes.c_int, [vp, vp, vp]),
         "eprop_reset": (ctypes.c_int, [vp]),
         "eprop_set_feedback": (ctypes.c_int, [vp, vp]),
@@ -119,6 +123,18 @@ def eprop_workspace_bytes(cfg: eprop_config) -> int:
     return int(load_library().eprop_workspace_bytes(ctypes.byref(cfg)))
 
 
+def eprop_block_lengths(cfg: eprop_config, T: int, t0: int = 0, online_every: int = 0,
+                        mode: int = 0) -> list:
+    """Block lengths of a run_sequence call of T steps, t0 steps after the
+    last reset (host only)."""
+    lib = load_library()
+    n = lib.eprop_block_lengths(ctypes.byref(cfg), int(T), int(t0), int(online_every), int(mode), None, 0)
+    _check(min(n, 0))
+    out = (ctypes.c_int32 * n)()
+    lib.eprop_block_lengths(ctypes.byref(cfg), int(T), int(t0), int(online_every), int(mode), out, n)
+    return list(out)
+
+
 def eprop_last_error(ctx=None) -> str:
     return load_library().eprop_last_error(ctx).decode()
 
@@ -166,6 +182,10 @@ def eprop_set_feedback(ctx, feedback: Optional[Sequence[Optional[torch.Tensor]]]
         arr = (ctypes.c_void_p * len(feedback))(*[_ptr(f) for f in feedback])
     _check(load_library().eprop_set_feedback(ctx, ctypes.cast(arr, ctypes.c_void_p)
                                              if arr is not None else None), ctx)
+
+
+def eprop_set_block_split(ctx, mode: int):
+    _check(load_library().eprop_set_block_split(ctx, int(mode)), ctx)
 
 
 def eprop_set_online(ctx, lr: float, every: int):
@@ -317,6 +337,10 @@ class EpropContext:
         """Online weight application: every ``every`` steps since the reset
         the weights in use become W0 - lr * G on the 2**-14 grid (0: off)."""
         eprop_set_online(self.ctx, lr, every)
+
+    def set_block_split(self, mode: int):
+        """EPROP_SPLIT_AUTO (default) or EPROP_SPLIT_EQUAL for later run_sequence calls."""
+        eprop_set_block_split(self.ctx, mode)
 
     def get_weights(self):
         """The weights in use: (W list, W_out list) as new device tensors."""

@@ -36,7 +36,7 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
         n = eprop.eprop_workspace_bytes(eprop.make_config(shape))
         traces = sum(4 * shape.batch * shape.n_pre(l) * (shape.n_rec + shape.n_adaptive)
                      for l in range(shape.n_layers))
-        # per-step vectors for three blocks of at most 256 steps (the forward
+        # per-step vectors for three blocks of at most 512 steps (the forward
         # writes one while the passes after it read the others; the filtered
         # presynaptic vector twice: fp32 and as fp16 pairs), plus one
         # block's eligibility coefficients per layer and slot (three per neuron
@@ -57,8 +57,9 @@ def test_workspace_size_has_no_sequence_length_and_scales_with_traces():
         qn = 1
         while qn * 512 < shape.n_rec:
             qn *= 2
-        indrive = 2 * 256 * shape.batch * (512 * qn + 1) * 4
-        assert traces <= n <= (traces * 1.05 + slots * 256 * per_step + slots * shape.n_layers * 256 * coef
+        kmax = 512
+        indrive = 2 * kmax * shape.batch * (512 * qn + 1) * 4
+        assert traces <= n <= (traces * 1.05 + slots * kmax * per_step + slots * shape.n_layers * kmax * coef
                                + partial + indrive + (16 << 20)), \
             (name, n, traces)
     # the same shape with any T needs the same workspace: T is not an input
@@ -202,3 +203,72 @@ def test_two_compartment_config_checks():
     lif = eprop.eprop_workspace_bytes(eprop.make_config(u.replace(neuron_model=0)))
     two = eprop.eprop_workspace_bytes(eprop.make_config(u))
     assert two > lif + 2 * 4 * u.batch * u.n_pre(0) * u.n_rec * 0.9
+
+
+def _check_blocks(cfg, T, t0, every, mode=eprop.EPROP_SPLIT_AUTO):
+    lens = eprop.eprop_block_lengths(cfg, T, t0, every, mode)
+    assert sum(lens) == T and all(1 <= n <= 512 for n in lens), (T, t0, every, lens)
+    t = t0
+    seg = []
+    for n in lens:
+        # no block holds a weight change: a change falls before every step
+        # whose count since the reset is a positive multiple of `every`
+        if every:
+            assert all(u % every != 0 for u in range(t + 1, t + n)), (T, t0, every, lens)
+        seg.append(n)
+        t += n
+        if (every and t % every == 0) or t == t0 + T:
+            # the blocks of one segment: one block of at most 256 steps; or
+            # blocks of equal length, at least two (the last may be shorter by
+            # the rounding); or a short first block and blocks of twice its
+            # length
+            S = sum(seg)
+            rest = seg[1:]
+            if S <= 256:
+                assert seg == [S]
+            else:
+                assert rest and all(r == rest[0] for r in rest[:-1])
+                assert 0 <= rest[0] - rest[-1] < len(seg)
+                nb = max(2, -(-S // 512))
+                equal = len(seg) == nb and all(x == seg[0] for x in seg[:-1])
+                short = mode == eprop.EPROP_SPLIT_AUTO and S > 512 and len(rest) == nb and \
+                    abs(2 * seg[0] - rest[0]) <= 2 and \
+                    2 * S / (2 * len(rest) + 1) <= 512 < 2 * S / (2 * len(rest) - 1)
+                assert equal or short, (S, seg)
+            seg = []
+    assert not seg
+    return lens
+
+
+def test_block_lengths_cover_the_call_and_end_at_weight_changes():
+    cfg = {name: eprop.make_config(shape) for name, shape in synth.WORKLOADS.items()}
+    c4 = cfg["ralif_b128_n1024_t1000"]
+    # the headline shape: a short first block pays; two layers of 2048
+    # neurons: it does not (the trace round trip costs more than the steps
+    # saved); up to 512 steps: two equal blocks
+    assert eprop.eprop_block_lengths(c4, 1000) == [200, 400, 400]
+    assert eprop.eprop_block_lengths(cfg["ralif2_b256_n2048_t2000"], 2000) == [500] * 4
+    assert eprop.eprop_block_lengths(cfg["ralif_b64_n512_t500"], 500) == [250, 250]
+    assert eprop.eprop_block_lengths(cfg["rlif_b32_n256_t250"], 250) == [250]
+    assert eprop.eprop_block_lengths(c4, 1000, 0, 256) == [256, 256, 256, 232]
+    assert eprop.eprop_block_lengths(c4, 300, 200, 256) == [56, 244]
+    assert eprop.eprop_block_lengths(c4, 1000, mode=eprop.EPROP_SPLIT_EQUAL) == [500, 500]
+    rng = np.random.default_rng(3)
+    for c in cfg.values():
+        for _ in range(150):
+            T = int(rng.integers(1, 5000))
+            t0 = int(rng.integers(0, 3000))
+            every = int(rng.choice([0, 1, 7, 64, 256, 300, 511, 512, 513, 1000, 2048]))
+            _check_blocks(c, T, t0, every)
+            _check_blocks(c, T, t0, every, eprop.EPROP_SPLIT_EQUAL)
+    for T in list(range(1, 1100)) + [1280, 1281, 1536, 1537, 4096]:
+        _check_blocks(c4, T, 0, 0)
+        _check_blocks(c4, T, 0, 0, eprop.EPROP_SPLIT_EQUAL)
+
+
+@pytest.mark.parametrize("bad", [(0, 0, 0, 0), (5, -1, 0, 0), (5, 0, -1, 0), (5, 0, 0, 2)])
+def test_block_lengths_reject_bad_arguments(bad):
+    cfg = eprop.make_config(synth.WORKLOADS["ralif_b128_n1024_t1000"])
+    with pytest.raises(eprop.EpropError) as e:
+        eprop.eprop_block_lengths(cfg, *bad)
+    assert e.value.code == eprop.EPROP_EINVAL

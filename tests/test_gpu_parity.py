@@ -35,8 +35,8 @@ DISTINCT = dict(kappa=f32(math.exp(-1 / 7)), rho=f32(math.exp(-1 / 50)))
 # Small shapes the oracle finishes in well under a second: ragged sizes that
 # leave partial 64x64 eligibility tiles, partial 16-step chunks and 4-step
 # quads, partial spike words, an adaptive/LIF boundary inside a tile, several
-# tiles over j, several batch splits, and sequences of several 256-step blocks
-# whose last block is short (one chunk; four chunks).
+# tiles over j, several batch splits, and sequences split into two and three
+# blocks (174 + 347 steps; 220 + 440 + 440).
 RAGGED = {
     "rlif_ragged": (small(**DISTINCT), 2, 4.0),
     "ralif_ragged_na13": (small(n_adaptive=13, **DISTINCT), 3, 4.0),
@@ -49,8 +49,8 @@ RAGGED = {
     "wide_1100": (small(batch=2, n_in=50, n_rec=1100, n_out=7, T=12, n_adaptive=550), 9, 4.0),
     "batch37_k33": (small(batch=37, n_in=70, n_rec=70, n_out=33, T=25, n_adaptive=35), 10, 4.0),
     "single_step": (small(T=1, n_adaptive=13), 11, 8.0),
-    "blocks_256_256_9": (small(n_adaptive=13, T=521, **DISTINCT), 12, 4.0),
-    "blocks_256_50": (small(batch=6, n_adaptive=29, T=306, **DISTINCT), 13, 4.0),
+    "blocks_174_347": (small(n_adaptive=13, T=521, **DISTINCT), 12, 4.0),
+    "blocks_220_440_440": (small(batch=6, n_adaptive=29, T=1100, **DISTINCT), 13, 4.0),
     # more classes than one wave's lanes (the readout's second path), up to
     # the largest class count the library accepts
     "classes_100": (small(batch=4, n_out=100, n_adaptive=13, **DISTINCT), 14, 4.0),
@@ -110,7 +110,7 @@ def test_grid_weights_take_the_integer_drive():
     ctx.close()
 
 
-@pytest.mark.parametrize("name", ["rlif_ragged", "ralif2_two_layers", "blocks_256_50", "wide_1100",
+@pytest.mark.parametrize("name", ["rlif_ragged", "ralif2_two_layers", "blocks_220_440_440", "wide_1100",
                                   "classes_100"])
 def test_off_grid_weights_take_the_float_drive(name):
     shape, seed, scale = RAGGED[name]
@@ -314,7 +314,7 @@ def test_online_off_and_reset_give_the_plain_run():
 
 # ---------------------------------------------------------------- random feedback
 @pytest.mark.parametrize("name", ["rlif_ragged", "ralif_ragged_na13", "ralif2_two_layers",
-                                  "blocks_256_50"])
+                                  "blocks_220_440_440"])
 def test_random_feedback_matches_oracle(name):
     # learning signal L = B^T delta with fixed matrices B (two layers: the
     # second layer keeps W_out, so both forms run in one context)
@@ -360,8 +360,8 @@ def test_feedback_kept_over_reset_and_cleared():
 
 # ---------------------------------------------------------------- reset path kept
 @pytest.mark.parametrize("name", ["rlif_ragged", "ralif_ragged_na13", "ralif_all_adaptive", "ff_alif",
-                                  "ralif2_two_layers", "blocks_256_50", "single_step", "classes_100",
-                                  "blocks_256_256_9", "wide_1100"])
+                                  "ralif2_two_layers", "blocks_220_440_440", "single_step", "classes_100",
+                                  "blocks_174_347", "wide_1100"])
 def test_reset_through_matches_oracle(name):
     shape, seed, scale = RAGGED[name]
     shape = shape.replace(reset_grad=1)
@@ -375,11 +375,24 @@ def test_reset_through_matches_oracle(name):
     banner(f"{name}: {errs}")
 
 
-# The eligibility kernel exists once per count of 16-step chunks in a block.
-# Fed in calls of these lengths, each call is one block of 1, 2, ..., 15
-# chunks (the last chunk partial but for the first); 16 chunks come with
-# every longer sequence.
-EVERY_CHUNK_COUNT = [1, 17, 33, 49, 65, 81, 97, 113, 129, 145, 161, 177, 193, 209, 240]
+# The eligibility kernel exists once per count of 16-step chunks in a block
+# (up to 32: blocks of at most 512 steps).  Under the equal split a call of up
+# to 256 steps is one block, one of 257..1024 steps two blocks of equal length
+# (eprop_block_lengths says so).  Fed in calls of these lengths, the blocks
+# hold 1, 2, ..., 32 chunks (the last chunk partial but for the first).
+EVERY_CHUNK_COUNT = [16 * k + 1 for k in range(16)] + [2 * (16 * k + 1) for k in range(16, 32)]
+
+
+def every_chunk_count_run(wl):
+    cfg = eprop.make_config(wl.shape)
+    blocks = [n for T in EVERY_CHUNK_COUNT
+              for n in eprop.eprop_block_lengths(cfg, T, mode=eprop.EPROP_SPLIT_EQUAL)]
+    assert sorted({-(-n // 16) for n in blocks}) == list(range(1, 33))
+    ctx = eprop.EpropContext(wl.shape, wl.W, wl.Wout)
+    ctx.set_block_split(eprop.EPROP_SPLIT_EQUAL)
+    gpu = gpu_run(wl, chunks=EVERY_CHUNK_COUNT, ctx=ctx)
+    ctx.close()
+    return gpu
 
 
 @pytest.mark.parametrize("reset_grad", [0, 1])
@@ -388,7 +401,7 @@ def test_every_chunk_count(reset_grad):
                   **DISTINCT)
     banner(f"every chunk count, reset_grad={reset_grad}, {shape}")
     wl = synth.make_workload(shape, 21, input_scale=4.0)
-    gpu = gpu_run(wl, chunks=EVERY_CHUNK_COUNT)
+    gpu = every_chunk_count_run(wl)
     errs, ref = check_against_oracle(wl, gpu)
     assert ref.spikes.any()
     banner(f"every chunk count: {errs}")
@@ -426,7 +439,7 @@ TWO_COMP = {
     "tc_ragged": (small(**TC, **DISTINCT), 2, 4.0),
     "tc_ff": (small(recurrent=0, **TC, **DISTINCT), 6, 4.0),
     "tc_two_layers": (small(batch=5, n_in=21, n_rec=45, n_out=4, n_layers=2, **TC, **DISTINCT), 4, 4.0),
-    "tc_blocks_256_50": (small(batch=6, T=306, **TC, **DISTINCT), 13, 4.0),
+    "tc_blocks_220_440_440": (small(batch=6, T=1100, **TC, **DISTINCT), 13, 4.0),
     "tc_wide_1100": (small(batch=2, n_in=50, n_rec=1100, n_out=7, T=12, **TC), 9, 4.0),
     "tc_positive_feedback": (small(bap=0.25, coupling=0.75, **TC, **DISTINCT), 8, 4.0),
     "tc_classes_100": (small(batch=4, n_out=100, **TC, **DISTINCT), 14, 4.0),
@@ -473,7 +486,7 @@ def test_two_compartment_every_chunk_count(reset_grad):
     shape = small(n_rec=70, T=sum(EVERY_CHUNK_COUNT), reset_grad=reset_grad, **TC, **DISTINCT)
     banner(f"two-compartment every chunk count, reset_grad={reset_grad}")
     wl = synth.make_workload(shape, 21, input_scale=4.0)
-    gpu = gpu_run(wl, chunks=EVERY_CHUNK_COUNT)
+    gpu = every_chunk_count_run(wl)
     errs, ref = check_against_oracle(wl, gpu)
     assert ref.spikes.any()
 
@@ -565,7 +578,7 @@ def adversarial_range_workload(reset_grad=0):
     """Mostly inhibitory inputs with a few strong excitatory channels (the
     pseudo-derivative is zero for most steps of most neurons) and a readout
     that becomes confident in the one label, so that the learning signal of a
-    neuron spans many decades within a 256-step block."""
+    neuron spans many decades within one block."""
     shape = synth.EpropShape(batch=4, n_in=40, n_rec=48, n_out=3, T=300, n_adaptive=24,
                              reset_grad=reset_grad, **DISTINCT)
     wl = synth.make_workload(shape, 77, input_scale=6.0)

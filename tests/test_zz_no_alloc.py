@@ -17,8 +17,8 @@ f32 = synth.f32
 DISTINCT = dict(kappa=f32(math.exp(-1 / 7)), rho=f32(math.exp(-1 / 50)))
 
 CASES = [
-    # two layers, two blocks (256 + 44 steps), partial tiles
-    (synth.EpropShape(batch=5, n_in=21, n_rec=45, n_out=4, T=300, n_layers=2, n_adaptive=22,
+    # two layers, two blocks (200 + 400 steps), partial tiles
+    (synth.EpropShape(batch=5, n_in=21, n_rec=45, n_out=4, T=600, n_layers=2, n_adaptive=22,
                       **DISTINCT), 4),
     # then a smaller one: one layer, fewer elements, neurons and steps
     (synth.EpropShape(batch=3, n_in=37, n_rec=29, n_out=5, T=40, n_adaptive=13, **DISTINCT), 3),
