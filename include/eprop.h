@@ -284,9 +284,11 @@ void eprop_destroy(eprop_ctx* ctx);
  * those calls; the weights are read on the stream.
  * The workspace is the library's static scratch, EPROP_STATIC_SCRATCH_BYTES
  * of device memory that every GPU the library runs on holds from the first
- * use of the library until the process ends; shapes whose
- * eprop_workspace_bytes exceeds it return EPROP_ENOSPACE (before any device
- * call).  The device is the one current on the calling thread, which must be
+ * use of the library until the process ends.  On one stream nothing
+ * overlaps, so a sequence here takes one set of per-block buffers, where
+ * eprop_workspace_bytes counts the three a context pipelines with; shapes
+ * whose workspace with one set exceeds the scratch return EPROP_ENOSPACE
+ * (before any device call).  The device is the one current on the calling thread, which must be
  * the stream's.  Every call on one GPU uses that GPU's one scratch array:
  * calls that overlap on a GPU (queued on different streams without ordering,
  * or from several host threads) race; calls queued on one stream do not.

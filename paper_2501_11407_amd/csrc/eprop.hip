@@ -709,7 +709,7 @@ int join_forward_stream(eprop_ctx* ctx) {
 // Argument checks shared by eprop_init and eprop_sequence_static (errors
 // reported through eprop_last_error(NULL)).
 int check_init_args(const eprop_config* cfg, const void* d_workspace, size_t ws_bytes,
-                    const float* const* d_weights) {
+                    const float* const* d_weights, int slots = kSlots) {
   std::string why;
   if (!valid_config(cfg, &why)) return fail(nullptr, EPROP_EINVAL, why);
   if (!d_workspace || !d_weights) return fail(nullptr, EPROP_EINVAL, "workspace or weights is NULL");
@@ -718,7 +718,7 @@ int check_init_args(const eprop_config* cfg, const void* d_workspace, size_t ws_
   for (int k = 0; k < 2 * cfg->n_layers; ++k)
     if (!d_weights[k]) return fail(nullptr, EPROP_EINVAL, "a weight pointer is NULL");
   Plan probe;
-  make_plan(*cfg, nullptr, &probe);
+  make_plan(*cfg, nullptr, &probe, slots);
   if (!plan_fits(probe, &why)) return fail(nullptr, EPROP_EINVAL, why);
   if (ws_bytes < probe.bytes)
     return fail(nullptr, EPROP_ENOSPACE,
@@ -857,9 +857,12 @@ int eprop_sequence_static(const eprop_config* cfg, const float* const* d_weights
   if (!valid_config(cfg, &why)) return fail(nullptr, EPROP_EINVAL, why);
   for (int k = 0; k < 2 * cfg->n_layers; ++k)
     if (!d_grads[k]) return fail(nullptr, EPROP_EINVAL, "a gradient pointer is NULL");
-  // the size check comes before any device call
-  const size_t need = eprop_workspace_bytes(cfg);
-  if (need == 0) return fail(nullptr, EPROP_EINVAL, g_last_error);
+  // the size check comes before any device call; everything runs on one
+  // stream, so one set of per-block buffers is enough
+  Plan probe;
+  make_plan(*cfg, nullptr, &probe, 1);
+  if (!plan_fits(probe, &why)) return fail(nullptr, EPROP_EINVAL, why);
+  const size_t need = probe.bytes;
   if (need > kScratchBytes)
     return fail(nullptr, EPROP_ENOSPACE,
                 "shape needs " + std::to_string(need) + " bytes of workspace; the static scratch holds " +
@@ -867,7 +870,7 @@ int eprop_sequence_static(const eprop_config* cfg, const float* const* d_weights
   void* ws = nullptr;
   int rc = scratch_address(&ws);
   if (rc) return rc;
-  rc = check_init_args(cfg, ws, kScratchBytes, d_weights);
+  rc = check_init_args(cfg, ws, kScratchBytes, d_weights, 1);
   if (rc) return rc;
   eprop_ctx ctx;   // host-side bookkeeping only, on this stack frame
   rc = setup_ctx(&ctx, cfg, (char*)ws, kScratchBytes, d_weights, (hipStream_t)hip_stream, true);
