@@ -170,11 +170,13 @@ int eprop_run_sequence(eprop_ctx* ctx, const uint8_t* d_x, int32_t T, const int3
  * The steps up to the next weight change (or the end of the call) form one
  * block when they number at most 256, else blocks of equal length (within a
  * step), at least two and each at most 512 steps, the block limit.  With
- * EPROP_SPLIT_AUTO (the default) a run of more than 512 steps may instead
- * start with a short block followed by blocks of twice its length, one block
- * more than the equal split, when a rough cost model of the shape says that
- * starting the first eligibility pass earlier saves more than the added trace
- * round trip costs.  EPROP_SPLIT_EQUAL always takes the equal split.
+ * EPROP_SPLIT_AUTO (the default) a rough cost model of the shape may change
+ * that in two places: a run of 128 to 256 steps is cut in two halves when the
+ * forward steps of a half cost more than one more trace round trip; and a run
+ * of more than 512 steps may start with a short block followed by blocks of
+ * twice its length, one block more than the equal split, when starting the
+ * first eligibility pass earlier saves more than the added round trip costs.
+ * EPROP_SPLIT_EQUAL always takes the equal split.
  */
 #define EPROP_SPLIT_AUTO 0
 #define EPROP_SPLIT_EQUAL 1

@@ -914,12 +914,16 @@ SplitCost split_cost(const Plan& P) {
 // up to the next change (or the end of the call), a segment, form one block
 // when they are at most Kmax / 2, else blocks of equal length (within a
 // step), at least two, so that the forward pass of the second block runs
-// beside the eligibility pass of the first.  A segment longer than Kmax may
+// beside the eligibility pass of the first.  A segment of at most Kmax / 2
+// (and at least 2 kMinHalf) steps is cut in two halves as well when the
+// forward steps of a half cost more than one more trace round trip.  A segment longer than Kmax may
 // instead start with a short block followed by k blocks of twice its length
 // (k the smallest count that keeps those at most Kmax), when that adds one
 // block to the equal split: the first eligibility pass then starts that many
 // forward steps earlier, which pays when the steps saved cost more than the
 // added trace round trip.
+constexpr long long kMinHalf = 64;   // shortest half of a segment cut in two
+
 struct Split {
   int32_t seg_end = 0;   // end of the current segment (call-local step)
   int blk = 0;           // length of its blocks after the first
@@ -933,7 +937,10 @@ int next_block(int32_t t, int32_t T, long long t_ctx, int32_t every, int mode,
   sp.seg_end = (int32_t)(t + seg);
   const long long K = kBlockSteps;
   long long first = seg, blk = seg;
-  if (seg > K / 2) {
+  if (seg <= K / 2) {
+    if (mode == EPROP_SPLIT_AUTO && seg >= 2 * kMinHalf && (double)(seg / 2) * cost.step_us > cost.round_trip_us)
+      first = blk = (seg + 1) / 2;
+  } else {
     const long long nb = std::max<long long>(2, (seg + K - 1) / K);
     first = blk = (seg + nb - 1) / nb;
     if (seg > K) {
