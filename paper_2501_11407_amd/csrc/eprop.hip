@@ -376,7 +376,8 @@ struct eprop_ctx {
   // internal streams: the forward kernel, and the passes between it and the
   // eligibility kernel (learning signal, readout gradient, coefficients)
   hipStream_t fwd_stream = nullptr, coef_stream = nullptr;
-  hipEvent_t ev_entry = nullptr, ev_fwd[kSlots] = {}, ev_coef[kSlots] = {}, ev_done[kSlots] = {};
+  hipEvent_t ev_entry = nullptr, ev_fwd[kSlots] = {}, ev_coef[kSlots] = {}, ev_out[kSlots] = {},
+            ev_done[kSlots] = {};
   // every kernel on the caller's stream, in issue order, with no streams or
   // events of the context's own (the entry point that allocates nothing)
   bool single_stream = false;
@@ -513,6 +514,25 @@ int apply_online(eprop_ctx* ctx) {
   return rc;
 }
 
+// Rough costs that decide the block split, in microseconds on MI355X: one
+// round trip of every layer's per-synapse traces through HBM at about half
+// its peak bandwidth (the fixed part of an eligibility pass), and one
+// timestep of the forward pass of every layer with the learning-signal and
+// coefficient passes that follow it.
+struct SplitCost {
+  double round_trip_us = 0, step_us = 0;
+};
+
+SplitCost split_cost(const Plan& P) {
+  const eprop_config& c = P.cfg;
+  SplitCost k;
+  const double per_syn = 1.0 + (double)P.na2 / c.n_rec + P.rt;   // traces per synapse
+  for (const Layer& L : P.layers)
+    k.round_trip_us += (double)c.batch * L.n_pre * c.n_rec * per_syn * 8.0 / 4.0e6;
+  k.step_us = c.n_layers * (2.5 + (double)c.batch * c.n_rec * 32.0 / 4.0e6);
+  return k;
+}
+
 // An online weight update falls before the step t steps after the reset.
 bool online_due(const eprop_ctx* ctx, long long t) {
   return ctx->online_every > 0 && t > 0 && t % ctx->online_every == 0 && ctx->online_applied != t;
@@ -612,13 +632,43 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     ctx->in_ready = true;
   }
 
-  // On the coefficient stream, per layer: learning signal, readout gradient
-  // and the block coefficients of the eligibility recursion.  The forward of
-  // the next block (other slot) runs meanwhile.
+  // On the coefficient stream: the first layer's input filter and p bits,
+  // then per layer the learning signal, the readout gradient and the block
+  // coefficients of the eligibility recursion; the forward of the next block
+  // (other slot) runs meanwhile.  Where an eligibility pass is long against
+  // the block's forward (its trace round trip above a quarter of the forward
+  // steps' cost), it waits for all of that: started earlier it would slow
+  // the next forward, the longer path.  Where it is short, the eligibility
+  // pass starts as early as it can: the input filter (it needs only x) is
+  // queued ahead of the wait for the forward, and the readout gradient after
+  // the coefficients, past the eligibility pass's wait.
+  const SplitCost cost = split_cost(P);
+  const bool early = ev && 4.0 * cost.round_trip_us < steps * cost.step_us;
+  if (early) {
+    if (ctx->slot_used[sl] &&
+        (rc = check(ctx, hipStreamWaitEvent(sc, ctx->ev_done[sl], 0), "stream wait")))
+      return rc;
+    if ((rc = check(ctx, eprop::launch_input_filter(ia, sc), "input filter kernel"))) return rc;
+  }
   if (ev && (rc = check(ctx, hipStreamWaitEvent(sc, ctx->ev_fwd[sl], 0), "stream wait"))) return rc;
-  if ((rc = check(ctx, eprop::launch_input_filter(ia, sc), "input filter kernel"))) return rc;
+  if (!early && (rc = check(ctx, eprop::launch_input_filter(ia, sc), "input filter kernel"))) return rc;
   const int rows = steps * P.Bp;
   const int kpad = (int)round_up(steps, 16);
+  auto readout_gradient = [&](int l) {
+    Layer& L = ctx->plan.layers[l];
+    // dW_out += sum over (t, b) of delta (x) ztilde, then fp64 accumulation
+    eprop::GemmArgs g;
+    g.A = L.deltaK[sl]; g.Bm = L.ztK[sl]; g.C = L.Cpart;
+    g.M = c.n_out; g.N = c.n_rec; g.K = rows; g.lda = P.ldk; g.ldb = P.ldn; g.ldc = c.n_rec;
+    choose_splits(g.M, g.N, g.K, P.out_splits, &g.splits, &g.k_chunk);
+    g.split_stride = (size_t)c.n_out * c.n_rec;
+    int r = check(ctx, eprop::launch_gemm_tn(g, sc), "readout gradient GEMM");
+    if (!r)
+      r = check(ctx, eprop::launch_accumulate(L.Cpart, g.splits, g.split_stride, c.n_out, c.n_rec,
+                                              L.accout, L.ldj, first, sc),
+                "readout gradient accumulation");
+    return r;
+  };
   for (int l = 0; l < c.n_layers; ++l) {
     Layer& L = ctx->plan.layers[l];
     // learning signal L[(t,b)][j] = sum_k delta[(t,b)][k] W_out[k][j]
@@ -627,18 +677,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     gl.M = rows; gl.N = c.n_rec; gl.K = P.ldk; gl.lda = P.ldk; gl.ldb = P.ldk; gl.ldc = L.ldv;
     gl.splits = 1; gl.k_chunk = P.ldk; gl.split_stride = 0;
     if ((rc = check(ctx, eprop::launch_gemm_nt(gl, sc), "learning-signal GEMM"))) return rc;
-
-    // dW_out += sum over (t, b) of delta (x) ztilde, then fp64 accumulation
-    eprop::GemmArgs g;
-    g.A = L.deltaK[sl]; g.Bm = L.ztK[sl]; g.C = L.Cpart;
-    g.M = c.n_out; g.N = c.n_rec; g.K = rows; g.lda = P.ldk; g.ldb = P.ldn; g.ldc = c.n_rec;
-    choose_splits(g.M, g.N, g.K, P.out_splits, &g.splits, &g.k_chunk);
-    g.split_stride = (size_t)c.n_out * c.n_rec;
-    if ((rc = check(ctx, eprop::launch_gemm_tn(g, sc), "readout gradient GEMM"))) return rc;
-    if ((rc = check(ctx, eprop::launch_accumulate(L.Cpart, g.splits, g.split_stride, c.n_out,
-                                                  c.n_rec, L.accout, L.ldj, first, sc),
-                    "readout gradient accumulation")))
-      return rc;
+    if (!early && (rc = readout_gradient(l))) return rc;
 
     eprop::CoefArgs ca;
     ca.psiK = L.psiK[sl]; ca.LK = L.LK[sl]; ca.ldv = L.ldv; ca.Bp = P.Bp;
@@ -657,6 +696,9 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   }
   if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_coef[sl], sc), "event record"))) return rc;
   if (ev && (rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_coef[sl], 0), "stream wait"))) return rc;
+  for (int l = 0; early && l < c.n_layers; ++l)
+    if ((rc = readout_gradient(l))) return rc;
+  if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_out[sl], sc), "event record"))) return rc;
 
   // On the caller's stream: the eligibility pass of every layer.
   for (int l = 0; l < c.n_layers; ++l) {
@@ -685,6 +727,10 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
       ctx->prof_n++;
     }
   }
+  // later work on the caller's stream (the next blocks, the gradient
+  // read-out, an online update) and the reuse of this slot also follow the
+  // readout gradient
+  if (ev && (rc = check(ctx, hipStreamWaitEvent(s, ctx->ev_out[sl], 0), "stream wait"))) return rc;
   if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_done[sl], s), "event record"))) return rc;
   ctx->slot_used[sl] = true;
   ctx->last_slot = sl;
@@ -755,6 +801,8 @@ int setup_ctx(eprop_ctx* ctx, const eprop_config* cfg, char* ws, size_t ws_bytes
       rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_in[k], hipEventDisableTiming), "event create");
     for (int k = 0; k < kSlots && !rc; ++k) {
       rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_fwd[k], hipEventDisableTiming), "event create");
+      if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_out[k], hipEventDisableTiming),
+                          "event create");
       if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_coef[k], hipEventDisableTiming),
                           "event create");
       if (!rc) rc = check(ctx, hipEventCreateWithFlags(&ctx->ev_done[k], hipEventDisableTiming),
@@ -890,25 +938,6 @@ int eprop_step(eprop_ctx* ctx, const uint8_t* d_x_t, const int32_t* d_labels, ui
 }
 
 namespace {
-
-// Rough costs that decide the block split, in microseconds on MI355X: one
-// round trip of every layer's per-synapse traces through HBM at about half
-// its peak bandwidth (the fixed part of an eligibility pass), and one
-// timestep of the forward pass of every layer with the learning-signal and
-// coefficient passes that follow it.
-struct SplitCost {
-  double round_trip_us = 0, step_us = 0;
-};
-
-SplitCost split_cost(const Plan& P) {
-  const eprop_config& c = P.cfg;
-  SplitCost k;
-  const double per_syn = 1.0 + (double)P.na2 / c.n_rec + P.rt;   // traces per synapse
-  for (const Layer& L : P.layers)
-    k.round_trip_us += (double)c.batch * L.n_pre * c.n_rec * per_syn * 8.0 / 4.0e6;
-  k.step_us = c.n_layers * (2.5 + (double)c.batch * c.n_rec * 32.0 / 4.0e6);
-  return k;
-}
 
 // Blocks of up to Kmax steps that end where the weights change.  The steps
 // up to the next change (or the end of the call), a segment, form one block
@@ -1109,7 +1138,7 @@ void eprop_destroy(eprop_ctx* ctx) {
   for (hipEvent_t e : {ctx->ev_pre, ctx->ev_in[0], ctx->ev_in[1]})
     if (e) (void)hipEventDestroy(e);
   for (int k = 0; k < kSlots; ++k)
-    for (hipEvent_t e : {ctx->ev_fwd[k], ctx->ev_coef[k], ctx->ev_done[k]})
+    for (hipEvent_t e : {ctx->ev_fwd[k], ctx->ev_coef[k], ctx->ev_out[k], ctx->ev_done[k]})
       if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : ctx->ev) (void)hipEventDestroy(e);
   ctx->alive = false;
