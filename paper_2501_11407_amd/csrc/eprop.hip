@@ -67,7 +67,8 @@ struct Layer {
   // per-block vectors in up to kSlots slots: the forward of block k+1 fills one
   // while the eligibility pass of block k reads another
   float *psiK[kSlots], *LK[kSlots], *deltaK[kSlots], *ztK[kSlots];
-  // the binary presynaptic values (one byte per step), and the block
+  // the binary presynaptic values (one bit per row and step, a 16-bit word
+  // per row and 16-step chunk), and the block
   // coefficients of the eligibility recursion as scaled fp16 pairs
   uint16_t* pbits[kSlots];
   uint32_t* coefO[kSlots];        // the coefficient operands, tile-major (OpLayout)
@@ -575,7 +576,7 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
   }
   // the first layer's input rows: their drive before the forward (already
   // computed on the input stream, or now on the forward stream); their
-  // filter and p bytes on the coefficient stream (below)
+  // filter and p bits on the coefficient stream (below)
   const Layer& L0 = P.layers[0];
   const int ib = ctx->in_buf;
   eprop::InputArgs ia;

@@ -59,7 +59,7 @@ struct FwdLayer {
   int n_inl, n_pre, ldi;
 };
 
-// The forward handles the p bytes, filter and zstart of the recurrent rows
+// The forward handles the p bits, filter and zstart of the recurrent rows
 // (and of every row of a second layer); the first layer's input rows, and
 // the input part of its drive, come from the input kernels below.
 struct FwdArgs {

@@ -101,8 +101,9 @@ __device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChu
 
 // ---------------------------------------------------------------- forward
 // One workgroup per batch element runs `steps` timesteps of every layer; the
-// neuron state stays in registers, the presynaptic filter of the rows the
-// workgroup handles and the readout in shared memory.  Thread 64 w + l (wave
+// neuron state and, for each thread's own presynaptic rows, the filter, the
+// chunk's p bits and the last spike stay in registers, the readout in shared
+// memory.  Thread 64 w + l (wave
 // w, lane l) holds the QN neurons 64 QN w + 64 q + l, q < QN (fwd_neuron): a
 // wave owns a contiguous range of neurons, its spike list, built by ballots
 // in ascending q, is ascending, and the waves' lists in wave order are the
@@ -118,7 +119,7 @@ __device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChu
 //      sequential sum over the active rows.  While the rows' loads are in
 //      flight: the filter zbar = alpha*zbar + p of the rows the workgroup
 //      handles (recurrent rows, and every row of a second layer; the first
-//      layer's input rows are input_filter_kernel's) and their p bytes.  Then
+//      layer's input rows are input_filter_kernel's) and their p bits.  Then
 //      the neuron step with one rounding per operation:
 //        v = alpha*v; v = v + I; v = v - thr*z_prev
 //        a = rho*a;   a = a + z_prev
@@ -1441,32 +1442,35 @@ __global__ __launch_bounds__(256) void coef_rt_kernel(CoefArgs a) {
 // For each batch element b of the split:
 //  * MFMA contractions C_U, C_V, C_H = coef_b[j][s] x p_b[i][s] over the
 //    block's steps (v_mfma_f32_16x16x32_f16 on the scaled fp16 pairs, four
-//    16x16 blocks per wave stacked along i), 16 steps ("a chunk") at a time,
-//    operands read from shared memory;
+//    16x16 blocks per wave stacked along i), 16 steps ("a chunk") at a time
+//    and two chunks per wait and barrier ("a pair"), operands read from
+//    shared memory;
 //  * then the elementwise update of the traces, each read once and written
-//    once (1 KiB contiguous per wave instruction), and of the gradient.
-// Operands stream through a ring of kRing chunk slots in shared memory:
-// the p_b bytes of the tile's 256 rows (one contiguous 4 KiB run, a wave
-// copies its own 64 rows) and the U, H (and V, W) rows of its 16 columns
-// (one contiguous 1 KiB run each, copied by waves 0, 1 (2, 3)) of the
-// chunk's 16 steps are copied by direct buffer-to-LDS loads (16 bytes per
+//    once (1 KiB contiguous per wave instruction), and of the gradient, at
+//    the end of the element's own iteration.
+// Operands stream through a ring of kRing pair slots in shared memory: the
+// p bits of the tile's 256 rows (512 bytes per chunk; a wave copies its own
+// 64 rows) and the tile's coefficient operands U, H (and V, W), one
+// contiguous run per chunk in the tile-major layout (one operand of 1 KiB
+// per copying wave), are copied by direct buffer-to-LDS loads (16 bytes per
 // lane, no registers, the chunk's position in a scalar offset) up to
-// kRing - 1 chunks ahead of the chunk being contracted, across batch
-// elements.  The block-start traces of a batch element (registers) and its
-// scalars (shared memory, double-buffered; with the block-start filter of the
-// tile's rows) travel with its first chunk.
-// Waits: copies and loads complete in order, so a chunk's copies are waited
-// for with an exact vmcnt; trace stores (which may complete out of order with
-// respect to loads) are drained once per batch element, at its second chunk.
-// The workgroup barrier carries no memory fence (a fence would drain every
-// copy in flight); shared-memory hazards are ordered by the waits and the
-// barrier alone.
+// kRing - 1 pairs ahead of the pair being contracted, across batch elements.
+// An element's scalars (shared memory, double-buffered; with the block-start
+// filter of the tile's rows) travel with its first pair; its block-start
+// traces (registers) are loaded during its iteration, one 16x16 block per
+// pair over its first four pairs.
+// Waits: the copies of a wave complete in order, so a pair's copies are
+// waited for with an exact vmcnt.  The workgroup barrier carries no memory
+// fence (a fence would drain every copy in flight); shared-memory hazards are
+// ordered by the waits and the barrier alone.
 // Lane (r, g) of block bi holds the 4 columns j = j0 + 4 g ..+3 of row
 // i = i0 + 64 w + 16 bi + r; the traces of a wave sub-tile are stored in
 // exactly this order (block bi at bi KiB, lane l at 16 l bytes).  A wave whose
 // 64 rows are all padding (past n_pre) reads and writes no traces.  The
 // gradient of the batch elements of one launch is summed in fp32 per lane and
 // added to the split's fp64 accumulator at the end.
+// Workgroup order (trace_kernel): the row tiles of one column tile and batch
+// split, which share every coefficient chunk, run on one XCD.
 // Buffer access: a wave-uniform base with a byte range (accesses outside it
 // read zero and write nothing) and a 32-bit per-lane byte offset.  The trace
 // streams use the non-temporal cache policy (bit 1 of the policy operand):
@@ -1607,18 +1611,18 @@ struct TraceTile {
     return make_rsrc((const char*)base + (t * 4 + w) * kSubTileBytes, live ? bytes : 0u);
   }
 
-  // Copies of chunk c of batch element b into ring slot sl: wave w copies
-  // the p bytes of its 64 rows (stored by the forward as [16-row group][step
-  // quad][row][4 steps], so that the operand reads below are free of bank
-  // conflicts), and wave X the 16 rows of coefficient operand X (lane l: row
-  // l / 4, its 16-byte unit u = (l % 4) ^ ((row / 2) % 4) stored at position
-  // l % 4, which keeps the MFMA operand reads free of bank conflicts).  With
-  // chunk 0 also the scalars (planes PPW w .. PPW w + PPW - 1 of the 16
-  // columns, and the block-start filter of the wave's rows) into scalar
-  // buffer par.  The copies are issued in two parts (P = 0: p; P = 1: the
-  // coefficient operand and the scalars), placed between MFMAs so that the
-  // vector-memory path works while the matrix cores do; the order of all
-  // copies is that of the full issue.
+  // Copies of the NC chunks c, c + 1 (< NC) of batch element b into pair
+  // slot sl: wave w copies the p bits of its 64 rows (one 16-bit word per
+  // row and chunk, 128 bytes, lanes 0-7), and a copying wave its coefficient
+  // operand of the tile (lane l: row l / 4, its 16-byte unit
+  // u = (l % 4) ^ ((row / 2) % 4) stored at position l % 4, which keeps the
+  // MFMA operand reads free of bank conflicts).  With chunk 0 also the
+  // scalars (planes PPW w .. PPW w + PPW - 1 of the 16 columns, and the
+  // block-start filter of the wave's rows) into scalar buffer par.  The
+  // copies are issued in two parts (P = 0: p; P = 1: the coefficient operand
+  // and the scalars), placed between MFMAs so that the vector-memory path
+  // works while the matrix cores do; the order of all copies is that of the
+  // full issue.
   template <int P, int NC>
   __device__ __forceinline__ void issue(int b_, int c, int sl, int par) const {
     const int b = __builtin_amdgcn_readfirstlane(b_);   // wave-uniform: scalar address arithmetic
