@@ -127,8 +127,9 @@ hipError_t launch_accumulate(const float* part, int splits, size_t split_stride,
 
 // The operands of the eligibility contractions are stored as scaled fp16
 // pairs: a value x (times a power-of-two scale 2^e) is hi = fp16(x 2^e) plus
-// lo = fp16(x 2^e - hi), together about 22 significant bits, in one 32-bit
-// word (hi in the low half).  Per 16-step chunk and row, 16 words (64 bytes).
+// lo = fp16(x 2^e - hi), together about 22 significant bits.  Per 16-step
+// chunk and row, 64 bytes: per quad of steps a 16-byte unit of the four hi
+// halves and then the four lo halves.
 // The presynaptic operand is binary (bits, expanded to fp16 in the kernel).
 constexpr int kChunk = 16;                     // steps per chunk
 constexpr int kKC = kBlockSteps / kChunk;      // chunks per block

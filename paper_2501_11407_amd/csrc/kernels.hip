@@ -82,20 +82,23 @@ __device__ __forceinline__ void split16(float x, _Float16& hi, _Float16& lo) {
   lo = (_Float16)(x - (float)hi);
 }
 
-// scaled value -> one 32-bit word: hi in the low half, lo in the high half
-__device__ __forceinline__ uint32_t pair_word(float x) {
-  _Float16 hi, lo;
-  split16(x, hi, lo);
-  return (uint32_t)__builtin_bit_cast(uint16_t, hi) | ((uint32_t)__builtin_bit_cast(uint16_t, lo) << 16);
-}
-
-// 16 values x scale -> the 64-byte pair record of a chunk row (one word per step)
+// 16 values x scale -> the 64-byte pair record of a chunk row: per quad of
+// steps 4u .. 4u+3 one 16-byte unit holding the four hi halves, then the
+// four lo halves, in step order
 __device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChunk], float scale) {
   u32x4* d = (u32x4*)dst;
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
-    d[u] = u32x4{pair_word(x[4 * u] * scale), pair_word(x[4 * u + 1] * scale),
-                 pair_word(x[4 * u + 2] * scale), pair_word(x[4 * u + 3] * scale)};
+  for (int u = 0; u < 4; ++u) {
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      _Float16 hi, lo;
+      split16(x[4 * u + e] * scale, hi, lo);
+      h[e] = __builtin_bit_cast(uint16_t, hi);
+      l[e] = __builtin_bit_cast(uint16_t, lo);
+    }
+    d[u] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
+  }
 }
 
 
@@ -1830,10 +1833,11 @@ struct TraceTile {
         };
 
         // Per output block and contraction X, one fp16 MFMA (K = 32) per
-        // chunk of 16 steps.  Lane g holds steps 4g..4g+3 as (hi, lo) pairs
-        // of k slots: A = X's words as they are (row r of the 16 columns, the
-        // same for every wave); B = (p, p) per step, which sums X_hi p +
-        // X_lo p (p is the binary presynaptic value, exact in fp16).
+        // chunk of 16 steps.  Lane g holds the 8 k slots of steps 4g..4g+3:
+        // A = X's unit as it is (the four hi halves, then the four lo
+        // halves; row r of the 16 columns, the same for every wave), B = the
+        // four p values twice, which sums X_hi p + X_lo p (p is the binary
+        // presynaptic value, exact in fp16).
         const char* slot = (const char*)(sm + (n % RING) * SLOT);
         const int sw = (r >> 1) & 3;   // unit order of this lane's row
         const f16x8 zero8 = {};
@@ -1856,14 +1860,16 @@ struct TraceTile {
         for (int h = 0; h < NC; ++h) {
 #pragma unroll
           for (int bi = 0; bi < 4; ++bi) {
-            // steps 4g .. 4g+3 of row 16 bi + r of the wave: four p bits ->
-            // (p, p) fp16 pairs (1.0 = 0x3C00 in both halves of word e); the
-            // 16 rows' words are 32 consecutive bytes, read by every g alike
-            const uint32_t pb = pw[h][bi] >> (4 * g);
-            u32x4 w1;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) w1[e] = ((pb >> e) & 1u) ? 0x3C003C00u : 0u;
-            const f16x8 bz = __builtin_bit_cast(f16x8, w1);
+            // steps 4g .. 4g+3 of row 16 bi + r of the wave: four p bits n
+            // -> the fp16 words (p0, p1) and (p2, p3) (1.0 = 0x3C00): with
+            // x = n (1 + 2^15), bits 0 and 16 of x are p0 and p1, bits 2 and
+            // 18 are p2 and p3, so each word is one mask and one multiply
+            // (24-bit operands); the 16 rows' words are 32 consecutive
+            // bytes, read by every g alike
+            const uint32_t x = __builtin_amdgcn_ubfe(pw[h][bi], 4 * g, 4) * 0x8001u;
+            const uint32_t p01 = (x & 0x10001u) * 0x3C00u;
+            const uint32_t p23 = (x & 0x40004u) * 0xF00u;
+            const f16x8 bz = __builtin_bit_cast(f16x8, u32x4{p01, p23, p01, p23});
             cU[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][0], bz, cU[bi], 0, 0, 0);
             cH[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][1], bz, cH[bi], 0, 0, 0);
             if constexpr (ALIF)
