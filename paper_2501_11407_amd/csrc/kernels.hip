@@ -82,23 +82,23 @@ __device__ __forceinline__ void split16(float x, _Float16& hi, _Float16& lo) {
   lo = (_Float16)(x - (float)hi);
 }
 
-// 16 values x scale -> the 64-byte pair record of a chunk row: per quad of
-// steps 4u .. 4u+3 one 16-byte unit holding the four hi halves, then the
-// four lo halves, in step order
+// 16 values x scale -> the 64-byte pair record of a chunk row: the 16 hi
+// halves in step order (units 0 and 1), then the 16 lo halves (units 2, 3)
 __device__ __forceinline__ void store_pairs(uint32_t* dst, const float (&x)[kChunk], float scale) {
-  u32x4* d = (u32x4*)dst;
+  uint32_t h[kChunk / 2], l[kChunk / 2];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    uint32_t h[4], l[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      _Float16 hi, lo;
-      split16(x[4 * u + e] * scale, hi, lo);
-      h[e] = __builtin_bit_cast(uint16_t, hi);
-      l[e] = __builtin_bit_cast(uint16_t, lo);
-    }
-    d[u] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), l[0] | (l[1] << 16), l[2] | (l[3] << 16)};
+  for (int e = 0; e < kChunk; e += 2) {
+    _Float16 h0, l0, h1, l1;
+    split16(x[e] * scale, h0, l0);
+    split16(x[e + 1] * scale, h1, l1);
+    h[e / 2] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+    l[e / 2] = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
   }
+  u32x4* d = (u32x4*)dst;
+  d[0] = u32x4{h[0], h[1], h[2], h[3]};
+  d[1] = u32x4{h[4], h[5], h[6], h[7]};
+  d[2] = u32x4{l[0], l[1], l[2], l[3]};
+  d[3] = u32x4{l[4], l[5], l[6], l[7]};
 }
 
 
@@ -1841,55 +1841,76 @@ struct TraceTile {
         const char* slot = (const char*)(sm + (n % RING) * SLOT);
         const int sw = (r >> 1) & 3;   // unit order of this lane's row
         const f16x8 zero8 = {};
-        // the pair's shared-memory reads in one batch: the coefficient
-        // operands and the p words of the four row blocks of both chunks
-        f16x8 ax[2][4];
-        uint32_t pw[2][4];
+        // Per output block and contraction X, two fp16 MFMAs (K = 32) per
+        // pair of chunks: lane group g holds the 8 k slots of pair steps
+        // 8g .. 8g+7 (chunk g / 2 of the pair), the first MFMA takes their hi
+        // halves, the second their lo halves, each against the same 8 p
+        // values, which sums X_hi p + X_lo p (p is the binary presynaptic
+        // value, exact in fp16).  A pair of one chunk (the last of an odd
+        // count) leaves lane groups 2 and 3 with zero operands.
+        const bool none = NC == 1 && g >= 2;
+        const char* hs = slot + (g >> 1) * HSLOT;   // this lane's chunk
+        // the pair's shared-memory reads in one batch: the hi and lo units of
+        // each coefficient operand and the p words of the four row blocks
+        f16x8 axh[4], axl[4];
+        uint32_t pw[4];
 #pragma unroll
-        for (int h = 0; h < NC; ++h) {
-#pragma unroll
-          for (int X = 0; X < 4; ++X)
-            ax[h][X] = ((X < 2) || (X == 2 && ALIF) || (X == 3 && RT))
-                           ? *(const f16x8*)(slot + h * HSLOT + kPBytes + X * kOpBytes + r * 64 + ((g ^ sw) << 4))
-                           : zero8;
-#pragma unroll
-          for (int bi = 0; bi < 4; ++bi)
-            pw[h][bi] = *(const uint16_t*)(slot + h * HSLOT + (kWaveRows * w + 16 * bi + r) * 2);
+        for (int X = 0; X < 4; ++X) {
+          const bool has = (X < 2) || (X == 2 && ALIF) || (X == 3 && RT);
+          const char* row = hs + kPBytes + X * kOpBytes + r * 64;
+          axh[X] = has ? *(const f16x8*)(row + (((g & 1) ^ sw) << 4)) : zero8;
+          axl[X] = has ? *(const f16x8*)(row + (((2 + (g & 1)) ^ sw) << 4)) : zero8;
+          if (NC == 1) {
+            axh[X] = none ? zero8 : axh[X];
+            axl[X] = none ? zero8 : axl[X];
+          }
         }
 #pragma unroll
-        for (int h = 0; h < NC; ++h) {
+        for (int bi = 0; bi < 4; ++bi)
+          pw[bi] = *(const uint16_t*)(hs + (kWaveRows * w + 16 * bi + r) * 2);
+        // pair steps 8g .. 8g+7 of row 16 bi + r of the wave: eight p bits n
+        // -> the fp16 words (p0, p1), (p2, p3), (p4, p5), (p6, p7) (1.0 =
+        // 0x3C00): with x = n (1 + 2^15), bits 2m and 2m + 16 of x are p_2m
+        // and p_2m+1, so each word is one mask and one multiply (24-bit
+        // operands); the 16 rows' words are 32 consecutive bytes, read by
+        // every g alike
+        auto expand = [&](int bi) {
+          uint32_t x = __builtin_amdgcn_ubfe(pw[bi], 8 * (g & 1), 8) * 0x8001u;
+          if (NC == 1) x = none ? 0u : x;
+          return __builtin_bit_cast(f16x8, u32x4{(x & 0x10001u) * 0x3C00u, (x & 0x40004u) * 0xF00u,
+                                                  (x & 0x100010u) * 0x3C0u, (x & 0x400040u) * 0xF0u});
+        };
+        auto mfma = [&](const f16x8 (&ax)[4], const f16x8& bz, int bi) {
+          cU[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[0], bz, cU[bi], 0, 0, 0);
+          cH[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[1], bz, cH[bi], 0, 0, 0);
+          if constexpr (ALIF)
+            cV[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[2], bz, cV[bi], 0, 0, 0);
+          if constexpr (RT)
+            cW[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[3], bz, cW[bi], 0, 0, 0);
+        };
 #pragma unroll
-          for (int bi = 0; bi < 4; ++bi) {
-            // steps 4g .. 4g+3 of row 16 bi + r of the wave: four p bits n
-            // -> the fp16 words (p0, p1) and (p2, p3) (1.0 = 0x3C00): with
-            // x = n (1 + 2^15), bits 0 and 16 of x are p0 and p1, bits 2 and
-            // 18 are p2 and p3, so each word is one mask and one multiply
-            // (24-bit operands); the 16 rows' words are 32 consecutive
-            // bytes, read by every g alike
-            const uint32_t x = __builtin_amdgcn_ubfe(pw[h][bi], 4 * g, 4) * 0x8001u;
-            const uint32_t p01 = (x & 0x10001u) * 0x3C00u;
-            const uint32_t p23 = (x & 0x40004u) * 0xF00u;
-            const f16x8 bz = __builtin_bit_cast(f16x8, u32x4{p01, p23, p01, p23});
-            cU[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][0], bz, cU[bi], 0, 0, 0);
-            cH[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][1], bz, cH[bi], 0, 0, 0);
-            if constexpr (ALIF)
-              cV[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][2], bz, cV[bi], 0, 0, 0);
-            if constexpr (RT)
-              cW[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[h][3], bz, cW[bi], 0, 0, 0);
-            if (h == 0 && bi == 1) {
-              __builtin_amdgcn_sched_barrier(0);
-              issue_next(std::integral_constant<int, 0>{});
-              __builtin_amdgcn_sched_barrier(0);
-            } else if (h == 0 && bi == 3) {
-              __builtin_amdgcn_sched_barrier(0);
-              issue_next(std::integral_constant<int, 1>{});
-              // the element's block-start traces, after pair 0's copies
-              if constexpr (spread && ps < 4)
-                load_traces(b, ps, ps + 1, E, A, Vm);
-              else if constexpr (!spread && ps == 0)
-                load_traces(b, 0, 4, E, A, Vm);
-              __builtin_amdgcn_sched_barrier(0);
-            }
+        for (int b2 = 0; b2 < 4; b2 += 2) {
+          // two row blocks at a time: their hi MFMAs, then their lo MFMAs,
+          // so that an accumulator's two MFMAs are not back to back
+          const f16x8 bz0 = expand(b2), bz1 = expand(b2 + 1);
+          mfma(axh, bz0, b2);
+          mfma(axh, bz1, b2 + 1);
+          if (b2 == 0) {
+            __builtin_amdgcn_sched_barrier(0);
+            issue_next(std::integral_constant<int, 0>{});
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          mfma(axl, bz0, b2);
+          mfma(axl, bz1, b2 + 1);
+          if (b2 == 0) {
+            __builtin_amdgcn_sched_barrier(0);
+            issue_next(std::integral_constant<int, 1>{});
+            // the element's block-start traces, after pair 0's copies
+            if constexpr (spread && ps < 4)
+              load_traces(b, ps, ps + 1, E, A, Vm);
+            else if constexpr (!spread && ps == 0)
+              load_traces(b, 0, 4, E, A, Vm);
+            __builtin_amdgcn_sched_barrier(0);
           }
         }
       };
