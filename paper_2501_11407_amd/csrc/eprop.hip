@@ -470,20 +470,26 @@ int clear_state(eprop_ctx* ctx) {
   const eprop_config& c = ctx->plan.cfg;
   const size_t B = c.batch, N = c.n_rec, K = c.n_out;
   hipStream_t s = ctx->stream;
-  // a fill kernel rather than memset nodes, so that a caller may capture it
-  int rc = check(ctx, eprop::launch_zero(ctx->plan.err_flag, sizeof(int), s), "reset");
+  // one fill kernel for every range rather than memset nodes, so that a
+  // caller may capture it
+  eprop::ZeroRanges zr{};
+  auto add = [&](void* p, size_t bytes) {
+    zr.p[zr.n] = p;
+    zr.bytes[zr.n] = bytes;
+    ++zr.n;
+  };
+  add(ctx->plan.err_flag, sizeof(int));
   for (Layer& L : ctx->plan.layers) {
-    if (rc) return rc;
-    hipError_t e = hipSuccess;
-    e = e ? e : eprop::launch_zero(L.v, sizeof(float) * B * N, s);
-    e = e ? e : eprop::launch_zero(L.a, sizeof(float) * B * N, s);
-    e = e ? e : eprop::launch_zero(L.ztil, sizeof(float) * B * N, s);
-    e = e ? e : eprop::launch_zero(L.zbar, sizeof(float) * B * L.n_pre, s);
-    e = e ? e : eprop::launch_zero(L.y, sizeof(float) * B * K, s);
-    e = e ? e : eprop::launch_zero(L.z, B * N, s);
-    e = e ? e : eprop::launch_zero(L.lossacc, sizeof(double) * B, s);
-    rc = check(ctx, e, "reset");
+    add(L.v, sizeof(float) * B * N);
+    add(L.a, sizeof(float) * B * N);
+    add(L.ztil, sizeof(float) * B * N);
+    add(L.zbar, sizeof(float) * B * L.n_pre);
+    add(L.y, sizeof(float) * B * K);
+    add(L.z, B * N);
+    add(L.lossacc, sizeof(double) * B);
   }
+  static_assert(1 + 7 * 2 <= eprop::ZeroRanges::kMax, "ranges of two layers");
+  int rc = check(ctx, eprop::launch_zero_many(zr, s), "reset");
   ctx->t = 0;
   ctx->online_applied = -1;
   return rc;

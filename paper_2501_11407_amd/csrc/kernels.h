@@ -228,6 +228,14 @@ hipError_t launch_pack16(const float* W, int n_rec, int n_pre, int16_t* W16, int
 hipError_t launch_set_flag(int* flag, int value, hipStream_t s);
 // Zeroes `bytes` bytes at `p` (a fill kernel, not a memset node).
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+// Up to kMax device ranges zeroed by one launch (ranges of 0 bytes allowed).
+struct ZeroRanges {
+  static constexpr int kMax = 16;
+  void* p[kMax];
+  size_t bytes[kMax];
+  int n;
+};
+hipError_t launch_zero_many(const ZeroRanges& r, hipStream_t s);
 
 // Online weight application for one layer: the weights in use become
 // W0 - lr * G rounded to the nearest multiple of 2^-14 (ties to even), G the

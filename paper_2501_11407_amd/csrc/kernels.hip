@@ -2120,6 +2120,23 @@ __global__ __launch_bounds__(256) void zero_kernel(unsigned char* p, size_t byte
   if (tid < bytes - tail0) p[tail0 + tid] = 0;
 }
 
+// Several ranges in one launch: blockIdx.y picks the range, the x blocks
+// stride over it as zero_kernel's do.
+__global__ __launch_bounds__(256) void zero_many_kernel(ZeroRanges r) {
+  const int k = blockIdx.y;
+  unsigned char* p = (unsigned char*)r.p[k];
+  const size_t bytes = r.bytes[k];
+  const size_t head = min(bytes, (size_t)((16 - ((uintptr_t)p & 15)) & 15));
+  const size_t nvec = (bytes - head) / 16;
+  const size_t tail0 = head + nvec * 16;
+  const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t nth = (size_t)gridDim.x * blockDim.x;
+  u32x4* body = (u32x4*)(p + head);
+  for (size_t q = tid; q < nvec; q += nth) body[q] = u32x4{0u, 0u, 0u, 0u};
+  if (tid < head) p[tid] = 0;
+  if (tid < bytes - tail0) p[tail0 + tid] = 0;
+}
+
 __global__ __launch_bounds__(256) void pack_kernel(const float* src, int rows, int cols, float* dst,
                                                    int ldd, int dst_rows, int transpose) {
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -2328,6 +2345,15 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
   if (bytes == 0) return hipSuccess;
   const long long blocks = std::min<long long>(8192, std::max<long long>(1, cdiv((long long)(bytes / 16), 256)));
   zero_kernel<<<(int)blocks, 256, 0, s>>>((unsigned char*)p, bytes);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_many(const ZeroRanges& r, hipStream_t s) {
+  if (r.n < 1 || r.n > ZeroRanges::kMax) return hipErrorInvalidValue;
+  long long blocks = 1;
+  for (int k = 0; k < r.n; ++k)
+    blocks = std::max<long long>(blocks, std::min<long long>(8192, cdiv((long long)(r.bytes[k] / 16), 256)));
+  zero_many_kernel<<<dim3((unsigned)blocks, (unsigned)r.n), 256, 0, s>>>(r);
   return hipGetLastError();
 }
 
