@@ -425,16 +425,21 @@ int pack_weights(eprop_ctx* ctx) {
   // the int16 drive weights are used when every layer's are exact
   int rc0 = check(ctx, eprop::launch_set_flag(ctx->plan.w16ok, 1, ctx->stream), "weight packing");
   if (rc0) return rc0;
+  // the row of zeros after each layer's drive rows (row n_pre of W16 and Wt),
+  // read by the forward's loads past a step's active list
+  eprop::ZeroRanges zr{};
+  for (Layer& L : ctx->plan.layers) {
+    zr.p[zr.n] = L.W16 + (size_t)L.n_pre * L.ldw;
+    zr.bytes[zr.n++] = sizeof(int16_t) * L.ldw;
+    zr.p[zr.n] = L.Wt + (size_t)L.n_pre * L.ldw;
+    zr.bytes[zr.n++] = sizeof(float) * L.ldw;
+  }
+  rc0 = check(ctx, eprop::launch_zero_many(zr, ctx->stream), "weight packing");
+  if (rc0) return rc0;
   for (Layer& L : ctx->plan.layers) {
     int rc16 = check(ctx, eprop::launch_pack16(L.W_src, c.n_rec, L.n_pre, L.W16,
                                                eprop::forward_qn(c.n_rec), ctx->plan.w16ok,
                                                ctx->stream), "weight packing");
-    if (rc16) return rc16;
-    rc16 = check(ctx, eprop::launch_zero((unsigned char*)(L.W16 + (size_t)L.n_pre * L.ldw),
-                                         sizeof(int16_t) * L.ldw, ctx->stream), "weight packing");
-    if (!rc16)
-      rc16 = check(ctx, eprop::launch_zero((unsigned char*)(L.Wt + (size_t)L.n_pre * L.ldw),
-                                           sizeof(float) * L.ldw, ctx->stream), "weight packing");
     if (rc16) return rc16;
     // drive weights transposed, Wt[i][j] = W[j][i], columns padded to the
     // forward workgroup size
