@@ -1054,24 +1054,26 @@ int eprop_get_grads(eprop_ctx* ctx, float* const* d_grads, double* d_loss) {
   const eprop_config& c = ctx->plan.cfg;
   for (int k = 0; k < 2 * c.n_layers; ++k)
     if (!d_grads[k]) return fail(ctx, EPROP_EINVAL, "a gradient pointer is NULL");
+  eprop::ReadoutArgs ro{};
+  ro.n_layers = c.n_layers;
   for (int l = 0; l < c.n_layers; ++l) {
     Layer& L = ctx->plan.layers[l];
-    eprop::GradsArgs g;
+    eprop::GradsArgs& g = ro.g[l];
     g.acc = L.acc; g.ldj = L.ldj; g.n_split = L.n_split; g.acc_stride = L.acc_stride;
     g.dW = d_grads[2 * l]; g.n_pre = L.n_pre; g.n_post = c.n_rec;
     g.n_inl = L.n_inl; g.recurrent = c.recurrent;
     g.accout = L.accout; g.ld_acc = L.ldj; g.dWout = d_grads[2 * l + 1]; g.K = c.n_out;
     g.valid = ctx->t > 0;
-    int rc = check(ctx, eprop::launch_grads(g, ctx->stream), "gradient read-out");
-    if (rc) return rc;
   }
   if (d_loss) {
     const Layer& L0 = ctx->plan.layers[0];
-    const size_t stride = c.n_layers > 1 ? (size_t)(ctx->plan.layers[1].lossacc - L0.lossacc) : 0;
-    int rc = check(ctx, eprop::launch_loss(L0.lossacc, c.batch, c.n_layers, stride, d_loss, ctx->stream),
-                   "loss read-out");
-    if (rc) return rc;
+    ro.lossacc = L0.lossacc;
+    ro.B = c.batch;
+    ro.layer_stride = c.n_layers > 1 ? (size_t)(ctx->plan.layers[1].lossacc - L0.lossacc) : 0;
+    ro.loss = d_loss;
   }
+  int rc = check(ctx, eprop::launch_readout(ro, ctx->stream), "gradient read-out");
+  if (rc) return rc;
   return EPROP_OK;
 }
 

@@ -206,9 +206,13 @@ struct GradsArgs {
   const double* accout; int ld_acc; float* dWout; int K;
   int valid;
 };
-hipError_t launch_grads(const GradsArgs& a, hipStream_t s);
-hipError_t launch_loss(const double* lossacc, int B, int n_layers, size_t layer_stride,
-                       double* out, hipStream_t s);
+// Every layer's dW and dW_out and (loss not NULL) the loss, in one launch.
+struct ReadoutArgs {
+  GradsArgs g[2];
+  int n_layers;
+  const double* lossacc; int B; size_t layer_stride; double* loss;
+};
+hipError_t launch_readout(const ReadoutArgs& r, hipStream_t s);
 
 // src [rows][cols] row-major -> dst [dst_rows][ldd] (transpose = 0) or
 // dst[c][r] = src[r][c] (transpose = 1); every other element of dst is zero.

@@ -1976,7 +1976,32 @@ constexpr size_t kTraceSmemOf(bool rt) {
 
 // ---------------------------------------------------------------- gradient read-out
 // 32x32 tiles through shared memory: acc is [i][j], dW is [j][i].
-__global__ __launch_bounds__(256) void grads_kernel(GradsArgs a) {
+// The read-out of a call to eprop_get_grads in one launch; blockIdx.z picks
+// the job: 2 l, layer l's dW (32 x 32 tiles on x, y, transposed through
+// shared memory, the split accumulators summed in split order); 2 l + 1,
+// layer l's dW_out (y = 0 only, one element per thread along x); 2 L, the
+// loss (one thread, a fixed summation order over layers and batch elements).
+__global__ __launch_bounds__(256) void readout_kernel(ReadoutArgs r) {
+  const int job = blockIdx.z;
+  if (job == 2 * r.n_layers) {
+    if (threadIdx.x != 0 || blockIdx.x != 0 || blockIdx.y != 0) return;
+    double s = 0.0;
+    for (int l = 0; l < r.n_layers; ++l)
+      for (int b = 0; b < r.B; ++b) s += r.lossacc[(size_t)l * r.layer_stride + b];
+    *r.loss = s;
+    return;
+  }
+  const GradsArgs& a = r.g[job >> 1];
+  if (job & 1) {
+    if (blockIdx.y != 0) return;
+    const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (long long)a.K * a.n_post) return;
+    const int k = (int)(idx / a.n_post), j = (int)(idx % a.n_post);
+    a.dWout[(size_t)k * a.n_post + j] = a.valid ? (float)a.accout[(size_t)k * a.ld_acc + j] : 0.0f;
+    return;
+  }
+  // the whole workgroup leaves together (its tile lies past the matrix)
+  if ((int)blockIdx.x * 32 >= a.n_pre || (int)blockIdx.y * 32 >= a.n_post) return;
   __shared__ double tile[32][33];
   const int i0 = blockIdx.x * 32, j0 = blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;   // 32 x 8
@@ -1995,23 +2020,6 @@ __global__ __launch_bounds__(256) void grads_kernel(GradsArgs a) {
       a.dW[(size_t)j * a.n_pre + i] = diag ? 0.0f : (float)tile[tx][yy];
     }
   }
-}
-
-__global__ __launch_bounds__(256) void grads_out_kernel(GradsArgs a) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  const int k = blockIdx.y;
-  if (j >= a.n_post) return;
-  a.dWout[(size_t)k * a.n_post + j] = a.valid ? (float)a.accout[(size_t)k * a.ld_acc + j] : 0.0f;
-}
-
-// One thread: a fixed summation order over layers and batch elements.
-__global__ void loss_kernel(const double* lossacc, int B, int n_layers, size_t layer_stride,
-                            double* out) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  double s = 0.0;
-  for (int l = 0; l < n_layers; ++l)
-    for (int b = 0; b < B; ++b) s += lossacc[(size_t)l * layer_stride + b];
-  *out = s;
 }
 
 // Workgroups of the weight-packing kernels: a fixed grid walks the weights,
@@ -2293,17 +2301,16 @@ hipError_t launch_trace(const TraceArgs& a, hipStream_t s) {
   return a.reset_through ? launch_trace_nch<true>(a, s, nch) : launch_trace_nch<false>(a, s, nch);
 }
 
-hipError_t launch_grads(const GradsArgs& a, hipStream_t s) {
-  dim3 grid(cdiv(a.n_pre, 32), cdiv(a.n_post, 32));
-  grads_kernel<<<grid, 256, 0, s>>>(a);
-  dim3 grid2(cdiv(a.n_post, 256), a.K);
-  grads_out_kernel<<<grid2, 256, 0, s>>>(a);
-  return hipGetLastError();
-}
-
-hipError_t launch_loss(const double* lossacc, int B, int n_layers, size_t layer_stride,
-                       double* out, hipStream_t s) {
-  loss_kernel<<<1, 64, 0, s>>>(lossacc, B, n_layers, layer_stride, out);
+hipError_t launch_readout(const ReadoutArgs& r, hipStream_t s) {
+  if (r.n_layers < 1 || r.n_layers > 2) return hipErrorInvalidValue;
+  long long gx = 1, gy = 1;
+  for (int l = 0; l < r.n_layers; ++l) {
+    const GradsArgs& a = r.g[l];
+    gx = std::max<long long>(gx, std::max<long long>(cdiv(a.n_pre, 32), cdiv((long long)a.K * a.n_post, 256)));
+    gy = std::max<long long>(gy, cdiv(a.n_post, 32));
+  }
+  const unsigned gz = 2 * r.n_layers + (r.loss ? 1 : 0);
+  readout_kernel<<<dim3((unsigned)gx, (unsigned)gy, gz), 256, 0, s>>>(r);
   return hipGetLastError();
 }
 
