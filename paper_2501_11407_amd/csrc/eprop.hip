@@ -626,20 +626,20 @@ int do_block(eprop_ctx* ctx, const uint8_t* x, int steps, const int32_t* labels,
     fa.mr[0] = (float)full.r[0]; fa.mr[1] = (float)full.r[1];
   }
   // the next block's input drive into the other buffer, while this forward
-  // runs (not when the weights change before the next block)
+  // runs (not when the weights change before the next block): the event that
+  // lets it start is recorded before the forward, whose launch comes first
+  // so that it does not wait for the host
   const bool pre = ev && x_next && steps_next > 0 && !online_due(ctx, ctx->t + steps);
-  if (pre) {
-    eprop::InputArgs nx = ia;
-    nx.x = x_next; nx.steps = steps_next; nx.Iin = P.Iin[ib ^ 1]; nx.nin = P.nin[ib ^ 1];
-    if ((rc = check(ctx, hipEventRecord(ctx->ev_pre, sf), "event record")) ||
-        (rc = check(ctx, hipStreamWaitEvent(ctx->in_stream, ctx->ev_pre, 0), "stream wait")) ||
-        (rc = check(ctx, eprop::launch_input_drive(nx, ctx->in_stream), "input drive kernel")) ||
-        (rc = check(ctx, hipEventRecord(ctx->ev_in[ib ^ 1], ctx->in_stream), "event record")))
-      return rc;
-  }
+  if (pre && (rc = check(ctx, hipEventRecord(ctx->ev_pre, sf), "event record"))) return rc;
   if ((rc = check(ctx, eprop::launch_forward(fa, sf), "forward kernel"))) return rc;
   if (ev && (rc = check(ctx, hipEventRecord(ctx->ev_fwd[sl], sf), "event record"))) return rc;
   if (pre) {
+    eprop::InputArgs nx = ia;
+    nx.x = x_next; nx.steps = steps_next; nx.Iin = P.Iin[ib ^ 1]; nx.nin = P.nin[ib ^ 1];
+    if ((rc = check(ctx, hipStreamWaitEvent(ctx->in_stream, ctx->ev_pre, 0), "stream wait")) ||
+        (rc = check(ctx, eprop::launch_input_drive(nx, ctx->in_stream), "input drive kernel")) ||
+        (rc = check(ctx, hipEventRecord(ctx->ev_in[ib ^ 1], ctx->in_stream), "event record")))
+      return rc;
     ctx->in_buf = ib ^ 1;
     ctx->in_ready = true;
   }
