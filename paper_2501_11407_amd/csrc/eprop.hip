@@ -348,8 +348,11 @@ void make_plan(const eprop_config& c, char* base, Plan* plan, int slots = kSlots
   // QN floats) where that fits beside an eligibility workgroup
   const size_t ring = (size_t)3 * qn * eprop::kFwdThreads * sizeof(float);
   const size_t fwd_smem = smem_base;
-  // with up to four neurons per thread (the spike lists of at most 64 KiB)
-  plan->svc = qn <= 4;
+  // with up to two neurons per thread: with more, the ninth wave's third
+  // wave on one SIMD would keep every eligibility workgroup off the forward's
+  // compute units (registers); measured on two layers of 2048 neurons, the
+  // forward without it lets the eligibility passes run beside it, 4% faster
+  plan->svc = qn <= 2;
   plan->smem = fwd_smem + (plan->svc ? ring : 0);
   plan->bytes = round_up(off, 256);
 }

@@ -737,8 +737,12 @@ __device__ __forceinline__ void forward_service_wave(const FwdArgs& A, const Fwd
 
 // Four waves per SIMD (128 registers) for one layer of at most two neurons
 // per thread; three (168) for two layers or four neurons per thread and
-// more, so that those do not spill up to four.  Either way an eligibility
-// workgroup fits beside the forward on its compute unit.
+// more, so that those do not spill up to four.  An eligibility workgroup
+// (168 registers per wave) fits beside the forward on its compute unit where
+// the forward's waves per SIMD times their registers leave 168: one layer of
+// at most two neurons per thread or two of one (nine waves, three on one
+// SIMD, at most 112 registers), and every form without the service wave
+// (eight waves, two per SIMD).
 template <int QN, int NL, bool SVC>
 __global__ __launch_bounds__(SVC ? kFwdThreads + 64 : kFwdThreads) __attribute__((amdgpu_waves_per_eu((QN >= 4 || NL > 1) ? 3 : 4))) void forward_kernel(FwdArgs A) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -2189,9 +2193,11 @@ hipError_t launch_forward_qn(const FwdArgs& a, hipStream_t s) {
 
 template <int QN, int NL>
 hipError_t launch_forward_svc(const FwdArgs& a, hipStream_t s) {
-  // up to four neurons per thread: always with the service wave (its ring
-  // fits); more: without
-  if constexpr (QN <= 4)
+  // up to two neurons per thread: always with the service wave; more:
+  // without (a ninth wave puts three waves on one SIMD, and with more than
+  // about 112 registers per wave an eligibility workgroup no longer fits
+  // beside the forward on its compute unit)
+  if constexpr (QN <= 2)
     return a.svc ? launch_forward_qn<QN, NL, true>(a, s) : hipErrorInvalidValue;
   else
     return a.svc ? hipErrorInvalidValue : launch_forward_qn<QN, NL, false>(a, s);
@@ -2199,7 +2205,7 @@ hipError_t launch_forward_svc(const FwdArgs& a, hipStream_t s) {
 
 hipError_t launch_forward(const FwdArgs& a, hipStream_t s) {
   const int qn = forward_qn(a.n_rec);
-  if (a.svc && qn > 4) return hipErrorInvalidValue;
+  if (a.svc && qn > 2) return hipErrorInvalidValue;
   const bool two = a.n_layers > 1;
   switch (qn) {
     case 1: return two ? launch_forward_svc<1, 2>(a, s) : launch_forward_svc<1, 1>(a, s);
