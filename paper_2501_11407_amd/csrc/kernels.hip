@@ -1892,6 +1892,12 @@ struct TraceTile {
           if constexpr (RT)
             cW[bi] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax[3], bz, cW[bi], 0, 0, 0);
         };
+        // the pair's MFMAs at a raised issue priority: a wave whose operands
+        // have arrived keeps the matrix pipe busy ahead of the waves still
+        // reading theirs (still below the forward's)
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(1);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int b2 = 0; b2 < 4; b2 += 2) {
           // two row blocks at a time: their hi MFMAs, then their lo MFMAs,
@@ -1917,6 +1923,9 @@ struct TraceTile {
             __builtin_amdgcn_sched_barrier(0);
           }
         }
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_sched_barrier(0);
       };
       for_each_index(pair, std::make_integer_sequence<int, NS>{});
       // The element's traces and gradient.  Its block-start traces were
