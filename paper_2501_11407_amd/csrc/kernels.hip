@@ -1514,10 +1514,6 @@ __device__ __forceinline__ void for_each_index(F&& f, std::integer_sequence<int,
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
-// Lane l copies 16 bytes from its own address g to lds + 16 l.
-__device__ __forceinline__ void dma16(const void* g, void* lds) {
-  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
-}
 // Lane l copies 16 bytes at byte voff + soff of the buffer r to lds + 16 l
 // (soff: a wave-uniform offset, so stepping through chunks costs no vector
 // instructions).
@@ -1559,7 +1555,7 @@ struct TraceTile {
   static constexpr int D = NS == 1 ? 1 : (NS - 1 < PREF ? NS - 1 : PREF);
   // Copies per wave per chunk: its p rows, and one coefficient operand for
   // the copying waves (wave X copies operand X: U, H, and V / W when present).
-  static constexpr int SC = 1;                                  // scalar copies per wave
+  static constexpr int SC = RT ? 1 : 2;                         // scalar copies per wave (planes, filter)
   static constexpr int EA = 4 * (1 + (ALIF ? 1 : 0) + (RT ? 1 : 0));   // trace loads per element
   static constexpr int ops(int s, bool cp) { return in_pair(s) * (1 + (cp ? 1 : 0)) + (s == 0 ? SC : 0); }
   // The block-start traces are loaded one 16 x 16 block bi of each trace per
@@ -1612,6 +1608,16 @@ struct TraceTile {
     opbase = (const char*)(a.O + a.ol.tile(jt_)) + (w == 3 && !ALIF ? 2 : w) * kOpBytes;
   }
 
+  // The lane index computed where it is used, from an operand the compiler
+  // cannot hoist: offsets derived from it then take no register across the
+  // element loop (at the register cap such values were spilled, and each
+  // reload waited for every copy in flight).
+  __device__ __forceinline__ static uint32_t lane_here() {
+    uint32_t ones = ~0u;
+    asm volatile("" : "+s"(ones));
+    return __builtin_amdgcn_mbcnt_hi(ones, __builtin_amdgcn_mbcnt_lo(ones, 0u));
+  }
+
   __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const float* base, int n_t, int b,
                                                              uint32_t bytes) const {
     const size_t t = ((size_t)b * (a.n_pre_pad / kTileI) + it) * n_t + jt;
@@ -1659,13 +1665,16 @@ struct TraceTile {
       if (c == 0) {
         float* sb = sm + RING * SLOT + par * SCAL + w * kScalWave;
         // lanes 0 .. 4 PPW - 1: plane PPW w + l / 4, columns 4 (l % 4) .. +3;
-        // lanes 16-31 (reset-stopped form): the filter of rows 64 w + 4 (l - 16) .. +3
-        const bool zs = !RT && lane >= 16 && lane < 32;
-        if (lane < 4 * PPW || zs) {
-          const float* src = lane < 16
-              ? a.S + ((size_t)(PPW * w + (lane >> 2)) * a.B + b) * a.ldc + j0 + (lane & 3) * 4
-              : a.zstart + (size_t)b * a.ldi + i0 + kWaveRows * w + (lane - 16) * 4;
-          dma16(src, sb);
+        // lanes 16-31 (reset-stopped form): the filter of rows 64 w + 4 (l - 16) .. +3.
+        // Buffer loads from a per-element scalar base and 32-bit lane
+        // offsets (computed here from the lane index).
+        const uint32_t l = lane_here();
+        const uint32_t pst = (uint32_t)(a.B * a.ldc) * 4u;           // bytes between planes
+        const auto sr = make_rsrc(a.S + (size_t)b * a.ldc + j0, (uint32_t)(PLANES - 1) * pst + kTileJ * 4u);
+        if (l < 4u * PPW) dma16b(sr, (uint32_t)(PPW * w + (l >> 2)) * pst + (l & 3u) * 16u, 0u, sb);
+        if constexpr (!RT) {
+          const auto zr = make_rsrc(a.zstart + (size_t)b * a.ldi + i0 + kWaveRows * w, kWaveRows * 4u);
+          if (l >= 16u && l < 32u) dma16b(zr, (l - 16u) * 16u, 0u, sb);
         }
       }
     }
@@ -1715,7 +1724,7 @@ struct TraceTile {
     const auto eR = tile_rsrc(a.ebar, a.n_jt, b, kSubTileBytes);
     const auto aR = ALIF ? tile_rsrc(a.epsa, a.n_jt_a, b, kSubTileBytes) : eR;
     const auto vR = RT ? tile_rsrc(a.epsv, a.n_jt, b, kSubTileBytes) : eR;
-    const int cj = 4 * g;
+    const int cj = 4 * (int)((lane_here() >> 4) & 3u);   // this lane group's columns
     auto plane = [&](int p) {
       return *(const f32x4*)(st + (p / PPW) * kScalWave + (p % PPW) * kTileJ + cj);
     };
@@ -1940,7 +1949,7 @@ struct TraceTile {
     }
     // the split's fp64 accumulator (row-major [n_pre_pad][ldj]); rows past
     // n_pre and columns past n_post are not written
-    const int jb = j0 + 4 * g;
+    const int jb = j0 + 4 * (int)((lane_here() >> 4) & 3u);
     if (!live || jb >= a.n_post) return;
     double* accp = a.acc + (size_t)split * a.acc_stride;
 #pragma unroll
@@ -2298,6 +2307,9 @@ hipError_t launch_trace_variant(const TraceArgs& a, hipStream_t s) {
   // eight XCDs times the groups per XCD times the row tiles of a group
   const long long wgs = 8ll * cdiv(a.n_jt * a.n_split, 8) * (a.n_pre_pad / kTileI);
   if (wgs > 0x7fffffffll) return hipErrorInvalidValue;
+  // the scalar planes are addressed by 32-bit offsets within one buffer
+  if ((unsigned long long)(RT ? kScalarPlanesRT : kScalarPlanes) * a.B * a.ldc * 4ull > 0xffffffffull)
+    return hipErrorInvalidValue;
   trace_kernel<RT, NCH><<<dim3((unsigned)wgs), 256, smem, s>>>(a);
   return hipGetLastError();
 }
